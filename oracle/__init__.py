@@ -1,0 +1,35 @@
+"""Plain fp64 CPU oracle for the GIST sub-GCN training step.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import, call or
+execute this package: only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` use it.  It shares no code with the HIP
+library (no kernels, headers, helpers or tables) and does not import it.
+
+What it computes, each function citing the passage it follows (paper:
+"GIST: Distributed Training for Large-Scale Graph Convolutional Networks"):
+
+* :mod:`oracle.partition` -- ``subGCNs`` feature partition (Section 3.1 and
+  its footnote; Algorithm 1), SplitMix64 + Fisher-Yates, plus the
+  categorical-mask variant of the theory appendix (Appendix A.1).
+* :mod:`oracle.minibatch` -- ``Cluster`` mini-batch: union of clusters,
+  induced subgraph, normalised aggregation matrix (Section 3.2 for the
+  mini-batch; eq. (1) for the self-looped degree-normalised matrix;
+  eq. "Aggregation Matrix" of Appendix A.2 for the theory form).
+* :mod:`oracle.layers` -- the sub-GCN layer forward and backward (eq. (1),
+  eq. (2)), the GraphSAGE-mean layer, softmax cross-entropy, SGD
+  (Section 3.2), slice gather (Section 3.1) and ``subAgg`` (Section 3.2).
+* :mod:`oracle.gist` -- one sub-GCN training step and one GIST round
+  (Algorithm 1) composed from the above.
+
+Floating point is fp64 throughout; fp32 inputs are widened exactly.  The
+matrices of the normalised adjacency are the one place where fp32 is part
+of the definition: the values are computed in fp64 and rounded once to fp32
+(round-to-nearest-even), which is what the library stores.
+
+Every function here is pinned by ``tests/test_oracle_*.py`` against facts
+the paper and the mathematics fix (published generator outputs, mask
+properties, spectra, closed-form gradients, finite differences, the
+two-layer sum decomposition); none is "parity unpinned".
+"""
+
+from . import partition, minibatch, layers, gist  # noqa: F401
