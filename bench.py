@@ -1,0 +1,327 @@
+#!/usr/bin/env python3
+"""Benchmark: one GIST round of the ultra-wide GraphSAGE-mean workload on one GPU.
+
+Workload (default ``--config c4``): 4-layer GraphSAGE-mean, hidden width
+32,768 split into m = 8 sub-GCNs of 4,096, on a 2,449,029-node stochastic
+block model (15,000 blocks, ~61.9M edges, 100 input features, 47 classes).
+One timed step is one pass of the whole hot path:
+
+  subGCNs partition of the three hidden widths (host)
+  -> gather of all 8 sub-GCN weight slices (device)
+  -> for each sub-GCN: cluster mini-batch of 10 blocks (host CSR build into
+     pinned memory, asynchronous upload, device feature-row gather),
+     forward through 4 layers, softmax cross-entropy, backward, SGD
+  -> subAgg of all 8 slices into the 16 GiB global model.
+
+Inputs are seeded synthetic data resident in HBM before timing starts.
+The reported value is ms per sub-GCN step = round time / m.  Kernel times
+come from HIP events the library records on the launch stream during the
+timed rounds (gist_profile_*).  The CPU baseline is the fp64 oracle timed on
+one sub-GCN step of the same workload.
+
+Prints ONE JSON line.  ``--gpus N`` with N > 1 exits: this build runs on one
+GPU (the multi-GPU design is described in the design doc).
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK = {"f32": 157.3, "bf16": 2516.6}   # dense MFMA TFLOP/s, MI355X
+HBM_PEAK_GBS = 8000.0
+METRIC = "sub-GCN fwd+bwd step ms; SpMM GB/s and GEMM TFLOP/s as % of MI355X peak"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--dtype", default="f32", choices=["f32", "bf16"])
+    ap.add_argument("--d-in", type=int, default=256, help="c5 input slice width")
+    ap.add_argument("--lr", type=float, default=0.01)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true",
+                    help="skip the library's per-launch event timing")
+    return ap.parse_args()
+
+
+# ---------------------------------------------------------------------------
+class RoundWorkload:
+    """A GIST round (partition, gather, m sub-GCN steps, subAgg) on one GPU."""
+
+    def __init__(self, cfg, ctx, dtype):
+        import torch
+        from paper_2102_10424_amd import gist as G
+        from paper_2102_10424_amd.step import BatchSlot, GistModel, SubGCN
+        self.cfg, self.ctx, self.G = cfg, ctx, G
+        t0 = time.time()
+        self.graph = cfg.make_graph()
+        log(f"[bench] graph n={self.graph.n} nnz={self.graph.nnz} ({time.time() - t0:.1f}s)")
+        self.gh = G.GraphHandle(self.graph)
+        self.X = torch.from_numpy(cfg.features_matrix()).cuda()
+        self.labels = cfg.labels()
+        theta = []
+        t0 = time.time()
+        for l in range(cfg.L):
+            parts = []
+            for p in range(cfg.n_parts()):
+                parts.append(torch.from_numpy(cfg.theta(l, p)).cuda())
+            theta.append(parts)
+        log(f"[bench] global theta on device ({time.time() - t0:.1f}s)")
+        self.model = GistModel(ctx, cfg.kind, cfg.widths, cfg.m, theta)
+        self.norm = "sage" if cfg.kind == "sage" else "gcn"
+        # capacities: the largest mini-batch of the clusters, generous nnz bound
+        if cfg.batch_clusters is None:
+            cap_n = self.graph.n
+            cap_nnz = self.graph.nnz + self.graph.n
+        else:
+            sizes = np.diff(self.graph.cluster_ptr)
+            cap_n = int(np.sort(sizes)[-cfg.batch_clusters:].sum())
+            cap_nnz = int(np.sort(np.diff(self.graph.rowptr))[-cap_n:].sum()) + cap_n
+        self.slots = [BatchSlot(ctx, self.norm, cap_n, cap_nnz, cfg.widths[0])
+                      for _ in range(cfg.m)]
+        self.full = None
+        self.runner = SubGCN(ctx, cfg.kind, self.model.slice_widths, cap_n,
+                             dtype=G.GIST_DTYPE_BF16_IN if dtype == "bf16" else G.GIST_DTYPE_F32)
+        self.lr = 0.01
+        self.t = 0
+
+    def step(self):
+        cfg, m = self.cfg, self.model
+        t = self.t
+        m.set_partitions({l: cfg.partition_seed(t, l) for l in range(1, cfg.L)})
+        for i in range(cfg.m):
+            m.gather(i)
+        for i in range(cfg.m):
+            if cfg.batch_clusters is None:
+                if self.full is None:
+                    self.full = self.slots[0].load(self.gh, None, self.X, self.labels)
+                b = self.full
+            else:
+                b = self.slots[i].load(self.gh, cfg.minibatch(t, i), self.X, self.labels)
+            self.runner.step(b, m.params[i], self.lr)
+        for i in range(cfg.m):
+            m.subagg(i)
+        self.t += 1
+
+    def steps_per_unit(self):
+        return self.cfg.m
+
+    def describe(self):
+        c = self.cfg
+        return {"workload": f"{c.name}: GIST round, {c.L}-layer "
+                            f"{'GraphSAGE-mean' if c.kind == 'sage' else 'GCN'}, hidden "
+                            f"{c.widths[1]} split m={c.m}, N={c.n_nodes}, "
+                            f"{'mini-batch ' + str(c.batch_clusters) + ' clusters' if c.batch_clusters else 'full graph'}",
+                "model": "GIST sub-GCN", "m": c.m, "widths": c.widths,
+                "global_batch": c.batch_clusters or c.n_nodes}
+
+    # ---- CPU baseline: the fp64 oracle on one sub-GCN step ---------------------
+    def cpu_baseline(self):
+        from oracle import gist as OG
+        from oracle import minibatch as OM
+        from oracle import partition as OP
+        cfg = self.cfg
+        parts = [None] * (cfg.L + 1)
+        for l in range(1, cfg.L):
+            parts[l] = OP.partition(cfg.widths[l], cfg.m, cfg.partition_seed(0, l))
+        sl = OG.slice_indices(parts, cfg.L, 0)
+        params = []
+        for l, (r, c) in enumerate(sl):
+            ps = []
+            for p in range(cfg.n_parts()):
+                rows = r if r is not None else None
+                th = cfg.theta(l, p, rows=rows) if rows is not None else cfg.theta(l, p)
+                ps.append(th if c is None else th[:, c])
+            params.append(ps[0] if cfg.kind == "gcn" else (ps[0], ps[1]))
+        csr = OM.build(self.graph, cfg.minibatch(0, 0), self.norm)
+        nm = csr["node_map"]
+        X = cfg.features_matrix(rows=nm)
+        y = self.labels[nm]
+        t0 = time.time()
+        OG.sub_gcn_step(cfg.kind, csr, X, y, params, self.lr)
+        dt = time.time() - t0
+        return dt * 1e3, "one sub-GCN step (fwd + loss + bwd + SGD) of round 0, sub-GCN 0, " \
+                         "fp64; excludes partition, slice gather and subAgg"
+
+
+class LayerWorkload:
+    """c5: one GCN layer fwd+bwd over the whole graph (output slice of m=8)."""
+
+    def __init__(self, cfg, ctx, dtype, d_in):
+        import torch
+        from paper_2102_10424_amd import gist as G
+        from paper_2102_10424_amd.step import BatchSlot
+        cfg.widths = [d_in, cfg.widths[1]]
+        self.cfg, self.ctx, self.G = cfg, ctx, G
+        self.d_in = d_in
+        t0 = time.time()
+        self.graph = cfg.make_graph()
+        log(f"[bench] graph n={self.graph.n} nnz={self.graph.nnz} ({time.time() - t0:.1f}s)")
+        gh = G.GraphHandle(self.graph)
+        n = self.graph.n
+        self.slot = BatchSlot(ctx, "gcn", n, self.graph.nnz + n, d_in)
+        self.X = torch.from_numpy(cfg.features_matrix()).cuda()
+        self.b = self.slot.load(gh, None, self.X, cfg.labels())
+        torch.cuda.synchronize()
+        idx, offs = G.gist_partition(cfg.widths[1], cfg.m, cfg.partition_seed(0, 1))
+        cols = torch.from_numpy(idx[offs[0]:offs[1]].copy()).cuda()
+        th = torch.from_numpy(cfg.theta(0, 0)).cuda()
+        self.s_out = int(offs[1] - offs[0])
+        self.W = torch.empty(d_in, self.s_out, device="cuda")
+        G.gist_gather_slice(ctx, th, cfg.widths[1], None, d_in, cols, self.s_out, self.W,
+                            self.s_out)
+        self.dHo = torch.from_numpy(cfg.upstream(n, self.s_out)).cuda()
+        self.desc = G.layer_desc(G.GIST_LAYER_GCN, G.GIST_ACT_RELU, n, d_in, self.s_out,
+                                 G.GIST_DTYPE_BF16_IN if dtype == "bf16" else G.GIST_DTYPE_F32)
+        f, bb = G.gist_layer_workspace_size(self.desc)
+        self.ws = torch.empty(max(f, bb), dtype=torch.uint8, device="cuda")
+        self.agg = torch.empty(n, d_in, device="cuda")
+        self.Ho = torch.empty(n, self.s_out, device="cuda")
+        self.dW = torch.empty(d_in, self.s_out, device="cuda")
+        self.dH = torch.empty(n, d_in, device="cuda")
+
+    def step(self):
+        G, b = self.G, self.b
+        G.gist_gcn_layer_fwd(self.ctx, self.desc, b.A, b.X, self.W, self.agg, self.Ho, self.ws)
+        G.gist_gcn_layer_bwd(self.ctx, self.desc, b.A, None, b.X, self.agg, self.Ho, self.W,
+                             self.dHo, self.dW, self.dH, self.ws)
+
+    def steps_per_unit(self):
+        return 1
+
+    def describe(self):
+        return {"workload": f"c5: one GCN layer fwd+bwd, full graph N={self.graph.n}, "
+                            f"nnz={self.graph.nnz + self.graph.n}, {self.d_in}->{self.s_out}",
+                "model": "GIST sub-GCN layer", "global_batch": self.graph.n,
+                "d_in": self.d_in, "s_out": self.s_out}
+
+    def cpu_baseline(self):
+        from oracle import layers as OL
+        from oracle import minibatch as OM
+        # bounded sample: 20,000 rows of the forward (their aggregation and transform)
+        csr = OM.build(self.graph, None, "gcn")
+        rows = np.arange(20000)
+        sub = dict(n=csr["n"], rowptr=np.concatenate([csr["rowptr"][:20001]]),
+                   col=csr["col"], val=csr["val"])
+        X = self.cfg.features_matrix()
+        W = self.W.cpu().numpy()
+        import scipy.sparse as sp
+        A = sp.csr_matrix((csr["val"].astype(np.float64), csr["col"], csr["rowptr"]),
+                          shape=(csr["n"], csr["n"]))[rows]
+        t0 = time.time()
+        AH = A @ X.astype(np.float64)
+        OL.relu(AH @ W.astype(np.float64))
+        dt = (time.time() - t0) * csr["n"] / rows.shape[0]
+        return dt * 1e3 * 3, ("forward of 20,000 rows (fp64 aggregation + transform), scaled "
+                              "to all rows and x3 for fwd+bwd")
+
+
+# ---------------------------------------------------------------------------
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build runs on exactly one GPU; --gpus must be 1 "
+                                   "(multi-GPU sharding is described in DESIGN.md)"}))
+        sys.exit(2)
+    import torch
+    from gist_synth import get_config
+    from paper_2102_10424_amd import gist as G
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    ctx = G.Context(0)
+    cfg = get_config(args.config)
+    if args.config == "c5":
+        wl = LayerWorkload(cfg, ctx, args.dtype, args.d_in)
+    else:
+        wl = RoundWorkload(cfg, ctx, args.dtype)
+        wl.lr = args.lr
+    for w in range(args.warmup):
+        wl.step()
+        torch.cuda.synchronize()
+        log(f"[bench] warmup {w + 1}/{args.warmup} done")
+    if not args.no_profile:
+        G.gist_profile_begin(ctx, 1 << 16)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        wl.step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    log(f"[bench] timed {args.steps} steps")
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    prof, dropped = ({}, 0)
+    if not args.no_profile:
+        prof, dropped = G.gist_profile_read(ctx)
+        G.gist_profile_end(ctx)
+    kernels = {}
+    for k, v in sorted(prof.items(), key=lambda kv: -kv[1]["ms"]):
+        e = dict(launches=v["launches"], ms_per_step=round(v["ms"] / args.steps, 4),
+                 avg_us=round(1e3 * v["ms"] / v["launches"], 2))
+        if v["flops"] and k.startswith("gemm_") and "reduce" not in k:
+            e["tflops"] = round(v["flops"] / (v["ms"] * 1e-3) / 1e12, 2)
+        if v["bytes"]:
+            e["gbs"] = round(v["bytes"] / (v["ms"] * 1e-3) / 1e9, 1)
+        kernels[k] = e
+    roofline = None
+    if prof:
+        dom, v = max(prof.items(), key=lambda kv: kv[1]["ms"])
+        avg_s = v["ms"] * 1e-3 / v["launches"]
+        if dom.startswith("gemm_") and "reduce" not in dom:
+            peak = PEAK["bf16" if "bf16" in dom else "f32"]
+            ach = v["flops"] / v["launches"] / avg_s / 1e12
+            roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2),
+                        "peak": peak, "unit": "TFLOP/s", "frac": round(ach / peak, 4),
+                        "traffic": None, "avg_launch_us": round(avg_s * 1e6, 2),
+                        "units_per_launch": round(v["flops"] / v["launches"] / 1e9, 3),
+                        "unit_desc": "GFLOP per launch (2 M N K)"}
+        else:
+            ach = v["bytes"] / v["launches"] / avg_s / 1e9
+            roofline = {"kernel": dom, "bound": "hbm", "achieved": round(ach, 1),
+                        "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+                        "traffic": None, "avg_launch_us": round(avg_s * 1e6, 2),
+                        "units_per_launch": round(v["bytes"] / v["launches"] / 1e9, 4),
+                        "unit_desc": "GB algorithmic per launch"}
+    per_unit = wl.steps_per_unit()
+    value = ms_step / per_unit
+    cpu = None
+    if not args.no_cpu_baseline:
+        try:
+            from threadpoolctl import threadpool_info
+            threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        except Exception:
+            threads = os.cpu_count() or 1
+        ms, what = wl.cpu_baseline()
+        cpu = {"value": round(ms, 2), "unit": "ms", "cores": int(threads), "kind": "oracle",
+               "sample": what}
+    out = {
+        "metric": METRIC, "value": round(value, 4), "unit": "ms",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3), "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16-in/f32-acc" if args.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded SBM / Chung-Lu / ER graphs, N(0,1) features, Glorot weights)",
+        "config": dict(wl.describe(), parallelism="single GPU, m sub-GCNs back to back",
+                       step="one GIST round" if per_unit > 1 else "one layer fwd+bwd",
+                       value="ms per sub-GCN step (round time / m)" if per_unit > 1
+                       else "ms per layer fwd+bwd"),
+        "roofline": roofline, "cpu_baseline": cpu, "kernels": kernels,
+        "profile_dropped": dropped,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

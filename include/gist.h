@@ -1,0 +1,306 @@
+/*
+ * gist.h -- C ABI of libgist, the GIST sub-GCN training step on AMD MI355X.
+ *
+ * GIST ("Graph Independent Subnetwork Training", Algorithm 1) splits every
+ * hidden feature dimension of a GCN into m disjoint random blocks (subGCNs,
+ * Section 3.1), trains each narrow sub-GCN on cluster mini-batches
+ * (subTrain, Section 3.2) and copies the trained weight slices back into the
+ * global model (subAgg, Section 3.2).  This library provides the pieces of
+ * that hot path:
+ *
+ *   gist_partition             subGCNs: random equal blocks of [0, d)   (host)
+ *   gist_build_minibatch_csr   Cluster mini-batch: induced, normalised  (host)
+ *   gist_gather_slice          Theta^(i) = Theta[D_in, D_out]           (device)
+ *   gist_gcn_layer_fwd/_bwd    eq. (2) sub-GCN layer, GCN and SAGE-mean (device)
+ *   gist_softmax_xent          loss and its gradient                    (device)
+ *   gist_sgd_update            one SGD step                             (device)
+ *   gist_subagg                subAgg: Theta[D_in, D_out] <- Theta^(i)  (device)
+ *
+ * Conventions
+ *  - Every matrix is row-major fp32 with the leading dimension stated.
+ *  - "device" pointers are HIP device memory on the context's device; the
+ *    caller owns every buffer.  The library never frees caller memory and
+ *    never allocates device memory inside these calls: scratch space is
+ *    passed in as a workspace sized by gist_layer_workspace_size().
+ *  - Device calls are asynchronous and ordered on the context's stream.
+ *    Host-side argument checks run before any launch and return an error
+ *    without launching anything; faults inside a kernel surface at the
+ *    caller's next synchronisation of that stream.
+ *  - Every call returns a gist_status; on failure gist_last_error() holds a
+ *    message (per thread).  No C++ exception crosses this interface.
+ *  - Zero-sized work (n == 0, nnz == 0) is a valid no-op returning GIST_OK.
+ */
+#ifndef GIST_H_
+#define GIST_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum gist_status {
+  GIST_OK = 0,
+  GIST_E_INVAL = -1,        /* bad shape, pointer, flag, m does not divide d,
+                               label or cluster id out of range, ...          */
+  GIST_E_NOMEM = -2,        /* caller buffer / workspace too small            */
+  GIST_E_DEVICE = -3,       /* HIP runtime error (text in gist_last_error)    */
+  GIST_E_UNSUPPORTED = -4,  /* valid request this build does not implement    */
+  GIST_E_NONFINITE = -5     /* GIST_SUBAGG_CHECK_FINITE found a NaN/Inf       */
+} gist_status;
+
+/* ---- errors --------------------------------------------------------- */
+
+/* Message of the calling thread's last failed call ("" if none).  The
+ * pointer stays valid until this thread's next gist_* call. */
+const char* gist_last_error(void);
+/* Static name of a status code. */
+const char* gist_status_str(gist_status s);
+
+/* ---- context -------------------------------------------------------- */
+
+typedef struct gist_ctx gist_ctx;
+
+/* Create a context bound to HIP device `device` and stream `hip_stream`
+ * (a hipStream_t; NULL = the default stream).  The stream is the caller's
+ * and is not destroyed by gist_destroy. */
+gist_status gist_create(int device, void* hip_stream, gist_ctx** out);
+gist_status gist_destroy(gist_ctx* ctx);
+gist_status gist_set_stream(gist_ctx* ctx, void* hip_stream);
+
+/* ---- subGCNs: feature partition (Section 3.1, Algorithm 1) ----------- */
+
+#define GIST_PART_CATEGORICAL 1u
+
+/* Partition the feature indices [0, d) into m disjoint blocks D^(0..m-1).
+ *
+ * Section 3.1 asks for a random, disjoint partition into equally sized
+ * blocks (its footnote's example for d = 4, m = 2: {1,4} and {2,3}, 1-based).
+ * The randomness is fixed so that any implementation reproduces it bit for
+ * bit: a SplitMix64 stream seeded with `seed` (Steele, Lea & Flood 2014)
+ * drives a Fisher-Yates shuffle of [0, d) (for i = d-1 down to 1, j uniform
+ * on [0, i] by rejection of draws >= 2^64 - (2^64 mod (i+1)), j = draw mod
+ * (i+1); swap); block k is shuffled positions [k d/m, (k+1) d/m), sorted.
+ * With GIST_PART_CATEGORICAL each index r (ascending) instead draws its block
+ * uniformly from [0, m) (the i.i.d. categorical masks of the convergence
+ * analysis, Appendix A.1); block sizes are then random and may be zero.
+ *
+ * Host only, synchronous.  Outputs (host memory, caller-allocated):
+ *   idx_out[d]     blocks concatenated, each ascending, 0-based
+ *   offs_out[m+1]  block k is idx_out[offs_out[k] .. offs_out[k+1])
+ * Errors: GIST_E_INVAL if d < 1, m < 1, m > d, a NULL pointer, unknown
+ * flags, or (equal blocks) d % m != 0.  Outputs are untouched on error. */
+gist_status gist_partition(int64_t d, int32_t m, uint64_t seed, uint32_t flags,
+                           int32_t* idx_out, int64_t* offs_out);
+
+/* ---- Cluster mini-batch (Section 3.2; eq. (1); Appendix A.2) --------- */
+
+typedef enum gist_norm {
+  /* Dt^-1/2 (A + I) Dt^-1/2, Dt = 1 + degree: the degree-normalised
+   * adjacency with self-loops of eq. (1) (renormalisation trick). */
+  GIST_NORM_GCN_SYM = 0,
+  /* D^-1 A: GraphSAGE's mean aggregator; no self-loop; a node without
+   * neighbours has an empty row.  Also emits the explicit transpose. */
+  GIST_NORM_SAGE_MEAN = 1,
+  /* I + D^-1/2 A D^-1/2: the aggregation matrix of the analysis. */
+  GIST_NORM_THEORY = 2
+} gist_norm;
+
+/* Global training graph: simple, undirected, no self-loops, stored as a
+ * symmetric CSR with strictly ascending columns; plus its clustering. */
+typedef struct gist_graph {
+  int64_t n;                     /* nodes                                 */
+  const int64_t* rowptr;         /* [n+1]                                 */
+  const int32_t* col;            /* [rowptr[n]]                           */
+  int32_t n_clusters;            /* c                                     */
+  const int64_t* cluster_ptr;    /* [c+1]                                 */
+  const int32_t* cluster_nodes;  /* [cluster_ptr[c]]: node ids per cluster */
+} gist_graph;
+
+/* Mini-batch CSR, host memory.  `cap_n` / `cap_nnz` are the capacities of
+ * the caller's arrays (rowptr and t_rowptr hold cap_n + 1 entries); `n` and
+ * `nnz` are outputs.  If `rowptr` is NULL the call only computes n and nnz
+ * (size query).  t_* are written only for GIST_NORM_SAGE_MEAN (then they
+ * are required). */
+typedef struct gist_csr {
+  int64_t n, nnz;                /* out                                   */
+  int64_t cap_n, cap_nnz;        /* in                                    */
+  int32_t* rowptr;               /* [n+1]                                 */
+  int32_t* col;                  /* [nnz], ascending per row              */
+  float* val;                    /* [nnz]                                 */
+  int32_t* node_map;             /* [n]: local row -> global node id      */
+  int32_t* t_rowptr;             /* transpose (SAGE only)                 */
+  int32_t* t_col;
+  float* t_val;
+} gist_csr;
+
+/* Build the normalised CSR of the subgraph induced by the union of the
+ * clusters `clusters[0 .. n_clusters)` (duplicates allowed, any order);
+ * n_clusters == -1 selects the whole graph (`clusters` may be NULL).
+ *
+ * Section 3.2 makes a mini-batch one cluster or a union of clusters; the
+ * subgraph keeps every edge with both ends selected and degrees are those
+ * of that induced subgraph.  Local rows are the selected nodes in ascending
+ * global id; columns ascend within each row.  Values are computed in fp64
+ * and rounded once to fp32: GCN 1/sqrt(Dt_i Dt_j), SAGE 1/deg_i, THEORY 1
+ * on the diagonal and 1/sqrt(deg_i deg_j) off it -- so GCN and THEORY
+ * matrices are bitwise symmetric.
+ *
+ * Host only, synchronous.  Errors: GIST_E_INVAL (NULL graph arrays, empty
+ * selection, cluster id out of range, bad norm), GIST_E_NOMEM (capacities
+ * too small; n/nnz still report the needed sizes), GIST_E_UNSUPPORTED
+ * (n or nnz >= 2^31). */
+gist_status gist_build_minibatch_csr(const gist_graph* g, const int32_t* clusters,
+                                     int32_t n_clusters, gist_norm norm,
+                                     gist_csr* out);
+
+/* ---- device CSR and layer descriptor -------------------------------- */
+
+typedef struct gist_csr_dev {   /* device memory, layout as gist_csr */
+  int64_t n, nnz;
+  const int32_t* rowptr;        /* [n+1] */
+  const int32_t* col;           /* [nnz] */
+  const float* val;             /* [nnz] */
+} gist_csr_dev;
+
+typedef enum gist_layer_kind { GIST_LAYER_GCN = 0, GIST_LAYER_SAGE_MEAN = 1 } gist_layer_kind;
+typedef enum gist_act { GIST_ACT_NONE = 0, GIST_ACT_RELU = 1 } gist_act;
+typedef enum gist_dtype {
+  GIST_DTYPE_F32 = 0,      /* fp32 operands, fp32 MFMA                        */
+  GIST_DTYPE_BF16_IN = 1   /* GEMM operands rounded to bf16 (nearest-even),    */
+                           /* fp32 accumulation; aggregation stays fp32        */
+} gist_dtype;
+typedef enum gist_order {
+  GIST_ORDER_AUTO = 0,        /* GCN: aggregate at min(s_in, s_out)        */
+  GIST_ORDER_AGG_FIRST = 1,   /* (Abar H) W                                 */
+  GIST_ORDER_XFORM_FIRST = 2  /* Abar (H W)  (GCN only)                     */
+} gist_order;
+
+typedef struct gist_layer_desc {
+  int32_t kind;    /* gist_layer_kind                                   */
+  int32_t act;     /* gist_act: RELU for hidden layers, NONE for the last */
+  int32_t dtype;   /* gist_dtype                                        */
+  int32_t order;   /* gist_order                                        */
+  int64_t n;       /* mini-batch rows                                   */
+  int32_t s_in;    /* sub-GCN input width  |D_l|  (d_0 at layer 0)       */
+  int32_t s_out;   /* sub-GCN output width |D_l+1| (d_L at the last layer) */
+} gist_layer_desc;
+
+/* Workspace (device bytes) that fwd and bwd need for this descriptor. */
+gist_status gist_layer_workspace_size(const gist_layer_desc* L, size_t* fwd_bytes,
+                                      size_t* bwd_bytes);
+
+/* Sub-GCN layer forward, eq. (2): H_out = act(Abar H W), W = Theta^(i)_l.
+ *
+ *   GCN:       Z = (Abar H) W   or  Abar (H W)  (same value; `order`)
+ *   SAGE-mean: Z = H W_self + (Abar H) W_neigh   -- GraphSAGE concatenates
+ *              the aggregated neighbourhood with the node itself; W holds
+ *              [W_self; W_neigh] as one (2 s_in) x s_out matrix.
+ *
+ * H [n x s_in], W [s_in x s_out] (SAGE [2 s_in x s_out]), H_out [n x s_out].
+ * agg_save [n x s_in] receives Abar H (required for SAGE and for GCN when
+ * aggregating first; may be NULL for GCN transform-first).  The ReLU mask
+ * for the backward pass is recovered from H_out (H_out > 0 iff Z > 0).
+ * Errors: GIST_E_INVAL (NULL pointers, widths < 1, unknown enums, SAGE with
+ * XFORM_FIRST), GIST_E_NOMEM (ws_bytes below gist_layer_workspace_size). */
+gist_status gist_gcn_layer_fwd(gist_ctx* ctx, const gist_layer_desc* L,
+                               const gist_csr_dev* A, const float* H,
+                               const float* W, float* agg_save, float* H_out,
+                               void* ws, size_t ws_bytes);
+
+/* Sub-GCN layer backward (chain rule of the forward).
+ *
+ *   dZ = dH_out * 1[H_out > 0] (ReLU) or dH_out (identity)
+ *   GCN:  dW = (Abar H)^T dZ,               dH = Abar^T (dZ W^T)
+ *   SAGE: dW = [H | Abar H]^T dZ  ([2 s_in x s_out]),
+ *         dH = dZ W_self^T + Abar^T (dZ W_neigh^T)
+ *
+ * A_T is the explicit transpose CSR (required for SAGE-mean; NULL for GCN
+ * means Abar is symmetric, as GIST_NORM_GCN_SYM / THEORY produce).
+ * dW is overwritten.  dH may be NULL (layer 0: no input gradient).
+ * Results are deterministic: no atomics, fixed reduction order. */
+gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* L,
+                               const gist_csr_dev* A, const gist_csr_dev* A_T,
+                               const float* H, const float* agg_save,
+                               const float* H_out, const float* W,
+                               const float* dH_out, float* dW, float* dH,
+                               void* ws, size_t ws_bytes);
+
+/* ---- loss (Section 3.1: the sub-GCN output keeps the global width, so the
+ *      loss is the usual one) ---------------------------------------- */
+
+/* Mean softmax cross-entropy over n rows of logits [n x C] with int32
+ * labels in [0, C): *loss_dev (one device float) = mean_v (logsumexp(z_v) -
+ * z_v,y_v); dlogits [n x C] = (softmax(z) - onehot(y)) / n.  `ws` needs
+ * gist_softmax_xent_workspace(n) bytes.  Labels out of range are a caller
+ * error: the kernel clamps nothing and reports it by writing NaN to
+ * *loss_dev. */
+size_t gist_softmax_xent_workspace(int64_t n);
+gist_status gist_softmax_xent(gist_ctx* ctx, int64_t n, int32_t C,
+                              const float* logits, const int32_t* labels,
+                              float* loss_dev, float* dlogits, void* ws,
+                              size_t ws_bytes);
+
+/* ---- subGCNs slice gather (Section 3.1) ----------------------------- */
+
+/* Ws[i][j] = Wg[rows[i]][cols[j]], i < nr, j < nc: the sub-GCN weight
+ * Theta^(i)_l = [Theta_l] restricted to rows D^(i)_l and columns
+ * D^(i)_{l+1}.  rows / cols are device int32 arrays; NULL selects all
+ * (0..nr-1 / 0..nc-1).  Also gathers mini-batch feature rows (cols NULL).
+ * Bit-exact copy.  Indices must lie inside Wg (checked only by the caller). */
+gist_status gist_gather_slice(gist_ctx* ctx, const float* Wg, int64_t ldg,
+                              const int32_t* rows, int32_t nr,
+                              const int32_t* cols, int32_t nc, float* Ws,
+                              int64_t lds);
+
+/* ---- subTrain update (Section 3.2) ---------------------------------- */
+
+/* W[k] -= lr * dW[k] for k < n, in fp32 (one rounding per element). */
+gist_status gist_sgd_update(gist_ctx* ctx, float* W, const float* dW, int64_t n,
+                            float lr);
+
+/* ---- subAgg (Section 3.2) ------------------------------------------- */
+
+#define GIST_SUBAGG_CHECK_FINITE 1u
+
+/* Wg[rows[i]][cols[j]] = Ws[i][j]: each worker's trained slice replaces the
+ * global entries it owns; blocks of different sub-GCNs never overlap, so
+ * calls for different sub-GCNs may run in any order.  Entries outside
+ * every block are left unchanged.  With GIST_SUBAGG_CHECK_FINITE the slice
+ * is first scanned (synchronously) and, if any entry is NaN or Inf, nothing
+ * is written and GIST_E_NONFINITE is returned. */
+gist_status gist_subagg(gist_ctx* ctx, float* Wg, int64_t ldg, const int32_t* rows,
+                        int32_t nr, const int32_t* cols, int32_t nc,
+                        const float* Ws, int64_t lds, uint32_t flags);
+
+/* ---- instrumentation ------------------------------------------------ */
+
+/* Per-kernel timing with HIP events recorded on the context's stream around
+ * every kernel launch the library makes, for measuring kernels against
+ * their rooflines.  gist_profile_begin(ctx, cap) creates `cap` event pairs
+ * (host-side set-up, outside any hot path) and starts recording; while
+ * recording, launches beyond `cap` are not timed (and counted as dropped).
+ * gist_profile_read synchronises the stream and aggregates the records per
+ * kernel variant into `out[0 .. *n)` (at most `out_cap` entries), then
+ * clears them; gist_profile_end stops recording and frees the events.
+ * `flops` counts 2 M N K per GEMM; `bytes` the algorithmic HBM bytes
+ * (each operand read once, each result written once). */
+typedef struct gist_prof_entry {
+  char name[48];      /* kernel variant, e.g. "gemm_f32_KR", "spmm_v4_l64" */
+  int64_t launches;
+  double ms;          /* summed event time */
+  double flops;       /* summed algorithmic flops */
+  double bytes;       /* summed algorithmic bytes */
+} gist_prof_entry;
+
+gist_status gist_profile_begin(gist_ctx* ctx, int64_t cap);
+gist_status gist_profile_read(gist_ctx* ctx, gist_prof_entry* out, int32_t out_cap,
+                              int32_t* n, int64_t* dropped);
+gist_status gist_profile_end(gist_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GIST_H_ */

@@ -1,0 +1,530 @@
+// Context, error state and the device entry points of libgist.
+//
+// The layer entry points only validate arguments and sequence kernels on
+// the context's stream; the arithmetic lives in spmm.hip, gemm.hip and
+// elementwise.hip.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <climits>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "gist_internal.h"
+
+namespace gist {
+
+namespace {
+thread_local std::string t_err;
+}
+
+gist_status set_error(gist_status s, const std::string& msg) {
+  t_err = msg;
+  return s;
+}
+
+void clear_error() { t_err.clear(); }
+
+gist_status check_launch(const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess)
+    return set_error(GIST_E_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+  return GIST_OK;
+}
+
+DeviceGuard::DeviceGuard(int dev) {
+  if (hipGetDevice(&prev_) == hipSuccess && prev_ != dev) {
+    changed_ = hipSetDevice(dev) == hipSuccess;
+  }
+}
+
+DeviceGuard::~DeviceGuard() {
+  if (changed_) (void)hipSetDevice(prev_);
+}
+
+// ---- launch timing ---------------------------------------------------------
+
+struct Profiler {
+  std::vector<hipEvent_t> ev;   // 2 per slot
+  std::vector<std::string> name;
+  std::vector<double> flops, bytes;
+  int64_t used = 0, dropped = 0;
+};
+
+namespace {
+thread_local Profiler* t_prof = nullptr;
+}
+
+ProfBind::ProfBind(gist_ctx* ctx) : prev_(t_prof) { t_prof = ctx ? ctx->prof : nullptr; }
+ProfBind::~ProfBind() { t_prof = prev_; }
+
+ProfScope::ProfScope(hipStream_t st, const char* name, double flops, double bytes) : st_(st) {
+  Profiler* p = t_prof;
+  if (!p) return;
+  if (p->used >= static_cast<int64_t>(p->name.size())) {
+    ++p->dropped;
+    return;
+  }
+  slot_ = static_cast<int>(p->used++);
+  p->name[slot_] = name;
+  p->flops[slot_] = flops;
+  p->bytes[slot_] = bytes;
+  (void)hipEventRecord(p->ev[2 * slot_], st);
+}
+
+ProfScope::~ProfScope() {
+  if (slot_ >= 0 && t_prof) (void)hipEventRecord(t_prof->ev[2 * slot_ + 1], st_);
+}
+
+}  // namespace gist
+
+using gist::set_error;
+
+#define GIST_TRY(expr)                 \
+  do {                                 \
+    gist_status _s = (expr);           \
+    if (_s != GIST_OK) return _s;      \
+  } while (0)
+
+extern "C" const char* gist_last_error(void) { return gist::t_err.c_str(); }
+
+extern "C" const char* gist_status_str(gist_status s) {
+  switch (s) {
+    case GIST_OK: return "GIST_OK";
+    case GIST_E_INVAL: return "GIST_E_INVAL";
+    case GIST_E_NOMEM: return "GIST_E_NOMEM";
+    case GIST_E_DEVICE: return "GIST_E_DEVICE";
+    case GIST_E_UNSUPPORTED: return "GIST_E_UNSUPPORTED";
+    case GIST_E_NONFINITE: return "GIST_E_NONFINITE";
+  }
+  return "GIST_E_UNKNOWN";
+}
+
+extern "C" gist_status gist_create(int device, void* hip_stream, gist_ctx** out) {
+  gist::clear_error();
+  if (!out) return set_error(GIST_E_INVAL, "gist_create: NULL out");
+  int count = 0;
+  hipError_t e = hipGetDeviceCount(&count);
+  if (e != hipSuccess || device < 0 || device >= count)
+    return set_error(GIST_E_DEVICE, "gist_create: no such HIP device");
+  gist::DeviceGuard g(device);
+  gist_ctx* c = new (std::nothrow) gist_ctx;
+  if (!c) return set_error(GIST_E_NOMEM, "gist_create: out of host memory");
+  c->device = device;
+  c->stream = static_cast<hipStream_t>(hip_stream);
+  if (hipMalloc(&c->d_flag, 4 * sizeof(int)) != hipSuccess) {
+    delete c;
+    return set_error(GIST_E_DEVICE, "gist_create: cannot allocate context flag");
+  }
+  *out = c;
+  return GIST_OK;
+}
+
+extern "C" gist_status gist_destroy(gist_ctx* ctx) {
+  gist::clear_error();
+  if (!ctx) return GIST_OK;
+  gist_profile_end(ctx);
+  {
+    gist::DeviceGuard g(ctx->device);
+    if (ctx->d_flag) (void)hipFree(ctx->d_flag);
+  }
+  delete ctx;
+  return GIST_OK;
+}
+
+extern "C" gist_status gist_set_stream(gist_ctx* ctx, void* hip_stream) {
+  gist::clear_error();
+  if (!ctx) return set_error(GIST_E_INVAL, "gist_set_stream: NULL ctx");
+  ctx->stream = static_cast<hipStream_t>(hip_stream);
+  return GIST_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Layer forward / backward
+// ---------------------------------------------------------------------------
+
+namespace {
+
+size_t fbytes(int64_t a, int64_t b) { return static_cast<size_t>(a) * static_cast<size_t>(b) * 4; }
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+int resolve_order(const gist_layer_desc* L) {
+  if (L->kind == GIST_LAYER_SAGE_MEAN) return GIST_ORDER_AGG_FIRST;
+  if (L->order != GIST_ORDER_AUTO) return L->order;
+  return L->s_in <= L->s_out ? GIST_ORDER_AGG_FIRST : GIST_ORDER_XFORM_FIRST;
+}
+
+gist_status check_desc(const gist_layer_desc* L) {
+  if (!L) return set_error(GIST_E_INVAL, "layer: NULL descriptor");
+  if (L->kind != GIST_LAYER_GCN && L->kind != GIST_LAYER_SAGE_MEAN)
+    return set_error(GIST_E_INVAL, "layer: unknown kind");
+  if (L->act != GIST_ACT_NONE && L->act != GIST_ACT_RELU)
+    return set_error(GIST_E_INVAL, "layer: unknown activation");
+  if (L->dtype != GIST_DTYPE_F32 && L->dtype != GIST_DTYPE_BF16_IN)
+    return set_error(GIST_E_INVAL, "layer: unknown dtype");
+  if (L->order < GIST_ORDER_AUTO || L->order > GIST_ORDER_XFORM_FIRST)
+    return set_error(GIST_E_INVAL, "layer: unknown order");
+  if (L->kind == GIST_LAYER_SAGE_MEAN && L->order == GIST_ORDER_XFORM_FIRST)
+    return set_error(GIST_E_INVAL, "layer: SAGE-mean aggregates first");
+  if (L->n < 0 || L->s_in < 1 || L->s_out < 1)
+    return set_error(GIST_E_INVAL, "layer: bad sizes");
+  if (L->n > INT32_MAX) return set_error(GIST_E_UNSUPPORTED, "layer: n exceeds int32 rows");
+  return GIST_OK;
+}
+
+gist_status check_csr(const gist_csr_dev* A, int64_t n, const char* what) {
+  if (!A) return set_error(GIST_E_INVAL, std::string(what) + ": NULL CSR");
+  if (A->n != n) return set_error(GIST_E_INVAL, std::string(what) + ": CSR rows != n");
+  if (A->nnz < 0 || A->nnz > INT32_MAX)
+    return set_error(GIST_E_UNSUPPORTED, std::string(what) + ": nnz outside int32");
+  if (n > 0 && (!A->rowptr || (A->nnz > 0 && (!A->col || !A->val))))
+    return set_error(GIST_E_INVAL, std::string(what) + ": NULL CSR arrays");
+  return GIST_OK;
+}
+
+// Workspace layout of the backward pass: [dZ | tmp | gemm scratch].
+struct BwdPlan {
+  size_t dz = 0, tmp = 0, gemm = 0;
+  size_t total() const { return align256(dz) + align256(tmp) + gemm; }
+};
+
+BwdPlan plan_bwd(const gist_layer_desc* L) {
+  BwdPlan p;
+  const int64_t n = L->n, si = L->s_in, so = L->s_out;
+  if (L->act == GIST_ACT_RELU) p.dz = fbytes(n, so);
+  const int order = resolve_order(L);
+  if (L->kind == GIST_LAYER_SAGE_MEAN) {
+    p.tmp = fbytes(n, si);  // dP = dZ W_neigh^T
+    p.gemm = std::max(gist::gemm_workspace(2 * si, so, n, L->dtype),
+                      gist::gemm_workspace(n, 2 * si, so, L->dtype));
+  } else if (order == GIST_ORDER_AGG_FIRST) {
+    p.tmp = fbytes(n, si);  // dP
+    p.gemm = std::max(gist::gemm_workspace(si, so, n, L->dtype),
+                      gist::gemm_workspace(n, si, so, L->dtype));
+  } else {
+    p.tmp = fbytes(n, so);  // G = Abar^T dZ
+    p.gemm = std::max(gist::gemm_workspace(si, so, n, L->dtype),
+                      gist::gemm_workspace(n, si, so, L->dtype));
+  }
+  return p;
+}
+
+size_t plan_fwd(const gist_layer_desc* L) {
+  const int order = resolve_order(L);
+  size_t t = 0;
+  const int64_t K = L->kind == GIST_LAYER_SAGE_MEAN ? 2 * int64_t(L->s_in) : L->s_in;
+  if (L->kind == GIST_LAYER_GCN && order == GIST_ORDER_XFORM_FIRST) t = fbytes(L->n, L->s_out);
+  return align256(t) + gist::gemm_workspace(L->n, L->s_out, K, L->dtype);
+}
+
+}  // namespace
+
+extern "C" gist_status gist_layer_workspace_size(const gist_layer_desc* L,
+                                                 size_t* fwd_bytes, size_t* bwd_bytes) {
+  gist::clear_error();
+  GIST_TRY(check_desc(L));
+  if (fwd_bytes) *fwd_bytes = plan_fwd(L);
+  if (bwd_bytes) *bwd_bytes = plan_bwd(L).total();
+  return GIST_OK;
+}
+
+extern "C" gist_status gist_gcn_layer_fwd(gist_ctx* ctx, const gist_layer_desc* L,
+                                          const gist_csr_dev* A, const float* H,
+                                          const float* W, float* agg_save,
+                                          float* H_out, void* ws, size_t ws_bytes) {
+  gist::clear_error();
+  if (!ctx) return set_error(GIST_E_INVAL, "layer_fwd: NULL ctx");
+  gist::ProfBind pb(ctx);
+  GIST_TRY(check_desc(L));
+  GIST_TRY(check_csr(A, L->n, "layer_fwd"));
+  const int64_t n = L->n, si = L->s_in, so = L->s_out;
+  const int order = resolve_order(L);
+  const bool sage = L->kind == GIST_LAYER_SAGE_MEAN;
+  if (n > 0 && (!H || !W || !H_out)) return set_error(GIST_E_INVAL, "layer_fwd: NULL pointer");
+  if (n > 0 && (sage || order == GIST_ORDER_AGG_FIRST) && !agg_save)
+    return set_error(GIST_E_INVAL, "layer_fwd: agg_save required");
+  const size_t need = plan_fwd(L);
+  if (ws_bytes < need || (need > 0 && !ws))
+    return set_error(GIST_E_NOMEM, "layer_fwd: workspace too small");
+  if (n == 0) return GIST_OK;
+  gist::DeviceGuard dg(ctx->device);
+  hipStream_t st = ctx->stream;
+  const bool relu = L->act == GIST_ACT_RELU;
+  gist::GemmOut out;
+  out.c0 = H_out;
+  out.ldc0 = so;
+  if (sage || order == GIST_ORDER_AGG_FIRST) {
+    GIST_TRY(gist::spmm(st, n, A->nnz, A->rowptr, A->col, A->val, H, si, int(si), agg_save, si,
+                        nullptr, 0, false));
+    gist::Operand a;
+    a.k_major = true;
+    if (sage) {  // [H | Abar H], concatenated along K
+      a.p0 = H; a.ld0 = si; a.p1 = agg_save; a.ld1 = si; a.split = si;
+    } else {
+      a.p0 = agg_save; a.ld0 = si;
+    }
+    gist::Operand b;  // W is (K x s_out) row-major: an N x K operand, N contiguous
+    b.p0 = W; b.ld0 = so; b.k_major = false;
+    out.relu = relu;
+    const int64_t K = sage ? 2 * si : si;
+    return gist::gemm(st, n, so, K, a, b, out, L->dtype, ws, ws_bytes);
+  }
+  // transform first: T = H W (workspace), H_out = act(Abar T)
+  float* T = static_cast<float*>(ws);
+  void* gws = static_cast<char*>(ws) + align256(fbytes(n, so));
+  gist::Operand a;
+  a.p0 = H; a.ld0 = si; a.k_major = true;
+  gist::Operand b;
+  b.p0 = W; b.ld0 = so; b.k_major = false;
+  gist::GemmOut t;
+  t.c0 = T; t.ldc0 = so;
+  GIST_TRY(gist::gemm(st, n, so, si, a, b, t, L->dtype, gws, ws_bytes - align256(fbytes(n, so))));
+  return gist::spmm(st, n, A->nnz, A->rowptr, A->col, A->val, T, so, int(so), H_out, so, nullptr, 0,
+                    relu);
+}
+
+extern "C" gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* L,
+                                          const gist_csr_dev* A, const gist_csr_dev* A_T,
+                                          const float* H, const float* agg_save,
+                                          const float* H_out, const float* W,
+                                          const float* dH_out, float* dW, float* dH,
+                                          void* ws, size_t ws_bytes) {
+  gist::clear_error();
+  if (!ctx) return set_error(GIST_E_INVAL, "layer_bwd: NULL ctx");
+  gist::ProfBind pb(ctx);
+  GIST_TRY(check_desc(L));
+  GIST_TRY(check_csr(A, L->n, "layer_bwd"));
+  const bool sage = L->kind == GIST_LAYER_SAGE_MEAN;
+  if (sage) GIST_TRY(check_csr(A_T, L->n, "layer_bwd (transpose)"));
+  else if (A_T) GIST_TRY(check_csr(A_T, L->n, "layer_bwd (transpose)"));
+  const int64_t n = L->n, si = L->s_in, so = L->s_out;
+  const int order = resolve_order(L);
+  const bool relu = L->act == GIST_ACT_RELU;
+  if (!dW || !W) return set_error(GIST_E_INVAL, "layer_bwd: NULL dW or W");
+  if (n > 0 && (!H || !dH_out || (relu && !H_out)))
+    return set_error(GIST_E_INVAL, "layer_bwd: NULL pointer");
+  if (n > 0 && (sage || order == GIST_ORDER_AGG_FIRST) && !agg_save)
+    return set_error(GIST_E_INVAL, "layer_bwd: agg_save required");
+  const BwdPlan p = plan_bwd(L);
+  if (ws_bytes < p.total() || (p.total() > 0 && !ws))
+    return set_error(GIST_E_NOMEM, "layer_bwd: workspace too small");
+  gist::DeviceGuard dg(ctx->device);
+  hipStream_t st = ctx->stream;
+  const int64_t wrows = sage ? 2 * si : si;
+  if (n == 0) return gist::fill_zero(st, dW, wrows * so);  // empty batch: zero gradient
+  char* base = static_cast<char*>(ws);
+  float* dZbuf = reinterpret_cast<float*>(base);
+  float* tmp = reinterpret_cast<float*>(base + align256(p.dz));
+  void* gws = base + align256(p.dz) + align256(p.tmp);
+  const size_t gbytes = p.gemm;
+  const float* dZ = dH_out;
+  if (relu) {
+    GIST_TRY(gist::relu_mask(st, n * so, dH_out, H_out, dZbuf));
+    dZ = dZbuf;
+  }
+  const gist_csr_dev* AT = A_T ? A_T : A;
+
+  gist::Operand dz_as_b;  // dZ (n x s_out): B operand of the weight gradient, N = s_out, K = n
+  dz_as_b.p0 = dZ; dz_as_b.ld0 = so; dz_as_b.k_major = false;
+  gist::GemmOut wout;
+  wout.c0 = dW; wout.ldc0 = so;
+
+  if (sage || order == GIST_ORDER_AGG_FIRST) {
+    // dW = [H | Abar H]^T dZ (SAGE) or (Abar H)^T dZ: A operand is (rows x n), n contiguous... as
+    // stored, element (r, k) of the transposed activation is act[k * ld + r].
+    gist::Operand a;
+    a.k_major = false;
+    if (sage) { a.p0 = H; a.ld0 = si; a.p1 = agg_save; a.ld1 = si; a.split = si; }
+    else { a.p0 = agg_save; a.ld0 = si; }
+    GIST_TRY(gist::gemm(st, wrows, so, n, a, dz_as_b, wout, L->dtype, gws, gbytes));
+    if (!dH) return GIST_OK;
+    // [dH_self | dP] = dZ W^T (SAGE), dP = dZ W^T (GCN): A = dZ (n x s_out, K contiguous),
+    // B = W^T as an N x K operand = W itself (rows = N, K contiguous).
+    gist::Operand a2;
+    a2.p0 = dZ; a2.ld0 = so; a2.k_major = true;
+    gist::Operand b2;
+    b2.p0 = W; b2.ld0 = so; b2.k_major = true;
+    gist::GemmOut o2;
+    if (sage) { o2.c0 = dH; o2.ldc0 = si; o2.c1 = tmp; o2.ldc1 = si; o2.c_split = si; }
+    else { o2.c0 = tmp; o2.ldc0 = si; }
+    GIST_TRY(gist::gemm(st, n, wrows, so, a2, b2, o2, L->dtype, gws, gbytes));
+    // dH (+)= Abar^T dP
+    return gist::spmm(st, n, AT->nnz, AT->rowptr, AT->col, AT->val, tmp, si, int(si), dH, si,
+                      sage ? dH : nullptr, si, false);
+  }
+  // GCN transform-first: G = Abar^T dZ; dW = H^T G; dH = G W^T
+  GIST_TRY(gist::spmm(st, n, AT->nnz, AT->rowptr, AT->col, AT->val, dZ, so, int(so), tmp, so, nullptr,
+                      0, false));
+  gist::Operand a;
+  a.p0 = H; a.ld0 = si; a.k_major = false;
+  gist::Operand g;
+  g.p0 = tmp; g.ld0 = so; g.k_major = false;
+  GIST_TRY(gist::gemm(st, si, so, n, a, g, wout, L->dtype, gws, gbytes));
+  if (!dH) return GIST_OK;
+  gist::Operand a2;
+  a2.p0 = tmp; a2.ld0 = so; a2.k_major = true;
+  gist::Operand b2;
+  b2.p0 = W; b2.ld0 = so; b2.k_major = true;
+  gist::GemmOut o2;
+  o2.c0 = dH; o2.ldc0 = si;
+  return gist::gemm(st, n, si, so, a2, b2, o2, L->dtype, gws, gbytes);
+}
+
+// ---------------------------------------------------------------------------
+// Loss, gather, SGD, subAgg
+// ---------------------------------------------------------------------------
+
+extern "C" size_t gist_softmax_xent_workspace(int64_t n) {
+  // one partial sum per 4-row block (one wave per row)
+  if (n < 0) n = 0;
+  return align256(static_cast<size_t>((n + 3) / 4 + 1) * sizeof(float));
+}
+
+extern "C" gist_status gist_softmax_xent(gist_ctx* ctx, int64_t n, int32_t C,
+                                         const float* logits, const int32_t* labels,
+                                         float* loss_dev, float* dlogits, void* ws,
+                                         size_t ws_bytes) {
+  gist::clear_error();
+  if (!ctx) return set_error(GIST_E_INVAL, "softmax_xent: NULL ctx");
+  gist::ProfBind pb(ctx);
+  if (n < 0 || C < 1) return set_error(GIST_E_INVAL, "softmax_xent: bad sizes");
+  if (!loss_dev || (n > 0 && (!logits || !labels || !dlogits)))
+    return set_error(GIST_E_INVAL, "softmax_xent: NULL pointer");
+  if (n > INT32_MAX) return set_error(GIST_E_UNSUPPORTED, "softmax_xent: n exceeds int32");
+  if (ws_bytes < gist_softmax_xent_workspace(n) || !ws)
+    return set_error(GIST_E_NOMEM, "softmax_xent: workspace too small");
+  gist::DeviceGuard dg(ctx->device);
+  return gist::softmax_xent(ctx->stream, n, C, logits, labels, loss_dev, dlogits,
+                            static_cast<float*>(ws));
+}
+
+extern "C" gist_status gist_gather_slice(gist_ctx* ctx, const float* Wg, int64_t ldg,
+                                         const int32_t* rows, int32_t nr,
+                                         const int32_t* cols, int32_t nc, float* Ws,
+                                         int64_t lds) {
+  gist::clear_error();
+  if (!ctx) return set_error(GIST_E_INVAL, "gather_slice: NULL ctx");
+  gist::ProfBind pb(ctx);
+  if (nr < 0 || nc < 0 || lds < nc || ldg < 1 || (!cols && ldg < nc))
+    return set_error(GIST_E_INVAL, "gather_slice: bad sizes");
+  if (nr == 0 || nc == 0) return GIST_OK;
+  if (!Wg || !Ws) return set_error(GIST_E_INVAL, "gather_slice: NULL pointer");
+  gist::DeviceGuard dg(ctx->device);
+  return gist::gather(ctx->stream, Wg, ldg, rows, nr, cols, nc, Ws, lds);
+}
+
+extern "C" gist_status gist_sgd_update(gist_ctx* ctx, float* W, const float* dW, int64_t n,
+                                       float lr) {
+  gist::clear_error();
+  if (!ctx) return set_error(GIST_E_INVAL, "sgd_update: NULL ctx");
+  gist::ProfBind pb(ctx);
+  if (n < 0) return set_error(GIST_E_INVAL, "sgd_update: n < 0");
+  if (n == 0) return GIST_OK;
+  if (!W || !dW) return set_error(GIST_E_INVAL, "sgd_update: NULL pointer");
+  gist::DeviceGuard dg(ctx->device);
+  return gist::sgd(ctx->stream, W, dW, n, lr);
+}
+
+extern "C" gist_status gist_subagg(gist_ctx* ctx, float* Wg, int64_t ldg,
+                                   const int32_t* rows, int32_t nr, const int32_t* cols,
+                                   int32_t nc, const float* Ws, int64_t lds, uint32_t flags) {
+  gist::clear_error();
+  if (!ctx) return set_error(GIST_E_INVAL, "subagg: NULL ctx");
+  gist::ProfBind pb(ctx);
+  if (flags & ~GIST_SUBAGG_CHECK_FINITE) return set_error(GIST_E_INVAL, "subagg: unknown flags");
+  if (nr < 0 || nc < 0 || lds < nc || ldg < 1 || (!cols && ldg < nc))
+    return set_error(GIST_E_INVAL, "subagg: bad sizes");
+  if (nr == 0 || nc == 0) return GIST_OK;
+  if (!Wg || !Ws) return set_error(GIST_E_INVAL, "subagg: NULL pointer");
+  gist::DeviceGuard dg(ctx->device);
+  if (flags & GIST_SUBAGG_CHECK_FINITE) {
+    GIST_TRY(gist::count_nonfinite(ctx->stream, Ws, lds, nr, nc, ctx->d_flag));
+    int bad = 0;
+    if (hipMemcpyAsync(&bad, ctx->d_flag, sizeof(int), hipMemcpyDeviceToHost, ctx->stream) !=
+            hipSuccess ||
+        hipStreamSynchronize(ctx->stream) != hipSuccess)
+      return gist::check_launch("subagg: finite check");
+    if (bad) return set_error(GIST_E_NONFINITE, "subagg: slice holds NaN or Inf; nothing written");
+  }
+  return gist::scatter(ctx->stream, Wg, ldg, rows, nr, cols, nc, Ws, lds);
+}
+
+// ---------------------------------------------------------------------------
+// Instrumentation
+// ---------------------------------------------------------------------------
+
+extern "C" gist_status gist_profile_begin(gist_ctx* ctx, int64_t cap) {
+  gist::clear_error();
+  if (!ctx) return set_error(GIST_E_INVAL, "profile_begin: NULL ctx");
+  if (cap < 1 || cap > (1 << 22)) return set_error(GIST_E_INVAL, "profile_begin: bad capacity");
+  gist_profile_end(ctx);
+  gist::DeviceGuard dg(ctx->device);
+  auto* p = new (std::nothrow) gist::Profiler;
+  if (!p) return set_error(GIST_E_NOMEM, "profile_begin: out of host memory");
+  p->ev.resize(static_cast<size_t>(2 * cap));
+  for (auto& e : p->ev) {
+    if (hipEventCreate(&e) != hipSuccess) {
+      e = nullptr;
+      for (auto& f : p->ev)
+        if (f) (void)hipEventDestroy(f);
+      delete p;
+      return set_error(GIST_E_DEVICE, "profile_begin: hipEventCreate failed");
+    }
+  }
+  p->name.resize(static_cast<size_t>(cap));
+  p->flops.assign(static_cast<size_t>(cap), 0.0);
+  p->bytes.assign(static_cast<size_t>(cap), 0.0);
+  ctx->prof = p;
+  return GIST_OK;
+}
+
+extern "C" gist_status gist_profile_read(gist_ctx* ctx, gist_prof_entry* out, int32_t out_cap,
+                                         int32_t* n, int64_t* dropped) {
+  gist::clear_error();
+  if (!ctx || !n) return set_error(GIST_E_INVAL, "profile_read: NULL argument");
+  *n = 0;
+  gist::Profiler* p = ctx->prof;
+  if (!p) return set_error(GIST_E_INVAL, "profile_read: profiling not started");
+  gist::DeviceGuard dg(ctx->device);
+  if (hipStreamSynchronize(ctx->stream) != hipSuccess) return gist::check_launch("profile_read");
+  std::map<std::string, gist_prof_entry> agg;
+  for (int64_t i = 0; i < p->used; ++i) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, p->ev[2 * i], p->ev[2 * i + 1]) != hipSuccess)
+      return gist::check_launch("profile_read: elapsed time");
+    gist_prof_entry& e = agg[p->name[i]];
+    std::strncpy(e.name, p->name[i].c_str(), sizeof(e.name) - 1);
+    e.launches += 1;
+    e.ms += ms;
+    e.flops += p->flops[i];
+    e.bytes += p->bytes[i];
+  }
+  if (dropped) *dropped = p->dropped;
+  int32_t k = 0;
+  for (auto& kv : agg) {
+    if (k >= out_cap) break;
+    if (out) out[k] = kv.second;
+    ++k;
+  }
+  *n = k;
+  p->used = 0;
+  p->dropped = 0;
+  return GIST_OK;
+}
+
+extern "C" gist_status gist_profile_end(gist_ctx* ctx) {
+  if (!ctx) return set_error(GIST_E_INVAL, "profile_end: NULL ctx");
+  gist::Profiler* p = ctx->prof;
+  if (!p) return GIST_OK;
+  gist::DeviceGuard dg(ctx->device);
+  (void)hipStreamSynchronize(ctx->stream);
+  for (auto& e : p->ev)
+    if (e) (void)hipEventDestroy(e);
+  delete p;
+  ctx->prof = nullptr;
+  return GIST_OK;
+}

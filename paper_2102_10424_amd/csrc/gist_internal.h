@@ -1,0 +1,120 @@
+// Internal declarations shared by the libgist sources (not part of the ABI).
+#pragma once
+
+#include <cstddef>
+#include <climits>
+#include <cstdint>
+#include <string>
+
+#include "../../include/gist.h"
+
+struct ihipStream_t;
+typedef struct ihipStream_t* hipStream_t;
+
+namespace gist {
+struct Profiler;
+}
+
+struct gist_ctx {
+  int device = 0;
+  hipStream_t stream = nullptr;
+  int* d_flag = nullptr;   // 4 ints of device memory owned by the context
+  gist::Profiler* prof = nullptr;
+};
+
+namespace gist {
+
+// Launch timing (gist_profile_*).  The entry points install the calling
+// context's profiler for the duration of the call (ProfBind); launchers wrap
+// each kernel launch in a ProfScope, which records an event pair on the
+// launch stream when a profiler is recording.
+class ProfBind {
+ public:
+  explicit ProfBind(gist_ctx* ctx);
+  ~ProfBind();
+ private:
+  Profiler* prev_;
+};
+
+class ProfScope {
+ public:
+  ProfScope(hipStream_t st, const char* name, double flops, double bytes);
+  ~ProfScope();
+ private:
+  int slot_ = -1;
+  hipStream_t st_;
+};
+
+// Thread-local error message; set_error returns the status for chaining.
+gist_status set_error(gist_status s, const std::string& msg);
+void clear_error();
+
+// Convert the last HIP error of a launch into GIST_E_DEVICE.
+gist_status check_launch(const char* what);
+
+// Make `ctx->device` current for the duration of a call.
+class DeviceGuard {
+ public:
+  explicit DeviceGuard(int dev);
+  ~DeviceGuard();
+ private:
+  int prev_ = -1;
+  bool changed_ = false;
+};
+
+// ---- kernel launchers (implemented in the .hip files) -------------------
+
+// Y[r, c] = sum_e val[e] * X[col[e], c]  (+ Add[r, c]) (ReLU optional),
+// r < n, c < width.  Row-major with leading dimensions.  `add` may alias Y.
+gist_status spmm(hipStream_t st, int64_t n, int64_t nnz, const int32_t* rowptr,
+                 const int32_t* col, const float* val, const float* X,
+                 int64_t ldx, int width, float* Y, int64_t ldy,
+                 const float* add, int64_t ld_add, bool relu);
+
+// Operand of a GEMM: logical R x K matrix (R = M for A, N for B).
+//   k_major == true : element (r, k) at p[r * ld + k]   (K contiguous)
+//   k_major == false: element (r, k) at p[k * ld + r]   (R contiguous)
+// A second pointer p1 takes over from index `split` along the concatenated
+// dimension: along K when k_major, along R otherwise (SAGE's [H | Abar H]).
+struct Operand {
+  const float* p0 = nullptr;
+  const float* p1 = nullptr;
+  int64_t ld0 = 0, ld1 = 0;
+  int64_t split = INT64_MAX;
+  bool k_major = true;
+};
+
+// C (M x N) = act(A (M x K) * B (K x N)), with B given as an N x K operand.
+// Columns >= c_split go to C1 (column index minus c_split).
+struct GemmOut {
+  float* c0 = nullptr;
+  float* c1 = nullptr;
+  int64_t ldc0 = 0, ldc1 = 0;
+  int64_t c_split = INT64_MAX;
+  bool relu = false;
+};
+
+size_t gemm_workspace(int64_t M, int64_t N, int64_t K, int dtype);
+gist_status gemm(hipStream_t st, int64_t M, int64_t N, int64_t K,
+                 const Operand& A, const Operand& B, const GemmOut& C, int dtype,
+                 void* ws, size_t ws_bytes);
+
+// dZ[i] = dH[i] * (Hout[i] > 0) over n x w (ld = w).
+gist_status relu_mask(hipStream_t st, int64_t count, const float* dH,
+                      const float* Hout, float* dZ);
+
+gist_status gather(hipStream_t st, const float* Wg, int64_t ldg,
+                   const int32_t* rows, int32_t nr, const int32_t* cols,
+                   int32_t nc, float* Ws, int64_t lds);
+gist_status scatter(hipStream_t st, float* Wg, int64_t ldg, const int32_t* rows,
+                    int32_t nr, const int32_t* cols, int32_t nc, const float* Ws,
+                    int64_t lds);
+gist_status count_nonfinite(hipStream_t st, const float* Ws, int64_t lds,
+                            int32_t nr, int32_t nc, int* d_count);
+gist_status fill_zero(hipStream_t st, float* p, int64_t count);
+gist_status sgd(hipStream_t st, float* W, const float* dW, int64_t n, float lr);
+gist_status softmax_xent(hipStream_t st, int64_t n, int C, const float* logits,
+                         const int32_t* labels, float* loss, float* dlogits,
+                         float* partials);
+
+}  // namespace gist

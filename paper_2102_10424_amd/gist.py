@@ -1,0 +1,328 @@
+"""ctypes binding of ``libgist.so`` (the C ABI declared in ``include/gist.h``).
+
+Argument marshalling only: every function here forwards to the entry point
+of the same name.  Device buffers are torch tensors (PyTorch supplies device
+memory and the current HIP stream); host buffers are NumPy arrays.  Errors
+raise :class:`GistError` carrying the library's status and message.
+
+The library must be built (``python -m paper_2102_10424_amd.build``); if it
+is missing this module raises on import rather than falling back to any
+other implementation.
+"""
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libgist.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        f"libgist.so not found at {LIB_PATH}: build it with "
+        "`python -m paper_2102_10424_amd.build` (hipcc, gfx950)")
+
+_lib = C.CDLL(LIB_PATH)
+
+# ---- enums / flags (mirror include/gist.h) ---------------------------------
+GIST_OK = 0
+GIST_E_INVAL = -1
+GIST_E_NOMEM = -2
+GIST_E_DEVICE = -3
+GIST_E_UNSUPPORTED = -4
+GIST_E_NONFINITE = -5
+
+GIST_PART_CATEGORICAL = 1
+GIST_NORM_GCN_SYM, GIST_NORM_SAGE_MEAN, GIST_NORM_THEORY = 0, 1, 2
+GIST_LAYER_GCN, GIST_LAYER_SAGE_MEAN = 0, 1
+GIST_ACT_NONE, GIST_ACT_RELU = 0, 1
+GIST_DTYPE_F32, GIST_DTYPE_BF16_IN = 0, 1
+GIST_ORDER_AUTO, GIST_ORDER_AGG_FIRST, GIST_ORDER_XFORM_FIRST = 0, 1, 2
+GIST_SUBAGG_CHECK_FINITE = 1
+
+NORM_BY_NAME = {"gcn": GIST_NORM_GCN_SYM, "sage": GIST_NORM_SAGE_MEAN,
+                "theory": GIST_NORM_THEORY}
+
+# Every symbol include/gist.h declares.
+EXPORTED = (
+    "gist_last_error", "gist_status_str", "gist_create", "gist_destroy",
+    "gist_set_stream", "gist_partition", "gist_build_minibatch_csr",
+    "gist_layer_workspace_size", "gist_gcn_layer_fwd", "gist_gcn_layer_bwd",
+    "gist_softmax_xent_workspace", "gist_softmax_xent", "gist_gather_slice",
+    "gist_sgd_update", "gist_subagg", "gist_profile_begin", "gist_profile_read",
+    "gist_profile_end",
+)
+
+
+class GistError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"{status_str(status)}: {msg}")
+        self.status = status
+
+
+# ---- structures --------------------------------------------------------------
+class gist_graph(C.Structure):
+    _fields_ = [("n", C.c_int64), ("rowptr", C.c_void_p), ("col", C.c_void_p),
+                ("n_clusters", C.c_int32), ("cluster_ptr", C.c_void_p),
+                ("cluster_nodes", C.c_void_p)]
+
+
+class gist_csr(C.Structure):
+    _fields_ = [("n", C.c_int64), ("nnz", C.c_int64), ("cap_n", C.c_int64),
+                ("cap_nnz", C.c_int64), ("rowptr", C.c_void_p), ("col", C.c_void_p),
+                ("val", C.c_void_p), ("node_map", C.c_void_p),
+                ("t_rowptr", C.c_void_p), ("t_col", C.c_void_p), ("t_val", C.c_void_p)]
+
+
+class gist_csr_dev(C.Structure):
+    _fields_ = [("n", C.c_int64), ("nnz", C.c_int64), ("rowptr", C.c_void_p),
+                ("col", C.c_void_p), ("val", C.c_void_p)]
+
+
+class gist_layer_desc(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("act", C.c_int32), ("dtype", C.c_int32),
+                ("order", C.c_int32), ("n", C.c_int64), ("s_in", C.c_int32),
+                ("s_out", C.c_int32)]
+
+
+class gist_prof_entry(C.Structure):
+    _fields_ = [("name", C.c_char * 48), ("launches", C.c_int64), ("ms", C.c_double),
+                ("flops", C.c_double), ("bytes", C.c_double)]
+
+
+_P = C.c_void_p
+_sigs = {
+    "gist_profile_begin": (C.c_int, [_P, C.c_int64]),
+    "gist_profile_read": (C.c_int, [_P, C.POINTER(gist_prof_entry), C.c_int32,
+                                    C.POINTER(C.c_int32), C.POINTER(C.c_int64)]),
+    "gist_profile_end": (C.c_int, [_P]),
+    "gist_last_error": (C.c_char_p, []),
+    "gist_status_str": (C.c_char_p, [C.c_int]),
+    "gist_create": (C.c_int, [C.c_int, _P, C.POINTER(_P)]),
+    "gist_destroy": (C.c_int, [_P]),
+    "gist_set_stream": (C.c_int, [_P, _P]),
+    "gist_partition": (C.c_int, [C.c_int64, C.c_int32, C.c_uint64, C.c_uint32, _P, _P]),
+    "gist_build_minibatch_csr": (C.c_int, [C.POINTER(gist_graph), _P, C.c_int32, C.c_int,
+                                           C.POINTER(gist_csr)]),
+    "gist_layer_workspace_size": (C.c_int, [C.POINTER(gist_layer_desc),
+                                            C.POINTER(C.c_size_t), C.POINTER(C.c_size_t)]),
+    "gist_gcn_layer_fwd": (C.c_int, [_P, C.POINTER(gist_layer_desc), C.POINTER(gist_csr_dev),
+                                     _P, _P, _P, _P, _P, C.c_size_t]),
+    "gist_gcn_layer_bwd": (C.c_int, [_P, C.POINTER(gist_layer_desc), C.POINTER(gist_csr_dev),
+                                     C.POINTER(gist_csr_dev), _P, _P, _P, _P, _P, _P, _P, _P,
+                                     C.c_size_t]),
+    "gist_softmax_xent_workspace": (C.c_size_t, [C.c_int64]),
+    "gist_softmax_xent": (C.c_int, [_P, C.c_int64, C.c_int32, _P, _P, _P, _P, _P, C.c_size_t]),
+    "gist_gather_slice": (C.c_int, [_P, _P, C.c_int64, _P, C.c_int32, _P, C.c_int32, _P,
+                                    C.c_int64]),
+    "gist_sgd_update": (C.c_int, [_P, _P, _P, C.c_int64, C.c_float]),
+    "gist_subagg": (C.c_int, [_P, _P, C.c_int64, _P, C.c_int32, _P, C.c_int32, _P, C.c_int64,
+                              C.c_uint32]),
+}
+for _name, (_res, _args) in _sigs.items():
+    _f = getattr(_lib, _name)
+    _f.restype = _res
+    _f.argtypes = _args
+
+
+def status_str(s):
+    return _lib.gist_status_str(int(s)).decode()
+
+
+def _check(status):
+    if status != GIST_OK:
+        raise GistError(status, _lib.gist_last_error().decode())
+
+
+def _ptr(x):
+    """Address of a torch tensor / NumPy array (None -> NULL)."""
+    if x is None:
+        return None
+    if isinstance(x, np.ndarray):
+        if not x.flags["C_CONTIGUOUS"]:
+            raise ValueError("host array must be C-contiguous")
+        return x.ctypes.data
+    return x.data_ptr()
+
+
+# ---- context -----------------------------------------------------------------
+class Context:
+    """A ``gist_ctx`` bound to a device and (by default) torch's current stream."""
+
+    def __init__(self, device=0, stream=None):
+        import torch
+        if stream is None:
+            stream = torch.cuda.current_stream(device).cuda_stream
+        h = _P()
+        _check(_lib.gist_create(int(device), _P(stream), C.byref(h)))
+        self.handle = h
+        self.device = device
+
+    def set_stream(self, stream):
+        _check(_lib.gist_set_stream(self.handle, _P(stream)))
+
+    def close(self):
+        if self.handle:
+            _lib.gist_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+# ---- host calls ----------------------------------------------------------------
+def gist_partition(d, m, seed, flags=0):
+    """Returns (idx int32[d], offs int64[m+1])."""
+    idx = np.empty(max(int(d), 1), dtype=np.int32)
+    offs = np.empty(max(int(m), 0) + 1, dtype=np.int64)
+    _check(_lib.gist_partition(int(d), int(m), int(seed) & (2**64 - 1), int(flags),
+                               _ptr(idx), _ptr(offs)))
+    return idx[:int(d)], offs
+
+
+def _graph_struct(graph):
+    keep = dict(rowptr=np.ascontiguousarray(graph.rowptr, dtype=np.int64),
+                col=np.ascontiguousarray(graph.col, dtype=np.int32),
+                cptr=np.ascontiguousarray(graph.cluster_ptr, dtype=np.int64),
+                cnodes=np.ascontiguousarray(graph.cluster_nodes, dtype=np.int32))
+    g = gist_graph(int(graph.n), _ptr(keep["rowptr"]), _ptr(keep["col"]),
+                   int(keep["cptr"].shape[0] - 1), _ptr(keep["cptr"]), _ptr(keep["cnodes"]))
+    return g, keep
+
+
+def gist_build_minibatch_csr(graph, clusters, norm):
+    """Mini-batch CSR of the union of ``clusters`` (None: full graph) as NumPy arrays."""
+    norm_id = NORM_BY_NAME[norm] if isinstance(norm, str) else int(norm)
+    g, keep = _graph_struct(graph)
+    if clusters is None:
+        sel, nsel = None, -1
+    else:
+        sel = np.ascontiguousarray(clusters, dtype=np.int32)
+        nsel = int(sel.shape[0])
+    q = gist_csr()
+    _check(_lib.gist_build_minibatch_csr(C.byref(g), _ptr(sel), nsel, norm_id, C.byref(q)))
+    n, nnz = int(q.n), int(q.nnz)
+    out = dict(n=n, nnz=nnz,
+               rowptr=np.empty(n + 1, dtype=np.int32), col=np.empty(max(nnz, 1), dtype=np.int32),
+               val=np.empty(max(nnz, 1), dtype=np.float32),
+               node_map=np.empty(max(n, 1), dtype=np.int32))
+    sage = norm_id == GIST_NORM_SAGE_MEAN
+    if sage:
+        out.update(t_rowptr=np.empty(n + 1, dtype=np.int32),
+                   t_col=np.empty(max(nnz, 1), dtype=np.int32),
+                   t_val=np.empty(max(nnz, 1), dtype=np.float32))
+    q.cap_n, q.cap_nnz = n, nnz
+    q.rowptr, q.col, q.val = _ptr(out["rowptr"]), _ptr(out["col"]), _ptr(out["val"])
+    q.node_map = _ptr(out["node_map"])
+    if sage:
+        q.t_rowptr, q.t_col, q.t_val = (_ptr(out["t_rowptr"]), _ptr(out["t_col"]),
+                                        _ptr(out["t_val"]))
+    _check(_lib.gist_build_minibatch_csr(C.byref(g), _ptr(sel), nsel, norm_id, C.byref(q)))
+    for k in ("col", "val", "t_col", "t_val"):
+        if k in out:
+            out[k] = out[k][:nnz]
+    out["node_map"] = out["node_map"][:n]
+    return out
+
+
+class GraphHandle:
+    """A ``gist_graph`` over NumPy arrays kept alive with it (build once, reuse)."""
+
+    def __init__(self, graph):
+        self.struct, self._keep = _graph_struct(graph)
+
+
+def build_minibatch_into(graph_handle, clusters, norm, q):
+    """``gist_build_minibatch_csr`` into caller-provided buffers described by ``q``."""
+    norm_id = NORM_BY_NAME[norm] if isinstance(norm, str) else int(norm)
+    if clusters is None:
+        sel, nsel = None, -1
+    else:
+        sel = np.ascontiguousarray(clusters, dtype=np.int32)
+        nsel = int(sel.shape[0])
+    _check(_lib.gist_build_minibatch_csr(C.byref(graph_handle.struct), _ptr(sel), nsel,
+                                         norm_id, C.byref(q)))
+    return q
+
+
+# ---- device calls --------------------------------------------------------------
+def csr_dev(n, nnz, rowptr, col, val):
+    """A ``gist_csr_dev`` over torch device tensors (the tensors must outlive it)."""
+    return gist_csr_dev(int(n), int(nnz), _ptr(rowptr), _ptr(col), _ptr(val))
+
+
+def layer_desc(kind, act, n, s_in, s_out, dtype=GIST_DTYPE_F32, order=GIST_ORDER_AUTO):
+    return gist_layer_desc(int(kind), int(act), int(dtype), int(order), int(n), int(s_in),
+                           int(s_out))
+
+
+def gist_layer_workspace_size(desc):
+    f, b = C.c_size_t(), C.c_size_t()
+    _check(_lib.gist_layer_workspace_size(C.byref(desc), C.byref(f), C.byref(b)))
+    return int(f.value), int(b.value)
+
+
+def _nbytes(t):
+    return 0 if t is None else t.numel() * t.element_size()
+
+
+def gist_gcn_layer_fwd(ctx, desc, A, H, W, agg_save, H_out, ws):
+    _check(_lib.gist_gcn_layer_fwd(ctx.handle, C.byref(desc), C.byref(A), _ptr(H), _ptr(W),
+                                   _ptr(agg_save), _ptr(H_out), _ptr(ws), _nbytes(ws)))
+
+
+def gist_gcn_layer_bwd(ctx, desc, A, A_T, H, agg_save, H_out, W, dH_out, dW, dH, ws):
+    _check(_lib.gist_gcn_layer_bwd(ctx.handle, C.byref(desc), C.byref(A),
+                                   C.byref(A_T) if A_T is not None else None, _ptr(H),
+                                   _ptr(agg_save), _ptr(H_out), _ptr(W), _ptr(dH_out),
+                                   _ptr(dW), _ptr(dH), _ptr(ws), _nbytes(ws)))
+
+
+def gist_softmax_xent_workspace(n):
+    return int(_lib.gist_softmax_xent_workspace(int(n)))
+
+
+def gist_softmax_xent(ctx, n, C_, logits, labels, loss_dev, dlogits, ws):
+    _check(_lib.gist_softmax_xent(ctx.handle, int(n), int(C_), _ptr(logits), _ptr(labels),
+                                  _ptr(loss_dev), _ptr(dlogits), _ptr(ws), _nbytes(ws)))
+
+
+def gist_gather_slice(ctx, Wg, ldg, rows, nr, cols, nc, Ws, lds):
+    _check(_lib.gist_gather_slice(ctx.handle, _ptr(Wg), int(ldg), _ptr(rows), int(nr),
+                                  _ptr(cols), int(nc), _ptr(Ws), int(lds)))
+
+
+def gist_sgd_update(ctx, W, dW, n, lr):
+    _check(_lib.gist_sgd_update(ctx.handle, _ptr(W), _ptr(dW), int(n), float(lr)))
+
+
+def gist_subagg(ctx, Wg, ldg, rows, nr, cols, nc, Ws, lds, flags=0):
+    _check(_lib.gist_subagg(ctx.handle, _ptr(Wg), int(ldg), _ptr(rows), int(nr), _ptr(cols),
+                            int(nc), _ptr(Ws), int(lds), int(flags)))
+
+
+# ---- instrumentation ------------------------------------------------------------
+def gist_profile_begin(ctx, cap=65536):
+    _check(_lib.gist_profile_begin(ctx.handle, int(cap)))
+
+
+def gist_profile_read(ctx):
+    """Synchronise and return {variant: dict(launches, ms, flops, bytes)}, plus dropped."""
+    buf = (gist_prof_entry * 256)()
+    n = C.c_int32()
+    dropped = C.c_int64()
+    _check(_lib.gist_profile_read(ctx.handle, buf, 256, C.byref(n), C.byref(dropped)))
+    out = {}
+    for i in range(n.value):
+        e = buf[i]
+        out[e.name.decode()] = dict(launches=int(e.launches), ms=float(e.ms),
+                                    flops=float(e.flops), bytes=float(e.bytes))
+    return out, int(dropped.value)
+
+
+def gist_profile_end(ctx):
+    _check(_lib.gist_profile_end(ctx.handle))

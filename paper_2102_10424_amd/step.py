@@ -1,0 +1,272 @@
+"""Sub-GCN training step and GIST round, sequenced over the C ABI.
+
+Nothing here computes: each stage is one ``libgist`` call enqueued on the
+context's stream (torch only provides the device buffers).
+
+* :class:`SubGCN` -- ``subTrain`` (Section 3.2): layer forward for every
+  layer (eq. (2)), softmax cross-entropy, layer backward in reverse, SGD.
+* :class:`GistModel` -- the global model of Algorithm 1 on one device:
+  ``subGCNs`` (partition + slice gather), m sub-GCN steps back to back,
+  ``subAgg`` (slice scatter).
+"""
+
+import numpy as np
+import torch
+
+from . import gist as G
+
+
+def _dev(x, device, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(x))
+    if dtype is not None:
+        t = t.to(dtype)
+    return t.to(device, non_blocking=False)
+
+
+class DeviceBatch:
+    """A mini-batch on the device: CSR (+ transpose for SAGE), features, labels."""
+
+    def __init__(self, csr, X_b, labels_b, device):
+        self.n = int(csr["n"])
+        self.nnz = int(csr["nnz"])
+        self._t = dict(rowptr=_dev(csr["rowptr"], device),
+                       col=_dev(csr["col"][:max(self.nnz, 1)], device),
+                       val=_dev(csr["val"][:max(self.nnz, 1)], device))
+        self.A = G.csr_dev(self.n, self.nnz, self._t["rowptr"], self._t["col"], self._t["val"])
+        self.A_T = None
+        if "t_rowptr" in csr:
+            self._t.update(t_rowptr=_dev(csr["t_rowptr"], device),
+                           t_col=_dev(csr["t_col"][:max(self.nnz, 1)], device),
+                           t_val=_dev(csr["t_val"][:max(self.nnz, 1)], device))
+            self.A_T = G.csr_dev(self.n, self.nnz, self._t["t_rowptr"], self._t["t_col"],
+                                 self._t["t_val"])
+        self.X = X_b
+        self.labels = labels_b
+
+
+class BatchSlot:
+    """Reusable buffers for one mini-batch: pinned host staging + device copies.
+
+    ``load`` builds the cluster mini-batch CSR on the host directly into
+    pinned memory (``gist_build_minibatch_csr``), enqueues asynchronous
+    uploads on the current stream, and gathers the batch's feature rows on
+    the device (``gist_gather_slice`` with the local->global node map).
+    """
+
+    def __init__(self, ctx, norm, cap_n, cap_nnz, d_in, device="cuda"):
+        self.ctx = ctx
+        self.norm = norm
+        self.sage = norm == "sage"
+        self.cap_n, self.cap_nnz = int(cap_n), int(cap_nnz)
+        self.device = device
+        pin = dict(pin_memory=True)
+        i32, f32 = torch.int32, torch.float32
+        self.h = dict(rowptr=torch.empty(cap_n + 1, dtype=i32, **pin),
+                      col=torch.empty(cap_nnz, dtype=i32, **pin),
+                      val=torch.empty(cap_nnz, dtype=f32, **pin),
+                      node_map=torch.empty(cap_n, dtype=i32, **pin),
+                      labels=torch.empty(cap_n, dtype=i32, **pin))
+        if self.sage:
+            self.h.update(t_rowptr=torch.empty(cap_n + 1, dtype=i32, **pin),
+                          t_col=torch.empty(cap_nnz, dtype=i32, **pin),
+                          t_val=torch.empty(cap_nnz, dtype=f32, **pin))
+        self.d = {k: torch.empty_like(v, device=device) for k, v in self.h.items()}
+        self.X = torch.empty(cap_n, d_in, device=device)
+        self.d_in = d_in
+        self.uploaded = None
+
+    def load(self, graph_struct, clusters, X_dev, labels_host):
+        """Build, upload and gather; returns a batch view with n, nnz, A, A_T, X, labels."""
+        if self.uploaded is not None:
+            self.uploaded.synchronize()  # previous upload from the staging buffers done
+        q = G.gist_csr()
+        q.cap_n, q.cap_nnz = self.cap_n, self.cap_nnz
+        h = self.h
+        q.rowptr, q.col, q.val = h["rowptr"].data_ptr(), h["col"].data_ptr(), h["val"].data_ptr()
+        q.node_map = h["node_map"].data_ptr()
+        if self.sage:
+            q.t_rowptr, q.t_col, q.t_val = (h["t_rowptr"].data_ptr(), h["t_col"].data_ptr(),
+                                            h["t_val"].data_ptr())
+        G.build_minibatch_into(graph_struct, clusters, self.norm, q)
+        n, nnz = int(q.n), int(q.nnz)
+        nm = h["node_map"].numpy()[:n]
+        h["labels"].numpy()[:n] = labels_host[nm]
+        for k in h:
+            cnt = n + 1 if k.endswith("rowptr") else (nnz if k.endswith(("col", "val")) else n)
+            if cnt:
+                self.d[k][:cnt].copy_(h[k][:cnt], non_blocking=True)
+        ev = torch.cuda.Event()
+        ev.record()
+        self.uploaded = ev
+        Xb = self.X[:n]
+        G.gist_gather_slice(self.ctx, X_dev, self.d_in, self.d["node_map"], n, None,
+                            self.d_in, Xb, self.d_in)
+        return _View(n, nnz, self.d, Xb, self.sage)
+
+
+class _View:
+    def __init__(self, n, nnz, d, X, sage):
+        self.n, self.nnz = n, nnz
+        self.A = G.csr_dev(n, nnz, d["rowptr"], d["col"], d["val"])
+        self.A_T = G.csr_dev(n, nnz, d["t_rowptr"], d["t_col"], d["t_val"]) if sage else None
+        self.X = X
+        self.labels = d["labels"][:n]
+
+
+class SubGCN:
+    """Buffers and call sequence of one sub-GCN's training step.
+
+    ``widths`` are the slice widths s_0..s_L; ``kind`` is "gcn" or "sage".
+    Parameters are device tensors ``params[l]`` of shape (s_l, s_{l+1})
+    (SAGE: (2 s_l, s_{l+1}), W_self stacked over W_neigh).
+    """
+
+    def __init__(self, ctx, kind, widths, n_cap, dtype=G.GIST_DTYPE_F32, device="cuda",
+                 order=G.GIST_ORDER_AUTO):
+        self.ctx = ctx
+        self.kind = kind
+        self.widths = list(widths)
+        self.L = len(widths) - 1
+        self.dtype = dtype
+        self.order = order
+        self.device = device
+        self.lkind = G.GIST_LAYER_SAGE_MEAN if kind == "sage" else G.GIST_LAYER_GCN
+        self.n_cap = 0
+        self.ws = torch.empty(0, dtype=torch.uint8, device=device)
+        self._alloc(n_cap)
+        self.dW = [torch.empty(self.wrows(l), widths[l + 1], device=device)
+                   for l in range(self.L)]
+        self.loss = torch.zeros(1, device=device)
+
+    def wrows(self, l):
+        return (2 if self.kind == "sage" else 1) * self.widths[l]
+
+    def _alloc(self, n_cap):
+        w, d = self.widths, self.device
+        self.n_cap = n_cap
+        self.H = [None] + [torch.empty(n_cap, w[l + 1], device=d) for l in range(self.L)]
+        self.agg = [torch.empty(n_cap, w[l], device=d) for l in range(self.L)]
+        self.dH = [torch.empty(n_cap, w[l], device=d) for l in range(self.L)]  # dH[l] wrt H_l
+        self.dlogits = torch.empty(n_cap, w[self.L], device=d)
+        self.loss_ws = torch.empty(G.gist_softmax_xent_workspace(n_cap), dtype=torch.uint8,
+                                   device=d)
+
+    def desc(self, l, n):
+        act = G.GIST_ACT_RELU if l < self.L - 1 else G.GIST_ACT_NONE
+        return G.layer_desc(self.lkind, act, n, self.widths[l], self.widths[l + 1],
+                            self.dtype, self.order)
+
+    def _workspace(self, n):
+        need = 0
+        for l in range(self.L):
+            f, b = G.gist_layer_workspace_size(self.desc(l, n))
+            need = max(need, f, b)
+        if self.ws.numel() < need:
+            self.ws = torch.empty(need, dtype=torch.uint8, device=self.device)
+        return self.ws
+
+    def forward(self, batch, params):
+        n = batch.n
+        if n > self.n_cap:
+            self._alloc(n)
+        ws = self._workspace(n)
+        H = batch.X
+        for l in range(self.L):
+            out = self.H[l + 1][:n]
+            G.gist_gcn_layer_fwd(self.ctx, self.desc(l, n), batch.A, H, params[l],
+                                 self.agg[l][:n], out, ws)
+            H = out
+        return self.H[self.L][:n]
+
+    def loss_and_grad(self, batch):
+        n = batch.n
+        G.gist_softmax_xent(self.ctx, n, self.widths[-1], self.H[self.L][:n], batch.labels,
+                            self.loss, self.dlogits[:n], self.loss_ws)
+
+    def backward(self, batch, params):
+        n = batch.n
+        ws = self._workspace(n)
+        dout = self.dlogits[:n]
+        for l in reversed(range(self.L)):
+            Hin = batch.X if l == 0 else self.H[l][:n]
+            dH = self.dH[l][:n] if l > 0 else None
+            G.gist_gcn_layer_bwd(self.ctx, self.desc(l, n), batch.A, batch.A_T, Hin,
+                                 self.agg[l][:n], self.H[l + 1][:n], params[l], dout,
+                                 self.dW[l], dH, ws)
+            dout = dH
+
+    def sgd(self, params, lr):
+        for l in range(self.L):
+            G.gist_sgd_update(self.ctx, params[l], self.dW[l], params[l].numel(), lr)
+
+    def step(self, batch, params, lr):
+        """``subTrain``: forward, loss, backward, SGD (all enqueued, nothing synced)."""
+        self.forward(batch, params)
+        self.loss_and_grad(batch)
+        self.backward(batch, params)
+        self.sgd(params, lr)
+
+
+class GistModel:
+    """Global parameters Theta on the device plus the subGCNs / subAgg calls.
+
+    ``theta[l]`` is a list of parts (GCN: [Theta_l]; SAGE: [W_self, W_neigh]),
+    each (d_l x d_{l+1}) fp32 on the device.
+    """
+
+    def __init__(self, ctx, kind, widths, m, theta, device="cuda"):
+        self.ctx = ctx
+        self.kind = kind
+        self.widths = list(widths)
+        self.L = len(widths) - 1
+        self.m = m
+        self.theta = theta
+        self.device = device
+        self.parts = 2 if kind == "sage" else 1
+        self.slice_widths = [widths[0]] + [widths[l] // m for l in range(1, self.L)] + [widths[-1]]
+        self.part_dev = [None] * (self.L + 1)
+        self.part_host = [None] * (self.L + 1)
+        # per sub-GCN parameter slices (SAGE: [W_self; W_neigh] stacked)
+        s = self.slice_widths
+        self.params = [[torch.empty(self.parts * s[l], s[l + 1], device=device)
+                        for l in range(self.L)] for _ in range(m)]
+
+    def set_partitions(self, seeds):
+        """``subGCNs`` partitions of every hidden width; ``seeds[l]`` for l = 1..L-1."""
+        for l in range(1, self.L):
+            idx, offs = G.gist_partition(self.widths[l], self.m, seeds[l])
+            self.part_host[l] = (idx, offs)
+            self.part_dev[l] = torch.from_numpy(idx).to(self.device)
+
+    def _block(self, l, i):
+        idx, offs = self.part_host[l]
+        return self.part_dev[l][int(offs[i]):int(offs[i + 1])], int(offs[i + 1] - offs[i])
+
+    def _rc(self, l, i):
+        if l == 0:
+            rows, nr = None, self.widths[0]
+        else:
+            rows, nr = self._block(l, i)
+        if l + 1 == self.L:
+            cols, nc = None, self.widths[-1]
+        else:
+            cols, nc = self._block(l + 1, i)
+        return rows, nr, cols, nc
+
+    def gather(self, i):
+        """Theta^(i)_l = Theta_l[D_l^(i), D_{l+1}^(i)] for every layer and part."""
+        for l in range(self.L):
+            rows, nr, cols, nc = self._rc(l, i)
+            for p in range(self.parts):
+                dst = self.params[i][l][p * nr:(p + 1) * nr]
+                G.gist_gather_slice(self.ctx, self.theta[l][p], self.widths[l + 1], rows, nr,
+                                    cols, nc, dst, nc)
+
+    def subagg(self, i, flags=0):
+        """Write sub-GCN i's trained slices back into Theta (replacement)."""
+        for l in range(self.L):
+            rows, nr, cols, nc = self._rc(l, i)
+            for p in range(self.parts):
+                src = self.params[i][l][p * nr:(p + 1) * nr]
+                G.gist_subagg(self.ctx, self.theta[l][p], self.widths[l + 1], rows, nr, cols,
+                              nc, src, nc, flags)

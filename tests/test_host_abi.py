@@ -1,0 +1,120 @@
+"""C-ABI library: loads, exports every declared symbol, and its host-side calls
+(partition, mini-batch CSR) match the oracle bit for bit.  No GPU needed:
+these entry points run on the host and launch nothing."""
+
+import os
+import re
+
+import numpy as np
+import pytest
+
+from gist_synth import get_config
+from gist_synth.graphs import chung_lu, erdos_renyi, sbm
+from oracle import minibatch as MB
+from oracle import partition as P
+
+G = pytest.importorskip("paper_2102_10424_amd.gist",
+                        reason="libgist.so not built (python -m paper_2102_10424_amd.build)")
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                      "include", "gist.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gist_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 15
+    lib = G._lib
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(G.EXPORTED) == names
+
+
+def test_status_strings():
+    assert G.status_str(0) == "GIST_OK"
+    assert G.status_str(-5) == "GIST_E_NONFINITE"
+
+
+@pytest.mark.parametrize("d,m", [(4, 2), (256, 2), (2048, 4), (4096, 4), (32768, 8),
+                                 (2048, 8), (97, 97), (10, 1), (1433, 1)])
+def test_partition_bit_exact(d, m):
+    for seed in (0, 1, 12345, 2**64 - 1):
+        idx, offs = G.gist_partition(d, m, seed)
+        oi, oo = P.partition(d, m, seed)
+        assert np.array_equal(idx, np.asarray(oi, dtype=np.int32))
+        assert np.array_equal(offs, np.asarray(oo, dtype=np.int64))
+
+
+@pytest.mark.parametrize("d,m", [(64, 4), (1000, 8), (5, 5)])
+def test_partition_categorical_bit_exact(d, m):
+    for seed in (3, 77):
+        idx, offs = G.gist_partition(d, m, seed, G.GIST_PART_CATEGORICAL)
+        oi, oo = P.partition(d, m, seed, categorical=True)
+        assert np.array_equal(idx, np.asarray(oi, dtype=np.int32))
+        assert np.array_equal(offs, np.asarray(oo, dtype=np.int64))
+
+
+@pytest.mark.parametrize("d,m,flags", [(10, 3, 0), (4, 0, 0), (4, 5, 0), (0, 1, 0), (8, 2, 4)])
+def test_partition_errors(d, m, flags):
+    with pytest.raises(G.GistError) as e:
+        G.gist_partition(d, m, 0, flags)
+    assert e.value.status == G.GIST_E_INVAL
+
+
+def _same_csr(a, b, sage):
+    assert a["n"] == b["n"] and a["nnz"] == b["nnz"]
+    keys = ["rowptr", "col", "val", "node_map"] + (["t_rowptr", "t_col", "t_val"] if sage else [])
+    for k in keys:
+        x = np.asarray(a[k])
+        y = np.asarray(b[k])
+        if k.endswith("val"):
+            assert x.dtype == np.float32 and y.dtype == np.float32
+            assert np.array_equal(x.view(np.uint32), y.view(np.uint32)), k
+        else:
+            assert np.array_equal(x.astype(np.int64), y.astype(np.int64)), k
+
+
+GRAPHS = {
+    "er": lambda: erdos_renyi(300, 700, seed=1, clusters=6),
+    "er_isolated": lambda: erdos_renyi(50, 20, seed=2, clusters=5),
+    "chung_lu": lambda: chung_lu(3000, 2.5, 5.0, seed=3),
+    "sbm": lambda: sbm(5000, 40, 25.0, 0.9, seed=4),
+}
+
+
+@pytest.mark.parametrize("gname", sorted(GRAPHS))
+@pytest.mark.parametrize("norm", ["gcn", "sage", "theory"])
+def test_minibatch_csr_bit_exact(gname, norm):
+    g = GRAPHS[gname]()
+    sels = [None]
+    if g.n_clusters > 1:
+        rng = np.random.default_rng(0)
+        sels += [[0], list(rng.choice(g.n_clusters, 3, replace=False)),
+                 [g.n_clusters - 1, 0, 0, g.n_clusters - 1]]
+    for sel in sels:
+        _same_csr(G.gist_build_minibatch_csr(g, sel, norm), MB.build(g, sel, norm),
+                  norm == "sage")
+
+
+def test_minibatch_csr_reddit_sized_batch():
+    cfg = get_config("c3")
+    g = cfg.make_graph()
+    sel = cfg.minibatch(0, 0)
+    a = G.gist_build_minibatch_csr(g, sel, "sage")
+    _same_csr(a, MB.build(g, sel, "sage"), True)
+    assert 3000 <= a["n"] <= 3200
+
+
+def test_minibatch_csr_errors():
+    g = erdos_renyi(30, 40, seed=1, clusters=3)
+    for sel in ([], [3], [-1]):
+        with pytest.raises(G.GistError) as e:
+            G.gist_build_minibatch_csr(g, sel, "gcn")
+        assert e.value.status == G.GIST_E_INVAL
+    with pytest.raises(G.GistError):
+        G.gist_build_minibatch_csr(g, None, 7)
