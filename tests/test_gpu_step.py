@@ -1,0 +1,185 @@
+"""Sub-GCN step parity at the workloads' real shapes (c1-c4), fp32.
+
+Two views of the same step, both through the C ABI:
+
+* layer-wise: every layer call of the step, at the config's mini-batch
+  shape and with the bench's launch configuration, is fed the oracle's own
+  intermediate values (rounded to fp32) and compared with the oracle's
+  outputs.  Because both sides read their ReLU decisions from the same
+  numbers, the 1e-4 bar measures the kernels alone.
+* chained: the step exactly as bench.py runs it (host CSR build into pinned
+  memory, upload, feature gather, 4 forward layers, loss, backward, SGD).
+  Forward activations, logits and loss are compared within 1e-4.  The
+  GPU's ReLU decisions must equal the oracle's except where the oracle's
+  pre-activation lies within rounding distance of zero (|Z| <= 1e-5 max|Z|,
+  where either decision is correct); if no decision differs, every
+  gradient and updated weight is compared within 1e-4 too.
+"""
+
+import numpy as np
+import pytest
+
+from gist_synth import get_config
+from oracle import gist as OG
+from oracle import layers as OL
+from oracle import minibatch as OM
+from oracle import partition as OP
+
+from gpu_util import FP32_TOL, csr_to_dev, log, relerr, to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+LR = 0.05
+_CACHE = {}
+
+
+def workload(name):
+    """Oracle-side inputs and fp64 step of sub-GCN 0, round 0 (cached)."""
+    if name in _CACHE:
+        return _CACHE[name]
+    cfg = get_config(name)
+    log(f"[{name}] generating inputs")
+    g = cfg.make_graph()
+    norm = "sage" if cfg.kind == "sage" else "gcn"
+    parts = [None] * (cfg.L + 1)
+    for l in range(1, cfg.L):
+        parts[l] = OP.partition(cfg.widths[l], cfg.m, cfg.partition_seed(0, l))
+    sl = OG.slice_indices(parts, cfg.L, 0)
+    params = []
+    for l, (r, c) in enumerate(sl):
+        ps = []
+        for p in range(cfg.n_parts()):
+            th = cfg.theta(l, p, rows=r) if r is not None else cfg.theta(l, p)
+            ps.append(np.ascontiguousarray(th if c is None else th[:, c]))
+        params.append(ps[0] if cfg.kind == "gcn" else (ps[0], ps[1]))
+    clusters = cfg.minibatch(0, 0)
+    csr = OM.build(g, clusters, norm)
+    nm = csr["node_map"]
+    X = cfg.features_matrix(rows=nm)
+    labels = cfg.labels()
+    y = labels[nm]
+    log(f"[{name}] oracle step n={csr['n']} nnz={csr['nnz']}")
+    ref = OG.sub_gcn_step(cfg.kind, csr, X, y, params, LR)
+    w = dict(cfg=cfg, g=g, norm=norm, clusters=clusters, csr=csr, X=X, y=y, labels=labels,
+             params=params, ref=ref)
+    _CACHE[name] = w
+    return w
+
+
+def stacked(kind, p):
+    return p if kind == "gcn" else np.concatenate([p[0], p[1]], axis=0)
+
+
+@pytest.fixture(scope="module")
+def G():
+    import torch
+    assert torch.cuda.is_available()
+    from paper_2102_10424_amd import gist
+    return gist
+
+
+@pytest.fixture(scope="module")
+def ctx(G):
+    return G.Context(0)
+
+
+CONFIGS = ["c1", "c2", "c3", "c4"]
+
+
+@pytest.mark.parametrize("name", CONFIGS)
+def test_step_layerwise(G, ctx, name):
+    import torch
+    w = workload(name)
+    cfg, csr, ref = w["cfg"], w["csr"], w["ref"]
+    kind = cfg.kind
+    s = cfg.slice_widths()
+    L, n = cfg.L, csr["n"]
+    A, k1 = csr_to_dev(csr)
+    AT, k2 = csr_to_dev(csr, transpose=True) if kind == "sage" else (None, None)
+    lk = G.GIST_LAYER_SAGE_MEAN if kind == "sage" else G.GIST_LAYER_GCN
+    for l in range(L):
+        act = G.GIST_ACT_RELU if l < L - 1 else G.GIST_ACT_NONE
+        desc = G.layer_desc(lk, act, n, s[l], s[l + 1])
+        fws, bws = G.gist_layer_workspace_size(desc)
+        ws = torch.empty(max(fws, bws, 1), dtype=torch.uint8, device="cuda")
+        Wl = to_dev(stacked(kind, ref_params(w, l)).astype(np.float32))
+        Hin = to_dev(ref["H"][l].astype(np.float32))
+        agg = torch.empty(n, s[l], device="cuda")
+        Ho = torch.empty(n, s[l + 1], device="cuda")
+        G.gist_gcn_layer_fwd(ctx, desc, A, Hin, Wl, agg, Ho, ws)
+        rec = ref["recs"][l]
+        e_h = relerr(to_host(Ho), rec["H_out"])
+        e_a = relerr(to_host(agg), rec["AH"]) if (kind == "sage" or s[l] <= s[l + 1]) else 0.0
+        # backward on the oracle's forward values
+        agg_in = to_dev(rec["AH"].astype(np.float32))
+        Ho_in = to_dev(rec["H_out"].astype(np.float32))
+        dHo = ref["dH"][l + 1] if l + 1 < L else ref["dlogits"]
+        dW = torch.empty(Wl.shape[0], s[l + 1], device="cuda")
+        dH = torch.empty(n, s[l], device="cuda") if l > 0 else None
+        G.gist_gcn_layer_bwd(ctx, desc, A, AT, Hin, agg_in, Ho_in, Wl,
+                             to_dev(np.asarray(dHo, dtype=np.float32)), dW, dH, ws)
+        e_w = relerr(to_host(dW), stacked(kind, ref["grads"][l]))
+        e_d = relerr(to_host(dH), ref["dH"][l]) if l > 0 else 0.0
+        log(f"[{name}] layer {l} ({s[l]}->{s[l + 1]}): H_out {e_h:.2e} agg {e_a:.2e} "
+            f"dW {e_w:.2e} dH {e_d:.2e}")
+        assert max(e_h, e_a, e_w, e_d) <= FP32_TOL
+    # loss on the oracle's logits
+    C = s[L]
+    loss = torch.zeros(1, device="cuda")
+    dl = torch.empty(n, C, device="cuda")
+    lws = torch.empty(G.gist_softmax_xent_workspace(n), dtype=torch.uint8, device="cuda")
+    G.gist_softmax_xent(ctx, n, C, to_dev(ref["H"][L].astype(np.float32)), to_dev(w["y"]),
+                        loss, dl, lws)
+    assert abs(float(to_host(loss)[0]) - ref["loss"]) <= FP32_TOL * abs(ref["loss"])
+    assert relerr(to_host(dl), ref["dlogits"]) <= FP32_TOL
+
+
+def ref_params(w, l):
+    return w["params"][l]
+
+
+@pytest.mark.parametrize("name", CONFIGS)
+def test_step_chained(G, ctx, name):
+    import torch
+    from paper_2102_10424_amd.step import BatchSlot, SubGCN
+    w = workload(name)
+    cfg, csr, ref = w["cfg"], w["csr"], w["ref"]
+    kind, L = cfg.kind, cfg.L
+    s = cfg.slice_widths()
+    X_all = torch.from_numpy(cfg.features_matrix()).cuda()
+    slot = BatchSlot(ctx, w["norm"], csr["n"], csr["nnz"], cfg.widths[0])
+    b = slot.load(G.GraphHandle(w["g"]), w["clusters"], X_all, w["labels"])
+    assert b.n == csr["n"] and b.nnz == csr["nnz"]
+    params = [to_dev(stacked(kind, p).astype(np.float32)) for p in w["params"]]
+    run = SubGCN(ctx, kind, s, b.n)
+    run.forward(b, params)
+    run.loss_and_grad(b)
+    run.backward(b, params)
+    run.sgd(params, LR)
+    torch.cuda.synchronize()
+    mism = 0
+    for l in range(L):
+        got = to_host(run.H[l + 1][:b.n])
+        e = relerr(got, ref["recs"][l]["H_out"])
+        log(f"[{name}] chained H_{l + 1}: {e:.2e}")
+        assert e <= FP32_TOL
+        if l < L - 1:
+            Z = ref["recs"][l]["Z"]
+            diff = (got > 0) != (Z > 0)
+            band = 1e-5 * np.max(np.abs(Z))
+            assert np.all(np.abs(Z[diff]) <= band), "ReLU decision differs outside rounding band"
+            mism += int(diff.sum())
+    loss = float(to_host(run.loss)[0])
+    assert abs(loss - ref["loss"]) <= FP32_TOL * abs(ref["loss"])
+    log(f"[{name}] chained loss {loss:.6f} (oracle {ref['loss']:.6f}); "
+        f"ReLU decisions differing within the rounding band: {mism}")
+    # the last layer's gradient involves no ReLU decision of the backward pass
+    e_last = relerr(to_host(run.dW[L - 1]), stacked(kind, ref["grads"][L - 1]))
+    log(f"[{name}] chained dW_{L - 1}: {e_last:.2e}")
+    assert e_last <= FP32_TOL
+    if mism == 0:
+        for l in range(L):
+            e = relerr(to_host(run.dW[l]), stacked(kind, ref["grads"][l]))
+            ew = relerr(to_host(params[l]), stacked(kind, ref["params"][l]))
+            log(f"[{name}] chained dW_{l} {e:.2e} W'_{l} {ew:.2e}")
+            assert e <= FP32_TOL and ew <= FP32_TOL
