@@ -55,6 +55,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the library's per-launch event timing")
+    ap.add_argument("--copy-calib", action="store_true",
+                    help="only run a plain 1 GiB row copy (counter calibration)")
     return ap.parse_args()
 
 
@@ -230,6 +232,26 @@ class LayerWorkload:
                               "to all rows and x3 for fwd+bwd")
 
 
+def copy_calibration(G, ctx):
+    """Plain copy of a known size: 16384 x 16384 fp32 (1 GiB read, 1 GiB written)
+    through the library's row-copy kernel (gather with no index lists), three
+    times.  HBM byte counters of these launches calibrate the counters read
+    on the other kernels."""
+    import torch
+    n = 16384
+    src = torch.randn(n, n, device="cuda")
+    dst = torch.empty_like(src)
+    G.gist_profile_begin(ctx, 16)
+    for _ in range(3):
+        G.gist_gather_slice(ctx, src, n, None, n, None, n, dst, n)
+    prof, _ = G.gist_profile_read(ctx)
+    G.gist_profile_end(ctx)
+    v = prof["gather_slice"]
+    print(json.dumps({"copy_bytes_read": n * n * 4, "copy_bytes_written": n * n * 4,
+                      "launches": v["launches"], "avg_us": 1e3 * v["ms"] / v["launches"],
+                      "gbs": v["bytes"] / (v["ms"] * 1e-3) / 1e9}), flush=True)
+
+
 # ---------------------------------------------------------------------------
 def main():
     args = parse()
@@ -243,6 +265,9 @@ def main():
     from paper_2102_10424_amd import gist as G
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     ctx = G.Context(0)
+    if args.copy_calib:
+        copy_calibration(G, ctx)
+        return
     cfg = get_config(args.config)
     if args.config == "c5":
         wl = LayerWorkload(cfg, ctx, args.dtype, args.d_in)

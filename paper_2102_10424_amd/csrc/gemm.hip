@@ -21,9 +21,15 @@
 // bf16-input: the same tile walk, operands rounded to bf16 (nearest-even)
 // when staged into LDS, v_mfma_f32_32x32x16_bf16 with fp32 accumulation.
 //
-// Small output grids split K over blocks (grid z); each split writes its
-// partial tile to the workspace and a second kernel sums the splits in a
-// fixed order, so results never depend on scheduling.
+// Work distribution (stream-K): the (tile, K step) iterations of the whole
+// product are dealt out in equal contiguous ranges to a fixed grid of 512
+// workgroups (two per CU on 256 CUs), so the machine stays evenly loaded
+// whatever the tile count -- M = 1,633 gives only 416 or 832 tiles, which
+// whole-tile scheduling would spread over 1.6 rounds.  A tile whose K range
+// is split between workgroups is written as partial tiles to the workspace
+// and summed by a second kernel in workgroup order: deterministic, and no
+// workgroup ever waits on another.  Products with plenty of tiles use one
+// whole tile per workgroup and skip the second kernel.
 
 #include <algorithm>
 #include <cstdio>
@@ -40,7 +46,8 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int BM = 128, BN = 128, BK = 32;
-constexpr int LDK = BK + 4;        // fp32 LDS row stride (floats)
+constexpr int LDK = BK + 4;        // fp32 LDS row stride, [row][k] layout (floats)
+constexpr int kTileF = BM * LDK;   // floats per fp32 operand tile
 constexpr int LDKH = BK + 8;       // bf16 LDS row stride (halves)
 constexpr int kThreads = 256;
 
@@ -67,66 +74,127 @@ __device__ __forceinline__ float op_elem(const OpDev& o, int64_t r, int64_t k) {
   }
 }
 
-// Stage a 128 x 32 tile (rows r0.., k0..) of an operand into registers:
-// 4 groups of 4 consecutive K values per thread.
+// Thread -> (row, k) of the 4-float group it stages, for a 128 x 32 tile.
+//   K-contiguous operands: 8 threads cover one row's 32 K values (128 B).
+//   Row-contiguous, scalar: consecutive threads take consecutive rows at one
+//     K and read 4 K values each.
+//   Row-contiguous, vector: each thread owns a 4 x 4 block (rows rr..rr+3,
+//     K values kk..kk+3) and loads it as 4 row vectors, one per K value
+//     (32 threads cover one K's 128 rows, 512 B); group i is the vector at
+//     K value kk + i, transposed into rows when staged.
 template <bool KMAJ, bool VEC>
-__device__ __forceinline__ void load_tile(const OpDev& o, int64_t R, int64_t K, int64_t r0,
-                                          int64_t k0, floatx4 (&reg)[4]) {
-  const int t = threadIdx.x;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    int rr, kk;
-    if constexpr (KMAJ) {  // 8 threads read one row's 32 K values (128 B)
-      const int idx = t + kThreads * i;
-      rr = idx >> 3;
-      kk = (idx & 7) * 4;
-    } else {  // consecutive threads read consecutive rows at fixed K
-      const int idx = t + kThreads * i;
-      rr = idx & 127;
-      kk = (idx >> 7) * 4;
-    }
-    const int64_t r = r0 + rr, k = k0 + kk;
-    floatx4 v = {0.f, 0.f, 0.f, 0.f};
-    if (r < R) {
-      if constexpr (KMAJ && VEC) {
-        if (k + 3 < K) {
-          const float* p = k < o.split ? o.p0 + r * o.ld0 + k : o.p1 + r * o.ld1 + (k - o.split);
-          v = *reinterpret_cast<const floatx4*>(p);
-        } else {
-#pragma unroll
-          for (int q = 0; q < 4; ++q)
-            if (k + q < K) v[q] = op_elem<KMAJ>(o, r, k + q);
-        }
-      } else {
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          if (k + q < K) v[q] = op_elem<KMAJ>(o, r, k + q);
-      }
-    }
-    reg[i] = v;
-  }
-}
-
-template <bool KMAJ>
 __device__ __forceinline__ void tile_coord(int i, int& rr, int& kk) {
   const int idx = threadIdx.x + kThreads * i;
   if constexpr (KMAJ) {
     rr = idx >> 3;
     kk = (idx & 7) * 4;
+  } else if constexpr (VEC) {
+    rr = (threadIdx.x & 31) * 4;
+    kk = (threadIdx.x >> 5) * 4 + i;
   } else {
     rr = idx & 127;
     kk = (idx >> 7) * 4;
   }
 }
 
-template <bool KMAJ>
-__device__ __forceinline__ void store_tile_f32(float* lds, const floatx4 (&reg)[4]) {
+// Stage a 128 x 32 tile (rows r0.., k0..) of an operand into registers:
+// 4 groups of 4 consecutive K values per thread.
+//
+// Full K tiles (FULLK: k0 + 32 <= K) take a branch-free path: rows past the
+// operand's edge read a clamped (valid) row, so the loads of a tile issue
+// back to back with no wait.  Only the last, partial K tile of a split checks
+// every element (it must contribute exact zeros beyond K).
+template <bool KMAJ, bool VEC, bool FULLK>
+__device__ __forceinline__ void load_tile(const OpDev& o, int64_t R, int64_t K, int64_t r0,
+                                          int64_t k0, floatx4 (&reg)[4]) {
+  const int t = threadIdx.x;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     int rr, kk;
-    tile_coord<KMAJ>(i, rr, kk);
-    *reinterpret_cast<floatx4*>(lds + rr * LDK + kk) = reg[i];
+    tile_coord<KMAJ, VEC>(i, rr, kk);
+    const int64_t r = r0 + rr, k = k0 + kk;
+    floatx4 v = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (!KMAJ && VEC) {
+      // 4 consecutive rows at one K: a 16-byte load along the contiguous dim.
+      // The vector path requires split % 128 == 0, so the whole tile lies on
+      // one side of the split and the pointer choice is uniform.
+      const bool lo = r0 < o.split;
+      const float* base = lo ? o.p0 : o.p1 - o.split;
+      const int64_t ld = lo ? o.ld0 : o.ld1;
+      if constexpr (FULLK) {
+        const int64_t rc = r < R ? r : R - 4;  // R % 4 == 0 on this path
+        v = *reinterpret_cast<const floatx4*>(base + k * ld + rc);
+      } else {
+        if (k < K) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (r + q < R) v[q] = base[k * ld + r + q];
+        }
+      }
+    } else {
+      const bool rin = r < R;
+      const int64_t rc = rin ? r : R - 1;
+      if constexpr (FULLK) {
+        if constexpr (KMAJ && VEC) {
+          // split % 128 == 0: the whole K step lies on one side of the split
+          const bool lo = k0 < o.split;
+          const float* base = lo ? o.p0 : o.p1 - o.split;
+          const int64_t ld = lo ? o.ld0 : o.ld1;
+          v = *reinterpret_cast<const floatx4*>(base + rc * ld + k);
+        } else if constexpr (KMAJ) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) v[q] = op_elem<KMAJ>(o, rc, k + q);
+        } else {
+          const float* base = rc < o.split ? o.p0 + rc : o.p1 + (rc - o.split);
+          const int64_t ld = rc < o.split ? o.ld0 : o.ld1;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) v[q] = base[(k + q) * ld];
+        }
+        // rows past the edge keep the clamped row's (finite) values: they only
+        // feed output rows / columns the epilogue never stores
+      } else {
+        if (rin) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (k + q < K) v[q] = op_elem<KMAJ>(o, r, k + q);
+        }
+      }
+    }
+    reg[i] = v;
+    (void)t;
   }
+}
+
+// Transpose a row-vector 4 x 4 block (reg[i][j] = element (rr + j, kk + i))
+// into row order (out[j][i]).
+__device__ __forceinline__ void transpose4(const floatx4 (&reg)[4], floatx4 (&out)[4]) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) out[j][i] = reg[i][j];
+}
+
+template <bool KMAJ, bool VEC>
+__device__ __forceinline__ void store_tile_f32(float* lds, const floatx4 (&reg)[4]) {
+  if constexpr (!KMAJ && VEC) {
+    floatx4 rows[4];
+    transpose4(reg, rows);
+    const int rr = (threadIdx.x & 31) * 4, kk = (threadIdx.x >> 5) * 4;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) *reinterpret_cast<floatx4*>(lds + (rr + j) * LDK + kk) = rows[j];
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      int rr, kk;
+      tile_coord<KMAJ, VEC>(i, rr, kk);
+      *reinterpret_cast<floatx4*>(lds + rr * LDK + kk) = reg[i];
+    }
+  }
+}
+
+// MFMA operand fragment: the 4 K values k0 .. k0+3 of tile row `row`.
+__device__ __forceinline__ floatx4 frag_f32(const float* lds, int row, int k0) {
+  return *reinterpret_cast<const floatx4*>(lds + row * LDK + k0);
 }
 
 // Round-to-nearest-even fp32 -> bf16 (NaN kept quiet).
@@ -137,53 +205,70 @@ __device__ __forceinline__ unsigned short f2bf(float f) {
   return static_cast<unsigned short>(u >> 16);
 }
 
-template <bool KMAJ>
+template <bool KMAJ, bool VEC>
 __device__ __forceinline__ void store_tile_bf16(unsigned short* lds, const floatx4 (&reg)[4]) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    int rr, kk;
-    tile_coord<KMAJ>(i, rr, kk);
+  auto put = [&](int rr, int kk, const floatx4& v) {
     ushort4 h;
-    h.x = f2bf(reg[i][0]);
-    h.y = f2bf(reg[i][1]);
-    h.z = f2bf(reg[i][2]);
-    h.w = f2bf(reg[i][3]);
+    h.x = f2bf(v[0]);
+    h.y = f2bf(v[1]);
+    h.z = f2bf(v[2]);
+    h.w = f2bf(v[3]);
     *reinterpret_cast<ushort4*>(lds + rr * LDKH + kk) = h;
+  };
+  if constexpr (!KMAJ && VEC) {
+    floatx4 rows[4];
+    transpose4(reg, rows);
+    const int rr = (threadIdx.x & 31) * 4, kk = (threadIdx.x >> 5) * 4;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) put(rr + j, kk, rows[j]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      int rr, kk;
+      tile_coord<KMAJ, VEC>(i, rr, kk);
+      put(rr, kk, reg[i]);
+    }
   }
 }
 
-// Map a linear tile id to (tile_m, tile_n): XCD-major, then column-major in
-// bands of 8 tile rows so the blocks an XCD runs together share B columns
-// and a narrow band of A rows.
-__device__ __forceinline__ void tile_of(int64_t bid, int64_t tiles, int tiles_m, int& tm,
-                                        int& tn) {
-  const int64_t l = xcd_remap(bid, tiles);
+// Tile id -> (tile_m, tile_n): column-major in bands of 8 tile rows, so the
+// tiles one XCD runs together share B columns and a narrow band of A rows.
+__device__ __forceinline__ void tile_coords(int64_t t, int tiles_m, int tiles_n, int& tm,
+                                            int& tn) {
   constexpr int kBand = 8;
-  const int tiles_n = static_cast<int>(tiles / tiles_m);
-  const int band = static_cast<int>(l / (static_cast<int64_t>(kBand) * tiles_n));
+  const int band = static_cast<int>(t / (static_cast<int64_t>(kBand) * tiles_n));
   const int rows_in_band = min(kBand, tiles_m - band * kBand);
-  const int64_t in_band = l - static_cast<int64_t>(band) * kBand * tiles_n;
+  const int64_t in_band = t - static_cast<int64_t>(band) * kBand * tiles_n;
   tm = band * kBand + static_cast<int>(in_band % rows_in_band);
   tn = static_cast<int>(in_band / rows_in_band);
 }
 
+struct Sched {
+  int64_t T;        // total iterations = tiles * nk
+  int64_t ipw;      // iterations per workgroup
+  int nk;           // K steps per tile
+  int tiles_m, tiles_n;
+};
+
+__device__ __forceinline__ void store_out(const OutDev& C, int64_t row, int64_t col, float v) {
+  if (C.relu) v = fmaxf(v, 0.f);
+  if (col < C.c_split) C.c0[row * C.ldc0 + col] = v;
+  else C.c1[row * C.ldc1 + (col - C.c_split)] = v;
+}
+
+// Two resident blocks per CU where that fits in registers without spilling
+// (fp32 with vector loads on both operands, or both K-contiguous).
 template <bool AK, bool BK_, bool AV, bool BV, bool BF16>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(int64_t M, int64_t N, int64_t K,
-                                                        OpDev A, OpDev B, OutDev C,
-                                                        int64_t k_per_split, float* partials,
-                                                        int tiles_m) {
-  constexpr int kStage = BF16 ? 0 : 2 * BM * LDK;  // floats per fp32 stage (A + B)
+constexpr int min_blocks() { return (!BF16 && ((AV && BV) || (AK && BK_))) ? 2 : 1; }
+
+template <bool AK, bool BK_, bool AV, bool BV, bool BF16>
+__global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) void gemm_kernel(int64_t M, int64_t N, int64_t K,
+                                                        OpDev A, OpDev B, OutDev C, Sched S,
+                                                        float* partials) {
+  constexpr int kStage = BF16 ? 0 : 2 * kTileF;    // floats per fp32 stage (A + B)
   constexpr int kStageH = BF16 ? 2 * BM * LDKH : 0;
   __shared__ __attribute__((aligned(16))) float lds_f[BF16 ? 1 : 2 * kStage];
   __shared__ __attribute__((aligned(16))) unsigned short lds_h[BF16 ? 2 * kStageH : 1];
-
-  const int64_t tiles = static_cast<int64_t>(gridDim.x);
-  int tm, tn;
-  tile_of(blockIdx.x, tiles, tiles_m, tm, tn);
-  const int64_t m0 = static_cast<int64_t>(tm) * BM, n0 = static_cast<int64_t>(tn) * BN;
-  const int64_t kbeg = static_cast<int64_t>(blockIdx.z) * k_per_split;
-  const int64_t kend = min(K, kbeg + k_per_split);
-  const int nk = static_cast<int>((kend - kbeg + BK - 1) / BK);
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -191,35 +276,19 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(int64_t M, int64_t N, in
   const int li = lane & 31, lh = lane >> 5;
 
   floatx16 acc[2][2];
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
-
   floatx4 ra[4], rb[4];
-  if (nk > 0) {
-    load_tile<AK, AV>(A, M, kend, m0, kbeg, ra);
-    load_tile<BK_, BV>(B, N, kend, n0, kbeg, rb);
-    if constexpr (BF16) {
-      store_tile_bf16<AK>(lds_h, ra);
-      store_tile_bf16<BK_>(lds_h + BM * LDKH, rb);
-    } else {
-      store_tile_f32<AK>(lds_f, ra);
-      store_tile_f32<BK_>(lds_f + BM * LDK, rb);
-    }
-  }
-  __syncthreads();
+  int64_t m0 = 0, n0 = 0;
 
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      const int64_t kn = kbeg + static_cast<int64_t>(kt + 1) * BK;
-      load_tile<AK, AV>(A, M, kend, m0, kn, ra);
-      load_tile<BK_, BV>(B, N, kend, n0, kn, rb);
+  auto stage = [&](int buf) {
+    if constexpr (BF16) {
+      store_tile_bf16<AK, AV>(lds_h + buf * kStageH, ra);
+      store_tile_bf16<BK_, BV>(lds_h + buf * kStageH + BM * LDKH, rb);
+    } else {
+      store_tile_f32<AK, AV>(lds_f + buf * kStage, ra);
+      store_tile_f32<BK_, BV>(lds_f + buf * kStage + kTileF, rb);
     }
+  };
+  auto compute = [&](int buf) {
     if constexpr (BF16) {
       const unsigned short* As = lds_h + buf * kStageH;
       const unsigned short* Bs = As + BM * LDKH;
@@ -240,14 +309,14 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(int64_t M, int64_t N, in
       }
     } else {
       const float* As = lds_f + buf * kStage;
-      const float* Bs = As + BM * LDK;
+      const float* Bs = As + kTileF;
 #pragma unroll
       for (int c = 0; c < BK / 8; ++c) {
         floatx4 av[2], bv[2];
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-          av[t] = *reinterpret_cast<const floatx4*>(As + (wm * 64 + t * 32 + li) * LDK + 8 * c + 4 * lh);
-          bv[t] = *reinterpret_cast<const floatx4*>(Bs + (wn * 64 + t * 32 + li) * LDK + 8 * c + 4 * lh);
+          av[t] = frag_f32(As, wm * 64 + t * 32 + li, 8 * c + 4 * lh);
+          bv[t] = frag_f32(Bs, wn * 64 + t * 32 + li, 8 * c + 4 * lh);
         }
 #pragma unroll
         for (int s = 0; s < 4; ++s)
@@ -256,99 +325,176 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(int64_t M, int64_t N, in
 #pragma unroll
             for (int b = 0; b < 2; ++b)
               acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[a][s], bv[b][s], acc[a][b], 0, 0, 0);
+        // one K chunk's fragments live at a time (keeps two waves per SIMD)
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
-    if (more) {
-      const int nb = buf ^ 1;
-      if constexpr (BF16) {
-        store_tile_bf16<AK>(lds_h + nb * kStageH, ra);
-        store_tile_bf16<BK_>(lds_h + nb * kStageH + BM * LDKH, rb);
-      } else {
-        store_tile_f32<AK>(lds_f + nb * kStage, ra);
-        store_tile_f32<BK_>(lds_f + nb * kStage + BM * LDK, rb);
-      }
-    }
-    __syncthreads();
-  }
+  };
 
-  // Epilogue.  Accumulator register r of lane l holds C row
-  // 8 (r / 4) + 4 (l / 32) + (r mod 4), column l mod 32 of its 32 x 32 tile.
-  const bool split = gridDim.z > 1;
-  float* part = split ? partials + static_cast<int64_t>(blockIdx.z) * M * N : nullptr;
+  const int64_t w = xcd_remap(blockIdx.x, gridDim.x);
+  int64_t it = w * S.ipw;
+  const int64_t it_end = min(S.T, it + S.ipw);
+  const int64_t first_tile = it / S.nk;
+  const bool k_ragged = K % BK != 0;
+
+  while (it < it_end) {
+    const int64_t tile = it / S.nk;
+    const int kb = static_cast<int>(it % S.nk);
+    const int ke = static_cast<int>(min<int64_t>(S.nk, kb + (it_end - it)));
+    int tm, tn;
+    tile_coords(tile, S.tiles_m, S.tiles_n, tm, tn);
+    m0 = static_cast<int64_t>(tm) * BM;
+    n0 = static_cast<int64_t>(tn) * BN;
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const int64_t col = n0 + wn * 64 + b * 32 + li;
-      if (col >= N) continue;
+      for (int b = 0; b < 2; ++b)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t row = m0 + wm * 64 + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
-        if (row >= M) continue;
-        float v = acc[a][b][r];
-        if (split) {
-          part[row * N + col] = v;
-        } else {
-          if (C.relu) v = fmaxf(v, 0.f);
-          if (col < C.c_split) C.c0[row * C.ldc0 + col] = v;
-          else C.c1[row * C.ldc1 + (col - C.c_split)] = v;
-        }
+        for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+
+    // K steps [kb, ke) of this tile; the tile's last step may be partial
+    const bool tail = ke == S.nk && k_ragged;
+    const int full_end = tail ? ke - 1 : ke;
+    __syncthreads();  // LDS of the previous segment fully consumed
+    if (kb < full_end) {
+      load_tile<AK, AV, true>(A, M, K, m0, static_cast<int64_t>(kb) * BK, ra);
+      load_tile<BK_, BV, true>(B, N, K, n0, static_cast<int64_t>(kb) * BK, rb);
+      stage(0);
+      __syncthreads();
+      // steady state: prefetch step j+1 into registers while step j computes
+      for (int j = kb; j + 1 < full_end; ++j) {
+        const int64_t kn = static_cast<int64_t>(j + 1) * BK;
+        load_tile<AK, AV, true>(A, M, K, m0, kn, ra);
+        load_tile<BK_, BV, true>(B, N, K, n0, kn, rb);
+        // keep the prefetch at the top of the iteration: without the fence
+        // the scheduler sinks the loads next to their LDS stores, and their
+        // latency is no longer hidden behind the step's MFMAs
+        __builtin_amdgcn_sched_barrier(0);
+        compute((j - kb) & 1);
+        __builtin_amdgcn_sched_barrier(0);
+        stage((j + 1 - kb) & 1);
+        __syncthreads();
       }
+      compute((full_end - 1 - kb) & 1);
     }
+    if (tail) {
+      const int buf = (full_end - kb) & 1;
+      const int64_t kn = static_cast<int64_t>(full_end) * BK;
+      load_tile<AK, AV, false>(A, M, K, m0, kn, ra);
+      load_tile<BK_, BV, false>(B, N, K, n0, kn, rb);
+      __syncthreads();
+      stage(buf);
+      __syncthreads();
+      compute(buf);
+    }
+
+    // Epilogue.  Accumulator register r of lane l holds C row
+    // 8 (r / 4) + 4 (l / 32) + (r mod 4), column l mod 32 of its 32 x 32 tile.
+    if (kb == 0 && ke == S.nk) {
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+          const int64_t col = n0 + wn * 64 + b * 32 + li;
+          if (col >= N) continue;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int64_t row = m0 + wm * 64 + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+            if (row < M) store_out(C, row, col, acc[a][b][r]);
+          }
+        }
+    } else {
+      // partial tile: slot 0 holds this workgroup's first tile, slot 1 its last
+      float* part = partials + (w * 2 + (tile == first_tile ? 0 : 1)) * (BM * BN);
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int rr = wm * 64 + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+            const int cc = wn * 64 + b * 32 + li;
+            part[rr * BN + cc] = acc[a][b][r];
+          }
+    }
+    it += ke - kb;
+  }
 }
 
-// Sum the K splits in order z = 0, 1, ... and apply the epilogue.
-__global__ __launch_bounds__(256) void splitk_reduce(int64_t M, int64_t N, int splits,
+// Sum the partial tiles of every tile split between workgroups, in
+// workgroup order, and apply the epilogue.  One block per tile; the partial
+// slots are resolved once per tile, then each thread sums float4 columns.
+constexpr int kMaxFixupParts = 1024;
+
+__global__ __launch_bounds__(256) void streamk_fixup(int64_t M, int64_t N, Sched S,
                                                      const float* __restrict__ partials,
                                                      OutDev C) {
-  const int64_t total = M * N;
-  for (int64_t i = blockIdx.x * 256ll + threadIdx.x; i < total; i += 256ll * gridDim.x) {
-    float s = 0.f;
-    for (int z = 0; z < splits; ++z) s += partials[static_cast<int64_t>(z) * total + i];
-    if (C.relu) s = fmaxf(s, 0.f);
-    const int64_t row = i / N, col = i % N;
-    if (col < C.c_split) C.c0[row * C.ldc0 + col] = s;
-    else C.c1[row * C.ldc1 + (col - C.c_split)] = s;
+  __shared__ int64_t slot_off[kMaxFixupParts];
+  const int64_t t = blockIdx.x;
+  const int64_t w_first = (t * S.nk) / S.ipw;
+  const int64_t w_last = ((t + 1) * S.nk - 1) / S.ipw;
+  if (w_first == w_last) return;  // computed whole and stored by one workgroup
+  const int parts = static_cast<int>(w_last - w_first + 1);
+  for (int j = threadIdx.x; j < parts; j += 256) {
+    const int64_t w = w_first + j;
+    slot_off[j] = (w * 2 + (((w * S.ipw) / S.nk) == t ? 0 : 1)) * (BM * BN);
+  }
+  __syncthreads();
+  int tm, tn;
+  tile_coords(t, S.tiles_m, S.tiles_n, tm, tn);
+  const int64_t m0 = static_cast<int64_t>(tm) * BM, n0 = static_cast<int64_t>(tn) * BN;
+  for (int e4 = threadIdx.x; e4 < BM * BN / 4; e4 += 256) {
+    const int e = e4 * 4;
+    const int64_t row = m0 + e / BN, col = n0 + e % BN;
+    if (row >= M || col >= N) continue;
+    floatx4 s = {0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < parts; ++j)
+      s += *reinterpret_cast<const floatx4*>(partials + slot_off[j] + e);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (col + q < N) store_out(C, row, col + q, s[q]);
   }
 }
 
-struct Plan {
-  int64_t tiles_m, tiles_n, splits, k_per_split;
-};
+constexpr int64_t kStreamWG = 512;   // two resident 256-thread blocks per CU, 256 CUs
 
-Plan make_plan(int64_t M, int64_t N, int64_t K) {
-  Plan p;
-  p.tiles_m = (M + BM - 1) / BM;
-  p.tiles_n = (N + BN - 1) / BN;
-  const int64_t tiles = p.tiles_m * p.tiles_n;
-  constexpr int64_t kTargetBlocks = 512;  // two rounds over 256 CUs
-  int64_t s = 1;
-  if (tiles < kTargetBlocks) {
-    s = std::max<int64_t>(1, kTargetBlocks / tiles);
-    s = std::min<int64_t>(s, std::max<int64_t>(1, K / 256));  // >= 256 of K per split
+Sched make_sched(int64_t M, int64_t N, int64_t K) {
+  Sched s;
+  s.tiles_m = static_cast<int>((M + BM - 1) / BM);
+  s.tiles_n = static_cast<int>((N + BN - 1) / BN);
+  s.nk = static_cast<int>((K + BK - 1) / BK);
+  const int64_t tiles = static_cast<int64_t>(s.tiles_m) * s.tiles_n;
+  s.T = tiles * s.nk;
+  if (tiles >= 4 * kStreamWG) {
+    s.ipw = s.nk;   // enough tiles: one whole tile per workgroup
+  } else {
+    s.ipw = (s.T + kStreamWG - 1) / kStreamWG;
   }
-  int64_t kps = (K + s - 1) / s;
-  kps = (kps + BK - 1) / BK * BK;
-  p.k_per_split = std::max<int64_t>(kps, BK);
-  p.splits = (K + p.k_per_split - 1) / p.k_per_split;
-  if (p.splits < 1) p.splits = 1;
-  return p;
+  return s;
 }
 
-bool op_vec_ok(const Operand& o) {
-  if (!o.k_major) return false;
+int64_t sched_groups(const Sched& s) { return (s.T + s.ipw - 1) / s.ipw; }
+bool sched_split(const Sched& s) { return s.ipw % s.nk != 0; }
+
+// 16-byte loads along the operand's contiguous dimension are legal when the
+// leading dimensions and base addresses are multiples of 4 floats (and, for
+// row-contiguous operands, the row count too).  A concatenation split must
+// fall on a 128 boundary, so that every K step and every tile lies on one
+// side of it and the pointer choice stays uniform.
+bool op_vec_ok(const Operand& o, int64_t R) {
   if (o.ld0 % 4 || !aligned16(o.p0)) return false;
-  if (o.p1 && (o.ld1 % 4 || !aligned16(o.p1) || o.split % 4)) return false;
+  if (o.p1 && (o.ld1 % 4 || !aligned16(o.p1) || o.split % 128)) return false;
+  if (!o.k_major && R % 4) return false;
   return true;
 }
 
 template <bool AK, bool BK_, bool BF16>
 void launch_kernel(hipStream_t st, bool av, bool bv, dim3 grid, int64_t M, int64_t N, int64_t K,
-                   const OpDev& A, const OpDev& B, const OutDev& C, int64_t kps, float* part,
-                   int tiles_m) {
+                   const OpDev& A, const OpDev& B, const OutDev& C, const Sched& S,
+                   float* part) {
 #define GIST_GEMM_LAUNCH(AV_, BV_)                                                         \
-  hipLaunchKernelGGL((gemm_kernel<AK, BK_, AV_, BV_, BF16>), grid, dim3(kThreads), 0, st, \
-                     M, N, K, A, B, C, kps, part, tiles_m)
+  hipLaunchKernelGGL((gemm_kernel<AK, BK_, AV_, BV_, BF16>), grid, dim3(kThreads), 0, st,    \
+                     M, N, K, A, B, C, S, part)
   if (av && bv) GIST_GEMM_LAUNCH(true, true);
   else if (av) GIST_GEMM_LAUNCH(true, false);
   else if (bv) GIST_GEMM_LAUNCH(false, true);
@@ -359,76 +505,78 @@ void launch_kernel(hipStream_t st, bool av, bool bv, dim3 grid, int64_t M, int64
 template <bool BF16>
 void dispatch(hipStream_t st, const Operand& A, const Operand& B, bool av, bool bv, dim3 grid,
               int64_t M, int64_t N, int64_t K, const OpDev& a, const OpDev& b, const OutDev& c,
-              int64_t kps, float* part, int tiles_m) {
-  // Only the K-contiguous orientation has a vector path (VEC implies KMAJ).
+              const Sched& S, float* part) {
   if (A.k_major && B.k_major)
-    launch_kernel<true, true, BF16>(st, av, bv, grid, M, N, K, a, b, c, kps, part, tiles_m);
+    launch_kernel<true, true, BF16>(st, av, bv, grid, M, N, K, a, b, c, S, part);
   else if (A.k_major)
-    launch_kernel<true, false, BF16>(st, av, false, grid, M, N, K, a, b, c, kps, part, tiles_m);
+    launch_kernel<true, false, BF16>(st, av, bv, grid, M, N, K, a, b, c, S, part);
   else if (B.k_major)
-    launch_kernel<false, true, BF16>(st, false, bv, grid, M, N, K, a, b, c, kps, part, tiles_m);
+    launch_kernel<false, true, BF16>(st, av, bv, grid, M, N, K, a, b, c, S, part);
   else
-    launch_kernel<false, false, BF16>(st, false, false, grid, M, N, K, a, b, c, kps, part,
-                                      tiles_m);
+    launch_kernel<false, false, BF16>(st, av, bv, grid, M, N, K, a, b, c, S, part);
 }
 
 }  // namespace
 
 size_t gemm_workspace(int64_t M, int64_t N, int64_t K, int /*dtype*/) {
   if (M <= 0 || N <= 0 || K <= 0) return 0;
-  const Plan p = make_plan(M, N, K);
-  if (p.splits <= 1) return 0;
-  return static_cast<size_t>(p.splits) * static_cast<size_t>(M) * static_cast<size_t>(N) *
-         sizeof(float);
+  const Sched s = make_sched(M, N, K);
+  if (!sched_split(s)) return 0;
+  return static_cast<size_t>(sched_groups(s)) * 2 * BM * BN * sizeof(float);
 }
 
 gist_status gemm(hipStream_t st, int64_t M, int64_t N, int64_t K, const Operand& A,
                  const Operand& B, const GemmOut& C, int dtype, void* ws, size_t ws_bytes) {
   if (M <= 0 || N <= 0) return GIST_OK;
   OutDev c{C.c0, C.c1, C.ldc0, C.ldc1, C.c_split, C.relu ? 1 : 0};
-  if (K <= 0) {
-    return set_error(GIST_E_UNSUPPORTED, "gemm: K == 0");
-  }
-  const Plan p = make_plan(M, N, K);
-  if (p.tiles_m * p.tiles_n > INT32_MAX || p.splits > 65535)
+  if (K <= 0) return set_error(GIST_E_UNSUPPORTED, "gemm: K == 0");
+  if (K > (static_cast<int64_t>(INT32_MAX) - BK) * BK)
+    return set_error(GIST_E_UNSUPPORTED, "gemm: K too large");
+  const Sched S = make_sched(M, N, K);
+  const int64_t groups = sched_groups(S);
+  const int64_t tiles = static_cast<int64_t>(S.tiles_m) * S.tiles_n;
+  if (groups > INT32_MAX || tiles > INT32_MAX)
     return set_error(GIST_E_UNSUPPORTED, "gemm: grid too large");
   float* part = nullptr;
-  if (p.splits > 1) {
+  const bool split = sched_split(S);
+  if (split) {
+    // a tile's iterations span at most ceil(nk / ipw) + 1 workgroups
+    if ((S.nk + S.ipw - 1) / S.ipw + 1 > kMaxFixupParts)
+      return set_error(GIST_E_UNSUPPORTED, "gemm: too many partial tiles per tile");
     const size_t need = gemm_workspace(M, N, K, dtype);
-    if (!ws || ws_bytes < need) return set_error(GIST_E_NOMEM, "gemm: split-K workspace too small");
+    if (!ws || ws_bytes < need) return set_error(GIST_E_NOMEM, "gemm: workspace too small");
     part = static_cast<float*>(ws);
   }
   OpDev a{A.p0, A.p1 ? A.p1 : A.p0, A.ld0, A.p1 ? A.ld1 : A.ld0, A.p1 ? A.split : INT64_MAX};
   OpDev b{B.p0, B.p1 ? B.p1 : B.p0, B.ld0, B.p1 ? B.ld1 : B.ld0, B.p1 ? B.split : INT64_MAX};
-  const bool av = op_vec_ok(A), bv = op_vec_ok(B);
-  dim3 grid(static_cast<unsigned>(p.tiles_m * p.tiles_n), 1, static_cast<unsigned>(p.splits));
-  const int tm = static_cast<int>(p.tiles_m);
+  const bool bf = dtype == GIST_DTYPE_BF16_IN;
+  const bool av = op_vec_ok(A, M);
+  const bool bv = op_vec_ok(B, N);
+  dim3 grid(static_cast<unsigned>(groups));
   {
-    // variant name: dtype, then the K-contiguous (K) / row-contiguous (R)
-    // orientation of A and B as read from memory
+    // variant name: dtype, the K-contiguous (K) / row-contiguous (R)
+    // orientation of A and B as read from memory, and whether each is read
+    // with 16-byte vector loads (v) or scalar loads (s) -- one name per
+    // kernel instantiation
     char name[32];
-    snprintf(name, sizeof(name), "gemm_%s_%c%c", dtype == GIST_DTYPE_BF16_IN ? "bf16" : "f32",
-             A.k_major ? 'K' : 'R', B.k_major ? 'K' : 'R');
+    snprintf(name, sizeof(name), "gemm_%s_%c%c_%c%c", bf ? "bf16" : "f32",
+             A.k_major ? 'K' : 'R', B.k_major ? 'K' : 'R', av ? 'v' : 's', bv ? 'v' : 's');
     const double md = static_cast<double>(M), nd = static_cast<double>(N),
                  kd = static_cast<double>(K);
     ProfScope ps(st, name, 2.0 * md * nd * kd, 4.0 * (md * kd + kd * nd + md * nd));
-    if (dtype == GIST_DTYPE_BF16_IN)
-      dispatch<true>(st, A, B, av, bv, grid, M, N, K, a, b, c, p.k_per_split, part, tm);
-    else
-      dispatch<false>(st, A, B, av, bv, grid, M, N, K, a, b, c, p.k_per_split, part, tm);
+    if (bf) dispatch<true>(st, A, B, av, bv, grid, M, N, K, a, b, c, S, part);
+    else dispatch<false>(st, A, B, av, bv, grid, M, N, K, a, b, c, S, part);
   }
   {
     gist_status s = check_launch("gemm");
     if (s != GIST_OK) return s;
   }
-  if (p.splits > 1) {
-    const int64_t total = M * N;
-    const int64_t blocks = std::min<int64_t>((total + 255) / 256, 4096);
-    ProfScope ps(st, "gemm_splitk_reduce", static_cast<double>(p.splits) * total,
-                 4.0 * static_cast<double>(p.splits + 1) * total);
-    hipLaunchKernelGGL(splitk_reduce, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, M,
-                       N, static_cast<int>(p.splits), part, c);
-    return check_launch("gemm split-K reduce");
+  if (split) {
+    ProfScope ps(st, "gemm_streamk_fixup", 0.0,
+                 4.0 * static_cast<double>(groups) * 2 * BM * BN + 4.0 * M * N);
+    hipLaunchKernelGGL(streamk_fixup, dim3(static_cast<unsigned>(tiles)), dim3(256), 0, st, M, N,
+                       S, part, c);
+    return check_launch("gemm stream-K fix-up");
   }
   return GIST_OK;
 }

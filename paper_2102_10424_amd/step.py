@@ -226,17 +226,32 @@ class GistModel:
         self.slice_widths = [widths[0]] + [widths[l] // m for l in range(1, self.L)] + [widths[-1]]
         self.part_dev = [None] * (self.L + 1)
         self.part_host = [None] * (self.L + 1)
+        self._pin = [None] * (self.L + 1)
+        self._part_event = None
         # per sub-GCN parameter slices (SAGE: [W_self; W_neigh] stacked)
         s = self.slice_widths
         self.params = [[torch.empty(self.parts * s[l], s[l + 1], device=device)
                         for l in range(self.L)] for _ in range(m)]
 
     def set_partitions(self, seeds):
-        """``subGCNs`` partitions of every hidden width; ``seeds[l]`` for l = 1..L-1."""
+        """``subGCNs`` partitions of every hidden width; ``seeds[l]`` for l = 1..L-1.
+
+        The indices are written into pinned host buffers and uploaded
+        asynchronously, so the host does not wait for the previous round.
+        """
+        if self._part_event is not None:
+            self._part_event.synchronize()   # last upload from the pinned buffers done
         for l in range(1, self.L):
-            idx, offs = G.gist_partition(self.widths[l], self.m, seeds[l])
+            d = self.widths[l]
+            if self._pin[l] is None:
+                self._pin[l] = torch.empty(d, dtype=torch.int32, pin_memory=True)
+                self.part_dev[l] = torch.empty(d, dtype=torch.int32, device=self.device)
+            idx, offs = G.gist_partition(d, self.m, seeds[l])
+            self._pin[l].numpy()[:] = idx
             self.part_host[l] = (idx, offs)
-            self.part_dev[l] = torch.from_numpy(idx).to(self.device)
+            self.part_dev[l].copy_(self._pin[l], non_blocking=True)
+        self._part_event = torch.cuda.Event()
+        self._part_event.record()
 
     def _block(self, l, i):
         idx, offs = self.part_host[l]
