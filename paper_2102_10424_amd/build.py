@@ -14,14 +14,14 @@ CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libgist.so")
 BUILD = os.path.join(PKG, "_build")
 
-HIP_SOURCES = ["api.hip", "spmm.hip", "gemm.hip", "elementwise.hip"]
+HIP_SOURCES = ["api.hip", "spmm.hip", "gemm.hip", "gemm_bf16.hip", "elementwise.hip"]
 HOST_SOURCES = ["host_partition.cpp", "host_minibatch.cpp"]
 
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 CXX = os.environ.get("CXX", "g++")
 
-# Device code: no packed-fp32 instructions (build flags),
+# Device code: no packed-fp32 instructions (some of their forms are unsafe here),
 # no floating-point contraction beyond what the source spells out.
 HIP_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

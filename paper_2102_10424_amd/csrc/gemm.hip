@@ -35,6 +35,7 @@
 #include <cstdio>
 
 #include "common.cuh"
+#include "gemm_common.cuh"
 #include "gist_internal.h"
 
 namespace gist {
@@ -48,7 +49,8 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 constexpr int BM = 128, BN = 128, BK = 32;
 constexpr int LDK = BK + 4;        // fp32 LDS row stride, [row][k] layout (floats)
 constexpr int kTileF = BM * LDK;   // floats per fp32 operand tile
-constexpr int LDKH = BK + 8;       // bf16 LDS row stride (halves)
+constexpr int KSH = 64;            // bf16 K step: two 32-wide load sub-tiles
+constexpr int LDKH = KSH + 8;      // bf16 LDS row stride (halves)
 constexpr int kThreads = 256;
 
 struct OpDev {
@@ -197,23 +199,21 @@ __device__ __forceinline__ floatx4 frag_f32(const float* lds, int row, int k0) {
   return *reinterpret_cast<const floatx4*>(lds + row * LDK + k0);
 }
 
-// Round-to-nearest-even fp32 -> bf16 (NaN kept quiet).
+// Round-to-nearest-even fp32 -> bf16 (gfx950 converts in hardware).
 __device__ __forceinline__ unsigned short f2bf(float f) {
-  unsigned int u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<unsigned short>((u >> 16) | 0x40);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return static_cast<unsigned short>(u >> 16);
+  return __builtin_bit_cast(unsigned short, static_cast<__bf16>(f));
 }
 
 template <bool KMAJ, bool VEC>
-__device__ __forceinline__ void store_tile_bf16(unsigned short* lds, const floatx4 (&reg)[4]) {
+__device__ __forceinline__ void store_tile_bf16(unsigned short* lds, const floatx4 (&reg)[4],
+                                                int koff) {
   auto put = [&](int rr, int kk, const floatx4& v) {
     ushort4 h;
     h.x = f2bf(v[0]);
     h.y = f2bf(v[1]);
     h.z = f2bf(v[2]);
     h.w = f2bf(v[3]);
-    *reinterpret_cast<ushort4*>(lds + rr * LDKH + kk) = h;
+    *reinterpret_cast<ushort4*>(lds + rr * LDKH + koff + kk) = h;
   };
   if constexpr (!KMAJ && VEC) {
     floatx4 rows[4];
@@ -229,18 +229,6 @@ __device__ __forceinline__ void store_tile_bf16(unsigned short* lds, const float
       put(rr, kk, reg[i]);
     }
   }
-}
-
-// Tile id -> (tile_m, tile_n): column-major in bands of 8 tile rows, so the
-// tiles one XCD runs together share B columns and a narrow band of A rows.
-__device__ __forceinline__ void tile_coords(int64_t t, int tiles_m, int tiles_n, int& tm,
-                                            int& tn) {
-  constexpr int kBand = 8;
-  const int band = static_cast<int>(t / (static_cast<int64_t>(kBand) * tiles_n));
-  const int rows_in_band = min(kBand, tiles_m - band * kBand);
-  const int64_t in_band = t - static_cast<int64_t>(band) * kBand * tiles_n;
-  tm = band * kBand + static_cast<int>(in_band % rows_in_band);
-  tn = static_cast<int>(in_band / rows_in_band);
 }
 
 struct Sched {
@@ -275,26 +263,46 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
   const int wm = wave >> 1, wn = wave & 1;
   const int li = lane & 31, lh = lane >> 5;
 
+  // K per pipeline step: one 32-wide load sub-tile for fp32, two for bf16
+  constexpr int KS = BF16 ? KSH : BK;
+  constexpr int SUB = KS / BK;
   floatx16 acc[2][2];
-  floatx4 ra[4], rb[4];
+  floatx4 ra[SUB][4], rb[SUB][4];
   int64_t m0 = 0, n0 = 0;
 
   auto stage = [&](int buf) {
     if constexpr (BF16) {
-      store_tile_bf16<AK, AV>(lds_h + buf * kStageH, ra);
-      store_tile_bf16<BK_, BV>(lds_h + buf * kStageH + BM * LDKH, rb);
+#pragma unroll
+      for (int s = 0; s < SUB; ++s) {
+        store_tile_bf16<AK, AV>(lds_h + buf * kStageH, ra[s], s * BK);
+        store_tile_bf16<BK_, BV>(lds_h + buf * kStageH + BM * LDKH, rb[s], s * BK);
+      }
     } else {
-      store_tile_f32<AK, AV>(lds_f + buf * kStage, ra);
-      store_tile_f32<BK_, BV>(lds_f + buf * kStage + kTileF, rb);
+      store_tile_f32<AK, AV>(lds_f + buf * kStage, ra[0]);
+      store_tile_f32<BK_, BV>(lds_f + buf * kStage + kTileF, rb[0]);
+    }
+  };
+  auto load_full = [&](int64_t k) {
+#pragma unroll
+    for (int s = 0; s < SUB; ++s) {
+      load_tile<AK, AV, true>(A, M, K, m0, k + s * BK, ra[s]);
+      load_tile<BK_, BV, true>(B, N, K, n0, k + s * BK, rb[s]);
+    }
+  };
+  auto load_edge = [&](int64_t k) {
+#pragma unroll
+    for (int s = 0; s < SUB; ++s) {
+      load_tile<AK, AV, false>(A, M, K, m0, k + s * BK, ra[s]);
+      load_tile<BK_, BV, false>(B, N, K, n0, k + s * BK, rb[s]);
     }
   };
   auto compute = [&](int buf) {
     if constexpr (BF16) {
       const unsigned short* As = lds_h + buf * kStageH;
       const unsigned short* Bs = As + BM * LDKH;
-      // two K chunks of 16; lane half h supplies K values 8h .. 8h+7
+      // K chunks of 16; lane half h supplies K values 8h .. 8h+7
 #pragma unroll
-      for (int c = 0; c < 2; ++c) {
+      for (int c = 0; c < KS / 16; ++c) {
         bf16x8 av[2], bv[2];
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
@@ -335,14 +343,14 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
   int64_t it = w * S.ipw;
   const int64_t it_end = min(S.T, it + S.ipw);
   const int64_t first_tile = it / S.nk;
-  const bool k_ragged = K % BK != 0;
+  const bool k_ragged = K % KS != 0;
 
   while (it < it_end) {
     const int64_t tile = it / S.nk;
     const int kb = static_cast<int>(it % S.nk);
     const int ke = static_cast<int>(min<int64_t>(S.nk, kb + (it_end - it)));
     int tm, tn;
-    tile_coords(tile, S.tiles_m, S.tiles_n, tm, tn);
+    tile_coords_banded(tile, S.tiles_m, S.tiles_n, tm, tn);
     m0 = static_cast<int64_t>(tm) * BM;
     n0 = static_cast<int64_t>(tn) * BN;
 #pragma unroll
@@ -357,15 +365,12 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
     const int full_end = tail ? ke - 1 : ke;
     __syncthreads();  // LDS of the previous segment fully consumed
     if (kb < full_end) {
-      load_tile<AK, AV, true>(A, M, K, m0, static_cast<int64_t>(kb) * BK, ra);
-      load_tile<BK_, BV, true>(B, N, K, n0, static_cast<int64_t>(kb) * BK, rb);
+      load_full(static_cast<int64_t>(kb) * KS);
       stage(0);
       __syncthreads();
       // steady state: prefetch step j+1 into registers while step j computes
       for (int j = kb; j + 1 < full_end; ++j) {
-        const int64_t kn = static_cast<int64_t>(j + 1) * BK;
-        load_tile<AK, AV, true>(A, M, K, m0, kn, ra);
-        load_tile<BK_, BV, true>(B, N, K, n0, kn, rb);
+        load_full(static_cast<int64_t>(j + 1) * KS);
         // keep the prefetch at the top of the iteration: without the fence
         // the scheduler sinks the loads next to their LDS stores, and their
         // latency is no longer hidden behind the step's MFMAs
@@ -379,9 +384,7 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
     }
     if (tail) {
       const int buf = (full_end - kb) & 1;
-      const int64_t kn = static_cast<int64_t>(full_end) * BK;
-      load_tile<AK, AV, false>(A, M, K, m0, kn, ra);
-      load_tile<BK_, BV, false>(B, N, K, n0, kn, rb);
+      load_edge(static_cast<int64_t>(full_end) * KS);
       __syncthreads();
       stage(buf);
       __syncthreads();
@@ -441,7 +444,7 @@ __global__ __launch_bounds__(256) void streamk_fixup(int64_t M, int64_t N, Sched
   }
   __syncthreads();
   int tm, tn;
-  tile_coords(t, S.tiles_m, S.tiles_n, tm, tn);
+  tile_coords_banded(t, S.tiles_m, S.tiles_n, tm, tn);
   const int64_t m0 = static_cast<int64_t>(tm) * BM, n0 = static_cast<int64_t>(tn) * BN;
   for (int e4 = threadIdx.x; e4 < BM * BN / 4; e4 += 256) {
     const int e = e4 * 4;
@@ -458,11 +461,12 @@ __global__ __launch_bounds__(256) void streamk_fixup(int64_t M, int64_t N, Sched
 
 constexpr int64_t kStreamWG = 512;   // two resident 256-thread blocks per CU, 256 CUs
 
-Sched make_sched(int64_t M, int64_t N, int64_t K) {
+Sched make_sched(int64_t M, int64_t N, int64_t K, int dtype) {
+  const int ks = dtype == GIST_DTYPE_BF16_IN ? KSH : BK;
   Sched s;
   s.tiles_m = static_cast<int>((M + BM - 1) / BM);
   s.tiles_n = static_cast<int>((N + BN - 1) / BN);
-  s.nk = static_cast<int>((K + BK - 1) / BK);
+  s.nk = static_cast<int>((K + ks - 1) / ks);
   const int64_t tiles = static_cast<int64_t>(s.tiles_m) * s.tiles_n;
   s.T = tiles * s.nk;
   if (tiles >= 4 * kStreamWG) {
@@ -518,9 +522,11 @@ void dispatch(hipStream_t st, const Operand& A, const Operand& B, bool av, bool 
 
 }  // namespace
 
-size_t gemm_workspace(int64_t M, int64_t N, int64_t K, int /*dtype*/) {
+size_t gemm_workspace(int64_t M, int64_t N, int64_t K, int dtype) {
   if (M <= 0 || N <= 0 || K <= 0) return 0;
-  const Sched s = make_sched(M, N, K);
+  if (dtype == GIST_DTYPE_BF16_IN && gemm_bf16_packed_eligible(M, N, K))
+    return gemm_bf16_packed_workspace(M, N, K);
+  const Sched s = make_sched(M, N, K, dtype);
   if (!sched_split(s)) return 0;
   return static_cast<size_t>(sched_groups(s)) * 2 * BM * BN * sizeof(float);
 }
@@ -530,9 +536,11 @@ gist_status gemm(hipStream_t st, int64_t M, int64_t N, int64_t K, const Operand&
   if (M <= 0 || N <= 0) return GIST_OK;
   OutDev c{C.c0, C.c1, C.ldc0, C.ldc1, C.c_split, C.relu ? 1 : 0};
   if (K <= 0) return set_error(GIST_E_UNSUPPORTED, "gemm: K == 0");
-  if (K > (static_cast<int64_t>(INT32_MAX) - BK) * BK)
+  if (dtype == GIST_DTYPE_BF16_IN && gemm_bf16_packed_eligible(M, N, K))
+    return gemm_bf16_packed(st, M, N, K, A, B, C, ws, ws_bytes);
+  if (K > (static_cast<int64_t>(INT32_MAX) - KSH) * BK)
     return set_error(GIST_E_UNSUPPORTED, "gemm: K too large");
-  const Sched S = make_sched(M, N, K);
+  const Sched S = make_sched(M, N, K, dtype);
   const int64_t groups = sched_groups(S);
   const int64_t tiles = static_cast<int64_t>(S.tiles_m) * S.tiles_n;
   if (groups > INT32_MAX || tiles > INT32_MAX)

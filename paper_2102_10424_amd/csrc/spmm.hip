@@ -141,6 +141,83 @@ __global__ __launch_bounds__(256) void spmm_kernel(
   store_vec<VEC>(Y + row * ldy + c0, acc);
 }
 
+// Wide rows (64 lanes per row): the row index is wave-uniform, so each
+// nonzero's (col, val) is broadcast with readlane into scalar registers and
+// the gather address is a scalar base plus the lane's column offset; eight
+// gathers are kept in flight per wave.
+template <int VEC>
+__global__ __launch_bounds__(256) void spmm_wide_kernel(
+    int n, const int* __restrict__ rowptr, const int* __restrict__ col,
+    const float* __restrict__ val, const float* __restrict__ X, int64_t ldx, int width,
+    float* Y, int64_t ldy, const float* add, int64_t ld_add, int relu, int col_tiles,
+    int64_t nblocks) {
+  constexpr int kUnroll = 8;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t logical = xcd_remap(blockIdx.x, nblocks);
+  const int64_t rblock = logical / col_tiles;
+  const int ctile = static_cast<int>(logical % col_tiles);
+  const int64_t row = rblock * kWaves + wave;
+  if (row >= n) return;
+  const int c0 = ctile * (64 * VEC) + lane * VEC;
+  const bool active = c0 < width;
+  const int e0 = rowptr[row], e1 = rowptr[row + 1];
+  const float* Xc = X + c0;
+  float acc[VEC];
+#pragma unroll
+  for (int v = 0; v < VEC; ++v) acc[v] = 0.f;
+  for (int base = e0; base < e1; base += 64) {
+    const int cnt = min(64, e1 - base);
+    int my_c = 0;
+    float my_v = 0.f;
+    if (lane < cnt) {
+      my_c = col[base + lane];
+      my_v = val[base + lane];
+    }
+    int j = 0;
+    for (; j + kUnroll <= cnt; j += kUnroll) {
+      int cj[kUnroll];
+      float vj[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        cj[u] = __builtin_amdgcn_readlane(my_c, j + u);
+        vj[u] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_v), j + u));
+      }
+      if (active) {
+        float x[kUnroll][VEC];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) load_vec<VEC>(Xc + static_cast<int64_t>(cj[u]) * ldx, x[u]);
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+#pragma unroll
+          for (int v = 0; v < VEC; ++v) acc[v] = fmaf(vj[u], x[u][v], acc[v]);
+      }
+    }
+    for (; j < cnt; ++j) {
+      const int cj = __builtin_amdgcn_readlane(my_c, j);
+      const float vj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_v), j));
+      if (active) {
+        float x[VEC];
+        load_vec<VEC>(Xc + static_cast<int64_t>(cj) * ldx, x);
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) acc[v] = fmaf(vj, x[v], acc[v]);
+      }
+    }
+  }
+  if (!active) return;
+  if (add) {
+    float a[VEC];
+    load_vec<VEC>(add + row * ld_add + c0, a);
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) acc[v] += a[v];
+  }
+  if (relu) {
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) acc[v] = fmaxf(acc[v], 0.f);
+  }
+  store_vec<VEC>(Y + row * ldy + c0, acc);
+}
+
 template <int VEC, int LPR>
 gist_status launch(hipStream_t st, int64_t n, int64_t nnz, const int32_t* rowptr, const int32_t* col,
                    const float* val, const float* X, int64_t ldx, int width, float* Y,
@@ -157,9 +234,15 @@ gist_status launch(hipStream_t st, int64_t n, int64_t nnz, const int32_t* rowptr
   const double bytes = 4.0 * (n + 1) + 8.0 * static_cast<double>(nnz) +
                        4.0 * static_cast<double>(n) * width * (add ? 3.0 : 2.0);
   ProfScope ps(st, name, 2.0 * static_cast<double>(nnz) * width, bytes);
-  hipLaunchKernelGGL((spmm_kernel<VEC, LPR>), dim3(static_cast<unsigned>(nblocks)), dim3(256),
-                     0, st, static_cast<int>(n), rowptr, col, val, X, ldx, width, Y, ldy, add,
-                     ld_add, relu ? 1 : 0, col_tiles, nblocks);
+  if constexpr (LPR == 64) {
+    hipLaunchKernelGGL((spmm_wide_kernel<VEC>), dim3(static_cast<unsigned>(nblocks)), dim3(256),
+                       0, st, static_cast<int>(n), rowptr, col, val, X, ldx, width, Y, ldy, add,
+                       ld_add, relu ? 1 : 0, col_tiles, nblocks);
+  } else {
+    hipLaunchKernelGGL((spmm_kernel<VEC, LPR>), dim3(static_cast<unsigned>(nblocks)), dim3(256),
+                       0, st, static_cast<int>(n), rowptr, col, val, X, ldx, width, Y, ldy, add,
+                       ld_add, relu ? 1 : 0, col_tiles, nblocks);
+  }
   return check_launch("spmm");
 }
 
@@ -188,10 +271,15 @@ gist_status spmm(hipStream_t st, int64_t n, int64_t nnz, const int32_t* rowptr, 
   if (n <= 0 || width <= 0) return GIST_OK;
   const bool v4 = width % 4 == 0 && ldx % 4 == 0 && ldy % 4 == 0 && aligned16(X) &&
                   aligned16(Y) && (!add || (ld_add % 4 == 0 && aligned16(add)));
-  if (v4) return launch_vec<4>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add, relu);
   const bool v2 = width % 2 == 0 && ldx % 2 == 0 && ldy % 2 == 0 && aligned8(X) &&
                   aligned8(Y) && (!add || (ld_add % 2 == 0 && aligned8(add)));
+  // Prefer the widest vector that still fills a 64-lane row; a row that
+  // would need fewer than 33 lanes at 16 bytes uses 8-byte vectors instead
+  // when that gives a full-wave row (e.g. width 100: 50 lanes x 2 floats).
+  if (v4 && (width > 128 || width <= 64))
+    return launch_vec<4>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add, relu);
   if (v2) return launch_vec<2>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add, relu);
+  if (v4) return launch_vec<4>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add, relu);
   return launch_vec<1>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add, relu);
 }
 

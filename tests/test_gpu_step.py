@@ -25,7 +25,7 @@ from oracle import layers as OL
 from oracle import minibatch as OM
 from oracle import partition as OP
 
-from gpu_util import FP32_TOL, csr_to_dev, log, relerr, to_dev, to_host
+from gpu_util import BF16_TOL, FP32_TOL, csr_to_dev, log, relerr, to_dev, to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -86,10 +86,13 @@ def ctx(G):
 CONFIGS = ["c1", "c2", "c3", "c4"]
 
 
-@pytest.mark.parametrize("name", CONFIGS)
-def test_step_layerwise(G, ctx, name):
+@pytest.mark.parametrize("name,dtype", [(c, "f32") for c in CONFIGS] + [("c3", "bf16"),
+                                                                        ("c4", "bf16")])
+def test_step_layerwise(G, ctx, name, dtype):
     import torch
     w = workload(name)
+    dt = G.GIST_DTYPE_BF16_IN if dtype == "bf16" else G.GIST_DTYPE_F32
+    tol = BF16_TOL if dtype == "bf16" else FP32_TOL
     cfg, csr, ref = w["cfg"], w["csr"], w["ref"]
     kind = cfg.kind
     s = cfg.slice_widths()
@@ -99,7 +102,7 @@ def test_step_layerwise(G, ctx, name):
     lk = G.GIST_LAYER_SAGE_MEAN if kind == "sage" else G.GIST_LAYER_GCN
     for l in range(L):
         act = G.GIST_ACT_RELU if l < L - 1 else G.GIST_ACT_NONE
-        desc = G.layer_desc(lk, act, n, s[l], s[l + 1])
+        desc = G.layer_desc(lk, act, n, s[l], s[l + 1], dt)
         fws, bws = G.gist_layer_workspace_size(desc)
         ws = torch.empty(max(fws, bws, 1), dtype=torch.uint8, device="cuda")
         Wl = to_dev(stacked(kind, ref_params(w, l)).astype(np.float32))
@@ -120,9 +123,9 @@ def test_step_layerwise(G, ctx, name):
                              to_dev(np.asarray(dHo, dtype=np.float32)), dW, dH, ws)
         e_w = relerr(to_host(dW), stacked(kind, ref["grads"][l]))
         e_d = relerr(to_host(dH), ref["dH"][l]) if l > 0 else 0.0
-        log(f"[{name}] layer {l} ({s[l]}->{s[l + 1]}): H_out {e_h:.2e} agg {e_a:.2e} "
+        log(f"[{name} {dtype}] layer {l} ({s[l]}->{s[l + 1]}): H_out {e_h:.2e} agg {e_a:.2e} "
             f"dW {e_w:.2e} dH {e_d:.2e}")
-        assert max(e_h, e_a, e_w, e_d) <= FP32_TOL
+        assert max(e_h, e_a, e_w, e_d) <= tol
     # loss on the oracle's logits
     C = s[L]
     loss = torch.zeros(1, device="cuda")
