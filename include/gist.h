@@ -15,6 +15,7 @@
  *   gist_softmax_xent          loss and its gradient                    (device)
  *   gist_sgd_update            one SGD step                             (device)
  *   gist_subagg                subAgg: Theta[D_in, D_out] <- Theta^(i)  (device)
+ *   gist_subagg_gather         subAgg of one round + gather of the next (device)
  *
  * Conventions
  *  - Every matrix is row-major fp32 with the leading dimension stated.
@@ -273,6 +274,54 @@ gist_status gist_sgd_update(gist_ctx* ctx, float* W, const float* dW, int64_t n,
 gist_status gist_subagg(gist_ctx* ctx, float* Wg, int64_t ldg, const int32_t* rows,
                         int32_t nr, const int32_t* cols, int32_t nc,
                         const float* Ws, int64_t lds, uint32_t flags);
+
+/* ---- subAgg of one round fused with the gather of the next ---------- */
+
+/* Inverse of a partition (host): rank[idx[k]] = k for k < d, i.e. the
+ * position of each index in the block-ordered list gist_partition returns;
+ * index r is then the (rank[r] - offs[b])-th member of the block b with
+ * offs[b] <= rank[r] < offs[b+1].  Errors: GIST_E_INVAL for NULL pointers,
+ * offsets that are not ascending from 0 to d, or an index outside [0, d) or
+ * listed twice. */
+gist_status gist_partition_inverse(int64_t d, int32_t m, const int32_t* idx,
+                                   const int64_t* offs, int32_t* rank_out);
+
+/* How one global weight matrix (rows x cols) is split among m sub-GCNs in
+ * one round (device memory).  A partitioned dimension is given by its ranks
+ * (gist_partition_inverse) and its m + 1 block offsets; NULL ranks and
+ * offsets mean the dimension is not partitioned (every sub-GCN holds all of
+ * it at its own index: the input width at layer 0, the output width at the
+ * last layer, Section 3.1).  Element (r, c) belongs to sub-GCN i when the
+ * partitioned dimensions place both r and c in block i; it sits in slice i
+ * at (position of r in block i, position of c in block i), an unpartitioned
+ * index keeping its own value.  `slices` is a device array of m device
+ * pointers, each slice row-major with leading dimension `ld`.  The kernels
+ * trust these arrays: ranks and offsets must describe a partition (as the
+ * two host calls return them) and each slice must hold its block. */
+typedef struct gist_slice_set {
+  const int32_t* row_rank;
+  const int64_t* row_offs;
+  const int32_t* col_rank;
+  const int64_t* col_offs;
+  float* const* slices;
+  int64_t ld;
+} gist_slice_set;
+
+/* One pass over Wg (rows x cols, leading dimension ldg) that first applies
+ * subAgg for the slices of `done` (every entry a sub-GCN owns is replaced by
+ * its trained value; entries owned by none keep theirs, Section 3.2) and then
+ * gathers the slices of `next` from the updated matrix -- the end of one
+ * round of Algorithm 1 and the start of the next.  Either set may be NULL
+ * (plain gather, or plain subAgg).  Equal to gist_subagg for every slice of
+ * `done` followed by gist_gather_slice for every slice of `next`, bit for
+ * bit; every row of Wg is read and rewritten whole, so HBM sees full-line
+ * writes instead of 1/m-dense scattered ones.  The partitions of `done`
+ * and `next` may differ.  At least one dimension of each set must be
+ * partitioned when m > 1, and ranks and offsets come in pairs (GIST_E_INVAL
+ * otherwise). */
+gist_status gist_subagg_gather(gist_ctx* ctx, float* Wg, int64_t rows, int64_t cols,
+                               int64_t ldg, int32_t m, const gist_slice_set* done,
+                               const gist_slice_set* next);
 
 /* ---- instrumentation ------------------------------------------------ */
 

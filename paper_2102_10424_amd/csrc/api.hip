@@ -453,6 +453,38 @@ extern "C" gist_status gist_subagg(gist_ctx* ctx, float* Wg, int64_t ldg,
   return gist::scatter(ctx->stream, Wg, ldg, rows, nr, cols, nc, Ws, lds);
 }
 
+extern "C" gist_status gist_subagg_gather(gist_ctx* ctx, float* Wg, int64_t rows, int64_t cols,
+                                          int64_t ldg, int32_t m, const gist_slice_set* done,
+                                          const gist_slice_set* next) {
+  gist::clear_error();
+  if (!ctx) return set_error(GIST_E_INVAL, "subagg_gather: NULL ctx");
+  gist::ProfBind pb(ctx);
+  if (rows < 0 || cols < 0 || m < 1 || ldg < cols) return set_error(GIST_E_INVAL, "subagg_gather: bad sizes");
+  if (rows > INT32_MAX || cols > INT32_MAX)
+    return set_error(GIST_E_UNSUPPORTED, "subagg_gather: dimension exceeds int32 ranks");
+  if (rows == 0 || cols == 0 || (!done && !next)) return GIST_OK;
+  if (!Wg) return set_error(GIST_E_INVAL, "subagg_gather: NULL matrix");
+  for (const gist_slice_set* s : {done, next}) {
+    if (!s) continue;
+    if (!s->slices || s->ld < 1) return set_error(GIST_E_INVAL, "subagg_gather: bad slice set");
+    if (!s->row_rank != !s->row_offs || !s->col_rank != !s->col_offs)
+      return set_error(GIST_E_INVAL, "subagg_gather: ranks and offsets come in pairs");
+    if (m > 1 && !s->row_rank && !s->col_rank)
+      return set_error(GIST_E_INVAL, "subagg_gather: m > 1 needs a partitioned dimension");
+  }
+  gist::DeviceGuard dg(ctx->device);
+  // algorithmic bytes: the matrix read once (and written once with `done`),
+  // plus the slices' elements read (done) and written (next)
+  double bytes = (done ? 8.0 : 4.0) * static_cast<double>(rows) * cols;
+  auto slice_elems = [&](const gist_slice_set* s) {
+    const double fr = s->row_rank ? 1.0 / m : 1.0, fc = s->col_rank ? 1.0 / m : 1.0;
+    return static_cast<double>(rows) * cols * fr * fc * m;
+  };
+  if (done) bytes += 4.0 * slice_elems(done);
+  if (next) bytes += 4.0 * slice_elems(next);
+  return gist::subagg_gather(ctx->stream, Wg, rows, cols, ldg, m, done, next, bytes);
+}
+
 // ---------------------------------------------------------------------------
 // Instrumentation
 // ---------------------------------------------------------------------------

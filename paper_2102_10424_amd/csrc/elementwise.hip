@@ -165,7 +165,267 @@ __global__ __launch_bounds__(kBlock) void xent_finish_kernel(int nparts, const f
   if (threadIdx.x == 0) loss[0] = n > 0 ? sh[0] / static_cast<float>(n) : 0.f;
 }
 
+
+// subAgg of one round fused with the gather of the next.  One block per
+// (row, 4*kBlock-column chunk) of the global matrix, one 4-column group per
+// thread and no loop: every load a thread issues (the matrix, the columns'
+// ranks, the trained values) is independent of its stores, so the latency
+// chain is paid once per thread and hidden by the other resident waves.
+// Every entry owned by a sub-GCN of `done` takes its trained value, the
+// group is written back whole (full-line writes), and the entries owned by
+// a sub-GCN of `next` are copied into its slice.
+//
+// A partitioned row belongs to one block b, found once per thread; its
+// slice row and block b's column-rank range [col_offs[b], col_offs[b+1])
+// then place each column with one compare.  Only an unpartitioned row (the
+// input width at layer 0) looks up each column's block.
+struct SliceSetDev {
+  const int* row_rank;
+  const int64_t* row_offs;
+  const int* col_rank;
+  const int64_t* col_offs;
+  float* const* slices;
+  int64_t ld;
+};
+
+// Block b of a partition with offs[b] <= k < offs[b+1] (empty blocks allowed).
+__device__ __forceinline__ int block_of(const int64_t* offs, int m, int64_t k) {
+  int lo = 0, hi = m;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (offs[mid] <= k) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+struct RowSel {
+  float* base;     // partitioned row: its row in the owner's slice
+  int64_t lo, hi;  // the owner's column-rank range
+};
+
+__device__ __forceinline__ RowSel row_select(const SliceSetDev& s, int m, int64_t r) {
+  RowSel q{nullptr, 0, 0};
+  if (s.row_rank) {
+    const int64_t kr = s.row_rank[r];
+    const int b = block_of(s.row_offs, m, kr);
+    q.base = s.slices[b] + (kr - s.row_offs[b]) * s.ld;
+    if (s.col_rank) { q.lo = s.col_offs[b]; q.hi = s.col_offs[b + 1]; }
+  }
+  return q;
+}
+
+// Address of element (r, c), column rank kc, in its owner's slice; nullptr
+// when no sub-GCN owns it.
+__device__ __forceinline__ float* slot_of(const SliceSetDev& s, int m, const RowSel& q, int64_t r,
+                                          int64_t c, int kc) {
+  if (s.row_rank) {
+    if (!s.col_rank) return q.base + c;
+    return (kc >= q.lo && kc < q.hi) ? q.base + (kc - q.lo) : nullptr;
+  }
+  if (!s.col_rank) return s.slices[0] + r * s.ld + c;   // m == 1
+  const int b = block_of(s.col_offs, m, kc);
+  return s.slices[b] + r * s.ld + (kc - s.col_offs[b]);
+}
+
+template <bool VEC4>
+__device__ __forceinline__ void ranks4(const int* rank, int64_t c0, int nq, int (&k)[4]) {
+  if (!rank) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) k[q] = 0;
+    return;
+  }
+  if constexpr (VEC4) {
+    const int4 t = *reinterpret_cast<const int4*>(rank + c0);
+    k[0] = t.x; k[1] = t.y; k[2] = t.z; k[3] = t.w;
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) k[q] = q < nq ? rank[c0 + q] : 0;
+  }
+}
+
+__device__ __forceinline__ int wave_min_int(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+__device__ __forceinline__ int wave_max_int(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// Fast path, used when every given set partitions the rows and the widths
+// are float4-aligned.  A row then has one owner per set, and the columns it
+// owns are block b's members: with ascending blocks (as gist_partition
+// returns them) the owned columns inside one wave's 256 consecutive columns
+// are consecutive members, i.e. one contiguous run of slice positions.  The
+// gather half stages that run in LDS at (position - first) and stores it
+// with consecutive lanes instead of one sparse store per column; a wave
+// whose owned positions are not contiguous stores them one by one.
+template <bool DONE, bool NEXT>
+__global__ __launch_bounds__(kBlock) void subagg_gather_rows_kernel(
+    float* __restrict__ Wg, int64_t rows, int64_t cols, int64_t ldg, int64_t chunks, int m,
+    SliceSetDev done, SliceSetDev next) {
+  __shared__ float stage[kBlock / 64][256];
+  const int64_t b = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t r = b / chunks;
+  if (r >= rows) return;   // block-uniform
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int64_t c0 = (b - r * chunks) * (4 * kBlock) + 4 * static_cast<int64_t>(threadIdx.x);
+  const bool in = c0 < cols;   // cols % 4 == 0: a group is wholly in or out
+  float* __restrict__ w = Wg + r * ldg + c0;
+  float v[4] = {0.f, 0.f, 0.f, 0.f};
+  if (in) {
+    const float4 t = *reinterpret_cast<const float4*>(w);
+    v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+  }
+  // Column keys: the rank when the columns are partitioned, else the
+  // column itself (owned by every row owner); -1 outside the matrix.
+  int kd[4], kn[4];
+  RowSel qd{nullptr, 0, 0}, qn{nullptr, 0, 0};
+  if (DONE) {
+    if (done.col_rank && in) ranks4<true>(done.col_rank, c0, 4, kd);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (!done.col_rank || !in) kd[q] = in ? static_cast<int>(c0 + q) : -1;
+    qd = row_select(done, m, r);
+    if (!done.col_rank) { qd.lo = 0; qd.hi = cols; }
+  }
+  if (NEXT) {
+    if (next.col_rank && in) ranks4<true>(next.col_rank, c0, 4, kn);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (!next.col_rank || !in) kn[q] = in ? static_cast<int>(c0 + q) : -1;
+    qn = row_select(next, m, r);
+    if (!next.col_rank) { qn.lo = 0; qn.hi = cols; }
+  }
+  if (DONE) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (kd[q] >= qd.lo && kd[q] < qd.hi) v[q] = qd.base[kd[q] - qd.lo];
+    if (in) *reinterpret_cast<float4*>(w) = make_float4(v[0], v[1], v[2], v[3]);
+  }
+  if (NEXT) {
+    int first = INT32_MAX, last = -1, cnt = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const bool own = kn[q] >= qn.lo && kn[q] < qn.hi;
+      if (own) { first = min(first, kn[q]); last = max(last, kn[q]); }
+      cnt += __popcll(__ballot(own));
+    }
+    first = wave_min_int(first);
+    last = wave_max_int(last);
+    const bool run = cnt > 0 && last - first + 1 == cnt;   // wave-uniform
+    if (run) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (kn[q] >= qn.lo && kn[q] < qn.hi) stage[wv][kn[q] - first] = v[q];
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (kn[q] >= qn.lo && kn[q] < qn.hi) qn.base[kn[q] - qn.lo] = v[q];
+    }
+    __syncthreads();
+    if (run) {
+      float* dst = qn.base + (first - qn.lo);
+      for (int j = lane; j < cnt; j += 64) dst[j] = stage[wv][j];
+    }
+  }
+}
+
+template <bool VEC4>
+__global__ __launch_bounds__(kBlock) void subagg_gather_kernel(float* __restrict__ Wg, int64_t rows,
+                                                              int64_t cols, int64_t ldg,
+                                                              int64_t chunks, int m,
+                                                              SliceSetDev done, int has_done,
+                                                              SliceSetDev next, int has_next) {
+  const int64_t b = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t r = b / chunks;
+  const int64_t c0 = (b - r * chunks) * (4 * kBlock) + 4 * static_cast<int64_t>(threadIdx.x);
+  if (r >= rows || c0 >= cols) return;
+  const int nq = cols - c0 < 4 ? static_cast<int>(cols - c0) : 4;
+  float* __restrict__ w = Wg + r * ldg + c0;
+  float v[4];
+  if constexpr (VEC4) {
+    const float4 t = *reinterpret_cast<const float4*>(w);
+    v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = q < nq ? w[q] : 0.f;
+  }
+  int kd[4], kn[4];
+  RowSel qd{nullptr, 0, 0}, qn{nullptr, 0, 0};
+  if (has_done) {
+    ranks4<VEC4>(done.col_rank, c0, nq, kd);
+    qd = row_select(done, m, r);
+  }
+  if (has_next) {
+    ranks4<VEC4>(next.col_rank, c0, nq, kn);
+    qn = row_select(next, m, r);
+  }
+  if (has_done) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float* p = q < nq ? slot_of(done, m, qd, r, c0 + q, kd[q]) : nullptr;
+      if (p) v[q] = *p;
+    }
+    if constexpr (VEC4) {
+      *reinterpret_cast<float4*>(w) = make_float4(v[0], v[1], v[2], v[3]);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (q < nq) w[q] = v[q];
+    }
+  }
+  if (has_next) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float* p = q < nq ? slot_of(next, m, qn, r, c0 + q, kn[q]) : nullptr;
+      if (p) *p = v[q];
+    }
+  }
+}
+
 }  // namespace
+
+gist_status subagg_gather(hipStream_t st, float* Wg, int64_t rows, int64_t cols, int64_t ldg,
+                          int m, const gist_slice_set* done, const gist_slice_set* next,
+                          double bytes) {
+  SliceSetDev d{}, n{};
+  if (done) d = SliceSetDev{done->row_rank, done->row_offs, done->col_rank, done->col_offs,
+                            done->slices, done->ld};
+  if (next) n = SliceSetDev{next->row_rank, next->row_offs, next->col_rank, next->col_offs,
+                            next->slices, next->ld};
+  const int64_t chunks = (cols + 4 * kBlock - 1) / (4 * kBlock);
+  if (rows * chunks > static_cast<int64_t>(UINT32_MAX))
+    return set_error(GIST_E_UNSUPPORTED, "subagg_gather: matrix too large for one launch");
+  bool vec = cols % 4 == 0 && ldg % 4 == 0 && aligned16(Wg);
+  for (const SliceSetDev* s : {&d, &n})
+    if (s->col_rank) vec = vec && aligned16(s->col_rank);
+  const dim3 grid(static_cast<unsigned>(rows * chunks));
+  ProfScope ps(st, "subagg_gather", 0.0, bytes);
+  const bool rows_part = (!done || done->row_rank) && (!next || next->row_rank);
+  if (vec && rows_part) {
+    const int dn = done ? 1 : 0, nx = next ? 1 : 0;
+    if (dn && nx)
+      hipLaunchKernelGGL((subagg_gather_rows_kernel<true, true>), grid, dim3(kBlock), 0, st, Wg,
+                         rows, cols, ldg, chunks, m, d, n);
+    else if (dn)
+      hipLaunchKernelGGL((subagg_gather_rows_kernel<true, false>), grid, dim3(kBlock), 0, st, Wg,
+                         rows, cols, ldg, chunks, m, d, n);
+    else
+      hipLaunchKernelGGL((subagg_gather_rows_kernel<false, true>), grid, dim3(kBlock), 0, st, Wg,
+                         rows, cols, ldg, chunks, m, d, n);
+  } else if (vec) {
+    hipLaunchKernelGGL(subagg_gather_kernel<true>, grid, dim3(kBlock), 0, st, Wg, rows, cols, ldg,
+                       chunks, m, d, done ? 1 : 0, n, next ? 1 : 0);
+  } else {
+    hipLaunchKernelGGL(subagg_gather_kernel<false>, grid, dim3(kBlock), 0, st, Wg, rows, cols, ldg,
+                       chunks, m, d, done ? 1 : 0, n, next ? 1 : 0);
+  }
+  return check_launch("subagg_gather");
+}
 
 gist_status relu_mask(hipStream_t st, int64_t count, const float* dH, const float* Hout,
                       float* dZ) {

@@ -76,3 +76,27 @@ extern "C" gist_status gist_partition(int64_t d, int32_t m, uint64_t seed,
   std::memcpy(idx_out, p.data(), sizeof(int32_t) * d);
   return GIST_OK;
 }
+
+extern "C" gist_status gist_partition_inverse(int64_t d, int32_t m, const int32_t* idx,
+                                              const int64_t* offs, int32_t* rank_out) {
+  using gist::set_error;
+  gist::clear_error();
+  if (!idx || !offs || !rank_out)
+    return set_error(GIST_E_INVAL, "gist_partition_inverse: NULL pointer");
+  if (d < 1 || m < 1 || d > INT32_MAX)
+    return set_error(GIST_E_INVAL, "gist_partition_inverse: bad sizes");
+  if (offs[0] != 0 || offs[m] != d)
+    return set_error(GIST_E_INVAL, "gist_partition_inverse: offsets do not cover [0, d)");
+  for (int32_t b = 0; b < m; ++b)
+    if (offs[b + 1] < offs[b])
+      return set_error(GIST_E_INVAL, "gist_partition_inverse: offsets not ascending");
+  std::vector<char> seen(static_cast<size_t>(d), 0);
+  for (int64_t k = 0; k < d; ++k) {
+    const int32_t r = idx[k];
+    if (r < 0 || r >= d || seen[r])
+      return set_error(GIST_E_INVAL, "gist_partition_inverse: index out of range or repeated");
+    seen[r] = 1;
+    rank_out[r] = static_cast<int32_t>(k);
+  }
+  return GIST_OK;
+}

@@ -23,6 +23,12 @@ if not os.path.exists(LIB_PATH):
         f"libgist.so not found at {LIB_PATH}: build it with "
         "`python -m paper_2102_10424_amd.build` (hipcc, gfx950)")
 
+# Device memory and streams come from PyTorch, so the library must run on
+# PyTorch's HIP runtime: importing torch first makes the dynamic loader bind
+# libgist's libamdhip64.so.7 to that already-loaded copy instead of loading a
+# second runtime that owns none of torch's allocations.
+import torch  # noqa: E402,F401  (load order matters, see above)
+
 _lib = C.CDLL(LIB_PATH)
 
 # ---- enums / flags (mirror include/gist.h) ---------------------------------
@@ -50,8 +56,8 @@ EXPORTED = (
     "gist_set_stream", "gist_partition", "gist_build_minibatch_csr",
     "gist_layer_workspace_size", "gist_gcn_layer_fwd", "gist_gcn_layer_bwd",
     "gist_softmax_xent_workspace", "gist_softmax_xent", "gist_gather_slice",
-    "gist_sgd_update", "gist_subagg", "gist_profile_begin", "gist_profile_read",
-    "gist_profile_end",
+    "gist_sgd_update", "gist_subagg", "gist_partition_inverse", "gist_subagg_gather",
+    "gist_profile_begin", "gist_profile_read", "gist_profile_end",
 )
 
 
@@ -86,6 +92,11 @@ class gist_layer_desc(C.Structure):
                 ("s_out", C.c_int32)]
 
 
+class gist_slice_set(C.Structure):
+    _fields_ = [("row_rank", C.c_void_p), ("row_offs", C.c_void_p), ("col_rank", C.c_void_p),
+                ("col_offs", C.c_void_p), ("slices", C.c_void_p), ("ld", C.c_int64)]
+
+
 class gist_prof_entry(C.Structure):
     _fields_ = [("name", C.c_char * 48), ("launches", C.c_int64), ("ms", C.c_double),
                 ("flops", C.c_double), ("bytes", C.c_double)]
@@ -97,6 +108,9 @@ _sigs = {
     "gist_profile_read": (C.c_int, [_P, C.POINTER(gist_prof_entry), C.c_int32,
                                     C.POINTER(C.c_int32), C.POINTER(C.c_int64)]),
     "gist_profile_end": (C.c_int, [_P]),
+    "gist_partition_inverse": (C.c_int, [C.c_int64, C.c_int32, _P, _P, _P]),
+    "gist_subagg_gather": (C.c_int, [_P, _P, C.c_int64, C.c_int64, C.c_int64, C.c_int32,
+                                     C.POINTER(gist_slice_set), C.POINTER(gist_slice_set)]),
     "gist_last_error": (C.c_char_p, []),
     "gist_status_str": (C.c_char_p, [C.c_int]),
     "gist_create": (C.c_int, [C.c_int, _P, C.POINTER(_P)]),
@@ -182,6 +196,16 @@ def gist_partition(d, m, seed, flags=0):
     _check(_lib.gist_partition(int(d), int(m), int(seed) & (2**64 - 1), int(flags),
                                _ptr(idx), _ptr(offs)))
     return idx[:int(d)], offs
+
+
+def gist_partition_inverse(idx, offs):
+    """rank int32[d] with rank[idx[k]] = k."""
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    offs = np.ascontiguousarray(offs, dtype=np.int64)
+    d, m = idx.shape[0], offs.shape[0] - 1
+    rank = np.empty(d, dtype=np.int32)
+    _check(_lib.gist_partition_inverse(d, m, _ptr(idx), _ptr(offs), _ptr(rank)))
+    return rank
 
 
 def _graph_struct(graph):
@@ -298,6 +322,18 @@ def gist_gather_slice(ctx, Wg, ldg, rows, nr, cols, nc, Ws, lds):
 
 def gist_sgd_update(ctx, W, dW, n, lr):
     _check(_lib.gist_sgd_update(ctx.handle, _ptr(W), _ptr(dW), int(n), float(lr)))
+
+
+def slice_set(row_rank, row_offs, col_rank, col_offs, slice_ptrs, ld):
+    """A ``gist_slice_set`` over device tensors (ranks int32, offsets int64, pointer table int64)."""
+    return gist_slice_set(_ptr(row_rank), _ptr(row_offs), _ptr(col_rank), _ptr(col_offs),
+                          _ptr(slice_ptrs), int(ld))
+
+
+def gist_subagg_gather(ctx, Wg, rows, cols, ldg, m, done, next_):
+    _check(_lib.gist_subagg_gather(ctx.handle, _ptr(Wg), int(rows), int(cols), int(ldg), int(m),
+                                   C.byref(done) if done is not None else None,
+                                   C.byref(next_) if next_ is not None else None))
 
 
 def gist_subagg(ctx, Wg, ldg, rows, nr, cols, nc, Ws, lds, flags=0):

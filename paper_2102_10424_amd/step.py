@@ -212,9 +212,17 @@ class GistModel:
 
     ``theta[l]`` is a list of parts (GCN: [Theta_l]; SAGE: [W_self, W_neigh]),
     each (d_l x d_{l+1}) fp32 on the device.
+
+    A round is ``set_partitions`` -> ``begin_round`` -> m sub-GCN steps on
+    ``params`` -> ``end_round``.  With ``fused`` (default) the subAgg of a
+    round is deferred and performed by the next round's ``begin_round`` in
+    the same pass over Theta as that round's gather (gist_subagg_gather);
+    ``finalize`` applies a pending subAgg.  The slices are double-buffered
+    so that the trained slices of round t and the gathered slices of round
+    t+1 never share memory.
     """
 
-    def __init__(self, ctx, kind, widths, m, theta, device="cuda"):
+    def __init__(self, ctx, kind, widths, m, theta, device="cuda", fused=True):
         self.ctx = ctx
         self.kind = kind
         self.widths = list(widths)
@@ -222,40 +230,66 @@ class GistModel:
         self.m = m
         self.theta = theta
         self.device = device
+        self.fused = fused
         self.parts = 2 if kind == "sage" else 1
         self.slice_widths = [widths[0]] + [widths[l] // m for l in range(1, self.L)] + [widths[-1]]
-        self.part_dev = [None] * (self.L + 1)
-        self.part_host = [None] * (self.L + 1)
-        self._pin = [None] * (self.L + 1)
-        self._part_event = None
-        # per sub-GCN parameter slices (SAGE: [W_self; W_neigh] stacked)
         s = self.slice_widths
-        self.params = [[torch.empty(self.parts * s[l], s[l + 1], device=device)
-                        for l in range(self.L)] for _ in range(m)]
+        nbuf = 2 if fused else 1
+        # per sub-GCN parameter slices (SAGE: [W_self; W_neigh] stacked)
+        self._bufs = [[[torch.empty(self.parts * s[l], s[l + 1], device=device)
+                        for l in range(self.L)] for _ in range(m)] for _ in range(nbuf)]
+        # device tables of the m slice pointers of every (buffer, layer, part)
+        self._ptrs = [[[torch.tensor([self._bufs[b][i][l].data_ptr() + 4 * p * s[l] * s[l + 1]
+                                      for i in range(m)], dtype=torch.int64).to(device)
+                        for p in range(self.parts)] for l in range(self.L)] for b in range(nbuf)]
+        self.buf = 0
+        self.params = self._bufs[0]
+        # two round slots of partition data: host (idx, offs); device
+        # [idx; rank] (int32) and offs (int64)
+        self._slot = 1
+        self._host = [[None] * (self.L + 1) for _ in range(2)]
+        self._pin = [[None] * (self.L + 1) for _ in range(2)]
+        self._dev = [[None] * (self.L + 1) for _ in range(2)]
+        self._doffs = [[None] * (self.L + 1) for _ in range(2)]
+        self._events = [None, None]
+        self.pending = None    # (slot, buffer) whose subAgg is outstanding
 
+    # -- partitions ---------------------------------------------------------
     def set_partitions(self, seeds):
         """``subGCNs`` partitions of every hidden width; ``seeds[l]`` for l = 1..L-1.
 
-        The indices are written into pinned host buffers and uploaded
-        asynchronously, so the host does not wait for the previous round.
+        Indices, ranks and offsets go through pinned buffers with
+        asynchronous uploads, so the host does not wait for earlier rounds.
         """
-        if self._part_event is not None:
-            self._part_event.synchronize()   # last upload from the pinned buffers done
+        slot = 1 - self._slot
+        if self._events[slot] is not None:
+            self._events[slot].synchronize()   # the pinned buffers' last upload is done
+        m = self.m
         for l in range(1, self.L):
             d = self.widths[l]
-            if self._pin[l] is None:
-                self._pin[l] = torch.empty(d, dtype=torch.int32, pin_memory=True)
-                self.part_dev[l] = torch.empty(d, dtype=torch.int32, device=self.device)
-            idx, offs = G.gist_partition(d, self.m, seeds[l])
-            self._pin[l].numpy()[:] = idx
-            self.part_host[l] = (idx, offs)
-            self.part_dev[l].copy_(self._pin[l], non_blocking=True)
-        self._part_event = torch.cuda.Event()
-        self._part_event.record()
+            if self._pin[slot][l] is None:
+                # int32 [idx; rank] followed by the int64 offsets (as 2(m+1) int32)
+                self._pin[slot][l] = torch.empty(2 * d + 2 * (m + 1), dtype=torch.int32,
+                                                 pin_memory=True)
+                self._dev[slot][l] = torch.empty(2, d, dtype=torch.int32, device=self.device)
+                self._doffs[slot][l] = torch.empty(m + 1, dtype=torch.int64, device=self.device)
+            idx, offs = G.gist_partition(d, m, seeds[l])
+            rank = G.gist_partition_inverse(idx, offs)
+            h = self._pin[slot][l].numpy()
+            h[:d], h[d:2 * d] = idx, rank
+            h[2 * d:].view(np.int64)[:] = offs
+            self._host[slot][l] = (idx, offs)
+            pin = self._pin[slot][l]
+            self._dev[slot][l].view(-1).copy_(pin[:2 * d], non_blocking=True)
+            self._doffs[slot][l].copy_(pin[2 * d:].view(torch.int64), non_blocking=True)
+        ev = torch.cuda.Event()
+        ev.record()
+        self._events[slot] = ev
+        self._slot = slot
 
     def _block(self, l, i):
-        idx, offs = self.part_host[l]
-        return self.part_dev[l][int(offs[i]):int(offs[i + 1])], int(offs[i + 1] - offs[i])
+        idx, offs = self._host[self._slot][l]
+        return self._dev[self._slot][l][0][int(offs[i]):int(offs[i + 1])], int(offs[i + 1] - offs[i])
 
     def _rc(self, l, i):
         if l == 0:
@@ -268,6 +302,16 @@ class GistModel:
             cols, nc = self._block(l + 1, i)
         return rows, nr, cols, nc
 
+    def _set(self, slot, buf, l, p):
+        """gist_slice_set of layer l, part p: partition `slot`, slice buffer `buf`."""
+        rr = ro = cr = co = None
+        if l > 0:
+            rr, ro = self._dev[slot][l][1], self._doffs[slot][l]
+        if l + 1 < self.L:
+            cr, co = self._dev[slot][l + 1][1], self._doffs[slot][l + 1]
+        return G.slice_set(rr, ro, cr, co, self._ptrs[buf][l][p], self.slice_widths[l + 1])
+
+    # -- per-slice calls ----------------------------------------------------
     def gather(self, i):
         """Theta^(i)_l = Theta_l[D_l^(i), D_{l+1}^(i)] for every layer and part."""
         for l in range(self.L):
@@ -285,3 +329,41 @@ class GistModel:
                 src = self.params[i][l][p * nr:(p + 1) * nr]
                 G.gist_subagg(self.ctx, self.theta[l][p], self.widths[l + 1], rows, nr, cols,
                               nc, src, nc, flags)
+
+    # -- rounds ---------------------------------------------------------------
+    def begin_round(self):
+        """Gather this round's slices (after any pending subAgg of the last one)."""
+        if not self.fused:
+            for i in range(self.m):
+                self.gather(i)
+            return
+        nxt = 1 - self.buf if self.pending is not None else self.buf
+        for l in range(self.L):
+            for p in range(self.parts):
+                done = (self._set(self.pending[0], self.pending[1], l, p)
+                        if self.pending is not None else None)
+                G.gist_subagg_gather(self.ctx, self.theta[l][p], self.widths[l],
+                                     self.widths[l + 1], self.widths[l + 1], self.m, done,
+                                     self._set(self._slot, nxt, l, p))
+        self.buf = nxt
+        self.params = self._bufs[nxt]
+        self.pending = None
+
+    def end_round(self):
+        """subAgg of this round's trained slices (deferred when fused)."""
+        if not self.fused:
+            for i in range(self.m):
+                self.subagg(i)
+            return
+        self.pending = (self._slot, self.buf)
+
+    def finalize(self):
+        """Apply a pending subAgg so that Theta holds every trained slice."""
+        if self.pending is None:
+            return
+        for l in range(self.L):
+            for p in range(self.parts):
+                G.gist_subagg_gather(self.ctx, self.theta[l][p], self.widths[l],
+                                     self.widths[l + 1], self.widths[l + 1], self.m,
+                                     self._set(self.pending[0], self.pending[1], l, p), None)
+        self.pending = None

@@ -59,6 +59,35 @@ def test_partition_categorical_bit_exact(d, m):
         assert np.array_equal(offs, np.asarray(oo, dtype=np.int64))
 
 
+def test_single_hip_runtime():
+    """The binding runs on PyTorch's HIP runtime; no second copy is loaded."""
+    maps = {line.split()[-1] for line in open("/proc/self/maps") if "libamdhip64" in line}
+    assert len(maps) == 1, maps
+
+
+@pytest.mark.parametrize("d,m,cat", [(64, 4, False), (32768, 8, False), (1000, 8, True),
+                                     (7, 1, False)])
+def test_partition_inverse(d, m, cat):
+    """The rank of index r is its place in the block-ordered list: block b's
+    k-th member r has offs[b] + k == rank[r], so rank is a bijection of
+    [0, d) that recovers each index's block and position."""
+    oi, oo = P.partition(d, m, 9, categorical=cat)
+    rank = G.gist_partition_inverse(np.asarray(oi, np.int32), np.asarray(oo, np.int64))
+    for b, blk in enumerate(P.blocks_of(oi, oo)):
+        for k, r in enumerate(blk):
+            assert rank[r] == oo[b] + k
+    assert sorted(rank.tolist()) == list(range(d))
+
+
+def test_partition_inverse_errors():
+    with pytest.raises(G.GistError):
+        G.gist_partition_inverse(np.array([0, 2, 1, 2], np.int32), np.array([0, 2, 4]))
+    with pytest.raises(G.GistError):
+        G.gist_partition_inverse(np.arange(4, dtype=np.int32), np.array([0, 3, 2, 4]))
+    with pytest.raises(G.GistError):
+        G.gist_partition_inverse(np.array([0, 1, 5], np.int32), np.array([0, 3]))
+
+
 @pytest.mark.parametrize("d,m,flags", [(10, 3, 0), (4, 0, 0), (4, 5, 0), (0, 1, 0), (8, 2, 4)])
 def test_partition_errors(d, m, flags):
     with pytest.raises(G.GistError) as e:
