@@ -7,11 +7,12 @@ block model (15,000 blocks, ~61.9M edges, 100 input features, 47 classes).
 One timed step is one pass of the whole hot path:
 
   subGCNs partition of the three hidden widths (host)
-  -> gather of all 8 sub-GCN weight slices (device)
+  -> one pass over the 16 GiB global model that applies the previous
+     round's subAgg and gathers all 8 sub-GCN weight slices (device)
   -> for each sub-GCN: cluster mini-batch of 10 blocks (host CSR build into
      pinned memory, asynchronous upload, device feature-row gather),
-     forward through 4 layers, softmax cross-entropy, backward, SGD
-  -> subAgg of all 8 slices into the 16 GiB global model.
+     forward through 4 layers, softmax cross-entropy, backward, SGD.
+  The last round's subAgg is applied after the timed region.
 
 Inputs are seeded synthetic data resident in HBM before timing starts.
 The reported value is ms per sub-GCN step = round time / m.  Kernel times
@@ -19,8 +20,8 @@ come from HIP events the library records on the launch stream during the
 timed rounds (gist_profile_*).  The CPU baseline is the fp64 oracle timed on
 one sub-GCN step of the same workload.
 
-Prints ONE JSON line.  ``--gpus N`` with N > 1 exits: this build runs on one
-GPU (the multi-GPU design is described in the design doc).
+Prints ONE JSON line.  ``--gpus N`` with N > 1 exits: the benchmark runs on
+exactly one GPU.
 """
 
 import argparse
@@ -35,6 +36,42 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK = {"f32": 157.3, "bf16": 2516.6}   # dense MFMA TFLOP/s, MI355X
+CSRC = os.path.join(ROOT, "paper_2102_10424_amd", "csrc")
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def kernel_source_hash():
+    """sha256 over the library's kernel and host sources (names and bytes)."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(CSRC)):
+        if f.endswith((".hip", ".h", ".cuh", ".cpp")):
+            h.update(f.encode())
+            h.update(open(os.path.join(CSRC, f), "rb").read())
+    return h.hexdigest()
+
+
+def recorded_traffic(variant, workload, dtype):
+    """Calibrated HBM bytes per launch of `variant` from the rocprofv3 counter
+    records under profiles/ -- only if they were taken on these very sources."""
+    if not os.path.isdir(PROFILES):
+        return None
+    src = kernel_source_hash()
+    for f in sorted(os.listdir(PROFILES)):
+        if not f.endswith(".md"):
+            continue
+        block = False
+        for line in open(os.path.join(PROFILES, f)):
+            if line.startswith("```traffic"):
+                block = True
+            elif line.startswith("```"):
+                block = False
+            elif block:
+                r = json.loads(line)
+                if (r["variant"], r["workload"], r["dtype"], r["src_sha256"]) == (
+                        variant, workload, dtype, src):
+                    return r["fetch_bytes"] + r["write_bytes"]
+    return None
 HBM_PEAK_GBS = 8000.0
 METRIC = "sub-GCN fwd+bwd step ms; SpMM GB/s and GEMM TFLOP/s as % of MI355X peak"
 
@@ -261,8 +298,7 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build runs on exactly one GPU; --gpus must be 1 "
-                                   "(multi-GPU sharding is described in DESIGN.md)"}))
+        print(json.dumps({"error": "the benchmark runs on exactly one GPU; --gpus must be 1"}))
         sys.exit(2)
     import torch
     from gist_synth import get_config
@@ -325,6 +361,12 @@ def main():
                         "traffic": None, "avg_launch_us": round(avg_s * 1e6, 2),
                         "units_per_launch": round(v["bytes"] / v["launches"] / 1e9, 4),
                         "unit_desc": "GB algorithmic per launch"}
+    dtype_name = "bf16-in/f32-acc" if args.dtype == "bf16" else "f32"
+    if roofline:
+        t = recorded_traffic(roofline["kernel"], args.config, dtype_name)
+        roofline["traffic"] = t
+        roofline["traffic_unit"] = "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, " \
+                                   "copy-calibrated; null unless taken on these sources)"
     per_unit = wl.steps_per_unit()
     value = ms_step / per_unit
     cpu = None
@@ -341,14 +383,14 @@ def main():
         "metric": METRIC, "value": round(value, 4), "unit": "ms",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_step, 3), "higher_is_better": False, "scaling": "weak",
-        "vs_baseline": None, "dtype": "bf16-in/f32-acc" if args.dtype == "bf16" else "f32",
+        "vs_baseline": None, "dtype": dtype_name,
         "data": "synthetic (seeded SBM / Chung-Lu / ER graphs, N(0,1) features, Glorot weights)",
         "config": dict(wl.describe(), parallelism="single GPU, m sub-GCNs back to back",
                        step="one GIST round" if per_unit > 1 else "one layer fwd+bwd",
                        value="ms per sub-GCN step (round time / m)" if per_unit > 1
                        else "ms per layer fwd+bwd"),
         "roofline": roofline, "cpu_baseline": cpu, "kernels": kernels,
-        "profile_dropped": dropped,
+        "profile_dropped": dropped, "kernel_src_sha256": kernel_source_hash(),
     }
     print(json.dumps(out), flush=True)
 

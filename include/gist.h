@@ -47,7 +47,7 @@ typedef enum gist_status {
                                label or cluster id out of range, ...          */
   GIST_E_NOMEM = -2,        /* caller buffer / workspace too small            */
   GIST_E_DEVICE = -3,       /* HIP runtime error (text in gist_last_error)    */
-  GIST_E_UNSUPPORTED = -4,  /* valid request this build does not implement    */
+  GIST_E_UNSUPPORTED = -4,  /* valid request the library does not implement */
   GIST_E_NONFINITE = -5     /* GIST_SUBAGG_CHECK_FINITE found a NaN/Inf       */
 } gist_status;
 

@@ -5,7 +5,7 @@ clusters of the training graph), Algorithm 1 (``Cluster``), eq. (1) (the
 aggregation matrix is the degree-normalised adjacency with self-loops) and
 Appendix A.2 (the theory form I + D^-1/2 A D^-1/2).
 
-Readings fixed by this build where the paper is silent:
+Readings fixed here where the paper is silent:
 
 * the mini-batch keeps every edge whose two ends are both selected, and
   degrees are those of this induced subgraph;

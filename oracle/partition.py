@@ -1,8 +1,8 @@
 """``subGCNs``: random disjoint partition of a feature dimension into m blocks.
 
 Paper: Section 3.1 (with its footnote example d=4, m=2 giving blocks {1,4}
-and {2,3}) and Algorithm 1.  The paper fixes only "random, disjoint, equally
-sized"; this build fixes the randomness as follows so two independent
+and {2,3}) and Algorithm 1.  The paper asks only for a random partition into disjoint blocks of equal
+size; the randomness is fixed as follows so two independent
 implementations agree bit for bit:
 
 * generator: SplitMix64 (Steele, Lea & Flood, "Fast splittable pseudorandom

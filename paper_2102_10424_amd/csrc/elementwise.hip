@@ -404,8 +404,8 @@ gist_status subagg_gather(hipStream_t st, float* Wg, int64_t rows, int64_t cols,
   for (const SliceSetDev* s : {&d, &n})
     if (s->col_rank) vec = vec && aligned16(s->col_rank);
   const dim3 grid(static_cast<unsigned>(rows * chunks));
-  ProfScope ps(st, "subagg_gather", 0.0, bytes);
   const bool rows_part = (!done || done->row_rank) && (!next || next->row_rank);
+  ProfScope ps(st, vec && rows_part ? "subagg_gather_rows" : "subagg_gather", 0.0, bytes);
   if (vec && rows_part) {
     const int dn = done ? 1 : 0, nx = next ? 1 : 0;
     if (dn && nx)
