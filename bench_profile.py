@@ -54,7 +54,7 @@ def variant_symbol(variant):
                 else re.escape(f"spmm_kernel<{v}, {l}>")) + "$"
     table = {
         "gemm_bf16_packed": r"gemm_bf16_kernel<", "gemm_bf16_fixup": r"fixup_bf16_kernel",
-        "cvt_bf16_K": r"cvt_bf16_kernel<true>", "cvt_bf16_R": r"cvt_bf16_kernel<false>",
+        "cvt_bf16_K": r"cvt_bf16_kernel<true,", "cvt_bf16_R": r"cvt_bf16_kernel<false,",
         "gemm_streamk_fixup": r"streamk_fixup", "subagg_gather_rows": r"subagg_gather_rows_kernel<",
         "subagg_gather": r"subagg_gather_kernel<", "gather_slice": r"gather_kernel",
         "subagg_scatter": r"scatter_kernel", "sgd_update": r"sgd_kernel",

@@ -3,20 +3,23 @@
 // with fp32 accumulation.
 //
 // Why a separate path: the bf16 matrix cores run 16x faster than fp32 ones,
-// so a kernel that streams fp32 operands (4 bytes per element) into a
-// 128 x 128 tile and rounds them while staging cannot feed them -- it is
-// bound by L2 traffic and conversion instructions.  Here
+// so a kernel that streams fp32 operands (4 bytes per element) and rounds
+// them while staging cannot feed them.  Here
 //
 //   1. cvt_bf16_kernel rounds an operand (nearest-even, in hardware) into a
 //      bf16 buffer [Rp][Kp], K contiguous, zero-padded to the tile grid
 //      (row-contiguous operands are transposed through LDS on the way);
-//   2. gemm_bf16_kernel multiplies the padded copies: 128 x 256 tiles (twice
-//      the arithmetic per byte of a 128 x 128 tile), K steps of 64, four
-//      waves each owning 128 rows x 64 columns (4 x 2 MFMA tiles of 32 x 32,
-//      v_mfma_f32_32x32x16_bf16), double-buffered LDS, no bounds checks in
-//      the loads thanks to the padding;
-//   3. stream-K over one workgroup per CU with the same deterministic
-//      partial-tile fix-up as the fp32 path.
+//   2. gemm_bf16_kernel multiplies the padded copies in 256 x 256 tiles with
+//      eight waves (two per SIMD, so one wave's MFMAs run while the other
+//      waits on memory), each owning 128 rows x 64 columns (4 x 2 MFMA tiles
+//      of 32 x 32, v_mfma_f32_32x32x16_bf16), K steps of 32, double-buffered
+//      LDS with 80-byte rows (conflict-free 16-byte fragment reads), no
+//      bounds checks in the loads thanks to the padding;
+//   3. work units are (K slice, tile) pairs, K-slice-major, so the units an
+//      XCD runs together cover neighbouring tiles over the same K range at
+//      the same time and share their operands in L2.  Shapes with too few
+//      tiles to fill the GPU split K into up to kMaxSplit slices whose fp32
+//      partials a fix-up kernel sums in slice order (deterministic).
 //
 // The result equals the in-kernel-rounding path's: both round the same fp32
 // values to bf16 with round-to-nearest-even and accumulate in fp32.
@@ -37,10 +40,13 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned short ushort8 __attribute__((ext_vector_type(8)));
 
-constexpr int TM = 128, TN = 256, TK = 64;
-constexpr int LDH = TK + 8;          // LDS row stride in halves (144 B)
-constexpr int kThr = 256;
-constexpr int kStreamGroups = 256;   // one 256-thread workgroup per CU
+constexpr int TM = 256, TN = 256, TK = 32;
+constexpr int LDH = TK + 8;          // LDS row stride in halves (80 B)
+constexpr int kThr = 512;            // 8 waves: 2 along M x 4 along N
+constexpr int kCUs = 256;            // MI355X compute units (one workgroup each)
+constexpr int kMaxSplit = 8;
+constexpr int kPad = 256;            // row padding of the bf16 copies (tile edge)
+constexpr int kPadK = 64;            // K padding (conversion tile)
 
 __device__ __forceinline__ unsigned short bf16_bits(float f) {
   return __builtin_bit_cast(unsigned short, static_cast<__bf16>(f));
@@ -49,34 +55,59 @@ __device__ __forceinline__ unsigned short bf16_bits(float f) {
 // ---- 1. conversion ---------------------------------------------------------
 
 // dst[r][k] = bf16(src(r, k)) for r < Rp, k < Kp; zero outside R x K.
-// One 64 x 64 tile per block, through LDS so both source orientations read
-// and write coalesced.
-template <bool KMAJ>
+// One 64 x 64 tile per block.  K-contiguous sources go straight from
+// registers to the packed rows; row-contiguous ones are transposed through
+// LDS.  VEC: 16-byte source loads (strides, bases and the concatenation
+// split are multiples of 4 floats, and the contiguous extent is too, so a
+// group of four is wholly inside or outside the matrix).
+template <bool KMAJ, bool VEC>
 __global__ __launch_bounds__(256) void cvt_bf16_kernel(OpView src, int64_t R, int64_t K,
                                                        unsigned short* __restrict__ dst,
                                                        int64_t Kp, int64_t tiles_k) {
-  __shared__ float tile[64][65];
   const int64_t tr = blockIdx.x / tiles_k, tk = blockIdx.x % tiles_k;
   const int64_t r0 = tr * 64, k0 = tk * 64;
   const int t = threadIdx.x;
-  // load: 64 x 64 floats, 16 per thread
+  const int rr = t >> 2, kk = (t & 3) * 16;   // output: row rr, K kk .. kk+15
+  float v[16];
+  if constexpr (KMAJ) {
+    const int64_t r = r0 + rr;
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int e = t + 256 * i;
-    int rr, kk;
-    if constexpr (KMAJ) { rr = e >> 6; kk = e & 63; }   // consecutive threads along K
-    else { kk = e >> 6; rr = e & 63; }                  // consecutive threads along R
-    const int64_t r = r0 + rr, k = k0 + kk;
-    tile[rr][kk] = (r < R && k < K) ? src.at<KMAJ>(r, k) : 0.f;
+    for (int g = 0; g < 4; ++g) {
+      const int64_t k = k0 + kk + 4 * g;
+      if constexpr (VEC) {
+        float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (r < R && k < K) x = src.at4<true>(r, k);
+        v[4 * g] = x.x; v[4 * g + 1] = x.y; v[4 * g + 2] = x.z; v[4 * g + 3] = x.w;
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[4 * g + q] = (r < R && k + q < K) ? src.at<true>(r, k + q) : 0.f;
+      }
+    }
+  } else {
+    __shared__ float tile[64][65];   // [r][k]
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e = t + 256 * i;
+      const int lk = e >> 4, lr = (e & 15) * 4;   // consecutive threads along R
+      const int64_t k = k0 + lk, r = r0 + lr;
+      if constexpr (VEC) {
+        float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (k < K && r < R) x = src.at4<false>(r, k);
+        tile[lr][lk] = x.x; tile[lr + 1][lk] = x.y; tile[lr + 2][lk] = x.z; tile[lr + 3][lk] = x.w;
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) tile[lr + q][lk] = (k < K && r + q < R) ? src.at<false>(r + q, k) : 0.f;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < 16; ++q) v[q] = tile[rr][kk + q];
   }
-  __syncthreads();
-  // store: 8 halves (16 B) per thread, K contiguous
-  const int rr = t >> 2, kk = (t & 3) * 16;
   ushort8 lo, hi;
 #pragma unroll
   for (int q = 0; q < 8; ++q) {
-    lo[q] = bf16_bits(tile[rr][kk + q]);
-    hi[q] = bf16_bits(tile[rr][kk + 8 + q]);
+    lo[q] = bf16_bits(v[q]);
+    hi[q] = bf16_bits(v[8 + q]);
   }
   unsigned short* d = dst + (r0 + rr) * Kp + k0 + kk;
   *reinterpret_cast<ushort8*>(d) = lo;
@@ -86,8 +117,11 @@ __global__ __launch_bounds__(256) void cvt_bf16_kernel(OpView src, int64_t R, in
 // ---- 2. the product ----------------------------------------------------------
 
 struct SchedB {
-  int64_t T, ipw;
-  int nk, tiles_m, tiles_n;
+  int64_t tiles;          // tiles_m * tiles_n
+  int tiles_m, tiles_n;
+  int nk;                 // K steps of the whole product
+  int split;              // K slices
+  int spu;                // K steps per slice
 };
 
 template <bool SPLIT_OUT>
@@ -100,139 +134,144 @@ __global__ __launch_bounds__(kThr) void gemm_bf16_kernel(int64_t M, int64_t N,
   const int t = threadIdx.x;
   const int lane = t & 63, wave = t >> 6;
   const int li = lane & 31, lh = lane >> 5;
+  const int wm = wave >> 2, wn = wave & 3;   // this wave's 128 x 64 block of the tile
+
+  const int64_t u = xcd_remap(blockIdx.x, gridDim.x);
+  const int ks = static_cast<int>(u / S.tiles);
+  const int64_t tile = u - static_cast<int64_t>(ks) * S.tiles;
+  int tm, tn;
+  tile_coords_banded(tile, S.tiles_m, S.tiles_n, tm, tn);
+  const int64_t m0 = static_cast<int64_t>(tm) * TM, n0 = static_cast<int64_t>(tn) * TN;
+  const int kb = ks * S.spu;
+  const int ke = min(S.nk, kb + S.spu);
 
   floatx16 acc[4][2];
-  ushort8 ra[4], rb[8];
-  int64_t m0 = 0, n0 = 0;
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
-  // loads: 8 threads cover one row's 64 halves (128 B); 32 rows per pass
-  const int lrow = t >> 3, lchunk = (t & 7) * 8;
-  auto load = [&](int64_t k) {
+  // loads: 4 threads cover one row's 32 halves (64 B); 128 rows per pass,
+  // two passes for A and two for B
+  ushort8 ra[2], rb[2];
+  const int lrow = t >> 2, lchunk = (t & 3) * 8;
+  auto gload = [&](int64_t k) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      ra[i] = *reinterpret_cast<const ushort8*>(A + (m0 + lrow + 32 * i) * Kp + k + lchunk);
+    for (int i = 0; i < 2; ++i)
+      ra[i] = *reinterpret_cast<const ushort8*>(A + (m0 + lrow + 128 * i) * Kp + k + lchunk);
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      rb[i] = *reinterpret_cast<const ushort8*>(B + (n0 + lrow + 32 * i) * Kp + k + lchunk);
+    for (int i = 0; i < 2; ++i)
+      rb[i] = *reinterpret_cast<const ushort8*>(B + (n0 + lrow + 128 * i) * Kp + k + lchunk);
   };
-  auto stage = [&](int buf) {
+  auto swrite = [&](int buf) {
     unsigned short* As = lds[buf];
     unsigned short* Bs = As + TM * LDH;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      *reinterpret_cast<ushort8*>(As + (lrow + 32 * i) * LDH + lchunk) = ra[i];
+    for (int i = 0; i < 2; ++i)
+      *reinterpret_cast<ushort8*>(As + (lrow + 128 * i) * LDH + lchunk) = ra[i];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      *reinterpret_cast<ushort8*>(Bs + (lrow + 32 * i) * LDH + lchunk) = rb[i];
+    for (int i = 0; i < 2; ++i)
+      *reinterpret_cast<ushort8*>(Bs + (lrow + 128 * i) * LDH + lchunk) = rb[i];
   };
-  auto compute = [&](int buf) {
+  // MFMA fragments of one 16-wide K chunk: A rows wm*128 + a*32 + lane%32,
+  // B rows wn*64 + b*32 + lane%32; lane half lh holds K elements 8*lh .. +7.
+  struct Frag { bf16x8 a[4], b[2]; };
+  auto rfrag = [&](int buf, int c, Frag& f) {
     const unsigned short* As = lds[buf];
     const unsigned short* Bs = As + TM * LDH;
 #pragma unroll
-    for (int c = 0; c < TK / 16; ++c) {
-      bf16x8 av[4], bv[2];
+    for (int a = 0; a < 4; ++a)
+      f.a[a] = *reinterpret_cast<const bf16x8*>(As + (wm * 128 + a * 32 + li) * LDH + 16 * c +
+                                                8 * lh);
 #pragma unroll
-      for (int a = 0; a < 4; ++a)
-        av[a] = *reinterpret_cast<const bf16x8*>(As + (a * 32 + li) * LDH + 16 * c + 8 * lh);
+    for (int b = 0; b < 2; ++b)
+      f.b[b] = *reinterpret_cast<const bf16x8*>(Bs + (wn * 64 + b * 32 + li) * LDH + 16 * c +
+                                                8 * lh);
+  };
+  auto mfma8 = [&](const Frag& f) {
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
 #pragma unroll
       for (int b = 0; b < 2; ++b)
-        bv[b] = *reinterpret_cast<const bf16x8*>(Bs + (wave * 64 + b * 32 + li) * LDH + 16 * c +
-                                                 8 * lh);
-#pragma unroll
-      for (int a = 0; a < 4; ++a)
-#pragma unroll
-        for (int b = 0; b < 2; ++b)
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[a], bv[b], acc[a][b], 0, 0, 0);
-    }
+        acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[a], f.b[b], acc[a][b], 0, 0, 0);
   };
 
-  const int64_t w = xcd_remap(blockIdx.x, gridDim.x);
-  int64_t it = w * S.ipw;
-  const int64_t it_end = min(S.T, it + S.ipw);
-  const int64_t first_tile = it / S.nk;
-  while (it < it_end) {
-    const int64_t tile = it / S.nk;
-    const int kb = static_cast<int>(it % S.nk);
-    const int ke = static_cast<int>(min<int64_t>(S.nk, kb + (it_end - it)));
-    int tm, tn;
-    tile_coords_banded(tile, S.tiles_m, S.tiles_n, tm, tn);
-    m0 = static_cast<int64_t>(tm) * TM;
-    n0 = static_cast<int64_t>(tn) * TN;
+  // Pipeline: step j multiplies LDS buffer (j-kb)&1.  After its first chunk
+  // the staging registers (step j+1, loaded during step j-1) go to the other
+  // buffer -- last read in step j-1, before the barrier that ended it -- and
+  // after the second chunk the loads of step j+2 are issued.
+  gload(static_cast<int64_t>(kb) * TK);
+  swrite(0);
+  if (kb + 1 < ke) gload(static_cast<int64_t>(kb + 1) * TK);
+  __syncthreads();
+  for (int j = kb; j < ke; ++j) {
+    const int buf = (j - kb) & 1;
+    Frag f0, f1;
+    rfrag(buf, 0, f0);
+    rfrag(buf, 1, f1);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma8(f0);
+    __builtin_amdgcn_sched_barrier(0);
+    if (j + 1 < ke) swrite(buf ^ 1);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma8(f1);
+    __builtin_amdgcn_sched_barrier(0);
+    if (j + 2 < ke) gload(static_cast<int64_t>(j + 2) * TK);
+    __syncthreads();
+  }
+
+  // acc[a][b] register r of lane l: tile row wm*128 + a*32 + 8(r/4) +
+  // 4(l/32) + r%4, tile column wn*64 + b*32 + l%32
+  if (S.split == 1) {
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const int64_t col = n0 + wn * 64 + b * 32 + li;
+        if (col >= N) continue;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int64_t row = m0 + wm * 128 + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+          if (row < M) C.store<SPLIT_OUT>(row, col, acc[a][b][r]);
+        }
+      }
+  } else {
+    float* part = partials + u * static_cast<int64_t>(TM * TN);   // slot (ks, tile)
 #pragma unroll
     for (int a = 0; a < 4; ++a)
 #pragma unroll
       for (int b = 0; b < 2; ++b)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
-    __syncthreads();
-    load(static_cast<int64_t>(kb) * TK);
-    stage(0);
-    __syncthreads();
-    for (int j = kb; j + 1 < ke; ++j) {
-      load(static_cast<int64_t>(j + 1) * TK);
-      __builtin_amdgcn_sched_barrier(0);
-      compute((j - kb) & 1);
-      __builtin_amdgcn_sched_barrier(0);
-      stage((j + 1 - kb) & 1);
-      __syncthreads();
-    }
-    compute((ke - 1 - kb) & 1);
-
-    // acc[a][b] register r of lane l: row a*32 + 8(r/4) + 4(l/32) + r%4,
-    // column wave*64 + b*32 + l%32 of the tile
-    if (kb == 0 && ke == S.nk) {
-#pragma unroll
-      for (int a = 0; a < 4; ++a)
-#pragma unroll
-        for (int b = 0; b < 2; ++b) {
-          const int64_t col = n0 + wave * 64 + b * 32 + li;
-          if (col >= N) continue;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int64_t row = m0 + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
-            if (row < M) C.store<SPLIT_OUT>(row, col, acc[a][b][r]);
-          }
-        }
-    } else {
-      float* part = partials + (w * 2 + (tile == first_tile ? 0 : 1)) * (TM * TN);
-#pragma unroll
-      for (int a = 0; a < 4; ++a)
-#pragma unroll
-        for (int b = 0; b < 2; ++b)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            part[(a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3)) * TN + wave * 64 + b * 32 + li] =
-                acc[a][b][r];
-    }
-    it += ke - kb;
+        for (int r = 0; r < 16; ++r)
+          part[(wm * 128 + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3)) * TN + wn * 64 + b * 32 +
+               li] = acc[a][b][r];
   }
 }
 
-// Sum split tiles' partials in workgroup order (one block per tile).
+// Sum the K slices' partials of one tile in slice order.  One block per
+// kFixRows rows of a tile (a tile alone would leave most CUs idle).
+constexpr int kFixRows = 16;
+
 __global__ __launch_bounds__(256) void fixup_bf16_kernel(int64_t M, int64_t N, SchedB S,
                                                          const float* __restrict__ partials,
                                                          OutView C) {
-  constexpr int kMaxParts = 512;
-  __shared__ int64_t slot_off[kMaxParts];
-  const int64_t t = blockIdx.x;
-  const int64_t w_first = (t * S.nk) / S.ipw;
-  const int64_t w_last = ((t + 1) * S.nk - 1) / S.ipw;
-  if (w_first == w_last) return;
-  const int parts = static_cast<int>(w_last - w_first + 1);
-  for (int j = threadIdx.x; j < parts; j += 256) {
-    const int64_t w = w_first + j;
-    slot_off[j] = (w * 2 + (((w * S.ipw) / S.nk) == t ? 0 : 1)) * (TM * TN);
-  }
-  __syncthreads();
+  constexpr int kChunks = TM / kFixRows;
+  const int64_t tile = blockIdx.x / kChunks;
+  const int r0 = static_cast<int>(blockIdx.x % kChunks) * kFixRows;
   int tm, tn;
-  tile_coords_banded(t, S.tiles_m, S.tiles_n, tm, tn);
+  tile_coords_banded(tile, S.tiles_m, S.tiles_n, tm, tn);
   const int64_t m0 = static_cast<int64_t>(tm) * TM, n0 = static_cast<int64_t>(tn) * TN;
-  for (int e4 = threadIdx.x; e4 < TM * TN / 4; e4 += 256) {
-    const int e = e4 * 4;
+  const int64_t slot = static_cast<int64_t>(TM * TN);
+#pragma unroll
+  for (int i = 0; i < kFixRows * TN / 4 / 256; ++i) {
+    const int e = r0 * TN + (threadIdx.x + 256 * i) * 4;
     const int64_t row = m0 + e / TN, col = n0 + e % TN;
     if (row >= M || col >= N) continue;
-    floatx4 s = {0.f, 0.f, 0.f, 0.f};
-    for (int j = 0; j < parts; ++j) s += *reinterpret_cast<const floatx4*>(partials + slot_off[j] + e);
+    floatx4 s = *reinterpret_cast<const floatx4*>(partials + tile * slot + e);
+    for (int k = 1; k < S.split; ++k)
+      s += *reinterpret_cast<const floatx4*>(partials + (k * S.tiles + tile) * slot + e);
 #pragma unroll
     for (int q = 0; q < 4; ++q)
       if (col + q < N) C.store<true>(row, col + q, s[q]);
@@ -243,29 +282,44 @@ struct Layout {
   int64_t Mp, Np, Kp;
   size_t a_bytes, b_bytes, part_bytes;
   SchedB S;
-  bool split;
   size_t total() const { return a_bytes + b_bytes + part_bytes; }
 };
 
 size_t up256(size_t x) { return (x + 255) & ~size_t(255); }
 
+// K slices for a product of `tiles` tiles and nk K steps: the fewest rounds
+// of kCUs workgroups times the steps per slice, plus the fix-up's traffic
+// (split + 1 partial tiles per output tile at ~4 TB/s) priced in K steps of
+// one workgroup (~0.8 us each at the measured rate).
+int choose_split(int64_t tiles, int nk) {
+  int best = 1;
+  double best_cost = 0.0;
+  for (int s = 1; s <= kMaxSplit; ++s) {
+    const int spu = (nk + s - 1) / s;
+    if (s > 1 && (spu < 8 || (s - 1) * spu >= nk)) break;
+    const double rounds = static_cast<double>((tiles * s + kCUs - 1) / kCUs);
+    double cost = rounds * spu;
+    if (s > 1) cost += static_cast<double>(tiles) * (s + 1) * TM * TN * 4.0 / 4e12 / 0.8e-6;
+    if (s == 1 || cost < best_cost) { best = s; best_cost = cost; }
+  }
+  return best;
+}
+
 Layout make_layout(int64_t M, int64_t N, int64_t K) {
   Layout L;
-  L.Mp = (M + TM - 1) / TM * TM;
-  L.Np = (N + TN - 1) / TN * TN;
-  L.Kp = (K + TK - 1) / TK * TK;
+  L.Mp = (M + kPad - 1) / kPad * kPad;
+  L.Np = (N + kPad - 1) / kPad * kPad;
+  L.Kp = (K + kPadK - 1) / kPadK * kPadK;
   L.a_bytes = up256(static_cast<size_t>(L.Mp) * L.Kp * 2);
   L.b_bytes = up256(static_cast<size_t>(L.Np) * L.Kp * 2);
   SchedB& s = L.S;
   s.tiles_m = static_cast<int>(L.Mp / TM);
   s.tiles_n = static_cast<int>(L.Np / TN);
+  s.tiles = static_cast<int64_t>(s.tiles_m) * s.tiles_n;
   s.nk = static_cast<int>(L.Kp / TK);
-  const int64_t tiles = static_cast<int64_t>(s.tiles_m) * s.tiles_n;
-  s.T = tiles * s.nk;
-  s.ipw = tiles >= 4 * kStreamGroups ? s.nk : (s.T + kStreamGroups - 1) / kStreamGroups;
-  L.split = s.ipw % s.nk != 0;
-  const int64_t groups = (s.T + s.ipw - 1) / s.ipw;
-  L.part_bytes = L.split ? static_cast<size_t>(groups) * 2 * TM * TN * sizeof(float) : 0;
+  s.split = choose_split(s.tiles, s.nk);
+  s.spu = (s.nk + s.split - 1) / s.split;
+  L.part_bytes = s.split > 1 ? static_cast<size_t>(s.split) * s.tiles * TM * TN * sizeof(float) : 0;
   return L;
 }
 
@@ -274,14 +328,21 @@ gist_status convert(hipStream_t st, const Operand& o, int64_t R, int64_t K, int6
   OpView v = OpView::from(o);
   const int64_t tiles_k = Kp / 64;
   const int64_t blocks = (Rp / 64) * tiles_k;
+  const bool vec = o.ld0 % 4 == 0 && aligned16(o.p0) &&
+                   (!o.p1 || (o.ld1 % 4 == 0 && aligned16(o.p1) && o.split % 4 == 0)) &&
+                   (o.k_major ? K % 4 == 0 : R % 4 == 0);
   ProfScope ps(st, o.k_major ? "cvt_bf16_K" : "cvt_bf16_R", 0.0,
                4.0 * static_cast<double>(R) * K + 2.0 * static_cast<double>(Rp) * Kp);
-  if (o.k_major)
-    hipLaunchKernelGGL(cvt_bf16_kernel<true>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st,
-                       v, R, K, dst, Kp, tiles_k);
+  const dim3 g(static_cast<unsigned>(blocks));
+  if (o.k_major && vec)
+    hipLaunchKernelGGL((cvt_bf16_kernel<true, true>), g, dim3(256), 0, st, v, R, K, dst, Kp, tiles_k);
+  else if (o.k_major)
+    hipLaunchKernelGGL((cvt_bf16_kernel<true, false>), g, dim3(256), 0, st, v, R, K, dst, Kp, tiles_k);
+  else if (vec)
+    hipLaunchKernelGGL((cvt_bf16_kernel<false, true>), g, dim3(256), 0, st, v, R, K, dst, Kp, tiles_k);
   else
-    hipLaunchKernelGGL(cvt_bf16_kernel<false>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
-                       st, v, R, K, dst, Kp, tiles_k);
+    hipLaunchKernelGGL((cvt_bf16_kernel<false, false>), g, dim3(256), 0, st, v, R, K, dst, Kp,
+                       tiles_k);
   return check_launch("bf16 conversion");
 }
 
@@ -300,8 +361,8 @@ gist_status gemm_bf16_packed(hipStream_t st, int64_t M, int64_t N, int64_t K, co
                              const Operand& B, const GemmOut& Cout, void* ws, size_t ws_bytes) {
   const Layout L = make_layout(M, N, K);
   if (!ws || ws_bytes < L.total()) return set_error(GIST_E_NOMEM, "gemm bf16: workspace too small");
-  const int64_t groups = (L.S.T + L.S.ipw - 1) / L.S.ipw;
-  if (groups > INT32_MAX || L.Mp % 64 || L.Np % 64)
+  const int64_t units = L.S.tiles * L.S.split;
+  if (units > INT32_MAX || L.S.tiles * (TM / kFixRows) > INT32_MAX || L.Kp / TK > INT32_MAX)
     return set_error(GIST_E_UNSUPPORTED, "gemm bf16: grid too large");
   char* base = static_cast<char*>(ws);
   auto* a16 = reinterpret_cast<unsigned short*>(base);
@@ -318,19 +379,20 @@ gist_status gemm_bf16_packed(hipStream_t st, int64_t M, int64_t N, int64_t K, co
                  2.0 * (static_cast<double>(M) * K + static_cast<double>(N) * K) +
                      4.0 * static_cast<double>(M) * N);
     if (split_out)
-      hipLaunchKernelGGL(gemm_bf16_kernel<true>, dim3(static_cast<unsigned>(groups)), dim3(kThr), 0,
+      hipLaunchKernelGGL(gemm_bf16_kernel<true>, dim3(static_cast<unsigned>(units)), dim3(kThr), 0,
                          st, M, N, a16, b16, L.Kp, c, L.S, part);
     else
-      hipLaunchKernelGGL(gemm_bf16_kernel<false>, dim3(static_cast<unsigned>(groups)), dim3(kThr),
+      hipLaunchKernelGGL(gemm_bf16_kernel<false>, dim3(static_cast<unsigned>(units)), dim3(kThr),
                          0, st, M, N, a16, b16, L.Kp, c, L.S, part);
   }
   s = check_launch("gemm bf16");
   if (s != GIST_OK) return s;
-  if (L.split) {
-    const int64_t tiles = static_cast<int64_t>(L.S.tiles_m) * L.S.tiles_n;
-    ProfScope ps(st, "gemm_bf16_fixup", 0.0, 0.0);
-    hipLaunchKernelGGL(fixup_bf16_kernel, dim3(static_cast<unsigned>(tiles)), dim3(256), 0, st, M, N,
-                       L.S, part, c);
+  if (L.S.split > 1) {
+    ProfScope ps(st, "gemm_bf16_fixup", 0.0,
+                 4.0 * static_cast<double>(L.S.split) * L.S.tiles * TM * TN +
+                     4.0 * static_cast<double>(M) * N);
+    hipLaunchKernelGGL(fixup_bf16_kernel, dim3(static_cast<unsigned>(L.S.tiles * (TM / kFixRows))),
+                       dim3(256), 0, st, M, N, L.S, part, c);
     return check_launch("gemm bf16 fix-up");
   }
   return GIST_OK;

@@ -26,6 +26,16 @@ struct OpView {
     if constexpr (KMAJ) return k < split ? p0[r * ld0 + k] : p1[r * ld1 + (k - split)];
     else return r < split ? p0[k * ld0 + r] : p1[k * ld1 + (r - split)];
   }
+  // Four consecutive elements along the contiguous dimension, starting at
+  // (r, k); the caller guarantees 16-byte alignment and that the four do
+  // not straddle `split`.
+  template <bool KMAJ>
+  __device__ __forceinline__ float4 at4(int64_t r, int64_t k) const {
+    const float* p;
+    if constexpr (KMAJ) p = k < split ? p0 + r * ld0 + k : p1 + r * ld1 + (k - split);
+    else p = r < split ? p0 + k * ld0 + r : p1 + k * ld1 + (r - split);
+    return *reinterpret_cast<const float4*>(p);
+  }
 };
 
 // Device view of a GemmOut: optional ReLU, columns >= c_split go to c1.
