@@ -19,7 +19,9 @@ What it computes, each function citing the passage it follows (paper:
   eq. (2)), the GraphSAGE-mean layer, softmax cross-entropy, SGD
   (Section 3.2), slice gather (Section 3.1) and ``subAgg`` (Section 3.2).
 * :mod:`oracle.gist` -- one sub-GCN training step and one GIST round
-  (Algorithm 1) composed from the above.
+  (Algorithm 1) composed from the above, and the whole loop of Algorithm 1
+  trained with Adam (the optimizer of the paper's experiments).
+* :mod:`oracle.optim` -- Adam (Kingma & Ba 2015, their Algorithm 1).
 
 Floating point is fp64 throughout; fp32 inputs are widened exactly.  The
 matrices of the normalised adjacency are the one place where fp32 is part
@@ -29,7 +31,8 @@ of the definition: the values are computed in fp64 and rounded once to fp32
 Every function here is pinned by ``tests/test_oracle_*.py`` against facts
 the paper and the mathematics fix (published generator outputs, mask
 properties, spectra, closed-form gradients, finite differences, the
-two-layer sum decomposition); none is "parity unpinned".
+two-layer sum decomposition, an independent Adam implementation); none is
+"parity unpinned".
 """
 
-from . import partition, minibatch, layers, gist  # noqa: F401
+from . import partition, minibatch, layers, gist, optim  # noqa: F401
