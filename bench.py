@@ -15,7 +15,10 @@ One timed step is one pass of the whole hot path:
   The last round's subAgg is applied after the timed region.
 
 Inputs are seeded synthetic data resident in HBM before timing starts.
-The reported value is ms per sub-GCN step = round time / m.  Kernel times
+The reported value is ms per sub-GCN step = round time / (m zeta), with zeta
+local steps per sub-GCN per round (default 1; ``--optimizer adam`` trains
+with Adam as the paper's experiments do, its moments carried with the
+weights through subAgg or reset each round).  Kernel times
 come from HIP events the library records on the launch stream during the
 timed rounds (gist_profile_*).  The CPU baseline is the fp64 oracle timed on
 one sub-GCN step of the same workload.
@@ -89,6 +92,11 @@ def parse():
     ap.add_argument("--dtype", default="f32", choices=["f32", "bf16"])
     ap.add_argument("--d-in", type=int, default=256, help="c5 input slice width")
     ap.add_argument("--lr", type=float, default=0.01)
+    ap.add_argument("--optimizer", default="sgd", choices=["sgd", "adam"],
+                    help="sub-GCN update (c1-c4): SGD, or Adam as in the paper's experiments")
+    ap.add_argument("--adam-policy", default="carry", choices=["carry", "reset"],
+                    help="Adam moments at subAgg: carried with the weights, or reset per round")
+    ap.add_argument("--zeta", type=int, default=1, help="local steps per sub-GCN per round")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the library's per-launch event timing")
@@ -101,7 +109,7 @@ def parse():
 class RoundWorkload:
     """A GIST round (partition, gather, m sub-GCN steps, subAgg) on one GPU."""
 
-    def __init__(self, cfg, ctx, dtype):
+    def __init__(self, cfg, ctx, dtype, optimizer="sgd", policy="carry", zeta=1):
         import torch
         from paper_2102_10424_amd import gist as G
         from paper_2102_10424_amd.step import BatchSlot, GistModel, SubGCN
@@ -120,7 +128,9 @@ class RoundWorkload:
                 parts.append(torch.from_numpy(cfg.theta(l, p)).cuda())
             theta.append(parts)
         log(f"[bench] global theta on device ({time.time() - t0:.1f}s)")
-        self.model = GistModel(ctx, cfg.kind, cfg.widths, cfg.m, theta)
+        self.adam = policy if optimizer == "adam" else None
+        self.zeta = zeta
+        self.model = GistModel(ctx, cfg.kind, cfg.widths, cfg.m, theta, adam=self.adam)
         self.norm = "sage" if cfg.kind == "sage" else "gcn"
         # capacities: the largest mini-batch of the clusters, generous nnz bound
         if cfg.batch_clusters is None:
@@ -140,17 +150,23 @@ class RoundWorkload:
 
     def step(self):
         cfg, m = self.cfg, self.model
-        t = self.t
+        t, zeta = self.t, self.zeta
         m.set_partitions({l: cfg.partition_seed(t, l) for l in range(1, cfg.L)})
         m.begin_round()   # subAgg of round t-1 fused with the gather of round t
         for i in range(cfg.m):
-            if cfg.batch_clusters is None:
-                if self.full is None:
-                    self.full = self.slots[0].load(self.gh, None, self.X, self.labels)
-                b = self.full
-            else:
-                b = self.slots[i].load(self.gh, cfg.minibatch(t, i), self.X, self.labels)
-            self.runner.step(b, m.params[i], self.lr)
+            for z in range(zeta):
+                if cfg.batch_clusters is None:
+                    if self.full is None:
+                        self.full = self.slots[0].load(self.gh, None, self.X, self.labels)
+                    b = self.full
+                else:
+                    b = self.slots[i].load(self.gh, cfg.minibatch(t, i, z), self.X, self.labels)
+                opt = None
+                if self.adam == "carry":
+                    opt = (m.M[i], m.V[i], t * zeta + z + 1, False)
+                elif self.adam == "reset":
+                    opt = (m.M[i], m.V[i], z + 1, z == 0)
+                self.runner.step(b, m.params[i], self.lr, adam=opt)
         m.end_round()
         self.t += 1
 
@@ -158,7 +174,7 @@ class RoundWorkload:
         self.model.finalize()
 
     def steps_per_unit(self):
-        return self.cfg.m
+        return self.cfg.m * self.zeta
 
     def describe(self):
         c = self.cfg
@@ -167,7 +183,8 @@ class RoundWorkload:
                             f"{c.widths[1]} split m={c.m}, N={c.n_nodes}, "
                             f"{'mini-batch ' + str(c.batch_clusters) + ' clusters' if c.batch_clusters else 'full graph'}",
                 "model": "GIST sub-GCN", "m": c.m, "widths": c.widths,
-                "global_batch": c.batch_clusters or c.n_nodes}
+                "global_batch": c.batch_clusters or c.n_nodes, "zeta": self.zeta,
+                "optimizer": f"adam ({self.adam} moments)" if self.adam else "sgd"}
 
     # ---- CPU baseline: the fp64 oracle on one sub-GCN step ---------------------
     def cpu_baseline(self):
@@ -312,7 +329,7 @@ def main():
     if args.config == "c5":
         wl = LayerWorkload(cfg, ctx, args.dtype, args.d_in)
     else:
-        wl = RoundWorkload(cfg, ctx, args.dtype)
+        wl = RoundWorkload(cfg, ctx, args.dtype, args.optimizer, args.adam_policy, args.zeta)
         wl.lr = args.lr
     for w in range(args.warmup):
         wl.step()
@@ -387,7 +404,7 @@ def main():
         "data": "synthetic (seeded SBM / Chung-Lu / ER graphs, N(0,1) features, Glorot weights)",
         "config": dict(wl.describe(), parallelism="single GPU, m sub-GCNs back to back",
                        step="one GIST round" if per_unit > 1 else "one layer fwd+bwd",
-                       value="ms per sub-GCN step (round time / m)" if per_unit > 1
+                       value="ms per sub-GCN step (round time / (m zeta))" if per_unit > 1
                        else "ms per layer fwd+bwd"),
         "roofline": roofline, "cpu_baseline": cpu, "kernels": kernels,
         "profile_dropped": dropped, "kernel_src_sha256": kernel_source_hash(),

@@ -14,6 +14,7 @@
  *   gist_gcn_layer_fwd/_bwd    eq. (2) sub-GCN layer, GCN and SAGE-mean (device)
  *   gist_softmax_xent          loss and its gradient                    (device)
  *   gist_sgd_update            one SGD step                             (device)
+ *   gist_adam_update           one Adam step (the experiments' optimizer) (device)
  *   gist_subagg                subAgg: Theta[D_in, D_out] <- Theta^(i)  (device)
  *   gist_subagg_gather         subAgg of one round + gather of the next (device)
  *
@@ -260,6 +261,23 @@ gist_status gist_gather_slice(gist_ctx* ctx, const float* Wg, int64_t ldg,
 /* W[k] -= lr * dW[k] for k < n, in fp32 (one rounding per element). */
 gist_status gist_sgd_update(gist_ctx* ctx, float* W, const float* dW, int64_t n,
                             float lr);
+
+/* One Adam step on n parameters -- the optimizer the paper's experiments
+ * train with (no weight decay), as defined by Kingma & Ba (ICLR 2015,
+ * Algorithm 1), step k >= 1 counting from 1:
+ *   m <- beta1 m + (1 - beta1) g,   v <- beta2 v + (1 - beta2) g^2,
+ *   W <- W - lr (m / (1 - beta1^k)) / (sqrt(v / (1 - beta2^k)) + eps).
+ * W, m, v are updated in place, g = dW is read; all device fp32 arrays of n
+ * elements.  The bias corrections are formed in double on the host and
+ * applied in fp32.  GIST_ADAM_FRESH treats the incoming m and v as zero (a
+ * sub-GCN whose moments restart, e.g. at the start of a round), so they
+ * need no clearing pass.  Errors: GIST_E_INVAL for n < 0, NULL pointers
+ * with n > 0, k < 1, beta outside [0, 1), eps < 0, a non-finite lr or
+ * unknown flags. */
+enum { GIST_ADAM_FRESH = 1 };
+gist_status gist_adam_update(gist_ctx* ctx, float* W, const float* dW, float* m, float* v,
+                             int64_t n, float lr, float beta1, float beta2, float eps,
+                             int64_t step, uint32_t flags);
 
 /* ---- subAgg (Section 3.2) ------------------------------------------- */
 

@@ -8,6 +8,7 @@
 
 #include <algorithm>
 #include <climits>
+#include <cmath>
 #include <cstdio>
 #include <cstring>
 #include <map>
@@ -427,6 +428,32 @@ extern "C" gist_status gist_sgd_update(gist_ctx* ctx, float* W, const float* dW,
   if (!W || !dW) return set_error(GIST_E_INVAL, "sgd_update: NULL pointer");
   gist::DeviceGuard dg(ctx->device);
   return gist::sgd(ctx->stream, W, dW, n, lr);
+}
+
+extern "C" gist_status gist_adam_update(gist_ctx* ctx, float* W, const float* dW, float* m,
+                                        float* v, int64_t n, float lr, float beta1, float beta2,
+                                        float eps, int64_t step, uint32_t flags) {
+  gist::clear_error();
+  if (!ctx) return set_error(GIST_E_INVAL, "adam_update: NULL ctx");
+  gist::ProfBind pb(ctx);
+  if (n < 0) return set_error(GIST_E_INVAL, "adam_update: n < 0");
+  if (step < 1) return set_error(GIST_E_INVAL, "adam_update: step counts from 1");
+  if (!(beta1 >= 0.f && beta1 < 1.f) || !(beta2 >= 0.f && beta2 < 1.f))
+    return set_error(GIST_E_INVAL, "adam_update: beta outside [0, 1)");
+  if (!(eps >= 0.f) || !std::isfinite(lr) || !std::isfinite(eps))
+    return set_error(GIST_E_INVAL, "adam_update: bad lr or eps");
+  if (flags & ~static_cast<uint32_t>(GIST_ADAM_FRESH))
+    return set_error(GIST_E_INVAL, "adam_update: unknown flags");
+  if (n == 0) return GIST_OK;
+  if (!W || !dW || !m || !v) return set_error(GIST_E_INVAL, "adam_update: NULL pointer");
+  const double bc1 = 1.0 - std::pow(static_cast<double>(beta1), static_cast<double>(step));
+  const double bc2 = 1.0 - std::pow(static_cast<double>(beta2), static_cast<double>(step));
+  if (!(bc1 > 0.0) || !(bc2 > 0.0))
+    return set_error(GIST_E_INVAL, "adam_update: zero bias correction (beta = 0 needs no step)");
+  gist::DeviceGuard dg(ctx->device);
+  return gist::adam(ctx->stream, W, dW, m, v, n, static_cast<float>(lr / bc1),
+                    static_cast<float>(1.0 / std::sqrt(bc2)), beta1, beta2, eps,
+                    (flags & GIST_ADAM_FRESH) != 0);
 }
 
 extern "C" gist_status gist_subagg(gist_ctx* ctx, float* Wg, int64_t ldg,

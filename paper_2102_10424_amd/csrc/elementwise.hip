@@ -53,6 +53,52 @@ __global__ __launch_bounds__(kBlock) void sgd_kernel(int64_t n, float* __restric
     W[i] = fmaf(-lr, dW[i], W[i]);
 }
 
+// Adam: four elements per thread per pass (16-byte accesses when the four
+// arrays are aligned), the scalar tail by the first threads.  step_size =
+// lr / (1 - beta1^k) and inv_sqrt_bc2 = 1 / sqrt(1 - beta2^k) come from
+// the host, so  W -= step_size m / (sqrt(v) inv_sqrt_bc2 + eps).
+struct AdamCoef {
+  float step_size, inv_sqrt_bc2, beta1, beta2, eps;
+};
+
+__device__ __forceinline__ void adam_one(float& w, float g, float& m, float& v, const AdamCoef& c,
+                                         bool fresh) {
+  const float m0 = fresh ? 0.f : m, v0 = fresh ? 0.f : v;
+  m = c.beta1 * m0 + (1.f - c.beta1) * g;
+  v = c.beta2 * v0 + (1.f - c.beta2) * (g * g);
+  w = w - c.step_size * m / (sqrtf(v) * c.inv_sqrt_bc2 + c.eps);
+}
+
+template <bool VEC4>
+__global__ __launch_bounds__(kBlock) void adam_kernel(int64_t n, float* __restrict__ W,
+                                                      const float* __restrict__ dW,
+                                                      float* __restrict__ M, float* __restrict__ V,
+                                                      AdamCoef c, int fresh) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+  const int64_t t0 = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  if constexpr (VEC4) {
+    const int64_t n4 = n / 4;
+    for (int64_t i = t0; i < n4; i += stride) {
+      float4 w = reinterpret_cast<float4*>(W)[i], m = reinterpret_cast<float4*>(M)[i],
+             v = reinterpret_cast<float4*>(V)[i];
+      const float4 g = reinterpret_cast<const float4*>(dW)[i];
+      adam_one(w.x, g.x, m.x, v.x, c, fresh);
+      adam_one(w.y, g.y, m.y, v.y, c, fresh);
+      adam_one(w.z, g.z, m.z, v.z, c, fresh);
+      adam_one(w.w, g.w, m.w, v.w, c, fresh);
+      reinterpret_cast<float4*>(W)[i] = w;
+      reinterpret_cast<float4*>(M)[i] = m;
+      reinterpret_cast<float4*>(V)[i] = v;
+    }
+    if (t0 < n - 4 * n4) {
+      const int64_t i = 4 * n4 + t0;
+      adam_one(W[i], dW[i], M[i], V[i], c, fresh);
+    }
+  } else {
+    for (int64_t i = t0; i < n; i += stride) adam_one(W[i], dW[i], M[i], V[i], c, fresh);
+  }
+}
+
 // One block per output row; threads stride over the row's columns.  The
 // global row is read in ascending column order, so the lines of a row are
 // streamed once.
@@ -450,6 +496,21 @@ gist_status sgd(hipStream_t st, float* W, const float* dW, int64_t n, float lr) 
   hipLaunchKernelGGL(sgd_kernel, dim3(grid_for(n, kBlock, 8192)), dim3(kBlock), 0, st, n, W, dW,
                      lr);
   return check_launch("sgd_update");
+}
+
+gist_status adam(hipStream_t st, float* W, const float* dW, float* m, float* v, int64_t n,
+                 float step_size, float inv_sqrt_bc2, float beta1, float beta2, float eps,
+                 bool fresh) {
+  const AdamCoef c{step_size, inv_sqrt_bc2, beta1, beta2, eps};
+  const bool vec = aligned16(W) && aligned16(dW) && aligned16(m) && aligned16(v);
+  ProfScope ps(st, "adam_update", 0.0, (fresh ? 12.0 : 20.0) * static_cast<double>(n));
+  if (vec)
+    hipLaunchKernelGGL(adam_kernel<true>, dim3(grid_for((n + 3) / 4, kBlock, 8192)), dim3(kBlock), 0,
+                       st, n, W, dW, m, v, c, fresh ? 1 : 0);
+  else
+    hipLaunchKernelGGL(adam_kernel<false>, dim3(grid_for(n, kBlock, 8192)), dim3(kBlock), 0, st, n,
+                       W, dW, m, v, c, fresh ? 1 : 0);
+  return check_launch("adam_update");
 }
 
 gist_status gather(hipStream_t st, const float* Wg, int64_t ldg, const int32_t* rows,

@@ -115,6 +115,9 @@ gist_status fill_zero(hipStream_t st, float* p, int64_t count);
 gist_status subagg_gather(hipStream_t st, float* Wg, int64_t rows, int64_t cols, int64_t ldg,
                           int m, const gist_slice_set* done, const gist_slice_set* next, double bytes);
 gist_status sgd(hipStream_t st, float* W, const float* dW, int64_t n, float lr);
+gist_status adam(hipStream_t st, float* W, const float* dW, float* m, float* v, int64_t n,
+                 float step_size, float inv_sqrt_bc2, float beta1, float beta2, float eps,
+                 bool fresh);
 gist_status softmax_xent(hipStream_t st, int64_t n, int C, const float* logits,
                          const int32_t* labels, float* loss, float* dlogits,
                          float* partials);

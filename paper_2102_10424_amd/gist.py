@@ -46,6 +46,7 @@ GIST_ACT_NONE, GIST_ACT_RELU = 0, 1
 GIST_DTYPE_F32, GIST_DTYPE_BF16_IN = 0, 1
 GIST_ORDER_AUTO, GIST_ORDER_AGG_FIRST, GIST_ORDER_XFORM_FIRST = 0, 1, 2
 GIST_SUBAGG_CHECK_FINITE = 1
+GIST_ADAM_FRESH = 1
 
 NORM_BY_NAME = {"gcn": GIST_NORM_GCN_SYM, "sage": GIST_NORM_SAGE_MEAN,
                 "theory": GIST_NORM_THEORY}
@@ -56,7 +57,8 @@ EXPORTED = (
     "gist_set_stream", "gist_partition", "gist_build_minibatch_csr",
     "gist_layer_workspace_size", "gist_gcn_layer_fwd", "gist_gcn_layer_bwd",
     "gist_softmax_xent_workspace", "gist_softmax_xent", "gist_gather_slice",
-    "gist_sgd_update", "gist_subagg", "gist_partition_inverse", "gist_subagg_gather",
+    "gist_sgd_update", "gist_adam_update", "gist_subagg", "gist_partition_inverse",
+    "gist_subagg_gather",
     "gist_profile_begin", "gist_profile_read", "gist_profile_end",
 )
 
@@ -109,6 +111,8 @@ _sigs = {
                                     C.POINTER(C.c_int32), C.POINTER(C.c_int64)]),
     "gist_profile_end": (C.c_int, [_P]),
     "gist_partition_inverse": (C.c_int, [C.c_int64, C.c_int32, _P, _P, _P]),
+    "gist_adam_update": (C.c_int, [_P, _P, _P, _P, _P, C.c_int64, C.c_float, C.c_float, C.c_float,
+                                   C.c_float, C.c_int64, C.c_uint32]),
     "gist_subagg_gather": (C.c_int, [_P, _P, C.c_int64, C.c_int64, C.c_int64, C.c_int32,
                                      C.POINTER(gist_slice_set), C.POINTER(gist_slice_set)]),
     "gist_last_error": (C.c_char_p, []),
@@ -322,6 +326,13 @@ def gist_gather_slice(ctx, Wg, ldg, rows, nr, cols, nc, Ws, lds):
 
 def gist_sgd_update(ctx, W, dW, n, lr):
     _check(_lib.gist_sgd_update(ctx.handle, _ptr(W), _ptr(dW), int(n), float(lr)))
+
+
+def gist_adam_update(ctx, W, dW, m, v, n, lr, step, beta1=0.9, beta2=0.999, eps=1e-8,
+                     flags=0):
+    _check(_lib.gist_adam_update(ctx.handle, _ptr(W), _ptr(dW), _ptr(m), _ptr(v), int(n),
+                                 float(lr), float(beta1), float(beta2), float(eps), int(step),
+                                 int(flags)))
 
 
 def slice_set(row_rank, row_offs, col_rank, col_offs, slice_ptrs, ld):

@@ -7,7 +7,9 @@ context's stream (torch only provides the device buffers).
   layer (eq. (2)), softmax cross-entropy, layer backward in reverse, SGD.
 * :class:`GistModel` -- the global model of Algorithm 1 on one device:
   ``subGCNs`` (partition + slice gather), m sub-GCN steps back to back,
-  ``subAgg`` (slice scatter).
+  ``subAgg`` (slice scatter), optionally with Adam moments.
+* :func:`gist_train` -- Algorithm 1: T rounds of zeta local steps per
+  sub-GCN, with SGD or Adam (the optimizer of the paper's experiments).
 """
 
 import numpy as np
@@ -178,10 +180,12 @@ class SubGCN:
             H = out
         return self.H[self.L][:n]
 
-    def loss_and_grad(self, batch):
+    def loss_and_grad(self, batch, loss_out=None):
+        """Loss into ``loss_out`` (a one-element device tensor) or ``self.loss``."""
         n = batch.n
         G.gist_softmax_xent(self.ctx, n, self.widths[-1], self.H[self.L][:n], batch.labels,
-                            self.loss, self.dlogits[:n], self.loss_ws)
+                            self.loss if loss_out is None else loss_out, self.dlogits[:n],
+                            self.loss_ws)
 
     def backward(self, batch, params):
         n = batch.n
@@ -199,12 +203,25 @@ class SubGCN:
         for l in range(self.L):
             G.gist_sgd_update(self.ctx, params[l], self.dW[l], params[l].numel(), lr)
 
-    def step(self, batch, params, lr):
-        """``subTrain``: forward, loss, backward, SGD (all enqueued, nothing synced)."""
+    def adam(self, params, M, V, lr, step, fresh=False, betas=(0.9, 0.999), eps=1e-8):
+        """Adam on every layer's slice with its moments M[l], V[l]; ``fresh``
+        restarts the moments from zero (gist_adam_update's GIST_ADAM_FRESH)."""
+        flags = G.GIST_ADAM_FRESH if fresh else 0
+        for l in range(self.L):
+            G.gist_adam_update(self.ctx, params[l], self.dW[l], M[l], V[l], params[l].numel(),
+                               lr, step, betas[0], betas[1], eps, flags)
+
+    def step(self, batch, params, lr, adam=None, loss_out=None):
+        """``subTrain``: forward, loss, backward, update (all enqueued, nothing
+        synced).  ``adam`` = (M, V, step, fresh) selects Adam, else SGD."""
         self.forward(batch, params)
-        self.loss_and_grad(batch)
+        self.loss_and_grad(batch, loss_out)
         self.backward(batch, params)
-        self.sgd(params, lr)
+        if adam is None:
+            self.sgd(params, lr)
+        else:
+            M, V, k, fresh = adam
+            self.adam(params, M, V, lr, k, fresh)
 
 
 class GistModel:
@@ -220,9 +237,18 @@ class GistModel:
     ``finalize`` applies a pending subAgg.  The slices are double-buffered
     so that the trained slices of round t and the gathered slices of round
     t+1 never share memory.
+
+    ``adam`` adds Adam moments per slice (``M``, ``V``, same layout as
+    ``params``).  The paper does not say what happens to them at subAgg:
+    ``"carry"`` keeps global moments of Theta's shape that are gathered and
+    aggregated exactly like the weights (in the same fused passes);
+    ``"reset"`` restarts every sub-GCN's moments at each round (the caller
+    passes ``fresh`` on its first local step), so no global moments exist.
     """
 
-    def __init__(self, ctx, kind, widths, m, theta, device="cuda", fused=True):
+    def __init__(self, ctx, kind, widths, m, theta, device="cuda", fused=True, adam=None):
+        if adam not in (None, "carry", "reset"):
+            raise ValueError("adam is None, 'carry' or 'reset'")
         self.ctx = ctx
         self.kind = kind
         self.widths = list(widths)
@@ -231,19 +257,22 @@ class GistModel:
         self.theta = theta
         self.device = device
         self.fused = fused
+        self.adam = adam
         self.parts = 2 if kind == "sage" else 1
         self.slice_widths = [widths[0]] + [widths[l] // m for l in range(1, self.L)] + [widths[-1]]
-        s = self.slice_widths
-        nbuf = 2 if fused else 1
-        # per sub-GCN parameter slices (SAGE: [W_self; W_neigh] stacked)
-        self._bufs = [[[torch.empty(self.parts * s[l], s[l + 1], device=device)
-                        for l in range(self.L)] for _ in range(m)] for _ in range(nbuf)]
-        # device tables of the m slice pointers of every (buffer, layer, part)
-        self._ptrs = [[[torch.tensor([self._bufs[b][i][l].data_ptr() + 4 * p * s[l] * s[l + 1]
-                                      for i in range(m)], dtype=torch.int64).to(device)
-                        for p in range(self.parts)] for l in range(self.L)] for b in range(nbuf)]
+        self.nbuf = 2 if fused else 1
+        self._bufs = self._slices()                 # per sub-GCN parameter slices
+        self._ptrs = self._tables(self._bufs)
+        self._mbufs = self._vbufs = None
+        self.Mg = self.Vg = None
+        if adam:
+            self._mbufs, self._vbufs = self._slices(), self._slices()
+            self._mptrs, self._vptrs = self._tables(self._mbufs), self._tables(self._vbufs)
+        if adam == "carry":
+            self.Mg = [[torch.zeros_like(t) for t in parts] for parts in theta]
+            self.Vg = [[torch.zeros_like(t) for t in parts] for parts in theta]
         self.buf = 0
-        self.params = self._bufs[0]
+        self._select(0)
         # two round slots of partition data: host (idx, offs); device
         # [idx; rank] (int32) and offs (int64)
         self._slot = 1
@@ -253,6 +282,39 @@ class GistModel:
         self._doffs = [[None] * (self.L + 1) for _ in range(2)]
         self._events = [None, None]
         self.pending = None    # (slot, buffer) whose subAgg is outstanding
+
+    def _slices(self):
+        """[buffer][sub-GCN][layer] slice tensors (SAGE: [W_self; W_neigh] stacked)."""
+        s = self.slice_widths
+        return [[[torch.empty(self.parts * s[l], s[l + 1], device=self.device)
+                  for l in range(self.L)] for _ in range(self.m)] for _ in range(self.nbuf)]
+
+    def _tables(self, bufs):
+        """Device tables of the m slice pointers of every (buffer, layer, part)."""
+        s = self.slice_widths
+        return [[[torch.tensor([bufs[b][i][l].data_ptr() + 4 * p * s[l] * s[l + 1]
+                                for i in range(self.m)], dtype=torch.int64).to(self.device)
+                  for p in range(self.parts)] for l in range(self.L)] for b in range(self.nbuf)]
+
+    def _select(self, b):
+        self.buf = b
+        self.params = self._bufs[b]
+        self.M = self._mbufs[b] if self._mbufs else None
+        self.V = self._vbufs[b] if self._vbufs else None
+
+    def _globals(self):
+        """(global matrices, slice pointer tables) that gather / subAgg move."""
+        out = [(self.theta, self._ptrs)]
+        if self.adam == "carry":
+            out += [(self.Mg, self._mptrs), (self.Vg, self._vptrs)]
+        return out
+
+    def _pairs(self, i):
+        """(global matrices, sub-GCN i's slices of the current buffer) pairs."""
+        out = [(self.theta, self.params[i])]
+        if self.adam == "carry":
+            out += [(self.Mg, self.M[i]), (self.Vg, self.V[i])]
+        return out
 
     # -- partitions ---------------------------------------------------------
     def set_partitions(self, seeds):
@@ -302,33 +364,34 @@ class GistModel:
             cols, nc = self._block(l + 1, i)
         return rows, nr, cols, nc
 
-    def _set(self, slot, buf, l, p):
-        """gist_slice_set of layer l, part p: partition `slot`, slice buffer `buf`."""
+    def _set(self, slot, table, l, p):
+        """gist_slice_set of layer l, part p: partition `slot`, slice pointer `table`."""
         rr = ro = cr = co = None
         if l > 0:
             rr, ro = self._dev[slot][l][1], self._doffs[slot][l]
         if l + 1 < self.L:
             cr, co = self._dev[slot][l + 1][1], self._doffs[slot][l + 1]
-        return G.slice_set(rr, ro, cr, co, self._ptrs[buf][l][p], self.slice_widths[l + 1])
+        return G.slice_set(rr, ro, cr, co, table[l][p], self.slice_widths[l + 1])
 
     # -- per-slice calls ----------------------------------------------------
     def gather(self, i):
-        """Theta^(i)_l = Theta_l[D_l^(i), D_{l+1}^(i)] for every layer and part."""
-        for l in range(self.L):
-            rows, nr, cols, nc = self._rc(l, i)
-            for p in range(self.parts):
-                dst = self.params[i][l][p * nr:(p + 1) * nr]
-                G.gist_gather_slice(self.ctx, self.theta[l][p], self.widths[l + 1], rows, nr,
-                                    cols, nc, dst, nc)
+        """Theta^(i)_l = Theta_l[D_l^(i), D_{l+1}^(i)] for every layer and part
+        (and the moments' slices with "carry")."""
+        for glob, sl in self._pairs(i):
+            for l in range(self.L):
+                rows, nr, cols, nc = self._rc(l, i)
+                for p in range(self.parts):
+                    G.gist_gather_slice(self.ctx, glob[l][p], self.widths[l + 1], rows, nr,
+                                        cols, nc, sl[l][p * nr:(p + 1) * nr], nc)
 
     def subagg(self, i, flags=0):
         """Write sub-GCN i's trained slices back into Theta (replacement)."""
-        for l in range(self.L):
-            rows, nr, cols, nc = self._rc(l, i)
-            for p in range(self.parts):
-                src = self.params[i][l][p * nr:(p + 1) * nr]
-                G.gist_subagg(self.ctx, self.theta[l][p], self.widths[l + 1], rows, nr, cols,
-                              nc, src, nc, flags)
+        for glob, sl in self._pairs(i):
+            for l in range(self.L):
+                rows, nr, cols, nc = self._rc(l, i)
+                for p in range(self.parts):
+                    G.gist_subagg(self.ctx, glob[l][p], self.widths[l + 1], rows, nr, cols,
+                                  nc, sl[l][p * nr:(p + 1) * nr], nc, flags)
 
     # -- rounds ---------------------------------------------------------------
     def begin_round(self):
@@ -338,15 +401,15 @@ class GistModel:
                 self.gather(i)
             return
         nxt = 1 - self.buf if self.pending is not None else self.buf
-        for l in range(self.L):
-            for p in range(self.parts):
-                done = (self._set(self.pending[0], self.pending[1], l, p)
-                        if self.pending is not None else None)
-                G.gist_subagg_gather(self.ctx, self.theta[l][p], self.widths[l],
-                                     self.widths[l + 1], self.widths[l + 1], self.m, done,
-                                     self._set(self._slot, nxt, l, p))
-        self.buf = nxt
-        self.params = self._bufs[nxt]
+        for glob, tables in self._globals():
+            for l in range(self.L):
+                for p in range(self.parts):
+                    done = (self._set(self.pending[0], tables[self.pending[1]], l, p)
+                            if self.pending is not None else None)
+                    G.gist_subagg_gather(self.ctx, glob[l][p], self.widths[l],
+                                         self.widths[l + 1], self.widths[l + 1], self.m, done,
+                                         self._set(self._slot, tables[nxt], l, p))
+        self._select(nxt)
         self.pending = None
 
     def end_round(self):
@@ -361,9 +424,41 @@ class GistModel:
         """Apply a pending subAgg so that Theta holds every trained slice."""
         if self.pending is None:
             return
-        for l in range(self.L):
-            for p in range(self.parts):
-                G.gist_subagg_gather(self.ctx, self.theta[l][p], self.widths[l],
-                                     self.widths[l + 1], self.widths[l + 1], self.m,
-                                     self._set(self.pending[0], self.pending[1], l, p), None)
+        for glob, tables in self._globals():
+            for l in range(self.L):
+                for p in range(self.parts):
+                    G.gist_subagg_gather(self.ctx, glob[l][p], self.widths[l],
+                                         self.widths[l + 1], self.widths[l + 1], self.m,
+                                         self._set(self.pending[0], tables[self.pending[1]], l, p),
+                                         None)
         self.pending = None
+
+
+def gist_train(model, runner, rounds, zeta, lr, partition_seeds, batch):
+    """Algorithm 1 on one device: ``rounds`` synchronisation rounds, each
+    ``subGCNs`` -> ``zeta`` local steps per sub-GCN (``subTrain``, back to
+    back) -> ``subAgg``.
+
+    ``partition_seeds(t)`` -> {l: seed} for the hidden widths;
+    ``batch(t, i, z)`` -> the loaded mini-batch of sub-GCN i's step z.
+    The optimizer is the model's: SGD, or Adam with the bias correction
+    counting every local step so far ("carry": k = t zeta + z + 1) or the
+    round's steps ("reset": k = z + 1, moments restarted at z = 0).
+    Returns the device tensor of losses [rounds, m, zeta]; nothing is synced.
+    """
+    losses = torch.empty(rounds, model.m, zeta, device=model.device)
+    for t in range(rounds):
+        model.set_partitions(partition_seeds(t))
+        model.begin_round()
+        for i in range(model.m):
+            for z in range(zeta):
+                b = batch(t, i, z)
+                opt = None
+                if model.adam == "carry":
+                    opt = (model.M[i], model.V[i], t * zeta + z + 1, False)
+                elif model.adam == "reset":
+                    opt = (model.M[i], model.V[i], z + 1, z == 0)
+                runner.step(b, model.params[i], lr, adam=opt, loss_out=losses[t, i, z:z + 1])
+        model.end_round()
+    model.finalize()
+    return losses
