@@ -249,6 +249,11 @@ __device__ __forceinline__ void store_out(const OutDev& C, int64_t row, int64_t 
 template <bool AK, bool BK_, bool AV, bool BV, bool BF16>
 constexpr int min_blocks() { return (!BF16 && ((AV && BV) || (AK && BK_))) ? 2 : 1; }
 
+// Double-buffered MFMA fragments (16 more VGPRs) where the variant still
+// fits two waves per SIMD with them.
+template <bool AK, bool BK_, bool AV, bool BV>
+constexpr bool kPipeFrag() { return AV && BV && AK == BK_; }
+
 template <bool AK, bool BK_, bool AV, bool BV, bool BF16>
 __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) void gemm_kernel(int64_t M, int64_t N, int64_t K,
                                                         OpDev A, OpDev B, OutDev C, Sched S,
@@ -318,23 +323,50 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
     } else {
       const float* As = lds_f + buf * kStage;
       const float* Bs = As + kTileF;
+      if constexpr (kPipeFrag<AK, BK_, AV, BV>()) {
+        // fragments of chunk c+1 are read while chunk c multiplies
+        floatx4 av[2][2], bv[2][2];
+        auto rd = [&](int c, int p) {
 #pragma unroll
-      for (int c = 0; c < BK / 8; ++c) {
-        floatx4 av[2], bv[2];
+          for (int t = 0; t < 2; ++t) {
+            av[p][t] = frag_f32(As, wm * 64 + t * 32 + li, 8 * c + 4 * lh);
+            bv[p][t] = frag_f32(Bs, wn * 64 + t * 32 + li, 8 * c + 4 * lh);
+          }
+        };
+        rd(0, 0);
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          av[t] = frag_f32(As, wm * 64 + t * 32 + li, 8 * c + 4 * lh);
-          bv[t] = frag_f32(Bs, wn * 64 + t * 32 + li, 8 * c + 4 * lh);
+        for (int c = 0; c < BK / 8; ++c) {
+          if (c + 1 < BK / 8) rd(c + 1, (c + 1) & 1);
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int a = 0; a < 2; ++a)
+#pragma unroll
+              for (int b = 0; b < 2; ++b)
+                acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[c & 1][a][s], bv[c & 1][b][s],
+                                                                 acc[a][b], 0, 0, 0);
+          __builtin_amdgcn_sched_barrier(0);
         }
+      } else {
 #pragma unroll
-        for (int s = 0; s < 4; ++s)
+        for (int c = 0; c < BK / 8; ++c) {
+          floatx4 av[2], bv[2];
 #pragma unroll
-          for (int a = 0; a < 2; ++a)
+          for (int t = 0; t < 2; ++t) {
+            av[t] = frag_f32(As, wm * 64 + t * 32 + li, 8 * c + 4 * lh);
+            bv[t] = frag_f32(Bs, wn * 64 + t * 32 + li, 8 * c + 4 * lh);
+          }
 #pragma unroll
-            for (int b = 0; b < 2; ++b)
-              acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[a][s], bv[b][s], acc[a][b], 0, 0, 0);
-        // one K chunk's fragments live at a time (keeps two waves per SIMD)
-        __builtin_amdgcn_sched_barrier(0);
+          for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int a = 0; a < 2; ++a)
+#pragma unroll
+              for (int b = 0; b < 2; ++b)
+                acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[a][s], bv[b][s], acc[a][b], 0, 0, 0);
+          // one K chunk's fragments live at a time (keeps two waves per SIMD)
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
     }
   };
