@@ -97,6 +97,8 @@ def parse():
     ap.add_argument("--adam-policy", default="carry", choices=["carry", "reset"],
                     help="Adam moments at subAgg: carried with the weights, or reset per round")
     ap.add_argument("--zeta", type=int, default=1, help="local steps per sub-GCN per round")
+    ap.add_argument("--shared-batch", action="store_true",
+                    help="all m sub-GCNs step on one shared mini-batch, as batched layer calls")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the library's per-launch event timing")
@@ -109,10 +111,10 @@ def parse():
 class RoundWorkload:
     """A GIST round (partition, gather, m sub-GCN steps, subAgg) on one GPU."""
 
-    def __init__(self, cfg, ctx, dtype, optimizer="sgd", policy="carry", zeta=1):
+    def __init__(self, cfg, ctx, dtype, optimizer="sgd", policy="carry", zeta=1, shared=False):
         import torch
         from paper_2102_10424_amd import gist as G
-        from paper_2102_10424_amd.step import BatchSlot, GistModel, SubGCN
+        from paper_2102_10424_amd.step import BatchSlot, GistModel, SubGCN, SubGCNBatch
         self.cfg, self.ctx, self.G = cfg, ctx, G
         t0 = time.time()
         self.graph = cfg.make_graph()
@@ -143,8 +145,12 @@ class RoundWorkload:
         self.slots = [BatchSlot(ctx, self.norm, cap_n, cap_nnz, cfg.widths[0])
                       for _ in range(cfg.m)]
         self.full = None
-        self.runner = SubGCN(ctx, cfg.kind, self.model.slice_widths, cap_n,
-                             dtype=G.GIST_DTYPE_BF16_IN if dtype == "bf16" else G.GIST_DTYPE_F32)
+        dt = G.GIST_DTYPE_BF16_IN if dtype == "bf16" else G.GIST_DTYPE_F32
+        self.shared = shared
+        if shared:
+            self.runner = SubGCNBatch(ctx, cfg.kind, self.model.slice_widths, cfg.m, cap_n, dtype=dt)
+        else:
+            self.runner = SubGCN(ctx, cfg.kind, self.model.slice_widths, cap_n, dtype=dt)
         self.lr = 0.01
         self.t = 0
 
@@ -153,6 +159,23 @@ class RoundWorkload:
         t, zeta = self.t, self.zeta
         m.set_partitions({l: cfg.partition_seed(t, l) for l in range(1, cfg.L)})
         m.begin_round()   # subAgg of round t-1 fused with the gather of round t
+        if self.shared:
+            for z in range(zeta):
+                if cfg.batch_clusters is None:
+                    if self.full is None:
+                        self.full = self.slots[0].load(self.gh, None, self.X, self.labels)
+                    b = self.full
+                else:
+                    b = self.slots[z % len(self.slots)].load(self.gh, cfg.minibatch(t, 0, z),
+                                                             self.X, self.labels)
+                opt = None
+                if self.adam:
+                    k = t * zeta + z + 1 if self.adam == "carry" else z + 1
+                    opt = (m.stacked("M"), m.stacked("V"), k, self.adam == "reset" and z == 0)
+                self.runner.step(b, m.stacked(), self.lr, adam=opt)
+            m.end_round()
+            self.t += 1
+            return
         for i in range(cfg.m):
             for z in range(zeta):
                 if cfg.batch_clusters is None:
@@ -184,6 +207,8 @@ class RoundWorkload:
                             f"{'mini-batch ' + str(c.batch_clusters) + ' clusters' if c.batch_clusters else 'full graph'}",
                 "model": "GIST sub-GCN", "m": c.m, "widths": c.widths,
                 "global_batch": c.batch_clusters or c.n_nodes, "zeta": self.zeta,
+                "batching": "m sub-GCNs on one shared mini-batch (batched layers)" if self.shared
+                            else "one mini-batch per sub-GCN",
                 "optimizer": f"adam ({self.adam} moments)" if self.adam else "sgd"}
 
     # ---- CPU baseline: the fp64 oracle on one sub-GCN step ---------------------
@@ -329,7 +354,8 @@ def main():
     if args.config == "c5":
         wl = LayerWorkload(cfg, ctx, args.dtype, args.d_in)
     else:
-        wl = RoundWorkload(cfg, ctx, args.dtype, args.optimizer, args.adam_policy, args.zeta)
+        wl = RoundWorkload(cfg, ctx, args.dtype, args.optimizer, args.adam_policy, args.zeta,
+                           args.shared_batch)
         wl.lr = args.lr
     for w in range(args.warmup):
         wl.step()

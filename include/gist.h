@@ -187,7 +187,23 @@ typedef struct gist_layer_desc {
   int64_t n;       /* mini-batch rows                                   */
   int32_t s_in;    /* sub-GCN input width  |D_l|  (d_0 at layer 0)       */
   int32_t s_out;   /* sub-GCN output width |D_l+1| (d_L at the last layer) */
+  int32_t groups;  /* G sub-GCNs batched on this mini-batch (0 means 1)  */
+  uint32_t flags;  /* GIST_LAYER_SHARED_INPUT | GIST_LAYER_GROUP_MAJOR_OUT */
 } gist_layer_desc;
+
+/* Batched sub-GCNs (G > 1): the layer of G sub-GCNs that share one
+ * mini-batch, each with its own weight slice -- the same results as G
+ * separate calls, with one full-width aggregation and grouped GEMMs.
+ * Layouts (row-major fp32):
+ *   H, agg_save, dH   n x (G s_in), sub-GCN g in columns [g s_in, (g+1) s_in);
+ *                     with GIST_LAYER_SHARED_INPUT one n x s_in matrix that
+ *                     every sub-GCN reads (the unpartitioned input layer:
+ *                     Abar H is formed once; dH must be NULL);
+ *   W, dW             G consecutive slices of (s_in or 2 s_in) x s_out;
+ *   H_out, dH_out     n x (G s_out), sub-GCN g in columns [g s_out, ...);
+ *                     with GIST_LAYER_GROUP_MAJOR_OUT G consecutive
+ *                     n x s_out blocks (each sub-GCN's logits contiguous). */
+enum { GIST_LAYER_SHARED_INPUT = 1, GIST_LAYER_GROUP_MAJOR_OUT = 2 };
 
 /* Workspace (device bytes) that fwd and bwd need for this descriptor. */
 gist_status gist_layer_workspace_size(const gist_layer_desc* L, size_t* fwd_bytes,

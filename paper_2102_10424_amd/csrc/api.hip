@@ -171,9 +171,52 @@ gist_status check_desc(const gist_layer_desc* L) {
     return set_error(GIST_E_INVAL, "layer: unknown order");
   if (L->kind == GIST_LAYER_SAGE_MEAN && L->order == GIST_ORDER_XFORM_FIRST)
     return set_error(GIST_E_INVAL, "layer: SAGE-mean aggregates first");
-  if (L->n < 0 || L->s_in < 1 || L->s_out < 1)
+  if (L->n < 0 || L->s_in < 1 || L->s_out < 1 || L->groups < 0)
     return set_error(GIST_E_INVAL, "layer: bad sizes");
+  if (L->flags & ~static_cast<uint32_t>(GIST_LAYER_SHARED_INPUT | GIST_LAYER_GROUP_MAJOR_OUT))
+    return set_error(GIST_E_INVAL, "layer: unknown flags");
   if (L->n > INT32_MAX) return set_error(GIST_E_UNSUPPORTED, "layer: n exceeds int32 rows");
+  const int64_t G = L->groups > 1 ? L->groups : 1;
+  if (G * L->s_in > INT32_MAX || G * L->s_out > INT32_MAX)
+    return set_error(GIST_E_UNSUPPORTED, "layer: batched width exceeds int32");
+  return GIST_OK;
+}
+
+// Layout of a (possibly batched) layer: leading dimensions and per-group
+// element offsets of the input-side (H, agg, dH) and output-side (H_out,
+// dH_out, dZ) tensors and of the weight slices.
+struct Lay {
+  int64_t G, n, si, so, wrows;
+  bool shared, gmajor;
+  int64_t ld_in, gs_in, ld_out, gs_out, gs_w;
+  int64_t w_in() const { return shared ? si : G * si; }   // aggregation width on the input side
+};
+
+Lay layout(const gist_layer_desc* L) {
+  Lay y;
+  y.G = L->groups > 1 ? L->groups : 1;
+  y.n = L->n; y.si = L->s_in; y.so = L->s_out;
+  y.wrows = (L->kind == GIST_LAYER_SAGE_MEAN ? 2 : 1) * y.si;
+  y.shared = (L->flags & GIST_LAYER_SHARED_INPUT) != 0;
+  y.gmajor = (L->flags & GIST_LAYER_GROUP_MAJOR_OUT) != 0;
+  y.ld_in = y.shared ? y.si : y.G * y.si;
+  y.gs_in = y.shared ? 0 : y.si;
+  y.ld_out = y.gmajor ? y.so : y.G * y.so;
+  y.gs_out = y.gmajor ? y.n * y.so : y.so;
+  y.gs_w = y.wrows * y.so;
+  return y;
+}
+
+// Abar X over an output-side tensor (dZ-like layout): one full-width call,
+// or one per group when the groups are stored one after another.
+gist_status spmm_out(hipStream_t st, const Lay& y, const gist_csr_dev* A, const float* X, float* Y,
+                     bool relu) {
+  if (!y.gmajor)
+    return gist::spmm(st, y.n, A->nnz, A->rowptr, A->col, A->val, X, y.ld_out, int(y.G * y.so), Y,
+                      y.ld_out, nullptr, 0, relu);
+  for (int64_t g = 0; g < y.G; ++g)
+    GIST_TRY(gist::spmm(st, y.n, A->nnz, A->rowptr, A->col, A->val, X + g * y.gs_out, y.so,
+                        int(y.so), Y + g * y.gs_out, y.so, nullptr, 0, relu));
   return GIST_OK;
 }
 
@@ -195,31 +238,25 @@ struct BwdPlan {
 
 BwdPlan plan_bwd(const gist_layer_desc* L) {
   BwdPlan p;
-  const int64_t n = L->n, si = L->s_in, so = L->s_out;
-  if (L->act == GIST_ACT_RELU) p.dz = fbytes(n, so);
+  const Lay y = layout(L);
+  const int64_t n = y.n, si = y.si, so = y.so, G = y.G;
+  if (L->act == GIST_ACT_RELU) p.dz = fbytes(n, G * so);
   const int order = resolve_order(L);
-  if (L->kind == GIST_LAYER_SAGE_MEAN) {
-    p.tmp = fbytes(n, si);  // dP = dZ W_neigh^T
-    p.gemm = std::max(gist::gemm_workspace(2 * si, so, n, L->dtype),
-                      gist::gemm_workspace(n, 2 * si, so, L->dtype));
-  } else if (order == GIST_ORDER_AGG_FIRST) {
-    p.tmp = fbytes(n, si);  // dP
-    p.gemm = std::max(gist::gemm_workspace(si, so, n, L->dtype),
-                      gist::gemm_workspace(n, si, so, L->dtype));
-  } else {
-    p.tmp = fbytes(n, so);  // G = Abar^T dZ
-    p.gemm = std::max(gist::gemm_workspace(si, so, n, L->dtype),
-                      gist::gemm_workspace(n, si, so, L->dtype));
-  }
+  if (L->kind == GIST_LAYER_SAGE_MEAN || order == GIST_ORDER_AGG_FIRST)
+    p.tmp = fbytes(n, G * si);  // dP = dZ W^T (W_neigh for SAGE)
+  else
+    p.tmp = fbytes(n, G * so);  // Abar^T dZ
+  p.gemm = std::max(gist::gemm_workspace(y.wrows, so, n, L->dtype, G),
+                    gist::gemm_workspace(n, y.wrows, so, L->dtype, G));
   return p;
 }
 
 size_t plan_fwd(const gist_layer_desc* L) {
+  const Lay y = layout(L);
   const int order = resolve_order(L);
   size_t t = 0;
-  const int64_t K = L->kind == GIST_LAYER_SAGE_MEAN ? 2 * int64_t(L->s_in) : L->s_in;
-  if (L->kind == GIST_LAYER_GCN && order == GIST_ORDER_XFORM_FIRST) t = fbytes(L->n, L->s_out);
-  return align256(t) + gist::gemm_workspace(L->n, L->s_out, K, L->dtype);
+  if (L->kind == GIST_LAYER_GCN && order == GIST_ORDER_XFORM_FIRST) t = fbytes(y.n, y.G * y.so);
+  return align256(t) + gist::gemm_workspace(y.n, y.so, y.wrows, L->dtype, y.G);
 }
 
 }  // namespace
@@ -242,7 +279,8 @@ extern "C" gist_status gist_gcn_layer_fwd(gist_ctx* ctx, const gist_layer_desc* 
   gist::ProfBind pb(ctx);
   GIST_TRY(check_desc(L));
   GIST_TRY(check_csr(A, L->n, "layer_fwd"));
-  const int64_t n = L->n, si = L->s_in, so = L->s_out;
+  const Lay y = layout(L);
+  const int64_t n = y.n, si = y.si, so = y.so, G = y.G;
   const int order = resolve_order(L);
   const bool sage = L->kind == GIST_LAYER_SAGE_MEAN;
   if (n > 0 && (!H || !W || !H_out)) return set_error(GIST_E_INVAL, "layer_fwd: NULL pointer");
@@ -255,37 +293,34 @@ extern "C" gist_status gist_gcn_layer_fwd(gist_ctx* ctx, const gist_layer_desc* 
   gist::DeviceGuard dg(ctx->device);
   hipStream_t st = ctx->stream;
   const bool relu = L->act == GIST_ACT_RELU;
-  gist::GemmOut out;
-  out.c0 = H_out;
-  out.ldc0 = so;
+  gist::Operand b;  // W_g is (K x s_out) row-major: an N x K operand, N contiguous
+  b.p0 = W; b.ld0 = so; b.k_major = false; b.gs0 = y.gs_w;
   if (sage || order == GIST_ORDER_AGG_FIRST) {
-    GIST_TRY(gist::spmm(st, n, A->nnz, A->rowptr, A->col, A->val, H, si, int(si), agg_save, si,
-                        nullptr, 0, false));
+    // one aggregation over every group's columns (or the shared input once)
+    GIST_TRY(gist::spmm(st, n, A->nnz, A->rowptr, A->col, A->val, H, y.ld_in, int(y.w_in()),
+                        agg_save, y.ld_in, nullptr, 0, false));
     gist::Operand a;
     a.k_major = true;
-    if (sage) {  // [H | Abar H], concatenated along K
-      a.p0 = H; a.ld0 = si; a.p1 = agg_save; a.ld1 = si; a.split = si;
+    if (sage) {  // [H_g | Abar H_g], concatenated along K
+      a.p0 = H; a.ld0 = y.ld_in; a.gs0 = y.gs_in;
+      a.p1 = agg_save; a.ld1 = y.ld_in; a.gs1 = y.gs_in; a.split = si;
     } else {
-      a.p0 = agg_save; a.ld0 = si;
+      a.p0 = agg_save; a.ld0 = y.ld_in; a.gs0 = y.gs_in;
     }
-    gist::Operand b;  // W is (K x s_out) row-major: an N x K operand, N contiguous
-    b.p0 = W; b.ld0 = so; b.k_major = false;
-    out.relu = relu;
-    const int64_t K = sage ? 2 * si : si;
-    return gist::gemm(st, n, so, K, a, b, out, L->dtype, ws, ws_bytes);
+    gist::GemmOut out;
+    out.c0 = H_out; out.ldc0 = y.ld_out; out.gs0 = y.gs_out; out.relu = relu;
+    return gist::gemm(st, n, so, y.wrows, a, b, out, L->dtype, ws, ws_bytes, G);
   }
-  // transform first: T = H W (workspace), H_out = act(Abar T)
+  // transform first: T_g = H_g W_g (workspace, laid out like H_out), H_out = act(Abar T)
   float* T = static_cast<float*>(ws);
-  void* gws = static_cast<char*>(ws) + align256(fbytes(n, so));
+  const size_t tb = align256(fbytes(n, G * so));
+  void* gws = static_cast<char*>(ws) + tb;
   gist::Operand a;
-  a.p0 = H; a.ld0 = si; a.k_major = true;
-  gist::Operand b;
-  b.p0 = W; b.ld0 = so; b.k_major = false;
+  a.p0 = H; a.ld0 = y.ld_in; a.gs0 = y.gs_in; a.k_major = true;
   gist::GemmOut t;
-  t.c0 = T; t.ldc0 = so;
-  GIST_TRY(gist::gemm(st, n, so, si, a, b, t, L->dtype, gws, ws_bytes - align256(fbytes(n, so))));
-  return gist::spmm(st, n, A->nnz, A->rowptr, A->col, A->val, T, so, int(so), H_out, so, nullptr, 0,
-                    relu);
+  t.c0 = T; t.ldc0 = y.ld_out; t.gs0 = y.gs_out;
+  GIST_TRY(gist::gemm(st, n, so, si, a, b, t, L->dtype, gws, ws_bytes - tb, G));
+  return spmm_out(st, y, A, T, H_out, relu);
 }
 
 extern "C" gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* L,
@@ -302,10 +337,13 @@ extern "C" gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* 
   const bool sage = L->kind == GIST_LAYER_SAGE_MEAN;
   if (sage) GIST_TRY(check_csr(A_T, L->n, "layer_bwd (transpose)"));
   else if (A_T) GIST_TRY(check_csr(A_T, L->n, "layer_bwd (transpose)"));
-  const int64_t n = L->n, si = L->s_in, so = L->s_out;
+  const Lay y = layout(L);
+  const int64_t n = y.n, si = y.si, so = y.so, G = y.G;
   const int order = resolve_order(L);
   const bool relu = L->act == GIST_ACT_RELU;
   if (!dW || !W) return set_error(GIST_E_INVAL, "layer_bwd: NULL dW or W");
+  if (dH && y.shared)
+    return set_error(GIST_E_INVAL, "layer_bwd: a shared input has no per-group dH");
   if (n > 0 && (!H || !dH_out || (relu && !H_out)))
     return set_error(GIST_E_INVAL, "layer_bwd: NULL pointer");
   if (n > 0 && (sage || order == GIST_ORDER_AGG_FIRST) && !agg_save)
@@ -315,8 +353,7 @@ extern "C" gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* 
     return set_error(GIST_E_NOMEM, "layer_bwd: workspace too small");
   gist::DeviceGuard dg(ctx->device);
   hipStream_t st = ctx->stream;
-  const int64_t wrows = sage ? 2 * si : si;
-  if (n == 0) return gist::fill_zero(st, dW, wrows * so);  // empty batch: zero gradient
+  if (n == 0) return gist::fill_zero(st, dW, G * y.wrows * so);  // empty batch: zero gradient
   char* base = static_cast<char*>(ws);
   float* dZbuf = reinterpret_cast<float*>(base);
   float* tmp = reinterpret_cast<float*>(base + align256(p.dz));
@@ -324,55 +361,60 @@ extern "C" gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* 
   const size_t gbytes = p.gemm;
   const float* dZ = dH_out;
   if (relu) {
-    GIST_TRY(gist::relu_mask(st, n * so, dH_out, H_out, dZbuf));
+    GIST_TRY(gist::relu_mask(st, n * G * so, dH_out, H_out, dZbuf));
     dZ = dZbuf;
   }
   const gist_csr_dev* AT = A_T ? A_T : A;
 
-  gist::Operand dz_as_b;  // dZ (n x s_out): B operand of the weight gradient, N = s_out, K = n
-  dz_as_b.p0 = dZ; dz_as_b.ld0 = so; dz_as_b.k_major = false;
+  gist::Operand dz_as_b;  // dZ_g (n x s_out): B operand of the weight gradient, N = s_out, K = n
+  dz_as_b.p0 = dZ; dz_as_b.ld0 = y.ld_out; dz_as_b.gs0 = y.gs_out; dz_as_b.k_major = false;
   gist::GemmOut wout;
-  wout.c0 = dW; wout.ldc0 = so;
+  wout.c0 = dW; wout.ldc0 = so; wout.gs0 = y.gs_w;
+  gist::Operand w_as_b;   // W_g^T as an N x K operand is W_g itself (rows = N, K contiguous)
+  w_as_b.p0 = W; w_as_b.ld0 = so; w_as_b.gs0 = y.gs_w; w_as_b.k_major = true;
+  const int64_t ld_p = G * si;   // dP / dH: n x (G s_in)
 
   if (sage || order == GIST_ORDER_AGG_FIRST) {
-    // dW = [H | Abar H]^T dZ (SAGE) or (Abar H)^T dZ: A operand is (rows x n), n contiguous... as
-    // stored, element (r, k) of the transposed activation is act[k * ld + r].
+    // dW_g = [H_g | Abar H_g]^T dZ_g (SAGE) or (Abar H_g)^T dZ_g: element (r, k) of the
+    // transposed activation is act[k * ld + r]
     gist::Operand a;
     a.k_major = false;
-    if (sage) { a.p0 = H; a.ld0 = si; a.p1 = agg_save; a.ld1 = si; a.split = si; }
-    else { a.p0 = agg_save; a.ld0 = si; }
-    GIST_TRY(gist::gemm(st, wrows, so, n, a, dz_as_b, wout, L->dtype, gws, gbytes));
+    if (sage) {
+      a.p0 = H; a.ld0 = y.ld_in; a.gs0 = y.gs_in;
+      a.p1 = agg_save; a.ld1 = y.ld_in; a.gs1 = y.gs_in; a.split = si;
+    } else {
+      a.p0 = agg_save; a.ld0 = y.ld_in; a.gs0 = y.gs_in;
+    }
+    GIST_TRY(gist::gemm(st, y.wrows, so, n, a, dz_as_b, wout, L->dtype, gws, gbytes, G));
     if (!dH) return GIST_OK;
-    // [dH_self | dP] = dZ W^T (SAGE), dP = dZ W^T (GCN): A = dZ (n x s_out, K contiguous),
-    // B = W^T as an N x K operand = W itself (rows = N, K contiguous).
+    // [dH_self | dP]_g = dZ_g W_g^T (SAGE), dP_g = dZ_g W_g^T (GCN)
     gist::Operand a2;
-    a2.p0 = dZ; a2.ld0 = so; a2.k_major = true;
-    gist::Operand b2;
-    b2.p0 = W; b2.ld0 = so; b2.k_major = true;
+    a2.p0 = dZ; a2.ld0 = y.ld_out; a2.gs0 = y.gs_out; a2.k_major = true;
     gist::GemmOut o2;
-    if (sage) { o2.c0 = dH; o2.ldc0 = si; o2.c1 = tmp; o2.ldc1 = si; o2.c_split = si; }
-    else { o2.c0 = tmp; o2.ldc0 = si; }
-    GIST_TRY(gist::gemm(st, n, wrows, so, a2, b2, o2, L->dtype, gws, gbytes));
-    // dH (+)= Abar^T dP
-    return gist::spmm(st, n, AT->nnz, AT->rowptr, AT->col, AT->val, tmp, si, int(si), dH, si,
-                      sage ? dH : nullptr, si, false);
+    if (sage) {
+      o2.c0 = dH; o2.ldc0 = ld_p; o2.gs0 = si;
+      o2.c1 = tmp; o2.ldc1 = ld_p; o2.gs1 = si; o2.c_split = si;
+    } else {
+      o2.c0 = tmp; o2.ldc0 = ld_p; o2.gs0 = si;
+    }
+    GIST_TRY(gist::gemm(st, n, y.wrows, so, a2, w_as_b, o2, L->dtype, gws, gbytes, G));
+    // dH (+)= Abar^T dP, every group at once
+    return gist::spmm(st, n, AT->nnz, AT->rowptr, AT->col, AT->val, tmp, ld_p, int(ld_p), dH, ld_p,
+                      sage ? dH : nullptr, ld_p, false);
   }
-  // GCN transform-first: G = Abar^T dZ; dW = H^T G; dH = G W^T
-  GIST_TRY(gist::spmm(st, n, AT->nnz, AT->rowptr, AT->col, AT->val, dZ, so, int(so), tmp, so, nullptr,
-                      0, false));
+  // GCN transform-first: T = Abar^T dZ (laid out like dZ); dW_g = H_g^T T_g; dH_g = T_g W_g^T
+  GIST_TRY(spmm_out(st, y, AT, dZ, tmp, false));
   gist::Operand a;
-  a.p0 = H; a.ld0 = si; a.k_major = false;
+  a.p0 = H; a.ld0 = y.ld_in; a.gs0 = y.gs_in; a.k_major = false;
   gist::Operand g;
-  g.p0 = tmp; g.ld0 = so; g.k_major = false;
-  GIST_TRY(gist::gemm(st, si, so, n, a, g, wout, L->dtype, gws, gbytes));
+  g.p0 = tmp; g.ld0 = y.ld_out; g.gs0 = y.gs_out; g.k_major = false;
+  GIST_TRY(gist::gemm(st, si, so, n, a, g, wout, L->dtype, gws, gbytes, G));
   if (!dH) return GIST_OK;
   gist::Operand a2;
-  a2.p0 = tmp; a2.ld0 = so; a2.k_major = true;
-  gist::Operand b2;
-  b2.p0 = W; b2.ld0 = so; b2.k_major = true;
+  a2.p0 = tmp; a2.ld0 = y.ld_out; a2.gs0 = y.gs_out; a2.k_major = true;
   gist::GemmOut o2;
-  o2.c0 = dH; o2.ldc0 = si;
-  return gist::gemm(st, n, si, so, a2, b2, o2, L->dtype, gws, gbytes);
+  o2.c0 = dH; o2.ldc0 = ld_p; o2.gs0 = si;
+  return gist::gemm(st, n, si, so, a2, w_as_b, o2, L->dtype, gws, gbytes, G);
 }
 
 // ---------------------------------------------------------------------------

@@ -57,6 +57,14 @@ struct OpDev {
   const float* p0;
   const float* p1;
   int64_t ld0, ld1, split;
+  int64_t gs0, gs1;   // group strides of p0 / p1
+
+  __device__ __forceinline__ OpDev group(int64_t g) const {
+    OpDev o = *this;
+    o.p0 += g * gs0;
+    o.p1 += g * gs1;
+    return o;
+  }
 };
 
 struct OutDev {
@@ -64,6 +72,14 @@ struct OutDev {
   float* c1;
   int64_t ldc0, ldc1, c_split;
   int relu;
+  int64_t gs0, gs1;
+
+  __device__ __forceinline__ OutDev group(int64_t g) const {
+    OutDev o = *this;
+    o.c0 += g * gs0;
+    o.c1 += g * gs1;
+    return o;
+  }
 };
 
 // Element (r, k) of an operand; r < R and k < K are checked by the caller.
@@ -232,10 +248,11 @@ __device__ __forceinline__ void store_tile_bf16(unsigned short* lds, const float
 }
 
 struct Sched {
-  int64_t T;        // total iterations = tiles * nk
+  int64_t T;        // total iterations = tiles * nk (tiles of all groups)
   int64_t ipw;      // iterations per workgroup
   int nk;           // K steps per tile
   int tiles_m, tiles_n;
+  int64_t tpg;      // tiles per group (tiles_m * tiles_n)
 };
 
 __device__ __forceinline__ void store_out(const OutDev& C, int64_t row, int64_t col, float v) {
@@ -274,6 +291,8 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
   floatx16 acc[2][2];
   floatx4 ra[SUB][4], rb[SUB][4];
   int64_t m0 = 0, n0 = 0;
+  OpDev Ag = A, Bg = B;   // this tile's group of A, B and C
+  OutDev Cg = C;
 
   auto stage = [&](int buf) {
     if constexpr (BF16) {
@@ -290,15 +309,15 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
   auto load_full = [&](int64_t k) {
 #pragma unroll
     for (int s = 0; s < SUB; ++s) {
-      load_tile<AK, AV, true>(A, M, K, m0, k + s * BK, ra[s]);
-      load_tile<BK_, BV, true>(B, N, K, n0, k + s * BK, rb[s]);
+      load_tile<AK, AV, true>(Ag, M, K, m0, k + s * BK, ra[s]);
+      load_tile<BK_, BV, true>(Bg, N, K, n0, k + s * BK, rb[s]);
     }
   };
   auto load_edge = [&](int64_t k) {
 #pragma unroll
     for (int s = 0; s < SUB; ++s) {
-      load_tile<AK, AV, false>(A, M, K, m0, k + s * BK, ra[s]);
-      load_tile<BK_, BV, false>(B, N, K, n0, k + s * BK, rb[s]);
+      load_tile<AK, AV, false>(Ag, M, K, m0, k + s * BK, ra[s]);
+      load_tile<BK_, BV, false>(Bg, N, K, n0, k + s * BK, rb[s]);
     }
   };
   auto compute = [&](int buf) {
@@ -381,10 +400,14 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
     const int64_t tile = it / S.nk;
     const int kb = static_cast<int>(it % S.nk);
     const int ke = static_cast<int>(min<int64_t>(S.nk, kb + (it_end - it)));
+    const int64_t grp = tile / S.tpg;
     int tm, tn;
-    tile_coords_banded(tile, S.tiles_m, S.tiles_n, tm, tn);
+    tile_coords_banded(tile - grp * S.tpg, S.tiles_m, S.tiles_n, tm, tn);
     m0 = static_cast<int64_t>(tm) * BM;
     n0 = static_cast<int64_t>(tn) * BN;
+    Ag = A.group(grp);
+    Bg = B.group(grp);
+    Cg = C.group(grp);
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
@@ -435,7 +458,7 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int64_t row = m0 + wm * 64 + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
-            if (row < M) store_out(C, row, col, acc[a][b][r]);
+            if (row < M) store_out(Cg, row, col, acc[a][b][r]);
           }
         }
     } else {
@@ -475,8 +498,10 @@ __global__ __launch_bounds__(256) void streamk_fixup(int64_t M, int64_t N, Sched
     slot_off[j] = (w * 2 + (((w * S.ipw) / S.nk) == t ? 0 : 1)) * (BM * BN);
   }
   __syncthreads();
+  const int64_t grp = t / S.tpg;
+  const OutDev Cg = C.group(grp);
   int tm, tn;
-  tile_coords_banded(t, S.tiles_m, S.tiles_n, tm, tn);
+  tile_coords_banded(t - grp * S.tpg, S.tiles_m, S.tiles_n, tm, tn);
   const int64_t m0 = static_cast<int64_t>(tm) * BM, n0 = static_cast<int64_t>(tn) * BN;
   for (int e4 = threadIdx.x; e4 < BM * BN / 4; e4 += 256) {
     const int e = e4 * 4;
@@ -487,19 +512,20 @@ __global__ __launch_bounds__(256) void streamk_fixup(int64_t M, int64_t N, Sched
       s += *reinterpret_cast<const floatx4*>(partials + slot_off[j] + e);
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      if (col + q < N) store_out(C, row, col + q, s[q]);
+      if (col + q < N) store_out(Cg, row, col + q, s[q]);
   }
 }
 
 constexpr int64_t kStreamWG = 512;   // two resident 256-thread blocks per CU, 256 CUs
 
-Sched make_sched(int64_t M, int64_t N, int64_t K, int dtype) {
+Sched make_sched(int64_t M, int64_t N, int64_t K, int dtype, int64_t groups = 1) {
   const int ks = dtype == GIST_DTYPE_BF16_IN ? KSH : BK;
   Sched s;
   s.tiles_m = static_cast<int>((M + BM - 1) / BM);
   s.tiles_n = static_cast<int>((N + BN - 1) / BN);
   s.nk = static_cast<int>((K + ks - 1) / ks);
-  const int64_t tiles = static_cast<int64_t>(s.tiles_m) * s.tiles_n;
+  s.tpg = static_cast<int64_t>(s.tiles_m) * s.tiles_n;
+  const int64_t tiles = s.tpg * groups;
   s.T = tiles * s.nk;
   if (tiles >= 4 * kStreamWG) {
     s.ipw = s.nk;   // enough tiles: one whole tile per workgroup
@@ -518,8 +544,8 @@ bool sched_split(const Sched& s) { return s.ipw % s.nk != 0; }
 // fall on a 128 boundary, so that every K step and every tile lies on one
 // side of it and the pointer choice stays uniform.
 bool op_vec_ok(const Operand& o, int64_t R) {
-  if (o.ld0 % 4 || !aligned16(o.p0)) return false;
-  if (o.p1 && (o.ld1 % 4 || !aligned16(o.p1) || o.split % 128)) return false;
+  if (o.ld0 % 4 || !aligned16(o.p0) || o.gs0 % 4) return false;
+  if (o.p1 && (o.ld1 % 4 || !aligned16(o.p1) || o.split % 128 || o.gs1 % 4)) return false;
   if (!o.k_major && R % 4) return false;
   return true;
 }
@@ -554,27 +580,42 @@ void dispatch(hipStream_t st, const Operand& A, const Operand& B, bool av, bool 
 
 }  // namespace
 
-size_t gemm_workspace(int64_t M, int64_t N, int64_t K, int dtype) {
-  if (M <= 0 || N <= 0 || K <= 0) return 0;
+size_t gemm_workspace(int64_t M, int64_t N, int64_t K, int dtype, int64_t groups) {
+  if (M <= 0 || N <= 0 || K <= 0 || groups <= 0) return 0;
   if (dtype == GIST_DTYPE_BF16_IN && gemm_bf16_packed_eligible(M, N, K))
-    return gemm_bf16_packed_workspace(M, N, K);
-  const Sched s = make_sched(M, N, K, dtype);
+    return gemm_bf16_packed_workspace(M, N, K);   // groups run one after another
+  const Sched s = make_sched(M, N, K, dtype, groups);
   if (!sched_split(s)) return 0;
   return static_cast<size_t>(sched_groups(s)) * 2 * BM * BN * sizeof(float);
 }
 
 gist_status gemm(hipStream_t st, int64_t M, int64_t N, int64_t K, const Operand& A,
-                 const Operand& B, const GemmOut& C, int dtype, void* ws, size_t ws_bytes) {
-  if (M <= 0 || N <= 0) return GIST_OK;
-  OutDev c{C.c0, C.c1, C.ldc0, C.ldc1, C.c_split, C.relu ? 1 : 0};
+                 const Operand& B, const GemmOut& C, int dtype, void* ws, size_t ws_bytes,
+                 int64_t ngroups) {
+  if (M <= 0 || N <= 0 || ngroups <= 0) return GIST_OK;
+  OutDev c{C.c0, C.c1, C.ldc0, C.ldc1, C.c_split, C.relu ? 1 : 0, C.gs0, C.gs1};
   if (K <= 0) return set_error(GIST_E_UNSUPPORTED, "gemm: K == 0");
-  if (dtype == GIST_DTYPE_BF16_IN && gemm_bf16_packed_eligible(M, N, K))
-    return gemm_bf16_packed(st, M, N, K, A, B, C, ws, ws_bytes);
+  if (dtype == GIST_DTYPE_BF16_IN && gemm_bf16_packed_eligible(M, N, K)) {
+    // the packed path converts each group's operands; groups run in turn
+    for (int64_t g = 0; g < ngroups; ++g) {
+      Operand ag = A, bg = B;
+      GemmOut cg = C;
+      ag.p0 += g * A.gs0;
+      if (A.p1) ag.p1 += g * A.gs1;
+      bg.p0 += g * B.gs0;
+      if (B.p1) bg.p1 += g * B.gs1;
+      cg.c0 += g * C.gs0;
+      if (C.c1) cg.c1 += g * C.gs1;
+      gist_status s = gemm_bf16_packed(st, M, N, K, ag, bg, cg, ws, ws_bytes);
+      if (s != GIST_OK) return s;
+    }
+    return GIST_OK;
+  }
   if (K > (static_cast<int64_t>(INT32_MAX) - KSH) * BK)
     return set_error(GIST_E_UNSUPPORTED, "gemm: K too large");
-  const Sched S = make_sched(M, N, K, dtype);
+  const Sched S = make_sched(M, N, K, dtype, ngroups);
   const int64_t groups = sched_groups(S);
-  const int64_t tiles = static_cast<int64_t>(S.tiles_m) * S.tiles_n;
+  const int64_t tiles = S.tpg * ngroups;
   if (groups > INT32_MAX || tiles > INT32_MAX)
     return set_error(GIST_E_UNSUPPORTED, "gemm: grid too large");
   float* part = nullptr;
@@ -583,12 +624,14 @@ gist_status gemm(hipStream_t st, int64_t M, int64_t N, int64_t K, const Operand&
     // a tile's iterations span at most ceil(nk / ipw) + 1 workgroups
     if ((S.nk + S.ipw - 1) / S.ipw + 1 > kMaxFixupParts)
       return set_error(GIST_E_UNSUPPORTED, "gemm: too many partial tiles per tile");
-    const size_t need = gemm_workspace(M, N, K, dtype);
+    const size_t need = gemm_workspace(M, N, K, dtype, ngroups);
     if (!ws || ws_bytes < need) return set_error(GIST_E_NOMEM, "gemm: workspace too small");
     part = static_cast<float*>(ws);
   }
-  OpDev a{A.p0, A.p1 ? A.p1 : A.p0, A.ld0, A.p1 ? A.ld1 : A.ld0, A.p1 ? A.split : INT64_MAX};
-  OpDev b{B.p0, B.p1 ? B.p1 : B.p0, B.ld0, B.p1 ? B.ld1 : B.ld0, B.p1 ? B.split : INT64_MAX};
+  OpDev a{A.p0, A.p1 ? A.p1 : A.p0, A.ld0, A.p1 ? A.ld1 : A.ld0, A.p1 ? A.split : INT64_MAX,
+          A.gs0, A.p1 ? A.gs1 : A.gs0};
+  OpDev b{B.p0, B.p1 ? B.p1 : B.p0, B.ld0, B.p1 ? B.ld1 : B.ld0, B.p1 ? B.split : INT64_MAX,
+          B.gs0, B.p1 ? B.gs1 : B.gs0};
   const bool bf = dtype == GIST_DTYPE_BF16_IN;
   const bool av = op_vec_ok(A, M);
   const bool bv = op_vec_ok(B, N);
@@ -603,7 +646,8 @@ gist_status gemm(hipStream_t st, int64_t M, int64_t N, int64_t K, const Operand&
              A.k_major ? 'K' : 'R', B.k_major ? 'K' : 'R', av ? 'v' : 's', bv ? 'v' : 's');
     const double md = static_cast<double>(M), nd = static_cast<double>(N),
                  kd = static_cast<double>(K);
-    ProfScope ps(st, name, 2.0 * md * nd * kd, 4.0 * (md * kd + kd * nd + md * nd));
+    const double gd = static_cast<double>(ngroups);
+    ProfScope ps(st, name, 2.0 * md * nd * kd * gd, 4.0 * (md * kd + kd * nd + md * nd) * gd);
     if (bf) dispatch<true>(st, A, B, av, bv, grid, M, N, K, a, b, c, S, part);
     else dispatch<false>(st, A, B, av, bv, grid, M, N, K, a, b, c, S, part);
   }
@@ -613,7 +657,7 @@ gist_status gemm(hipStream_t st, int64_t M, int64_t N, int64_t K, const Operand&
   }
   if (split) {
     ProfScope ps(st, "gemm_streamk_fixup", 0.0,
-                 4.0 * static_cast<double>(groups) * 2 * BM * BN + 4.0 * M * N);
+                 4.0 * static_cast<double>(groups) * 2 * BM * BN + 4.0 * M * N * ngroups);
     hipLaunchKernelGGL(streamk_fixup, dim3(static_cast<unsigned>(tiles)), dim3(256), 0, st, M, N,
                        S, part, c);
     return check_launch("gemm stream-K fix-up");

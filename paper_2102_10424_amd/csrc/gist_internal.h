@@ -82,6 +82,7 @@ struct Operand {
   int64_t ld0 = 0, ld1 = 0;
   int64_t split = INT64_MAX;
   bool k_major = true;
+  int64_t gs0 = 0, gs1 = 0;   // element offsets of p0 / p1 between GEMM groups
 };
 
 // C (M x N) = act(A (M x K) * B (K x N)), with B given as an N x K operand.
@@ -92,12 +93,15 @@ struct GemmOut {
   int64_t ldc0 = 0, ldc1 = 0;
   int64_t c_split = INT64_MAX;
   bool relu = false;
+  int64_t gs0 = 0, gs1 = 0;   // element offsets of c0 / c1 between GEMM groups
 };
 
-size_t gemm_workspace(int64_t M, int64_t N, int64_t K, int dtype);
+// `groups` independent products of the same shape: group g reads A and B
+// and writes C at the pointers offset by g times their group strides.
+size_t gemm_workspace(int64_t M, int64_t N, int64_t K, int dtype, int64_t groups = 1);
 gist_status gemm(hipStream_t st, int64_t M, int64_t N, int64_t K,
                  const Operand& A, const Operand& B, const GemmOut& C, int dtype,
-                 void* ws, size_t ws_bytes);
+                 void* ws, size_t ws_bytes, int64_t groups = 1);
 
 // dZ[i] = dH[i] * (Hout[i] > 0) over n x w (ld = w).
 gist_status relu_mask(hipStream_t st, int64_t count, const float* dH,

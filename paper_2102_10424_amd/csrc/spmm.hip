@@ -7,8 +7,9 @@
 // of X.  The row's (col, val) pairs are read cooperatively, one per lane, and
 // broadcast within the lane group, so each nonzero's index is loaded once
 // per group instead of once per lane.  Features wider than 64 * VEC are split
-// into column tiles.  Blocks are ordered XCD-major so each XCD's L2 sees a
-// contiguous range of rows (block-ordered graphs keep neighbours close).
+// into column tiles.  Blocks are ordered XCD-major, column tile major: each
+// XCD's L2 sees a contiguous range of rows of one column slab at a time
+// (block-ordered graphs keep neighbours close).
 // No atomics: every output element is written by exactly one lane, and the
 // nonzeros of a row are summed in storage order, so results are bitwise
 // reproducible.
@@ -72,8 +73,11 @@ __global__ __launch_bounds__(256) void spmm_kernel(
   const int grp = lane / LPR;       // row slot inside the wave
   const int gl = lane % LPR;        // lane inside the row group
   const int64_t logical = xcd_remap(blockIdx.x, nblocks);
-  const int64_t rblock = logical / col_tiles;
-  const int ctile = static_cast<int>(logical % col_tiles);
+  // column tile major: an XCD's contiguous range of blocks covers all rows
+  // of one or a few column slabs, whose gathered rows then fit its L2
+  const int64_t rblocks = nblocks / col_tiles;
+  const int ctile = static_cast<int>(logical / rblocks);
+  const int64_t rblock = logical - static_cast<int64_t>(ctile) * rblocks;
   const int64_t row = (rblock * kWaves + wave) * RPW + grp;
   const int c0 = ctile * (LPR * VEC) + gl * VEC;
   const bool active = row < n && c0 < width;
@@ -155,8 +159,11 @@ __global__ __launch_bounds__(256) void spmm_wide_kernel(
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int64_t logical = xcd_remap(blockIdx.x, nblocks);
-  const int64_t rblock = logical / col_tiles;
-  const int ctile = static_cast<int>(logical % col_tiles);
+  // column tile major: an XCD's contiguous range of blocks covers all rows
+  // of one or a few column slabs, whose gathered rows then fit its L2
+  const int64_t rblocks = nblocks / col_tiles;
+  const int ctile = static_cast<int>(logical / rblocks);
+  const int64_t rblock = logical - static_cast<int64_t>(ctile) * rblocks;
   const int64_t row = rblock * kWaves + wave;
   if (row >= n) return;
   const int c0 = ctile * (64 * VEC) + lane * VEC;

@@ -47,6 +47,7 @@ GIST_DTYPE_F32, GIST_DTYPE_BF16_IN = 0, 1
 GIST_ORDER_AUTO, GIST_ORDER_AGG_FIRST, GIST_ORDER_XFORM_FIRST = 0, 1, 2
 GIST_SUBAGG_CHECK_FINITE = 1
 GIST_ADAM_FRESH = 1
+GIST_LAYER_SHARED_INPUT, GIST_LAYER_GROUP_MAJOR_OUT = 1, 2
 
 NORM_BY_NAME = {"gcn": GIST_NORM_GCN_SYM, "sage": GIST_NORM_SAGE_MEAN,
                 "theory": GIST_NORM_THEORY}
@@ -91,7 +92,7 @@ class gist_csr_dev(C.Structure):
 class gist_layer_desc(C.Structure):
     _fields_ = [("kind", C.c_int32), ("act", C.c_int32), ("dtype", C.c_int32),
                 ("order", C.c_int32), ("n", C.c_int64), ("s_in", C.c_int32),
-                ("s_out", C.c_int32)]
+                ("s_out", C.c_int32), ("groups", C.c_int32), ("flags", C.c_uint32)]
 
 
 class gist_slice_set(C.Structure):
@@ -283,9 +284,10 @@ def csr_dev(n, nnz, rowptr, col, val):
     return gist_csr_dev(int(n), int(nnz), _ptr(rowptr), _ptr(col), _ptr(val))
 
 
-def layer_desc(kind, act, n, s_in, s_out, dtype=GIST_DTYPE_F32, order=GIST_ORDER_AUTO):
+def layer_desc(kind, act, n, s_in, s_out, dtype=GIST_DTYPE_F32, order=GIST_ORDER_AUTO,
+               groups=1, flags=0):
     return gist_layer_desc(int(kind), int(act), int(dtype), int(order), int(n), int(s_in),
-                           int(s_out))
+                           int(s_out), int(groups), int(flags))
 
 
 def gist_layer_workspace_size(desc):

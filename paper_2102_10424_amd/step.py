@@ -224,6 +224,122 @@ class SubGCN:
             self.adam(params, M, V, lr, k, fresh)
 
 
+class SubGCNBatch:
+    """m sub-GCNs stepping on one shared mini-batch, as batched layer calls.
+
+    The same arithmetic as m ``SubGCN`` steps on that batch, with one
+    full-width aggregation per layer and grouped GEMMs (the layer
+    descriptor's ``groups``).  The unpartitioned input is read once
+    (``GIST_LAYER_SHARED_INPUT``: Abar X is formed once); hidden activations
+    are n x (m s_l) with sub-GCN i in columns [i s_l, (i+1) s_l); the logits
+    are group-major ([m][n][C]) so each sub-GCN's loss is one call.
+    Parameters and gradients are per layer [m][rows][cols] tensors.
+    """
+
+    def __init__(self, ctx, kind, widths, m, n_cap, dtype=G.GIST_DTYPE_F32, device="cuda"):
+        self.ctx = ctx
+        self.kind = kind
+        self.widths = list(widths)
+        self.L = len(widths) - 1
+        self.m = m
+        self.dtype = dtype
+        self.device = device
+        self.lkind = G.GIST_LAYER_SAGE_MEAN if kind == "sage" else G.GIST_LAYER_GCN
+        self.parts = 2 if kind == "sage" else 1
+        self.n_cap = 0
+        self.ws = torch.empty(0, dtype=torch.uint8, device=device)
+        self._alloc(n_cap)
+        w = self.widths
+        self.dW = [torch.empty(m, self.parts * w[l], w[l + 1], device=device) for l in range(self.L)]
+        self.loss = torch.zeros(m, device=device)
+
+    def _alloc(self, n_cap):
+        w, d, m, L = self.widths, self.device, self.m, self.L
+        self.n_cap = n_cap
+        self.H = [None] + [torch.empty(n_cap, m * w[l + 1], device=d) for l in range(L - 1)]
+        self.agg = [torch.empty(n_cap, w[0], device=d)] + \
+                   [torch.empty(n_cap, m * w[l], device=d) for l in range(1, L)]
+        self.dH = [None] + [torch.empty(n_cap, m * w[l], device=d) for l in range(1, L)]
+        # group-major logits and their gradient: flat, viewed as [m][n][C] per batch
+        self._logits = torch.empty(m * n_cap * w[L], device=d)
+        self._dlogits = torch.empty(m * n_cap * w[L], device=d)
+        self.loss_ws = torch.empty(G.gist_softmax_xent_workspace(n_cap), dtype=torch.uint8,
+                                   device=d)
+
+    def _gm(self, flat, n):
+        C = self.widths[-1]
+        return flat[:self.m * n * C].view(self.m, n, C)
+
+    def _out(self, l, n):
+        """Layer l's output for a batch of n rows (the last one group-major)."""
+        return self.H[l + 1][:n] if l + 1 < self.L else self._gm(self._logits, n)
+
+    def desc(self, l, n):
+        act = G.GIST_ACT_RELU if l < self.L - 1 else G.GIST_ACT_NONE
+        flags = (G.GIST_LAYER_SHARED_INPUT if l == 0 else 0) | \
+                (G.GIST_LAYER_GROUP_MAJOR_OUT if l == self.L - 1 else 0)
+        return G.layer_desc(self.lkind, act, n, self.widths[l], self.widths[l + 1], self.dtype,
+                            G.GIST_ORDER_AUTO, groups=self.m, flags=flags)
+
+    def _workspace(self, n):
+        need = 0
+        for l in range(self.L):
+            f, b = G.gist_layer_workspace_size(self.desc(l, n))
+            need = max(need, f, b)
+        if self.ws.numel() < need:
+            self.ws = torch.empty(need, dtype=torch.uint8, device=self.device)
+        return self.ws
+
+    def logits(self, i):
+        return self._gm(self._logits, self.n)[i]
+
+    def forward(self, batch, params):
+        n = batch.n
+        if n > self.n_cap:
+            raise ValueError("batch larger than the runner's capacity")
+        self.n = n
+        ws = self._workspace(n)
+        H = batch.X
+        for l in range(self.L):
+            out = self._out(l, n)
+            G.gist_gcn_layer_fwd(self.ctx, self.desc(l, n), batch.A, H, params[l],
+                                 self.agg[l][:n], out, ws)
+            H = out
+
+    def loss_and_grad(self, batch):
+        n, C = batch.n, self.widths[-1]
+        logits, dlogits = self._gm(self._logits, n), self._gm(self._dlogits, n)
+        for i in range(self.m):
+            G.gist_softmax_xent(self.ctx, n, C, logits[i], batch.labels, self.loss[i:i + 1],
+                                dlogits[i], self.loss_ws)
+
+    def backward(self, batch, params):
+        n = batch.n
+        ws = self._workspace(n)
+        dout = self._gm(self._dlogits, n)
+        for l in reversed(range(self.L)):
+            Hin = batch.X if l == 0 else self.H[l][:n]
+            dH = self.dH[l][:n] if l > 0 else None
+            G.gist_gcn_layer_bwd(self.ctx, self.desc(l, n), batch.A, batch.A_T, Hin,
+                                 self.agg[l][:n], self._out(l, n), params[l], dout,
+                                 self.dW[l], dH, ws)
+            dout = dH
+
+    def step(self, batch, params, lr, adam=None):
+        """All m sub-GCNs' ``subTrain`` step on the shared batch: SGD, or
+        Adam with ``adam`` = (M, V, step, fresh) over the stacked moments."""
+        self.forward(batch, params)
+        self.loss_and_grad(batch)
+        self.backward(batch, params)
+        for l in range(self.L):
+            if adam is None:
+                G.gist_sgd_update(self.ctx, params[l], self.dW[l], params[l].numel(), lr)
+            else:
+                M, V, k, fresh = adam
+                G.gist_adam_update(self.ctx, params[l], self.dW[l], M[l], V[l], params[l].numel(),
+                                   lr, k, flags=G.GIST_ADAM_FRESH if fresh else 0)
+
+
 class GistModel:
     """Global parameters Theta on the device plus the subGCNs / subAgg calls.
 
@@ -284,10 +400,26 @@ class GistModel:
         self.pending = None    # (slot, buffer) whose subAgg is outstanding
 
     def _slices(self):
-        """[buffer][sub-GCN][layer] slice tensors (SAGE: [W_self; W_neigh] stacked)."""
+        """[buffer][sub-GCN][layer] slice tensors (SAGE: [W_self; W_neigh] stacked).
+
+        Each (buffer, layer) is one [m][rows][cols] tensor and the per
+        sub-GCN slices are views of it, so a batched step can address all m
+        slices of a layer as one array (see ``stacked``)."""
         s = self.slice_widths
-        return [[[torch.empty(self.parts * s[l], s[l + 1], device=self.device)
-                  for l in range(self.L)] for _ in range(self.m)] for _ in range(self.nbuf)]
+        big = [[torch.empty(self.m, self.parts * s[l], s[l + 1], device=self.device)
+                for l in range(self.L)] for _ in range(self.nbuf)]
+        return [[[big[b][l][i] for l in range(self.L)] for i in range(self.m)]
+                for b in range(self.nbuf)]
+
+    def stacked(self, which="params"):
+        """Per layer, the current buffer's [m][rows][cols] tensor of all slices."""
+        bufs = {"params": self.params, "M": self.M, "V": self.V}[which]
+        out = []
+        for l in range(self.L):
+            t = bufs[0][l]
+            out.append(torch.as_strided(t, (self.m,) + tuple(t.shape),
+                                        (t.numel(),) + tuple(t.stride())))
+        return out
 
     def _tables(self, bufs):
         """Device tables of the m slice pointers of every (buffer, layer, part)."""
