@@ -22,6 +22,8 @@ What it computes, each function citing the passage it follows (paper:
   (Algorithm 1) composed from the above, and the whole loop of Algorithm 1
   trained with Adam (the optimizer of the paper's experiments).
 * :mod:`oracle.optim` -- Adam (Kingma & Ba 2015, their Algorithm 1).
+* :mod:`oracle.gat` -- the graph attention layer GIST is also applied to
+  (Section 3; Table 2), single head as Velickovic et al. 2018 define it.
 
 Floating point is fp64 throughout; fp32 inputs are widened exactly.  The
 matrices of the normalised adjacency are the one place where fp32 is part
@@ -35,4 +37,4 @@ two-layer sum decomposition, an independent Adam implementation); none is
 "parity unpinned".
 """
 
-from . import partition, minibatch, layers, gist, optim  # noqa: F401
+from . import partition, minibatch, layers, gist, optim, gat  # noqa: F401
