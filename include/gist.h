@@ -12,6 +12,7 @@
  *   gist_build_minibatch_csr   Cluster mini-batch: induced, normalised  (host)
  *   gist_gather_slice          Theta^(i) = Theta[D_in, D_out]           (device)
  *   gist_gcn_layer_fwd/_bwd    eq. (2) sub-GCN layer, GCN and SAGE-mean (device)
+ *   gist_gat_layer_fwd/_bwd    the graph attention layer GIST also trains (device)
  *   gist_softmax_xent          loss and its gradient                    (device)
  *   gist_sgd_update            one SGD step                             (device)
  *   gist_adam_update           one Adam step (the experiments' optimizer) (device)
@@ -244,6 +245,46 @@ gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* L,
                                const float* H_out, const float* W,
                                const float* dH_out, float* dW, float* dH,
                                void* ws, size_t ws_bytes);
+
+/* ---- graph attention layer ------------------------------------------ */
+
+/* The GAT layer the paper trains with GIST alongside GCN and GraphSAGE
+ * (Section 3, architecture-agnostic training; Table 2).  Single head, as
+ * Velickovic et al. (ICLR 2018) define it:
+ *   P = H W,  u = P a_src,  v = P a_dst,  e_ij = LeakyReLU(u_i + v_j),
+ *   alpha_ij = softmax of e_i. over the pattern N(i) u {i},
+ *   Z_i = sum_j alpha_ij P_j,  H_out = ReLU(Z) (act) or Z.
+ * A sub-GCN's slice of a_src / a_dst is their entries D_{l+1}^(i), the
+ * output features its slice of W keeps.  A is the pattern N(i) u {i}: a
+ * symmetric CSR with ascending columns (the GCN matrix of an undirected
+ * graph has it); its values are ignored.  H (n x s_in), W (s_in x s_out),
+ * P_save / H_out / dH_out (n x s_out) row-major; a_src, a_dst (s_out);
+ * alpha_save (nnz, in A's entry order).  P_save and alpha_save come out of
+ * the forward and go into the backward.  dW is overwritten; dH == NULL
+ * skips the input gradient.  Errors as gist_gcn_layer_fwd. */
+typedef struct gist_gat_desc {
+  int64_t n;       /* rows                                               */
+  int64_t nnz;     /* entries of the pattern                             */
+  int32_t s_in;
+  int32_t s_out;
+  int32_t act;     /* gist_act                                           */
+  int32_t dtype;   /* gist_dtype of the two GEMMs                        */
+  float slope;     /* LeakyReLU slope for negative scores (0.2 in the GAT paper) */
+  int32_t reserved;  /* 0 */
+} gist_gat_desc;
+
+gist_status gist_gat_workspace_size(const gist_gat_desc* D, size_t* fwd_bytes,
+                                    size_t* bwd_bytes);
+gist_status gist_gat_layer_fwd(gist_ctx* ctx, const gist_gat_desc* D, const gist_csr_dev* A,
+                               const float* H, const float* W, const float* a_src,
+                               const float* a_dst, float* P_save, float* alpha_save,
+                               float* H_out, void* ws, size_t ws_bytes);
+gist_status gist_gat_layer_bwd(gist_ctx* ctx, const gist_gat_desc* D, const gist_csr_dev* A,
+                               const float* H, const float* P_save, const float* alpha_save,
+                               const float* H_out, const float* W, const float* a_src,
+                               const float* a_dst, const float* dH_out, float* dW,
+                               float* da_src, float* da_dst, float* dH, void* ws,
+                               size_t ws_bytes);
 
 /* ---- loss (Section 3.1: the sub-GCN output keeps the global width, so the
  *      loss is the usual one) ---------------------------------------- */

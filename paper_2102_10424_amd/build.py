@@ -14,7 +14,7 @@ CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libgist.so")
 BUILD = os.path.join(PKG, "_build")
 
-HIP_SOURCES = ["api.hip", "spmm.hip", "gemm.hip", "gemm_bf16.hip", "elementwise.hip"]
+HIP_SOURCES = ["api.hip", "spmm.hip", "gemm.hip", "gemm_bf16.hip", "elementwise.hip", "gat.hip"]
 HOST_SOURCES = ["host_partition.cpp", "host_minibatch.cpp"]
 
 ARCH = "gfx950"

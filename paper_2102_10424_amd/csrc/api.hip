@@ -418,6 +418,179 @@ extern "C" gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* 
 }
 
 // ---------------------------------------------------------------------------
+// Graph attention layer
+// ---------------------------------------------------------------------------
+
+namespace {
+
+gist_status check_gat(const gist_gat_desc* D, const gist_csr_dev* A, const char* what) {
+  if (!D) return set_error(GIST_E_INVAL, std::string(what) + ": NULL descriptor");
+  if (D->n < 0 || D->nnz < 0 || D->s_in < 1 || D->s_out < 1 || D->reserved != 0)
+    return set_error(GIST_E_INVAL, std::string(what) + ": bad sizes");
+  if (D->act != GIST_ACT_NONE && D->act != GIST_ACT_RELU)
+    return set_error(GIST_E_INVAL, std::string(what) + ": unknown activation");
+  if (D->dtype != GIST_DTYPE_F32 && D->dtype != GIST_DTYPE_BF16_IN)
+    return set_error(GIST_E_INVAL, std::string(what) + ": unknown dtype");
+  if (!std::isfinite(D->slope)) return set_error(GIST_E_INVAL, std::string(what) + ": bad slope");
+  if (D->n > INT32_MAX) return set_error(GIST_E_UNSUPPORTED, std::string(what) + ": n exceeds int32");
+  if (A) {
+    GIST_TRY(check_csr(A, D->n, what));
+    if (A->nnz != D->nnz) return set_error(GIST_E_INVAL, std::string(what) + ": CSR nnz != desc nnz");
+  }
+  return GIST_OK;
+}
+
+// backward workspace: [dZ | u | v | dpre | du | dv | tpos | alpha_t | dP | gemv | gemm]
+struct GatPlan {
+  size_t dz, uv, dpre, dudv, tpos, alpha_t, dp, gemv, gemm;
+  size_t total() const {
+    return align256(dz) + align256(uv) + align256(dpre) + align256(dudv) + align256(tpos) +
+           align256(alpha_t) + align256(dp) + align256(gemv) + gemm;
+  }
+};
+
+GatPlan plan_gat_bwd(const gist_gat_desc* D) {
+  GatPlan p{};
+  const int64_t n = D->n, si = D->s_in, so = D->s_out;
+  p.dz = D->act == GIST_ACT_RELU ? fbytes(n, so) : 0;
+  p.uv = fbytes(2, n);
+  p.dpre = fbytes(1, D->nnz);
+  p.dudv = fbytes(2, n);
+  p.tpos = static_cast<size_t>(D->nnz) * sizeof(int);
+  p.alpha_t = fbytes(1, D->nnz);
+  p.dp = fbytes(n, so);
+  p.gemv = gist::gat_gemv_workspace(n, static_cast<int>(so));
+  p.gemm = std::max(gist::gemm_workspace(si, so, n, D->dtype),
+                    gist::gemm_workspace(n, si, so, D->dtype));
+  return p;
+}
+
+size_t plan_gat_fwd(const gist_gat_desc* D) {
+  return align256(fbytes(2, D->n)) + gist::gemm_workspace(D->n, D->s_out, D->s_in, D->dtype);
+}
+
+}  // namespace
+
+extern "C" gist_status gist_gat_workspace_size(const gist_gat_desc* D, size_t* fwd_bytes,
+                                               size_t* bwd_bytes) {
+  gist::clear_error();
+  GIST_TRY(check_gat(D, nullptr, "gat_workspace_size"));
+  if (fwd_bytes) *fwd_bytes = plan_gat_fwd(D);
+  if (bwd_bytes) *bwd_bytes = plan_gat_bwd(D).total();
+  return GIST_OK;
+}
+
+extern "C" gist_status gist_gat_layer_fwd(gist_ctx* ctx, const gist_gat_desc* D,
+                                          const gist_csr_dev* A, const float* H, const float* W,
+                                          const float* a_src, const float* a_dst, float* P_save,
+                                          float* alpha_save, float* H_out, void* ws,
+                                          size_t ws_bytes) {
+  gist::clear_error();
+  if (!ctx) return set_error(GIST_E_INVAL, "gat_fwd: NULL ctx");
+  gist::ProfBind pb(ctx);
+  GIST_TRY(check_gat(D, A, "gat_fwd"));
+  const int64_t n = D->n, si = D->s_in, so = D->s_out;
+  if (n > 0 && (!H || !W || !a_src || !a_dst || !P_save || !H_out || (D->nnz > 0 && !alpha_save)))
+    return set_error(GIST_E_INVAL, "gat_fwd: NULL pointer");
+  const size_t need = plan_gat_fwd(D);
+  if (ws_bytes < need || (need > 0 && !ws)) return set_error(GIST_E_NOMEM, "gat_fwd: workspace too small");
+  if (n == 0) return GIST_OK;
+  gist::DeviceGuard dg(ctx->device);
+  hipStream_t st = ctx->stream;
+  float* u = static_cast<float*>(ws);
+  float* v = u + n;
+  void* gws = static_cast<char*>(ws) + align256(fbytes(2, n));
+  const size_t gbytes = ws_bytes - align256(fbytes(2, n));
+  // P = H W
+  gist::Operand a;
+  a.p0 = H; a.ld0 = si; a.k_major = true;
+  gist::Operand b;
+  b.p0 = W; b.ld0 = so; b.k_major = false;
+  gist::GemmOut pc;
+  pc.c0 = P_save; pc.ldc0 = so;
+  GIST_TRY(gist::gemm(st, n, so, si, a, b, pc, D->dtype, gws, gbytes));
+  GIST_TRY(gist::gat_scores(st, n, static_cast<int>(so), P_save, so, a_src, a_dst, u, v));
+  GIST_TRY(gist::gat_softmax(st, n, D->nnz, A->rowptr, A->col, u, v, D->slope, alpha_save));
+  // H_out = act(A_alpha P)
+  return gist::spmm(st, n, D->nnz, A->rowptr, A->col, alpha_save, P_save, so, int(so), H_out, so,
+                    nullptr, 0, D->act == GIST_ACT_RELU);
+}
+
+extern "C" gist_status gist_gat_layer_bwd(gist_ctx* ctx, const gist_gat_desc* D,
+                                          const gist_csr_dev* A, const float* H,
+                                          const float* P_save, const float* alpha_save,
+                                          const float* H_out, const float* W, const float* a_src,
+                                          const float* a_dst, const float* dH_out, float* dW,
+                                          float* da_src, float* da_dst, float* dH, void* ws,
+                                          size_t ws_bytes) {
+  gist::clear_error();
+  if (!ctx) return set_error(GIST_E_INVAL, "gat_bwd: NULL ctx");
+  gist::ProfBind pb(ctx);
+  GIST_TRY(check_gat(D, A, "gat_bwd"));
+  const int64_t n = D->n, si = D->s_in, so = D->s_out;
+  const bool relu = D->act == GIST_ACT_RELU;
+  if (!dW || !W || !a_src || !a_dst || !da_src || !da_dst)
+    return set_error(GIST_E_INVAL, "gat_bwd: NULL pointer");
+  if (n > 0 && (!H || !P_save || !dH_out || (relu && !H_out) || (D->nnz > 0 && !alpha_save)))
+    return set_error(GIST_E_INVAL, "gat_bwd: NULL pointer");
+  const GatPlan p = plan_gat_bwd(D);
+  if (ws_bytes < p.total() || (p.total() > 0 && !ws))
+    return set_error(GIST_E_NOMEM, "gat_bwd: workspace too small");
+  gist::DeviceGuard dg(ctx->device);
+  hipStream_t st = ctx->stream;
+  if (n == 0) {   // empty batch: zero gradients
+    GIST_TRY(gist::fill_zero(st, dW, si * so));
+    GIST_TRY(gist::fill_zero(st, da_src, so));
+    return gist::fill_zero(st, da_dst, so);
+  }
+  char* c = static_cast<char*>(ws);
+  auto take = [&](size_t bytes) { char* r = c; c += align256(bytes); return r; };
+  float* dZbuf = reinterpret_cast<float*>(take(p.dz));
+  float* u = reinterpret_cast<float*>(take(p.uv));
+  float* v = u + n;
+  float* dpre = reinterpret_cast<float*>(take(p.dpre));
+  float* du = reinterpret_cast<float*>(take(p.dudv));
+  float* dv = du + n;
+  int* tpos = reinterpret_cast<int*>(take(p.tpos));
+  float* alpha_t = reinterpret_cast<float*>(take(p.alpha_t));
+  float* dP = reinterpret_cast<float*>(take(p.dp));
+  float* part = reinterpret_cast<float*>(take(p.gemv));
+  void* gws = c;
+  const float* dZ = dH_out;
+  if (relu) {
+    GIST_TRY(gist::relu_mask(st, n * so, dH_out, H_out, dZbuf));
+    dZ = dZbuf;
+  }
+  const int s = static_cast<int>(so);
+  GIST_TRY(gist::gat_scores(st, n, s, P_save, so, a_src, a_dst, u, v));
+  GIST_TRY(gist::gat_edge_grad(st, n, D->nnz, s, A->rowptr, A->col, alpha_save, dZ, so, P_save, so,
+                               u, v, D->slope, dpre, du));
+  GIST_TRY(gist::gat_mirror(st, n, D->nnz, A->rowptr, A->col, tpos));
+  GIST_TRY(gist::gat_mirror_sums(st, n, D->nnz, A->rowptr, tpos, dpre, alpha_save, dv, alpha_t));
+  // dP = A_alpha^T dZ (the pattern is symmetric: row j lists the i with alpha_ij)
+  GIST_TRY(gist::spmm(st, n, D->nnz, A->rowptr, A->col, alpha_t, dZ, so, s, dP, so, nullptr, 0,
+                      false));
+  GIST_TRY(gist::gat_gemv_t(st, n, s, P_save, so, du, dv, da_src, da_dst, part));
+  GIST_TRY(gist::gat_rank2(st, n, s, dP, so, du, dv, a_src, a_dst));
+  // dW = H^T dP; dH = dP W^T
+  gist::Operand a;
+  a.p0 = H; a.ld0 = si; a.k_major = false;
+  gist::Operand g;
+  g.p0 = dP; g.ld0 = so; g.k_major = false;
+  gist::GemmOut wout;
+  wout.c0 = dW; wout.ldc0 = so;
+  GIST_TRY(gist::gemm(st, si, so, n, a, g, wout, D->dtype, gws, p.gemm));
+  if (!dH) return GIST_OK;
+  gist::Operand a2;
+  a2.p0 = dP; a2.ld0 = so; a2.k_major = true;
+  gist::Operand b2;
+  b2.p0 = W; b2.ld0 = so; b2.k_major = true;
+  gist::GemmOut o2;
+  o2.c0 = dH; o2.ldc0 = si;
+  return gist::gemm(st, n, si, so, a2, b2, o2, D->dtype, gws, p.gemm);
+}
+
+// ---------------------------------------------------------------------------
 // Loss, gather, SGD, subAgg
 // ---------------------------------------------------------------------------
 

@@ -119,6 +119,25 @@ gist_status fill_zero(hipStream_t st, float* p, int64_t count);
 gist_status subagg_gather(hipStream_t st, float* Wg, int64_t rows, int64_t cols, int64_t ldg,
                           int m, const gist_slice_set* done, const gist_slice_set* next, double bytes);
 gist_status sgd(hipStream_t st, float* W, const float* dW, int64_t n, float lr);
+// graph attention steps (gat.hip)
+gist_status gat_scores(hipStream_t st, int64_t n, int s, const float* P, int64_t ldp,
+                       const float* a_src, const float* a_dst, float* u, float* v);
+gist_status gat_softmax(hipStream_t st, int64_t n, int64_t nnz, const int* rowptr, const int* col,
+                        const float* u, const float* v, float slope, float* alpha);
+gist_status gat_edge_grad(hipStream_t st, int64_t n, int64_t nnz, int s, const int* rowptr,
+                          const int* col, const float* alpha, const float* dZ, int64_t ldz,
+                          const float* P, int64_t ldp, const float* u, const float* v, float slope,
+                          float* dpre, float* du);
+gist_status gat_mirror(hipStream_t st, int64_t n, int64_t nnz, const int* rowptr, const int* col,
+                       int* tpos);
+gist_status gat_mirror_sums(hipStream_t st, int64_t n, int64_t nnz, const int* rowptr,
+                            const int* tpos, const float* dpre, const float* alpha, float* dv,
+                            float* alpha_t);
+gist_status gat_rank2(hipStream_t st, int64_t n, int s, float* dP, int64_t ld, const float* du,
+                      const float* dv, const float* a_src, const float* a_dst);
+size_t gat_gemv_workspace(int64_t n, int s);
+gist_status gat_gemv_t(hipStream_t st, int64_t n, int s, const float* P, int64_t ldp,
+                       const float* du, const float* dv, float* da_src, float* da_dst, float* part);
 gist_status adam(hipStream_t st, float* W, const float* dW, float* m, float* v, int64_t n,
                  float step_size, float inv_sqrt_bc2, float beta1, float beta2, float eps,
                  bool fresh);

@@ -57,6 +57,7 @@ EXPORTED = (
     "gist_last_error", "gist_status_str", "gist_create", "gist_destroy",
     "gist_set_stream", "gist_partition", "gist_build_minibatch_csr",
     "gist_layer_workspace_size", "gist_gcn_layer_fwd", "gist_gcn_layer_bwd",
+    "gist_gat_workspace_size", "gist_gat_layer_fwd", "gist_gat_layer_bwd",
     "gist_softmax_xent_workspace", "gist_softmax_xent", "gist_gather_slice",
     "gist_sgd_update", "gist_adam_update", "gist_subagg", "gist_partition_inverse",
     "gist_subagg_gather",
@@ -95,6 +96,12 @@ class gist_layer_desc(C.Structure):
                 ("s_out", C.c_int32), ("groups", C.c_int32), ("flags", C.c_uint32)]
 
 
+class gist_gat_desc(C.Structure):
+    _fields_ = [("n", C.c_int64), ("nnz", C.c_int64), ("s_in", C.c_int32), ("s_out", C.c_int32),
+                ("act", C.c_int32), ("dtype", C.c_int32), ("slope", C.c_float),
+                ("reserved", C.c_int32)]
+
+
 class gist_slice_set(C.Structure):
     _fields_ = [("row_rank", C.c_void_p), ("row_offs", C.c_void_p), ("col_rank", C.c_void_p),
                 ("col_offs", C.c_void_p), ("slices", C.c_void_p), ("ld", C.c_int64)]
@@ -116,6 +123,12 @@ _sigs = {
                                    C.c_float, C.c_int64, C.c_uint32]),
     "gist_subagg_gather": (C.c_int, [_P, _P, C.c_int64, C.c_int64, C.c_int64, C.c_int32,
                                      C.POINTER(gist_slice_set), C.POINTER(gist_slice_set)]),
+    "gist_gat_workspace_size": (C.c_int, [C.POINTER(gist_gat_desc), C.POINTER(C.c_size_t),
+                                          C.POINTER(C.c_size_t)]),
+    "gist_gat_layer_fwd": (C.c_int, [_P, C.POINTER(gist_gat_desc), C.POINTER(gist_csr_dev)] +
+                           [_P] * 8 + [C.c_size_t]),
+    "gist_gat_layer_bwd": (C.c_int, [_P, C.POINTER(gist_gat_desc), C.POINTER(gist_csr_dev)] +
+                           [_P] * 13 + [C.c_size_t]),
     "gist_last_error": (C.c_char_p, []),
     "gist_status_str": (C.c_char_p, [C.c_int]),
     "gist_create": (C.c_int, [C.c_int, _P, C.POINTER(_P)]),
@@ -335,6 +348,32 @@ def gist_adam_update(ctx, W, dW, m, v, n, lr, step, beta1=0.9, beta2=0.999, eps=
     _check(_lib.gist_adam_update(ctx.handle, _ptr(W), _ptr(dW), _ptr(m), _ptr(v), int(n),
                                  float(lr), float(beta1), float(beta2), float(eps), int(step),
                                  int(flags)))
+
+
+def gat_desc(n, nnz, s_in, s_out, act, dtype=GIST_DTYPE_F32, slope=0.2):
+    return gist_gat_desc(int(n), int(nnz), int(s_in), int(s_out), int(act), int(dtype),
+                         float(slope), 0)
+
+
+def gist_gat_workspace_size(desc):
+    f, b = C.c_size_t(), C.c_size_t()
+    _check(_lib.gist_gat_workspace_size(C.byref(desc), C.byref(f), C.byref(b)))
+    return int(f.value), int(b.value)
+
+
+def gist_gat_layer_fwd(ctx, desc, A, H, W, a_src, a_dst, P_save, alpha_save, H_out, ws):
+    _check(_lib.gist_gat_layer_fwd(ctx.handle, C.byref(desc), C.byref(A), _ptr(H), _ptr(W),
+                                   _ptr(a_src), _ptr(a_dst), _ptr(P_save), _ptr(alpha_save),
+                                   _ptr(H_out), _ptr(ws), 0 if ws is None else ws.numel()))
+
+
+def gist_gat_layer_bwd(ctx, desc, A, H, P_save, alpha_save, H_out, W, a_src, a_dst, dH_out, dW,
+                       da_src, da_dst, dH, ws):
+    _check(_lib.gist_gat_layer_bwd(ctx.handle, C.byref(desc), C.byref(A), _ptr(H), _ptr(P_save),
+                                   _ptr(alpha_save), _ptr(H_out), _ptr(W), _ptr(a_src),
+                                   _ptr(a_dst), _ptr(dH_out), _ptr(dW), _ptr(da_src),
+                                   _ptr(da_dst), _ptr(dH), _ptr(ws),
+                                   0 if ws is None else ws.numel()))
 
 
 def slice_set(row_rank, row_offs, col_rank, col_offs, slice_ptrs, ld):

@@ -1,0 +1,129 @@
+"""GPU parity of the graph attention layer against the fp64 oracle
+(oracle.gat, Velickovic et al.'s single-head layer that the paper trains
+with GIST): the transform P, the attention alpha of every entry and the
+output, then dW, da_src, da_dst and dH with the backward fed the oracle's
+forward values (so every ReLU / LeakyReLU decision comes from the same
+numbers), normwise within 1e-4 (fp32) or 2e-2 (bf16-input GEMMs).  Cases
+span several graphs, ragged widths, both activations, a row longer than the
+kernel's register-kept 512 entries (a hub), and bitwise determinism."""
+
+import numpy as np
+import pytest
+
+from gist_synth.graphs import Graph, _csr_from_undirected, chung_lu, erdos_renyi, sbm
+from oracle import gat as GA
+from oracle import minibatch as MB
+
+from gpu_util import BF16_TOL, FP32_TOL, csr_to_dev, log, relerr, to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def G():
+    from paper_2102_10424_amd import gist
+    return gist
+
+
+@pytest.fixture(scope="module")
+def ctx(G):
+    return G.Context(0)
+
+
+def _hub_graph():
+    """An ER graph plus one node joined to 700 others (a 701-entry row)."""
+    base = erdos_renyi(1000, 3000, seed=9)
+    rng = np.random.default_rng(9)
+    rows = np.repeat(np.arange(base.n), np.diff(base.rowptr))
+    keep = rows < base.col
+    u, v = list(rows[keep]), list(base.col[keep])
+    hub = 0
+    others = rng.choice(np.arange(1, base.n), 700, replace=False)
+    u += [hub] * 700
+    v += list(others)
+    rp, col = _csr_from_undirected(base.n, u, v)
+    return Graph(base.n, rp, col, np.array([0, base.n], np.int64), np.arange(base.n, dtype=np.int32))
+
+
+GRAPHS = {"er300": erdos_renyi(300, 900, seed=5), "sbm1500": sbm(1500, 10, 30.0, 0.9, seed=7),
+          "cl2000": chung_lu(2000, 2.5, 5.0, seed=6), "hub1000": _hub_graph()}
+
+CASES = [
+    # graph, s_in, s_out, act, dtype
+    ("er300", 40, 56, 1, "f32"),
+    ("er300", 64, 7, 0, "f32"),
+    ("sbm1500", 130, 260, 1, "f32"),
+    ("cl2000", 33, 17, 1, "f32"),
+    ("hub1000", 48, 64, 1, "f32"),
+    ("sbm1500", 600, 520, 1, "bf16"),
+]
+
+
+def _run(G, ctx, gname, si, so, act, dt, seed=0):
+    import torch
+    g = GRAPHS[gname]
+    csr = MB.build(g, None, "gcn")        # pattern of A + I
+    n, nnz = csr["n"], csr["nnz"]
+    rng = np.random.default_rng(seed + si)
+    H = rng.standard_normal((n, si)).astype(np.float32)
+    W = (rng.standard_normal((si, so)) / np.sqrt(si)).astype(np.float32)
+    a1 = (rng.standard_normal(so) * 0.3).astype(np.float32)
+    a2 = (rng.standard_normal(so) * 0.3).astype(np.float32)
+    dHo = rng.standard_normal((n, so)).astype(np.float32)
+    slope = 0.2
+    f = GA.gat_forward(csr, H, W, a1, a2, act == 1, slope)
+    b = GA.gat_backward(csr, H, f, W, a1, a2, dHo, act == 1, slope)
+    A, keep = csr_to_dev(csr)
+    dtype = G.GIST_DTYPE_BF16_IN if dt == "bf16" else G.GIST_DTYPE_F32
+    desc = G.gat_desc(n, nnz, si, so, act, dtype, slope)
+    fws, bws = G.gist_gat_workspace_size(desc)
+    ws = torch.empty(max(fws, bws, 1), dtype=torch.uint8, device="cuda")
+    Hd, Wd, a1d, a2d = to_dev(H), to_dev(W), to_dev(a1), to_dev(a2)
+    P = torch.empty(n, so, device="cuda")
+    alpha = torch.empty(max(nnz, 1), device="cuda")
+    Ho = torch.empty(n, so, device="cuda")
+    G.gist_gat_layer_fwd(ctx, desc, A, Hd, Wd, a1d, a2d, P, alpha, Ho, ws)
+    got = dict(P=to_host(P), alpha=to_host(alpha)[:nnz], H_out=to_host(Ho))
+    # backward on the oracle's forward values
+    dW = torch.empty(si, so, device="cuda")
+    da1 = torch.empty(so, device="cuda")
+    da2 = torch.empty(so, device="cuda")
+    dH = torch.empty(n, si, device="cuda")
+    G.gist_gat_layer_bwd(ctx, desc, A, Hd, to_dev(f["P"].astype(np.float32)),
+                         to_dev(f["alpha"].astype(np.float32)), to_dev(f["H_out"].astype(np.float32)),
+                         Wd, a1d, a2d, to_dev(dHo), dW, da1, da2, dH, ws)
+    got.update(dW=to_host(dW), da_src=to_host(da1), da_dst=to_host(da2), dH=to_host(dH))
+    want = dict(P=f["P"], alpha=f["alpha"], H_out=f["H_out"], dW=b["dW"], da_src=b["da_src"],
+                da_dst=b["da_dst"], dH=b["dH"])
+    return got, want
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"{c[0]}-{c[1]}x{c[2]}-a{c[3]}-{c[4]}" for c in CASES])
+def test_gat_layer_matches_oracle(G, ctx, case):
+    gname, si, so, act, dt = case
+    log(f"gat {case}")
+    got, want = _run(G, ctx, gname, si, so, act, dt)
+    tol = BF16_TOL if dt == "bf16" else FP32_TOL
+    for k in want:
+        e = relerr(got[k], want[k])
+        log(f"  {k}: {e:.3e}")
+        assert e <= tol, (k, e)
+
+
+def test_gat_bitwise_deterministic(G, ctx):
+    a, _ = _run(G, ctx, "sbm1500", 130, 260, 1, "f32", seed=3)
+    b, _ = _run(G, ctx, "sbm1500", 130, 260, 1, "f32", seed=3)
+    for k in a:
+        assert np.array_equal(a[k].view(np.uint32), b[k].view(np.uint32)), k
+
+
+def test_gat_errors(G, ctx):
+    import torch
+    t = torch.zeros(64, device="cuda")
+    A = G.csr_dev(4, 4, torch.arange(5, dtype=torch.int32, device="cuda"),
+                  torch.arange(4, dtype=torch.int32, device="cuda"), t)
+    with pytest.raises(G.GistError) as e:    # desc nnz disagrees with the CSR
+        G.gist_gat_layer_fwd(ctx, G.gat_desc(4, 5, 2, 2, 1), A, t, t, t, t, t, t, t, None)
+    assert e.value.status == G.GIST_E_INVAL
+    with pytest.raises(G.GistError):
+        G.gist_gat_workspace_size(G.gat_desc(4, 4, 2, 2, 7))

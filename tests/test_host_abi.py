@@ -147,3 +147,45 @@ def test_minibatch_csr_errors():
         assert e.value.status == G.GIST_E_INVAL
     with pytest.raises(G.GistError):
         G.gist_build_minibatch_csr(g, None, 7)
+
+
+def _prototypes():
+    """name -> list of parameter texts, for every function the header declares."""
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    out = {}
+    for m in re.finditer(r"\b(gist_[a-z_0-9]+)\s*\(([^;{]*?)\)\s*;", text):
+        params = [p.strip() for p in m.group(2).split(",")]
+        out[m.group(1)] = [] if params == ["void"] else params
+    return out
+
+
+def _ctype_kind(t):
+    import ctypes as C
+    if t is None:
+        return None
+    if t in (C.c_void_p, C.c_char_p) or getattr(t, "_type_", None) is not None and hasattr(t, "contents"):
+        return "ptr"
+    return {C.c_int64: "i64", C.c_int32: "i32", C.c_uint32: "u32", C.c_uint64: "u64",
+            C.c_float: "f32", C.c_double: "f64", C.c_size_t: "u64"}.get(t, repr(t))
+
+
+def _param_kind(p):
+    if "*" in p:
+        return "ptr"
+    base = p.rsplit(" ", 1)[0].replace("const ", "").strip()
+    if base.startswith("gist_"):      # the header's enums are int-sized
+        return "i32"
+    return {"int64_t": "i64", "int32_t": "i32", "int": "i32", "uint32_t": "u32", "uint64_t": "u64",
+            "float": "f32", "double": "f64", "size_t": "u64", "gist_status": "i32"}[base]
+
+
+def test_binding_signatures_match_header():
+    """Every ctypes prototype of the binding has the header's arity and
+    parameter kinds (pointer, width and signedness of integers, float)."""
+    protos = _prototypes()
+    assert sorted(protos) == declared_functions()
+    for name, params in protos.items():
+        f = getattr(G._lib, name)
+        got = [_ctype_kind(t) for t in f.argtypes]
+        want = [_param_kind(p) for p in params]
+        assert got == want, (name, got, want)
