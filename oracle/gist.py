@@ -2,9 +2,21 @@
 
 A model is a list of per-layer parameters: for GCN layer l a matrix
 Theta_l (d_l x d_{l+1}); for GraphSAGE-mean a pair (Theta_self, Theta_neigh)
-of that shape.  Hidden layers use ReLU, the last layer the identity, the
-loss is mean softmax cross-entropy (Section 3.1: the sub-GCN output has the
-global output dimension, so the loss is unchanged).
+of that shape; for GAT a triple (Theta_l, a_src, a_dst) with the attention
+vectors of length d_{l+1} (``oracle.gat``).  Hidden layers use ReLU, the
+last layer the identity, the loss is mean softmax cross-entropy (Section
+3.1: the sub-GCN output has the global output dimension, so the loss is
+unchanged).
+
+GAT under GIST (Section 3: the method applies to GAT unchanged; the paper
+trains GAT models with it, Table 2).  A sub-GCN's attention vectors of
+layer l are their entries D_{l+1}^(i), the output features its Theta slice
+keeps.  The output layer's attention vectors live in the unpartitioned
+output dimension, so every sub-GCN trains its own full copy; the paper does
+not say how subAgg combines them.  The reading here is that of independent
+subnet training, which GIST extends: a parameter that no partition splits
+becomes the mean of the m trained copies (for one sub-GCN, the copy itself).
+With Adam's "carry" policy its moments are averaged the same way.
 
 ``sub_gcn_step`` is ``subTrain`` (Section 3.2): forward through eq. (2) on
 one mini-batch, loss, backward, one SGD step.  ``gist_round`` is one pass of
@@ -24,8 +36,21 @@ what becomes of Adam's moments at ``subAgg``; two readings are provided:
 
 import numpy as np
 
+from . import gat as _g
 from . import layers as _l
 from . import optim as _o
+
+GAT_SLOPE = 0.2    # LeakyReLU slope of the attention scores (the GAT paper's)
+
+
+def _parts(kind, p):
+    """A layer's parameters as a tuple of arrays."""
+    return (p,) if kind == "gcn" else tuple(p)
+
+
+def _pack(kind, arrs):
+    arrs = list(arrs)
+    return arrs[0] if kind == "gcn" else tuple(arrs)
 
 
 def forward(kind, csr, X, params):
@@ -37,6 +62,9 @@ def forward(kind, csr, X, params):
         act = l < L - 1
         if kind == "gcn":
             rec = _l.gcn_forward(csr, H[-1], params[l], act)
+        elif kind == "gat":
+            W, a1, a2 = params[l]
+            rec = _g.gat_forward(csr, H[-1], W, a1, a2, act, GAT_SLOPE)
         else:
             rec = _l.sage_forward(csr, H[-1], params[l][0], params[l][1], act)
         recs.append(rec)
@@ -56,6 +84,11 @@ def backward(kind, csr, H, recs, params, dlogits):
             b = _l.gcn_backward(csr, H[l], recs[l], params[l], dH, act,
                                 need_dH=l > 0)
             grads[l] = b["dW"]
+        elif kind == "gat":
+            W, a1, a2 = params[l]
+            b = _g.gat_backward(csr, H[l], recs[l], W, a1, a2, dH, act, GAT_SLOPE,
+                                need_dH=l > 0)
+            grads[l] = (b["dW"], b["da_src"], b["da_dst"])
         else:
             b = _l.sage_backward(csr, H[l], recs[l], params[l][0], params[l][1],
                                  dH, act, need_dH=l > 0)
@@ -66,10 +99,8 @@ def backward(kind, csr, H, recs, params, dlogits):
 
 
 def sgd_params(kind, params, grads, lr):
-    if kind == "gcn":
-        return [_l.sgd(w, g, lr) for w, g in zip(params, grads)]
-    return [(_l.sgd(w[0], g[0], lr), _l.sgd(w[1], g[1], lr))
-            for w, g in zip(params, grads)]
+    return [_pack(kind, (_l.sgd(w, g, lr) for w, g in zip(_parts(kind, p), _parts(kind, gr))))
+            for p, gr in zip(params, grads)]
 
 
 def sub_gcn_step(kind, csr, X, labels, params, lr):
@@ -103,19 +134,55 @@ def slice_indices(partitions, L, i):
     return out
 
 
+def _vec_rows(kind):
+    """Which parts of a layer are vectors over the output features (GAT's a)."""
+    return (False, True, True) if kind == "gat" else (False,) * (1 if kind == "gcn" else 2)
+
+
 def gather_params(kind, theta, sl):
-    if kind == "gcn":
-        return [_l.gather_slice(theta[l], r, c) for l, (r, c) in enumerate(sl)]
-    return [(_l.gather_slice(theta[l][0], r, c), _l.gather_slice(theta[l][1], r, c))
-            for l, (r, c) in enumerate(sl)]
+    """Sub-GCN slices of every layer: rows D_l, columns D_{l+1} of each
+    matrix; entries D_{l+1} of each attention vector."""
+    out = []
+    for l, (r, c) in enumerate(sl):
+        arrs = []
+        for x, vec in zip(_parts(kind, theta[l]), _vec_rows(kind)):
+            arrs.append(_l.gather_slice(x[None, :], None, c)[0] if vec else
+                        _l.gather_slice(x, r, c))
+        out.append(_pack(kind, arrs))
+    return out
 
 
 def scatter_params(kind, theta, sl, params):
-    if kind == "gcn":
-        return [_l.subagg(theta[l], r, c, params[l]) for l, (r, c) in enumerate(sl)]
-    return [(_l.subagg(theta[l][0], r, c, params[l][0]),
-             _l.subagg(theta[l][1], r, c, params[l][1]))
-            for l, (r, c) in enumerate(sl)]
+    """Replacement ``subAgg`` of one sub-GCN's slices.  Parts that no
+    partition splits (GAT's output-layer attention vectors, c = None) are
+    left to :func:`sub_agg`, which averages them."""
+    out = []
+    for l, (r, c) in enumerate(sl):
+        arrs = []
+        for x, y, vec in zip(_parts(kind, theta[l]), _parts(kind, params[l]), _vec_rows(kind)):
+            if not vec:
+                arrs.append(_l.subagg(x, r, c, y))
+            elif c is None:
+                arrs.append(x)
+            else:
+                arrs.append(_l.subagg(x[None, :], None, c, y[None, :])[0])
+        out.append(_pack(kind, arrs))
+    return out
+
+
+def sub_agg(kind, theta, sls, trained):
+    """``subAgg`` of a round: every sub-GCN's slices replace their entries of
+    ``theta`` (``sls[i]``, ``trained[i]``); GAT's output-layer attention
+    vectors become the mean of the m trained copies."""
+    for sl, p in zip(sls, trained):
+        theta = scatter_params(kind, theta, sl, p)
+    if kind == "gat":
+        L = len(theta)
+        W = theta[L - 1][0]
+        a1 = np.mean([_l.as_f64(p[L - 1][1]) for p in trained], axis=0)
+        a2 = np.mean([_l.as_f64(p[L - 1][2]) for p in trained], axis=0)
+        theta = list(theta[:L - 1]) + [(W, a1, a2)]
+    return theta
 
 
 def gist_round(kind, theta, partitions, batches, lr, zeta=1):
@@ -139,30 +206,23 @@ def gist_round(kind, theta, partitions, batches, lr, zeta=1):
             li.append(st["loss"])
         trained.append(p)
         losses.append(li)
-    new = theta
-    for i in range(m):
-        new = scatter_params(kind, new, slice_indices(partitions, L, i), trained[i])
+    new = sub_agg(kind, theta, [slice_indices(partitions, L, i) for i in range(m)], trained)
     return new, trained, losses
 
 
 def zeros_like_params(kind, params):
-    if kind == "gcn":
-        return [np.zeros(np.shape(w)) for w in params]
-    return [(np.zeros(np.shape(a)), np.zeros(np.shape(b))) for a, b in params]
+    return [_pack(kind, (np.zeros(np.shape(x)) for x in _parts(kind, p))) for p in params]
 
 
 def adam_params(kind, params, grads, M, V, step, lr):
-    """Adam on every parameter matrix with its own moments."""
-    if kind == "gcn":
-        out = [_o.adam(w, g, mm, vv, step, lr) for w, g, mm, vv in zip(params, grads, M, V)]
-        return [o[0] for o in out], [o[1] for o in out], [o[2] for o in out]
+    """Adam on every parameter array with its own moments."""
     P, M1, V1 = [], [], []
-    for (ws, wn), (gs, gn), (ms, mn), (vs, vn) in zip(params, grads, M, V):
-        a = _o.adam(ws, gs, ms, vs, step, lr)
-        b = _o.adam(wn, gn, mn, vn, step, lr)
-        P.append((a[0], b[0]))
-        M1.append((a[1], b[1]))
-        V1.append((a[2], b[2]))
+    for p, g, mm, vv in zip(params, grads, M, V):
+        out = [_o.adam(*a, step, lr) for a in zip(_parts(kind, p), _parts(kind, g),
+                                                 _parts(kind, mm), _parts(kind, vv))]
+        P.append(_pack(kind, (o[0] for o in out)))
+        M1.append(_pack(kind, (o[1] for o in out)))
+        V1.append(_pack(kind, (o[2] for o in out)))
     return P, M1, V1
 
 
@@ -210,17 +270,15 @@ def gist_train(kind, theta, rounds, zeta, lr, partitions, batches, policy="carry
                 li.append(st["loss"])
             trained.append((sl, p, mm, vv))
             lt.append(li)
-        for sl, p, mm, vv in trained:
-            theta = scatter_params(kind, theta, sl, p)
-            if policy == "carry":
-                Mg = scatter_params(kind, Mg, sl, mm)
-                Vg = scatter_params(kind, Vg, sl, vv)
+        sls = [tr[0] for tr in trained]
+        theta = sub_agg(kind, theta, sls, [tr[1] for tr in trained])
+        if policy == "carry":
+            Mg = sub_agg(kind, Mg, sls, [tr[2] for tr in trained])
+            Vg = sub_agg(kind, Vg, sls, [tr[3] for tr in trained])
         losses.append(lt)
     return theta, Mg, Vg, losses
 
 
 def as_float32_params(kind, params):
-    if kind == "gcn":
-        return [np.asarray(w, dtype=np.float32) for w in params]
-    return [(np.asarray(a, dtype=np.float32), np.asarray(b, dtype=np.float32))
-            for a, b in params]
+    return [_pack(kind, (np.asarray(x, dtype=np.float32) for x in _parts(kind, p)))
+            for p in params]
