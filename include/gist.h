@@ -18,6 +18,7 @@
  *   gist_adam_update           one Adam step (the experiments' optimizer) (device)
  *   gist_subagg                subAgg: Theta[D_in, D_out] <- Theta^(i)  (device)
  *   gist_subagg_gather         subAgg of one round + gather of the next (device)
+ *   gist_subagg_mean           subAgg of an unsplit parameter: mean of copies (device)
  *
  * Conventions
  *  - Every matrix is row-major fp32 with the leading dimension stated.
@@ -349,6 +350,22 @@ gist_status gist_adam_update(gist_ctx* ctx, float* W, const float* dW, float* m,
 gist_status gist_subagg(gist_ctx* ctx, float* Wg, int64_t ldg, const int32_t* rows,
                         int32_t nr, const int32_t* cols, int32_t nc,
                         const float* Ws, int64_t lds, uint32_t flags);
+
+/* subAgg of a parameter that no partition splits: a GAT output layer's
+ * attention vectors live in the unpartitioned class dimension, so every
+ * sub-GCN trains a full copy.  The paper is silent on how those copies are
+ * combined; this is the rule of independent subnet training, which GIST
+ * extends -- the mean of the m trained copies:
+ *   Wg[r][c] = (sum_{i<m} slices[i][r * lds + c]) / m,  r < rows, c < cols,
+ * summed in double in the order i = 0, 1, ..., m-1, divided in double and
+ * rounded once to fp32 (bitwise reproducible).  `slices` is a device array
+ * of m device pointers, each to a rows x cols row-major block with row
+ * stride lds; Wg is row-major with stride ldg and must not overlap them.
+ * Errors: GIST_E_INVAL for negative sizes, m < 1, ldg < cols, lds < cols
+ * or NULL pointers when rows * cols > 0. */
+gist_status gist_subagg_mean(gist_ctx* ctx, float* Wg, int64_t rows, int64_t cols,
+                             int64_t ldg, int32_t m, const float* const* slices,
+                             int64_t lds);
 
 /* ---- subAgg of one round fused with the gather of the next ---------- */
 

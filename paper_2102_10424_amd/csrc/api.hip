@@ -645,6 +645,20 @@ extern "C" gist_status gist_sgd_update(gist_ctx* ctx, float* W, const float* dW,
   return gist::sgd(ctx->stream, W, dW, n, lr);
 }
 
+extern "C" gist_status gist_subagg_mean(gist_ctx* ctx, float* Wg, int64_t rows, int64_t cols,
+                                        int64_t ldg, int32_t m, const float* const* slices,
+                                        int64_t lds) {
+  gist::clear_error();
+  if (!ctx) return set_error(GIST_E_INVAL, "subagg_mean: NULL ctx");
+  gist::ProfBind pb(ctx);
+  if (rows < 0 || cols < 0 || m < 1 || ldg < cols || lds < cols)
+    return set_error(GIST_E_INVAL, "subagg_mean: bad sizes");
+  if (rows == 0 || cols == 0) return GIST_OK;
+  if (!Wg || !slices) return set_error(GIST_E_INVAL, "subagg_mean: NULL pointer");
+  gist::DeviceGuard dg(ctx->device);
+  return gist::subagg_mean(ctx->stream, Wg, rows, cols, ldg, m, slices, lds);
+}
+
 extern "C" gist_status gist_adam_update(gist_ctx* ctx, float* W, const float* dW, float* m,
                                         float* v, int64_t n, float lr, float beta1, float beta2,
                                         float eps, int64_t step, uint32_t flags) {

@@ -134,6 +134,21 @@ __global__ __launch_bounds__(kBlock) void scatter_kernel(float* __restrict__ Wg,
   }
 }
 
+// Wg[r][c] = mean over the m slices, summed in double in slice order.
+__global__ __launch_bounds__(kBlock) void subagg_mean_kernel(float* __restrict__ Wg, int64_t rows,
+                                                             int64_t cols, int64_t ldg, int m,
+                                                             const float* const* __restrict__ slices,
+                                                             int64_t lds) {
+  const int64_t count = rows * cols;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+  for (int64_t e = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x; e < count; e += stride) {
+    const int64_t r = e / cols, c = e - r * cols;
+    double s = 0.0;
+    for (int i = 0; i < m; ++i) s += static_cast<double>(slices[i][r * lds + c]);
+    Wg[r * ldg + c] = static_cast<float>(s / m);
+  }
+}
+
 __global__ __launch_bounds__(kBlock) void zero_kernel(float* __restrict__ p, int64_t count) {
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
   for (int64_t i = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x; i < count; i += stride)
@@ -489,6 +504,16 @@ gist_status fill_zero(hipStream_t st, float* p, int64_t count) {
   hipLaunchKernelGGL(zero_kernel, dim3(grid_for(count, kBlock, 8192)), dim3(kBlock), 0, st, p,
                      count);
   return check_launch("fill_zero");
+}
+
+gist_status subagg_mean(hipStream_t st, float* Wg, int64_t rows, int64_t cols, int64_t ldg, int m,
+                        const float* const* slices, int64_t lds) {
+  const int64_t count = rows * cols;
+  if (count <= 0) return GIST_OK;
+  ProfScope ps(st, "subagg_mean", static_cast<double>(m) * count, 4.0 * (m + 1.0) * count);
+  hipLaunchKernelGGL(subagg_mean_kernel, dim3(grid_for(count, kBlock, 8192)), dim3(kBlock), 0, st,
+                     Wg, rows, cols, ldg, m, slices, lds);
+  return check_launch("subagg_mean");
 }
 
 gist_status sgd(hipStream_t st, float* W, const float* dW, int64_t n, float lr) {

@@ -72,8 +72,16 @@ __global__ __launch_bounds__(kBlock) void gat_softmax_kernel(int64_t n, const in
 
 // Backward through the attention of row i (one wave per row):
 //   dalpha_ij = dZ_i . P_j,  c_i = sum_j alpha_ij dalpha_ij,
-//   dpre_ij = alpha_ij (dalpha_ij - c_i) * LeakyReLU'(u_i + v_j),
-//   du_i = sum_j dpre_ij.
+//   t_ij = alpha_ij (dalpha_ij - c_i),
+//   dpre_ij = t_ij * LeakyReLU'(u_i + v_j),   du_i = sum_j dpre_ij.
+// Since sum_j t_ij = c_i (1 - sum_j alpha_ij) = 0, du_i equals
+// (1 - slope) T+ = -(1 - slope) T- with T+ / T- the sums of t over the
+// entries with positive / non-positive scores; the kernel takes the form
+// over the smaller of the two sets.  A row whose scores all lie on one side
+// then has du_i = 0 exactly (a_src cannot change its attention, whatever
+// the rounding of alpha), where the plain sum would leave a rounding
+// residue that an optimizer normalising by |g| (Adam) would turn into a
+// full-size step.
 // The first kKeep * 64 dalpha of a row stay in registers (lane l keeps
 // entry 64 c + l of chunk c); a longer row's remaining entries recompute
 // theirs in the second pass, so nothing is read back from memory.
@@ -113,26 +121,31 @@ __global__ __launch_bounds__(kBlock) void gat_edge_grad_kernel(
   for (int p = e0 + 64 * kKeep; p < e1; ++p)
     c = fmaf(alpha[p], dot_row(dz, P + static_cast<int64_t>(col[p]) * ldp, s, lane), c);
   const float ui = u[i];
-  float dsum = 0.f;
+  float tpos = 0.f, tneg = 0.f;
+  int npos = 0;
 #pragma unroll
   for (int cc = 0; cc < kKeep; ++cc) {
     const int p = e0 + 64 * cc + lane;
-    float d = 0.f;
+    float t = 0.f;
+    bool pos = false;
     if (p < e1) {
-      const float pre = ui + v[col[p]];
-      d = alpha[p] * (keep[cc] - c) * (pre > 0.f ? 1.f : slope);
-      dpre[p] = d;
+      pos = ui + v[col[p]] > 0.f;
+      t = alpha[p] * (keep[cc] - c);
+      dpre[p] = pos ? t : slope * t;
     }
-    dsum += wave_sum(d);
+    npos += __popcll(__ballot(pos));
+    tpos += wave_sum(pos ? t : 0.f);
+    tneg += wave_sum(pos ? 0.f : t);
   }
   for (int p = e0 + 64 * kKeep; p < e1; ++p) {
     const float da = dot_row(dz, P + static_cast<int64_t>(col[p]) * ldp, s, lane);
-    const float pre = ui + v[col[p]];
-    const float d = alpha[p] * (da - c) * (pre > 0.f ? 1.f : slope);
-    if (lane == 0) dpre[p] = d;
-    dsum += d;
+    const bool pos = ui + v[col[p]] > 0.f;
+    const float t = alpha[p] * (da - c);
+    if (lane == 0) dpre[p] = pos ? t : slope * t;
+    if (pos) { tpos += t; ++npos; } else { tneg += t; }
   }
-  if (lane == 0) du[i] = dsum;
+  const int nneg = (e1 - e0) - npos;
+  if (lane == 0) du[i] = npos <= nneg ? (1.f - slope) * tpos : -((1.f - slope) * tneg);
 }
 
 // tpos[q] = p where entry q of row j is (j, i) and entry p of row i is

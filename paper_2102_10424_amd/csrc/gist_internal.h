@@ -119,6 +119,8 @@ gist_status fill_zero(hipStream_t st, float* p, int64_t count);
 gist_status subagg_gather(hipStream_t st, float* Wg, int64_t rows, int64_t cols, int64_t ldg,
                           int m, const gist_slice_set* done, const gist_slice_set* next, double bytes);
 gist_status sgd(hipStream_t st, float* W, const float* dW, int64_t n, float lr);
+gist_status subagg_mean(hipStream_t st, float* Wg, int64_t rows, int64_t cols, int64_t ldg, int m,
+                        const float* const* slices, int64_t lds);
 // graph attention steps (gat.hip)
 gist_status gat_scores(hipStream_t st, int64_t n, int s, const float* P, int64_t ldp,
                        const float* a_src, const float* a_dst, float* u, float* v);

@@ -60,7 +60,7 @@ EXPORTED = (
     "gist_gat_workspace_size", "gist_gat_layer_fwd", "gist_gat_layer_bwd",
     "gist_softmax_xent_workspace", "gist_softmax_xent", "gist_gather_slice",
     "gist_sgd_update", "gist_adam_update", "gist_subagg", "gist_partition_inverse",
-    "gist_subagg_gather",
+    "gist_subagg_gather", "gist_subagg_mean",
     "gist_profile_begin", "gist_profile_read", "gist_profile_end",
 )
 
@@ -123,6 +123,8 @@ _sigs = {
                                    C.c_float, C.c_int64, C.c_uint32]),
     "gist_subagg_gather": (C.c_int, [_P, _P, C.c_int64, C.c_int64, C.c_int64, C.c_int32,
                                      C.POINTER(gist_slice_set), C.POINTER(gist_slice_set)]),
+    "gist_subagg_mean": (C.c_int, [_P, _P, C.c_int64, C.c_int64, C.c_int64, C.c_int32, _P,
+                                   C.c_int64]),
     "gist_gat_workspace_size": (C.c_int, [C.POINTER(gist_gat_desc), C.POINTER(C.c_size_t),
                                           C.POINTER(C.c_size_t)]),
     "gist_gat_layer_fwd": (C.c_int, [_P, C.POINTER(gist_gat_desc), C.POINTER(gist_csr_dev)] +
@@ -386,6 +388,12 @@ def gist_subagg_gather(ctx, Wg, rows, cols, ldg, m, done, next_):
     _check(_lib.gist_subagg_gather(ctx.handle, _ptr(Wg), int(rows), int(cols), int(ldg), int(m),
                                    C.byref(done) if done is not None else None,
                                    C.byref(next_) if next_ is not None else None))
+
+
+def gist_subagg_mean(ctx, Wg, rows, cols, ldg, m, slice_ptrs, lds):
+    """Wg = mean of the m slices; ``slice_ptrs`` is a device int64 tensor of their addresses."""
+    _check(_lib.gist_subagg_mean(ctx.handle, _ptr(Wg), int(rows), int(cols), int(ldg), int(m),
+                                 _ptr(slice_ptrs), int(lds)))
 
 
 def gist_subagg(ctx, Wg, ldg, rows, nr, cols, nc, Ws, lds, flags=0):

@@ -4,7 +4,8 @@ Nothing here computes: each stage is one ``libgist`` call enqueued on the
 context's stream (torch only provides the device buffers).
 
 * :class:`SubGCN` -- ``subTrain`` (Section 3.2): layer forward for every
-  layer (eq. (2)), softmax cross-entropy, layer backward in reverse, SGD.
+  layer (eq. (2), or the GAT layer), softmax cross-entropy, layer backward
+  in reverse, SGD or Adam.
 * :class:`GistModel` -- the global model of Algorithm 1 on one device:
   ``subGCNs`` (partition + slice gather), m sub-GCN steps back to back,
   ``subAgg`` (slice scatter), optionally with Adam moments.
@@ -16,6 +17,8 @@ import numpy as np
 import torch
 
 from . import gist as G
+
+GAT_SLOPE = 0.2    # LeakyReLU slope of GAT's attention scores (the GAT paper's)
 
 
 def _dev(x, device, dtype=None):
@@ -118,15 +121,24 @@ class _View:
 class SubGCN:
     """Buffers and call sequence of one sub-GCN's training step.
 
-    ``widths`` are the slice widths s_0..s_L; ``kind`` is "gcn" or "sage".
-    Parameters are device tensors ``params[l]`` of shape (s_l, s_{l+1})
-    (SAGE: (2 s_l, s_{l+1}), W_self stacked over W_neigh).
+    ``widths`` are the slice widths s_0..s_L; ``kind`` is "gcn", "sage" or
+    "gat".  Parameters are device tensors ``params[l]`` of shape
+    (s_l, s_{l+1}) (SAGE: (2 s_l, s_{l+1}), W_self stacked over W_neigh;
+    GAT: (s_l + 2, s_{l+1}), Theta followed by the rows a_src and a_dst), and
+    the gradients ``dW[l]`` have the same layout, so one optimizer call
+    updates a layer.  A GAT batch's CSR is the pattern of A + I (the GCN
+    matrix; its values are not read).
     """
 
     def __init__(self, ctx, kind, widths, n_cap, dtype=G.GIST_DTYPE_F32, device="cuda",
                  order=G.GIST_ORDER_AUTO):
+        if kind not in ("gcn", "sage", "gat"):
+            raise ValueError("kind is 'gcn', 'sage' or 'gat'")
         self.ctx = ctx
         self.kind = kind
+        self.gat = kind == "gat"
+        self.nnz_cap = 0
+        self.alpha = None
         self.widths = list(widths)
         self.L = len(widths) - 1
         self.dtype = dtype
@@ -141,42 +153,65 @@ class SubGCN:
         self.loss = torch.zeros(1, device=device)
 
     def wrows(self, l):
+        if self.gat:
+            return self.widths[l] + 2
         return (2 if self.kind == "sage" else 1) * self.widths[l]
 
     def _alloc(self, n_cap):
         w, d = self.widths, self.device
         self.n_cap = n_cap
         self.H = [None] + [torch.empty(n_cap, w[l + 1], device=d) for l in range(self.L)]
-        self.agg = [torch.empty(n_cap, w[l], device=d) for l in range(self.L)]
+        # GCN / SAGE save the aggregation Abar H; GAT saves the transform P = H Theta
+        self.agg = [torch.empty(n_cap, w[l + 1] if self.gat else w[l], device=d)
+                    for l in range(self.L)]
         self.dH = [torch.empty(n_cap, w[l], device=d) for l in range(self.L)]  # dH[l] wrt H_l
         self.dlogits = torch.empty(n_cap, w[self.L], device=d)
         self.loss_ws = torch.empty(G.gist_softmax_xent_workspace(n_cap), dtype=torch.uint8,
                                    device=d)
 
-    def desc(self, l, n):
+    def desc(self, l, n, nnz=0):
         act = G.GIST_ACT_RELU if l < self.L - 1 else G.GIST_ACT_NONE
+        if self.gat:
+            return G.gat_desc(n, nnz, self.widths[l], self.widths[l + 1], act, self.dtype,
+                              GAT_SLOPE)
         return G.layer_desc(self.lkind, act, n, self.widths[l], self.widths[l + 1],
                             self.dtype, self.order)
 
-    def _workspace(self, n):
+    def _workspace(self, n, nnz=0):
         need = 0
         for l in range(self.L):
-            f, b = G.gist_layer_workspace_size(self.desc(l, n))
+            if self.gat:
+                f, b = G.gist_gat_workspace_size(self.desc(l, n, nnz))
+            else:
+                f, b = G.gist_layer_workspace_size(self.desc(l, n))
             need = max(need, f, b)
         if self.ws.numel() < need:
             self.ws = torch.empty(need, dtype=torch.uint8, device=self.device)
         return self.ws
 
+    def _gat_parts(self, t, l):
+        """(Theta, a_src, a_dst) views of a GAT layer's stacked parameters."""
+        s = self.widths[l]
+        return t[:s], t[s], t[s + 1]
+
     def forward(self, batch, params):
-        n = batch.n
+        n, nnz = batch.n, batch.nnz
         if n > self.n_cap:
             self._alloc(n)
-        ws = self._workspace(n)
+        if self.gat and (self.alpha is None or nnz > self.nnz_cap):
+            self.nnz_cap = max(nnz, 1)
+            self.alpha = [torch.empty(self.nnz_cap, device=self.device) for _ in range(self.L)]
+        ws = self._workspace(n, nnz)
         H = batch.X
         for l in range(self.L):
             out = self.H[l + 1][:n]
-            G.gist_gcn_layer_fwd(self.ctx, self.desc(l, n), batch.A, H, params[l],
-                                 self.agg[l][:n], out, ws)
+            if self.gat:
+                W, a1, a2 = self._gat_parts(params[l], l)
+                G.gist_gat_layer_fwd(self.ctx, self.desc(l, n, nnz), batch.A, H, W, a1, a2,
+                                     self.agg[l][:n], self.alpha[l][:nnz], out, ws)
+            else:
+                G.gist_gcn_layer_fwd(self.ctx, self.desc(l, n), batch.A, H, params[l],
+                                     self.agg[l][:n], out, ws)
             H = out
         return self.H[self.L][:n]
 
@@ -188,15 +223,22 @@ class SubGCN:
                             self.loss_ws)
 
     def backward(self, batch, params):
-        n = batch.n
-        ws = self._workspace(n)
+        n, nnz = batch.n, batch.nnz
+        ws = self._workspace(n, nnz)
         dout = self.dlogits[:n]
         for l in reversed(range(self.L)):
             Hin = batch.X if l == 0 else self.H[l][:n]
             dH = self.dH[l][:n] if l > 0 else None
-            G.gist_gcn_layer_bwd(self.ctx, self.desc(l, n), batch.A, batch.A_T, Hin,
-                                 self.agg[l][:n], self.H[l + 1][:n], params[l], dout,
-                                 self.dW[l], dH, ws)
+            if self.gat:
+                W, a1, a2 = self._gat_parts(params[l], l)
+                gW, g1, g2 = self._gat_parts(self.dW[l], l)
+                G.gist_gat_layer_bwd(self.ctx, self.desc(l, n, nnz), batch.A, Hin,
+                                     self.agg[l][:n], self.alpha[l][:nnz], self.H[l + 1][:n],
+                                     W, a1, a2, dout, gW, g1, g2, dH, ws)
+            else:
+                G.gist_gcn_layer_bwd(self.ctx, self.desc(l, n), batch.A, batch.A_T, Hin,
+                                     self.agg[l][:n], self.H[l + 1][:n], params[l], dout,
+                                     self.dW[l], dH, ws)
             dout = dH
 
     def sgd(self, params, lr):
@@ -237,6 +279,8 @@ class SubGCNBatch:
     """
 
     def __init__(self, ctx, kind, widths, m, n_cap, dtype=G.GIST_DTYPE_F32, device="cuda"):
+        if kind not in ("gcn", "sage"):
+            raise ValueError("batched sub-GCNs are GCN or SAGE")
         self.ctx = ctx
         self.kind = kind
         self.widths = list(widths)
@@ -343,8 +387,17 @@ class SubGCNBatch:
 class GistModel:
     """Global parameters Theta on the device plus the subGCNs / subAgg calls.
 
-    ``theta[l]`` is a list of parts (GCN: [Theta_l]; SAGE: [W_self, W_neigh]),
-    each (d_l x d_{l+1}) fp32 on the device.
+    ``theta[l]`` is a list of parts, each with d_{l+1} columns: GCN
+    [Theta_l]; SAGE [W_self, W_neigh]; GAT [Theta_l, A_l] with A_l the
+    2 x d_{l+1} matrix whose rows are a_src and a_dst.  A sub-GCN's slice of
+    a layer stacks its parts' slices row-wise in one (rows x s_{l+1}) matrix
+    (the layout :class:`SubGCN` takes).  Rows of a weight part follow the
+    partition D_l (all rows at l = 0); rows of GAT's attention part are
+    never partitioned; columns follow D_{l+1} (all at the last layer).  A
+    part split along neither (GAT's output-layer attention vectors) is
+    trained in full by every sub-GCN and aggregated as the mean of the m
+    copies (gist_subagg_mean); every other part is aggregated by
+    replacement.
 
     A round is ``set_partitions`` -> ``begin_round`` -> m sub-GCN steps on
     ``params`` -> ``end_round``.  With ``fused`` (default) the subAgg of a
@@ -365,6 +418,8 @@ class GistModel:
     def __init__(self, ctx, kind, widths, m, theta, device="cuda", fused=True, adam=None):
         if adam not in (None, "carry", "reset"):
             raise ValueError("adam is None, 'carry' or 'reset'")
+        if kind not in ("gcn", "sage", "gat"):
+            raise ValueError("kind is 'gcn', 'sage' or 'gat'")
         self.ctx = ctx
         self.kind = kind
         self.widths = list(widths)
@@ -374,7 +429,7 @@ class GistModel:
         self.device = device
         self.fused = fused
         self.adam = adam
-        self.parts = 2 if kind == "sage" else 1
+        self.parts = 1 if kind == "gcn" else 2
         self.slice_widths = [widths[0]] + [widths[l] // m for l in range(1, self.L)] + [widths[-1]]
         self.nbuf = 2 if fused else 1
         self._bufs = self._slices()                 # per sub-GCN parameter slices
@@ -399,14 +454,33 @@ class GistModel:
         self._events = [None, None]
         self.pending = None    # (slot, buffer) whose subAgg is outstanding
 
+    # -- layout ---------------------------------------------------------------
+    def _layout(self, l):
+        """Layer l's parts: [(row offset in the slice, slice rows, global rows,
+        rows follow D_l)]."""
+        s = self.slice_widths[l]
+        if self.kind == "gat":
+            return [(0, s, self.widths[l], True), (s, 2, 2, False)]
+        return [(p * s, s, self.widths[l], True) for p in range(self.parts)]
+
+    def _row_split(self, l, p):
+        return l > 0 and self._layout(l)[p][3]
+
+    def _shared(self, l, p):
+        """Split along neither dimension: every sub-GCN trains the whole part."""
+        return not self._row_split(l, p) and l + 1 == self.L
+
+    def _slice_rows(self, l):
+        return sum(part[1] for part in self._layout(l))
+
     def _slices(self):
-        """[buffer][sub-GCN][layer] slice tensors (SAGE: [W_self; W_neigh] stacked).
+        """[buffer][sub-GCN][layer] slice tensors (parts stacked row-wise).
 
         Each (buffer, layer) is one [m][rows][cols] tensor and the per
         sub-GCN slices are views of it, so a batched step can address all m
         slices of a layer as one array (see ``stacked``)."""
         s = self.slice_widths
-        big = [[torch.empty(self.m, self.parts * s[l], s[l + 1], device=self.device)
+        big = [[torch.empty(self.m, self._slice_rows(l), s[l + 1], device=self.device)
                 for l in range(self.L)] for _ in range(self.nbuf)]
         return [[[big[b][l][i] for l in range(self.L)] for i in range(self.m)]
                 for b in range(self.nbuf)]
@@ -424,9 +498,10 @@ class GistModel:
     def _tables(self, bufs):
         """Device tables of the m slice pointers of every (buffer, layer, part)."""
         s = self.slice_widths
-        return [[[torch.tensor([bufs[b][i][l].data_ptr() + 4 * p * s[l] * s[l + 1]
+        return [[[torch.tensor([bufs[b][i][l].data_ptr() + 4 * off * s[l + 1]
                                 for i in range(self.m)], dtype=torch.int64).to(self.device)
-                  for p in range(self.parts)] for l in range(self.L)] for b in range(self.nbuf)]
+                  for off, _, _, _ in self._layout(l)] for l in range(self.L)]
+                for b in range(self.nbuf)]
 
     def _select(self, b):
         self.buf = b
@@ -435,10 +510,11 @@ class GistModel:
         self.V = self._vbufs[b] if self._vbufs else None
 
     def _globals(self):
-        """(global matrices, slice pointer tables) that gather / subAgg move."""
-        out = [(self.theta, self._ptrs)]
+        """(global matrices, slice pointer tables, slice buffers) that gather /
+        subAgg move."""
+        out = [(self.theta, self._ptrs, self._bufs)]
         if self.adam == "carry":
-            out += [(self.Mg, self._mptrs), (self.Vg, self._vptrs)]
+            out += [(self.Mg, self._mptrs, self._mbufs), (self.Vg, self._vptrs, self._vbufs)]
         return out
 
     def _pairs(self, i):
@@ -485,11 +561,10 @@ class GistModel:
         idx, offs = self._host[self._slot][l]
         return self._dev[self._slot][l][0][int(offs[i]):int(offs[i + 1])], int(offs[i + 1] - offs[i])
 
-    def _rc(self, l, i):
-        if l == 0:
-            rows, nr = None, self.widths[0]
-        else:
-            rows, nr = self._block(l, i)
+    def _rc(self, l, i, p):
+        """(rows, nr, cols, nc) of sub-GCN i's slice of layer l, part p."""
+        nrows = self._layout(l)[p][1]
+        rows, nr = self._block(l, i) if self._row_split(l, p) else (None, nrows)
         if l + 1 == self.L:
             cols, nc = None, self.widths[-1]
         else:
@@ -499,11 +574,15 @@ class GistModel:
     def _set(self, slot, table, l, p):
         """gist_slice_set of layer l, part p: partition `slot`, slice pointer `table`."""
         rr = ro = cr = co = None
-        if l > 0:
+        if self._row_split(l, p):
             rr, ro = self._dev[slot][l][1], self._doffs[slot][l]
         if l + 1 < self.L:
             cr, co = self._dev[slot][l + 1][1], self._doffs[slot][l + 1]
         return G.slice_set(rr, ro, cr, co, table[l][p], self.slice_widths[l + 1])
+
+    def _view(self, sl, l, p):
+        off, nrows = self._layout(l)[p][:2]
+        return sl[l][off:off + nrows]
 
     # -- per-slice calls ----------------------------------------------------
     def gather(self, i):
@@ -511,19 +590,48 @@ class GistModel:
         (and the moments' slices with "carry")."""
         for glob, sl in self._pairs(i):
             for l in range(self.L):
-                rows, nr, cols, nc = self._rc(l, i)
                 for p in range(self.parts):
+                    rows, nr, cols, nc = self._rc(l, i, p)
                     G.gist_gather_slice(self.ctx, glob[l][p], self.widths[l + 1], rows, nr,
-                                        cols, nc, sl[l][p * nr:(p + 1) * nr], nc)
+                                        cols, nc, self._view(sl, l, p), nc)
 
     def subagg(self, i, flags=0):
-        """Write sub-GCN i's trained slices back into Theta (replacement)."""
+        """Write sub-GCN i's trained slices back into Theta (replacement);
+        parts split along neither dimension wait for :meth:`subagg_shared`."""
         for glob, sl in self._pairs(i):
             for l in range(self.L):
-                rows, nr, cols, nc = self._rc(l, i)
                 for p in range(self.parts):
+                    if self._shared(l, p):
+                        continue
+                    rows, nr, cols, nc = self._rc(l, i, p)
                     G.gist_subagg(self.ctx, glob[l][p], self.widths[l + 1], rows, nr, cols,
-                                  nc, sl[l][p * nr:(p + 1) * nr], nc, flags)
+                                  nc, self._view(sl, l, p), nc, flags)
+
+    def subagg_shared(self, buf=None):
+        """Unsplit parts: Theta's entries become the mean of the m trained copies
+        of slice buffer ``buf`` (default: the current one)."""
+        buf = self.buf if buf is None else buf
+        for glob, tables, _ in self._globals():
+            for l in range(self.L):
+                for p in range(self.parts):
+                    if self._shared(l, p):
+                        grows = self._layout(l)[p][2]
+                        G.gist_subagg_mean(self.ctx, glob[l][p], grows, self.widths[l + 1],
+                                           self.widths[l + 1], self.m, tables[buf][l][p],
+                                           self.slice_widths[l + 1])
+
+    def _gather_shared(self, buf):
+        """Every sub-GCN's copy of each unsplit part, into slice buffer ``buf``."""
+        for glob, _, bufs in self._globals():
+            for l in range(self.L):
+                for p in range(self.parts):
+                    if self._shared(l, p):
+                        grows = self._layout(l)[p][2]
+                        for i in range(self.m):
+                            G.gist_gather_slice(self.ctx, glob[l][p], self.widths[l + 1], None,
+                                                grows, None, self.widths[l + 1],
+                                                self._view(bufs[buf][i], l, p),
+                                                self.slice_widths[l + 1])
 
     # -- rounds ---------------------------------------------------------------
     def begin_round(self):
@@ -533,14 +641,19 @@ class GistModel:
                 self.gather(i)
             return
         nxt = 1 - self.buf if self.pending is not None else self.buf
-        for glob, tables in self._globals():
+        if self.pending is not None:
+            self.subagg_shared(self.pending[1])
+        for glob, tables, _ in self._globals():
             for l in range(self.L):
                 for p in range(self.parts):
+                    if self._shared(l, p):
+                        continue
                     done = (self._set(self.pending[0], tables[self.pending[1]], l, p)
                             if self.pending is not None else None)
-                    G.gist_subagg_gather(self.ctx, glob[l][p], self.widths[l],
+                    G.gist_subagg_gather(self.ctx, glob[l][p], self._layout(l)[p][2],
                                          self.widths[l + 1], self.widths[l + 1], self.m, done,
                                          self._set(self._slot, tables[nxt], l, p))
+        self._gather_shared(nxt)
         self._select(nxt)
         self.pending = None
 
@@ -549,6 +662,7 @@ class GistModel:
         if not self.fused:
             for i in range(self.m):
                 self.subagg(i)
+            self.subagg_shared()
             return
         self.pending = (self._slot, self.buf)
 
@@ -556,10 +670,13 @@ class GistModel:
         """Apply a pending subAgg so that Theta holds every trained slice."""
         if self.pending is None:
             return
-        for glob, tables in self._globals():
+        self.subagg_shared(self.pending[1])
+        for glob, tables, _ in self._globals():
             for l in range(self.L):
                 for p in range(self.parts):
-                    G.gist_subagg_gather(self.ctx, glob[l][p], self.widths[l],
+                    if self._shared(l, p):
+                        continue
+                    G.gist_subagg_gather(self.ctx, glob[l][p], self._layout(l)[p][2],
                                          self.widths[l + 1], self.widths[l + 1], self.m,
                                          self._set(self.pending[0], tables[self.pending[1]], l, p),
                                          None)

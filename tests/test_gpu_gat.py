@@ -127,3 +127,80 @@ def test_gat_errors(G, ctx):
     assert e.value.status == G.GIST_E_INVAL
     with pytest.raises(G.GistError):
         G.gist_gat_workspace_size(G.gat_desc(4, 4, 2, 2, 7))
+
+
+@pytest.mark.parametrize("clusters", [None, (0, 3, 4, 9)])
+def test_gat_sub_gcn_step_matches_oracle(G, ctx, clusters):
+    """One SGD ``subTrain`` step of a 3-layer GAT sub-GCN (SubGCN runner over
+    the C ABI) against oracle.gist.sub_gcn_step: loss, logits, every layer's
+    gradients (Theta, a_src, a_dst) and the updated parameters."""
+    import torch
+    from oracle import gist as OG
+    from paper_2102_10424_amd.step import BatchSlot, SubGCN
+    g = GRAPHS["sbm1500"]
+    widths = [24, 40, 16, 6]
+    L = len(widths) - 1
+    rng = np.random.default_rng(21)
+    X = rng.standard_normal((g.n, widths[0])).astype(np.float32)
+    y = rng.integers(0, widths[-1], g.n).astype(np.int32)
+    P = [(rng.standard_normal((widths[l] + 2, widths[l + 1])) * 0.3).astype(np.float32)
+         for l in range(L)]
+    cl = None if clusters is None else np.array(clusters, dtype=np.int32)
+    log(f"gat step clusters={clusters}")
+    slot = BatchSlot(ctx, "gcn", g.n, g.nnz + g.n, widths[0])
+    b = slot.load(G.GraphHandle(g), cl, to_dev(X), y)
+    runner = SubGCN(ctx, "gat", widths, b.n)
+    params = [to_dev(p.copy()) for p in P]
+    runner.step(b, params, 0.05)
+    torch.cuda.synchronize()
+    csr = MB.build(g, cl, "gcn")
+    nm = csr["node_map"]
+    op = [(p[:widths[l]], p[widths[l]], p[widths[l] + 1]) for l, p in enumerate(P)]
+    ref = OG.sub_gcn_step("gat", csr, X[nm], y[nm], op, 0.05)
+    assert abs(float(to_host(runner.loss)[0]) - ref["loss"]) <= FP32_TOL * abs(ref["loss"])
+    assert relerr(to_host(runner.H[L][:b.n]), ref["H"][L]) <= FP32_TOL
+    for l in range(L):
+        gW, g1, g2 = ref["grads"][l]
+        want = np.concatenate([gW, g1[None], g2[None]])
+        e = relerr(to_host(runner.dW[l]), want)
+        pw = ref["params"][l]
+        ep = relerr(to_host(params[l]), np.concatenate([pw[0], pw[1][None], pw[2][None]]))
+        log(f"  layer {l}: grads {e:.2e} params {ep:.2e}")
+        assert e <= FP32_TOL and ep <= FP32_TOL
+
+
+@pytest.mark.parametrize("sign", [1.0, -1.0])
+def test_gat_one_sided_scores_give_exact_zero_da_src(G, ctx, sign):
+    """When every score of a row lies on one side of the LeakyReLU, u_i
+    cannot change that row's attention (the softmax removes a per-row
+    shift), so du_i -- and with every row one-sided, da_src -- is zero.
+    The kernel reaches that zero exactly (the oracle's fp64 sum leaves a
+    residue near 1e-18 relative); the other outputs match the oracle."""
+    import torch
+    g = GRAPHS["sbm1500"]
+    csr = MB.build(g, None, "gcn")
+    n, nnz, si, so = csr["n"], csr["nnz"], 24, 16
+    rng = np.random.default_rng(8)
+    H = rng.uniform(0.1, 1.0, (n, si)).astype(np.float32)      # P = H W > 0
+    W = rng.uniform(0.1, 1.0, (si, so)).astype(np.float32) / si
+    a1 = (sign * rng.uniform(0.1, 1.0, so)).astype(np.float32)   # u, v all of one sign
+    a2 = (sign * rng.uniform(0.1, 1.0, so)).astype(np.float32)
+    dHo = rng.standard_normal((n, so)).astype(np.float32)
+    f = GA.gat_forward(csr, H, W, a1, a2, False, 0.2)
+    assert np.all(np.sign(f["pre"]) == sign)
+    b = GA.gat_backward(csr, H, f, W, a1, a2, dHo, False, 0.2)
+    assert np.max(np.abs(b["da_src"])) <= 1e-12 * np.max(np.abs(b["da_dst"]))
+    A, keep = csr_to_dev(csr)
+    desc = G.gat_desc(n, nnz, si, so, 0, G.GIST_DTYPE_F32, 0.2)
+    fws, bws = G.gist_gat_workspace_size(desc)
+    ws = torch.empty(max(fws, bws, 1), dtype=torch.uint8, device="cuda")
+    dW = torch.empty(si, so, device="cuda")
+    da1 = torch.full((so,), 5.0, device="cuda")
+    da2 = torch.empty(so, device="cuda")
+    dH = torch.empty(n, si, device="cuda")
+    G.gist_gat_layer_bwd(ctx, desc, A, to_dev(H), to_dev(f["P"].astype(np.float32)),
+                         to_dev(f["alpha"].astype(np.float32)), to_dev(f["H_out"].astype(np.float32)),
+                         to_dev(W), to_dev(a1), to_dev(a2), to_dev(dHo), dW, da1, da2, dH, ws)
+    assert np.all(to_host(da1) == 0.0)
+    for got, want in ((dW, b["dW"]), (da2, b["da_dst"]), (dH, b["dH"])):
+        assert relerr(to_host(got), want) <= FP32_TOL

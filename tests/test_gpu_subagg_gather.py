@@ -151,18 +151,20 @@ def test_subagg_gather_errors(G, ctx):
     G.gist_subagg_gather(ctx, T, 0, 8, 8, 2, unpart, unpart)
 
 
-@pytest.mark.parametrize("kind", ["gcn", "sage"])
+@pytest.mark.parametrize("kind", ["gcn", "sage", "gat"])
 def test_fused_rounds_match_separate_calls(G, ctx, kind):
     """Three rounds of a GistModel with fused subAgg/gather and with the
-    separate calls, the training replaced by a fixed change of every slice:
-    Theta and every slice agree bit for bit."""
+    separate calls, the training replaced by a fixed change of every slice
+    (different per sub-GCN, so GAT's shared output-layer attention vectors
+    average distinct copies): Theta and every slice agree bit for bit."""
     import torch
     from paper_2102_10424_amd.step import GistModel
     widths, m = [40, 64, 96, 7], 4
-    parts = 2 if kind == "sage" else 1
+    parts = 1 if kind == "gcn" else 2
     rng = np.random.default_rng(5)
-    theta0 = [[rng.standard_normal((widths[l], widths[l + 1])).astype(np.float32)
-               for _ in range(parts)] for l in range(3)]
+    rows = lambda l, p: 2 if kind == "gat" and p == 1 else widths[l]
+    theta0 = [[rng.standard_normal((rows(l, p), widths[l + 1])).astype(np.float32)
+               for p in range(parts)] for l in range(3)]
     models = []
     for fused in (True, False):
         th = [[to_dev(t.copy()) for t in ps] for ps in theta0]
