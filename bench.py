@@ -10,7 +10,8 @@ One timed step is one pass of the whole hot path:
   -> one pass over the 16 GiB global model that applies the previous
      round's subAgg and gathers all 8 sub-GCN weight slices (device)
   -> for each sub-GCN: cluster mini-batch of 10 blocks (host CSR build into
-     pinned memory, asynchronous upload, device feature-row gather),
+     pinned memory on worker threads, a few batches ahead of use;
+     asynchronous upload, device feature-row gather),
      forward through 4 layers, softmax cross-entropy, backward, SGD.
   The last round's subAgg is applied after the timed region.
 
@@ -88,7 +89,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5", "c6"])
     ap.add_argument("--dtype", default="f32", choices=["f32", "bf16"])
     ap.add_argument("--d-in", type=int, default=256, help="c5 input slice width")
     ap.add_argument("--lr", type=float, default=0.01)
@@ -114,7 +115,8 @@ class RoundWorkload:
     def __init__(self, cfg, ctx, dtype, optimizer="sgd", policy="carry", zeta=1, shared=False):
         import torch
         from paper_2102_10424_amd import gist as G
-        from paper_2102_10424_amd.step import BatchSlot, GistModel, SubGCN, SubGCNBatch
+        from paper_2102_10424_amd.step import (BatchPipeline, BatchSlot, GistModel, SubGCN,
+                                               SubGCNBatch)
         self.cfg, self.ctx, self.G = cfg, ctx, G
         t0 = time.time()
         self.graph = cfg.make_graph()
@@ -142,9 +144,15 @@ class RoundWorkload:
             sizes = np.diff(self.graph.cluster_ptr)
             cap_n = int(np.sort(sizes)[-cfg.batch_clusters:].sum())
             cap_nnz = int(np.sort(np.diff(self.graph.rowptr))[-cap_n:].sum()) + cap_n
-        self.slots = [BatchSlot(ctx, self.norm, cap_n, cap_nnz, cfg.widths[0])
-                      for _ in range(cfg.m)]
         self.full = None
+        self.pipe = None
+        if cfg.batch_clusters is None:
+            self.slots = [BatchSlot(ctx, self.norm, cap_n, cap_nnz, cfg.widths[0])]
+        else:
+            # mini-batches are built on host worker threads ahead of use
+            self.pipe = BatchPipeline(ctx, self.norm, cap_n, cap_nnz, cfg.widths[0], self.gh,
+                                      self.X, self.labels, self._cluster_order(shared, zeta),
+                                      depth=8, workers=4)
         dt = G.GIST_DTYPE_BF16_IN if dtype == "bf16" else G.GIST_DTYPE_F32
         self.shared = shared
         if shared:
@@ -154,6 +162,22 @@ class RoundWorkload:
         self.lr = 0.01
         self.t = 0
 
+    def _cluster_order(self, shared, zeta):
+        """The clusters of every mini-batch, in the order the rounds take them."""
+        cfg, t = self.cfg, 0
+        while True:
+            for i in range(1 if shared else cfg.m):
+                for z in range(zeta):
+                    yield cfg.minibatch(t, i, z)
+            t += 1
+
+    def _batch(self, t, i, z):
+        if self.cfg.batch_clusters is None:
+            if self.full is None:
+                self.full = self.slots[0].load(self.gh, None, self.X, self.labels)
+            return self.full
+        return self.pipe.next()
+
     def step(self):
         cfg, m = self.cfg, self.model
         t, zeta = self.t, self.zeta
@@ -161,13 +185,7 @@ class RoundWorkload:
         m.begin_round()   # subAgg of round t-1 fused with the gather of round t
         if self.shared:
             for z in range(zeta):
-                if cfg.batch_clusters is None:
-                    if self.full is None:
-                        self.full = self.slots[0].load(self.gh, None, self.X, self.labels)
-                    b = self.full
-                else:
-                    b = self.slots[z % len(self.slots)].load(self.gh, cfg.minibatch(t, 0, z),
-                                                             self.X, self.labels)
+                b = self._batch(t, 0, z)
                 opt = None
                 if self.adam:
                     k = t * zeta + z + 1 if self.adam == "carry" else z + 1
@@ -178,12 +196,7 @@ class RoundWorkload:
             return
         for i in range(cfg.m):
             for z in range(zeta):
-                if cfg.batch_clusters is None:
-                    if self.full is None:
-                        self.full = self.slots[0].load(self.gh, None, self.X, self.labels)
-                    b = self.full
-                else:
-                    b = self.slots[i].load(self.gh, cfg.minibatch(t, i, z), self.X, self.labels)
+                b = self._batch(t, i, z)
                 opt = None
                 if self.adam == "carry":
                     opt = (m.M[i], m.V[i], t * zeta + z + 1, False)
@@ -195,6 +208,8 @@ class RoundWorkload:
 
     def finish(self):
         self.model.finalize()
+        if self.pipe is not None:
+            self.pipe.close()
 
     def steps_per_unit(self):
         return self.cfg.m * self.zeta
@@ -202,7 +217,7 @@ class RoundWorkload:
     def describe(self):
         c = self.cfg
         return {"workload": f"{c.name}: GIST round, {c.L}-layer "
-                            f"{'GraphSAGE-mean' if c.kind == 'sage' else 'GCN'}, hidden "
+                            f"{dict(sage='GraphSAGE-mean', gcn='GCN', gat='GAT')[c.kind]}, hidden "
                             f"{c.widths[1]} split m={c.m}, N={c.n_nodes}, "
                             f"{'mini-batch ' + str(c.batch_clusters) + ' clusters' if c.batch_clusters else 'full graph'}",
                 "model": "GIST sub-GCN", "m": c.m, "widths": c.widths,
@@ -225,10 +240,13 @@ class RoundWorkload:
         for l, (r, c) in enumerate(sl):
             ps = []
             for p in range(cfg.n_parts()):
-                rows = r if r is not None else None
+                rows = r if r is not None and not (cfg.kind == "gat" and p == 1) else None
                 th = cfg.theta(l, p, rows=rows) if rows is not None else cfg.theta(l, p)
                 ps.append(th if c is None else th[:, c])
-            params.append(ps[0] if cfg.kind == "gcn" else (ps[0], ps[1]))
+            if cfg.kind == "gat":
+                params.append((ps[0], ps[1][0], ps[1][1]))
+            else:
+                params.append(ps[0] if cfg.kind == "gcn" else (ps[0], ps[1]))
         csr = OM.build(self.graph, cfg.minibatch(0, 0), self.norm)
         nm = csr["node_map"]
         X = cfg.features_matrix(rows=nm)
@@ -380,7 +398,7 @@ def main():
     for k, v in sorted(prof.items(), key=lambda kv: -kv[1]["ms"]):
         e = dict(launches=v["launches"], ms_per_step=round(v["ms"] / args.steps, 4),
                  avg_us=round(1e3 * v["ms"] / v["launches"], 2))
-        if v["flops"] and k.startswith("gemm_") and "reduce" not in k:
+        if v["flops"] and k.startswith("gemm_") and "reduce" not in k and "fixup" not in k:
             e["tflops"] = round(v["flops"] / (v["ms"] * 1e-3) / 1e12, 2)
         if v["bytes"]:
             e["gbs"] = round(v["bytes"] / (v["ms"] * 1e-3) / 1e9, 1)
@@ -389,7 +407,7 @@ def main():
     if prof:
         dom, v = max(prof.items(), key=lambda kv: kv[1]["ms"])
         avg_s = v["ms"] * 1e-3 / v["launches"]
-        if dom.startswith("gemm_") and "reduce" not in dom:
+        if dom.startswith("gemm_") and "reduce" not in dom and "fixup" not in dom:
             peak = PEAK["bf16" if "bf16" in dom else "f32"]
             ach = v["flops"] / v["launches"] / avg_s / 1e12
             roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2),

@@ -14,6 +14,9 @@ Sizes follow the paper's datasets (Table 5) and experiments (Tables 1-3):
   random blocks (Amazon2M-sized, the ultra-wide model of Table 3).
 * ``c5`` one GCN layer over the whole c4 graph, input slice d_in in
   {100, 256, 512}, output = one 256-wide slice of a 2,048-wide layer (m=8).
+* ``c6`` 3-layer GAT, m=4, on the c3 graph (same graph, features, labels
+  and 20-block mini-batches), hidden 256 split into 4 x 64, 41 classes: the
+  256-dimensional GAT the paper trains on Reddit (Table 2).
 
 Seeds: config ``k`` uses base seed 100 + k; every array is a named stream of
 that base (see :mod:`gist_synth.seeds`).
@@ -34,7 +37,7 @@ from .seeds import (STREAM_FEATURES, STREAM_LABELS, STREAM_THETA,
 @dataclass
 class Config:
     name: str
-    kind: str                 # "gcn" | "sage"
+    kind: str                 # "gcn" | "sage" | "gat"
     widths: List[int]         # d_0 .. d_L (global model)
     m: int                    # number of sub-GCNs
     graph: dict               # generator name + parameters
@@ -100,13 +103,17 @@ class Config:
                                  STREAM_LABELS, self.classes)
 
     def theta(self, layer, part=0, rows=None):
-        """Global weight Theta_layer (d_l x d_{l+1}); SAGE part 0 = W_self, 1 = W_neigh."""
+        """Global weight Theta_layer (d_l x d_{l+1}); SAGE part 0 = W_self,
+        1 = W_neigh; GAT part 1 = the attention vectors [a_src; a_dst]
+        (2 x d_{l+1}, Glorot-uniform over that shape)."""
         fi, fo = self.widths[layer], self.widths[layer + 1]
+        if self.kind == "gat" and part == 1:
+            fi = 2
         return _t.glorot_uniform(fi, fo, self.seed, STREAM_THETA, layer, part,
                                  rows=rows)
 
     def n_parts(self):
-        return 2 if self.kind == "sage" else 1
+        return 1 if self.kind == "gcn" else 2
 
     def partition_seed(self, t, layer):
         """Seed of the feature partition of hidden dim ``layer`` in round ``t``."""
@@ -147,6 +154,11 @@ CONFIGS = {
     # c5: widths = [d_in, 2048]; the step uses output slice 0 of the m=8 split.
     "c5": Config("c5", "gcn", [256, 2048], 8, dict(_SBM_C4), "normal",
                  extra=dict(graph_seed=104, d_in_sweep=(100, 256, 512))),
+    # c6: the c3 graph (graph_seed 103) with a GAT model.
+    "c6": Config("c6", "gat", [602, 256, 256, 41], 4,
+                 dict(kind="sbm", n=232_965, blocks=1500, mean_degree=50.0,
+                      intra=0.9), "normal", batch_clusters=20,
+                 extra=dict(graph_seed=103)),
 }
 
 

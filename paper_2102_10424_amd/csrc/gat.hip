@@ -82,70 +82,96 @@ __global__ __launch_bounds__(kBlock) void gat_softmax_kernel(int64_t n, const in
 // the rounding of alpha), where the plain sum would leave a rounding
 // residue that an optimizer normalising by |g| (Adam) would turn into a
 // full-size step.
-// The first kKeep * 64 dalpha of a row stay in registers (lane l keeps
-// entry 64 c + l of chunk c); a longer row's remaining entries recompute
-// theirs in the second pass, so nothing is read back from memory.
-constexpr int kKeep = 8;
+//
+// The dot products dZ_i . P_j are computed by groups of G lanes (G a power
+// of two sized to the feature width, each lane covering about 16 features
+// with float4 loads where rows are 16-byte aligned), 64 / G entries per
+// pass.  The first kKeep dalpha of a row are kept in LDS for the second
+// pass (one lane per entry); a longer row's remaining entries recompute
+// theirs in the second pass, so nothing is read back from global memory.
+constexpr int kKeep = 512;
+constexpr int kWaves = kBlock / 64;
 
-__device__ __forceinline__ float dot_row(const float* __restrict__ a, const float* __restrict__ b, int s,
-                                         int lane) {
+template <int VEC>
+__device__ __forceinline__ float group_dot(const float* __restrict__ a, const float* __restrict__ b,
+                                           int s, int gl, int G) {
   float part = 0.f;
-  for (int k = lane; k < s; k += 64) part = fmaf(a[k], b[k], part);
-  return wave_sum(part);
+  if constexpr (VEC == 4) {
+    for (int k = gl * 4; k < s; k += G * 4) {
+      const float4 x = *reinterpret_cast<const float4*>(a + k);
+      const float4 y = *reinterpret_cast<const float4*>(b + k);
+      part = fmaf(x.x, y.x, part);
+      part = fmaf(x.y, y.y, part);
+      part = fmaf(x.z, y.z, part);
+      part = fmaf(x.w, y.w, part);
+    }
+  } else {
+    for (int k = gl; k < s; k += G) part = fmaf(a[k], b[k], part);
+  }
+  for (int off = G >> 1; off > 0; off >>= 1) part += __shfl_xor(part, off);
+  return part;    // every lane of the group holds the group's sum
 }
 
+template <int VEC>
 __global__ __launch_bounds__(kBlock) void gat_edge_grad_kernel(
-    int64_t n, int s, const int* __restrict__ rowptr, const int* __restrict__ col,
+    int64_t n, int s, int G, const int* __restrict__ rowptr, const int* __restrict__ col,
     const float* __restrict__ alpha, const float* __restrict__ dZ, int64_t ldz,
     const float* __restrict__ P, int64_t ldp, const float* __restrict__ u,
     const float* __restrict__ v, float slope, float* __restrict__ dpre, float* __restrict__ du) {
+  __shared__ float keep_lds[kWaves][kKeep];
   const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
   const int64_t i = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) >> 6;
-  if (i >= n) return;
-  const int e0 = rowptr[i], e1 = rowptr[i + 1];
-  const float* dz = dZ + i * ldz;
-  float keep[kKeep];
-  float c = 0.f;
-#pragma unroll
-  for (int cc = 0; cc < kKeep; ++cc) {
-    keep[cc] = 0.f;
-    const int b = e0 + 64 * cc;
-    if (b >= e1) continue;
-    const int end = min(e1, b + 64);
-    for (int p = b; p < end; ++p) {
-      const float da = dot_row(dz, P + static_cast<int64_t>(col[p]) * ldp, s, lane);
-      if (lane == p - b) keep[cc] = da;
-      c = fmaf(alpha[p], da, c);
+  const bool active = i < n;
+  const int e0 = active ? rowptr[i] : 0, e1 = active ? rowptr[i + 1] : 0;
+  const int len = e1 - e0;
+  const int E = 64 / G;                 // entries per pass
+  const int gi = lane / G, gl = lane % G;
+  const float* dz = dZ + (active ? i : 0) * ldz;
+  float* keep = keep_lds[wave];
+  // pass 1: dalpha of every entry, c_i
+  float cpart = 0.f;
+  for (int b = 0; b < len; b += E) {
+    const int q = b + gi;
+    const bool valid = q < len;
+    const int p = e0 + (valid ? q : 0);
+    const float da = group_dot<VEC>(dz, P + static_cast<int64_t>(col[p]) * ldp, s, gl, G);
+    if (valid && gl == 0) {
+      if (q < kKeep) keep[q] = da;
+      cpart = fmaf(alpha[p], da, cpart);
     }
   }
-  for (int p = e0 + 64 * kKeep; p < e1; ++p)
-    c = fmaf(alpha[p], dot_row(dz, P + static_cast<int64_t>(col[p]) * ldp, s, lane), c);
-  const float ui = u[i];
+  const float c = wave_sum(cpart);
+  __syncthreads();   // the kept dalpha are visible to every lane of the wave
+  // pass 2: t, dpre, and the one-sided sums for du
+  const float ui = active ? u[i] : 0.f;
   float tpos = 0.f, tneg = 0.f;
   int npos = 0;
-#pragma unroll
-  for (int cc = 0; cc < kKeep; ++cc) {
-    const int p = e0 + 64 * cc + lane;
-    float t = 0.f;
-    bool pos = false;
-    if (p < e1) {
-      pos = ui + v[col[p]] > 0.f;
-      t = alpha[p] * (keep[cc] - c);
-      dpre[p] = pos ? t : slope * t;
-    }
-    npos += __popcll(__ballot(pos));
-    tpos += wave_sum(pos ? t : 0.f);
-    tneg += wave_sum(pos ? 0.f : t);
-  }
-  for (int p = e0 + 64 * kKeep; p < e1; ++p) {
-    const float da = dot_row(dz, P + static_cast<int64_t>(col[p]) * ldp, s, lane);
+  const int nkeep = min(len, kKeep);
+  for (int q = lane; q < nkeep; q += 64) {
+    const int p = e0 + q;
     const bool pos = ui + v[col[p]] > 0.f;
-    const float t = alpha[p] * (da - c);
-    if (lane == 0) dpre[p] = pos ? t : slope * t;
+    const float t = alpha[p] * (keep[q] - c);
+    dpre[p] = pos ? t : slope * t;
     if (pos) { tpos += t; ++npos; } else { tneg += t; }
   }
-  const int nneg = (e1 - e0) - npos;
-  if (lane == 0) du[i] = npos <= nneg ? (1.f - slope) * tpos : -((1.f - slope) * tneg);
+  for (int b = kKeep; b < len; b += E) {    // rows longer than kKeep: recompute
+    const int q = b + gi;
+    const bool valid = q < len;
+    const int p = e0 + (valid ? q : 0);
+    const float da = group_dot<VEC>(dz, P + static_cast<int64_t>(col[p]) * ldp, s, gl, G);
+    if (valid && gl == 0) {
+      const bool pos = ui + v[col[p]] > 0.f;
+      const float t = alpha[p] * (da - c);
+      dpre[p] = pos ? t : slope * t;
+      if (pos) { tpos += t; ++npos; } else { tneg += t; }
+    }
+  }
+  tpos = wave_sum(tpos);
+  tneg = wave_sum(tneg);
+  for (int off = 32; off > 0; off >>= 1) npos += __shfl_xor(npos, off);
+  const int nneg = len - npos;
+  if (active && lane == 0) du[i] = npos <= nneg ? (1.f - slope) * tpos : -((1.f - slope) * tneg);
 }
 
 // tpos[q] = p where entry q of row j is (j, i) and entry p of row i is
@@ -172,23 +198,30 @@ __global__ __launch_bounds__(kBlock) void gat_mirror_kernel(int64_t n, const int
 }
 
 // dv_j = sum over row j's entries q of dpre[tpos[q]]; alpha_t[q] =
-// alpha[tpos[q]] (the transposed attention in row j's order).  One thread
-// per row.
+// alpha[tpos[q]] (the transposed attention in row j's order).  One wave per
+// row, entries in chunks of 64.
 __global__ __launch_bounds__(kBlock) void gat_mirror_sums_kernel(int64_t n, const int* __restrict__ rowptr,
                                                                  const int* __restrict__ tpos,
                                                                  const float* __restrict__ dpre,
                                                                  const float* __restrict__ alpha,
                                                                  float* __restrict__ dv,
                                                                  float* __restrict__ alpha_t) {
-  const int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int64_t j = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) >> 6;
   if (j >= n) return;
-  float s = 0.f;
-  for (int q = rowptr[j]; q < rowptr[j + 1]; ++q) {
-    const int p = tpos[q];
-    s += p >= 0 ? dpre[p] : 0.f;
-    alpha_t[q] = p >= 0 ? alpha[p] : 0.f;
+  const int e0 = rowptr[j], e1 = rowptr[j + 1];
+  float sum = 0.f;
+  for (int b = e0; b < e1; b += 64) {
+    const int q = b + lane;
+    float x = 0.f;
+    if (q < e1) {
+      const int p = tpos[q];
+      x = p >= 0 ? dpre[p] : 0.f;
+      alpha_t[q] = p >= 0 ? alpha[p] : 0.f;
+    }
+    sum += wave_sum(x);
   }
-  dv[j] = s;
+  if (lane == 0) dv[j] = sum;
 }
 
 // dP_ik += du_i a_src_k + dv_i a_dst_k.
@@ -207,28 +240,52 @@ __global__ __launch_bounds__(kBlock) void gat_rank2_kernel(int64_t n, int s, flo
   }
 }
 
-// da_src = P^T du, da_dst = P^T dv in two deterministic stages: partial sums
-// over chunks of kRowsPerChunk rows (one thread per column), then the chunks
-// summed in order.
-constexpr int kRowsPerChunk = 128;
+// da_src = P^T du, da_dst = P^T dv in two deterministic stages.  Stage 1:
+// one block per (64-column group, chunk of rows); wave w sums rows
+// r0 + w, r0 + w + 4, ... of the chunk (lane = column), then the four wave
+// sums are added in wave order.  Stage 2: per column, the chunk sums in
+// chunk order.  At most kMaxChunks chunks, each a multiple of 4 rows.
+constexpr int kMaxChunks = 1024;
 
-__global__ __launch_bounds__(kBlock) void gat_gemv_partial_kernel(int64_t n, int s, const float* __restrict__ P,
+__host__ __device__ inline int64_t gemv_rows_per_chunk(int64_t n) {
+  int64_t r = (n + kMaxChunks - 1) / kMaxChunks;
+  r = r < 64 ? 64 : r;
+  return (r + 3) / 4 * 4;
+}
+
+__global__ __launch_bounds__(kBlock) void gat_gemv_partial_kernel(int64_t n, int s, int64_t rpc,
+                                                                  const float* __restrict__ P,
                                                                   int64_t ldp, const float* __restrict__ du,
                                                                   const float* __restrict__ dv,
                                                                   float* __restrict__ part) {
-  const int k = blockIdx.x * kBlock + threadIdx.x;
+  __shared__ float red[2][kWaves][64];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int k = blockIdx.x * 64 + lane;
   const int64_t chunk = blockIdx.y;
-  if (k >= s) return;
-  const int64_t r0 = chunk * kRowsPerChunk;
-  const int64_t r1 = min<int64_t>(n, r0 + kRowsPerChunk);
+  const int64_t r0 = chunk * rpc;
+  const int64_t r1 = min<int64_t>(n, r0 + rpc);
   float a = 0.f, b = 0.f;
-  for (int64_t i = r0; i < r1; ++i) {
-    const float x = P[i * ldp + k];
-    a = fmaf(x, du[i], a);
-    b = fmaf(x, dv[i], b);
+  if (k < s) {
+    for (int64_t r = r0 + wave; r < r1; r += kWaves) {
+      const float x = P[r * ldp + k];
+      a = fmaf(x, du[r], a);
+      b = fmaf(x, dv[r], b);
+    }
   }
-  part[(chunk * 2) * s + k] = a;
-  part[(chunk * 2 + 1) * s + k] = b;
+  red[0][wave][lane] = a;
+  red[1][wave][lane] = b;
+  __syncthreads();
+  if (wave == 0 && k < s) {
+    float sa = 0.f, sb = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      sa += red[0][w][lane];
+      sb += red[1][w][lane];
+    }
+    part[(chunk * 2) * s + k] = sa;
+    part[(chunk * 2 + 1) * s + k] = sb;
+  }
 }
 
 __global__ __launch_bounds__(kBlock) void gat_gemv_final_kernel(int64_t chunks, int s,
@@ -238,6 +295,7 @@ __global__ __launch_bounds__(kBlock) void gat_gemv_final_kernel(int64_t chunks, 
   const int k = blockIdx.x * kBlock + threadIdx.x;
   if (k >= s) return;
   float a = 0.f, b = 0.f;
+#pragma unroll 8
   for (int64_t c = 0; c < chunks; ++c) {
     a += part[(c * 2) * s + k];
     b += part[(c * 2 + 1) * s + k];
@@ -281,8 +339,17 @@ gist_status gat_edge_grad(hipStream_t st, int64_t n, int64_t nnz, int s, const i
                           float* dpre, float* du) {
   ProfScope ps(st, "gat_edge_grad", 2.0 * nnz * s,
                4.0 * (static_cast<double>(nnz) * s + static_cast<double>(n) * s) + 16.0 * nnz);
-  hipLaunchKernelGGL(gat_edge_grad_kernel, dim3(rows_grid(n)), dim3(kBlock), 0, st, n, s, rowptr,
-                     col, alpha, dZ, ldz, P, ldp, u, v, slope, dpre, du);
+  // lanes per entry: a power of two giving each lane about 16 features
+  const bool vec = s % 4 == 0 && ldz % 4 == 0 && ldp % 4 == 0 &&
+                   reinterpret_cast<uintptr_t>(dZ) % 16 == 0 && reinterpret_cast<uintptr_t>(P) % 16 == 0;
+  int G = 1;
+  while (G < 64 && G * 16 < s) G <<= 1;
+  if (vec)
+    hipLaunchKernelGGL(gat_edge_grad_kernel<4>, dim3(rows_grid(n)), dim3(kBlock), 0, st, n, s, G,
+                       rowptr, col, alpha, dZ, ldz, P, ldp, u, v, slope, dpre, du);
+  else
+    hipLaunchKernelGGL(gat_edge_grad_kernel<1>, dim3(rows_grid(n)), dim3(kBlock), 0, st, n, s, G,
+                       rowptr, col, alpha, dZ, ldz, P, ldp, u, v, slope, dpre, du);
   return check_launch("gat_edge_grad");
 }
 
@@ -299,8 +366,8 @@ gist_status gat_mirror(hipStream_t st, int64_t n, int64_t nnz, const int* rowptr
 gist_status gat_mirror_sums(hipStream_t st, int64_t n, int64_t nnz, const int* rowptr, const int* tpos,
                             const float* dpre, const float* alpha, float* dv, float* alpha_t) {
   ProfScope ps(st, "gat_mirror_sums", 0.0, 16.0 * nnz + 4.0 * n);
-  hipLaunchKernelGGL(gat_mirror_sums_kernel, dim3(static_cast<unsigned>((n + kBlock - 1) / kBlock)),
-                     dim3(kBlock), 0, st, n, rowptr, tpos, dpre, alpha, dv, alpha_t);
+  hipLaunchKernelGGL(gat_mirror_sums_kernel, dim3(rows_grid(n)), dim3(kBlock), 0, st, n, rowptr,
+                     tpos, dpre, alpha, dv, alpha_t);
   return check_launch("gat_mirror_sums");
 }
 
@@ -313,20 +380,21 @@ gist_status gat_rank2(hipStream_t st, int64_t n, int s, float* dP, int64_t ld, c
 }
 
 size_t gat_gemv_workspace(int64_t n, int s) {
-  const int64_t chunks = (n + kRowsPerChunk - 1) / kRowsPerChunk;
+  const int64_t rpc = gemv_rows_per_chunk(n);
+  const int64_t chunks = (n + rpc - 1) / rpc;
   return static_cast<size_t>(chunks) * 2 * s * sizeof(float);
 }
 
 gist_status gat_gemv_t(hipStream_t st, int64_t n, int s, const float* P, int64_t ldp, const float* du,
                        const float* dv, float* da_src, float* da_dst, float* part) {
-  const int64_t chunks = (n + kRowsPerChunk - 1) / kRowsPerChunk;
-  if (chunks > 65535) return set_error(GIST_E_UNSUPPORTED, "gat: too many rows");
+  const int64_t rpc = gemv_rows_per_chunk(n);
+  const int64_t chunks = (n + rpc - 1) / rpc;
   ProfScope ps(st, "gat_gemv_t", 4.0 * n * s, 4.0 * static_cast<double>(n) * s);
-  const unsigned cx = static_cast<unsigned>((s + kBlock - 1) / kBlock);
+  const unsigned cx = static_cast<unsigned>((s + 63) / 64);
   hipLaunchKernelGGL(gat_gemv_partial_kernel, dim3(cx, static_cast<unsigned>(chunks)), dim3(kBlock),
-                     0, st, n, s, P, ldp, du, dv, part);
-  hipLaunchKernelGGL(gat_gemv_final_kernel, dim3(cx), dim3(kBlock), 0, st, chunks, s, part, da_src,
-                     da_dst);
+                     0, st, n, s, rpc, P, ldp, du, dv, part);
+  hipLaunchKernelGGL(gat_gemv_final_kernel, dim3(static_cast<unsigned>((s + kBlock - 1) / kBlock)),
+                     dim3(kBlock), 0, st, chunks, s, part, da_src, da_dst);
   return check_launch("gat_gemv_t");
 }
 

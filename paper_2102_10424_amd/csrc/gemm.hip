@@ -480,40 +480,45 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
 }
 
 // Sum the partial tiles of every tile split between workgroups, in
-// workgroup order, and apply the epilogue.  One block per tile; the partial
-// slots are resolved once per tile, then each thread sums float4 columns.
+// workgroup order, and apply the epilogue.  Grid: (tile, 8-row chunk of the
+// tile), so that a tile split over many workgroups (a thin dW = H^T dZ with
+// a long K) is still summed by 16 blocks; each thread sums one float4 of
+// every partial, in workgroup order (bitwise the same for any grid shape).
 constexpr int kMaxFixupParts = 1024;
+constexpr int kFixRows = 8;
+constexpr int kFixChunks = BM / kFixRows;
+static_assert(kFixRows * BN == 4 * 256, "one float4 per thread per partial");
 
 __global__ __launch_bounds__(256) void streamk_fixup(int64_t M, int64_t N, Sched S,
                                                      const float* __restrict__ partials,
                                                      OutDev C) {
   __shared__ int64_t slot_off[kMaxFixupParts];
   const int64_t t = blockIdx.x;
+  const int chunk = blockIdx.y;
   const int64_t w_first = (t * S.nk) / S.ipw;
   const int64_t w_last = ((t + 1) * S.nk - 1) / S.ipw;
   if (w_first == w_last) return;  // computed whole and stored by one workgroup
+  const int64_t grp = t / S.tpg;
+  int tm, tn;
+  tile_coords_banded(t - grp * S.tpg, S.tiles_m, S.tiles_n, tm, tn);
+  const int64_t m0 = static_cast<int64_t>(tm) * BM, n0 = static_cast<int64_t>(tn) * BN;
+  if (m0 + chunk * kFixRows >= M) return;   // the chunk lies below the matrix
   const int parts = static_cast<int>(w_last - w_first + 1);
   for (int j = threadIdx.x; j < parts; j += 256) {
     const int64_t w = w_first + j;
     slot_off[j] = (w * 2 + (((w * S.ipw) / S.nk) == t ? 0 : 1)) * (BM * BN);
   }
   __syncthreads();
-  const int64_t grp = t / S.tpg;
   const OutDev Cg = C.group(grp);
-  int tm, tn;
-  tile_coords_banded(t - grp * S.tpg, S.tiles_m, S.tiles_n, tm, tn);
-  const int64_t m0 = static_cast<int64_t>(tm) * BM, n0 = static_cast<int64_t>(tn) * BN;
-  for (int e4 = threadIdx.x; e4 < BM * BN / 4; e4 += 256) {
-    const int e = e4 * 4;
-    const int64_t row = m0 + e / BN, col = n0 + e % BN;
-    if (row >= M || col >= N) continue;
-    floatx4 s = {0.f, 0.f, 0.f, 0.f};
-    for (int j = 0; j < parts; ++j)
-      s += *reinterpret_cast<const floatx4*>(partials + slot_off[j] + e);
+  const int e = chunk * kFixRows * BN + threadIdx.x * 4;
+  const int64_t row = m0 + e / BN, col = n0 + e % BN;
+  if (row >= M || col >= N) return;
+  floatx4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+  for (int j = 0; j < parts; ++j) s += *reinterpret_cast<const floatx4*>(partials + slot_off[j] + e);
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (col + q < N) store_out(Cg, row, col + q, s[q]);
-  }
+  for (int q = 0; q < 4; ++q)
+    if (col + q < N) store_out(Cg, row, col + q, s[q]);
 }
 
 constexpr int64_t kStreamWG = 512;   // two resident 256-thread blocks per CU, 256 CUs
@@ -658,8 +663,8 @@ gist_status gemm(hipStream_t st, int64_t M, int64_t N, int64_t K, const Operand&
   if (split) {
     ProfScope ps(st, "gemm_streamk_fixup", 0.0,
                  4.0 * static_cast<double>(groups) * 2 * BM * BN + 4.0 * M * N * ngroups);
-    hipLaunchKernelGGL(streamk_fixup, dim3(static_cast<unsigned>(tiles)), dim3(256), 0, st, M, N,
-                       S, part, c);
+    hipLaunchKernelGGL(streamk_fixup, dim3(static_cast<unsigned>(tiles), kFixChunks), dim3(256), 0,
+                       st, M, N, S, part, c);
     return check_launch("gemm stream-K fix-up");
   }
   return GIST_OK;

@@ -79,9 +79,12 @@ class BatchSlot:
         self.X = torch.empty(cap_n, d_in, device=device)
         self.d_in = d_in
         self.uploaded = None
+        self.built = None
 
-    def load(self, graph_struct, clusters, X_dev, labels_host):
-        """Build, upload and gather; returns a batch view with n, nnz, A, A_T, X, labels."""
+    def build(self, graph_struct, clusters, labels_host):
+        """Host half of ``load``: the mini-batch CSR and labels into the pinned
+        staging buffers (after the previous upload from them has completed).
+        Touches no device memory, so it may run on a worker thread."""
         if self.uploaded is not None:
             self.uploaded.synchronize()  # previous upload from the staging buffers done
         q = G.gist_csr()
@@ -96,6 +99,13 @@ class BatchSlot:
         n, nnz = int(q.n), int(q.nnz)
         nm = h["node_map"].numpy()[:n]
         h["labels"].numpy()[:n] = labels_host[nm]
+        self.built = (n, nnz)
+
+    def upload(self, X_dev):
+        """Device half of ``load``: asynchronous uploads of the built batch on
+        the current stream and the device gather of its feature rows."""
+        n, nnz = self.built
+        h = self.h
         for k in h:
             cnt = n + 1 if k.endswith("rowptr") else (nnz if k.endswith(("col", "val")) else n)
             if cnt:
@@ -107,6 +117,58 @@ class BatchSlot:
         G.gist_gather_slice(self.ctx, X_dev, self.d_in, self.d["node_map"], n, None,
                             self.d_in, Xb, self.d_in)
         return _View(n, nnz, self.d, Xb, self.sage)
+
+    def load(self, graph_struct, clusters, X_dev, labels_host):
+        """Build, upload and gather; returns a batch view with n, nnz, A, A_T, X, labels."""
+        self.build(graph_struct, clusters, labels_host)
+        return self.upload(X_dev)
+
+
+class BatchPipeline:
+    """Cluster mini-batches built ahead of use on host worker threads.
+
+    A ring of ``depth`` :class:`BatchSlot` s; batch k is built (host CSR,
+    ``gist_build_minibatch_csr`` -- which releases the interpreter lock) into
+    slot k mod depth by a pool of ``workers`` threads while earlier batches
+    are uploaded and trained on.  ``next()`` returns the batches in the order
+    of ``clusters_iter``; each is uploaded on the current stream when it is
+    taken, after every kernel enqueued on the slot's previous batch, so a
+    slot's device buffers are never overwritten while in use.
+    """
+
+    def __init__(self, ctx, norm, cap_n, cap_nnz, d_in, graph_struct, X_dev, labels_host,
+                 clusters_iter, depth=8, workers=4):
+        from collections import deque
+        from concurrent.futures import ThreadPoolExecutor
+        self.slots = [BatchSlot(ctx, norm, cap_n, cap_nnz, d_in) for _ in range(depth)]
+        self.graph, self.X, self.labels = graph_struct, X_dev, labels_host
+        self.src = iter(clusters_iter)
+        self.pool = ThreadPoolExecutor(max_workers=workers)
+        self.pending = deque()
+        self.k = 0           # next batch to submit
+        for _ in range(depth):
+            self._submit()
+
+    def _submit(self):
+        try:
+            clusters = next(self.src)
+        except StopIteration:
+            return
+        slot = self.slots[self.k % len(self.slots)]
+        self.pending.append((slot, self.pool.submit(slot.build, self.graph, clusters, self.labels)))
+        self.k += 1
+
+    def next(self):
+        slot, fut = self.pending.popleft()
+        fut.result()
+        view = slot.upload(self.X)
+        self._submit()       # reuses this slot: its build waits for the upload just enqueued
+        return view
+
+    def close(self):
+        for _, fut in self.pending:
+            fut.cancel()
+        self.pool.shutdown(wait=True)
 
 
 class _View:

@@ -1,4 +1,5 @@
-"""Sub-GCN step parity at the workloads' real shapes (c1-c4), fp32.
+"""Sub-GCN step parity at the workloads' real shapes (c1-c4, and the GAT
+workload c6), fp32 (and bf16-input GEMMs where noted).
 
 Two views of the same step, both through the C ABI:
 
@@ -13,7 +14,8 @@ Two views of the same step, both through the C ABI:
   GPU's ReLU decisions must equal the oracle's except where the oracle's
   pre-activation lies within rounding distance of zero (|Z| <= 1e-5 max|Z|,
   where either decision is correct); if no decision differs, every
-  gradient and updated weight is compared within 1e-4 too.
+  gradient and updated weight is compared within 1e-4 too.  For GAT the
+  same holds for the LeakyReLU decisions of the attention scores.
 """
 
 import numpy as np
@@ -49,9 +51,13 @@ def workload(name):
     for l, (r, c) in enumerate(sl):
         ps = []
         for p in range(cfg.n_parts()):
-            th = cfg.theta(l, p, rows=r) if r is not None else cfg.theta(l, p)
+            rr = None if cfg.kind == "gat" and p == 1 else r     # attention rows: all
+            th = cfg.theta(l, p, rows=rr) if rr is not None else cfg.theta(l, p)
             ps.append(np.ascontiguousarray(th if c is None else th[:, c]))
-        params.append(ps[0] if cfg.kind == "gcn" else (ps[0], ps[1]))
+        if cfg.kind == "gat":
+            params.append((ps[0], ps[1][0], ps[1][1]))
+        else:
+            params.append(ps[0] if cfg.kind == "gcn" else (ps[0], ps[1]))
     clusters = cfg.minibatch(0, 0)
     csr = OM.build(g, clusters, norm)
     nm = csr["node_map"]
@@ -67,6 +73,8 @@ def workload(name):
 
 
 def stacked(kind, p):
+    if kind == "gat":
+        return np.concatenate([p[0], p[1][None], p[2][None]], axis=0)
     return p if kind == "gcn" else np.concatenate([p[0], p[1]], axis=0)
 
 
@@ -141,7 +149,52 @@ def ref_params(w, l):
     return w["params"][l]
 
 
-@pytest.mark.parametrize("name", CONFIGS)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_step_layerwise_gat(G, ctx, dtype):
+    """c6: every GAT layer call of the step at the mini-batch shape, fed the
+    oracle's intermediate values; transform, attention, output and all
+    gradients against the oracle."""
+    import torch
+    name = "c6"
+    w = workload(name)
+    dt = G.GIST_DTYPE_BF16_IN if dtype == "bf16" else G.GIST_DTYPE_F32
+    tol = BF16_TOL if dtype == "bf16" else FP32_TOL
+    cfg, csr, ref = w["cfg"], w["csr"], w["ref"]
+    s = cfg.slice_widths()
+    L, n, nnz = cfg.L, csr["n"], csr["nnz"]
+    A, k1 = csr_to_dev(csr)
+    for l in range(L):
+        act = G.GIST_ACT_RELU if l < L - 1 else G.GIST_ACT_NONE
+        desc = G.gat_desc(n, nnz, s[l], s[l + 1], act, dt, OG.GAT_SLOPE)
+        fws, bws = G.gist_gat_workspace_size(desc)
+        ws = torch.empty(max(fws, bws, 1), dtype=torch.uint8, device="cuda")
+        Wp, a1, a2 = (to_dev(np.asarray(x, dtype=np.float32)) for x in w["params"][l])
+        Hin = to_dev(ref["H"][l].astype(np.float32))
+        P = torch.empty(n, s[l + 1], device="cuda")
+        alpha = torch.empty(nnz, device="cuda")
+        Ho = torch.empty(n, s[l + 1], device="cuda")
+        G.gist_gat_layer_fwd(ctx, desc, A, Hin, Wp, a1, a2, P, alpha, Ho, ws)
+        rec = ref["recs"][l]
+        e_f = max(relerr(to_host(P), rec["P"]), relerr(to_host(alpha), rec["alpha"]),
+                  relerr(to_host(Ho), rec["H_out"]))
+        dHo = ref["dH"][l + 1] if l + 1 < L else ref["dlogits"]
+        dW = torch.empty(s[l], s[l + 1], device="cuda")
+        g1 = torch.empty(s[l + 1], device="cuda")
+        g2 = torch.empty(s[l + 1], device="cuda")
+        dH = torch.empty(n, s[l], device="cuda") if l > 0 else None
+        G.gist_gat_layer_bwd(ctx, desc, A, Hin, to_dev(rec["P"].astype(np.float32)),
+                             to_dev(rec["alpha"].astype(np.float32)),
+                             to_dev(rec["H_out"].astype(np.float32)), Wp, a1, a2,
+                             to_dev(np.asarray(dHo, dtype=np.float32)), dW, g1, g2, dH, ws)
+        gW, ga1, ga2 = ref["grads"][l]
+        e_b = max(relerr(to_host(dW), gW), relerr(to_host(g1), ga1), relerr(to_host(g2), ga2),
+                  relerr(to_host(dH), ref["dH"][l]) if l > 0 else 0.0)
+        log(f"[{name} {dtype}] GAT layer {l} ({s[l]}->{s[l + 1]}, n={n}, nnz={nnz}): "
+            f"forward {e_f:.2e} backward {e_b:.2e}")
+        assert e_f <= tol and e_b <= tol
+
+
+@pytest.mark.parametrize("name", CONFIGS + ["c6"])
 def test_step_chained(G, ctx, name):
     import torch
     from paper_2102_10424_amd.step import BatchSlot, SubGCN
@@ -172,6 +225,9 @@ def test_step_chained(G, ctx, name):
             band = 1e-5 * np.max(np.abs(Z))
             assert np.all(np.abs(Z[diff]) <= band), "ReLU decision differs outside rounding band"
             mism += int(diff.sum())
+        if kind == "gat":     # LeakyReLU decisions of scores near zero may differ too
+            pre = ref["recs"][l]["pre"]
+            mism += int(np.sum(np.abs(pre) <= 1e-5 * np.max(np.abs(pre))))
     loss = float(to_host(run.loss)[0])
     assert abs(loss - ref["loss"]) <= FP32_TOL * abs(ref["loss"])
     log(f"[{name}] chained loss {loss:.6f} (oracle {ref['loss']:.6f}); "
