@@ -324,73 +324,108 @@ __device__ __forceinline__ int wave_max_int(int v) {
 // gather half stages that run in LDS at (position - first) and stores it
 // with consecutive lanes instead of one sparse store per column; a wave
 // whose owned positions are not contiguous stores them one by one.
+//
+// A block covers kRowChunks chunks of 1024 columns of one row: every
+// thread issues its kRowChunks Theta loads before the row's owner is
+// resolved (a chain of dependent loads: rank, block search, slice
+// pointer), which is done once per block, so each block keeps 16 KB in
+// flight behind one latency chain.
+constexpr int kRowChunks = 4;
+
 template <bool DONE, bool NEXT>
 __global__ __launch_bounds__(kBlock) void subagg_gather_rows_kernel(
-    float* __restrict__ Wg, int64_t rows, int64_t cols, int64_t ldg, int64_t chunks, int m,
+    float* __restrict__ Wg, int64_t rows, int64_t cols, int64_t ldg, int64_t groups, int m,
     SliceSetDev done, SliceSetDev next) {
-  __shared__ float stage[kBlock / 64][256];
+  __shared__ float stage[kRowChunks][kBlock / 64][256];
   const int64_t b = xcd_remap(blockIdx.x, gridDim.x);
-  const int64_t r = b / chunks;
+  const int64_t r = b / groups;
   if (r >= rows) return;   // block-uniform
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int64_t c0 = (b - r * chunks) * (4 * kBlock) + 4 * static_cast<int64_t>(threadIdx.x);
-  const bool in = c0 < cols;   // cols % 4 == 0: a group is wholly in or out
-  float* __restrict__ w = Wg + r * ldg + c0;
-  float v[4] = {0.f, 0.f, 0.f, 0.f};
-  if (in) {
-    const float4 t = *reinterpret_cast<const float4*>(w);
-    v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+  const int64_t g0 = (b - r * groups) * (kRowChunks * 4 * kBlock) + 4 * static_cast<int64_t>(threadIdx.x);
+  float* __restrict__ wrow = Wg + r * ldg;
+  float v[kRowChunks][4];
+  bool in[kRowChunks];
+#pragma unroll
+  for (int j = 0; j < kRowChunks; ++j) {
+    const int64_t c0 = g0 + j * (4 * kBlock);
+    in[j] = c0 < cols;   // cols % 4 == 0: a group is wholly in or out
+    float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (in[j]) t = *reinterpret_cast<const float4*>(wrow + c0);
+    v[j][0] = t.x; v[j][1] = t.y; v[j][2] = t.z; v[j][3] = t.w;
   }
   // Column keys: the rank when the columns are partitioned, else the
   // column itself (owned by every row owner); -1 outside the matrix.
-  int kd[4], kn[4];
+  int kd[kRowChunks][4], kn[kRowChunks][4];
   RowSel qd{nullptr, 0, 0}, qn{nullptr, 0, 0};
-  if (DONE) {
-    if (done.col_rank && in) ranks4<true>(done.col_rank, c0, 4, kd);
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (!done.col_rank || !in) kd[q] = in ? static_cast<int>(c0 + q) : -1;
+  for (int j = 0; j < kRowChunks; ++j) {
+    const int64_t c0 = g0 + j * (4 * kBlock);
+    if (DONE) {
+      if (done.col_rank && in[j]) ranks4<true>(done.col_rank, c0, 4, kd[j]);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (!done.col_rank || !in[j]) kd[j][q] = in[j] ? static_cast<int>(c0 + q) : -1;
+    }
+    if (NEXT) {
+      if (next.col_rank && in[j]) ranks4<true>(next.col_rank, c0, 4, kn[j]);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (!next.col_rank || !in[j]) kn[j][q] = in[j] ? static_cast<int>(c0 + q) : -1;
+    }
+  }
+  if (DONE) {
     qd = row_select(done, m, r);
     if (!done.col_rank) { qd.lo = 0; qd.hi = cols; }
   }
   if (NEXT) {
-    if (next.col_rank && in) ranks4<true>(next.col_rank, c0, 4, kn);
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (!next.col_rank || !in) kn[q] = in ? static_cast<int>(c0 + q) : -1;
     qn = row_select(next, m, r);
     if (!next.col_rank) { qn.lo = 0; qn.hi = cols; }
   }
   if (DONE) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (kd[q] >= qd.lo && kd[q] < qd.hi) v[q] = qd.base[kd[q] - qd.lo];
-    if (in) *reinterpret_cast<float4*>(w) = make_float4(v[0], v[1], v[2], v[3]);
+    for (int j = 0; j < kRowChunks; ++j) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (kd[j][q] >= qd.lo && kd[j][q] < qd.hi) v[j][q] = qd.base[kd[j][q] - qd.lo];
+      if (in[j])
+        *reinterpret_cast<float4*>(wrow + g0 + j * (4 * kBlock)) =
+            make_float4(v[j][0], v[j][1], v[j][2], v[j][3]);
+    }
   }
   if (NEXT) {
-    int first = INT32_MAX, last = -1, cnt = 0;
+    int first[kRowChunks], cnt[kRowChunks];
+    bool run[kRowChunks];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const bool own = kn[q] >= qn.lo && kn[q] < qn.hi;
-      if (own) { first = min(first, kn[q]); last = max(last, kn[q]); }
-      cnt += __popcll(__ballot(own));
-    }
-    first = wave_min_int(first);
-    last = wave_max_int(last);
-    const bool run = cnt > 0 && last - first + 1 == cnt;   // wave-uniform
-    if (run) {
+    for (int j = 0; j < kRowChunks; ++j) {
+      int f = INT32_MAX, l = -1, c = 0;
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if (kn[q] >= qn.lo && kn[q] < qn.hi) stage[wv][kn[q] - first] = v[q];
-    } else {
+      for (int q = 0; q < 4; ++q) {
+        const bool own = kn[j][q] >= qn.lo && kn[j][q] < qn.hi;
+        if (own) { f = min(f, kn[j][q]); l = max(l, kn[j][q]); }
+        c += __popcll(__ballot(own));
+      }
+      f = wave_min_int(f);
+      l = wave_max_int(l);
+      first[j] = f;
+      cnt[j] = c;
+      run[j] = c > 0 && l - f + 1 == c;   // wave-uniform
+      if (run[j]) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if (kn[q] >= qn.lo && kn[q] < qn.hi) qn.base[kn[q] - qn.lo] = v[q];
+        for (int q = 0; q < 4; ++q)
+          if (kn[j][q] >= qn.lo && kn[j][q] < qn.hi) stage[j][wv][kn[j][q] - f] = v[j][q];
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (kn[j][q] >= qn.lo && kn[j][q] < qn.hi) qn.base[kn[j][q] - qn.lo] = v[j][q];
+      }
     }
     __syncthreads();
-    if (run) {
-      float* dst = qn.base + (first - qn.lo);
-      for (int j = lane; j < cnt; j += 64) dst[j] = stage[wv][j];
+#pragma unroll
+    for (int j = 0; j < kRowChunks; ++j) {
+      if (run[j]) {
+        float* dst = qn.base + (first[j] - qn.lo);
+        for (int i = lane; i < cnt[j]; i += 64) dst[i] = stage[j][wv][i];
+      }
     }
   }
 }
@@ -469,15 +504,17 @@ gist_status subagg_gather(hipStream_t st, float* Wg, int64_t rows, int64_t cols,
   ProfScope ps(st, vec && rows_part ? "subagg_gather_rows" : "subagg_gather", 0.0, bytes);
   if (vec && rows_part) {
     const int dn = done ? 1 : 0, nx = next ? 1 : 0;
+    const int64_t groups = (chunks + kRowChunks - 1) / kRowChunks;
+    const dim3 rgrid(static_cast<unsigned>(rows * groups));
     if (dn && nx)
-      hipLaunchKernelGGL((subagg_gather_rows_kernel<true, true>), grid, dim3(kBlock), 0, st, Wg,
-                         rows, cols, ldg, chunks, m, d, n);
+      hipLaunchKernelGGL((subagg_gather_rows_kernel<true, true>), rgrid, dim3(kBlock), 0, st, Wg,
+                         rows, cols, ldg, groups, m, d, n);
     else if (dn)
-      hipLaunchKernelGGL((subagg_gather_rows_kernel<true, false>), grid, dim3(kBlock), 0, st, Wg,
-                         rows, cols, ldg, chunks, m, d, n);
+      hipLaunchKernelGGL((subagg_gather_rows_kernel<true, false>), rgrid, dim3(kBlock), 0, st, Wg,
+                         rows, cols, ldg, groups, m, d, n);
     else
-      hipLaunchKernelGGL((subagg_gather_rows_kernel<false, true>), grid, dim3(kBlock), 0, st, Wg,
-                         rows, cols, ldg, chunks, m, d, n);
+      hipLaunchKernelGGL((subagg_gather_rows_kernel<false, true>), rgrid, dim3(kBlock), 0, st, Wg,
+                         rows, cols, ldg, groups, m, d, n);
   } else if (vec) {
     hipLaunchKernelGGL(subagg_gather_kernel<true>, grid, dim3(kBlock), 0, st, Wg, rows, cols, ldg,
                        chunks, m, d, done ? 1 : 0, n, next ? 1 : 0);
