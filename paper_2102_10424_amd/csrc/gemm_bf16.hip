@@ -48,6 +48,14 @@ constexpr int kMaxSplit = 8;
 constexpr int kPad = 256;            // row padding of the bf16 copies (tile edge)
 constexpr int kPadK = 64;            // K padding (conversion tile)
 
+// Workgroup barrier that orders LDS only: waits for this wave's LDS
+// accesses, not its global loads, so prefetches stay in flight across it.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 __device__ __forceinline__ unsigned short bf16_bits(float f) {
   return __builtin_bit_cast(unsigned short, static_cast<__bf16>(f));
 }
@@ -219,7 +227,7 @@ __global__ __launch_bounds__(kThr) void gemm_bf16_kernel(int64_t M, int64_t N,
     mfma8(f1);
     __builtin_amdgcn_sched_barrier(0);
     if (j + 2 < ke) gload(static_cast<int64_t>(j + 2) * TK);
-    __syncthreads();
+    lds_barrier();
   }
 
   // acc[a][b] register r of lane l: tile row wm*128 + a*32 + 8(r/4) +
