@@ -58,7 +58,11 @@ def variant_symbol(variant):
         "gemm_streamk_fixup": r"streamk_fixup", "subagg_gather_rows": r"subagg_gather_rows_kernel<",
         "subagg_gather": r"subagg_gather_kernel<", "gather_slice": r"gather_kernel",
         "subagg_scatter": r"scatter_kernel", "sgd_update": r"sgd_kernel",
-        "relu_mask": r"relu_mask_kernel",
+        "relu_mask": r"relu_mask_kernel", "subagg_mean": r"subagg_mean_kernel",
+        "gat_scores": r"gat_scores_kernel", "gat_softmax": r"gat_softmax_kernel",
+        "gat_edge_grad": r"gat_edge_grad_kernel<", "gat_mirror": r"gat_mirror_kernel",
+        "gat_mirror_sums": r"gat_mirror_sums_kernel", "gat_rank2": r"gat_rank2_kernel",
+        "gat_gemv_t": r"gat_gemv_partial_kernel",
     }
     return "^" + table[variant] if variant in table else None
 
@@ -108,7 +112,7 @@ def main():
     for k in ("bench", "trace", "fetch", "write", "calib_fetch", "calib_write", "title", "out"):
         ap.add_argument("--" + k.replace("_", "-"), required=True)
     ap.add_argument("--cmd", action="append", default=[])
-    ap.add_argument("--workload", required=True, help="config name the run used (c1..c5)")
+    ap.add_argument("--workload", required=True, help="config name the run used (c1..c6)")
     a = ap.parse_args()
     res = json.load(open(a.bench))
     steps = res["steps"]
