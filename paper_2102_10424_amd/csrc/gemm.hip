@@ -96,10 +96,16 @@ __device__ __forceinline__ float op_elem(const OpDev& o, int64_t r, int64_t k) {
 //   K-contiguous operands: 8 threads cover one row's 32 K values (128 B).
 //   Row-contiguous, scalar: consecutive threads take consecutive rows at one
 //     K and read 4 K values each.
-//   Row-contiguous, vector: each thread owns a 4 x 4 block (rows rr..rr+3,
-//     K values kk..kk+3) and loads it as 4 row vectors, one per K value
-//     (32 threads cover one K's 128 rows, 512 B); group i is the vector at
-//     K value kk + i, transposed into rows when staged.
+//   Row-contiguous, vector: each thread owns a 4 x 4 block (rows 4g..4g+3,
+//     K values 4q..4q+3) and loads it as 4 row vectors, one per K value;
+//     group i is the vector at K value 4q + i, transposed into rows when
+//     staged.  Lane bits (0 | 1-2 | 3-5) of a wave pick (g mod 2 | q mod 4 |
+//     g / 2 mod 8); the wave picks g / 16 and q / 4.  Each run of eight
+//     lanes (one LDS write pass) then holds both row-block parities times
+//     four K groups, so its 16-byte stores into the [row][k] tile (row
+//     stride LDK = 36 floats) land in eight distinct groups of four banks;
+//     with consecutive row blocks per run they fell into two (4-way
+//     conflicts).  Sixteen lanes still read 256 contiguous bytes per K value.
 template <bool KMAJ, bool VEC>
 __device__ __forceinline__ void tile_coord(int i, int& rr, int& kk) {
   const int idx = threadIdx.x + kThreads * i;
@@ -107,8 +113,9 @@ __device__ __forceinline__ void tile_coord(int i, int& rr, int& kk) {
     rr = idx >> 3;
     kk = (idx & 7) * 4;
   } else if constexpr (VEC) {
-    rr = (threadIdx.x & 31) * 4;
-    kk = (threadIdx.x >> 5) * 4 + i;
+    const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+    rr = 4 * ((l & 1) + 2 * ((l >> 3) & 7) + 16 * (w & 1));
+    kk = 4 * (((l >> 1) & 3) + 4 * (w >> 1)) + i;
   } else {
     rr = idx & 127;
     kk = (idx >> 7) * 4;
@@ -197,7 +204,8 @@ __device__ __forceinline__ void store_tile_f32(float* lds, const floatx4 (&reg)[
   if constexpr (!KMAJ && VEC) {
     floatx4 rows[4];
     transpose4(reg, rows);
-    const int rr = (threadIdx.x & 31) * 4, kk = (threadIdx.x >> 5) * 4;
+    int rr, kk;
+    tile_coord<KMAJ, VEC>(0, rr, kk);
 #pragma unroll
     for (int j = 0; j < 4; ++j) *reinterpret_cast<floatx4*>(lds + (rr + j) * LDK + kk) = rows[j];
   } else {
@@ -234,7 +242,8 @@ __device__ __forceinline__ void store_tile_bf16(unsigned short* lds, const float
   if constexpr (!KMAJ && VEC) {
     floatx4 rows[4];
     transpose4(reg, rows);
-    const int rr = (threadIdx.x & 31) * 4, kk = (threadIdx.x >> 5) * 4;
+    int rr, kk;
+    tile_coord<KMAJ, VEC>(0, rr, kk);
 #pragma unroll
     for (int j = 0; j < 4; ++j) put(rr + j, kk, rows[j]);
   } else {
