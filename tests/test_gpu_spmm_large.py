@@ -4,7 +4,8 @@ well as normwise: the GCN forward aggregation on a clustered graph at
 widths that fill one 64-lane column tile, leave a ragged tile and span
 several, and on a cluster-free (Erdos-Renyi) graph; and the SAGE backward
 dH = dZ W_self^T + Abar^T (dZ W_neigh^T), whose transposed aggregation adds
-the self term inside the kernel."""
+the self term (already in dH: the Add operand aliases the output) inside the
+kernel."""
 
 import numpy as np
 import pytest
