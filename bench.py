@@ -98,6 +98,8 @@ def parse():
     ap.add_argument("--adam-policy", default="carry", choices=["carry", "reset"],
                     help="Adam moments at subAgg: carried with the weights, or reset per round")
     ap.add_argument("--zeta", type=int, default=1, help="local steps per sub-GCN per round")
+    ap.add_argument("--streams", type=int, default=1,
+                    help="HIP streams the m sub-GCN steps of a round are spread over")
     ap.add_argument("--shared-batch", action="store_true",
                     help="all m sub-GCNs step on one shared mini-batch, as batched layer calls")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -112,7 +114,8 @@ def parse():
 class RoundWorkload:
     """A GIST round (partition, gather, m sub-GCN steps, subAgg) on one GPU."""
 
-    def __init__(self, cfg, ctx, dtype, optimizer="sgd", policy="carry", zeta=1, shared=False):
+    def __init__(self, cfg, ctx, dtype, optimizer="sgd", policy="carry", zeta=1, shared=False,
+                 streams=1):
         import torch
         from paper_2102_10424_amd import gist as G
         from paper_2102_10424_amd.step import (BatchPipeline, BatchSlot, GistModel, SubGCN,
@@ -146,37 +149,49 @@ class RoundWorkload:
             cap_nnz = int(np.sort(np.diff(self.graph.rowptr))[-cap_n:].sum()) + cap_n
         self.full = None
         self.pipe = None
+        # sub-GCN i of a round runs on stream i mod streams (its own context,
+        # runner buffers and mini-batch pipeline); stream 0 is torch's current
+        self.nstreams = 1 if shared else max(1, streams)
+        self.streams = [torch.cuda.current_stream()] + [torch.cuda.Stream()
+                                                         for _ in range(self.nstreams - 1)]
+        self.ctxs = [ctx] + [G.Context(0, stream=st.cuda_stream) for st in self.streams[1:]]
         if cfg.batch_clusters is None:
             self.slots = [BatchSlot(ctx, self.norm, cap_n, cap_nnz, cfg.widths[0])]
         else:
             # mini-batches are built on host worker threads ahead of use
-            self.pipe = BatchPipeline(ctx, self.norm, cap_n, cap_nnz, cfg.widths[0], self.gh,
-                                      self.X, self.labels, self._cluster_order(shared, zeta),
-                                      depth=8, workers=4)
+            self.pipes = [BatchPipeline(c, self.norm, cap_n, cap_nnz, cfg.widths[0], self.gh,
+                                        self.X, self.labels,
+                                        self._cluster_order(shared, zeta, k, self.nstreams),
+                                        depth=8, workers=4 if self.nstreams == 1 else 2)
+                          for k, c in enumerate(self.ctxs)]
+            self.pipe = self.pipes[0]
         dt = G.GIST_DTYPE_BF16_IN if dtype == "bf16" else G.GIST_DTYPE_F32
         self.shared = shared
         if shared:
             self.runner = SubGCNBatch(ctx, cfg.kind, self.model.slice_widths, cfg.m, cap_n, dtype=dt)
         else:
-            self.runner = SubGCN(ctx, cfg.kind, self.model.slice_widths, cap_n, dtype=dt)
+            self.runners = [SubGCN(c, cfg.kind, self.model.slice_widths, cap_n, dtype=dt)
+                            for c in self.ctxs]
+            self.runner = self.runners[0]
         self.lr = 0.01
         self.t = 0
 
-    def _cluster_order(self, shared, zeta):
-        """The clusters of every mini-batch, in the order the rounds take them."""
+    def _cluster_order(self, shared, zeta, k=0, nstreams=1):
+        """The clusters of every mini-batch of stream k, in the order the
+        rounds take them (sub-GCNs k, k + nstreams, ...)."""
         cfg, t = self.cfg, 0
         while True:
-            for i in range(1 if shared else cfg.m):
+            for i in range(k, 1 if shared else cfg.m, nstreams):
                 for z in range(zeta):
                     yield cfg.minibatch(t, i, z)
             t += 1
 
-    def _batch(self, t, i, z):
+    def _batch(self, t, i, z, k=0):
         if self.cfg.batch_clusters is None:
             if self.full is None:
                 self.full = self.slots[0].load(self.gh, None, self.X, self.labels)
             return self.full
-        return self.pipe.next()
+        return self.pipes[k].next()
 
     def step(self):
         cfg, m = self.cfg, self.model
@@ -194,22 +209,34 @@ class RoundWorkload:
             m.end_round()
             self.t += 1
             return
+        import torch
+        if self.nstreams > 1:   # the other streams start after the fused pass
+            ev = torch.cuda.Event()
+            ev.record(self.streams[0])
+            for st in self.streams[1:]:
+                st.wait_event(ev)
         for i in range(cfg.m):
-            for z in range(zeta):
-                b = self._batch(t, i, z)
-                opt = None
-                if self.adam == "carry":
-                    opt = (m.M[i], m.V[i], t * zeta + z + 1, False)
-                elif self.adam == "reset":
-                    opt = (m.M[i], m.V[i], z + 1, z == 0)
-                self.runner.step(b, m.params[i], self.lr, adam=opt)
+            k = i % self.nstreams
+            with torch.cuda.stream(self.streams[k]):
+                for z in range(zeta):
+                    b = self._batch(t, i, z, k)
+                    opt = None
+                    if self.adam == "carry":
+                        opt = (m.M[i], m.V[i], t * zeta + z + 1, False)
+                    elif self.adam == "reset":
+                        opt = (m.M[i], m.V[i], z + 1, z == 0)
+                    self.runners[k].step(b, m.params[i], self.lr, adam=opt)
+        for st in self.streams[1:]:   # subAgg waits for every stream's steps
+            ev = torch.cuda.Event()
+            ev.record(st)
+            self.streams[0].wait_event(ev)
         m.end_round()
         self.t += 1
 
     def finish(self):
         self.model.finalize()
-        if self.pipe is not None:
-            self.pipe.close()
+        for p in getattr(self, "pipes", []):
+            p.close()
 
     def steps_per_unit(self):
         return self.cfg.m * self.zeta
@@ -373,14 +400,16 @@ def main():
         wl = LayerWorkload(cfg, ctx, args.dtype, args.d_in)
     else:
         wl = RoundWorkload(cfg, ctx, args.dtype, args.optimizer, args.adam_policy, args.zeta,
-                           args.shared_batch)
+                           args.shared_batch, args.streams)
         wl.lr = args.lr
+    ctxs = getattr(wl, "ctxs", [ctx])
     for w in range(args.warmup):
         wl.step()
         torch.cuda.synchronize()
         log(f"[bench] warmup {w + 1}/{args.warmup} done")
     if not args.no_profile:
-        G.gist_profile_begin(ctx, 1 << 16)
+        for c in ctxs:
+            G.gist_profile_begin(c, 1 << 16)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
@@ -391,8 +420,14 @@ def main():
     ms_step = (t1 - t0) * 1e3 / args.steps
     prof, dropped = ({}, 0)
     if not args.no_profile:
-        prof, dropped = G.gist_profile_read(ctx)
-        G.gist_profile_end(ctx)
+        for c in ctxs:   # every stream's launches (their event times may overlap)
+            p, d = G.gist_profile_read(c)
+            G.gist_profile_end(c)
+            dropped += d
+            for k, v in p.items():
+                acc = prof.setdefault(k, dict(launches=0, ms=0.0, flops=0.0, bytes=0.0))
+                for f in acc:
+                    acc[f] += v[f]
     wl.finish()   # a deferred subAgg (after the timed region and the profile)
     kernels = {}
     for k, v in sorted(prof.items(), key=lambda kv: -kv[1]["ms"]):
