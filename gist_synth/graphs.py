@@ -6,7 +6,7 @@ strictly ascending within each row) plus a clustering (``cluster_ptr``
 int64[c+1], ``cluster_nodes`` int32[n]).  Node ids are block-contiguous, so
 cluster ``b`` is the id range ``[cluster_ptr[b], cluster_ptr[b+1])`` -- the
 order a METIS-reordered graph would have (the paper clusters with METIS,
-Section 3, and ClusterGCN-style mini-batches are unions of clusters).
+Section 2, and ClusterGCN-style mini-batches are unions of clusters).
 
 Three families cover the workloads' degree structure:
 

@@ -3,9 +3,9 @@
  *
  * GIST ("Graph Independent Subnetwork Training", Algorithm 1) splits every
  * hidden feature dimension of a GCN into m disjoint random blocks (subGCNs,
- * Section 3.1), trains each narrow sub-GCN on cluster mini-batches
- * (subTrain, Section 3.2) and copies the trained weight slices back into the
- * global model (subAgg, Section 3.2).  This library provides the pieces of
+ * Section 2.1), trains each narrow sub-GCN on cluster mini-batches
+ * (subTrain, Section 2.2) and copies the trained weight slices back into the
+ * global model (subAgg, Section 2.2).  This library provides the pieces of
  * that hot path:
  *
  *   gist_partition             subGCNs: random equal blocks of [0, d)   (host)
@@ -73,13 +73,13 @@ gist_status gist_create(int device, void* hip_stream, gist_ctx** out);
 gist_status gist_destroy(gist_ctx* ctx);
 gist_status gist_set_stream(gist_ctx* ctx, void* hip_stream);
 
-/* ---- subGCNs: feature partition (Section 3.1, Algorithm 1) ----------- */
+/* ---- subGCNs: feature partition (Section 2.1, Algorithm 1) ----------- */
 
 #define GIST_PART_CATEGORICAL 1u
 
 /* Partition the feature indices [0, d) into m disjoint blocks D^(0..m-1).
  *
- * Section 3.1 asks for a random, disjoint partition into equally sized
+ * Section 2.1 asks for a random, disjoint partition into equally sized
  * blocks (its footnote's example for d = 4, m = 2: {1,4} and {2,3}, 1-based).
  * The randomness is fixed so that any implementation reproduces it bit for
  * bit: a SplitMix64 stream seeded with `seed` (Steele, Lea & Flood 2014)
@@ -88,7 +88,7 @@ gist_status gist_set_stream(gist_ctx* ctx, void* hip_stream);
  * (i+1); swap); block k is shuffled positions [k d/m, (k+1) d/m), sorted.
  * With GIST_PART_CATEGORICAL each index r (ascending) instead draws its block
  * uniformly from [0, m) (the i.i.d. categorical masks of the convergence
- * analysis, Appendix A.1); block sizes are then random and may be zero.
+ * analysis, Appendix C.1); block sizes are then random and may be zero.
  *
  * Host only, synchronous.  Outputs (host memory, caller-allocated):
  *   idx_out[d]     blocks concatenated, each ascending, 0-based
@@ -98,7 +98,7 @@ gist_status gist_set_stream(gist_ctx* ctx, void* hip_stream);
 gist_status gist_partition(int64_t d, int32_t m, uint64_t seed, uint32_t flags,
                            int32_t* idx_out, int64_t* offs_out);
 
-/* ---- Cluster mini-batch (Section 3.2; eq. (1); Appendix A.2) --------- */
+/* ---- Cluster mini-batch (Section 2.2; eq. (1); Appendix C.2) --------- */
 
 typedef enum gist_norm {
   /* Dt^-1/2 (A + I) Dt^-1/2, Dt = 1 + degree: the degree-normalised
@@ -143,7 +143,7 @@ typedef struct gist_csr {
  * clusters `clusters[0 .. n_clusters)` (duplicates allowed, any order);
  * n_clusters == -1 selects the whole graph (`clusters` may be NULL).
  *
- * Section 3.2 makes a mini-batch one cluster or a union of clusters; the
+ * Section 2.2 makes a mini-batch one cluster or a union of clusters; the
  * subgraph keeps every edge with both ends selected and degrees are those
  * of that induced subgraph.  Local rows are the selected nodes in ascending
  * global id; columns ascend within each row.  Values are computed in fp64
@@ -250,7 +250,7 @@ gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* L,
 /* ---- graph attention layer ------------------------------------------ */
 
 /* The GAT layer the paper trains with GIST alongside GCN and GraphSAGE
- * (Section 3, architecture-agnostic training; Table 2).  Single head, as
+ * (Section 2.3, architecture-agnostic training; Table 2).  Single head, as
  * Velickovic et al. (ICLR 2018) define it:
  *   P = H W,  u = P a_src,  v = P a_dst,  e_ij = LeakyReLU(u_i + v_j),
  *   alpha_ij = softmax of e_i. over the pattern N(i) u {i},
@@ -287,7 +287,7 @@ gist_status gist_gat_layer_bwd(gist_ctx* ctx, const gist_gat_desc* D, const gist
                                float* da_src, float* da_dst, float* dH, void* ws,
                                size_t ws_bytes);
 
-/* ---- loss (Section 3.1: the sub-GCN output keeps the global width, so the
+/* ---- loss (Section 2.1: the sub-GCN output keeps the global width, so the
  *      loss is the usual one) ---------------------------------------- */
 
 /* Mean softmax cross-entropy over n rows of logits [n x C] with int32
@@ -302,7 +302,7 @@ gist_status gist_softmax_xent(gist_ctx* ctx, int64_t n, int32_t C,
                               float* loss_dev, float* dlogits, void* ws,
                               size_t ws_bytes);
 
-/* ---- subGCNs slice gather (Section 3.1) ----------------------------- */
+/* ---- subGCNs slice gather (Section 2.1) ----------------------------- */
 
 /* Ws[i][j] = Wg[rows[i]][cols[j]], i < nr, j < nc: the sub-GCN weight
  * Theta^(i)_l = [Theta_l] restricted to rows D^(i)_l and columns
@@ -314,7 +314,7 @@ gist_status gist_gather_slice(gist_ctx* ctx, const float* Wg, int64_t ldg,
                               const int32_t* cols, int32_t nc, float* Ws,
                               int64_t lds);
 
-/* ---- subTrain update (Section 3.2) ---------------------------------- */
+/* ---- subTrain update (Section 2.2) ---------------------------------- */
 
 /* W[k] -= lr * dW[k] for k < n, in fp32 (one rounding per element). */
 gist_status gist_sgd_update(gist_ctx* ctx, float* W, const float* dW, int64_t n,
@@ -337,7 +337,7 @@ gist_status gist_adam_update(gist_ctx* ctx, float* W, const float* dW, float* m,
                              int64_t n, float lr, float beta1, float beta2, float eps,
                              int64_t step, uint32_t flags);
 
-/* ---- subAgg (Section 3.2) ------------------------------------------- */
+/* ---- subAgg (Section 2.2) ------------------------------------------- */
 
 #define GIST_SUBAGG_CHECK_FINITE 1u
 
@@ -383,7 +383,7 @@ gist_status gist_partition_inverse(int64_t d, int32_t m, const int32_t* idx,
  * (gist_partition_inverse) and its m + 1 block offsets; NULL ranks and
  * offsets mean the dimension is not partitioned (every sub-GCN holds all of
  * it at its own index: the input width at layer 0, the output width at the
- * last layer, Section 3.1).  Element (r, c) belongs to sub-GCN i when the
+ * last layer, Section 2.1).  Element (r, c) belongs to sub-GCN i when the
  * partitioned dimensions place both r and c in block i; it sits in slice i
  * at (position of r in block i, position of c in block i), an unpartitioned
  * index keeping its own value.  `slices` is a device array of m device
@@ -401,7 +401,7 @@ typedef struct gist_slice_set {
 
 /* One pass over Wg (rows x cols, leading dimension ldg) that first applies
  * subAgg for the slices of `done` (every entry a sub-GCN owns is replaced by
- * its trained value; entries owned by none keep theirs, Section 3.2) and then
+ * its trained value; entries owned by none keep theirs, Section 2.2) and then
  * gathers the slices of `next` from the updated matrix -- the end of one
  * round of Algorithm 1 and the start of the next.  Either set may be NULL
  * (plain gather, or plain subAgg).  Equal to gist_subagg for every slice of

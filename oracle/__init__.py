@@ -8,22 +8,22 @@ library (no kernels, headers, helpers or tables) and does not import it.
 What it computes, each function citing the passage it follows (paper:
 "GIST: Distributed Training for Large-Scale Graph Convolutional Networks"):
 
-* :mod:`oracle.partition` -- ``subGCNs`` feature partition (Section 3.1 and
+* :mod:`oracle.partition` -- ``subGCNs`` feature partition (Section 2.1 and
   its footnote; Algorithm 1), SplitMix64 + Fisher-Yates, plus the
-  categorical-mask variant of the theory appendix (Appendix A.1).
+  categorical-mask variant of the theory appendix (Appendix C.1).
 * :mod:`oracle.minibatch` -- ``Cluster`` mini-batch: union of clusters,
-  induced subgraph, normalised aggregation matrix (Section 3.2 for the
+  induced subgraph, normalised aggregation matrix (Section 2.2 for the
   mini-batch; eq. (1) for the self-looped degree-normalised matrix;
-  eq. "Aggregation Matrix" of Appendix A.2 for the theory form).
+  eq. "Aggregation Matrix" of Appendix C.2 for the theory form).
 * :mod:`oracle.layers` -- the sub-GCN layer forward and backward (eq. (1),
   eq. (2)), the GraphSAGE-mean layer, softmax cross-entropy, SGD
-  (Section 3.2), slice gather (Section 3.1) and ``subAgg`` (Section 3.2).
+  (Section 2.2), slice gather (Section 2.1) and ``subAgg`` (Section 2.2).
 * :mod:`oracle.gist` -- one sub-GCN training step and one GIST round
   (Algorithm 1) composed from the above, and the whole loop of Algorithm 1
   trained with Adam (the optimizer of the paper's experiments).
 * :mod:`oracle.optim` -- Adam (Kingma & Ba 2015, their Algorithm 1).
 * :mod:`oracle.gat` -- the graph attention layer GIST is also applied to
-  (Section 3; Table 2), single head as Velickovic et al. 2018 define it.
+  (Section 2.3; Table 2), single head as Velickovic et al. 2018 define it.
 
 Floating point is fp64 throughout; fp32 inputs are widened exactly.  The
 matrices of the normalised adjacency are the one place where fp32 is part

@@ -1,7 +1,7 @@
 """Graph attention layer (GAT) forward and backward in fp64 -- test
 infrastructure, never called by the product path.
 
-The paper applies GIST to GAT models (Section 3, architecture-agnostic
+The paper applies GIST to GAT models (Section 2.3, architecture-agnostic
 training; Section 5 and Table 2, Reddit experiments) without restating the
 layer; it cites Velickovic et al., "Graph Attention Networks" (ICLR 2018),
 whose single-head layer this module follows:
@@ -15,7 +15,7 @@ whose single-head layer this module follows:
 Readings (the paper is silent): one head; ReLU as the hidden activation,
 like the other layers here; LeakyReLU slope given by the caller (0.2 in
 the GAT paper); a sub-GCN's slice of a_src and a_dst is their entries
-D_{l+1}^(i), the same output features its slice of W keeps (Section 3.1),
+D_{l+1}^(i), the same output features its slice of W keeps (Section 2.1),
 so each sub-GCN attends with its own features.
 
 The pattern N(i) u {i} is the stored CSR's (the GCN matrix with self-loops

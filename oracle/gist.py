@@ -8,7 +8,7 @@ last layer the identity, the loss is mean softmax cross-entropy (Section
 3.1: the sub-GCN output has the global output dimension, so the loss is
 unchanged).
 
-GAT under GIST (Section 3: the method applies to GAT unchanged; the paper
+GAT under GIST (Section 2.3: the method applies to GAT unchanged; the paper
 trains GAT models with it, Table 2).  A sub-GCN's attention vectors of
 layer l are their entries D_{l+1}^(i), the output features its Theta slice
 keeps.  The output layer's attention vectors live in the unpartitioned
@@ -18,7 +18,7 @@ subnet training, which GIST extends: a parameter that no partition splits
 becomes the mean of the m trained copies (for one sub-GCN, the copy itself).
 With Adam's "carry" policy its moments are averaged the same way.
 
-``sub_gcn_step`` is ``subTrain`` (Section 3.2): forward through eq. (2) on
+``sub_gcn_step`` is ``subTrain`` (Section 2.2): forward through eq. (2) on
 one mini-batch, loss, backward, one SGD step.  ``gist_round`` is one pass of
 the loop body of Algorithm 1: ``subGCNs`` (gather the m slices given the
 partitions), zeta local steps per sub-GCN, then ``subAgg``.
@@ -117,7 +117,7 @@ def slice_indices(partitions, L, i):
 
     ``partitions[l]`` is the (idx, offs) partition of hidden width d_l for
     l = 1..L-1 (entries 0 and L unused): the input and output dimensions are
-    not partitioned (Section 3.1), so rows of layer 0 and columns of layer
+    not partitioned (Section 2.1), so rows of layer 0 and columns of layer
     L-1 are all kept (None).
     """
     out = []

@@ -4,16 +4,16 @@ Paper:
 
 * eq. (1) and eq. (2): H_{l+1} = sigma(Abar H_l Theta_l) for the full and the
   sub-GCN layer (no rescaling of the sub-GCN); the last layer's activation
-  is the identity and the loss is unchanged by GIST (Section 3.1);
-* GraphSAGE (Section 4, related work): the aggregated neighbourhood is
+  is the identity and the loss is unchanged by GIST (Section 2.1);
+* GraphSAGE (Section 3, related work): the aggregated neighbourhood is
   concatenated with the node's own representation.  With the mean
   aggregator this is Z = H Theta_self + (D^-1 A) H Theta_neigh, i.e. the
   concatenation [H | Abar H] times [Theta_self; Theta_neigh];
-* ``subTrain`` is one SGD step (Section 3.2); the theory writes the same
+* ``subTrain`` is one SGD step (Section 2.2); the theory writes the same
   update as theta <- theta - eta dL/dtheta (eq. "GIST_procedure");
-* Theta^(i)_l = rows D^(i)_l and columns D^(i)_{l+1} of Theta_l (Section 3.1);
+* Theta^(i)_l = rows D^(i)_l and columns D^(i)_{l+1} of Theta_l (Section 2.1);
 * ``subAgg`` replaces those entries of the global Theta with the trained
-  slice and leaves every other entry unchanged (Section 3.2).
+  slice and leaves every other entry unchanged (Section 2.2).
 
 The backward pass is the chain rule of the forward written out: the ReLU
 derivative is 1[Z > 0]; the aggregation's adjoint is the transpose of the
@@ -128,7 +128,7 @@ def sgd(W, dW, lr):
 
 
 def gather_slice(theta, rows, cols):
-    """Theta[rows, cols] (None: all rows / all columns), Section 3.1."""
+    """Theta[rows, cols] (None: all rows / all columns), Section 2.1."""
     theta = np.asarray(theta)
     r = np.arange(theta.shape[0]) if rows is None else np.asarray(rows)
     c = np.arange(theta.shape[1]) if cols is None else np.asarray(cols)

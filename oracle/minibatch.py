@@ -1,9 +1,9 @@
 """``Cluster`` mini-batch: induced subgraph of a union of clusters, normalised.
 
-Paper: Section 3.2 (a mini-batch is one cluster or the union of several
+Paper: Section 2.2 (a mini-batch is one cluster or the union of several
 clusters of the training graph), Algorithm 1 (``Cluster``), eq. (1) (the
 aggregation matrix is the degree-normalised adjacency with self-loops) and
-Appendix A.2 (the theory form I + D^-1/2 A D^-1/2).
+Appendix C.2 (the theory form I + D^-1/2 A D^-1/2).
 
 Readings fixed here where the paper is silent:
 

@@ -1,6 +1,6 @@
 """``subGCNs``: random disjoint partition of a feature dimension into m blocks.
 
-Paper: Section 3.1 (with its footnote example d=4, m=2 giving blocks {1,4}
+Paper: Section 2.1 (with its footnote example d=4, m=2 giving blocks {1,4}
 and {2,3}) and Algorithm 1.  The paper asks only for a random partition into disjoint blocks of equal
 size; the randomness is fixed as follows so two independent
 implementations agree bit for bit:
@@ -15,7 +15,7 @@ implementations agree bit for bit:
 * block k is the slice p[k d/m : (k+1) d/m] sorted ascending; indices are
   0-based.
 
-The categorical variant follows the masks of Appendix A.1: each index r
+The categorical variant follows the masks of Appendix C.1: each index r
 independently joins block j with probability 1/m (one rejection draw per r,
 r ascending); block sizes are then random.
 """

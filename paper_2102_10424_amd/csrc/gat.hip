@@ -1,5 +1,5 @@
 // Graph attention layer (the GAT models the paper trains with GIST,
-// Section 3 and Table 2; single head as Velickovic et al. define it):
+// Section 2.3 and Table 2; single head as Velickovic et al. define it):
 //   P = H W,  u = P a_src,  v = P a_dst,  e_ij = LeakyReLU(u_i + v_j),
 //   alpha = row softmax of e over the pattern N(i) u {i},  Z = A_alpha P.
 // The GEMMs and the alpha-weighted aggregation reuse the library's GEMM and

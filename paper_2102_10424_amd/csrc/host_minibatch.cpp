@@ -1,4 +1,4 @@
-// Cluster mini-batch CSR (Section 3.2; eq. (1); Appendix A.2), host side.
+// Cluster mini-batch CSR (Section 2.2; eq. (1); Appendix C.2), host side.
 //
 // The mini-batch is the subgraph induced by a union of clusters.  Rows are
 // the selected nodes in ascending global id; a global edge is kept when both

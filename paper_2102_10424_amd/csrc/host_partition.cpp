@@ -1,11 +1,11 @@
-// subGCNs feature partition (Section 3.1, Algorithm 1), host side.
+// subGCNs feature partition (Section 2.1, Algorithm 1), host side.
 //
 // A random disjoint partition of [0, d) into m equal blocks.  The random
 // stream is SplitMix64 (Steele, Lea & Flood, OOPSLA 2014) seeded with the
 // caller's seed; a Fisher-Yates shuffle with rejection-sampled bounded draws
 // orders the indices; block k takes shuffled positions [k d/m, (k+1) d/m)
 // and sorts them.  The categorical flag instead assigns each index r
-// (ascending) to a uniformly drawn block, as in the masks of Appendix A.1.
+// (ascending) to a uniformly drawn block, as in the masks of Appendix C.1.
 
 #include <algorithm>
 #include <cstring>

@@ -3,7 +3,7 @@
 Nothing here computes: each stage is one ``libgist`` call enqueued on the
 context's stream (torch only provides the device buffers).
 
-* :class:`SubGCN` -- ``subTrain`` (Section 3.2): layer forward for every
+* :class:`SubGCN` -- ``subTrain`` (Section 2.2): layer forward for every
   layer (eq. (2), or the GAT layer), softmax cross-entropy, layer backward
   in reverse, SGD or Adam.
 * :class:`GistModel` -- the global model of Algorithm 1 on one device:

@@ -1,7 +1,7 @@
 """GPU parity of the fused subAgg + gather pass (end of one round of
 Algorithm 1, start of the next): bit-exact against the oracle's subAgg of
 every trained slice followed by the gather of every new slice, for both
-partitioned and unpartitioned dimensions (Section 3.1), unaligned widths,
+partitioned and unpartitioned dimensions (Section 2.1), unaligned widths,
 padded leading dimensions, m = 1, and either half alone.  A model-level case
 checks that fused rounds leave Theta bit-identical to separate subAgg and
 gather calls."""

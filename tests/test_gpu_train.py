@@ -10,7 +10,7 @@ optimizer of the paper's experiments), through the C ABI.
   oracle.gist.gist_train on the same seeded inputs: Theta within 1e-4
   normwise, its change over training within 1e-3, every loss within 1e-4.
 * m = 1: the loop equals plain Adam training of the full model on the GPU,
-  bit for bit (Section 3.1: one sub-GCN is the whole GCN).
+  bit for bit (Section 2.1: one sub-GCN is the whole GCN).
 * GAT models in the same loop (the output layer's attention vectors, which
   every sub-GCN trains in full, aggregated as the mean of the m copies), and
   gist_subagg_mean bit for bit against the fp64 mean rounded to fp32.

@@ -1,4 +1,4 @@
-"""Pins of the oracle's step and round (Algorithm 1; Sections 3.1-3.2; Appendix A).
+"""Pins of the oracle's step and round (Algorithm 1; Sections 2.1-2.2; Appendix C).
 
 * m = 1: the single sub-GCN is the full GCN;
 * two layers with unpartitioned input and output: the full model's logits
@@ -7,7 +7,7 @@
 * after ``subAgg`` the two-layer full model equals the sum of the trained
   sub-GCNs; entries outside every block are untouched; a skipped worker
   leaves its block at the old values;
-* Appendix A's procedure: the additive form theta + sum_j (theta_j,zeta -
+* Appendix C's procedure: the additive form theta + sum_j (theta_j,zeta -
   theta_j,0) equals replacement; the aggregated 1/m-scaled model satisfies
   the global error decomposition lemma.
 """
@@ -133,7 +133,7 @@ def test_round_on_clusters_untouched_entries_and_skipped_worker():
 
 
 def test_theory_procedure_additive_equals_replace_and_error_decomposition():
-    """Appendix A.1 procedure and the global error decomposition lemma."""
+    """Appendix C.1 procedure and the global error decomposition lemma."""
     n, d, d1, m, zeta, eta = 8, 3, 16, 4, 3, 0.05
     g = erdos_renyi(n, 12, seed=13)
     csr = MB.build(g, None, "theory")

@@ -5,7 +5,7 @@
   softmax of a full n x n score matrix), which shares nothing with the
   oracle's sparse forward and hand-written backward;
 * m = 1 GIST training with Adam is ordinary training of the full GAT model
-  (Section 3.1), against torch autograd + torch.optim.Adam, both moment
+  (Section 2.1), against torch autograd + torch.optim.Adam, both moment
   policies;
 * subAgg: every sub-GCN re-gathers exactly its trained slices (matrices and
   hidden-layer attention vectors); the output layer's shared attention

@@ -4,7 +4,7 @@
 * special graphs reduce the layer to plain dense products: no edges
   (GCN: Abar = I), the complete graph (every aggregated row is the mean),
   a star (SAGE-mean: centre gets the leaves' mean, leaves get the centre);
-* the one-hidden-layer theory model's closed-form gradient (Appendix A.1,
+* the one-hidden-layer theory model's closed-form gradient (Appendix C.1,
   with the squared loss halved so the printed gradient has no factor 2) is
   reproduced by the generic layer backward;
 * softmax cross-entropy: uniform logits give log C.
@@ -148,7 +148,7 @@ def test_association_orders_agree(tiny):
 
 
 def test_theory_model_gradient_closed_form():
-    """Appendix A.1: one hidden layer, fixed output weights a, sub-GCN mask."""
+    """Appendix C.1: one hidden layer, fixed output weights a, sub-GCN mask."""
     n, d, d1, m = 6, 3, 8, 2
     g = erdos_renyi(n, 8, seed=11)
     csr = MB.build(g, None, "theory")

@@ -3,7 +3,7 @@
 Checked against brute force on dense matrices and against spectral facts:
 the self-looped symmetric normalisation has the eigenvector D~^{1/2} 1 with
 eigenvalue 1 and spectrum in (-1, 1]; the theory form I + D^-1/2 A D^-1/2
-has spectrum in [0, 2] (Appendix A.2), reaching 2 on a bipartite graph;
+has spectrum in [0, 2] (Appendix C.2), reaching 2 on a bipartite graph;
 mean-aggregation rows sum to one.
 """
 

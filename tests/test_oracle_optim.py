@@ -9,7 +9,7 @@ Adam (Kingma & Ba 2015, the optimizer of the paper's experiments):
 * with eps = 0 the update is invariant to a positive scaling of the gradients.
 
 The loop (Algorithm 1 with Adam):
-* m = 1 reproduces ordinary training of the full model (Section 3.1: one
+* m = 1 reproduces ordinary training of the full model (Section 2.1: one
   sub-GCN is the whole GCN), checked against a torch autograd + Adam loop:
   "carry" equals one optimizer kept across rounds, "reset" a fresh optimizer
   per round;

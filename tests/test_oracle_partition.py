@@ -1,4 +1,4 @@
-"""Pins of the oracle's ``subGCNs`` partition (Section 3.1; Appendix A.1 masks)."""
+"""Pins of the oracle's ``subGCNs`` partition (Section 2.1; Appendix C.1 masks)."""
 
 import os
 
@@ -77,7 +77,7 @@ def test_partition_invariants(d, m):
 
 
 def test_mask_properties():
-    # Appendix A.1: sum_j M^(j)_r = 1 and M^(j)_r M^(j')_r = 0 for j != j'.
+    # Appendix C.1: sum_j M^(j)_r = 1 and M^(j)_r M^(j')_r = 0 for j != j'.
     d, m = 64, 4
     for cat in (False, True):
         idx, offs = P.partition(d, m, 7, categorical=cat)
