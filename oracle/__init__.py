@@ -24,6 +24,10 @@ What it computes, each function citing the passage it follows (paper:
 * :mod:`oracle.optim` -- Adam (Kingma & Ba 2015, their Algorithm 1).
 * :mod:`oracle.gat` -- the graph attention layer GIST is also applied to
   (Section 2.3; Table 2), single head as Velickovic et al. 2018 define it.
+* :mod:`oracle.ladies` -- LADIES layer-wise sampled mini-batches, the node
+  sampling GIST is combined with in place of graph partitioning
+  (Section 5.4, Appendix A.6), as Zou et al. 2019 define it; the GCN layers
+  of :mod:`oracle.layers` take its rectangular per-layer matrices.
 
 Floating point is fp64 throughout; fp32 inputs are widened exactly.  The
 matrices of the normalised adjacency are the one place where fp32 is part
@@ -37,4 +41,4 @@ two-layer sum decomposition, an independent Adam implementation); none is
 "parity unpinned".
 """
 
-from . import partition, minibatch, layers, gist, optim, gat  # noqa: F401
+from . import partition, minibatch, layers, gist, optim, gat, ladies  # noqa: F401

@@ -53,6 +53,17 @@ def _pack(kind, arrs):
     return arrs[0] if kind == "gcn" else tuple(arrs)
 
 
+def _layer_csr(kind, csr, l):
+    """The aggregation matrix of layer l: one matrix for every layer (a
+    ``Cluster`` mini-batch), or one per layer (a layer-sampled mini-batch,
+    ``oracle.ladies``; GCN only, since its matrices are rectangular)."""
+    if isinstance(csr, (list, tuple)):
+        if kind != "gcn":
+            raise ValueError("per-layer matrices are supported for GCN only")
+        return csr[l]
+    return csr
+
+
 def forward(kind, csr, X, params):
     """Forward pass; returns the list of layer records (AH, Z, H_out) and inputs."""
     H = [_l.as_f64(X)]
@@ -61,12 +72,13 @@ def forward(kind, csr, X, params):
     for l in range(L):
         act = l < L - 1
         if kind == "gcn":
-            rec = _l.gcn_forward(csr, H[-1], params[l], act)
+            rec = _l.gcn_forward(_layer_csr(kind, csr, l), H[-1], params[l], act)
         elif kind == "gat":
             W, a1, a2 = params[l]
-            rec = _g.gat_forward(csr, H[-1], W, a1, a2, act, GAT_SLOPE)
+            rec = _g.gat_forward(_layer_csr(kind, csr, l), H[-1], W, a1, a2, act, GAT_SLOPE)
         else:
-            rec = _l.sage_forward(csr, H[-1], params[l][0], params[l][1], act)
+            rec = _l.sage_forward(_layer_csr(kind, csr, l), H[-1], params[l][0], params[l][1],
+                                  act)
         recs.append(rec)
         H.append(rec["H_out"])
     return H, recs
@@ -81,17 +93,17 @@ def backward(kind, csr, H, recs, params, dlogits):
     for l in reversed(range(L)):
         act = l < L - 1
         if kind == "gcn":
-            b = _l.gcn_backward(csr, H[l], recs[l], params[l], dH, act,
+            b = _l.gcn_backward(_layer_csr(kind, csr, l), H[l], recs[l], params[l], dH, act,
                                 need_dH=l > 0)
             grads[l] = b["dW"]
         elif kind == "gat":
             W, a1, a2 = params[l]
-            b = _g.gat_backward(csr, H[l], recs[l], W, a1, a2, dH, act, GAT_SLOPE,
-                                need_dH=l > 0)
+            b = _g.gat_backward(_layer_csr(kind, csr, l), H[l], recs[l], W, a1, a2, dH, act,
+                                GAT_SLOPE, need_dH=l > 0)
             grads[l] = (b["dW"], b["da_src"], b["da_dst"])
         else:
-            b = _l.sage_backward(csr, H[l], recs[l], params[l][0], params[l][1],
-                                 dH, act, need_dH=l > 0)
+            b = _l.sage_backward(_layer_csr(kind, csr, l), H[l], recs[l], params[l][0],
+                                 params[l][1], dH, act, need_dH=l > 0)
             grads[l] = (b["dW_self"], b["dW_neigh"])
         dH = b.get("dH")
         dHs[l] = dH

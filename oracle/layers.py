@@ -31,12 +31,18 @@ def as_f64(x):
 
 
 def adjacency(csr, transpose=False):
-    """The stored aggregation matrix (or its explicit transpose) as fp64 CSR."""
+    """The stored aggregation matrix (or its explicit transpose) as fp64 CSR.
+
+    A matrix with ``n_in`` (columns) different from ``n`` (rows) aggregates
+    from one node set into another (a layer-sampled mini-batch); its stored
+    transpose has the swapped shape."""
     key = "t_" if transpose else ""
     n = csr["n"]
+    n_in = csr.get("n_in", n)
+    shape = (n_in, n) if transpose else (n, n_in)
     return sp.csr_matrix((csr[key + "val"].astype(np.float64),
                           csr[key + "col"].astype(np.int64),
-                          csr[key + "rowptr"].astype(np.int64)), shape=(n, n))
+                          csr[key + "rowptr"].astype(np.int64)), shape=shape)
 
 
 def aggregate(csr, H):
