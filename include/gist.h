@@ -10,6 +10,7 @@
  *
  *   gist_partition             subGCNs: random equal blocks of [0, d)   (host)
  *   gist_build_minibatch_csr   Cluster mini-batch: induced, normalised  (host)
+ *   gist_ladies_sample         LADIES layer-sampled mini-batch (GCN)    (host)
  *   gist_gather_slice          Theta^(i) = Theta[D_in, D_out]           (device)
  *   gist_gcn_layer_fwd/_bwd    eq. (2) sub-GCN layer, GCN and SAGE-mean (device)
  *   gist_gat_layer_fwd/_bwd    the graph attention layer GIST also trains (device)
@@ -159,6 +160,54 @@ gist_status gist_build_minibatch_csr(const gist_graph* g, const int32_t* cluster
                                      int32_t n_clusters, gist_norm norm,
                                      gist_csr* out);
 
+/* ---- LADIES layer-sampled mini-batch (Section 5.4; Appendix A.6) ---- */
+
+/* One layer of a layer-sampled mini-batch, host memory.  Layer l aggregates
+ * from the node set V_l (its columns) into V_{l+1} (its rows); V_{l+1} is a
+ * subset of V_l.  `cap_n` / `cap_nnz` are the capacities of the caller's
+ * arrays: nodes holds cap_n entries, rowptr and t_rowptr cap_n + 1, the
+ * entry arrays cap_nnz.  n_out, n_in and nnz are outputs. */
+typedef struct gist_ladies_layer {
+  int64_t n_out, n_in, nnz;      /* out: |V_{l+1}|, |V_l|, entries        */
+  int64_t cap_n, cap_nnz;        /* in                                    */
+  int32_t* nodes;                /* [n_in]: V_l, ascending global ids     */
+  int32_t* rowptr;               /* [n_out+1]                             */
+  int32_t* col;                  /* [nnz]: positions in V_l, ascending    */
+  float* val;                    /* [nnz]                                 */
+  int32_t* t_rowptr;             /* [n_in+1]: the transpose, rows V_l     */
+  int32_t* t_col;                /* [nnz]: positions in V_{l+1}, ascending */
+  float* t_val;                  /* [nnz]                                 */
+} gist_ladies_layer;
+
+/* LADIES (Zou et al., NeurIPS 2019), the layer-wise importance sampling
+ * GIST is combined with in place of graph partitioning, for an L-layer GCN.
+ *
+ * A is the full-graph GCN matrix (gist_build_minibatch_csr over the whole
+ * graph with GIST_NORM_GCN_SYM; n, rowptr, col, val are read).  `batch`
+ * holds the b output nodes V_L, strictly ascending.  For l = L-1 down to 0:
+ *   q_j = sum over i in V_{l+1} (ascending) of A_ij^2, in double;
+ *   p_j = q_j / Q with Q the sum of q_j over ascending j;
+ *   s draws, each from the next output x of one SplitMix64 stream seeded
+ *   `seed` (shared by all layers, layer L-1 first): t = (x >> 11) 2^-53 Q,
+ *   node = the smallest j whose prefix sum q_0 + ... + q_j exceeds t (the
+ *   largest j with q_j > 0 if t reached Q);
+ *   V_l = distinct draws and V_{l+1}, ascending;
+ *   row i of layer l: every entry (i, j) of A with j in V_l, ascending j,
+ *   value w_ij = A_ij / (max(s,1) p_j), divided by the row's sum of w
+ *   (ascending j) and rounded once to float.
+ * The transpose is written too (rows V_l, entries in ascending row).
+ * layers[l] describes layer l (0 = the input layer).  b == 0 gives empty
+ * layers and draws nothing.
+ *
+ * If every layers[l].rowptr is NULL the call only reports the sizes.
+ * Host only, synchronous, thread-safe (per-thread scratch).  Errors:
+ * GIST_E_INVAL (NULL arguments, L < 1, s < 0, batch not strictly ascending
+ * or out of range), GIST_E_NOMEM (a capacity too small; every layer's
+ * n_out, n_in and nnz still report the needed sizes), GIST_E_UNSUPPORTED
+ * (A->n >= 2^31). */
+gist_status gist_ladies_sample(const gist_csr* A, const int32_t* batch, int64_t b, int32_t L,
+                               int32_t s, uint64_t seed, gist_ladies_layer* layers);
+
 /* ---- device CSR and layer descriptor -------------------------------- */
 
 typedef struct gist_csr_dev {   /* device memory, layout as gist_csr */
@@ -191,7 +240,16 @@ typedef struct gist_layer_desc {
   int32_t s_out;   /* sub-GCN output width |D_l+1| (d_L at the last layer) */
   int32_t groups;  /* G sub-GCNs batched on this mini-batch (0 means 1)  */
   uint32_t flags;  /* GIST_LAYER_SHARED_INPUT | GIST_LAYER_GROUP_MAJOR_OUT */
+  int64_t n_in;    /* input rows (columns of Abar); 0 means n.  GCN only  */
+                   /* when different from n (a layer-sampled batch)       */
 } gist_layer_desc;
+
+/* Rectangular layers (n_in != n): Abar is n x n_in and aggregates the
+ * n_in input rows H into n output rows, as a layer-sampled mini-batch does
+ * (gist_ladies_sample).  H and dH have n_in rows; agg_save, H_out and
+ * dH_out have n.  The backward pass needs the explicit transpose A_T
+ * (n_in rows).  Only GCN layers may be rectangular.  With no output rows
+ * (n == 0) the backward pass zeroes dW and dH. */
 
 /* Batched sub-GCNs (G > 1): the layer of G sub-GCNs that share one
  * mini-batch, each with its own weight slice -- the same results as G
@@ -236,8 +294,9 @@ gist_status gist_gcn_layer_fwd(gist_ctx* ctx, const gist_layer_desc* L,
  *   SAGE: dW = [H | Abar H]^T dZ  ([2 s_in x s_out]),
  *         dH = dZ W_self^T + Abar^T (dZ W_neigh^T)
  *
- * A_T is the explicit transpose CSR (required for SAGE-mean; NULL for GCN
- * means Abar is symmetric, as GIST_NORM_GCN_SYM / THEORY produce).
+ * A_T is the explicit transpose CSR (required for SAGE-mean and for
+ * rectangular layers; NULL for a square GCN layer means Abar is symmetric,
+ * as GIST_NORM_GCN_SYM / THEORY produce).
  * dW is overwritten.  dH may be NULL (layer 0: no input gradient).
  * Results are deterministic: no atomics, fixed reduction order. */
 gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* L,

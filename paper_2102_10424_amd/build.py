@@ -15,7 +15,7 @@ OUT = os.path.join(PKG, "libgist.so")
 BUILD = os.path.join(PKG, "_build")
 
 HIP_SOURCES = ["api.hip", "spmm.hip", "gemm.hip", "gemm_bf16.hip", "elementwise.hip", "gat.hip"]
-HOST_SOURCES = ["host_partition.cpp", "host_minibatch.cpp"]
+HOST_SOURCES = ["host_partition.cpp", "host_minibatch.cpp", "host_ladies.cpp"]
 
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -176,6 +176,11 @@ gist_status check_desc(const gist_layer_desc* L) {
   if (L->flags & ~static_cast<uint32_t>(GIST_LAYER_SHARED_INPUT | GIST_LAYER_GROUP_MAJOR_OUT))
     return set_error(GIST_E_INVAL, "layer: unknown flags");
   if (L->n > INT32_MAX) return set_error(GIST_E_UNSUPPORTED, "layer: n exceeds int32 rows");
+  if (L->n_in < 0) return set_error(GIST_E_INVAL, "layer: bad n_in");
+  if (L->n_in > INT32_MAX) return set_error(GIST_E_UNSUPPORTED, "layer: n_in exceeds int32 rows");
+  const int64_t n_in = L->n_in > 0 ? L->n_in : L->n;
+  if (n_in != L->n && L->kind != GIST_LAYER_GCN)
+    return set_error(GIST_E_INVAL, "layer: only GCN layers may be rectangular (n_in != n)");
   const int64_t G = L->groups > 1 ? L->groups : 1;
   if (G * L->s_in > INT32_MAX || G * L->s_out > INT32_MAX)
     return set_error(GIST_E_UNSUPPORTED, "layer: batched width exceeds int32");
@@ -186,16 +191,17 @@ gist_status check_desc(const gist_layer_desc* L) {
 // element offsets of the input-side (H, agg, dH) and output-side (H_out,
 // dH_out, dZ) tensors and of the weight slices.
 struct Lay {
-  int64_t G, n, si, so, wrows;
+  int64_t G, n, n_in, si, so, wrows;
   bool shared, gmajor;
   int64_t ld_in, gs_in, ld_out, gs_out, gs_w;
+  int64_t gs_out_in;   // group stride of an output-width tensor with n_in rows
   int64_t w_in() const { return shared ? si : G * si; }   // aggregation width on the input side
 };
 
 Lay layout(const gist_layer_desc* L) {
   Lay y;
   y.G = L->groups > 1 ? L->groups : 1;
-  y.n = L->n; y.si = L->s_in; y.so = L->s_out;
+  y.n = L->n; y.n_in = L->n_in > 0 ? L->n_in : L->n; y.si = L->s_in; y.so = L->s_out;
   y.wrows = (L->kind == GIST_LAYER_SAGE_MEAN ? 2 : 1) * y.si;
   y.shared = (L->flags & GIST_LAYER_SHARED_INPUT) != 0;
   y.gmajor = (L->flags & GIST_LAYER_GROUP_MAJOR_OUT) != 0;
@@ -203,20 +209,22 @@ Lay layout(const gist_layer_desc* L) {
   y.gs_in = y.shared ? 0 : y.si;
   y.ld_out = y.gmajor ? y.so : y.G * y.so;
   y.gs_out = y.gmajor ? y.n * y.so : y.so;
+  y.gs_out_in = y.gmajor ? y.n_in * y.so : y.so;
   y.gs_w = y.wrows * y.so;
   return y;
 }
 
-// Abar X over an output-side tensor (dZ-like layout): one full-width call,
-// or one per group when the groups are stored one after another.
-gist_status spmm_out(hipStream_t st, const Lay& y, const gist_csr_dev* A, const float* X, float* Y,
-                     bool relu) {
+// A X over output-width tensors (dZ-like layout), A with `rows` rows: one
+// full-width call, or one per group when the groups are stored one after
+// another (group strides gx of X and gy of Y).
+gist_status spmm_out(hipStream_t st, const Lay& y, const gist_csr_dev* A, int64_t rows,
+                     const float* X, int64_t gx, float* Y, int64_t gy, bool relu) {
   if (!y.gmajor)
-    return gist::spmm(st, y.n, A->nnz, A->rowptr, A->col, A->val, X, y.ld_out, int(y.G * y.so), Y,
-                      y.ld_out, nullptr, 0, relu);
+    return gist::spmm(st, rows, A->nnz, A->rowptr, A->col, A->val, X, y.ld_out, int(y.G * y.so),
+                      Y, y.ld_out, nullptr, 0, relu);
   for (int64_t g = 0; g < y.G; ++g)
-    GIST_TRY(gist::spmm(st, y.n, A->nnz, A->rowptr, A->col, A->val, X + g * y.gs_out, y.so,
-                        int(y.so), Y + g * y.gs_out, y.so, nullptr, 0, relu));
+    GIST_TRY(gist::spmm(st, rows, A->nnz, A->rowptr, A->col, A->val, X + g * gx, y.so,
+                        int(y.so), Y + g * gy, y.so, nullptr, 0, relu));
   return GIST_OK;
 }
 
@@ -239,24 +247,28 @@ struct BwdPlan {
 BwdPlan plan_bwd(const gist_layer_desc* L) {
   BwdPlan p;
   const Lay y = layout(L);
-  const int64_t n = y.n, si = y.si, so = y.so, G = y.G;
+  const int64_t n = y.n, n_in = y.n_in, si = y.si, so = y.so, G = y.G;
   if (L->act == GIST_ACT_RELU) p.dz = fbytes(n, G * so);
   const int order = resolve_order(L);
-  if (L->kind == GIST_LAYER_SAGE_MEAN || order == GIST_ORDER_AGG_FIRST)
+  if (L->kind == GIST_LAYER_SAGE_MEAN || order == GIST_ORDER_AGG_FIRST) {
     p.tmp = fbytes(n, G * si);  // dP = dZ W^T (W_neigh for SAGE)
-  else
-    p.tmp = fbytes(n, G * so);  // Abar^T dZ
-  p.gemm = std::max(gist::gemm_workspace(y.wrows, so, n, L->dtype, G),
-                    gist::gemm_workspace(n, y.wrows, so, L->dtype, G));
+    p.gemm = std::max(gist::gemm_workspace(y.wrows, so, n, L->dtype, G),
+                      gist::gemm_workspace(n, y.wrows, so, L->dtype, G));
+  } else {
+    p.tmp = fbytes(n_in, G * so);  // Abar^T dZ
+    p.gemm = std::max(gist::gemm_workspace(si, so, n_in, L->dtype, G),
+                      gist::gemm_workspace(n_in, si, so, L->dtype, G));
+  }
   return p;
 }
 
 size_t plan_fwd(const gist_layer_desc* L) {
   const Lay y = layout(L);
   const int order = resolve_order(L);
-  size_t t = 0;
-  if (L->kind == GIST_LAYER_GCN && order == GIST_ORDER_XFORM_FIRST) t = fbytes(y.n, y.G * y.so);
-  return align256(t) + gist::gemm_workspace(y.n, y.so, y.wrows, L->dtype, y.G);
+  if (L->kind == GIST_LAYER_GCN && order == GIST_ORDER_XFORM_FIRST)
+    return align256(fbytes(y.n_in, y.G * y.so)) +
+           gist::gemm_workspace(y.n_in, y.so, y.si, L->dtype, y.G);
+  return gist::gemm_workspace(y.n, y.so, y.wrows, L->dtype, y.G);
 }
 
 }  // namespace
@@ -280,7 +292,7 @@ extern "C" gist_status gist_gcn_layer_fwd(gist_ctx* ctx, const gist_layer_desc* 
   GIST_TRY(check_desc(L));
   GIST_TRY(check_csr(A, L->n, "layer_fwd"));
   const Lay y = layout(L);
-  const int64_t n = y.n, si = y.si, so = y.so, G = y.G;
+  const int64_t n = y.n, n_in = y.n_in, si = y.si, so = y.so, G = y.G;
   const int order = resolve_order(L);
   const bool sage = L->kind == GIST_LAYER_SAGE_MEAN;
   if (n > 0 && (!H || !W || !H_out)) return set_error(GIST_E_INVAL, "layer_fwd: NULL pointer");
@@ -311,16 +323,17 @@ extern "C" gist_status gist_gcn_layer_fwd(gist_ctx* ctx, const gist_layer_desc* 
     out.c0 = H_out; out.ldc0 = y.ld_out; out.gs0 = y.gs_out; out.relu = relu;
     return gist::gemm(st, n, so, y.wrows, a, b, out, L->dtype, ws, ws_bytes, G);
   }
-  // transform first: T_g = H_g W_g (workspace, laid out like H_out), H_out = act(Abar T)
+  // transform first: T_g = H_g W_g over the n_in input rows (workspace, laid out
+  // like H_out), H_out = act(Abar T)
   float* T = static_cast<float*>(ws);
-  const size_t tb = align256(fbytes(n, G * so));
+  const size_t tb = align256(fbytes(n_in, G * so));
   void* gws = static_cast<char*>(ws) + tb;
   gist::Operand a;
   a.p0 = H; a.ld0 = y.ld_in; a.gs0 = y.gs_in; a.k_major = true;
   gist::GemmOut t;
-  t.c0 = T; t.ldc0 = y.ld_out; t.gs0 = y.gs_out;
-  GIST_TRY(gist::gemm(st, n, so, si, a, b, t, L->dtype, gws, ws_bytes - tb, G));
-  return spmm_out(st, y, A, T, H_out, relu);
+  t.c0 = T; t.ldc0 = y.ld_out; t.gs0 = y.gs_out_in;
+  GIST_TRY(gist::gemm(st, n_in, so, si, a, b, t, L->dtype, gws, ws_bytes - tb, G));
+  return spmm_out(st, y, A, n, T, y.gs_out_in, H_out, y.gs_out, relu);
 }
 
 extern "C" gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* L,
@@ -335,10 +348,10 @@ extern "C" gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* 
   GIST_TRY(check_desc(L));
   GIST_TRY(check_csr(A, L->n, "layer_bwd"));
   const bool sage = L->kind == GIST_LAYER_SAGE_MEAN;
-  if (sage) GIST_TRY(check_csr(A_T, L->n, "layer_bwd (transpose)"));
-  else if (A_T) GIST_TRY(check_csr(A_T, L->n, "layer_bwd (transpose)"));
   const Lay y = layout(L);
-  const int64_t n = y.n, si = y.si, so = y.so, G = y.G;
+  const int64_t n = y.n, n_in = y.n_in, si = y.si, so = y.so, G = y.G;
+  if (sage || n_in != n) GIST_TRY(check_csr(A_T, n_in, "layer_bwd (transpose)"));
+  else if (A_T) GIST_TRY(check_csr(A_T, n_in, "layer_bwd (transpose)"));
   const int order = resolve_order(L);
   const bool relu = L->act == GIST_ACT_RELU;
   if (!dW || !W) return set_error(GIST_E_INVAL, "layer_bwd: NULL dW or W");
@@ -353,7 +366,10 @@ extern "C" gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* 
     return set_error(GIST_E_NOMEM, "layer_bwd: workspace too small");
   gist::DeviceGuard dg(ctx->device);
   hipStream_t st = ctx->stream;
-  if (n == 0) return gist::fill_zero(st, dW, G * y.wrows * so);  // empty batch: zero gradient
+  if (n == 0) {  // no output rows: zero gradients
+    GIST_TRY(gist::fill_zero(st, dW, G * y.wrows * so));
+    return dH && n_in > 0 ? gist::fill_zero(st, dH, n_in * G * si) : GIST_OK;
+  }
   char* base = static_cast<char*>(ws);
   float* dZbuf = reinterpret_cast<float*>(base);
   float* tmp = reinterpret_cast<float*>(base + align256(p.dz));
@@ -372,7 +388,7 @@ extern "C" gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* 
   wout.c0 = dW; wout.ldc0 = so; wout.gs0 = y.gs_w;
   gist::Operand w_as_b;   // W_g^T as an N x K operand is W_g itself (rows = N, K contiguous)
   w_as_b.p0 = W; w_as_b.ld0 = so; w_as_b.gs0 = y.gs_w; w_as_b.k_major = true;
-  const int64_t ld_p = G * si;   // dP / dH: n x (G s_in)
+  const int64_t ld_p = G * si;   // dP: n x (G s_in); dH: n_in x (G s_in)
 
   if (sage || order == GIST_ORDER_AGG_FIRST) {
     // dW_g = [H_g | Abar H_g]^T dZ_g (SAGE) or (Abar H_g)^T dZ_g: element (r, k) of the
@@ -399,22 +415,23 @@ extern "C" gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* 
     }
     GIST_TRY(gist::gemm(st, n, y.wrows, so, a2, w_as_b, o2, L->dtype, gws, gbytes, G));
     // dH (+)= Abar^T dP, every group at once
-    return gist::spmm(st, n, AT->nnz, AT->rowptr, AT->col, AT->val, tmp, ld_p, int(ld_p), dH, ld_p,
-                      sage ? dH : nullptr, ld_p, false);
+    return gist::spmm(st, n_in, AT->nnz, AT->rowptr, AT->col, AT->val, tmp, ld_p, int(ld_p), dH,
+                      ld_p, sage ? dH : nullptr, ld_p, false);
   }
-  // GCN transform-first: T = Abar^T dZ (laid out like dZ); dW_g = H_g^T T_g; dH_g = T_g W_g^T
-  GIST_TRY(spmm_out(st, y, AT, dZ, tmp, false));
+  // GCN transform-first: T = Abar^T dZ (n_in rows, laid out like dZ); dW_g = H_g^T T_g;
+  // dH_g = T_g W_g^T
+  GIST_TRY(spmm_out(st, y, AT, n_in, dZ, y.gs_out, tmp, y.gs_out_in, false));
   gist::Operand a;
   a.p0 = H; a.ld0 = y.ld_in; a.gs0 = y.gs_in; a.k_major = false;
   gist::Operand g;
-  g.p0 = tmp; g.ld0 = y.ld_out; g.gs0 = y.gs_out; g.k_major = false;
-  GIST_TRY(gist::gemm(st, si, so, n, a, g, wout, L->dtype, gws, gbytes, G));
+  g.p0 = tmp; g.ld0 = y.ld_out; g.gs0 = y.gs_out_in; g.k_major = false;
+  GIST_TRY(gist::gemm(st, si, so, n_in, a, g, wout, L->dtype, gws, gbytes, G));
   if (!dH) return GIST_OK;
   gist::Operand a2;
-  a2.p0 = tmp; a2.ld0 = y.ld_out; a2.gs0 = y.gs_out; a2.k_major = true;
+  a2.p0 = tmp; a2.ld0 = y.ld_out; a2.gs0 = y.gs_out_in; a2.k_major = true;
   gist::GemmOut o2;
   o2.c0 = dH; o2.ldc0 = ld_p; o2.gs0 = si;
-  return gist::gemm(st, n, si, so, a2, w_as_b, o2, L->dtype, gws, gbytes, G);
+  return gist::gemm(st, n_in, si, so, a2, w_as_b, o2, L->dtype, gws, gbytes, G);
 }
 
 // ---------------------------------------------------------------------------

@@ -13,31 +13,7 @@
 
 #include "gist_internal.h"
 
-namespace {
-
-class SplitMix64 {
- public:
-  explicit SplitMix64(uint64_t seed) : s_(seed) {}
-  uint64_t next() {
-    s_ += 0x9E3779B97F4A7C15ull;
-    uint64_t z = s_;
-    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
-    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
-    return z ^ (z >> 31);
-  }
-  // Uniform on [0, bound): reject the incomplete top range of 2^64.
-  uint64_t below(uint64_t bound) {
-    const uint64_t rem = (0ull - bound) % bound;  // 2^64 mod bound
-    for (;;) {
-      const uint64_t r = next();
-      if (rem == 0 || r < 0ull - rem) return r % bound;
-    }
-  }
- private:
-  uint64_t s_;
-};
-
-}  // namespace
+using gist::SplitMix64;
 
 extern "C" gist_status gist_partition(int64_t d, int32_t m, uint64_t seed,
                                       uint32_t flags, int32_t* idx_out,

@@ -55,7 +55,7 @@ NORM_BY_NAME = {"gcn": GIST_NORM_GCN_SYM, "sage": GIST_NORM_SAGE_MEAN,
 # Every symbol include/gist.h declares.
 EXPORTED = (
     "gist_last_error", "gist_status_str", "gist_create", "gist_destroy",
-    "gist_set_stream", "gist_partition", "gist_build_minibatch_csr",
+    "gist_set_stream", "gist_partition", "gist_build_minibatch_csr", "gist_ladies_sample",
     "gist_layer_workspace_size", "gist_gcn_layer_fwd", "gist_gcn_layer_bwd",
     "gist_gat_workspace_size", "gist_gat_layer_fwd", "gist_gat_layer_bwd",
     "gist_softmax_xent_workspace", "gist_softmax_xent", "gist_gather_slice",
@@ -93,7 +93,15 @@ class gist_csr_dev(C.Structure):
 class gist_layer_desc(C.Structure):
     _fields_ = [("kind", C.c_int32), ("act", C.c_int32), ("dtype", C.c_int32),
                 ("order", C.c_int32), ("n", C.c_int64), ("s_in", C.c_int32),
-                ("s_out", C.c_int32), ("groups", C.c_int32), ("flags", C.c_uint32)]
+                ("s_out", C.c_int32), ("groups", C.c_int32), ("flags", C.c_uint32),
+                ("n_in", C.c_int64)]
+
+
+class gist_ladies_layer(C.Structure):
+    _fields_ = [("n_out", C.c_int64), ("n_in", C.c_int64), ("nnz", C.c_int64),
+                ("cap_n", C.c_int64), ("cap_nnz", C.c_int64), ("nodes", C.c_void_p),
+                ("rowptr", C.c_void_p), ("col", C.c_void_p), ("val", C.c_void_p),
+                ("t_rowptr", C.c_void_p), ("t_col", C.c_void_p), ("t_val", C.c_void_p)]
 
 
 class gist_gat_desc(C.Structure):
@@ -139,6 +147,8 @@ _sigs = {
     "gist_partition": (C.c_int, [C.c_int64, C.c_int32, C.c_uint64, C.c_uint32, _P, _P]),
     "gist_build_minibatch_csr": (C.c_int, [C.POINTER(gist_graph), _P, C.c_int32, C.c_int,
                                            C.POINTER(gist_csr)]),
+    "gist_ladies_sample": (C.c_int, [C.POINTER(gist_csr), _P, C.c_int64, C.c_int32, C.c_int32,
+                                     C.c_uint64, C.POINTER(gist_ladies_layer)]),
     "gist_layer_workspace_size": (C.c_int, [C.POINTER(gist_layer_desc),
                                             C.POINTER(C.c_size_t), C.POINTER(C.c_size_t)]),
     "gist_gcn_layer_fwd": (C.c_int, [_P, C.POINTER(gist_layer_desc), C.POINTER(gist_csr_dev),
@@ -273,6 +283,74 @@ def gist_build_minibatch_csr(graph, clusters, norm):
     return out
 
 
+class CsrHandle:
+    """A host ``gist_csr`` over NumPy arrays kept alive with it (the full-graph
+    matrix that ``gist_ladies_sample`` samples from)."""
+
+    def __init__(self, csr):
+        self._keep = dict(rowptr=np.ascontiguousarray(csr["rowptr"], dtype=np.int32),
+                          col=np.ascontiguousarray(csr["col"], dtype=np.int32),
+                          val=np.ascontiguousarray(csr["val"], dtype=np.float32))
+        n, nnz = int(csr["n"]), int(csr["nnz"])
+        self.struct = gist_csr(n, nnz, n, nnz, _ptr(self._keep["rowptr"]), _ptr(self._keep["col"]),
+                               _ptr(self._keep["val"]), None, None, None, None)
+        self.n, self.nnz = n, nnz
+
+
+_LADIES_ARRAYS = (("nodes", np.int32, "n"), ("rowptr", np.int32, "n1"), ("col", np.int32, "z"),
+                  ("val", np.float32, "z"), ("t_rowptr", np.int32, "n1"),
+                  ("t_col", np.int32, "z"), ("t_val", np.float32, "z"))
+
+
+def ladies_layers(L, caps=None):
+    """An array of L ``gist_ladies_layer`` s; with ``caps`` = [(cap_n, cap_nnz)] * L
+    each gets NumPy buffers of those capacities (returned alongside)."""
+    arr = (gist_ladies_layer * L)()
+    bufs = []
+    for l in range(L):
+        if caps is None:
+            bufs.append(None)
+            continue
+        cn, cz = int(caps[l][0]), int(caps[l][1])
+        size = dict(n=max(cn, 1), n1=cn + 1, z=max(cz, 1))
+        b = {k: np.empty(size[w], dtype=t) for k, t, w in _LADIES_ARRAYS}
+        arr[l].cap_n, arr[l].cap_nnz = cn, cz
+        for k, _, _ in _LADIES_ARRAYS:
+            setattr(arr[l], k, _ptr(b[k]))
+        bufs.append(b)
+    return arr, bufs
+
+
+def ladies_sample_into(A_handle, batch, L, s, seed, arr):
+    """``gist_ladies_sample`` into the layer descriptors ``arr`` (host buffers)."""
+    batch = np.ascontiguousarray(batch, dtype=np.int32)
+    _check(_lib.gist_ladies_sample(C.byref(A_handle.struct), _ptr(batch), int(batch.shape[0]),
+                                   int(L), int(s), int(seed) & (2**64 - 1), arr))
+    return arr
+
+
+def gist_ladies_sample(A, batch, L, s, seed):
+    """LADIES mini-batch as NumPy arrays: dict(nodes=[V_0..V_L], layers=[dict per layer]).
+
+    ``A``: the full-graph GCN CSR (dict or :class:`CsrHandle`)."""
+    h = A if isinstance(A, CsrHandle) else CsrHandle(A)
+    q, _ = ladies_layers(L)
+    ladies_sample_into(h, batch, L, s, seed, q)      # size query
+    arr, bufs = ladies_layers(L, [(q[l].n_in, q[l].nnz) for l in range(L)])
+    ladies_sample_into(h, batch, L, s, seed, arr)
+    layers, nodes = [], []
+    for l in range(L):
+        d, b = arr[l], bufs[l]
+        n_out, n_in, nnz = int(d.n_out), int(d.n_in), int(d.nnz)
+        layers.append(dict(n=n_out, n_in=n_in, nnz=nnz, rowptr=b["rowptr"][:n_out + 1],
+                           col=b["col"][:nnz], val=b["val"][:nnz],
+                           t_rowptr=b["t_rowptr"][:n_in + 1], t_col=b["t_col"][:nnz],
+                           t_val=b["t_val"][:nnz]))
+        nodes.append(b["nodes"][:n_in])
+    nodes.append(np.ascontiguousarray(batch, dtype=np.int32))
+    return dict(nodes=nodes, layers=layers)
+
+
 class GraphHandle:
     """A ``gist_graph`` over NumPy arrays kept alive with it (build once, reuse)."""
 
@@ -300,9 +378,10 @@ def csr_dev(n, nnz, rowptr, col, val):
 
 
 def layer_desc(kind, act, n, s_in, s_out, dtype=GIST_DTYPE_F32, order=GIST_ORDER_AUTO,
-               groups=1, flags=0):
+               groups=1, flags=0, n_in=0):
+    """``n_in``: input rows of a rectangular (layer-sampled) GCN layer; 0 means n."""
     return gist_layer_desc(int(kind), int(act), int(dtype), int(order), int(n), int(s_in),
-                           int(s_out), int(groups), int(flags))
+                           int(s_out), int(groups), int(flags), int(n_in))
 
 
 def gist_layer_workspace_size(desc):

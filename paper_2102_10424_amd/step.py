@@ -48,6 +48,13 @@ class DeviceBatch:
         self.X = X_b
         self.labels = labels_b
 
+    def rows(self, l):
+        """Rows of the activations entering layer l (every layer: the batch)."""
+        return self.n
+
+    def adj(self, l):
+        return self.A, self.A_T
+
 
 class BatchSlot:
     """Reusable buffers for one mini-batch: pinned host staging + device copies.
@@ -125,7 +132,8 @@ class BatchSlot:
 
 
 class BatchPipeline:
-    """Cluster mini-batches built ahead of use on host worker threads.
+    """Mini-batches built ahead of use on host worker threads (cluster
+    mini-batches, or LADIES ones with :meth:`ladies`).
 
     A ring of ``depth`` :class:`BatchSlot` s; batch k is built (host CSR,
     ``gist_build_minibatch_csr`` -- which releases the interpreter lock) into
@@ -137,25 +145,37 @@ class BatchPipeline:
     """
 
     def __init__(self, ctx, norm, cap_n, cap_nnz, d_in, graph_struct, X_dev, labels_host,
-                 clusters_iter, depth=8, workers=4):
+                 clusters_iter, depth=8, workers=4, slots=None, build=None):
         from collections import deque
         from concurrent.futures import ThreadPoolExecutor
-        self.slots = [BatchSlot(ctx, norm, cap_n, cap_nnz, d_in) for _ in range(depth)]
+        self.slots = slots if slots is not None else \
+            [BatchSlot(ctx, norm, cap_n, cap_nnz, d_in) for _ in range(depth)]
         self.graph, self.X, self.labels = graph_struct, X_dev, labels_host
+        self._build = build if build is not None else \
+            (lambda slot, item: slot.build(self.graph, item, self.labels))
         self.src = iter(clusters_iter)
         self.pool = ThreadPoolExecutor(max_workers=workers)
         self.pending = deque()
         self.k = 0           # next batch to submit
-        for _ in range(depth):
+        for _ in range(len(self.slots)):
             self._submit()
+
+    @classmethod
+    def ladies(cls, ctx, L, b, s, max_degree, d_in, A_handle, X_dev, labels_host, items,
+               depth=8, workers=4):
+        """A pipeline of LADIES mini-batches; ``items`` yields (output nodes, seed)."""
+        slots = [LadiesSlot(ctx, L, b, s, max_degree, d_in) for _ in range(depth)]
+        return cls(ctx, None, 0, 0, d_in, None, X_dev, labels_host, items, workers=workers,
+                   slots=slots,
+                   build=lambda slot, item: slot.build(A_handle, item[0], item[1], labels_host))
 
     def _submit(self):
         try:
-            clusters = next(self.src)
+            item = next(self.src)
         except StopIteration:
             return
         slot = self.slots[self.k % len(self.slots)]
-        self.pending.append((slot, self.pool.submit(slot.build, self.graph, clusters, self.labels)))
+        self.pending.append((slot, self.pool.submit(self._build, slot, item)))
         self.k += 1
 
     def next(self):
@@ -178,6 +198,123 @@ class _View:
         self.A_T = G.csr_dev(n, nnz, d["t_rowptr"], d["t_col"], d["t_val"]) if sage else None
         self.X = X
         self.labels = d["labels"][:n]
+
+    def rows(self, l):
+        return self.n
+
+    def adj(self, l):
+        return self.A, self.A_T
+
+
+class LadiesSlot:
+    """Reusable buffers for one LADIES mini-batch (Section 5.4, Appendix A.6:
+    layer-wise sampling in place of graph partitioning, GCN only).
+
+    ``build`` runs ``gist_ladies_sample`` on the host straight into pinned
+    per-layer staging buffers; ``upload`` enqueues their copies on the
+    current stream and gathers the input layer's feature rows (V_0) on the
+    device.  Capacities follow from the batch size b and the draws s per
+    layer: |V_l| <= b + (L - l) s, and a layer's entries are at most its
+    rows times (largest degree + 1).
+    """
+
+    def __init__(self, ctx, L, b, s, max_degree, d_in, device="cuda"):
+        self.ctx, self.L, self.b, self.s = ctx, L, int(b), int(s)
+        self.device = device
+        pin = dict(pin_memory=True)
+        i32, f32 = torch.int32, torch.float32
+        self.caps = []
+        for l in range(L):
+            cap_n = self.b + (L - l) * self.s
+            rows = self.b + (L - l - 1) * self.s
+            self.caps.append((cap_n, rows * (int(max_degree) + 1)))
+        self.h, self.d = [], []
+        self.arr = (G.gist_ladies_layer * L)()
+        for l, (cn, cz) in enumerate(self.caps):
+            h = dict(nodes=torch.empty(cn, dtype=i32, **pin),
+                     rowptr=torch.empty(cn + 1, dtype=i32, **pin),
+                     col=torch.empty(cz, dtype=i32, **pin), val=torch.empty(cz, dtype=f32, **pin),
+                     t_rowptr=torch.empty(cn + 1, dtype=i32, **pin),
+                     t_col=torch.empty(cz, dtype=i32, **pin),
+                     t_val=torch.empty(cz, dtype=f32, **pin))
+            self.h.append(h)
+            self.d.append({k: torch.empty_like(v, device=device) for k, v in h.items()})
+            a = self.arr[l]
+            a.cap_n, a.cap_nnz = cn, cz
+            for k, v in h.items():
+                setattr(a, k, v.data_ptr())
+        self.batch_h = torch.empty(self.b, dtype=i32, **pin)
+        self.labels_h = torch.empty(self.b, dtype=i32, **pin)
+        self.labels_d = torch.empty(self.b, dtype=i32, device=device)
+        self.X = torch.empty(self.caps[0][0], d_in, device=device)
+        self.d_in = d_in
+        self.uploaded = None
+        self.built = None
+
+    def build(self, A_handle, batch, seed, labels_host):
+        """Host half: sample the layers and stage the labels of the output nodes."""
+        if self.uploaded is not None:
+            self.uploaded.synchronize()
+        batch = np.asarray(batch, dtype=np.int32)
+        nb = batch.shape[0]
+        if nb > self.b:
+            raise ValueError("batch larger than the slot's capacity")
+        self.batch_h.numpy()[:nb] = batch
+        G.ladies_sample_into(A_handle, self.batch_h.numpy()[:nb], self.L, self.s, seed, self.arr)
+        self.labels_h.numpy()[:nb] = labels_host[batch]
+        self.built = (nb, [(int(a.n_out), int(a.n_in), int(a.nnz)) for a in self.arr])
+
+    def upload(self, X_dev):
+        """Device half: asynchronous uploads on the current stream and the
+        gather of the input nodes' features."""
+        nb, sizes = self.built
+        for l, (n_out, n_in, nnz) in enumerate(sizes):
+            h, d = self.h[l], self.d[l]
+            cnt = dict(nodes=n_in, rowptr=n_out + 1, t_rowptr=n_in + 1)
+            for k in h:
+                c = cnt.get(k, nnz)
+                if c:
+                    d[k][:c].copy_(h[k][:c], non_blocking=True)
+        if nb:
+            self.labels_d[:nb].copy_(self.labels_h[:nb], non_blocking=True)
+        ev = torch.cuda.Event()
+        ev.record()
+        self.uploaded = ev
+        n0 = sizes[0][1]
+        Xb = self.X[:n0]
+        if n0:
+            G.gist_gather_slice(self.ctx, X_dev, self.d_in, self.d[0]["nodes"], n0, None,
+                                self.d_in, Xb, self.d_in)
+        return LadiesView(sizes, self.d, Xb, self.labels_d[:nb])
+
+    def load(self, A_handle, batch, seed, X_dev, labels_host):
+        self.build(A_handle, batch, seed, labels_host)
+        return self.upload(X_dev)
+
+
+class LadiesView:
+    """A loaded LADIES mini-batch: per-layer rectangular matrices (rows
+    V_{l+1}, columns V_l) with their transposes, the features of V_0 and
+    the labels of the output nodes V_L."""
+
+    def __init__(self, sizes, d, X, labels):
+        self.sizes = sizes
+        self._rows = [s[1] for s in sizes] + [sizes[-1][0]]
+        self._A = [G.csr_dev(n_out, nnz, d[l]["rowptr"], d[l]["col"], d[l]["val"])
+                   for l, (n_out, n_in, nnz) in enumerate(sizes)]
+        self._AT = [G.csr_dev(n_in, nnz, d[l]["t_rowptr"], d[l]["t_col"], d[l]["t_val"])
+                    for l, (n_out, n_in, nnz) in enumerate(sizes)]
+        self.X = X
+        self.labels = labels
+        self.n = self._rows[-1]
+        self.nnz = sum(s[2] for s in sizes)
+
+    def rows(self, l):
+        """|V_l|: rows of the activations entering layer l (l = L: the output nodes)."""
+        return self._rows[l]
+
+    def adj(self, l):
+        return self._A[l], self._AT[l]
 
 
 class SubGCN:
@@ -231,21 +368,25 @@ class SubGCN:
         self.loss_ws = torch.empty(G.gist_softmax_xent_workspace(n_cap), dtype=torch.uint8,
                                    device=d)
 
-    def desc(self, l, n, nnz=0):
+    def desc(self, l, n, nnz=0, n_in=0):
+        """Layer l's descriptor for n output rows (n_in input rows, 0: n)."""
         act = G.GIST_ACT_RELU if l < self.L - 1 else G.GIST_ACT_NONE
         if self.gat:
             return G.gat_desc(n, nnz, self.widths[l], self.widths[l + 1], act, self.dtype,
                               GAT_SLOPE)
         return G.layer_desc(self.lkind, act, n, self.widths[l], self.widths[l + 1],
-                            self.dtype, self.order)
+                            self.dtype, self.order, n_in=n_in)
 
-    def _workspace(self, n, nnz=0):
+    def _ldesc(self, batch, l):
+        return self.desc(l, batch.rows(l + 1), batch.nnz, batch.rows(l))
+
+    def _workspace(self, batch):
         need = 0
         for l in range(self.L):
             if self.gat:
-                f, b = G.gist_gat_workspace_size(self.desc(l, n, nnz))
+                f, b = G.gist_gat_workspace_size(self._ldesc(batch, l))
             else:
-                f, b = G.gist_layer_workspace_size(self.desc(l, n))
+                f, b = G.gist_layer_workspace_size(self._ldesc(batch, l))
             need = max(need, f, b)
         if self.ws.numel() < need:
             self.ws = torch.empty(need, dtype=torch.uint8, device=self.device)
@@ -257,48 +398,56 @@ class SubGCN:
         return t[:s], t[s], t[s + 1]
 
     def forward(self, batch, params):
-        n, nnz = batch.n, batch.nnz
-        if n > self.n_cap:
-            self._alloc(n)
+        """Every layer's forward.  A batch gives the rows entering each layer
+        (``rows(l)``) and each layer's matrix (``adj(l)``): the same for every
+        layer for a cluster mini-batch, per layer for a LADIES one."""
+        nnz = batch.nnz
+        n_max = max(batch.rows(l) for l in range(self.L + 1))
+        if n_max > self.n_cap:
+            self._alloc(n_max)
         if self.gat and (self.alpha is None or nnz > self.nnz_cap):
             self.nnz_cap = max(nnz, 1)
             self.alpha = [torch.empty(self.nnz_cap, device=self.device) for _ in range(self.L)]
-        ws = self._workspace(n, nnz)
+        ws = self._workspace(batch)
         H = batch.X
         for l in range(self.L):
+            n = batch.rows(l + 1)
+            A = batch.adj(l)[0]
             out = self.H[l + 1][:n]
             if self.gat:
                 W, a1, a2 = self._gat_parts(params[l], l)
-                G.gist_gat_layer_fwd(self.ctx, self.desc(l, n, nnz), batch.A, H, W, a1, a2,
+                G.gist_gat_layer_fwd(self.ctx, self._ldesc(batch, l), A, H, W, a1, a2,
                                      self.agg[l][:n], self.alpha[l][:nnz], out, ws)
             else:
-                G.gist_gcn_layer_fwd(self.ctx, self.desc(l, n), batch.A, H, params[l],
+                G.gist_gcn_layer_fwd(self.ctx, self._ldesc(batch, l), A, H, params[l],
                                      self.agg[l][:n], out, ws)
             H = out
-        return self.H[self.L][:n]
+        return self.H[self.L][:batch.rows(self.L)]
 
     def loss_and_grad(self, batch, loss_out=None):
         """Loss into ``loss_out`` (a one-element device tensor) or ``self.loss``."""
-        n = batch.n
+        n = batch.rows(self.L)
         G.gist_softmax_xent(self.ctx, n, self.widths[-1], self.H[self.L][:n], batch.labels,
                             self.loss if loss_out is None else loss_out, self.dlogits[:n],
                             self.loss_ws)
 
     def backward(self, batch, params):
-        n, nnz = batch.n, batch.nnz
-        ws = self._workspace(n, nnz)
-        dout = self.dlogits[:n]
+        nnz = batch.nnz
+        ws = self._workspace(batch)
+        dout = self.dlogits[:batch.rows(self.L)]
         for l in reversed(range(self.L)):
-            Hin = batch.X if l == 0 else self.H[l][:n]
-            dH = self.dH[l][:n] if l > 0 else None
+            n, n_in = batch.rows(l + 1), batch.rows(l)
+            A, A_T = batch.adj(l)
+            Hin = batch.X if l == 0 else self.H[l][:n_in]
+            dH = self.dH[l][:n_in] if l > 0 else None
             if self.gat:
                 W, a1, a2 = self._gat_parts(params[l], l)
                 gW, g1, g2 = self._gat_parts(self.dW[l], l)
-                G.gist_gat_layer_bwd(self.ctx, self.desc(l, n, nnz), batch.A, Hin,
+                G.gist_gat_layer_bwd(self.ctx, self._ldesc(batch, l), A, Hin,
                                      self.agg[l][:n], self.alpha[l][:nnz], self.H[l + 1][:n],
                                      W, a1, a2, dout, gW, g1, g2, dH, ws)
             else:
-                G.gist_gcn_layer_bwd(self.ctx, self.desc(l, n), batch.A, batch.A_T, Hin,
+                G.gist_gcn_layer_bwd(self.ctx, self._ldesc(batch, l), A, A_T, Hin,
                                      self.agg[l][:n], self.H[l + 1][:n], params[l], dout,
                                      self.dW[l], dH, ws)
             dout = dH

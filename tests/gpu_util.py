@@ -51,4 +51,5 @@ def csr_to_dev(csr, transpose=False):
                  np.zeros(1, np.int32))
     val = to_dev(np.asarray(csr[k + "val"], dtype=np.float32)[:max(nnz, 1)] if nnz else
                  np.zeros(1, np.float32))
-    return G.csr_dev(csr["n"], nnz, rp, col, val), (rp, col, val)
+    rows = csr.get("n_in", csr["n"]) if transpose else csr["n"]   # rectangular: n x n_in
+    return G.csr_dev(rows, nnz, rp, col, val), (rp, col, val)

@@ -189,3 +189,109 @@ def test_binding_signatures_match_header():
         got = [_ctype_kind(t) for t in f.argtypes]
         want = [_param_kind(p) for p in params]
         assert got == want, (name, got, want)
+
+
+# ---- LADIES sampler ------------------------------------------------------------------
+
+def _same_ladies(lib, ora):
+    L = len(ora["layers"])
+    assert len(lib["layers"]) == L
+    for l in range(L + 1):
+        assert np.array_equal(np.asarray(lib["nodes"][l], np.int64),
+                              np.asarray(ora["nodes"][l], np.int64)), l
+    for l in range(L):
+        a, b = lib["layers"][l], ora["layers"][l]
+        assert (a["n"], a["n_in"], a["nnz"]) == (b["n"], b["n_in"], b["nnz"]), l
+        for k in ("rowptr", "col", "t_rowptr", "t_col"):
+            assert np.array_equal(np.asarray(a[k], np.int64), np.asarray(b[k], np.int64)), (l, k)
+        for k in ("val", "t_val"):
+            assert a[k].dtype == np.float32 and b[k].dtype == np.float32
+            assert np.array_equal(a[k].view(np.uint32), b[k].view(np.uint32)), (l, k)
+
+
+LADIES_GRAPHS = {
+    "er": lambda: erdos_renyi(400, 1200, seed=5),
+    "chung_lu": lambda: chung_lu(3000, 2.2, 6.0, seed=6),      # hubs: very uneven p
+    "sbm": lambda: sbm(5000, 40, 25.0, 0.9, seed=7),
+}
+
+
+@pytest.mark.parametrize("gname", sorted(LADIES_GRAPHS))
+@pytest.mark.parametrize("L,s,b", [(1, 64, 16), (2, 128, 40), (3, 50, 9), (2, 0, 12),
+                                   (2, 1, 1), (2, 1000, 100)])
+def test_ladies_sample_bit_exact(gname, L, s, b):
+    from oracle import ladies as LD
+    g = LADIES_GRAPHS[gname]()
+    A = MB.build(g, None, "gcn")
+    h = G.CsrHandle(A)
+    rng = np.random.default_rng(L * 1000 + s + b)
+    for seed in (0, 77, 2**64 - 1):
+        batch = np.sort(rng.choice(g.n, b, replace=False))
+        _same_ladies(G.gist_ladies_sample(h, batch, L, s, seed), LD.sample(A, batch, L, s, seed))
+
+
+def test_ladies_sample_reddit_sized():
+    """Batch of 512 output nodes, 512 draws per layer, on the 232,965-node graph."""
+    from oracle import ladies as LD
+    g = get_config("c3").make_graph()
+    A = G.gist_build_minibatch_csr(g, None, "gcn")
+    batch = np.sort(np.random.default_rng(11).choice(g.n, 512, replace=False))
+    for L in (2, 3):
+        lib = G.gist_ladies_sample(A, batch, L, 512, 1234 + L)
+        _same_ladies(lib, LD.sample(A, batch, L, 512, 1234 + L))
+        assert lib["layers"][0]["n_in"] > 512
+
+
+def test_ladies_sample_edge_cases_and_errors():
+    from oracle import ladies as LD
+    g = erdos_renyi(50, 20, seed=2)             # many isolated nodes
+    A = MB.build(g, None, "gcn")
+    deg = np.diff(g.rowptr)
+    iso = int(np.nonzero(deg == 0)[0][0])
+    for batch in ([], [iso], sorted({0, iso, 49})):
+        _same_ladies(G.gist_ladies_sample(A, batch, 2, 8, 3), LD.sample(A, batch, 2, 8, 3))
+    h = G.CsrHandle(A)
+    for batch in ([3, 2], [50], [-1], [4, 4]):
+        with pytest.raises(G.GistError) as e:
+            G.gist_ladies_sample(h, batch, 2, 8, 3)
+        assert e.value.status == G.GIST_E_INVAL
+    with pytest.raises(G.GistError):
+        G.gist_ladies_sample(h, [1], 0, 8, 3)
+    with pytest.raises(G.GistError):
+        G.gist_ladies_sample(h, [1], 1, -1, 3)
+    # capacity too small: NOMEM, and the sizes are still reported
+    q, _ = G.ladies_layers(2)
+    G.ladies_sample_into(h, [0, 1, 2], 2, 8, 3, q)
+    need = [(q[l].n_in, q[l].nnz) for l in range(2)]
+    arr, _ = G.ladies_layers(2, [(need[0][0] - 1, need[0][1]), need[1]])
+    with pytest.raises(G.GistError) as e:
+        G.ladies_sample_into(h, [0, 1, 2], 2, 8, 3, arr)
+    assert e.value.status == G.GIST_E_NOMEM
+    assert [(arr[l].n_in, arr[l].nnz) for l in range(2)] == need
+
+
+def test_struct_layouts_match_header(tmp_path):
+    """Offsets and sizes of every ctypes structure equal the C compiler's for
+    the header's struct of the same name."""
+    import ctypes as C
+    import subprocess
+    structs = [G.gist_graph, G.gist_csr, G.gist_csr_dev, G.gist_layer_desc, G.gist_gat_desc,
+               G.gist_slice_set, G.gist_prof_entry, G.gist_ladies_layer]
+    lines = ["#include <stdio.h>", "#include <stddef.h>", f'#include "{HEADER}"',
+             "int main(void) {"]
+    for st in structs:
+        lines.append(f'  printf("%zu\\n", sizeof({st.__name__}));')
+        for f in st._fields_:
+            lines.append(f'  printf("%zu\\n", offsetof({st.__name__}, {f[0]}));')
+    lines.append("  return 0; }")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", str(src), "-o", str(exe)], check=True)
+    got = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True,
+                                          check=True).stdout.split()]
+    want = []
+    for st in structs:
+        want.append(C.sizeof(st))
+        want += [getattr(st, f[0]).offset for f in st._fields_]
+    assert got == want
