@@ -89,7 +89,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5", "c6"])
+    ap.add_argument("--config", default="c4",
+                    choices=["c1", "c2", "c3", "c4", "c5", "c6", "c7"])
     ap.add_argument("--dtype", default="f32", choices=["f32", "bf16"])
     ap.add_argument("--d-in", type=int, default=256, help="c5 input slice width")
     ap.add_argument("--lr", type=float, default=0.01)
@@ -139,8 +140,14 @@ class RoundWorkload:
         self.zeta = zeta
         self.model = GistModel(ctx, cfg.kind, cfg.widths, cfg.m, theta, adam=self.adam)
         self.norm = "sage" if cfg.kind == "sage" else "gcn"
+        self.ladies = cfg.ladies
+        if self.ladies and shared:
+            raise ValueError("LADIES mini-batches are per sub-GCN (no shared batch)")
         # capacities: the largest mini-batch of the clusters, generous nnz bound
-        if cfg.batch_clusters is None:
+        if self.ladies:
+            cap_n = self.ladies["batch"] + cfg.L * self.ladies["samples"]
+            cap_nnz = 0
+        elif cfg.batch_clusters is None:
             cap_n = self.graph.n
             cap_nnz = self.graph.nnz + self.graph.n
         else:
@@ -155,7 +162,20 @@ class RoundWorkload:
         self.streams = [torch.cuda.current_stream()] + [torch.cuda.Stream()
                                                          for _ in range(self.nstreams - 1)]
         self.ctxs = [ctx] + [G.Context(0, stream=st.cuda_stream) for st in self.streams[1:]]
-        if cfg.batch_clusters is None:
+        if self.ladies:
+            # LADIES mini-batches sampled from the full-graph GCN matrix on host workers
+            t0 = time.time()
+            self.A_full = G.CsrHandle(G.gist_build_minibatch_csr(self.graph, None, "gcn"))
+            max_deg = int(np.max(np.diff(self.graph.rowptr)))
+            log(f"[bench] full GCN matrix nnz={self.A_full.nnz} ({time.time() - t0:.1f}s)")
+            self.pipes = [BatchPipeline.ladies(c, cfg.L, self.ladies["batch"],
+                                               self.ladies["samples"], max_deg, cfg.widths[0],
+                                               self.A_full, self.X, self.labels,
+                                               self._ladies_order(zeta, k, self.nstreams),
+                                               depth=8, workers=8 if self.nstreams == 1 else 4)
+                          for k, c in enumerate(self.ctxs)]
+            self.pipe = self.pipes[0]
+        elif cfg.batch_clusters is None:
             self.slots = [BatchSlot(ctx, self.norm, cap_n, cap_nnz, cfg.widths[0])]
         else:
             # mini-batches are built on host worker threads ahead of use
@@ -186,8 +206,17 @@ class RoundWorkload:
                     yield cfg.minibatch(t, i, z)
             t += 1
 
+    def _ladies_order(self, zeta, k=0, nstreams=1):
+        """(output nodes, draw seed) of every LADIES mini-batch of stream k."""
+        cfg, t = self.cfg, 0
+        while True:
+            for i in range(k, cfg.m, nstreams):
+                for z in range(zeta):
+                    yield cfg.ladies_batch(t, i, z), cfg.ladies_seed(t, i, z)
+            t += 1
+
     def _batch(self, t, i, z, k=0):
-        if self.cfg.batch_clusters is None:
+        if self.cfg.batch_clusters is None and not self.ladies:
             if self.full is None:
                 self.full = self.slots[0].load(self.gh, None, self.X, self.labels)
             return self.full
@@ -243,12 +272,19 @@ class RoundWorkload:
 
     def describe(self):
         c = self.cfg
+        if self.ladies:
+            batch = (f"LADIES mini-batch: {self.ladies['batch']} output nodes, "
+                     f"{self.ladies['samples']} draws per layer")
+        elif c.batch_clusters:
+            batch = f"mini-batch {c.batch_clusters} clusters"
+        else:
+            batch = "full graph"
         return {"workload": f"{c.name}: GIST round, {c.L}-layer "
                             f"{dict(sage='GraphSAGE-mean', gcn='GCN', gat='GAT')[c.kind]}, hidden "
-                            f"{c.widths[1]} split m={c.m}, N={c.n_nodes}, "
-                            f"{'mini-batch ' + str(c.batch_clusters) + ' clusters' if c.batch_clusters else 'full graph'}",
+                            f"{c.widths[1]} split m={c.m}, N={c.n_nodes}, {batch}",
                 "model": "GIST sub-GCN", "m": c.m, "widths": c.widths,
-                "global_batch": c.batch_clusters or c.n_nodes, "zeta": self.zeta,
+                "global_batch": (self.ladies["batch"] if self.ladies else
+                                 c.batch_clusters or c.n_nodes), "zeta": self.zeta,
                 "batching": "m sub-GCNs on one shared mini-batch (batched layers)" if self.shared
                             else "one mini-batch per sub-GCN",
                 "optimizer": f"adam ({self.adam} moments)" if self.adam else "sgd"}
@@ -274,15 +310,28 @@ class RoundWorkload:
                 params.append((ps[0], ps[1][0], ps[1][1]))
             else:
                 params.append(ps[0] if cfg.kind == "gcn" else (ps[0], ps[1]))
-        csr = OM.build(self.graph, cfg.minibatch(0, 0), self.norm)
-        nm = csr["node_map"]
-        X = cfg.features_matrix(rows=nm)
-        y = self.labels[nm]
+        if self.ladies:
+            from oracle import ladies as OLD
+            A = OM.build(self.graph, None, "gcn")
+            t0 = time.time()
+            smp = OLD.sample(A, cfg.ladies_batch(0, 0), cfg.L, self.ladies["samples"],
+                             cfg.ladies_seed(0, 0))
+            t_s = time.time() - t0
+            csr = smp["layers"]
+            X = cfg.features_matrix(rows=smp["nodes"][0])
+            y = self.labels[smp["nodes"][cfg.L]]
+        else:
+            csr = OM.build(self.graph, cfg.minibatch(0, 0), self.norm)
+            nm = csr["node_map"]
+            X = cfg.features_matrix(rows=nm)
+            y = self.labels[nm]
+            t_s = 0.0
         t0 = time.time()
         OG.sub_gcn_step(cfg.kind, csr, X, y, params, self.lr)
-        dt = time.time() - t0
+        dt = time.time() - t0 + t_s
         return dt * 1e3, "one sub-GCN step (fwd + loss + bwd + SGD) of round 0, sub-GCN 0, " \
-                         "fp64; excludes partition, slice gather and subAgg"
+                         "fp64" + (", with its LADIES sampling" if self.ladies else "") + \
+                         "; excludes partition, slice gather and subAgg"
 
 
 class LayerWorkload:
@@ -411,11 +460,15 @@ def main():
         for c in ctxs:
             G.gist_profile_begin(c, 1 << 16)
     torch.cuda.synchronize()
+    pipes = getattr(wl, "pipes", [])
+    for p in pipes:
+        p.wait_s = 0.0
     t0 = time.perf_counter()
     for s in range(args.steps):
         wl.step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    host_wait_ms = sum(p.wait_s for p in pipes) * 1e3 / args.steps
     log(f"[bench] timed {args.steps} steps")
     ms_step = (t1 - t0) * 1e3 / args.steps
     prof, dropped = ({}, 0)
@@ -486,6 +539,7 @@ def main():
                        value="ms per sub-GCN step (round time / (m zeta))" if per_unit > 1
                        else "ms per layer fwd+bwd"),
         "roofline": roofline, "cpu_baseline": cpu, "kernels": kernels,
+        "host_batch_wait_ms_per_step": round(host_wait_ms, 3),
         "profile_dropped": dropped, "kernel_src_sha256": kernel_source_hash(),
     }
     print(json.dumps(out), flush=True)

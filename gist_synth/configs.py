@@ -17,6 +17,9 @@ Sizes follow the paper's datasets (Table 5) and experiments (Tables 1-3):
 * ``c6`` 3-layer GAT, m=4, on the c3 graph (same graph, features, labels
   and 20-block mini-batches), hidden 256 split into 4 x 64, 41 classes: the
   256-dimensional GAT the paper trains on Reddit (Table 2).
+* ``c7`` GIST with LADIES layer sampling (Section 5.4, Table 4): 2-layer GCN
+  602-256-41, m=4, on the c3 graph; a mini-batch is 512 output nodes drawn
+  uniformly and 512 LADIES draws per layer.
 
 Seeds: config ``k`` uses base seed 100 + k; every array is a named stream of
 that base (see :mod:`gist_synth.seeds`).
@@ -30,7 +33,7 @@ import numpy as np
 from . import graphs as _g
 from . import tensors as _t
 from .seeds import (STREAM_FEATURES, STREAM_LABELS, STREAM_THETA,
-                    STREAM_PARTITION, STREAM_MINIBATCH, STREAM_UPSTREAM,
+                    STREAM_PARTITION, STREAM_MINIBATCH, STREAM_UPSTREAM, STREAM_LADIES,
                     derive_seed, generator)
 
 
@@ -131,6 +134,22 @@ class Config:
         return np.sort(g.choice(c, size=self.batch_clusters, replace=False)
                        ).astype(np.int32)
 
+    @property
+    def ladies(self):
+        """LADIES sizes dict(batch=b, samples=s), or None (cluster mini-batches)."""
+        return self.extra.get("ladies")
+
+    def ladies_batch(self, t, i, z=0):
+        """Output nodes of sub-GCN ``i``'s LADIES mini-batch at round ``t``, step
+        ``z``: ``batch`` distinct nodes drawn uniformly, ascending."""
+        g = generator(self.seed, STREAM_MINIBATCH, t, i, z)
+        return np.sort(g.choice(self.n_nodes, size=self.ladies["batch"], replace=False)
+                       ).astype(np.int32)
+
+    def ladies_seed(self, t, i, z=0):
+        """Seed of the LADIES draws of that mini-batch."""
+        return derive_seed(self.seed, STREAM_LADIES, t, i, z)
+
     def upstream(self, n, w, rows=None):
         """Seeded N(0,1) upstream gradient dH' (n x w) for single-layer workloads."""
         return _t.normal_rows((n, w), self.seed, STREAM_UPSTREAM, w, rows=rows)
@@ -159,6 +178,11 @@ CONFIGS = {
                  dict(kind="sbm", n=232_965, blocks=1500, mean_degree=50.0,
                       intra=0.9), "normal", batch_clusters=20,
                  extra=dict(graph_seed=103)),
+    # c7: the c3 graph with a 2-layer GCN trained on LADIES mini-batches.
+    "c7": Config("c7", "gcn", [602, 256, 41], 4,
+                 dict(kind="sbm", n=232_965, blocks=1500, mean_degree=50.0,
+                      intra=0.9), "normal",
+                 extra=dict(graph_seed=103, ladies=dict(batch=512, samples=512))),
 }
 
 

@@ -17,6 +17,7 @@ STREAM_THETA = 4
 STREAM_PARTITION = 5
 STREAM_MINIBATCH = 6
 STREAM_UPSTREAM = 7
+STREAM_LADIES = 8
 
 
 def derive_seed(base, *keys):

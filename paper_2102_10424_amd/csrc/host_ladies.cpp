@@ -12,8 +12,9 @@
 // probability and weight, one rounding to float), so the result does not
 // depend on threads or vector width.  Only the columns the rows V_{l+1}
 // touch are visited: the distribution is kept compact (touched columns in
-// ascending order), which gives the same prefix sums as the full vector,
-// since the untouched columns add exact zeros.
+// ascending order, read off a bitmap of the graph's nodes), which gives the
+// same prefix sums as the full vector, since the untouched columns add
+// exact zeros.
 
 #include <algorithm>
 #include <cmath>
@@ -25,25 +26,32 @@
 
 namespace {
 
+// Per-node state, one record per graph node so that a visit of node j
+// touches one cache line: its importance q (zero outside the current layer's
+// touched columns) and its position in V_l, valid when `stamp` is current.
+struct NodeState {
+  double q;
+  int32_t pos;
+  uint32_t stamp;
+};
+
 // Per-thread scratch, sized to the graph once.
 struct Scratch {
-  std::vector<double> q;         // importance per global node (touched ones only non-zero)
-  std::vector<int32_t> pos;      // global node -> position in V_l, valid when stamp matches
-  std::vector<uint32_t> stamp;
+  std::vector<NodeState> node;
   uint32_t cur = 0;
-  std::vector<int32_t> touched;  // columns with q != 0
+  std::vector<uint64_t> seen;    // bitmap of the columns touched by the current layer
+  std::vector<int32_t> touched;  // columns with q > 0, ascending
   std::vector<double> prefix;
   void resize(int64_t n) {
-    if (static_cast<int64_t>(q.size()) != n) {
-      q.assign(static_cast<size_t>(n), 0.0);
-      pos.assign(static_cast<size_t>(n), 0);
-      stamp.assign(static_cast<size_t>(n), 0u);
+    if (static_cast<int64_t>(node.size()) != n) {
+      node.assign(static_cast<size_t>(n), NodeState{0.0, 0, 0u});
+      seen.assign(static_cast<size_t>((n + 63) / 64), 0ull);
       cur = 0;
     }
   }
   void next_stamp() {
     if (++cur == 0) {
-      std::fill(stamp.begin(), stamp.end(), 0u);
+      for (NodeState& x : node) x.stamp = 0u;
       cur = 1;
     }
   }
@@ -98,34 +106,37 @@ extern "C" gist_status gist_ladies_sample(const gist_csr* A, const int32_t* batc
       continue;
     }
     // importance of every column the rows V_{l+1} touch, rows in ascending order
-    S.touched.clear();
     for (int32_t i : V) {
       for (int32_t e = rp[i]; e < rp[i + 1]; ++e) {
         const int32_t j = ac[e];
         const double a = static_cast<double>(av[e]);
-        if (S.q[j] == 0.0) S.touched.push_back(j);
-        S.q[j] += a * a;
+        S.node[j].q += a * a;
+        S.seen[static_cast<size_t>(j) >> 6] |= 1ull << (j & 63);
       }
     }
-    std::sort(S.touched.begin(), S.touched.end());
-    S.touched.erase(std::unique(S.touched.begin(), S.touched.end()), S.touched.end());
-    // a column whose entries were all zero stays at q = 0 and is never drawn
-    S.touched.erase(std::remove_if(S.touched.begin(), S.touched.end(),
-                                   [&](int32_t j) { return !(S.q[j] > 0.0); }),
-                    S.touched.end());
+    // touched columns in ascending order (clearing the bitmap); a column whose
+    // entries were all zero keeps q = 0 and is never drawn
+    S.touched.clear();
+    for (size_t w = 0; w < S.seen.size(); ++w) {
+      uint64_t x = S.seen[w];
+      if (!x) continue;
+      S.seen[w] = 0;
+      while (x) {
+        const int32_t j = static_cast<int32_t>(w * 64 + static_cast<size_t>(__builtin_ctzll(x)));
+        x &= x - 1;
+        if (S.node[j].q > 0.0) S.touched.push_back(j);
+      }
+    }
     S.prefix.resize(S.touched.size());
     double run = 0.0;
     for (size_t k = 0; k < S.touched.size(); ++k) {
-      run += S.q[S.touched[k]];
+      run += S.node[S.touched[k]].q;
       S.prefix[k] = run;
     }
     const double Q = run;
     draws.clear();
-    if (s > 0 && S.touched.empty()) {
-      for (int32_t i : V)
-        for (int32_t e = rp[i]; e < rp[i + 1]; ++e) S.q[ac[e]] = 0.0;
+    if (s > 0 && S.touched.empty())   // every q is zero (and the bitmap clear)
       return set_error(GIST_E_INVAL, "gist_ladies_sample: no node has positive importance");
-    }
     if (s > 0) {
       for (int32_t k = 0; k < s; ++k) {
         const double u = static_cast<double>(rng.next() >> 11) * 0x1.0p-53;
@@ -143,8 +154,8 @@ extern "C" gist_status gist_ladies_sample(const gist_csr* A, const int32_t* batc
     std::set_union(draws.begin(), draws.end(), V.begin(), V.end(), std::back_inserter(Y.nodes));
     S.next_stamp();
     for (size_t k = 0; k < Y.nodes.size(); ++k) {
-      S.pos[Y.nodes[k]] = static_cast<int32_t>(k);
-      S.stamp[Y.nodes[k]] = S.cur;
+      S.node[Y.nodes[k]].pos = static_cast<int32_t>(k);
+      S.node[Y.nodes[k]].stamp = S.cur;
     }
     // rows: A_ij / (s p_j) over the kept columns, normalised by the row sum
     Y.col.clear();
@@ -154,11 +165,11 @@ extern "C" gist_status gist_ladies_sample(const gist_csr* A, const int32_t* batc
       const int32_t i = V[static_cast<size_t>(r)];
       w.clear();
       for (int32_t e = rp[i]; e < rp[i + 1]; ++e) {
-        const int32_t j = ac[e];
-        if (S.stamp[j] != S.cur) continue;
-        const double p = S.q[j] / Q;
+        const NodeState& x = S.node[ac[e]];
+        if (x.stamp != S.cur) continue;
+        const double p = x.q / Q;
         w.push_back(static_cast<double>(av[e]) / (s_eff * p));
-        Y.col.push_back(S.pos[j]);
+        Y.col.push_back(x.pos);
       }
       double sum = 0.0;
       for (double x : w) sum += x;
@@ -181,7 +192,7 @@ extern "C" gist_status gist_ladies_sample(const gist_csr* A, const int32_t* batc
         Y.t_val[d] = Y.val[e];
       }
     }
-    for (int32_t j : S.touched) S.q[j] = 0.0;   // leave the scratch zeroed
+    for (int32_t j : S.touched) S.node[j].q = 0.0;   // leave the scratch zeroed
     V = Y.nodes;
   }
 

@@ -156,6 +156,7 @@ class BatchPipeline:
         self.src = iter(clusters_iter)
         self.pool = ThreadPoolExecutor(max_workers=workers)
         self.pending = deque()
+        self.wait_s = 0.0    # time next() spent waiting for host builds
         self.k = 0           # next batch to submit
         for _ in range(len(self.slots)):
             self._submit()
@@ -180,6 +181,11 @@ class BatchPipeline:
 
     def next(self):
         slot, fut = self.pending.popleft()
+        if not fut.done():           # the host build is behind: time spent waiting for it
+            import time
+            t0 = time.perf_counter()
+            fut.result()
+            self.wait_s += time.perf_counter() - t0
         fut.result()
         view = slot.upload(self.X)
         self._submit()       # reuses this slot: its build waits for the upload just enqueued
@@ -210,13 +216,18 @@ class LadiesSlot:
     """Reusable buffers for one LADIES mini-batch (Section 5.4, Appendix A.6:
     layer-wise sampling in place of graph partitioning, GCN only).
 
-    ``build`` runs ``gist_ladies_sample`` on the host straight into pinned
-    per-layer staging buffers; ``upload`` enqueues their copies on the
-    current stream and gathers the input layer's feature rows (V_0) on the
-    device.  Capacities follow from the batch size b and the draws s per
-    layer: |V_l| <= b + (L - l) s, and a layer's entries are at most its
-    rows times (largest degree + 1).
+    ``build`` runs ``gist_ladies_sample`` on the host into pinned per-layer
+    staging arrays sized by the capacities, then packs what it produced
+    (every layer's node list, row pointers, entries and transpose, and the
+    output nodes' labels) into one contiguous pinned buffer; ``upload``
+    enqueues that buffer as a single copy on the current stream and gathers
+    the input layer's feature rows (V_0) on the device.  Capacities follow
+    from the batch size b and the draws s per layer: |V_l| <= b + (L - l) s,
+    and a layer's entries are at most its rows times (largest degree + 1).
     """
+
+    _ORDER = ("nodes", "rowptr", "t_rowptr", "col", "t_col", "val", "t_val")
+    _ALIGN = 64      # elements (256 bytes) between packed arrays
 
     def __init__(self, ctx, L, b, s, max_degree, d_in, device="cuda"):
         self.ctx, self.L, self.b, self.s = ctx, L, int(b), int(s)
@@ -228,8 +239,9 @@ class LadiesSlot:
             cap_n = self.b + (L - l) * self.s
             rows = self.b + (L - l - 1) * self.s
             self.caps.append((cap_n, rows * (int(max_degree) + 1)))
-        self.h, self.d = [], []
+        self.h = []
         self.arr = (G.gist_ladies_layer * L)()
+        total = 0
         for l, (cn, cz) in enumerate(self.caps):
             h = dict(nodes=torch.empty(cn, dtype=i32, **pin),
                      rowptr=torch.empty(cn + 1, dtype=i32, **pin),
@@ -238,54 +250,76 @@ class LadiesSlot:
                      t_col=torch.empty(cz, dtype=i32, **pin),
                      t_val=torch.empty(cz, dtype=f32, **pin))
             self.h.append(h)
-            self.d.append({k: torch.empty_like(v, device=device) for k, v in h.items()})
             a = self.arr[l]
             a.cap_n, a.cap_nnz = cn, cz
             for k, v in h.items():
                 setattr(a, k, v.data_ptr())
-        self.batch_h = torch.empty(self.b, dtype=i32, **pin)
-        self.labels_h = torch.empty(self.b, dtype=i32, **pin)
-        self.labels_d = torch.empty(self.b, dtype=i32, device=device)
+                total += self._pad(v.numel())
+        total += self._pad(self.b)          # labels
+        # packed transfer buffer: 4-byte elements (int32, float32 viewed as int32)
+        self.packed_h = torch.empty(total, dtype=i32, **pin)
+        self.packed_d = torch.empty(total, dtype=i32, device=device)
         self.X = torch.empty(self.caps[0][0], d_in, device=device)
         self.d_in = d_in
         self.uploaded = None
         self.built = None
 
+    @classmethod
+    def _pad(cls, n):
+        return (int(n) + cls._ALIGN - 1) // cls._ALIGN * cls._ALIGN
+
     def build(self, A_handle, batch, seed, labels_host):
-        """Host half: sample the layers and stage the labels of the output nodes."""
+        """Host half: sample the layers, pack them and the output nodes' labels."""
         if self.uploaded is not None:
-            self.uploaded.synchronize()
+            self.uploaded.synchronize()     # the previous upload from packed_h is done
         batch = np.asarray(batch, dtype=np.int32)
         nb = batch.shape[0]
         if nb > self.b:
             raise ValueError("batch larger than the slot's capacity")
-        self.batch_h.numpy()[:nb] = batch
-        G.ladies_sample_into(A_handle, self.batch_h.numpy()[:nb], self.L, self.s, seed, self.arr)
-        self.labels_h.numpy()[:nb] = labels_host[batch]
-        self.built = (nb, [(int(a.n_out), int(a.n_in), int(a.nnz)) for a in self.arr])
+        G.ladies_sample_into(A_handle, batch, self.L, self.s, seed, self.arr)
+        packed = self.packed_h.numpy()
+        off, offs, sizes = 0, [], []
+        for l in range(self.L):
+            a = self.arr[l]
+            n_out, n_in, nnz = int(a.n_out), int(a.n_in), int(a.nnz)
+            cnt = dict(nodes=n_in, rowptr=n_out + 1, t_rowptr=n_in + 1)
+            o = {}
+            for k in self._ORDER:
+                c = cnt.get(k, nnz)
+                src = self.h[l][k].numpy()[:c]
+                packed[off:off + c] = src.view(np.int32)
+                o[k] = off
+                off += self._pad(c)
+            offs.append(o)
+            sizes.append((n_out, n_in, nnz))
+        packed[off:off + nb] = labels_host[batch]
+        lab = off
+        off += self._pad(nb)
+        self.built = (nb, sizes, offs, lab, off)
 
     def upload(self, X_dev):
-        """Device half: asynchronous uploads on the current stream and the
+        """Device half: one asynchronous copy on the current stream and the
         gather of the input nodes' features."""
-        nb, sizes = self.built
-        for l, (n_out, n_in, nnz) in enumerate(sizes):
-            h, d = self.h[l], self.d[l]
-            cnt = dict(nodes=n_in, rowptr=n_out + 1, t_rowptr=n_in + 1)
-            for k in h:
-                c = cnt.get(k, nnz)
-                if c:
-                    d[k][:c].copy_(h[k][:c], non_blocking=True)
-        if nb:
-            self.labels_d[:nb].copy_(self.labels_h[:nb], non_blocking=True)
+        nb, sizes, offs, lab, total = self.built
+        d = self.packed_d
+        d[:total].copy_(self.packed_h[:total], non_blocking=True)
         ev = torch.cuda.Event()
         ev.record()
         self.uploaded = ev
+        f32 = torch.float32
+        views = []
+        for l, (n_out, n_in, nnz) in enumerate(sizes):
+            o = offs[l]
+            v = {k: d[o[k]:] for k in ("nodes", "rowptr", "t_rowptr", "col", "t_col")}
+            v["val"] = d[o["val"]:o["val"] + max(nnz, 1)].view(f32)
+            v["t_val"] = d[o["t_val"]:o["t_val"] + max(nnz, 1)].view(f32)
+            views.append(v)
         n0 = sizes[0][1]
         Xb = self.X[:n0]
         if n0:
-            G.gist_gather_slice(self.ctx, X_dev, self.d_in, self.d[0]["nodes"], n0, None,
+            G.gist_gather_slice(self.ctx, X_dev, self.d_in, views[0]["nodes"], n0, None,
                                 self.d_in, Xb, self.d_in)
-        return LadiesView(sizes, self.d, Xb, self.labels_d[:nb])
+        return LadiesView(sizes, views, Xb, d[lab:lab + nb])
 
     def load(self, A_handle, batch, seed, X_dev, labels_host):
         self.build(A_handle, batch, seed, labels_host)
