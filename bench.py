@@ -103,6 +103,8 @@ def parse():
                     help="HIP streams the m sub-GCN steps of a round are spread over")
     ap.add_argument("--shared-batch", action="store_true",
                     help="all m sub-GCNs step on one shared mini-batch, as batched layer calls")
+    ap.add_argument("--graphs", action="store_true",
+                    help="LADIES workloads: replay every sub-GCN step from a HIP graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the library's per-launch event timing")
@@ -116,11 +118,11 @@ class RoundWorkload:
     """A GIST round (partition, gather, m sub-GCN steps, subAgg) on one GPU."""
 
     def __init__(self, cfg, ctx, dtype, optimizer="sgd", policy="carry", zeta=1, shared=False,
-                 streams=1):
+                 streams=1, graphs=False):
         import torch
         from paper_2102_10424_amd import gist as G
-        from paper_2102_10424_amd.step import (BatchPipeline, BatchSlot, GistModel, SubGCN,
-                                               SubGCNBatch)
+        from paper_2102_10424_amd.step import (BatchPipeline, BatchSlot, GistModel,
+                                               LadiesGraphRunner, SubGCN, SubGCNBatch)
         self.cfg, self.ctx, self.G = cfg, ctx, G
         t0 = time.time()
         self.graph = cfg.make_graph()
@@ -143,6 +145,9 @@ class RoundWorkload:
         self.ladies = cfg.ladies
         if self.ladies and shared:
             raise ValueError("LADIES mini-batches are per sub-GCN (no shared batch)")
+        if graphs and (not self.ladies or optimizer != "sgd"):
+            raise ValueError("--graphs replays LADIES sub-GCN steps with SGD")
+        self.use_graphs = self.graphs = graphs
         # capacities: the largest mini-batch of the clusters, generous nnz bound
         if self.ladies:
             cap_n = self.ladies["batch"] + cfg.L * self.ladies["samples"]
@@ -172,7 +177,9 @@ class RoundWorkload:
                                                self.ladies["samples"], max_deg, cfg.widths[0],
                                                self.A_full, self.X, self.labels,
                                                self._ladies_order(zeta, k, self.nstreams),
-                                               depth=8, workers=8 if self.nstreams == 1 else 4)
+                                               depth=12 if graphs else 8,
+                                               workers=(12 if graphs else 8) // self.nstreams,
+                                               fixed=graphs)
                           for k, c in enumerate(self.ctxs)]
             self.pipe = self.pipes[0]
         elif cfg.batch_clusters is None:
@@ -193,6 +200,11 @@ class RoundWorkload:
             self.runners = [SubGCN(c, cfg.kind, self.model.slice_widths, cap_n, dtype=dt)
                             for c in self.ctxs]
             self.runner = self.runners[0]
+            if graphs:
+                self.graph_runners = [
+                    LadiesGraphRunner(c, self.model.slice_widths, cfg.L, self.ladies["batch"],
+                                      self.ladies["samples"], cfg.widths[0], self.X, dtype=dt)
+                    for c in self.ctxs]
         self.lr = 0.01
         self.t = 0
 
@@ -207,12 +219,14 @@ class RoundWorkload:
             t += 1
 
     def _ladies_order(self, zeta, k=0, nstreams=1):
-        """(output nodes, draw seed) of every LADIES mini-batch of stream k."""
+        """Every LADIES mini-batch of stream k, as a callable the pipeline's
+        worker evaluates to (output nodes, draw seed)."""
         cfg, t = self.cfg, 0
         while True:
             for i in range(k, cfg.m, nstreams):
                 for z in range(zeta):
-                    yield cfg.ladies_batch(t, i, z), cfg.ladies_seed(t, i, z)
+                    yield (lambda t=t, i=i, z=z: (cfg.ladies_batch(t, i, z),
+                                                  cfg.ladies_seed(t, i, z)))
             t += 1
 
     def _batch(self, t, i, z, k=0):
@@ -247,6 +261,11 @@ class RoundWorkload:
         for i in range(cfg.m):
             k = i % self.nstreams
             with torch.cuda.stream(self.streams[k]):
+                if self.use_graphs:
+                    gr = self.graph_runners[k]
+                    for z in range(zeta):
+                        self.pipes[k].take(lambda slot: gr.step(slot, m.params[i], self.lr))
+                    continue
                 for z in range(zeta):
                     b = self._batch(t, i, z, k)
                     opt = None
@@ -287,7 +306,9 @@ class RoundWorkload:
                                  c.batch_clusters or c.n_nodes), "zeta": self.zeta,
                 "batching": "m sub-GCNs on one shared mini-batch (batched layers)" if self.shared
                             else "one mini-batch per sub-GCN",
-                "optimizer": f"adam ({self.adam} moments)" if self.adam else "sgd"}
+                "optimizer": f"adam ({self.adam} moments)" if self.adam else "sgd",
+                "launch": "each sub-GCN step replayed from a HIP graph" if self.graphs
+                          else "kernels launched one by one"}
 
     # ---- CPU baseline: the fp64 oracle on one sub-GCN step ---------------------
     def cpu_baseline(self):
@@ -449,14 +470,17 @@ def main():
         wl = LayerWorkload(cfg, ctx, args.dtype, args.d_in)
     else:
         wl = RoundWorkload(cfg, ctx, args.dtype, args.optimizer, args.adam_policy, args.zeta,
-                           args.shared_batch, args.streams)
+                           args.shared_batch, args.streams, args.graphs)
         wl.lr = args.lr
     ctxs = getattr(wl, "ctxs", [ctx])
     for w in range(args.warmup):
         wl.step()
         torch.cuda.synchronize()
         log(f"[bench] warmup {w + 1}/{args.warmup} done")
-    if not args.no_profile:
+    # graph replays carry no per-kernel events: their kernels are profiled in
+    # an eager pass of the same steps after the timed region
+    profile_timed = not args.no_profile and not args.graphs
+    if profile_timed:
         for c in ctxs:
             G.gist_profile_begin(c, 1 << 16)
     torch.cuda.synchronize()
@@ -472,6 +496,14 @@ def main():
     log(f"[bench] timed {args.steps} steps")
     ms_step = (t1 - t0) * 1e3 / args.steps
     prof, dropped = ({}, 0)
+    if args.graphs and not args.no_profile:
+        wl.use_graphs = False
+        for c in ctxs:
+            G.gist_profile_begin(c, 1 << 16)
+        for s in range(args.steps):
+            wl.step()
+        torch.cuda.synchronize()
+        log(f"[bench] profiled {args.steps} eager steps")
     if not args.no_profile:
         for c in ctxs:   # every stream's launches (their event times may overlap)
             p, d = G.gist_profile_read(c)
@@ -540,6 +572,8 @@ def main():
                        else "ms per layer fwd+bwd"),
         "roofline": roofline, "cpu_baseline": cpu, "kernels": kernels,
         "host_batch_wait_ms_per_step": round(host_wait_ms, 3),
+        "kernels_from": ("an eager pass of the same number of steps after the timed graph "
+                         "replays" if args.graphs else "the timed steps"),
         "profile_dropped": dropped, "kernel_src_sha256": kernel_source_hash(),
     }
     print(json.dumps(out), flush=True)

@@ -14,7 +14,9 @@
 // touch are visited: the distribution is kept compact (touched columns in
 // ascending order, read off a bitmap of the graph's nodes), which gives the
 // same prefix sums as the full vector, since the untouched columns add
-// exact zeros.
+// exact zeros.  Membership in V_l is a second bitmap (a few tens of KB, so
+// it stays in cache): the pass that builds the rows reads a node's
+// importance and position only for the few entries that are kept.
 
 #include <algorithm>
 #include <cmath>
@@ -26,33 +28,28 @@
 
 namespace {
 
-// Per-node state, one record per graph node so that a visit of node j
-// touches one cache line: its importance q (zero outside the current layer's
-// touched columns) and its position in V_l, valid when `stamp` is current.
-struct NodeState {
-  double q;
-  int32_t pos;
-  uint32_t stamp;
-};
+inline void set_bit(std::vector<uint64_t>& b, int32_t j) {
+  b[static_cast<size_t>(j) >> 6] |= 1ull << (j & 63);
+}
+inline bool get_bit(const std::vector<uint64_t>& b, int32_t j) {
+  return (b[static_cast<size_t>(j) >> 6] >> (j & 63)) & 1ull;
+}
 
-// Per-thread scratch, sized to the graph once.
+// Per-thread scratch, sized to the graph once.  Between calls q is zero and
+// both bitmaps are clear.
 struct Scratch {
-  std::vector<NodeState> node;
-  uint32_t cur = 0;
-  std::vector<uint64_t> seen;    // bitmap of the columns touched by the current layer
+  std::vector<double> q;         // importance per node (non-zero: touched this layer)
+  std::vector<int32_t> pos;      // position in V_l, valid where `member` is set
+  std::vector<uint64_t> seen;    // columns touched by the current layer's rows
+  std::vector<uint64_t> member;  // V_l
   std::vector<int32_t> touched;  // columns with q > 0, ascending
-  std::vector<double> prefix;
+  std::vector<double> prefix;    // running sums of q over `touched`
   void resize(int64_t n) {
-    if (static_cast<int64_t>(node.size()) != n) {
-      node.assign(static_cast<size_t>(n), NodeState{0.0, 0, 0u});
+    if (static_cast<int64_t>(q.size()) != n) {
+      q.assign(static_cast<size_t>(n), 0.0);
+      pos.assign(static_cast<size_t>(n), 0);
       seen.assign(static_cast<size_t>((n + 63) / 64), 0ull);
-      cur = 0;
-    }
-  }
-  void next_stamp() {
-    if (++cur == 0) {
-      for (NodeState& x : node) x.stamp = 0u;
-      cur = 1;
+      member.assign(static_cast<size_t>((n + 63) / 64), 0ull);
     }
   }
 };
@@ -105,18 +102,30 @@ extern "C" gist_status gist_ladies_sample(const gist_csr* A, const int32_t* batc
       Y.t_rowptr.assign(1, 0);
       continue;
     }
-    // importance of every column the rows V_{l+1} touch, rows in ascending order
-    for (int32_t i : V) {
-      for (int32_t e = rp[i]; e < rp[i + 1]; ++e) {
+    // importance of every column the rows V_{l+1} touch, rows in ascending
+    // order; the next rows' entries and the importance slots a row is about
+    // to update are prefetched (the rows lie anywhere in the graph)
+    for (size_t r = 0; r < V.size(); ++r) {
+      if (r + 2 < V.size()) {
+        __builtin_prefetch(ac + rp[V[r + 2]]);
+        __builtin_prefetch(av + rp[V[r + 2]]);
+      }
+      const int32_t i = V[r];
+      const int32_t e0 = rp[i], e1 = rp[i + 1];
+      for (int32_t e = e0; e < e1 && e < e0 + 8; ++e) __builtin_prefetch(&S.q[ac[e]], 1);
+      for (int32_t e = e0; e < e1; ++e) {
+        if (e + 8 < e1) __builtin_prefetch(&S.q[ac[e + 8]], 1);
         const int32_t j = ac[e];
         const double a = static_cast<double>(av[e]);
-        S.node[j].q += a * a;
-        S.seen[static_cast<size_t>(j) >> 6] |= 1ull << (j & 63);
+        S.q[j] += a * a;
+        set_bit(S.seen, j);
       }
     }
-    // touched columns in ascending order (clearing the bitmap); a column whose
-    // entries were all zero keeps q = 0 and is never drawn
+    // touched columns in ascending order with their running sums (clearing the
+    // bitmap); a column whose entries were all zero keeps q = 0, never drawn
     S.touched.clear();
+    S.prefix.clear();
+    double run = 0.0;
     for (size_t w = 0; w < S.seen.size(); ++w) {
       uint64_t x = S.seen[w];
       if (!x) continue;
@@ -124,18 +133,17 @@ extern "C" gist_status gist_ladies_sample(const gist_csr* A, const int32_t* batc
       while (x) {
         const int32_t j = static_cast<int32_t>(w * 64 + static_cast<size_t>(__builtin_ctzll(x)));
         x &= x - 1;
-        if (S.node[j].q > 0.0) S.touched.push_back(j);
+        const double qj = S.q[j];
+        if (qj > 0.0) {
+          S.touched.push_back(j);
+          run += qj;
+          S.prefix.push_back(run);
+        }
       }
-    }
-    S.prefix.resize(S.touched.size());
-    double run = 0.0;
-    for (size_t k = 0; k < S.touched.size(); ++k) {
-      run += S.node[S.touched[k]].q;
-      S.prefix[k] = run;
     }
     const double Q = run;
     draws.clear();
-    if (s > 0 && S.touched.empty())   // every q is zero (and the bitmap clear)
+    if (s > 0 && S.touched.empty())   // every q is zero (and the bitmaps clear)
       return set_error(GIST_E_INVAL, "gist_ladies_sample: no node has positive importance");
     if (s > 0) {
       for (int32_t k = 0; k < s; ++k) {
@@ -152,24 +160,27 @@ extern "C" gist_status gist_ladies_sample(const gist_csr* A, const int32_t* batc
     draws.erase(std::unique(draws.begin(), draws.end()), draws.end());
     Y.nodes.clear();
     std::set_union(draws.begin(), draws.end(), V.begin(), V.end(), std::back_inserter(Y.nodes));
-    S.next_stamp();
     for (size_t k = 0; k < Y.nodes.size(); ++k) {
-      S.node[Y.nodes[k]].pos = static_cast<int32_t>(k);
-      S.node[Y.nodes[k]].stamp = S.cur;
+      S.pos[Y.nodes[k]] = static_cast<int32_t>(k);
+      set_bit(S.member, Y.nodes[k]);
     }
     // rows: A_ij / (s p_j) over the kept columns, normalised by the row sum
     Y.col.clear();
     Y.val.clear();
     std::vector<double> w;
     for (int64_t r = 0; r < n_out; ++r) {
+      if (r + 2 < n_out) {
+        __builtin_prefetch(ac + rp[V[static_cast<size_t>(r) + 2]]);
+        __builtin_prefetch(av + rp[V[static_cast<size_t>(r) + 2]]);
+      }
       const int32_t i = V[static_cast<size_t>(r)];
       w.clear();
       for (int32_t e = rp[i]; e < rp[i + 1]; ++e) {
-        const NodeState& x = S.node[ac[e]];
-        if (x.stamp != S.cur) continue;
-        const double p = x.q / Q;
+        const int32_t j = ac[e];
+        if (!get_bit(S.member, j)) continue;
+        const double p = S.q[j] / Q;
         w.push_back(static_cast<double>(av[e]) / (s_eff * p));
-        Y.col.push_back(x.pos);
+        Y.col.push_back(S.pos[j]);
       }
       double sum = 0.0;
       for (double x : w) sum += x;
@@ -192,7 +203,8 @@ extern "C" gist_status gist_ladies_sample(const gist_csr* A, const int32_t* batc
         Y.t_val[d] = Y.val[e];
       }
     }
-    for (int32_t j : S.touched) S.node[j].q = 0.0;   // leave the scratch zeroed
+    for (int32_t j : S.touched) S.q[j] = 0.0;   // leave the scratch zeroed
+    for (int32_t j : Y.nodes) S.member[static_cast<size_t>(j) >> 6] = 0;
     V = Y.nodes;
   }
 

@@ -163,12 +163,15 @@ class BatchPipeline:
 
     @classmethod
     def ladies(cls, ctx, L, b, s, max_degree, d_in, A_handle, X_dev, labels_host, items,
-               depth=8, workers=4):
-        """A pipeline of LADIES mini-batches; ``items`` yields (output nodes, seed)."""
-        slots = [LadiesSlot(ctx, L, b, s, max_degree, d_in) for _ in range(depth)]
+               depth=8, workers=4, fixed=False):
+        """A pipeline of LADIES mini-batches; ``items`` yields (output nodes,
+        seed), or a callable returning them (evaluated on the worker thread)."""
+        slots = [LadiesSlot(ctx, L, b, s, max_degree, d_in, fixed=fixed) for _ in range(depth)]
+        def build(slot, item):
+            nodes, seed = item() if callable(item) else item
+            slot.build(A_handle, nodes, seed, labels_host)
         return cls(ctx, None, 0, 0, d_in, None, X_dev, labels_host, items, workers=workers,
-                   slots=slots,
-                   build=lambda slot, item: slot.build(A_handle, item[0], item[1], labels_host))
+                   slots=slots, build=build)
 
     def _submit(self):
         try:
@@ -179,7 +182,10 @@ class BatchPipeline:
         self.pending.append((slot, self.pool.submit(self._build, slot, item)))
         self.k += 1
 
-    def next(self):
+    def take(self, use):
+        """Hand the next built slot to ``use(slot)``, which must enqueue every
+        read of the slot's host buffers (and record ``slot.uploaded``) before
+        it returns; the slot is then refilled with a later batch."""
         slot, fut = self.pending.popleft()
         if not fut.done():           # the host build is behind: time spent waiting for it
             import time
@@ -187,9 +193,13 @@ class BatchPipeline:
             fut.result()
             self.wait_s += time.perf_counter() - t0
         fut.result()
-        view = slot.upload(self.X)
+        out = use(slot)
         self._submit()       # reuses this slot: its build waits for the upload just enqueued
-        return view
+        return out
+
+    def next(self):
+        """The next batch, uploaded on the current stream."""
+        return self.take(lambda slot: slot.upload(self.X))
 
     def close(self):
         for _, fut in self.pending:
@@ -219,19 +229,29 @@ class LadiesSlot:
     ``build`` runs ``gist_ladies_sample`` on the host into pinned per-layer
     staging arrays sized by the capacities, then packs what it produced
     (every layer's node list, row pointers, entries and transpose, and the
-    output nodes' labels) into one contiguous pinned buffer; ``upload``
+    output nodes' labels) into one pinned transfer buffer; ``upload``
     enqueues that buffer as a single copy on the current stream and gathers
     the input layer's feature rows (V_0) on the device.  Capacities follow
     from the batch size b and the draws s per layer: |V_l| <= b + (L - l) s,
     and a layer's entries are at most its rows times (largest degree + 1).
+
+    With ``fixed=True`` the transfer buffer has a fixed layout at the
+    capacities (see :meth:`fixed_layout`), every node set padded to its
+    capacity: padded rows are empty (their row pointers repeat the last
+    one), padded input nodes are node 0.  The layer shapes are then the
+    same for every batch, which :class:`LadiesGraphRunner` relies on; the
+    results are those of the unpadded batch, since empty rows aggregate to
+    zero and contribute nothing to any gradient.
     """
 
     _ORDER = ("nodes", "rowptr", "t_rowptr", "col", "t_col", "val", "t_val")
     _ALIGN = 64      # elements (256 bytes) between packed arrays
 
-    def __init__(self, ctx, L, b, s, max_degree, d_in, device="cuda"):
+    def __init__(self, ctx, L, b, s, max_degree, d_in, device="cuda", fixed=False,
+                 fixed_nnz_per_row=16):
         self.ctx, self.L, self.b, self.s = ctx, L, int(b), int(s)
         self.device = device
+        self.fixed = fixed
         pin = dict(pin_memory=True)
         i32, f32 = torch.int32, torch.float32
         self.caps = []
@@ -256,9 +276,21 @@ class LadiesSlot:
                 setattr(a, k, v.data_ptr())
                 total += self._pad(v.numel())
         total += self._pad(self.b)          # labels
-        # packed transfer buffer: 4-byte elements (int32, float32 viewed as int32)
+        if fixed:
+            self.layout = self.fixed_layout(L, b, s, fixed_nnz_per_row)
+            total = max(total, self.layout["total"])
+        # transfer buffer: 4-byte elements (int32, float32 viewed as int32)
         self.packed_h = torch.empty(total, dtype=i32, **pin)
         self.packed_d = torch.empty(total, dtype=i32, device=device)
+        if fixed:
+            # the sampler writes straight into the fixed layout's sections
+            self.arr_fixed = (G.gist_ladies_layer * L)()
+            base = self.packed_h.data_ptr()
+            for l, fl in enumerate(self.layout["layers"]):
+                a = self.arr_fixed[l]
+                a.cap_n, a.cap_nnz = fl["n_in"], fl["nnz"]
+                for k in self._ORDER:
+                    setattr(a, k, base + 4 * fl["off"][k])
         self.X = torch.empty(self.caps[0][0], d_in, device=device)
         self.d_in = d_in
         self.uploaded = None
@@ -268,16 +300,61 @@ class LadiesSlot:
     def _pad(cls, n):
         return (int(n) + cls._ALIGN - 1) // cls._ALIGN * cls._ALIGN
 
+    @classmethod
+    def fixed_layout(cls, L, b, s, nnz_per_row):
+        """Offsets of the fixed transfer layout: per layer l the padded sizes
+        (rows |V_{l+1}| cap, input nodes |V_l| cap, entries cap) and each
+        array's offset, then the labels; ``total`` elements in all.  Both row
+        pointer arrays hold |V_l| cap + 1 entries, the sampler's capacity
+        contract."""
+        off, layers = 0, []
+        for l in range(L):
+            n_in = b + (L - l) * s
+            n_out = b + (L - l - 1) * s
+            nnz = n_out * int(nnz_per_row)
+            cnt = dict(nodes=n_in, rowptr=n_in + 1, t_rowptr=n_in + 1, col=nnz, t_col=nnz,
+                       val=nnz, t_val=nnz)
+            o = {}
+            for k in cls._ORDER:
+                o[k] = off
+                off += cls._pad(cnt[k])
+            layers.append(dict(n_out=n_out, n_in=n_in, nnz=nnz, off=o))
+        lab = off
+        off += cls._pad(b)
+        return dict(layers=layers, labels=lab, total=off)
+
     def build(self, A_handle, batch, seed, labels_host):
         """Host half: sample the layers, pack them and the output nodes' labels."""
         if self.uploaded is not None:
             self.uploaded.synchronize()     # the previous upload from packed_h is done
         batch = np.asarray(batch, dtype=np.int32)
         nb = batch.shape[0]
-        if nb > self.b:
-            raise ValueError("batch larger than the slot's capacity")
-        G.ladies_sample_into(A_handle, batch, self.L, self.s, seed, self.arr)
+        if nb > self.b or (self.fixed and nb != self.b):
+            raise ValueError("batch size does not match the slot")
         packed = self.packed_h.numpy()
+        if self.fixed:
+            try:
+                G.ladies_sample_into(A_handle, batch, self.L, self.s, seed, self.arr_fixed)
+            except G.GistError as e:   # more entries than the fixed layout holds
+                if e.status != G.GIST_E_NOMEM:
+                    raise
+            else:
+                sizes, offs = [], []
+                for l, fl in enumerate(self.layout["layers"]):
+                    a = self.arr_fixed[l]
+                    n_out, n_in, nnz = int(a.n_out), int(a.n_in), int(a.nnz)
+                    o = fl["off"]    # pad to the fixed shapes: empty rows, node 0
+                    packed[o["rowptr"] + n_out + 1:o["rowptr"] + fl["n_out"] + 1] = nnz
+                    packed[o["t_rowptr"] + n_in + 1:o["t_rowptr"] + fl["n_in"] + 1] = nnz
+                    packed[o["nodes"] + n_in:o["nodes"] + fl["n_in"]] = 0
+                    offs.append(o)
+                    sizes.append((n_out, n_in, nnz))
+                lab = self.layout["labels"]
+                packed[lab:lab + nb] = labels_host[batch]
+                self.built = (nb, sizes, offs, lab, self.layout["total"], True)
+                return
+        # compact layout: sample into the staging arrays, pack what was produced
+        G.ladies_sample_into(A_handle, batch, self.L, self.s, seed, self.arr)
         off, offs, sizes = 0, [], []
         for l in range(self.L):
             a = self.arr[l]
@@ -286,26 +363,31 @@ class LadiesSlot:
             o = {}
             for k in self._ORDER:
                 c = cnt.get(k, nnz)
-                src = self.h[l][k].numpy()[:c]
-                packed[off:off + c] = src.view(np.int32)
                 o[k] = off
                 off += self._pad(c)
+                packed[o[k]:o[k] + c] = self.h[l][k].numpy()[:c].view(np.int32)
             offs.append(o)
             sizes.append((n_out, n_in, nnz))
         packed[off:off + nb] = labels_host[batch]
-        lab = off
-        off += self._pad(nb)
-        self.built = (nb, sizes, offs, lab, off)
+        self.built = (nb, sizes, offs, off, off + self._pad(nb), False)
+
+    def fits_fixed(self):
+        """Whether the last built batch is in the fixed layout (else it is
+        packed compactly: its entries exceeded the fixed capacity)."""
+        return self.built[5]
+
+    def mark_uploaded(self):
+        ev = torch.cuda.Event()
+        ev.record()
+        self.uploaded = ev
 
     def upload(self, X_dev):
         """Device half: one asynchronous copy on the current stream and the
         gather of the input nodes' features."""
-        nb, sizes, offs, lab, total = self.built
+        nb, sizes, offs, lab, total, fits = self.built
         d = self.packed_d
         d[:total].copy_(self.packed_h[:total], non_blocking=True)
-        ev = torch.cuda.Event()
-        ev.record()
-        self.uploaded = ev
+        self.mark_uploaded()
         f32 = torch.float32
         views = []
         for l, (n_out, n_in, nnz) in enumerate(sizes):
@@ -324,6 +406,86 @@ class LadiesSlot:
     def load(self, A_handle, batch, seed, X_dev, labels_host):
         self.build(A_handle, batch, seed, labels_host)
         return self.upload(X_dev)
+
+
+class LadiesGraphRunner:
+    """Sub-GCN steps on LADIES mini-batches replayed from HIP graphs.
+
+    A LADIES step is a few dozen small launches (c7: GEMMs of at most
+    1536 x 602 x 64), so issuing them one by one costs more host time than
+    they take on the device.  Here each step is captured once into a graph
+    (torch's CUDAGraph over the library's launches) at the fixed shapes of
+    ``LadiesSlot(fixed=True)`` and replayed: per step the host enqueues one
+    copy of the batch into this runner's device buffer and one graph launch.
+    The graph holds the feature gather, every layer's forward, the loss,
+    every layer's backward and the SGD update.  A graph is kept per
+    parameter set (the sub-GCN's slice buffers) and learning rate.
+    """
+
+    def __init__(self, ctx, widths, L, b, s, d_in, X_dev, dtype=G.GIST_DTYPE_F32,
+                 fixed_nnz_per_row=16, device="cuda"):
+        self.ctx, self.L, self.d_in, self.X_dev = ctx, L, d_in, X_dev
+        self.layout = LadiesSlot.fixed_layout(L, b, s, fixed_nnz_per_row)
+        self.dev = torch.empty(self.layout["total"], dtype=torch.int32, device=device)
+        lay = self.layout["layers"]
+        sizes = [(fl["n_out"], fl["n_in"], fl["nnz"]) for fl in lay]
+        views = []
+        for fl in lay:
+            o = fl["off"]
+            v = {k: self.dev[o[k]:] for k in ("nodes", "rowptr", "t_rowptr", "col", "t_col")}
+            v["val"] = self.dev[o["val"]:o["val"] + fl["nnz"]].view(torch.float32)
+            v["t_val"] = self.dev[o["t_val"]:o["t_val"] + fl["nnz"]].view(torch.float32)
+            views.append(v)
+        self.n0 = lay[0]["n_in"]
+        self.X = torch.empty(self.n0, d_in, device=device)
+        lab = self.layout["labels"]
+        self.view = LadiesView(sizes, views, self.X, self.dev[lab:lab + b])
+        self.nodes0 = views[0]["nodes"]
+        self.run = SubGCN(ctx, "gcn", widths, self.n0, dtype=dtype, device=device)
+        self.run._workspace(self.view)      # sized before any capture
+        self.graphs = {}
+
+    def _body(self, params, lr):
+        G.gist_gather_slice(self.ctx, self.X_dev, self.d_in, self.nodes0, self.n0, None,
+                            self.d_in, self.X, self.d_in)
+        self.run.forward(self.view, params)
+        self.run.loss_and_grad(self.view)
+        self.run.backward(self.view, params)
+        self.run.sgd(params, lr)
+
+    def _capture(self, params, lr):
+        cur = torch.cuda.current_stream()
+        side = torch.cuda.Stream()
+        side.wait_stream(cur)
+        g = torch.cuda.CUDAGraph()
+        self.ctx.set_stream(side.cuda_stream)
+        try:
+            with torch.cuda.graph(g, stream=side, capture_error_mode="thread_local"):
+                self._body(params, lr)
+        finally:
+            self.ctx.set_stream(cur.cuda_stream)
+        cur.wait_stream(side)
+        return g
+
+    def step(self, slot, params, lr):
+        """One sub-GCN step on the batch built in ``slot`` (fixed layout): the
+        batch is copied into this runner's buffer, then the step's graph is
+        replayed (captured on first use of these parameters)."""
+        if not slot.fits_fixed():    # rare: too many entries for the graph's layout
+            self.run.step(slot.upload(self.X_dev), params, lr)
+            return
+        total = self.layout["total"]
+        self.dev.copy_(slot.packed_h[:total], non_blocking=True)
+        slot.mark_uploaded()
+        key = (tuple(p.data_ptr() for p in params), float(lr))
+        g = self.graphs.get(key)
+        if g is None:
+            g = self.graphs[key] = self._capture(params, lr)
+        g.replay()
+
+    @property
+    def loss(self):
+        return self.run.loss
 
 
 class LadiesView:

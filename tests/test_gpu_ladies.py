@@ -321,3 +321,72 @@ def test_gist_train_on_ladies_batches(G, ctx, policy, size):
         assert e <= FP32_TOL and d <= 1e-3
     want_l = np.array([[li for li in lt] for lt in lo])
     assert np.max(np.abs(losses - want_l) / np.abs(want_l)) <= FP32_TOL
+
+
+def test_graph_runner_replays_match_eager_and_oracle(G, ctx):
+    """Sub-GCN steps replayed from HIP graphs (fixed, padded shapes) against
+    eager steps on the same batches and against the oracle's chained SGD
+    steps; two parameter sets alternate (two graphs), and eager library work
+    and synchronisations run between the replays."""
+    import torch
+    from paper_2102_10424_amd.step import LadiesGraphRunner, LadiesSlot, SubGCN
+    widths = (50, 96, 64, 12)
+    w = _Workload(4000, 40, widths, 64, 256, seed=9)
+    L, lr = w.L, 0.05
+    Ah, Xd = G.CsrHandle(w.A), to_dev(w.X)
+    fixed = LadiesSlot(ctx, L, w.b, w.s, w.max_degree, widths[0], fixed=True)
+    plain = LadiesSlot(ctx, L, w.b, w.s, w.max_degree, widths[0])
+    gr = LadiesGraphRunner(ctx, widths, L, w.b, w.s, widths[0], Xd)
+    eager = SubGCN(ctx, "gcn", widths, 1)
+    sets = 2
+    pg = [[to_dev(t.copy()) for t in w.theta] for _ in range(sets)]
+    pe = [[to_dev(t.copy()) for t in w.theta] for _ in range(sets)]
+    po = [[t.astype(np.float64) for t in w.theta] for _ in range(sets)]
+    for k in range(6):
+        j = k % sets
+        key = 500 + k
+        log(f"graph replay {k}: parameter set {j}")
+        fixed.build(Ah, w.batch_nodes(key), key, w.y)
+        assert fixed.fits_fixed()
+        gr.step(fixed, pg[j], lr)
+        b = plain.load(Ah, w.batch_nodes(key), key, Xd, w.y)
+        eager.step(b, pe[j], lr)
+        torch.cuda.synchronize()
+        layers, Xo, yo = w.oracle_batch(key)
+        po[j] = OG.sub_gcn_step("gcn", layers, Xo, yo, po[j], lr)["params"]
+        for l in range(L):
+            g_, e_ = to_host(pg[j][l]), to_host(pe[j][l])
+            assert relerr(g_, e_) <= 1e-5, (k, l)
+            assert relerr(g_, po[j][l]) <= FP32_TOL, (k, l)
+        assert abs(float(to_host(gr.loss)[0]) - float(to_host(eager.loss)[0])) <= 1e-5
+    assert len(gr.graphs) == sets
+    # an eager step through the fixed layout's own upload agrees as well
+    fixed.build(Ah, w.batch_nodes(900), 900, w.y)
+    b = fixed.upload(Xd)
+    assert [b.rows(l) for l in range(L + 1)] == [plain.load(Ah, w.batch_nodes(900), 900, Xd,
+                                                            w.y).rows(l) for l in range(L + 1)]
+
+
+def test_graph_runner_falls_back_when_the_layout_is_full(G, ctx):
+    """A batch with more entries than the fixed layout holds is packed
+    compactly and stepped eagerly by the runner, with the same result."""
+    import torch
+    from paper_2102_10424_amd.step import LadiesGraphRunner, LadiesSlot, SubGCN
+    widths = (30, 40, 7)
+    w = _Workload(3000, 30, widths, 32, 128, seed=12)
+    Ah, Xd = G.CsrHandle(w.A), to_dev(w.X)
+    slot = LadiesSlot(ctx, w.L, w.b, w.s, w.max_degree, widths[0], fixed=True,
+                      fixed_nnz_per_row=1)
+    gr = LadiesGraphRunner(ctx, widths, w.L, w.b, w.s, widths[0], Xd, fixed_nnz_per_row=1)
+    eager = SubGCN(ctx, "gcn", widths, 1)
+    pg = [to_dev(t.copy()) for t in w.theta]
+    pe = [to_dev(t.copy()) for t in w.theta]
+    plain = LadiesSlot(ctx, w.L, w.b, w.s, w.max_degree, widths[0])
+    slot.build(Ah, w.batch_nodes(3), 3, w.y)
+    assert not slot.fits_fixed()
+    gr.step(slot, pg, 0.05)
+    eager.step(plain.load(Ah, w.batch_nodes(3), 3, Xd, w.y), pe, 0.05)
+    torch.cuda.synchronize()
+    for a, b in zip(pg, pe):
+        assert torch.equal(a, b)
+    assert not gr.graphs
