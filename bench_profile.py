@@ -112,7 +112,7 @@ def main():
     for k in ("bench", "trace", "fetch", "write", "calib_fetch", "calib_write", "title", "out"):
         ap.add_argument("--" + k.replace("_", "-"), required=True)
     ap.add_argument("--cmd", action="append", default=[])
-    ap.add_argument("--workload", required=True, help="config name the run used (c1..c6)")
+    ap.add_argument("--workload", required=True, help="config name the run used (c1..c7)")
     a = ap.parse_args()
     res = json.load(open(a.bench))
     steps = res["steps"]

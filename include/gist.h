@@ -20,6 +20,7 @@
  *   gist_subagg                subAgg: Theta[D_in, D_out] <- Theta^(i)  (device)
  *   gist_subagg_gather         subAgg of one round + gather of the next (device)
  *   gist_subagg_mean           subAgg of an unsplit parameter: mean of copies (device)
+ *   gist_capture_* / replay_*  record library calls once, replay them      (device)
  *
  * Conventions
  *  - Every matrix is row-major fp32 with the leading dimension stated.
@@ -498,6 +499,49 @@ gist_status gist_profile_begin(gist_ctx* ctx, int64_t cap);
 gist_status gist_profile_read(gist_ctx* ctx, gist_prof_entry* out, int32_t out_cap,
                               int32_t* n, int64_t* dropped);
 gist_status gist_profile_end(gist_ctx* ctx);
+
+/* ---- replays: HIP graphs of library calls -------------------------- */
+
+/* A step of many small launches (a sub-GCN step on a LADIES mini-batch) can
+ * cost more host time to issue than device time to run.  These calls record
+ * a sequence of library calls once and replay it with one launch.
+ *
+ * gist_capture_begin starts capturing the calls made on `ctx` from this
+ * thread (hipStreamBeginCapture, thread-local mode): they are recorded, not
+ * run.  The context's stream must not be the default stream, and the
+ * context must not be recording a profile.  Only device calls with fixed
+ * shapes and buffers belong in a capture: a replay repeats the recorded
+ * launches with the recorded arguments, so the buffers must outlive it and
+ * their contents (not their sizes) are what changes between replays.
+ * gist_capture_end ends the capture and instantiates the replay (caller
+ * owns it; gist_replay_destroy frees it).  Errors: GIST_E_INVAL, and
+ * GIST_E_DEVICE if the runtime rejected the capture (a failed call inside
+ * it ends the capture too; the caller must still call gist_capture_end).
+ *
+ * gist_replay_launch enqueues on the stream of `ctx` (any context on the
+ * same device): first a copy of `bytes` from `src` to device `dst` (skipped
+ * when bytes == 0), made by a kernel that reads `src` directly, so src must
+ * be device memory or pinned host memory (hipHostMalloc; torch's
+ * pin_memory), then a record of `copied` (may be NULL: after it, src may be
+ * reused), then the replay.  All asynchronous. */
+typedef struct gist_replay gist_replay;
+typedef struct gist_event gist_event;
+gist_status gist_capture_begin(gist_ctx* ctx);
+gist_status gist_capture_end(gist_ctx* ctx, gist_replay** out);
+gist_status gist_replay_launch(gist_ctx* ctx, gist_replay* r, void* dst, const void* src,
+                               size_t bytes, gist_event* copied);
+gist_status gist_replay_destroy(gist_replay* r);
+/* The copy of gist_replay_launch on its own: `bytes` from `src` (device or
+ * pinned host memory) to device `dst` by a kernel on the stream of `ctx`,
+ * then a record of `copied` (may be NULL).  Small uploads made this way
+ * stay on the compute queue (no copy-engine hand-off). */
+gist_status gist_copy(gist_ctx* ctx, void* dst, const void* src, size_t bytes,
+                      gist_event* copied);
+/* A device event (no timing) for gist_replay_launch: create, wait for its
+ * last record on the host, destroy. */
+gist_status gist_event_create(gist_event** out);
+gist_status gist_event_synchronize(gist_event* e);
+gist_status gist_event_destroy(gist_event* e);
 
 #ifdef __cplusplus
 }

@@ -833,3 +833,139 @@ extern "C" gist_status gist_profile_end(gist_ctx* ctx) {
   ctx->prof = nullptr;
   return GIST_OK;
 }
+
+// ---------------------------------------------------------------------------
+// Replays: HIP graphs of library calls, and events
+// ---------------------------------------------------------------------------
+
+struct gist_replay {
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t exec = nullptr;
+};
+
+struct gist_event {
+  hipEvent_t ev = nullptr;
+};
+
+namespace {
+gist_status hip_fail(const char* what, hipError_t e) {
+  (void)hipGetLastError();   // clear the runtime's record of it
+  return set_error(GIST_E_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+}  // namespace
+
+extern "C" gist_status gist_capture_begin(gist_ctx* ctx) {
+  gist::clear_error();
+  if (!ctx) return set_error(GIST_E_INVAL, "capture_begin: NULL ctx");
+  if (!ctx->stream)
+    return set_error(GIST_E_INVAL, "capture_begin: the context's stream is the default stream");
+  if (ctx->prof)
+    return set_error(GIST_E_INVAL, "capture_begin: the context is recording a profile");
+  gist::DeviceGuard dg(ctx->device);
+  hipError_t e = hipStreamBeginCapture(ctx->stream, hipStreamCaptureModeThreadLocal);
+  if (e != hipSuccess) return hip_fail("capture_begin", e);
+  return GIST_OK;
+}
+
+extern "C" gist_status gist_capture_end(gist_ctx* ctx, gist_replay** out) {
+  gist::clear_error();
+  if (!ctx || !out) return set_error(GIST_E_INVAL, "capture_end: NULL argument");
+  *out = nullptr;
+  gist::DeviceGuard dg(ctx->device);
+  hipGraph_t g = nullptr;
+  if (hipStreamEndCapture(ctx->stream, &g) != hipSuccess || !g) {
+    if (g) (void)hipGraphDestroy(g);
+    (void)hipGetLastError();
+    return set_error(GIST_E_DEVICE, "capture_end: the capture failed (a call made during it "
+                                    "is not capturable, or the capture was invalidated)");
+  }
+  hipGraphExec_t e = nullptr;
+  const hipError_t ie = hipGraphInstantiate(&e, g, nullptr, nullptr, 0);
+  if (ie != hipSuccess) {
+    (void)hipGraphDestroy(g);
+    return hip_fail("capture_end (instantiate)", ie);
+  }
+  gist_replay* r = new (std::nothrow) gist_replay;
+  if (!r) {
+    (void)hipGraphExecDestroy(e);
+    (void)hipGraphDestroy(g);
+    return set_error(GIST_E_NOMEM, "capture_end: out of host memory");
+  }
+  r->graph = g;
+  r->exec = e;
+  *out = r;
+  return GIST_OK;
+}
+
+extern "C" gist_status gist_replay_launch(gist_ctx* ctx, gist_replay* r, void* dst,
+                                          const void* src, size_t bytes, gist_event* copied) {
+  gist::clear_error();
+  if (!ctx || !r) return set_error(GIST_E_INVAL, "replay_launch: NULL argument");
+  if (bytes && (!dst || !src)) return set_error(GIST_E_INVAL, "replay_launch: NULL copy buffer");
+  gist::DeviceGuard dg(ctx->device);
+  gist::ProfBind pb(ctx);
+  hipError_t e = hipSuccess;
+  // the copy is a kernel on the stream reading the pinned source over the
+  // host link: unlike a copy-engine transfer it needs no hand-off between
+  // engines before the replay starts
+  if (bytes) GIST_TRY(gist::pull_copy(ctx->stream, dst, src, static_cast<int64_t>(bytes)));
+  if (copied && (e = hipEventRecord(copied->ev, ctx->stream)) != hipSuccess)
+    return hip_fail("replay_launch (event)", e);
+  if ((e = hipGraphLaunch(r->exec, ctx->stream)) != hipSuccess)
+    return hip_fail("replay_launch", e);
+  return GIST_OK;
+}
+
+extern "C" gist_status gist_copy(gist_ctx* ctx, void* dst, const void* src, size_t bytes,
+                                 gist_event* copied) {
+  gist::clear_error();
+  if (!ctx) return set_error(GIST_E_INVAL, "copy: NULL ctx");
+  if (bytes && (!dst || !src)) return set_error(GIST_E_INVAL, "copy: NULL buffer");
+  gist::ProfBind pb(ctx);
+  gist::DeviceGuard dg(ctx->device);
+  if (bytes) GIST_TRY(gist::pull_copy(ctx->stream, dst, src, static_cast<int64_t>(bytes)));
+  if (copied) {
+    const hipError_t e = hipEventRecord(copied->ev, ctx->stream);
+    if (e != hipSuccess) return hip_fail("copy (event)", e);
+  }
+  return GIST_OK;
+}
+
+extern "C" gist_status gist_replay_destroy(gist_replay* r) {
+  gist::clear_error();
+  if (!r) return GIST_OK;
+  if (r->exec) (void)hipGraphExecDestroy(r->exec);
+  if (r->graph) (void)hipGraphDestroy(r->graph);
+  delete r;
+  return GIST_OK;
+}
+
+extern "C" gist_status gist_event_create(gist_event** out) {
+  gist::clear_error();
+  if (!out) return set_error(GIST_E_INVAL, "event_create: NULL out");
+  gist_event* e = new (std::nothrow) gist_event;
+  if (!e) return set_error(GIST_E_NOMEM, "event_create: out of host memory");
+  const hipError_t he = hipEventCreateWithFlags(&e->ev, hipEventDisableTiming);
+  if (he != hipSuccess) {
+    delete e;
+    return hip_fail("event_create", he);
+  }
+  *out = e;
+  return GIST_OK;
+}
+
+extern "C" gist_status gist_event_synchronize(gist_event* e) {
+  gist::clear_error();
+  if (!e) return set_error(GIST_E_INVAL, "event_synchronize: NULL event");
+  const hipError_t he = hipEventSynchronize(e->ev);
+  if (he != hipSuccess) return hip_fail("event_synchronize", he);
+  return GIST_OK;
+}
+
+extern "C" gist_status gist_event_destroy(gist_event* e) {
+  gist::clear_error();
+  if (!e) return GIST_OK;
+  if (e->ev) (void)hipEventDestroy(e->ev);
+  delete e;
+  return GIST_OK;
+}

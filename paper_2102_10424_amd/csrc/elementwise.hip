@@ -159,6 +159,27 @@ __global__ void zero_int_kernel(int* p) {
   if (threadIdx.x == 0 && blockIdx.x == 0) p[0] = 0;
 }
 
+// Copy of `n16` 16-byte words, then `tail` single bytes, from `src` (which
+// may be pinned host memory: the reads then cross the host link) to `dst`.
+__global__ __launch_bounds__(kBlock) void pull_kernel(uint4* __restrict__ dst,
+                                                      const uint4* __restrict__ src, int64_t n16,
+                                                      int64_t tail) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+  const int64_t t0 = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
+  for (int64_t i = t0; i < n16; i += stride) dst[i] = src[i];
+  if (t0 < tail)
+    reinterpret_cast<unsigned char*>(dst + n16)[t0] =
+        reinterpret_cast<const unsigned char*>(src + n16)[t0];
+}
+
+__global__ __launch_bounds__(kBlock) void pull_bytes_kernel(unsigned char* __restrict__ dst,
+                                                            const unsigned char* __restrict__ src,
+                                                            int64_t n) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+  for (int64_t i = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x; i < n; i += stride)
+    dst[i] = src[i];
+}
+
 __global__ __launch_bounds__(kBlock) void nonfinite_kernel(const float* __restrict__ Ws, int64_t lds,
                                                            int nr, int nc, int* flag) {
   const int64_t total = static_cast<int64_t>(nr) * nc;
@@ -541,6 +562,23 @@ gist_status fill_zero(hipStream_t st, float* p, int64_t count) {
   hipLaunchKernelGGL(zero_kernel, dim3(grid_for(count, kBlock, 8192)), dim3(kBlock), 0, st, p,
                      count);
   return check_launch("fill_zero");
+}
+
+gist_status pull_copy(hipStream_t st, void* dst, const void* src, int64_t bytes) {
+  if (bytes <= 0) return GIST_OK;
+  ProfScope ps(st, "pull_copy", 0.0, 2.0 * static_cast<double>(bytes));
+  const bool a16 = (reinterpret_cast<uintptr_t>(dst) % 16 == 0) &&
+                   (reinterpret_cast<uintptr_t>(src) % 16 == 0);
+  if (a16) {
+    const int64_t n16 = bytes / 16, tail = bytes % 16;
+    hipLaunchKernelGGL(pull_kernel, dim3(grid_for(n16 > 0 ? n16 : 1, kBlock, 2048)), dim3(kBlock),
+                       0, st, static_cast<uint4*>(dst), static_cast<const uint4*>(src), n16, tail);
+  } else {
+    hipLaunchKernelGGL(pull_bytes_kernel, dim3(grid_for(bytes, kBlock, 2048)), dim3(kBlock), 0, st,
+                       static_cast<unsigned char*>(dst), static_cast<const unsigned char*>(src),
+                       bytes);
+  }
+  return check_launch("pull_copy");
 }
 
 gist_status subagg_mean(hipStream_t st, float* Wg, int64_t rows, int64_t cols, int64_t ldg, int m,

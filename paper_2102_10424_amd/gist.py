@@ -62,6 +62,9 @@ EXPORTED = (
     "gist_sgd_update", "gist_adam_update", "gist_subagg", "gist_partition_inverse",
     "gist_subagg_gather", "gist_subagg_mean",
     "gist_profile_begin", "gist_profile_read", "gist_profile_end",
+    "gist_capture_begin", "gist_capture_end", "gist_replay_launch", "gist_replay_destroy",
+    "gist_copy",
+    "gist_event_create", "gist_event_synchronize", "gist_event_destroy",
 )
 
 
@@ -163,6 +166,14 @@ _sigs = {
     "gist_sgd_update": (C.c_int, [_P, _P, _P, C.c_int64, C.c_float]),
     "gist_subagg": (C.c_int, [_P, _P, C.c_int64, _P, C.c_int32, _P, C.c_int32, _P, C.c_int64,
                               C.c_uint32]),
+    "gist_capture_begin": (C.c_int, [_P]),
+    "gist_capture_end": (C.c_int, [_P, C.POINTER(_P)]),
+    "gist_replay_launch": (C.c_int, [_P, _P, _P, _P, C.c_size_t, _P]),
+    "gist_replay_destroy": (C.c_int, [_P]),
+    "gist_copy": (C.c_int, [_P, _P, _P, C.c_size_t, _P]),
+    "gist_event_create": (C.c_int, [C.POINTER(_P)]),
+    "gist_event_synchronize": (C.c_int, [_P]),
+    "gist_event_destroy": (C.c_int, [_P]),
 }
 for _name, (_res, _args) in _sigs.items():
     _f = getattr(_lib, _name)
@@ -478,6 +489,73 @@ def gist_subagg_mean(ctx, Wg, rows, cols, ldg, m, slice_ptrs, lds):
 def gist_subagg(ctx, Wg, ldg, rows, nr, cols, nc, Ws, lds, flags=0):
     _check(_lib.gist_subagg(ctx.handle, _ptr(Wg), int(ldg), _ptr(rows), int(nr), _ptr(cols),
                             int(nc), _ptr(Ws), int(lds), int(flags)))
+
+
+# ---- replays ---------------------------------------------------------------------
+class Replay:
+    """A captured sequence of library calls (``gist_capture_end``), freed with it."""
+
+    def __init__(self, handle):
+        self.handle = handle
+
+    def close(self):
+        if self.handle:
+            _lib.gist_replay_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Event:
+    """A ``gist_event``: recorded by ``gist_replay_launch``, waited on by ``synchronize``."""
+
+    def __init__(self):
+        h = _P()
+        _check(_lib.gist_event_create(C.byref(h)))
+        self.handle = h
+
+    def synchronize(self):
+        _check(_lib.gist_event_synchronize(self.handle))
+
+    def __del__(self):
+        try:
+            if self.handle:
+                _lib.gist_event_destroy(self.handle)
+                self.handle = None
+        except Exception:
+            pass
+
+
+def gist_capture_begin(ctx):
+    _check(_lib.gist_capture_begin(ctx.handle))
+
+
+def gist_capture_end(ctx):
+    h = _P()
+    _check(_lib.gist_capture_end(ctx.handle, C.byref(h)))
+    return Replay(h)
+
+
+def gist_replay_launch(ctx, replay, dst=None, src=None, nbytes=0, copied=None):
+    """Copy ``nbytes`` from host ``src`` to device ``dst`` (tensors or addresses), record
+    ``copied``, launch ``replay`` -- all on the stream of ``ctx``."""
+    d = dst if isinstance(dst, int) or dst is None else _ptr(dst)
+    s_ = src if isinstance(src, int) or src is None else _ptr(src)
+    _check(_lib.gist_replay_launch(ctx.handle, replay.handle, d, s_, int(nbytes),
+                                   copied.handle if copied is not None else None))
+
+
+def gist_copy(ctx, dst, src, nbytes, copied=None):
+    """``nbytes`` from ``src`` (device or pinned host) to device ``dst``, by a kernel on
+    the stream of ``ctx``; then record ``copied``."""
+    d = dst if isinstance(dst, int) else _ptr(dst)
+    s_ = src if isinstance(src, int) else _ptr(src)
+    _check(_lib.gist_copy(ctx.handle, d, s_, int(nbytes),
+                          copied.handle if copied is not None else None))
 
 
 # ---- instrumentation ------------------------------------------------------------

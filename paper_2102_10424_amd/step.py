@@ -293,6 +293,7 @@ class LadiesSlot:
                     setattr(a, k, base + 4 * fl["off"][k])
         self.X = torch.empty(self.caps[0][0], d_in, device=device)
         self.d_in = d_in
+        self.event = G.Event()      # recorded by gist_replay_launch after its copy
         self.uploaded = None
         self.built = None
 
@@ -413,18 +414,22 @@ class LadiesGraphRunner:
 
     A LADIES step is a few dozen small launches (c7: GEMMs of at most
     1536 x 602 x 64), so issuing them one by one costs more host time than
-    they take on the device.  Here each step is captured once into a graph
-    (torch's CUDAGraph over the library's launches) at the fixed shapes of
-    ``LadiesSlot(fixed=True)`` and replayed: per step the host enqueues one
-    copy of the batch into this runner's device buffer and one graph launch.
-    The graph holds the feature gather, every layer's forward, the loss,
-    every layer's backward and the SGD update.  A graph is kept per
-    parameter set (the sub-GCN's slice buffers) and learning rate.
+    they take on the device.  Here each step is recorded once
+    (``gist_capture_begin`` / ``_end`` on a context of its own, on a side
+    stream) at the fixed shapes of ``LadiesSlot(fixed=True)``: the feature
+    gather, every layer's forward, the loss, every layer's backward and the
+    SGD update.  Per step the host then makes one library call,
+    ``gist_replay_launch``: the copy of the batch into this runner's device
+    buffer, an event that frees the slot, and the replay, on the stream of
+    ``ctx``.  A replay is kept per parameter set (the sub-GCN's slice
+    buffers) and learning rate.
     """
 
     def __init__(self, ctx, widths, L, b, s, d_in, X_dev, dtype=G.GIST_DTYPE_F32,
                  fixed_nnz_per_row=16, device="cuda"):
         self.ctx, self.L, self.d_in, self.X_dev = ctx, L, d_in, X_dev
+        self.cap_stream = torch.cuda.Stream()
+        self.cap_ctx = G.Context(ctx.device, stream=self.cap_stream.cuda_stream)
         self.layout = LadiesSlot.fixed_layout(L, b, s, fixed_nnz_per_row)
         self.dev = torch.empty(self.layout["total"], dtype=torch.int32, device=device)
         lay = self.layout["layers"]
@@ -441,12 +446,13 @@ class LadiesGraphRunner:
         lab = self.layout["labels"]
         self.view = LadiesView(sizes, views, self.X, self.dev[lab:lab + b])
         self.nodes0 = views[0]["nodes"]
-        self.run = SubGCN(ctx, "gcn", widths, self.n0, dtype=dtype, device=device)
+        self.run = SubGCN(self.cap_ctx, "gcn", widths, self.n0, dtype=dtype, device=device)
         self.run._workspace(self.view)      # sized before any capture
-        self.graphs = {}
+        self.nbytes = 4 * self.layout["total"]
+        self.replays = {}
 
     def _body(self, params, lr):
-        G.gist_gather_slice(self.ctx, self.X_dev, self.d_in, self.nodes0, self.n0, None,
+        G.gist_gather_slice(self.cap_ctx, self.X_dev, self.d_in, self.nodes0, self.n0, None,
                             self.d_in, self.X, self.d_in)
         self.run.forward(self.view, params)
         self.run.loss_and_grad(self.view)
@@ -454,34 +460,36 @@ class LadiesGraphRunner:
         self.run.sgd(params, lr)
 
     def _capture(self, params, lr):
-        cur = torch.cuda.current_stream()
-        side = torch.cuda.Stream()
-        side.wait_stream(cur)
-        g = torch.cuda.CUDAGraph()
-        self.ctx.set_stream(side.cuda_stream)
+        # everything the capture reads was allocated and written before it
+        torch.cuda.synchronize()
+        G.gist_capture_begin(self.cap_ctx)
         try:
-            with torch.cuda.graph(g, stream=side, capture_error_mode="thread_local"):
-                self._body(params, lr)
+            self._body(params, lr)
         finally:
-            self.ctx.set_stream(cur.cuda_stream)
-        cur.wait_stream(side)
-        return g
+            replay = G.gist_capture_end(self.cap_ctx)
+        return replay
 
     def step(self, slot, params, lr):
-        """One sub-GCN step on the batch built in ``slot`` (fixed layout): the
-        batch is copied into this runner's buffer, then the step's graph is
-        replayed (captured on first use of these parameters)."""
-        if not slot.fits_fixed():    # rare: too many entries for the graph's layout
-            self.run.step(slot.upload(self.X_dev), params, lr)
-            return
-        total = self.layout["total"]
-        self.dev.copy_(slot.packed_h[:total], non_blocking=True)
-        slot.mark_uploaded()
+        """One sub-GCN step on the batch built in ``slot`` (fixed layout): one
+        library call copies it into this runner's buffer and replays the step
+        (recorded on first use of these parameters)."""
         key = (tuple(p.data_ptr() for p in params), float(lr))
-        g = self.graphs.get(key)
-        if g is None:
-            g = self.graphs[key] = self._capture(params, lr)
-        g.replay()
+        if not slot.fits_fixed():    # rare: too many entries for the fixed layout
+            self.cap_ctx.set_stream(torch.cuda.current_stream().cuda_stream)
+            try:
+                self.run.step(slot.upload(self.X_dev), params, lr)
+            finally:
+                self.cap_ctx.set_stream(self.cap_stream.cuda_stream)
+            return
+        r = self.replays.get(key)
+        if r is None:
+            r = self.replays[key] = self._capture(params, lr)
+        G.gist_replay_launch(self.ctx, r, self.dev, slot.packed_h, self.nbytes, slot.event)
+        slot.uploaded = slot.event
+
+    @property
+    def graphs(self):
+        return self.replays
 
     @property
     def loss(self):
@@ -859,6 +867,7 @@ class GistModel:
         self._dev = [[None] * (self.L + 1) for _ in range(2)]
         self._doffs = [[None] * (self.L + 1) for _ in range(2)]
         self._events = [None, None]
+        self._gevents = [None, None]   # gist events recorded after the partition uploads
         self.pending = None    # (slot, buffer) whose subAgg is outstanding
 
     # -- layout ---------------------------------------------------------------
@@ -957,11 +966,12 @@ class GistModel:
             h[2 * d:].view(np.int64)[:] = offs
             self._host[slot][l] = (idx, offs)
             pin = self._pin[slot][l]
-            self._dev[slot][l].view(-1).copy_(pin[:2 * d], non_blocking=True)
-            self._doffs[slot][l].copy_(pin[2 * d:].view(torch.int64), non_blocking=True)
-        ev = torch.cuda.Event()
-        ev.record()
-        self._events[slot] = ev
+            G.gist_copy(self.ctx, self._dev[slot][l], pin, 8 * d)
+            G.gist_copy(self.ctx, self._doffs[slot][l], pin[2 * d:], 8 * (m + 1))
+        if self._gevents[slot] is None:
+            self._gevents[slot] = G.Event()
+        G.gist_copy(self.ctx, None, None, 0, self._gevents[slot])
+        self._events[slot] = self._gevents[slot]
         self._slot = slot
 
     def _block(self, l, i):
