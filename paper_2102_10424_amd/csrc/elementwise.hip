@@ -159,6 +159,29 @@ __global__ void zero_int_kernel(int* p) {
   if (threadIdx.x == 0 && blockIdx.x == 0) p[0] = 0;
 }
 
+// dst (cols x rows, leading dimension ldd) = transpose of src (rows x cols,
+// leading dimension lds), through a 64 x 65 LDS tile (the extra column keeps
+// the column reads of the tile free of bank conflicts).  Both the reads and
+// the writes go along the contiguous dimension, 64 floats per wave row.
+__global__ __launch_bounds__(kBlock) void transpose_kernel(const float* __restrict__ src,
+                                                           int64_t rows, int64_t cols,
+                                                           int64_t lds, float* __restrict__ dst,
+                                                           int64_t ldd) {
+  __shared__ float tile[64][65];
+  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * 64;
+  const int64_t c0 = static_cast<int64_t>(blockIdx.x) * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < 64; i += kBlock / 64) {
+    const int64_t r = r0 + i, c = c0 + tx;
+    if (r < rows && c < cols) tile[i][tx] = src[r * lds + c];
+  }
+  __syncthreads();
+  for (int i = ty; i < 64; i += kBlock / 64) {
+    const int64_t c = c0 + i, r = r0 + tx;
+    if (c < cols && r < rows) dst[c * ldd + r] = tile[tx][i];
+  }
+}
+
 // Copy of `n16` 16-byte words, then `tail` single bytes, from `src` (which
 // may be pinned host memory: the reads then cross the host link) to `dst`.
 __global__ __launch_bounds__(kBlock) void pull_kernel(uint4* __restrict__ dst,
@@ -562,6 +585,18 @@ gist_status fill_zero(hipStream_t st, float* p, int64_t count) {
   hipLaunchKernelGGL(zero_kernel, dim3(grid_for(count, kBlock, 8192)), dim3(kBlock), 0, st, p,
                      count);
   return check_launch("fill_zero");
+}
+
+gist_status transpose(hipStream_t st, const float* src, int64_t rows, int64_t cols, int64_t lds,
+                      float* dst, int64_t ldd) {
+  if (rows <= 0 || cols <= 0) return GIST_OK;
+  const int64_t gx = (cols + 63) / 64, gy = (rows + 63) / 64;
+  if (gx > INT32_MAX || gy > 65535)
+    return set_error(GIST_E_UNSUPPORTED, "transpose: matrix too large");
+  ProfScope ps(st, "transpose", 0.0, 8.0 * static_cast<double>(rows) * cols);
+  hipLaunchKernelGGL(transpose_kernel, dim3(static_cast<unsigned>(gx), static_cast<unsigned>(gy)),
+                     dim3(kBlock), 0, st, src, rows, cols, lds, dst, ldd);
+  return check_launch("transpose");
 }
 
 gist_status pull_copy(hipStream_t st, void* dst, const void* src, int64_t bytes) {

@@ -112,6 +112,7 @@ RECT = [
     ("sbm5000", 1, 33, 7, 0, 2),
     ("sbm5000", 0, 256, 256, 1, 2),
     ("cl3000", 0, 5, 300, 1, 1),
+    ("sbm5000", 0, 1030, 1024, 1, 2),  # dW from node-contiguous copies (K = n_in)
 ]
 
 

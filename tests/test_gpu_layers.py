@@ -108,6 +108,10 @@ CASES = [
     ("sage", "sbm1500", 100, 256, 1, 0),
     ("sage", "sbm1500", 602, 260, 1, 0),
     ("sage", "cl2000", 256, 41, 0, 0),
+    # weight gradients large enough (M, N >= 1024) for node-contiguous operand copies
+    ("sage", "sbm1500", 512, 1024, 1, 0),
+    ("gcn", "er300", 1030, 1100, 1, 1),
+    ("gcn", "sbm1500", 1100, 1030, 0, 2),
 ]
 
 
