@@ -104,7 +104,8 @@ def parse():
     ap.add_argument("--shared-batch", action="store_true",
                     help="all m sub-GCNs step on one shared mini-batch, as batched layer calls")
     ap.add_argument("--graphs", action="store_true",
-                    help="LADIES workloads: replay every sub-GCN step from a HIP graph")
+                    help="replay every sub-GCN step from a HIP graph (SGD, a mini-batch per "
+                         "sub-GCN: cluster or LADIES batches at fixed padded shapes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the library's per-launch event timing")
@@ -121,8 +122,9 @@ class RoundWorkload:
                  streams=1, graphs=False):
         import torch
         from paper_2102_10424_amd import gist as G
-        from paper_2102_10424_amd.step import (BatchPipeline, BatchSlot, GistModel,
-                                               LadiesGraphRunner, SubGCN, SubGCNBatch)
+        from paper_2102_10424_amd.step import (BatchPipeline, BatchSlot, ClusterGraphRunner,
+                                               FixedBatchSlot, GistModel, LadiesGraphRunner,
+                                               SubGCN, SubGCNBatch)
         self.cfg, self.ctx, self.G = cfg, ctx, G
         t0 = time.time()
         self.graph = cfg.make_graph()
@@ -145,8 +147,9 @@ class RoundWorkload:
         self.ladies = cfg.ladies
         if self.ladies and shared:
             raise ValueError("LADIES mini-batches are per sub-GCN (no shared batch)")
-        if graphs and (not self.ladies or optimizer != "sgd"):
-            raise ValueError("--graphs replays LADIES sub-GCN steps with SGD")
+        if graphs and (optimizer != "sgd" or shared or
+                       not (self.ladies or cfg.batch_clusters)):
+            raise ValueError("--graphs replays SGD sub-GCN steps on per-sub-GCN mini-batches")
         self.use_graphs = self.graphs = graphs
         # capacities: the largest mini-batch of the clusters, generous nnz bound
         if self.ladies:
@@ -189,7 +192,10 @@ class RoundWorkload:
             self.pipes = [BatchPipeline(c, self.norm, cap_n, cap_nnz, cfg.widths[0], self.gh,
                                         self.X, self.labels,
                                         self._cluster_order(shared, zeta, k, self.nstreams),
-                                        depth=8, workers=4 if self.nstreams == 1 else 2)
+                                        depth=8, workers=(12 if graphs else 4) // self.nstreams,
+                                        slots=[FixedBatchSlot(c, self.norm, cap_n, cap_nnz,
+                                                              cfg.widths[0])
+                                               for _ in range(12 if graphs else 8)])
                           for k, c in enumerate(self.ctxs)]
             self.pipe = self.pipes[0]
         dt = G.GIST_DTYPE_BF16_IN if dtype == "bf16" else G.GIST_DTYPE_F32
@@ -200,10 +206,15 @@ class RoundWorkload:
             self.runners = [SubGCN(c, cfg.kind, self.model.slice_widths, cap_n, dtype=dt)
                             for c in self.ctxs]
             self.runner = self.runners[0]
-            if graphs:
+            if graphs and self.ladies:
                 self.graph_runners = [
                     LadiesGraphRunner(c, self.model.slice_widths, cfg.L, self.ladies["batch"],
                                       self.ladies["samples"], cfg.widths[0], self.X, dtype=dt)
+                    for c in self.ctxs]
+            elif graphs:
+                self.graph_runners = [
+                    ClusterGraphRunner(c, cfg.kind, self.model.slice_widths, cap_n, cap_nnz,
+                                       cfg.widths[0], self.X, dtype=dt)
                     for c in self.ctxs]
         self.lr = 0.01
         self.t = 0

@@ -361,6 +361,15 @@ gist_status gist_softmax_xent(gist_ctx* ctx, int64_t n, int32_t C,
                               const float* logits, const int32_t* labels,
                               float* loss_dev, float* dlogits, void* ws,
                               size_t ws_bytes);
+/* The same over a batch padded to n rows, with the number of real rows in
+ * device memory (*n_valid_dev, one int32, read by the kernels, so that a
+ * replayed step can change it): the loss is the mean over rows
+ * [0, n_valid) and the gradient rows [n_valid, n) are zero.  A count
+ * outside [0, n] is clamped.  Same workspace; errors as gist_softmax_xent. */
+gist_status gist_softmax_xent_padded(gist_ctx* ctx, int64_t n, int32_t C,
+                                     const float* logits, const int32_t* labels,
+                                     const int32_t* n_valid_dev, float* loss_dev,
+                                     float* dlogits, void* ws, size_t ws_bytes);
 
 /* ---- subGCNs slice gather (Section 2.1) ----------------------------- */
 

@@ -690,6 +690,25 @@ extern "C" gist_status gist_softmax_xent(gist_ctx* ctx, int64_t n, int32_t C,
                             static_cast<float*>(ws));
 }
 
+extern "C" gist_status gist_softmax_xent_padded(gist_ctx* ctx, int64_t n, int32_t C,
+                                                const float* logits, const int32_t* labels,
+                                                const int32_t* n_valid_dev, float* loss_dev,
+                                                float* dlogits, void* ws, size_t ws_bytes) {
+  gist::clear_error();
+  if (!ctx) return set_error(GIST_E_INVAL, "softmax_xent_padded: NULL ctx");
+  if (!n_valid_dev) return set_error(GIST_E_INVAL, "softmax_xent_padded: NULL row count");
+  gist::ProfBind pb(ctx);
+  if (n < 0 || C < 1) return set_error(GIST_E_INVAL, "softmax_xent_padded: bad sizes");
+  if (!loss_dev || (n > 0 && (!logits || !labels || !dlogits)))
+    return set_error(GIST_E_INVAL, "softmax_xent_padded: NULL pointer");
+  if (n > INT32_MAX) return set_error(GIST_E_UNSUPPORTED, "softmax_xent_padded: n exceeds int32");
+  if (ws_bytes < gist_softmax_xent_workspace(n) || !ws)
+    return set_error(GIST_E_NOMEM, "softmax_xent_padded: workspace too small");
+  gist::DeviceGuard dg(ctx->device);
+  return gist::softmax_xent(ctx->stream, n, C, logits, labels, loss_dev, dlogits,
+                            static_cast<float*>(ws), n_valid_dev);
+}
+
 extern "C" gist_status gist_gather_slice(gist_ctx* ctx, const float* Wg, int64_t ldg,
                                          const int32_t* rows, int32_t nr,
                                          const int32_t* cols, int32_t nc, float* Ws,

@@ -217,16 +217,28 @@ __global__ __launch_bounds__(kBlock) void nonfinite_kernel(const float* __restri
 
 // Softmax cross-entropy: one wave per row (classes strided over lanes);
 // per-block partial sums of the row losses, summed in order afterwards.
+// Rows at or past the valid count (n, or *n_dev when given, clamped to
+// [0, n]) are padding: their gradient rows are zero and they add nothing.
+__device__ __forceinline__ int valid_rows(int n, const int* n_dev) {
+  if (!n_dev) return n;
+  const int v = *n_dev;
+  return v < 0 ? 0 : (v > n ? n : v);
+}
+
 __global__ __launch_bounds__(kBlock) void xent_rows_kernel(int n, int C,
                                                            const float* __restrict__ Z,
                                                            const int* __restrict__ y,
                                                            float* __restrict__ dZ,
-                                                           float* __restrict__ partials) {
+                                                           float* __restrict__ partials,
+                                                           const int* __restrict__ n_dev) {
   __shared__ float wloss[kBlock / 64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t row = static_cast<int64_t>(blockIdx.x) * (kBlock / 64) + wave;
+  const int nv = valid_rows(n, n_dev);
   float row_loss = 0.f;
-  if (row < n) {
+  if (row >= nv && row < n) {
+    for (int j = lane; j < C; j += 64) dZ[row * C + j] = 0.f;
+  } else if (row < n) {
     const float* z = Z + row * C;
     float* g = dZ + row * C;
     const int label = y[row];
@@ -237,7 +249,7 @@ __global__ __launch_bounds__(kBlock) void xent_rows_kernel(int n, int C,
     for (int j = lane; j < C; j += 64) s += expf(z[j] - mx);
     s = wave_sum(s);
     const float lse = mx + logf(s);
-    const float inv_n = 1.0f / static_cast<float>(n);
+    const float inv_n = 1.0f / static_cast<float>(nv);
     float zy = 0.f;
     for (int j = lane; j < C; j += 64) {
       const float p = expf(z[j] - lse);
@@ -257,7 +269,9 @@ __global__ __launch_bounds__(kBlock) void xent_rows_kernel(int n, int C,
 }
 
 __global__ __launch_bounds__(kBlock) void xent_finish_kernel(int nparts, const float* __restrict__ partials,
-                                                             int n, float* loss) {
+                                                             int n, float* loss,
+                                                             const int* __restrict__ n_dev) {
+  n = valid_rows(n, n_dev);
   __shared__ float sh[kBlock];
   float s = 0.f;
   for (int i = threadIdx.x; i < nparts; i += kBlock) s += partials[i];
@@ -676,16 +690,17 @@ gist_status count_nonfinite(hipStream_t st, const float* Ws, int64_t lds, int32_
 }
 
 gist_status softmax_xent(hipStream_t st, int64_t n, int C, const float* logits,
-                         const int32_t* labels, float* loss, float* dlogits, float* partials) {
+                         const int32_t* labels, float* loss, float* dlogits, float* partials,
+                         const int32_t* n_dev) {
   const int rows_per_block = kBlock / 64;
   const int nparts = static_cast<int>((n + rows_per_block - 1) / rows_per_block);
   if (n > 0) {
     ProfScope ps(st, "softmax_xent_rows", 0.0, 8.0 * static_cast<double>(n) * C + 4.0 * n);
     hipLaunchKernelGGL(xent_rows_kernel, dim3(static_cast<unsigned>(nparts)), dim3(kBlock), 0,
-                       st, static_cast<int>(n), C, logits, labels, dlogits, partials);
+                       st, static_cast<int>(n), C, logits, labels, dlogits, partials, n_dev);
   }
   hipLaunchKernelGGL(xent_finish_kernel, dim3(1), dim3(kBlock), 0, st, nparts, partials,
-                     static_cast<int>(n), loss);
+                     static_cast<int>(n), loss, n_dev);
   return check_launch("softmax_xent");
 }
 

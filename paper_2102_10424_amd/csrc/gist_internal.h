@@ -176,6 +176,6 @@ gist_status adam(hipStream_t st, float* W, const float* dW, float* m, float* v, 
                  bool fresh);
 gist_status softmax_xent(hipStream_t st, int64_t n, int C, const float* logits,
                          const int32_t* labels, float* loss, float* dlogits,
-                         float* partials);
+                         float* partials, const int32_t* n_dev = nullptr);
 
 }  // namespace gist

@@ -58,7 +58,8 @@ EXPORTED = (
     "gist_set_stream", "gist_partition", "gist_build_minibatch_csr", "gist_ladies_sample",
     "gist_layer_workspace_size", "gist_gcn_layer_fwd", "gist_gcn_layer_bwd",
     "gist_gat_workspace_size", "gist_gat_layer_fwd", "gist_gat_layer_bwd",
-    "gist_softmax_xent_workspace", "gist_softmax_xent", "gist_gather_slice",
+    "gist_softmax_xent_workspace", "gist_softmax_xent", "gist_softmax_xent_padded",
+    "gist_gather_slice",
     "gist_sgd_update", "gist_adam_update", "gist_subagg", "gist_partition_inverse",
     "gist_subagg_gather", "gist_subagg_mean",
     "gist_profile_begin", "gist_profile_read", "gist_profile_end",
@@ -161,6 +162,8 @@ _sigs = {
                                      C.c_size_t]),
     "gist_softmax_xent_workspace": (C.c_size_t, [C.c_int64]),
     "gist_softmax_xent": (C.c_int, [_P, C.c_int64, C.c_int32, _P, _P, _P, _P, _P, C.c_size_t]),
+    "gist_softmax_xent_padded": (C.c_int, [_P, C.c_int64, C.c_int32, _P, _P, _P, _P, _P, _P,
+                                           C.c_size_t]),
     "gist_gather_slice": (C.c_int, [_P, _P, C.c_int64, _P, C.c_int32, _P, C.c_int32, _P,
                                     C.c_int64]),
     "gist_sgd_update": (C.c_int, [_P, _P, _P, C.c_int64, C.c_float]),
@@ -424,6 +427,14 @@ def gist_softmax_xent_workspace(n):
 def gist_softmax_xent(ctx, n, C_, logits, labels, loss_dev, dlogits, ws):
     _check(_lib.gist_softmax_xent(ctx.handle, int(n), int(C_), _ptr(logits), _ptr(labels),
                                   _ptr(loss_dev), _ptr(dlogits), _ptr(ws), _nbytes(ws)))
+
+
+def gist_softmax_xent_padded(ctx, n, C_, logits, labels, n_valid_dev, loss_dev, dlogits, ws):
+    """Loss over a batch padded to n rows; the real row count is the device int32
+    ``n_valid_dev``."""
+    _check(_lib.gist_softmax_xent_padded(ctx.handle, int(n), int(C_), _ptr(logits), _ptr(labels),
+                                         _ptr(n_valid_dev), _ptr(loss_dev), _ptr(dlogits),
+                                         _ptr(ws), _nbytes(ws)))
 
 
 def gist_gather_slice(ctx, Wg, ldg, rows, nr, cols, nc, Ws, lds):

@@ -28,6 +28,16 @@ def _dev(x, device, dtype=None):
     return t.to(device, non_blocking=False)
 
 
+def _wait(event):
+    """Wait for a slot's last upload to complete; returns the seconds waited."""
+    if event is None:
+        return 0.0
+    import time
+    t0 = time.perf_counter()
+    event.synchronize()
+    return time.perf_counter() - t0
+
+
 class DeviceBatch:
     """A mini-batch on the device: CSR (+ transpose for SAGE), features, labels."""
 
@@ -86,14 +96,15 @@ class BatchSlot:
         self.X = torch.empty(cap_n, d_in, device=device)
         self.d_in = d_in
         self.uploaded = None
+        self.event = None
         self.built = None
+        self.sync_s = 0.0
 
     def build(self, graph_struct, clusters, labels_host):
         """Host half of ``load``: the mini-batch CSR and labels into the pinned
         staging buffers (after the previous upload from them has completed).
         Touches no device memory, so it may run on a worker thread."""
-        if self.uploaded is not None:
-            self.uploaded.synchronize()  # previous upload from the staging buffers done
+        self.sync_s = _wait(self.uploaded)   # previous upload from the staging buffers done
         q = G.gist_csr()
         q.cap_n, q.cap_nnz = self.cap_n, self.cap_nnz
         h = self.h
@@ -109,17 +120,22 @@ class BatchSlot:
         self.built = (n, nnz)
 
     def upload(self, X_dev):
-        """Device half of ``load``: asynchronous uploads of the built batch on
-        the current stream and the device gather of its feature rows."""
+        """Device half of ``load``: asynchronous uploads of the built batch and
+        the device gather of its feature rows, on the stream of the slot's
+        context.  The uploads are kernel pulls from the pinned staging
+        buffers (``gist_copy``): they stay on the compute queue, where a
+        copy-engine transfer would make the next kernel wait for a hand-off
+        between engines."""
         n, nnz = self.built
         h = self.h
         for k in h:
             cnt = n + 1 if k.endswith("rowptr") else (nnz if k.endswith(("col", "val")) else n)
             if cnt:
-                self.d[k][:cnt].copy_(h[k][:cnt], non_blocking=True)
-        ev = torch.cuda.Event()
-        ev.record()
-        self.uploaded = ev
+                G.gist_copy(self.ctx, self.d[k], h[k], 4 * cnt)
+        if self.event is None:
+            self.event = G.Event()
+        G.gist_copy(self.ctx, None, None, 0, self.event)
+        self.uploaded = self.event
         Xb = self.X[:n]
         G.gist_gather_slice(self.ctx, X_dev, self.d_in, self.d["node_map"], n, None,
                             self.d_in, Xb, self.d_in)
@@ -129,6 +145,97 @@ class BatchSlot:
         """Build, upload and gather; returns a batch view with n, nnz, A, A_T, X, labels."""
         self.build(graph_struct, clusters, labels_host)
         return self.upload(X_dev)
+
+
+class FixedBatchSlot:
+    """A cluster mini-batch in a fixed layout at the slot's capacities, for
+    :class:`ClusterGraphRunner`.
+
+    ``build`` writes the CSR (and the SAGE transpose), node map and labels
+    straight into one pinned buffer at fixed offsets and pads them: rows
+    past the batch are empty (their row pointers repeat nnz), their node is
+    0 and their label 0, and the real row count is stored as one int32 for
+    the padded loss.  Shapes are then the same for every batch; empty rows
+    aggregate to zero (GCN, SAGE and GAT alike) and the loss ignores them,
+    so no result changes.
+    """
+
+    _ALIGN = 64
+
+    def __init__(self, ctx, norm, cap_n, cap_nnz, d_in, device="cuda"):
+        self.ctx, self.d_in, self.device = ctx, d_in, device
+        self.norm, self.sage = norm, norm == "sage"
+        self.cap_n, self.cap_nnz = int(cap_n), int(cap_nnz)
+        self.layout = self.fixed_layout(self.sage, self.cap_n, self.cap_nnz)
+        self.packed_h = torch.empty(self.layout["total"], dtype=torch.int32, pin_memory=True)
+        base = self.packed_h.data_ptr()
+        o = self.layout["off"]
+        q = G.gist_csr()
+        q.cap_n, q.cap_nnz = self.cap_n, self.cap_nnz
+        q.rowptr, q.col, q.val = base + 4 * o["rowptr"], base + 4 * o["col"], base + 4 * o["val"]
+        q.node_map = base + 4 * o["node_map"]
+        if self.sage:
+            q.t_rowptr, q.t_col, q.t_val = (base + 4 * o["t_rowptr"], base + 4 * o["t_col"],
+                                            base + 4 * o["t_val"])
+        self.q = q
+        self.event = G.Event()
+        self.uploaded = None
+        self.n = self.nnz = 0
+        self.packed_d = None      # device copy for eager use (upload), made on first use
+        self.X = None
+
+    @classmethod
+    def fixed_layout(cls, sage, cap_n, cap_nnz):
+        pad = lambda n: (int(n) + cls._ALIGN - 1) // cls._ALIGN * cls._ALIGN
+        cnt = dict(rowptr=cap_n + 1, col=cap_nnz, val=cap_nnz, node_map=cap_n, labels=cap_n,
+                   n_valid=1)
+        if sage:
+            cnt.update(t_rowptr=cap_n + 1, t_col=cap_nnz, t_val=cap_nnz)
+        off, o = 0, {}
+        for k, c in cnt.items():
+            o[k] = off
+            off += pad(c)
+        return dict(off=o, total=off)
+
+    def build(self, graph_struct, clusters, labels_host):
+        """Host half: the batch into the fixed layout (after the last upload from it)."""
+        self.sync_s = _wait(self.uploaded)
+        G.build_minibatch_into(graph_struct, clusters, self.norm, self.q)
+        n, nnz = int(self.q.n), int(self.q.nnz)
+        h, o, cap = self.packed_h.numpy(), self.layout["off"], self.cap_n
+        h[o["rowptr"] + n + 1:o["rowptr"] + cap + 1] = nnz
+        if self.sage:
+            h[o["t_rowptr"] + n + 1:o["t_rowptr"] + cap + 1] = nnz
+        nm = h[o["node_map"]:o["node_map"] + n]
+        h[o["labels"]:o["labels"] + n] = labels_host[nm]
+        h[o["node_map"] + n:o["node_map"] + cap] = 0
+        h[o["labels"] + n:o["labels"] + cap] = 0
+        h[o["n_valid"]] = n
+        self.n, self.nnz = n, nnz
+
+    def upload(self, X_dev):
+        """Eager use: copy the batch to this slot's device buffer (one kernel
+        pull on the stream of the slot's context) and gather its feature
+        rows; returns a view with the real sizes."""
+        if self.packed_d is None:
+            self.packed_d = torch.empty_like(self.packed_h, device=self.device)
+            self.X = torch.empty(self.cap_n, self.d_in, device=self.device)
+        c = self.ctx
+        G.gist_copy(c, self.packed_d, self.packed_h, 4 * self.layout["total"], self.event)
+        self.uploaded = self.event
+        o, d, n = self.layout["off"], self.packed_d, self.n
+        f32 = torch.float32
+        v = dict(rowptr=d[o["rowptr"]:], col=d[o["col"]:],
+                 val=d[o["val"]:o["val"] + max(self.nnz, 1)].view(f32),
+                 labels=d[o["labels"]:o["labels"] + n])
+        if self.sage:
+            v.update(t_rowptr=d[o["t_rowptr"]:], t_col=d[o["t_col"]:],
+                     t_val=d[o["t_val"]:o["t_val"] + max(self.nnz, 1)].view(f32))
+        Xb = self.X[:n]
+        if n:
+            G.gist_gather_slice(c, X_dev, self.d_in, d[o["node_map"]:], n, None, self.d_in, Xb,
+                                self.d_in)
+        return _View(n, self.nnz, v, Xb, self.sage)
 
 
 class BatchPipeline:
@@ -191,7 +298,9 @@ class BatchPipeline:
             import time
             t0 = time.perf_counter()
             fut.result()
-            self.wait_s += time.perf_counter() - t0
+            # less the part of it the build spent waiting for the device to
+            # release the slot (back-pressure when the device is the limit)
+            self.wait_s += max(0.0, time.perf_counter() - t0 - getattr(slot, "sync_s", 0.0))
         fut.result()
         out = use(slot)
         self._submit()       # reuses this slot: its build waits for the upload just enqueued
@@ -326,8 +435,7 @@ class LadiesSlot:
 
     def build(self, A_handle, batch, seed, labels_host):
         """Host half: sample the layers, pack them and the output nodes' labels."""
-        if self.uploaded is not None:
-            self.uploaded.synchronize()     # the previous upload from packed_h is done
+        self.sync_s = _wait(self.uploaded)   # the previous upload from packed_h is done
         batch = np.asarray(batch, dtype=np.int32)
         nb = batch.shape[0]
         if nb > self.b or (self.fixed and nb != self.b):
@@ -377,18 +485,13 @@ class LadiesSlot:
         packed compactly: its entries exceeded the fixed capacity)."""
         return self.built[5]
 
-    def mark_uploaded(self):
-        ev = torch.cuda.Event()
-        ev.record()
-        self.uploaded = ev
-
     def upload(self, X_dev):
         """Device half: one asynchronous copy on the current stream and the
         gather of the input nodes' features."""
         nb, sizes, offs, lab, total, fits = self.built
         d = self.packed_d
-        d[:total].copy_(self.packed_h[:total], non_blocking=True)
-        self.mark_uploaded()
+        G.gist_copy(self.ctx, d, self.packed_h, 4 * total, self.event)
+        self.uploaded = self.event
         f32 = torch.float32
         views = []
         for l, (n_out, n_in, nnz) in enumerate(sizes):
@@ -407,6 +510,74 @@ class LadiesSlot:
     def load(self, A_handle, batch, seed, X_dev, labels_host):
         self.build(A_handle, batch, seed, labels_host)
         return self.upload(X_dev)
+
+
+class ClusterGraphRunner:
+    """Sub-GCN steps on cluster mini-batches replayed from HIP graphs (the
+    counterpart of :class:`LadiesGraphRunner` for GCN, SAGE and GAT layers).
+
+    Every batch is run at the capacity shape of :class:`FixedBatchSlot` (n
+    rows, nnz entries): the step (feature gather, forward, padded loss,
+    backward, SGD) is recorded once per parameter set and learning rate on
+    a side-stream context, and each step is one ``gist_replay_launch``
+    that pulls the batch from pinned memory into this runner's buffer.
+    """
+
+    def __init__(self, ctx, kind, widths, cap_n, cap_nnz, d_in, X_dev, dtype=G.GIST_DTYPE_F32,
+                 device="cuda"):
+        self.ctx, self.d_in, self.X_dev = ctx, d_in, X_dev
+        self.cap_stream = torch.cuda.Stream()
+        self.cap_ctx = G.Context(ctx.device, stream=self.cap_stream.cuda_stream)
+        norm = "sage" if kind == "sage" else "gcn"
+        self.layout = FixedBatchSlot.fixed_layout(norm == "sage", cap_n, cap_nnz)
+        self.dev = torch.empty(self.layout["total"], dtype=torch.int32, device=device)
+        o, d = self.layout["off"], self.dev
+        f32 = torch.float32
+        view = dict(rowptr=d[o["rowptr"]:], col=d[o["col"]:],
+                    val=d[o["val"]:o["val"] + cap_nnz].view(f32),
+                    labels=d[o["labels"]:o["labels"] + cap_n])
+        if norm == "sage":
+            view.update(t_rowptr=d[o["t_rowptr"]:], t_col=d[o["t_col"]:],
+                        t_val=d[o["t_val"]:o["t_val"] + cap_nnz].view(f32))
+        self.node_map = d[o["node_map"]:o["node_map"] + cap_n]
+        self.X = torch.empty(cap_n, d_in, device=device)
+        self.view = _View(cap_n, cap_nnz, view, self.X, norm == "sage")
+        self.view.n_dev = d[o["n_valid"]:o["n_valid"] + 1]
+        self.cap_n = cap_n
+        self.run = SubGCN(self.cap_ctx, kind, widths, cap_n, dtype=dtype, device=device)
+        self.run.prepare(self.view)
+        self.nbytes = 4 * self.layout["total"]
+        self.replays = {}
+
+    def _body(self, params, lr):
+        G.gist_gather_slice(self.cap_ctx, self.X_dev, self.d_in, self.node_map, self.cap_n, None,
+                            self.d_in, self.X, self.d_in)
+        self.run.forward(self.view, params)
+        self.run.loss_and_grad(self.view)
+        self.run.backward(self.view, params)
+        self.run.sgd(params, lr)
+
+    def _capture(self, params, lr):
+        torch.cuda.synchronize()
+        G.gist_capture_begin(self.cap_ctx)
+        try:
+            self._body(params, lr)
+        finally:
+            replay = G.gist_capture_end(self.cap_ctx)
+        return replay
+
+    def step(self, slot, params, lr):
+        """One sub-GCN step on the batch built in ``slot``."""
+        key = (tuple(p.data_ptr() for p in params), float(lr))
+        r = self.replays.get(key)
+        if r is None:
+            r = self.replays[key] = self._capture(params, lr)
+        G.gist_replay_launch(self.ctx, r, self.dev, slot.packed_h, self.nbytes, slot.event)
+        slot.uploaded = slot.event
+
+    @property
+    def loss(self):
+        return self.run.loss
 
 
 class LadiesGraphRunner:
@@ -629,11 +800,28 @@ class SubGCN:
         return self.H[self.L][:batch.rows(self.L)]
 
     def loss_and_grad(self, batch, loss_out=None):
-        """Loss into ``loss_out`` (a one-element device tensor) or ``self.loss``."""
+        """Loss into ``loss_out`` (a one-element device tensor) or ``self.loss``.
+        A padded batch (``n_dev``: its real row count on the device) takes the
+        mean over its real rows."""
         n = batch.rows(self.L)
-        G.gist_softmax_xent(self.ctx, n, self.widths[-1], self.H[self.L][:n], batch.labels,
-                            self.loss if loss_out is None else loss_out, self.dlogits[:n],
-                            self.loss_ws)
+        out = self.loss if loss_out is None else loss_out
+        n_dev = getattr(batch, "n_dev", None)
+        if n_dev is not None:
+            G.gist_softmax_xent_padded(self.ctx, n, self.widths[-1], self.H[self.L][:n],
+                                       batch.labels, n_dev, out, self.dlogits[:n], self.loss_ws)
+        else:
+            G.gist_softmax_xent(self.ctx, n, self.widths[-1], self.H[self.L][:n], batch.labels,
+                                out, self.dlogits[:n], self.loss_ws)
+
+    def prepare(self, batch):
+        """Allocate every buffer a step on ``batch`` needs (before a capture)."""
+        n_max = max(batch.rows(l) for l in range(self.L + 1))
+        if n_max > self.n_cap:
+            self._alloc(n_max)
+        if self.gat and (self.alpha is None or batch.nnz > self.nnz_cap):
+            self.nnz_cap = max(batch.nnz, 1)
+            self.alpha = [torch.empty(self.nnz_cap, device=self.device) for _ in range(self.L)]
+        self._workspace(batch)
 
     def backward(self, batch, params):
         nnz = batch.nnz

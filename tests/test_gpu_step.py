@@ -242,3 +242,69 @@ def test_step_chained(G, ctx, name):
             ew = relerr(to_host(params[l]), stacked(kind, ref["params"][l]))
             log(f"[{name}] chained dW_{l} {e:.2e} W'_{l} {ew:.2e}")
             assert e <= FP32_TOL and ew <= FP32_TOL
+
+
+@pytest.mark.parametrize("kind,norm", [("gcn", "gcn"), ("sage", "sage"), ("gat", "gcn")])
+def test_cluster_graph_runner_matches_eager_and_oracle(G, ctx, kind, norm):
+    """Sub-GCN steps on cluster mini-batches replayed from HIP graphs at the
+    slots' capacity shapes (empty padded rows, the padded loss) against eager
+    steps on the same batches and the oracle's chained SGD steps; batches of
+    different sizes, two parameter sets, eager work between the replays."""
+    import torch
+    from gist_synth.graphs import sbm
+    from oracle import minibatch as MB
+    from paper_2102_10424_amd.step import BatchSlot, ClusterGraphRunner, FixedBatchSlot, SubGCN
+    g = sbm(3000, 60, 15.0, 0.9, seed=31)
+    widths = [24, 40, 32, 5]
+    rng = np.random.default_rng(7)
+    X = rng.standard_normal((g.n, widths[0])).astype(np.float32)
+    y = rng.integers(0, widths[-1], g.n).astype(np.int32)
+    wr = lambda l: widths[l] + 2 if kind == "gat" else (2 if kind == "sage" else 1) * widths[l]
+    theta = [(rng.standard_normal((wr(l), widths[l + 1])) * 0.3).astype(np.float32)
+             for l in range(3)]
+    sizes = np.diff(g.cluster_ptr)
+    cap_n = int(np.sort(sizes)[-5:].sum())
+    cap_nnz = int(np.sort(np.diff(g.rowptr))[-cap_n:].sum()) + cap_n
+    gh, Xd = G.GraphHandle(g), to_dev(X)
+    fixed = FixedBatchSlot(ctx, norm, cap_n, cap_nnz, widths[0])
+    plain = BatchSlot(ctx, norm, cap_n, cap_nnz, widths[0])
+    gr = ClusterGraphRunner(ctx, kind, widths, cap_n, cap_nnz, widths[0], Xd)
+    eager = SubGCN(ctx, kind, widths, cap_n)
+    pg = [[to_dev(t.copy()) for t in theta] for _ in range(2)]
+    pe = [[to_dev(t.copy()) for t in theta] for _ in range(2)]
+    po = [[t.astype(np.float64) for t in theta] for _ in range(2)]
+    ns = set()
+    for k in range(5):
+        j = k % 2
+        clusters = np.sort(rng.choice(g.n_clusters, 1 + k % 5, replace=False)).astype(np.int32)
+        log(f"cluster replay {kind} step {k}: {len(clusters)} clusters")
+        fixed.build(gh, clusters, y)
+        ns.add(fixed.n)
+        gr.step(fixed, pg[j], 0.05)
+        b = plain.load(gh, clusters, Xd, y)
+        eager.step(b, pe[j], 0.05)
+        torch.cuda.synchronize()
+        csr = MB.build(g, clusters, norm)
+        nm = csr["node_map"]
+        ref = [OG._pack(kind, OL_split(kind, t, widths[l])) for l, t in enumerate(po[j])]
+        st = OG.sub_gcn_step(kind, csr, X[nm], y[nm], ref, 0.05)
+        po[j] = [np.concatenate([np.atleast_2d(a) for a in OG._parts(kind, p)])
+                 for p in st["params"]]
+        assert abs(float(to_host(gr.loss)[0]) - st["loss"]) <= FP32_TOL * abs(st["loss"])
+        for l in range(3):
+            g_, e_ = to_host(pg[j][l]), to_host(pe[j][l])
+            assert relerr(g_, e_) <= 1e-5, (k, l)
+            assert relerr(g_, po[j][l]) <= FP32_TOL, (k, l)
+    assert len(ns) > 1 and len(gr.replays) == 2
+    # the fixed slot's own eager upload gives the same batch
+    b = fixed.upload(Xd)
+    assert b.n == fixed.n and b.nnz == fixed.nnz
+
+
+def OL_split(kind, t, rows):
+    """A layer's stacked device-layout parameters as the oracle's parts."""
+    if kind == "gcn":
+        return (t,)
+    if kind == "sage":
+        return (t[:rows], t[rows:])
+    return (t[:rows], t[rows], t[rows + 1])
