@@ -40,6 +40,59 @@ def test_softmax_xent(G, ctx, n, C):
     assert relerr(to_host(dZ), wg) <= FP32_TOL
 
 
+@pytest.mark.parametrize("n,C,valid", [(64, 41, 50), (3200, 41, 3107), (10, 7, 0), (10, 7, 10),
+                                       (10, 7, 25), (10, 7, -3)])
+def test_softmax_xent_padded(G, ctx, n, C, valid):
+    """A batch padded to n rows with the real count on the device: the loss is
+    the oracle's over the first rows (a count outside [0, n] clamped), the
+    padded rows' gradient is zero, and without padding the result is bit for
+    bit the unpadded call's."""
+    import torch
+    log(f"xent padded n={n} C={C} valid={valid}")
+    rng = np.random.default_rng(n + C + valid)
+    Z = (rng.standard_normal((n, C)) * 3).astype(np.float32)
+    y = rng.integers(0, C, n).astype(np.int32)
+    loss = torch.full((1,), float("nan"), device="cuda")
+    dZ = torch.full((n, C), float("nan"), device="cuda")
+    ws = torch.empty(G.gist_softmax_xent_workspace(n), dtype=torch.uint8, device="cuda")
+    nv = to_dev(np.array([valid], dtype=np.int32))
+    G.gist_softmax_xent_padded(ctx, n, C, to_dev(Z), to_dev(y), nv, loss, dZ, ws)
+    k = min(max(valid, 0), n)
+    got_l, got_g = float(to_host(loss)[0]), to_host(dZ)
+    assert np.all(got_g[k:] == 0)
+    if k == 0:
+        assert got_l == 0.0
+        return
+    wl, wg = OL.softmax_xent(Z[:k], y[:k])
+    assert abs(got_l - wl) / abs(wl) <= FP32_TOL
+    assert relerr(got_g[:k], wg) <= FP32_TOL
+    if k == n:
+        loss2 = torch.zeros(1, device="cuda")
+        dZ2 = torch.empty(n, C, device="cuda")
+        G.gist_softmax_xent(ctx, n, C, to_dev(Z), to_dev(y), loss2, dZ2, ws)
+        assert torch.equal(loss, loss2) and torch.equal(dZ, dZ2)
+
+
+def test_copy_pulls_from_pinned_and_device_memory(G, ctx):
+    """gist_copy: every byte count (aligned, unaligned, tails), from pinned
+    host memory and from device memory, and the event it records."""
+    import torch
+    src_h = torch.randint(0, 255, (100003,), dtype=torch.uint8).pin_memory()
+    src_d = src_h.cuda()
+    ev = G.Event()
+    for nbytes in (0, 1, 15, 16, 17, 4096, 100000, 100003):
+        for src, off in ((src_h, 0), (src_h, 3), (src_d, 0), (src_d, 5)):
+            if off + nbytes > src.numel():
+                continue
+            dst = torch.zeros(100016, dtype=torch.uint8, device="cuda")
+            G.gist_copy(ctx, dst, src.data_ptr() + off, nbytes, ev)
+            ev.synchronize()
+            got = dst.cpu().numpy()
+            want = src_h.numpy()[off:off + nbytes]
+            assert np.array_equal(got[:nbytes], want), (nbytes, off)
+            assert not got[nbytes:].any()
+
+
 def test_softmax_bad_label_reports_nan(G, ctx):
     import torch
     Z = torch.zeros(4, 3, device="cuda")

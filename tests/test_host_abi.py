@@ -295,3 +295,21 @@ def test_struct_layouts_match_header(tmp_path):
         want.append(C.sizeof(st))
         want += [getattr(st, f[0]).offset for f in st._fields_]
     assert got == want
+
+
+def test_replay_and_copy_argument_errors():
+    """Host-side checks of the replay / copy / event entry points (no device
+    work is reached)."""
+    import ctypes as C
+    lib = G._lib
+    assert lib.gist_capture_begin(None) == G.GIST_E_INVAL
+    out = C.c_void_p()
+    assert lib.gist_capture_end(None, C.byref(out)) == G.GIST_E_INVAL
+    assert lib.gist_replay_launch(None, None, None, None, 0, None) == G.GIST_E_INVAL
+    assert lib.gist_copy(None, None, None, 0, None) == G.GIST_E_INVAL
+    assert lib.gist_event_create(None) == G.GIST_E_INVAL
+    assert lib.gist_event_synchronize(None) == G.GIST_E_INVAL
+    assert lib.gist_replay_destroy(None) == G.GIST_OK
+    assert lib.gist_event_destroy(None) == G.GIST_OK
+    assert lib.gist_softmax_xent_padded(None, 1, 1, None, None, None, None, None, None, 0) == \
+        G.GIST_E_INVAL
