@@ -119,13 +119,16 @@ class RoundWorkload:
     """A GIST round (partition, gather, m sub-GCN steps, subAgg) on one GPU."""
 
     def __init__(self, cfg, ctx, dtype, optimizer="sgd", policy="carry", zeta=1, shared=False,
-                 streams=1, graphs=False):
+                 streams=1, graphs=False, lr=0.01):
         import torch
         from paper_2102_10424_amd import gist as G
         from paper_2102_10424_amd.step import (BatchPipeline, BatchSlot, ClusterGraphRunner,
                                                FixedBatchSlot, GistModel, LadiesGraphRunner,
                                                SubGCN, SubGCNBatch)
         self.cfg, self.ctx, self.G = cfg, ctx, G
+        self.lr = lr
+        self.adam = policy if optimizer == "adam" else None
+        self.use_graphs = self.graphs = graphs
         t0 = time.time()
         self.graph = cfg.make_graph()
         log(f"[bench] graph n={self.graph.n} nnz={self.graph.nnz} ({time.time() - t0:.1f}s)")
@@ -140,17 +143,14 @@ class RoundWorkload:
                 parts.append(torch.from_numpy(cfg.theta(l, p)).cuda())
             theta.append(parts)
         log(f"[bench] global theta on device ({time.time() - t0:.1f}s)")
-        self.adam = policy if optimizer == "adam" else None
         self.zeta = zeta
         self.model = GistModel(ctx, cfg.kind, cfg.widths, cfg.m, theta, adam=self.adam)
         self.norm = "sage" if cfg.kind == "sage" else "gcn"
         self.ladies = cfg.ladies
         if self.ladies and shared:
             raise ValueError("LADIES mini-batches are per sub-GCN (no shared batch)")
-        if graphs and (optimizer != "sgd" or shared or
-                       not (self.ladies or cfg.batch_clusters)):
-            raise ValueError("--graphs replays SGD sub-GCN steps on per-sub-GCN mini-batches")
-        self.use_graphs = self.graphs = graphs
+        if graphs and (shared or not (self.ladies or cfg.batch_clusters)):
+            raise ValueError("--graphs replays sub-GCN steps on per-sub-GCN mini-batches")
         # capacities: the largest mini-batch of the clusters, generous nnz bound
         if self.ladies:
             cap_n = self.ladies["batch"] + cfg.L * self.ladies["samples"]
@@ -195,7 +195,8 @@ class RoundWorkload:
                                         depth=8, workers=(12 if graphs else 4) // self.nstreams,
                                         slots=[FixedBatchSlot(c, self.norm, cap_n, cap_nnz,
                                                               cfg.widths[0])
-                                               for _ in range(12 if graphs else 8)])
+                                               for _ in range(12 if graphs else 8)],
+                                        build=self._fixed_build)
                           for k, c in enumerate(self.ctxs)]
             self.pipe = self.pipes[0]
         dt = G.GIST_DTYPE_BF16_IN if dtype == "bf16" else G.GIST_DTYPE_F32
@@ -216,18 +217,32 @@ class RoundWorkload:
                     ClusterGraphRunner(c, cfg.kind, self.model.slice_widths, cap_n, cap_nnz,
                                        cfg.widths[0], self.X, dtype=dt)
                     for c in self.ctxs]
-        self.lr = 0.01
         self.t = 0
+
+    def _coef(self, t, z):
+        """Adam coefficients of local step z of round t (a replayed Adam step
+        reads them from its batch), or None."""
+        if not (self.graphs and self.adam):
+            return None
+        carry = self.adam == "carry"
+        k = t * self.zeta + z + 1 if carry else z + 1
+        flags = self.G.GIST_ADAM_FRESH if (not carry and z == 0) else 0
+        return self.G.gist_adam_coefficients(self.lr, k, flags=flags)
 
     def _cluster_order(self, shared, zeta, k=0, nstreams=1):
         """The clusters of every mini-batch of stream k, in the order the
-        rounds take them (sub-GCNs k, k + nstreams, ...)."""
+        rounds take them (sub-GCNs k, k + nstreams, ...), with the step's Adam
+        coefficients."""
         cfg, t = self.cfg, 0
         while True:
             for i in range(k, 1 if shared else cfg.m, nstreams):
                 for z in range(zeta):
-                    yield cfg.minibatch(t, i, z)
+                    yield (lambda t=t, i=i, z=z: (cfg.minibatch(t, i, z), self._coef(t, z)))
             t += 1
+
+    def _fixed_build(self, slot, item):
+        clusters, coef = item()
+        slot.build(self.gh, clusters, self.labels, coef=coef)
 
     def _ladies_order(self, zeta, k=0, nstreams=1):
         """Every LADIES mini-batch of stream k, as a callable the pipeline's
@@ -237,7 +252,7 @@ class RoundWorkload:
             for i in range(k, cfg.m, nstreams):
                 for z in range(zeta):
                     yield (lambda t=t, i=i, z=z: (cfg.ladies_batch(t, i, z),
-                                                  cfg.ladies_seed(t, i, z)))
+                                                  cfg.ladies_seed(t, i, z), self._coef(t, z)))
             t += 1
 
     def _batch(self, t, i, z, k=0):
@@ -274,8 +289,9 @@ class RoundWorkload:
             with torch.cuda.stream(self.streams[k]):
                 if self.use_graphs:
                     gr = self.graph_runners[k]
+                    adam = (m.M[i], m.V[i]) if self.adam else None
                     for z in range(zeta):
-                        self.pipes[k].take(lambda slot: gr.step(slot, m.params[i], self.lr))
+                        self.pipes[k].take(lambda slot: gr.step(slot, m.params[i], self.lr, adam))
                     continue
                 for z in range(zeta):
                     b = self._batch(t, i, z, k)
@@ -481,8 +497,7 @@ def main():
         wl = LayerWorkload(cfg, ctx, args.dtype, args.d_in)
     else:
         wl = RoundWorkload(cfg, ctx, args.dtype, args.optimizer, args.adam_policy, args.zeta,
-                           args.shared_batch, args.streams, args.graphs)
-        wl.lr = args.lr
+                           args.shared_batch, args.streams, args.graphs, args.lr)
     ctxs = getattr(wl, "ctxs", [ctx])
     for w in range(args.warmup):
         wl.step()

@@ -17,6 +17,7 @@
  *   gist_softmax_xent          loss and its gradient                    (device)
  *   gist_sgd_update            one SGD step                             (device)
  *   gist_adam_update           one Adam step (the experiments' optimizer) (device)
+ *   gist_adam_update_dev       the same, coefficients read from the device (device)
  *   gist_subagg                subAgg: Theta[D_in, D_out] <- Theta^(i)  (device)
  *   gist_subagg_gather         subAgg of one round + gather of the next (device)
  *   gist_subagg_mean           subAgg of an unsplit parameter: mean of copies (device)
@@ -405,6 +406,21 @@ enum { GIST_ADAM_FRESH = 1 };
 gist_status gist_adam_update(gist_ctx* ctx, float* W, const float* dW, float* m, float* v,
                              int64_t n, float lr, float beta1, float beta2, float eps,
                              int64_t step, uint32_t flags);
+
+/* The step-dependent coefficients of gist_adam_update, host only:
+ * coef3 = {lr / (1 - beta1^k), 1 / sqrt(1 - beta2^k), 1 if GIST_ADAM_FRESH
+ * else 0}, formed in double and rounded once to float, with the same
+ * checks and errors.  gist_adam_update_dev reads these three floats from
+ * device memory (`coef_dev`) when its kernel runs, so a recorded step
+ * (gist_capture_begin) advances k and the fresh flag through the contents
+ * of one buffer; with the same coefficients it updates W, m and v exactly
+ * as gist_adam_update does.  Errors as gist_adam_update (coef_dev NULL:
+ * GIST_E_INVAL). */
+gist_status gist_adam_coefficients(float lr, float beta1, float beta2, float eps,
+                                   int64_t step, uint32_t flags, float* coef3);
+gist_status gist_adam_update_dev(gist_ctx* ctx, float* W, const float* dW, float* m, float* v,
+                                 int64_t n, float beta1, float beta2, float eps,
+                                 const float* coef_dev);
 
 /* ---- subAgg (Section 2.2) ------------------------------------------- */
 

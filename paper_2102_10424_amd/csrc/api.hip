@@ -750,6 +750,37 @@ extern "C" gist_status gist_subagg_mean(gist_ctx* ctx, float* Wg, int64_t rows, 
   return gist::subagg_mean(ctx->stream, Wg, rows, cols, ldg, m, slices, lds);
 }
 
+namespace {
+// The step-dependent Adam coefficients, formed in double and rounded once:
+// {lr / (1 - beta1^k), 1 / sqrt(1 - beta2^k), fresh}.
+gist_status adam_coef(const char* what, float lr, float beta1, float beta2, float eps,
+                      int64_t step, uint32_t flags, float* out) {
+  if (step < 1) return set_error(GIST_E_INVAL, std::string(what) + ": step counts from 1");
+  if (!(beta1 >= 0.f && beta1 < 1.f) || !(beta2 >= 0.f && beta2 < 1.f))
+    return set_error(GIST_E_INVAL, std::string(what) + ": beta outside [0, 1)");
+  if (!(eps >= 0.f) || !std::isfinite(lr) || !std::isfinite(eps))
+    return set_error(GIST_E_INVAL, std::string(what) + ": bad lr or eps");
+  if (flags & ~static_cast<uint32_t>(GIST_ADAM_FRESH))
+    return set_error(GIST_E_INVAL, std::string(what) + ": unknown flags");
+  const double bc1 = 1.0 - std::pow(static_cast<double>(beta1), static_cast<double>(step));
+  const double bc2 = 1.0 - std::pow(static_cast<double>(beta2), static_cast<double>(step));
+  if (!(bc1 > 0.0) || !(bc2 > 0.0))
+    return set_error(GIST_E_INVAL,
+                     std::string(what) + ": zero bias correction (beta = 0 needs no step)");
+  out[0] = static_cast<float>(lr / bc1);
+  out[1] = static_cast<float>(1.0 / std::sqrt(bc2));
+  out[2] = (flags & GIST_ADAM_FRESH) ? 1.f : 0.f;
+  return GIST_OK;
+}
+}  // namespace
+
+extern "C" gist_status gist_adam_coefficients(float lr, float beta1, float beta2, float eps,
+                                              int64_t step, uint32_t flags, float* coef3) {
+  gist::clear_error();
+  if (!coef3) return set_error(GIST_E_INVAL, "adam_coefficients: NULL out");
+  return adam_coef("adam_coefficients", lr, beta1, beta2, eps, step, flags, coef3);
+}
+
 extern "C" gist_status gist_adam_update(gist_ctx* ctx, float* W, const float* dW, float* m,
                                         float* v, int64_t n, float lr, float beta1, float beta2,
                                         float eps, int64_t step, uint32_t flags) {
@@ -757,23 +788,30 @@ extern "C" gist_status gist_adam_update(gist_ctx* ctx, float* W, const float* dW
   if (!ctx) return set_error(GIST_E_INVAL, "adam_update: NULL ctx");
   gist::ProfBind pb(ctx);
   if (n < 0) return set_error(GIST_E_INVAL, "adam_update: n < 0");
-  if (step < 1) return set_error(GIST_E_INVAL, "adam_update: step counts from 1");
-  if (!(beta1 >= 0.f && beta1 < 1.f) || !(beta2 >= 0.f && beta2 < 1.f))
-    return set_error(GIST_E_INVAL, "adam_update: beta outside [0, 1)");
-  if (!(eps >= 0.f) || !std::isfinite(lr) || !std::isfinite(eps))
-    return set_error(GIST_E_INVAL, "adam_update: bad lr or eps");
-  if (flags & ~static_cast<uint32_t>(GIST_ADAM_FRESH))
-    return set_error(GIST_E_INVAL, "adam_update: unknown flags");
+  float c[3];
+  GIST_TRY(adam_coef("adam_update", lr, beta1, beta2, eps, step, flags, c));
   if (n == 0) return GIST_OK;
   if (!W || !dW || !m || !v) return set_error(GIST_E_INVAL, "adam_update: NULL pointer");
-  const double bc1 = 1.0 - std::pow(static_cast<double>(beta1), static_cast<double>(step));
-  const double bc2 = 1.0 - std::pow(static_cast<double>(beta2), static_cast<double>(step));
-  if (!(bc1 > 0.0) || !(bc2 > 0.0))
-    return set_error(GIST_E_INVAL, "adam_update: zero bias correction (beta = 0 needs no step)");
   gist::DeviceGuard dg(ctx->device);
-  return gist::adam(ctx->stream, W, dW, m, v, n, static_cast<float>(lr / bc1),
-                    static_cast<float>(1.0 / std::sqrt(bc2)), beta1, beta2, eps,
-                    (flags & GIST_ADAM_FRESH) != 0);
+  return gist::adam(ctx->stream, W, dW, m, v, n, c[0], c[1], beta1, beta2, eps, c[2] != 0.f);
+}
+
+extern "C" gist_status gist_adam_update_dev(gist_ctx* ctx, float* W, const float* dW, float* m,
+                                            float* v, int64_t n, float beta1, float beta2,
+                                            float eps, const float* coef_dev) {
+  gist::clear_error();
+  if (!ctx) return set_error(GIST_E_INVAL, "adam_update_dev: NULL ctx");
+  gist::ProfBind pb(ctx);
+  if (n < 0) return set_error(GIST_E_INVAL, "adam_update_dev: n < 0");
+  if (!(beta1 >= 0.f && beta1 < 1.f) || !(beta2 >= 0.f && beta2 < 1.f))
+    return set_error(GIST_E_INVAL, "adam_update_dev: beta outside [0, 1)");
+  if (!(eps >= 0.f) || !std::isfinite(eps))
+    return set_error(GIST_E_INVAL, "adam_update_dev: bad eps");
+  if (!coef_dev) return set_error(GIST_E_INVAL, "adam_update_dev: NULL coefficients");
+  if (n == 0) return GIST_OK;
+  if (!W || !dW || !m || !v) return set_error(GIST_E_INVAL, "adam_update_dev: NULL pointer");
+  gist::DeviceGuard dg(ctx->device);
+  return gist::adam(ctx->stream, W, dW, m, v, n, 0.f, 0.f, beta1, beta2, eps, false, coef_dev);
 }
 
 extern "C" gist_status gist_subagg(gist_ctx* ctx, float* Wg, int64_t ldg,

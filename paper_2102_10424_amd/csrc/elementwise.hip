@@ -69,11 +69,19 @@ __device__ __forceinline__ void adam_one(float& w, float g, float& m, float& v, 
   w = w - c.step_size * m / (sqrtf(v) * c.inv_sqrt_bc2 + c.eps);
 }
 
+// coef_dev (optional): {step_size, inv_sqrt_bc2, fresh} read from device
+// memory instead of the arguments, so that a replayed step advances them.
 template <bool VEC4>
 __global__ __launch_bounds__(kBlock) void adam_kernel(int64_t n, float* __restrict__ W,
                                                       const float* __restrict__ dW,
                                                       float* __restrict__ M, float* __restrict__ V,
-                                                      AdamCoef c, int fresh) {
+                                                      AdamCoef c, int fresh,
+                                                      const float* __restrict__ coef_dev) {
+  if (coef_dev) {
+    c.step_size = coef_dev[0];
+    c.inv_sqrt_bc2 = coef_dev[1];
+    fresh = coef_dev[2] != 0.f;
+  }
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
   const int64_t t0 = blockIdx.x * static_cast<int64_t>(kBlock) + threadIdx.x;
   if constexpr (VEC4) {
@@ -649,16 +657,16 @@ gist_status sgd(hipStream_t st, float* W, const float* dW, int64_t n, float lr) 
 
 gist_status adam(hipStream_t st, float* W, const float* dW, float* m, float* v, int64_t n,
                  float step_size, float inv_sqrt_bc2, float beta1, float beta2, float eps,
-                 bool fresh) {
+                 bool fresh, const float* coef_dev) {
   const AdamCoef c{step_size, inv_sqrt_bc2, beta1, beta2, eps};
   const bool vec = aligned16(W) && aligned16(dW) && aligned16(m) && aligned16(v);
   ProfScope ps(st, "adam_update", 0.0, (fresh ? 12.0 : 20.0) * static_cast<double>(n));
   if (vec)
     hipLaunchKernelGGL(adam_kernel<true>, dim3(grid_for((n + 3) / 4, kBlock, 8192)), dim3(kBlock), 0,
-                       st, n, W, dW, m, v, c, fresh ? 1 : 0);
+                       st, n, W, dW, m, v, c, fresh ? 1 : 0, coef_dev);
   else
     hipLaunchKernelGGL(adam_kernel<false>, dim3(grid_for(n, kBlock, 8192)), dim3(kBlock), 0, st, n,
-                       W, dW, m, v, c, fresh ? 1 : 0);
+                       W, dW, m, v, c, fresh ? 1 : 0, coef_dev);
   return check_launch("adam_update");
 }
 

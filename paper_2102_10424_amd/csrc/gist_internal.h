@@ -173,7 +173,7 @@ gist_status gat_gemv_t(hipStream_t st, int64_t n, int s, const float* P, int64_t
                        const float* du, const float* dv, float* da_src, float* da_dst, float* part);
 gist_status adam(hipStream_t st, float* W, const float* dW, float* m, float* v, int64_t n,
                  float step_size, float inv_sqrt_bc2, float beta1, float beta2, float eps,
-                 bool fresh);
+                 bool fresh, const float* coef_dev = nullptr);
 gist_status softmax_xent(hipStream_t st, int64_t n, int C, const float* logits,
                          const int32_t* labels, float* loss, float* dlogits,
                          float* partials, const int32_t* n_dev = nullptr);

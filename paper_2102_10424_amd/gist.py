@@ -60,7 +60,8 @@ EXPORTED = (
     "gist_gat_workspace_size", "gist_gat_layer_fwd", "gist_gat_layer_bwd",
     "gist_softmax_xent_workspace", "gist_softmax_xent", "gist_softmax_xent_padded",
     "gist_gather_slice",
-    "gist_sgd_update", "gist_adam_update", "gist_subagg", "gist_partition_inverse",
+    "gist_sgd_update", "gist_adam_update", "gist_adam_coefficients", "gist_adam_update_dev",
+    "gist_subagg", "gist_partition_inverse",
     "gist_subagg_gather", "gist_subagg_mean",
     "gist_profile_begin", "gist_profile_read", "gist_profile_end",
     "gist_capture_begin", "gist_capture_end", "gist_replay_launch", "gist_replay_destroy",
@@ -133,6 +134,10 @@ _sigs = {
     "gist_partition_inverse": (C.c_int, [C.c_int64, C.c_int32, _P, _P, _P]),
     "gist_adam_update": (C.c_int, [_P, _P, _P, _P, _P, C.c_int64, C.c_float, C.c_float, C.c_float,
                                    C.c_float, C.c_int64, C.c_uint32]),
+    "gist_adam_coefficients": (C.c_int, [C.c_float, C.c_float, C.c_float, C.c_float, C.c_int64,
+                                         C.c_uint32, _P]),
+    "gist_adam_update_dev": (C.c_int, [_P, _P, _P, _P, _P, C.c_int64, C.c_float, C.c_float,
+                                       C.c_float, _P]),
     "gist_subagg_gather": (C.c_int, [_P, _P, C.c_int64, C.c_int64, C.c_int64, C.c_int32,
                                      C.POINTER(gist_slice_set), C.POINTER(gist_slice_set)]),
     "gist_subagg_mean": (C.c_int, [_P, _P, C.c_int64, C.c_int64, C.c_int64, C.c_int32, _P,
@@ -451,6 +456,19 @@ def gist_adam_update(ctx, W, dW, m, v, n, lr, step, beta1=0.9, beta2=0.999, eps=
     _check(_lib.gist_adam_update(ctx.handle, _ptr(W), _ptr(dW), _ptr(m), _ptr(v), int(n),
                                  float(lr), float(beta1), float(beta2), float(eps), int(step),
                                  int(flags)))
+
+
+def gist_adam_coefficients(lr, step, beta1=0.9, beta2=0.999, eps=1e-8, flags=0):
+    """float32[3] {lr / (1 - beta1^k), 1 / sqrt(1 - beta2^k), fresh} for gist_adam_update_dev."""
+    out = np.empty(3, dtype=np.float32)
+    _check(_lib.gist_adam_coefficients(float(lr), float(beta1), float(beta2), float(eps),
+                                       int(step), int(flags), _ptr(out)))
+    return out
+
+
+def gist_adam_update_dev(ctx, W, dW, m, v, n, coef_dev, beta1=0.9, beta2=0.999, eps=1e-8):
+    _check(_lib.gist_adam_update_dev(ctx.handle, _ptr(W), _ptr(dW), _ptr(m), _ptr(v), int(n),
+                                     float(beta1), float(beta2), float(eps), _ptr(coef_dev)))
 
 
 def gat_desc(n, nnz, s_in, s_out, act, dtype=GIST_DTYPE_F32, slope=0.2):

@@ -188,7 +188,7 @@ class FixedBatchSlot:
     def fixed_layout(cls, sage, cap_n, cap_nnz):
         pad = lambda n: (int(n) + cls._ALIGN - 1) // cls._ALIGN * cls._ALIGN
         cnt = dict(rowptr=cap_n + 1, col=cap_nnz, val=cap_nnz, node_map=cap_n, labels=cap_n,
-                   n_valid=1)
+                   n_valid=1, coef=3)
         if sage:
             cnt.update(t_rowptr=cap_n + 1, t_col=cap_nnz, t_val=cap_nnz)
         off, o = 0, {}
@@ -197,8 +197,10 @@ class FixedBatchSlot:
             off += pad(c)
         return dict(off=o, total=off)
 
-    def build(self, graph_struct, clusters, labels_host):
-        """Host half: the batch into the fixed layout (after the last upload from it)."""
+    def build(self, graph_struct, clusters, labels_host, coef=None):
+        """Host half: the batch into the fixed layout (after the last upload from
+        it); ``coef`` (float32[3], ``gist_adam_coefficients``) rides along for a
+        replayed Adam step."""
         self.sync_s = _wait(self.uploaded)
         G.build_minibatch_into(graph_struct, clusters, self.norm, self.q)
         n, nnz = int(self.q.n), int(self.q.nnz)
@@ -211,6 +213,8 @@ class FixedBatchSlot:
         h[o["node_map"] + n:o["node_map"] + cap] = 0
         h[o["labels"] + n:o["labels"] + cap] = 0
         h[o["n_valid"]] = n
+        if coef is not None:
+            h[o["coef"]:o["coef"] + 3] = np.asarray(coef, dtype=np.float32).view(np.int32)
         self.n, self.nnz = n, nnz
 
     def upload(self, X_dev):
@@ -272,11 +276,13 @@ class BatchPipeline:
     def ladies(cls, ctx, L, b, s, max_degree, d_in, A_handle, X_dev, labels_host, items,
                depth=8, workers=4, fixed=False):
         """A pipeline of LADIES mini-batches; ``items`` yields (output nodes,
-        seed), or a callable returning them (evaluated on the worker thread)."""
+        seed[, Adam coefficients]), or a callable returning them (evaluated on
+        the worker thread)."""
         slots = [LadiesSlot(ctx, L, b, s, max_degree, d_in, fixed=fixed) for _ in range(depth)]
         def build(slot, item):
-            nodes, seed = item() if callable(item) else item
-            slot.build(A_handle, nodes, seed, labels_host)
+            item = item() if callable(item) else item
+            slot.build(A_handle, item[0], item[1], labels_host,
+                       coef=item[2] if len(item) > 2 else None)
         return cls(ctx, None, 0, 0, d_in, None, X_dev, labels_host, items, workers=workers,
                    slots=slots, build=build)
 
@@ -431,10 +437,13 @@ class LadiesSlot:
             layers.append(dict(n_out=n_out, n_in=n_in, nnz=nnz, off=o))
         lab = off
         off += cls._pad(b)
-        return dict(layers=layers, labels=lab, total=off)
+        coef = off
+        off += cls._pad(3)
+        return dict(layers=layers, labels=lab, coef=coef, total=off)
 
-    def build(self, A_handle, batch, seed, labels_host):
-        """Host half: sample the layers, pack them and the output nodes' labels."""
+    def build(self, A_handle, batch, seed, labels_host, coef=None):
+        """Host half: sample the layers, pack them and the output nodes' labels
+        (and, fixed layout, the Adam coefficients ``coef`` of a replayed step)."""
         self.sync_s = _wait(self.uploaded)   # the previous upload from packed_h is done
         batch = np.asarray(batch, dtype=np.int32)
         nb = batch.shape[0]
@@ -460,6 +469,9 @@ class LadiesSlot:
                     sizes.append((n_out, n_in, nnz))
                 lab = self.layout["labels"]
                 packed[lab:lab + nb] = labels_host[batch]
+                if coef is not None:
+                    c = self.layout["coef"]
+                    packed[c:c + 3] = np.asarray(coef, dtype=np.float32).view(np.int32)
                 self.built = (nb, sizes, offs, lab, self.layout["total"], True)
                 return
         # compact layout: sample into the staging arrays, pack what was produced
@@ -512,22 +524,72 @@ class LadiesSlot:
         return self.upload(X_dev)
 
 
-class ClusterGraphRunner:
+class _Replayer:
+    """Shared part of the replay runners: a side-stream context to record
+    on, and one recorded step per (parameter set, optimizer state, lr).
+
+    A step is recorded with SGD (its learning rate fixed in the recording),
+    or with Adam (``adam`` = (M, V) moment slices): then the coefficients
+    are read from the batch's device buffer (``gist_adam_update_dev``), so
+    the same recording serves every step k and both moment policies.
+    """
+
+    def _init_replay(self, ctx):
+        self.ctx = ctx
+        self.cap_stream = torch.cuda.Stream()
+        self.cap_ctx = G.Context(ctx.device, stream=self.cap_stream.cuda_stream)
+        self.replays = {}
+
+    def _update(self, params, lr, adam):
+        if adam is None:
+            self.run.sgd(params, lr)
+        else:
+            M, V = adam
+            self.run.adam_dev(params, M, V, self.coef_dev)
+
+    def _capture(self, params, lr, adam):
+        torch.cuda.synchronize()    # everything the recording reads exists and is written
+        G.gist_capture_begin(self.cap_ctx)
+        try:
+            self._body(params, lr, adam)
+        finally:
+            replay = G.gist_capture_end(self.cap_ctx)
+        return replay
+
+    def _replay(self, slot, params, lr, adam):
+        key = (tuple(p.data_ptr() for p in params),
+               None if adam is None else tuple(t.data_ptr() for m in adam for t in m),
+               None if adam is not None else float(lr))
+        r = self.replays.get(key)
+        if r is None:
+            r = self.replays[key] = self._capture(params, lr, adam)
+        G.gist_replay_launch(self.ctx, r, self.dev, slot.packed_h, self.nbytes, slot.event)
+        slot.uploaded = slot.event
+
+    @property
+    def graphs(self):
+        return self.replays
+
+    @property
+    def loss(self):
+        return self.run.loss
+
+
+class ClusterGraphRunner(_Replayer):
     """Sub-GCN steps on cluster mini-batches replayed from HIP graphs (the
     counterpart of :class:`LadiesGraphRunner` for GCN, SAGE and GAT layers).
 
     Every batch is run at the capacity shape of :class:`FixedBatchSlot` (n
     rows, nnz entries): the step (feature gather, forward, padded loss,
-    backward, SGD) is recorded once per parameter set and learning rate on
-    a side-stream context, and each step is one ``gist_replay_launch``
-    that pulls the batch from pinned memory into this runner's buffer.
+    backward, SGD or Adam) is recorded once per parameter set on a
+    side-stream context, and each step is one ``gist_replay_launch`` that
+    pulls the batch from pinned memory into this runner's buffer.
     """
 
     def __init__(self, ctx, kind, widths, cap_n, cap_nnz, d_in, X_dev, dtype=G.GIST_DTYPE_F32,
                  device="cuda"):
-        self.ctx, self.d_in, self.X_dev = ctx, d_in, X_dev
-        self.cap_stream = torch.cuda.Stream()
-        self.cap_ctx = G.Context(ctx.device, stream=self.cap_stream.cuda_stream)
+        self._init_replay(ctx)
+        self.d_in, self.X_dev = d_in, X_dev
         norm = "sage" if kind == "sage" else "gcn"
         self.layout = FixedBatchSlot.fixed_layout(norm == "sage", cap_n, cap_nnz)
         self.dev = torch.empty(self.layout["total"], dtype=torch.int32, device=device)
@@ -540,6 +602,7 @@ class ClusterGraphRunner:
             view.update(t_rowptr=d[o["t_rowptr"]:], t_col=d[o["t_col"]:],
                         t_val=d[o["t_val"]:o["t_val"] + cap_nnz].view(f32))
         self.node_map = d[o["node_map"]:o["node_map"] + cap_n]
+        self.coef_dev = d[o["coef"]:o["coef"] + 3].view(f32)
         self.X = torch.empty(cap_n, d_in, device=device)
         self.view = _View(cap_n, cap_nnz, view, self.X, norm == "sage")
         self.view.n_dev = d[o["n_valid"]:o["n_valid"] + 1]
@@ -547,40 +610,22 @@ class ClusterGraphRunner:
         self.run = SubGCN(self.cap_ctx, kind, widths, cap_n, dtype=dtype, device=device)
         self.run.prepare(self.view)
         self.nbytes = 4 * self.layout["total"]
-        self.replays = {}
 
-    def _body(self, params, lr):
+    def _body(self, params, lr, adam):
         G.gist_gather_slice(self.cap_ctx, self.X_dev, self.d_in, self.node_map, self.cap_n, None,
                             self.d_in, self.X, self.d_in)
         self.run.forward(self.view, params)
         self.run.loss_and_grad(self.view)
         self.run.backward(self.view, params)
-        self.run.sgd(params, lr)
+        self._update(params, lr, adam)
 
-    def _capture(self, params, lr):
-        torch.cuda.synchronize()
-        G.gist_capture_begin(self.cap_ctx)
-        try:
-            self._body(params, lr)
-        finally:
-            replay = G.gist_capture_end(self.cap_ctx)
-        return replay
-
-    def step(self, slot, params, lr):
-        """One sub-GCN step on the batch built in ``slot``."""
-        key = (tuple(p.data_ptr() for p in params), float(lr))
-        r = self.replays.get(key)
-        if r is None:
-            r = self.replays[key] = self._capture(params, lr)
-        G.gist_replay_launch(self.ctx, r, self.dev, slot.packed_h, self.nbytes, slot.event)
-        slot.uploaded = slot.event
-
-    @property
-    def loss(self):
-        return self.run.loss
+    def step(self, slot, params, lr, adam=None):
+        """One sub-GCN step on the batch built in ``slot``; ``adam`` = (M, V)
+        for Adam with the coefficients the slot carries."""
+        self._replay(slot, params, lr, adam)
 
 
-class LadiesGraphRunner:
+class LadiesGraphRunner(_Replayer):
     """Sub-GCN steps on LADIES mini-batches replayed from HIP graphs.
 
     A LADIES step is a few dozen small launches (c7: GEMMs of at most
@@ -589,18 +634,16 @@ class LadiesGraphRunner:
     (``gist_capture_begin`` / ``_end`` on a context of its own, on a side
     stream) at the fixed shapes of ``LadiesSlot(fixed=True)``: the feature
     gather, every layer's forward, the loss, every layer's backward and the
-    SGD update.  Per step the host then makes one library call,
+    update.  Per step the host then makes one library call,
     ``gist_replay_launch``: the copy of the batch into this runner's device
     buffer, an event that frees the slot, and the replay, on the stream of
-    ``ctx``.  A replay is kept per parameter set (the sub-GCN's slice
-    buffers) and learning rate.
+    ``ctx``.
     """
 
     def __init__(self, ctx, widths, L, b, s, d_in, X_dev, dtype=G.GIST_DTYPE_F32,
                  fixed_nnz_per_row=16, device="cuda"):
-        self.ctx, self.L, self.d_in, self.X_dev = ctx, L, d_in, X_dev
-        self.cap_stream = torch.cuda.Stream()
-        self.cap_ctx = G.Context(ctx.device, stream=self.cap_stream.cuda_stream)
+        self._init_replay(ctx)
+        self.L, self.d_in, self.X_dev = L, d_in, X_dev
         self.layout = LadiesSlot.fixed_layout(L, b, s, fixed_nnz_per_row)
         self.dev = torch.empty(self.layout["total"], dtype=torch.int32, device=device)
         lay = self.layout["layers"]
@@ -614,57 +657,38 @@ class LadiesGraphRunner:
             views.append(v)
         self.n0 = lay[0]["n_in"]
         self.X = torch.empty(self.n0, d_in, device=device)
-        lab = self.layout["labels"]
+        lab, c = self.layout["labels"], self.layout["coef"]
         self.view = LadiesView(sizes, views, self.X, self.dev[lab:lab + b])
+        self.coef_dev = self.dev[c:c + 3].view(torch.float32)
         self.nodes0 = views[0]["nodes"]
         self.run = SubGCN(self.cap_ctx, "gcn", widths, self.n0, dtype=dtype, device=device)
-        self.run._workspace(self.view)      # sized before any capture
+        self.run.prepare(self.view)
         self.nbytes = 4 * self.layout["total"]
-        self.replays = {}
 
-    def _body(self, params, lr):
+    def _body(self, params, lr, adam):
         G.gist_gather_slice(self.cap_ctx, self.X_dev, self.d_in, self.nodes0, self.n0, None,
                             self.d_in, self.X, self.d_in)
         self.run.forward(self.view, params)
         self.run.loss_and_grad(self.view)
         self.run.backward(self.view, params)
-        self.run.sgd(params, lr)
+        self._update(params, lr, adam)
 
-    def _capture(self, params, lr):
-        # everything the capture reads was allocated and written before it
-        torch.cuda.synchronize()
-        G.gist_capture_begin(self.cap_ctx)
-        try:
-            self._body(params, lr)
-        finally:
-            replay = G.gist_capture_end(self.cap_ctx)
-        return replay
-
-    def step(self, slot, params, lr):
+    def step(self, slot, params, lr, adam=None):
         """One sub-GCN step on the batch built in ``slot`` (fixed layout): one
         library call copies it into this runner's buffer and replays the step
-        (recorded on first use of these parameters)."""
-        key = (tuple(p.data_ptr() for p in params), float(lr))
+        (recorded on first use of these parameters).  ``adam`` = (M, V) for
+        Adam with the coefficients the slot carries."""
         if not slot.fits_fixed():    # rare: too many entries for the fixed layout
+            if adam is not None:
+                raise ValueError("a batch beyond the fixed layout cannot take a replayed "
+                                 "Adam step")
             self.cap_ctx.set_stream(torch.cuda.current_stream().cuda_stream)
             try:
                 self.run.step(slot.upload(self.X_dev), params, lr)
             finally:
                 self.cap_ctx.set_stream(self.cap_stream.cuda_stream)
             return
-        r = self.replays.get(key)
-        if r is None:
-            r = self.replays[key] = self._capture(params, lr)
-        G.gist_replay_launch(self.ctx, r, self.dev, slot.packed_h, self.nbytes, slot.event)
-        slot.uploaded = slot.event
-
-    @property
-    def graphs(self):
-        return self.replays
-
-    @property
-    def loss(self):
-        return self.run.loss
+        self._replay(slot, params, lr, adam)
 
 
 class LadiesView:
@@ -855,6 +879,13 @@ class SubGCN:
         for l in range(self.L):
             G.gist_adam_update(self.ctx, params[l], self.dW[l], M[l], V[l], params[l].numel(),
                                lr, step, betas[0], betas[1], eps, flags)
+
+    def adam_dev(self, params, M, V, coef_dev, betas=(0.9, 0.999), eps=1e-8):
+        """Adam with the step's coefficients read from the device buffer
+        ``coef_dev`` (``gist_adam_update_dev``): what a replayed step uses."""
+        for l in range(self.L):
+            G.gist_adam_update_dev(self.ctx, params[l], self.dW[l], M[l], V[l], params[l].numel(),
+                                   coef_dev, betas[0], betas[1], eps)
 
     def step(self, batch, params, lr, adam=None, loss_out=None):
         """``subTrain``: forward, loss, backward, update (all enqueued, nothing

@@ -391,3 +391,38 @@ def test_graph_runner_falls_back_when_the_layout_is_full(G, ctx):
     for a, b in zip(pg, pe):
         assert torch.equal(a, b)
     assert not gr.graphs
+
+
+def test_graph_runner_adam_replays_match_eager(G, ctx):
+    """LADIES steps replayed with Adam (the coefficients of steps 1..4 carried
+    by the batches, the 'reset' policy's fresh first step included): weights
+    and moments match eager gist_adam_update steps on the same batches."""
+    import torch
+    from paper_2102_10424_amd.step import LadiesGraphRunner, LadiesSlot, SubGCN
+    widths = (40, 64, 9)
+    w = _Workload(3000, 30, widths, 48, 160, seed=21)
+    Ah, Xd = G.CsrHandle(w.A), to_dev(w.X)
+    fixed = LadiesSlot(ctx, w.L, w.b, w.s, w.max_degree, widths[0], fixed=True)
+    plain = LadiesSlot(ctx, w.L, w.b, w.s, w.max_degree, widths[0])
+    gr = LadiesGraphRunner(ctx, widths, w.L, w.b, w.s, widths[0], Xd)
+    eager = SubGCN(ctx, "gcn", widths, 1)
+    pg = [to_dev(t.copy()) for t in w.theta]
+    pe = [to_dev(t.copy()) for t in w.theta]
+    Mg, Vg = [torch.full_like(t, 7.0) for t in pg], [torch.full_like(t, 7.0) for t in pg]
+    Me, Ve = [torch.full_like(t, 7.0) for t in pg], [torch.full_like(t, 7.0) for t in pg]
+    lr = 0.01
+    for k, (step, fresh) in enumerate([(1, True), (2, False), (3, False), (1, True)]):
+        key = 70 + k
+        log(f"ladies adam replay {k}: step {step} fresh {fresh}")
+        flags = G.GIST_ADAM_FRESH if fresh else 0
+        fixed.build(Ah, w.batch_nodes(key), key, w.y,
+                    coef=G.gist_adam_coefficients(lr, step, flags=flags))
+        gr.step(fixed, pg, lr, adam=(Mg, Vg))
+        eager.step(plain.load(Ah, w.batch_nodes(key), key, Xd, w.y), pe, lr,
+                   adam=(Me, Ve, step, fresh))
+        torch.cuda.synchronize()
+        for l in range(w.L):
+            assert relerr(to_host(pg[l]), to_host(pe[l])) <= 1e-5, (k, l)
+            assert relerr(to_host(Mg[l]), to_host(Me[l])) <= 1e-5, (k, l)
+            assert relerr(to_host(Vg[l]), to_host(Ve[l])) <= 1e-5, (k, l)
+    assert len(gr.graphs) == 1

@@ -244,12 +244,17 @@ def test_step_chained(G, ctx, name):
             assert e <= FP32_TOL and ew <= FP32_TOL
 
 
-@pytest.mark.parametrize("kind,norm", [("gcn", "gcn"), ("sage", "sage"), ("gat", "gcn")])
-def test_cluster_graph_runner_matches_eager_and_oracle(G, ctx, kind, norm):
+@pytest.mark.parametrize("kind,norm,opt", [("gcn", "gcn", "sgd"), ("sage", "sage", "sgd"),
+                                          ("gat", "gcn", "sgd"), ("gcn", "gcn", "adam"),
+                                          ("gat", "gcn", "adam")])
+def test_cluster_graph_runner_matches_eager_and_oracle(G, ctx, kind, norm, opt):
     """Sub-GCN steps on cluster mini-batches replayed from HIP graphs at the
     slots' capacity shapes (empty padded rows, the padded loss) against eager
-    steps on the same batches and the oracle's chained SGD steps; batches of
-    different sizes, two parameter sets, eager work between the replays."""
+    steps on the same batches, and (SGD) the oracle's chained steps; batches
+    of different sizes, two parameter sets, eager work between the replays.
+    With Adam the recorded step reads the coefficients of step k from the
+    batch (k = 1, 2, 3 per parameter set): weights and both moments match
+    the eager gist_adam_update steps."""
     import torch
     from gist_synth.graphs import sbm
     from oracle import minibatch as MB
@@ -273,28 +278,39 @@ def test_cluster_graph_runner_matches_eager_and_oracle(G, ctx, kind, norm):
     pg = [[to_dev(t.copy()) for t in theta] for _ in range(2)]
     pe = [[to_dev(t.copy()) for t in theta] for _ in range(2)]
     po = [[t.astype(np.float64) for t in theta] for _ in range(2)]
+    zeros = lambda: [[torch.zeros_like(t) for t in pg[0]] for _ in range(2)]
+    Mg, Vg, Me, Ve = zeros(), zeros(), zeros(), zeros()
     ns = set()
-    for k in range(5):
-        j = k % 2
+    lr = 0.05 if opt == "sgd" else 0.01
+    for k in range(6):
+        j, step = k % 2, k // 2 + 1
         clusters = np.sort(rng.choice(g.n_clusters, 1 + k % 5, replace=False)).astype(np.int32)
-        log(f"cluster replay {kind} step {k}: {len(clusters)} clusters")
-        fixed.build(gh, clusters, y)
+        log(f"cluster replay {kind} {opt} step {k}: {len(clusters)} clusters")
+        coef = G.gist_adam_coefficients(lr, step) if opt == "adam" else None
+        fixed.build(gh, clusters, y, coef=coef)
         ns.add(fixed.n)
-        gr.step(fixed, pg[j], 0.05)
+        gr.step(fixed, pg[j], lr, adam=(Mg[j], Vg[j]) if opt == "adam" else None)
         b = plain.load(gh, clusters, Xd, y)
-        eager.step(b, pe[j], 0.05)
+        eager.step(b, pe[j], lr, adam=(Me[j], Ve[j], step, False) if opt == "adam" else None)
         torch.cuda.synchronize()
+        for l in range(3):
+            g_, e_ = to_host(pg[j][l]), to_host(pe[j][l])
+            assert relerr(g_, e_) <= 1e-5, (k, l)
+            if opt == "adam":
+                assert relerr(to_host(Mg[j][l]), to_host(Me[j][l])) <= 1e-5, (k, l)
+                assert relerr(to_host(Vg[j][l]), to_host(Ve[j][l])) <= 1e-5, (k, l)
+        assert abs(float(to_host(gr.loss)[0]) - float(to_host(eager.loss)[0])) <= 1e-5
+        if opt != "sgd":
+            continue
         csr = MB.build(g, clusters, norm)
         nm = csr["node_map"]
         ref = [OG._pack(kind, OL_split(kind, t, widths[l])) for l, t in enumerate(po[j])]
-        st = OG.sub_gcn_step(kind, csr, X[nm], y[nm], ref, 0.05)
+        st = OG.sub_gcn_step(kind, csr, X[nm], y[nm], ref, lr)
         po[j] = [np.concatenate([np.atleast_2d(a) for a in OG._parts(kind, p)])
                  for p in st["params"]]
         assert abs(float(to_host(gr.loss)[0]) - st["loss"]) <= FP32_TOL * abs(st["loss"])
         for l in range(3):
-            g_, e_ = to_host(pg[j][l]), to_host(pe[j][l])
-            assert relerr(g_, e_) <= 1e-5, (k, l)
-            assert relerr(g_, po[j][l]) <= FP32_TOL, (k, l)
+            assert relerr(to_host(pg[j][l]), po[j][l]) <= FP32_TOL, (k, l)
     assert len(ns) > 1 and len(gr.replays) == 2
     # the fixed slot's own eager upload gives the same batch
     b = fixed.upload(Xd)
