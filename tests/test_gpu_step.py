@@ -312,9 +312,17 @@ def test_cluster_graph_runner_matches_eager_and_oracle(G, ctx, kind, norm, opt):
         for l in range(3):
             assert relerr(to_host(pg[j][l]), po[j][l]) <= FP32_TOL, (k, l)
     assert len(ns) > 1 and len(gr.replays) == 2
-    # the fixed slot's own eager upload gives the same batch
+    # the fixed slot's own eager upload (the bench's kernel-by-kernel path)
+    # gives the same batch: an eager step on it equals one on the plain slot
     b = fixed.upload(Xd)
     assert b.n == fixed.n and b.nnz == fixed.nnz
+    p1 = [to_dev(t.copy()) for t in theta]
+    p2 = [to_dev(t.copy()) for t in theta]
+    eager.step(b, p1, lr)
+    eager.step(plain.load(gh, clusters, Xd, y), p2, lr)   # the last batch again
+    torch.cuda.synchronize()
+    for a, c in zip(p1, p2):
+        assert torch.equal(a, c)
 
 
 def OL_split(kind, t, rows):
