@@ -13,6 +13,7 @@
  *   gist_ladies_sample         LADIES layer-sampled mini-batch (GCN)    (host)
  *   gist_gather_slice          Theta^(i) = Theta[D_in, D_out]           (device)
  *   gist_gcn_layer_fwd/_bwd    eq. (2) sub-GCN layer, GCN and SAGE-mean (device)
+ *   gist_gcn_layer_bwd_sgd     the backward pass with the SGD step fused   (device)
  *   gist_gat_layer_fwd/_bwd    the graph attention layer GIST also trains (device)
  *   gist_softmax_xent          loss and its gradient                    (device)
  *   gist_sgd_update            one SGD step                             (device)
@@ -307,6 +308,23 @@ gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* L,
                                const float* H_out, const float* W,
                                const float* dH_out, float* dW, float* dH,
                                void* ws, size_t ws_bytes);
+
+/* The same backward pass with subTrain's SGD step fused in (Algorithm 1; the
+ * update of gist_sgd_update): W <- W - lr dW in place, where dW is the
+ * weight gradient above, without writing dW anywhere.  The input gradient dH
+ * is formed from the weights before the step.  W and dH_out ... ws as in
+ * gist_gcn_layer_bwd (W is device memory, updated in place; every group's
+ * slice for G > 1).  Bitwise the same W and dH as gist_gcn_layer_bwd
+ * followed by gist_sgd_update(W, dW, lr): the GEMM writing the gradient
+ * applies fmaf(-lr, dW_ij, W_ij) to each element once, in its epilogue.
+ * Saves the gradient's write and the separate pass that reads it.  With no
+ * output rows (n == 0) W is unchanged.  Errors as gist_gcn_layer_bwd, and
+ * GIST_E_INVAL for a non-finite lr. */
+gist_status gist_gcn_layer_bwd_sgd(gist_ctx* ctx, const gist_layer_desc* L,
+                                   const gist_csr_dev* A, const gist_csr_dev* A_T,
+                                   const float* H, const float* agg_save,
+                                   const float* H_out, float* W, const float* dH_out,
+                                   float lr, float* dH, void* ws, size_t ws_bytes);
 
 /* ---- graph attention layer ------------------------------------------ */
 

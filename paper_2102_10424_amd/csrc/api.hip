@@ -363,38 +363,45 @@ extern "C" gist_status gist_gcn_layer_fwd(gist_ctx* ctx, const gist_layer_desc* 
   return spmm_out(st, y, A, n, T, y.gs_out_in, H_out, y.gs_out, relu);
 }
 
-extern "C" gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* L,
-                                          const gist_csr_dev* A, const gist_csr_dev* A_T,
-                                          const float* H, const float* agg_save,
-                                          const float* H_out, const float* W,
-                                          const float* dH_out, float* dW, float* dH,
-                                          void* ws, size_t ws_bytes) {
+namespace {
+
+// The backward pass of eq. (2).  W_sgd == nullptr: dW is written.  Else the
+// SGD step W_sgd <- W_sgd - lr dW is applied by the weight-gradient GEMM's
+// epilogue (W == W_sgd, dW == nullptr), after the input gradient has read W.
+gist_status layer_bwd(gist_ctx* ctx, const gist_layer_desc* L, const gist_csr_dev* A,
+                      const gist_csr_dev* A_T, const float* H, const float* agg_save,
+                      const float* H_out, const float* W, const float* dH_out, float* dW,
+                      float* W_sgd, float lr, float* dH, void* ws, size_t ws_bytes,
+                      const std::string& what) {
   gist::clear_error();
-  if (!ctx) return set_error(GIST_E_INVAL, "layer_bwd: NULL ctx");
+  if (!ctx) return set_error(GIST_E_INVAL, what + ": NULL ctx");
   gist::ProfBind pb(ctx);
   GIST_TRY(check_desc(L));
-  GIST_TRY(check_csr(A, L->n, "layer_bwd"));
+  GIST_TRY(check_csr(A, L->n, what.c_str()));
   const bool sage = L->kind == GIST_LAYER_SAGE_MEAN;
   const Lay y = layout(L);
   const int64_t n = y.n, n_in = y.n_in, si = y.si, so = y.so, G = y.G;
-  if (sage || n_in != n) GIST_TRY(check_csr(A_T, n_in, "layer_bwd (transpose)"));
-  else if (A_T) GIST_TRY(check_csr(A_T, n_in, "layer_bwd (transpose)"));
+  const std::string wt = what + " (transpose)";
+  if (sage || n_in != n) GIST_TRY(check_csr(A_T, n_in, wt.c_str()));
+  else if (A_T) GIST_TRY(check_csr(A_T, n_in, wt.c_str()));
   const int order = resolve_order(L);
   const bool relu = L->act == GIST_ACT_RELU;
-  if (!dW || !W) return set_error(GIST_E_INVAL, "layer_bwd: NULL dW or W");
+  const bool fused = W_sgd != nullptr;
+  if (!W || (!fused && !dW)) return set_error(GIST_E_INVAL, what + ": NULL dW or W");
+  if (fused && !std::isfinite(lr)) return set_error(GIST_E_INVAL, what + ": lr not finite");
   if (dH && y.shared)
-    return set_error(GIST_E_INVAL, "layer_bwd: a shared input has no per-group dH");
+    return set_error(GIST_E_INVAL, what + ": a shared input has no per-group dH");
   if (n > 0 && (!H || !dH_out || (relu && !H_out)))
-    return set_error(GIST_E_INVAL, "layer_bwd: NULL pointer");
+    return set_error(GIST_E_INVAL, what + ": NULL pointer");
   if (n > 0 && (sage || order == GIST_ORDER_AGG_FIRST) && !agg_save)
-    return set_error(GIST_E_INVAL, "layer_bwd: agg_save required");
+    return set_error(GIST_E_INVAL, what + ": agg_save required");
   const BwdPlan p = plan_bwd(L);
   if (ws_bytes < p.total() || (p.total() > 0 && !ws))
-    return set_error(GIST_E_NOMEM, "layer_bwd: workspace too small");
+    return set_error(GIST_E_NOMEM, what + ": workspace too small");
   gist::DeviceGuard dg(ctx->device);
   hipStream_t st = ctx->stream;
-  if (n == 0) {  // no output rows: zero gradients
-    GIST_TRY(gist::fill_zero(st, dW, G * y.wrows * so));
+  if (n == 0) {  // no output rows: zero gradients (a zero step leaves W as it is)
+    if (!fused) GIST_TRY(gist::fill_zero(st, dW, G * y.wrows * so));
     return dH && n_in > 0 ? gist::fill_zero(st, dH, n_in * G * si) : GIST_OK;
   }
   char* base = static_cast<char*>(ws);
@@ -414,8 +421,9 @@ extern "C" gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* 
 
   gist::Operand dz_as_b;  // dZ_g (n x s_out): B operand of the weight gradient, N = s_out, K = n
   dz_as_b.p0 = dZ; dz_as_b.ld0 = y.ld_out; dz_as_b.gs0 = y.gs_out; dz_as_b.k_major = false;
-  gist::GemmOut wout;
-  wout.c0 = dW; wout.ldc0 = so; wout.gs0 = y.gs_w;
+  gist::GemmOut wout;     // dW_g, or the SGD step on W_g
+  wout.c0 = fused ? W_sgd : dW; wout.ldc0 = so; wout.gs0 = y.gs_w;
+  wout.sgd = fused; wout.lr = lr;
   gist::Operand w_as_b;   // W_g^T as an N x K operand is W_g itself (rows = N, K contiguous)
   w_as_b.p0 = W; w_as_b.ld0 = so; w_as_b.gs0 = y.gs_w; w_as_b.k_major = true;
   const int64_t ld_p = G * si;   // dP: n x (G s_in); dH: n_in x (G s_in)
@@ -423,20 +431,21 @@ extern "C" gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* 
   if (sage || order == GIST_ORDER_AGG_FIRST) {
     // dW_g = [H_g | Abar H_g]^T dZ_g (SAGE) or (Abar H_g)^T dZ_g: element (r, k) of the
     // transposed activation is act[k * ld + r]
-    if (p.tdw) {   // node-contiguous copies: [H | Abar H]^T (wrows x n) and dZ^T (so x n)
-      const int64_t n4 = round4(n);
-      if (sage) {
-        GIST_TRY(gist::transpose(st, H, n, si, y.ld_in, tA, n4));
-        GIST_TRY(gist::transpose(st, agg_save, n, si, y.ld_in, tA + si * n4, n4));
-      } else {
-        GIST_TRY(gist::transpose(st, agg_save, n, si, y.ld_in, tA, n4));
+    auto weight_grad = [&]() -> gist_status {
+      if (p.tdw) {   // node-contiguous copies: [H | Abar H]^T (wrows x n) and dZ^T (so x n)
+        const int64_t n4 = round4(n);
+        if (sage) {
+          GIST_TRY(gist::transpose(st, H, n, si, y.ld_in, tA, n4));
+          GIST_TRY(gist::transpose(st, agg_save, n, si, y.ld_in, tA + si * n4, n4));
+        } else {
+          GIST_TRY(gist::transpose(st, agg_save, n, si, y.ld_in, tA, n4));
+        }
+        GIST_TRY(gist::transpose(st, dZ, n, so, y.ld_out, tB, n4));
+        gist::Operand at, bt;
+        at.p0 = tA; at.ld0 = n4; at.k_major = true;
+        bt.p0 = tB; bt.ld0 = n4; bt.k_major = true;
+        return gist::gemm(st, y.wrows, so, n, at, bt, wout, L->dtype, gws, gbytes, 1);
       }
-      GIST_TRY(gist::transpose(st, dZ, n, so, y.ld_out, tB, n4));
-      gist::Operand at, bt;
-      at.p0 = tA; at.ld0 = n4; at.k_major = true;
-      bt.p0 = tB; bt.ld0 = n4; bt.k_major = true;
-      GIST_TRY(gist::gemm(st, y.wrows, so, n, at, bt, wout, L->dtype, gws, gbytes, 1));
-    } else {
       gist::Operand a;
       a.k_major = false;
       if (sage) {
@@ -445,48 +454,86 @@ extern "C" gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* 
       } else {
         a.p0 = agg_save; a.ld0 = y.ld_in; a.gs0 = y.gs_in;
       }
-      GIST_TRY(gist::gemm(st, y.wrows, so, n, a, dz_as_b, wout, L->dtype, gws, gbytes, G));
+      return gist::gemm(st, y.wrows, so, n, a, dz_as_b, wout, L->dtype, gws, gbytes, G);
+    };
+    auto input_grad = [&]() -> gist_status {
+      if (!dH) return GIST_OK;
+      // [dH_self | dP]_g = dZ_g W_g^T (SAGE), dP_g = dZ_g W_g^T (GCN)
+      gist::Operand a2;
+      a2.p0 = dZ; a2.ld0 = y.ld_out; a2.gs0 = y.gs_out; a2.k_major = true;
+      gist::GemmOut o2;
+      if (sage) {
+        o2.c0 = dH; o2.ldc0 = ld_p; o2.gs0 = si;
+        o2.c1 = tmp; o2.ldc1 = ld_p; o2.gs1 = si; o2.c_split = si;
+      } else {
+        o2.c0 = tmp; o2.ldc0 = ld_p; o2.gs0 = si;
+      }
+      GIST_TRY(gist::gemm(st, n, y.wrows, so, a2, w_as_b, o2, L->dtype, gws, gbytes, G));
+      // dH (+)= Abar^T dP, every group at once
+      return gist::spmm(st, n_in, AT->nnz, AT->rowptr, AT->col, AT->val, tmp, ld_p, int(ld_p),
+                        dH, ld_p, sage ? dH : nullptr, ld_p, false);
+    };
+    if (fused) {
+      GIST_TRY(input_grad());
+      return weight_grad();
     }
-    if (!dH) return GIST_OK;
-    // [dH_self | dP]_g = dZ_g W_g^T (SAGE), dP_g = dZ_g W_g^T (GCN)
-    gist::Operand a2;
-    a2.p0 = dZ; a2.ld0 = y.ld_out; a2.gs0 = y.gs_out; a2.k_major = true;
-    gist::GemmOut o2;
-    if (sage) {
-      o2.c0 = dH; o2.ldc0 = ld_p; o2.gs0 = si;
-      o2.c1 = tmp; o2.ldc1 = ld_p; o2.gs1 = si; o2.c_split = si;
-    } else {
-      o2.c0 = tmp; o2.ldc0 = ld_p; o2.gs0 = si;
-    }
-    GIST_TRY(gist::gemm(st, n, y.wrows, so, a2, w_as_b, o2, L->dtype, gws, gbytes, G));
-    // dH (+)= Abar^T dP, every group at once
-    return gist::spmm(st, n_in, AT->nnz, AT->rowptr, AT->col, AT->val, tmp, ld_p, int(ld_p), dH,
-                      ld_p, sage ? dH : nullptr, ld_p, false);
+    GIST_TRY(weight_grad());
+    return input_grad();
   }
   // GCN transform-first: T = Abar^T dZ (n_in rows, laid out like dZ); dW_g = H_g^T T_g;
   // dH_g = T_g W_g^T
   GIST_TRY(spmm_out(st, y, AT, n_in, dZ, y.gs_out, tmp, y.gs_out_in, false));
-  if (p.tdw) {   // node-contiguous copies H^T (si x n_in) and T^T (so x n_in)
-    const int64_t n4 = round4(n_in);
-    GIST_TRY(gist::transpose(st, H, n_in, si, y.ld_in, tA, n4));
-    GIST_TRY(gist::transpose(st, tmp, n_in, so, y.ld_out, tB, n4));
-    gist::Operand at, bt;
-    at.p0 = tA; at.ld0 = n4; at.k_major = true;
-    bt.p0 = tB; bt.ld0 = n4; bt.k_major = true;
-    GIST_TRY(gist::gemm(st, si, so, n_in, at, bt, wout, L->dtype, gws, gbytes, 1));
-  } else {
+  auto weight_grad = [&]() -> gist_status {
+    if (p.tdw) {   // node-contiguous copies H^T (si x n_in) and T^T (so x n_in)
+      const int64_t n4 = round4(n_in);
+      GIST_TRY(gist::transpose(st, H, n_in, si, y.ld_in, tA, n4));
+      GIST_TRY(gist::transpose(st, tmp, n_in, so, y.ld_out, tB, n4));
+      gist::Operand at, bt;
+      at.p0 = tA; at.ld0 = n4; at.k_major = true;
+      bt.p0 = tB; bt.ld0 = n4; bt.k_major = true;
+      return gist::gemm(st, si, so, n_in, at, bt, wout, L->dtype, gws, gbytes, 1);
+    }
     gist::Operand a;
     a.p0 = H; a.ld0 = y.ld_in; a.gs0 = y.gs_in; a.k_major = false;
     gist::Operand g;
     g.p0 = tmp; g.ld0 = y.ld_out; g.gs0 = y.gs_out_in; g.k_major = false;
-    GIST_TRY(gist::gemm(st, si, so, n_in, a, g, wout, L->dtype, gws, gbytes, G));
+    return gist::gemm(st, si, so, n_in, a, g, wout, L->dtype, gws, gbytes, G);
+  };
+  auto input_grad = [&]() -> gist_status {
+    if (!dH) return GIST_OK;
+    gist::Operand a2;
+    a2.p0 = tmp; a2.ld0 = y.ld_out; a2.gs0 = y.gs_out_in; a2.k_major = true;
+    gist::GemmOut o2;
+    o2.c0 = dH; o2.ldc0 = ld_p; o2.gs0 = si;
+    return gist::gemm(st, n_in, si, so, a2, w_as_b, o2, L->dtype, gws, gbytes, G);
+  };
+  if (fused) {
+    GIST_TRY(input_grad());
+    return weight_grad();
   }
-  if (!dH) return GIST_OK;
-  gist::Operand a2;
-  a2.p0 = tmp; a2.ld0 = y.ld_out; a2.gs0 = y.gs_out_in; a2.k_major = true;
-  gist::GemmOut o2;
-  o2.c0 = dH; o2.ldc0 = ld_p; o2.gs0 = si;
-  return gist::gemm(st, n_in, si, so, a2, w_as_b, o2, L->dtype, gws, gbytes, G);
+  GIST_TRY(weight_grad());
+  return input_grad();
+}
+
+}  // namespace
+
+extern "C" gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* L,
+                                          const gist_csr_dev* A, const gist_csr_dev* A_T,
+                                          const float* H, const float* agg_save,
+                                          const float* H_out, const float* W,
+                                          const float* dH_out, float* dW, float* dH,
+                                          void* ws, size_t ws_bytes) {
+  return layer_bwd(ctx, L, A, A_T, H, agg_save, H_out, W, dH_out, dW, nullptr, 0.f, dH, ws,
+                   ws_bytes, "layer_bwd");
+}
+
+extern "C" gist_status gist_gcn_layer_bwd_sgd(gist_ctx* ctx, const gist_layer_desc* L,
+                                              const gist_csr_dev* A, const gist_csr_dev* A_T,
+                                              const float* H, const float* agg_save,
+                                              const float* H_out, float* W, const float* dH_out,
+                                              float lr, float* dH, void* ws, size_t ws_bytes) {
+  return layer_bwd(ctx, L, A, A_T, H, agg_save, H_out, W, dH_out, nullptr, W, lr, dH, ws,
+                   ws_bytes, "layer_bwd_sgd");
 }
 
 // ---------------------------------------------------------------------------

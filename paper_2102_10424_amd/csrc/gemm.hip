@@ -73,6 +73,8 @@ struct OutDev {
   int64_t ldc0, ldc1, c_split;
   int relu;
   int64_t gs0, gs1;
+  int sgd;     // C <- fmaf(-lr, product, C): a fused SGD step on weights in C
+  float lr;
 
   __device__ __forceinline__ OutDev group(int64_t g) const {
     OutDev o = *this;
@@ -264,10 +266,15 @@ struct Sched {
   int64_t tpg;      // tiles per group (tiles_m * tiles_n)
 };
 
+__device__ __forceinline__ float* out_ptr(const OutDev& C, int64_t row, int64_t col) {
+  return col < C.c_split ? C.c0 + row * C.ldc0 + col : C.c1 + row * C.ldc1 + (col - C.c_split);
+}
+
 __device__ __forceinline__ void store_out(const OutDev& C, int64_t row, int64_t col, float v) {
   if (C.relu) v = fmaxf(v, 0.f);
-  if (col < C.c_split) C.c0[row * C.ldc0 + col] = v;
-  else C.c1[row * C.ldc1 + (col - C.c_split)] = v;
+  float* p = out_ptr(C, row, col);
+  if (C.sgd) v = fmaf(-C.lr, v, *p);
+  *p = v;
 }
 
 // Two resident blocks per CU where that fits in registers without spilling
@@ -464,6 +471,23 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
         for (int b = 0; b < 2; ++b) {
           const int64_t col = n0 + wn * 64 + b * 32 + li;
           if (col >= N) continue;
+          if (Cg.sgd) {
+            // fused SGD step: the sub-tile's 16 weights are read before any is
+            // written (one memory latency, not sixteen; reading the next
+            // sub-tile's ahead would need registers these kernels lack)
+            float w[16];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int64_t row = m0 + wm * 64 + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+              w[r] = row < M ? *out_ptr(Cg, row, col) : 0.f;
+            }
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int64_t row = m0 + wm * 64 + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+              if (row < M) *out_ptr(Cg, row, col) = fmaf(-Cg.lr, acc[a][b][r], w[r]);
+            }
+            continue;
+          }
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int64_t row = m0 + wm * 64 + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
@@ -607,7 +631,8 @@ gist_status gemm(hipStream_t st, int64_t M, int64_t N, int64_t K, const Operand&
                  const Operand& B, const GemmOut& C, int dtype, void* ws, size_t ws_bytes,
                  int64_t ngroups) {
   if (M <= 0 || N <= 0 || ngroups <= 0) return GIST_OK;
-  OutDev c{C.c0, C.c1, C.ldc0, C.ldc1, C.c_split, C.relu ? 1 : 0, C.gs0, C.gs1};
+  OutDev c{C.c0, C.c1, C.ldc0, C.ldc1, C.c_split, C.relu ? 1 : 0, C.gs0, C.gs1,
+           C.sgd ? 1 : 0, C.lr};
   if (K <= 0) return set_error(GIST_E_UNSUPPORTED, "gemm: K == 0");
   if (dtype == GIST_DTYPE_BF16_IN && gemm_bf16_packed_eligible(M, N, K)) {
     // the packed path converts each group's operands; groups run in turn

@@ -232,7 +232,34 @@ __global__ __launch_bounds__(kThr) void gemm_bf16_kernel(int64_t M, int64_t N,
 
   // acc[a][b] register r of lane l: tile row wm*128 + a*32 + 8(r/4) +
   // 4(l/32) + r%4, tile column wn*64 + b*32 + l%32
-  if (S.split == 1) {
+  if (S.split == 1 && C.sgd) {
+    // fused SGD step, C <- fmaf(-lr, acc, C): the weights of the next 32 x 32
+    // sub-tile are read while the current one is written, so a tile waits for
+    // memory once, not once per weight
+    float w[2][16];
+    auto fetch = [&](int t, float (&dst)[16]) {
+      const int a = t >> 1, b = t & 1;
+      const int64_t col = n0 + wn * 64 + b * 32 + li;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = m0 + wm * 128 + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+        dst[r] = (row < M && col < N) ? *C.ptr<SPLIT_OUT>(row, col) : 0.f;
+      }
+    };
+    fetch(0, w[0]);
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      if (t + 1 < 8) fetch(t + 1, w[(t + 1) & 1]);
+      const int a = t >> 1, b = t & 1;
+      const int64_t col = n0 + wn * 64 + b * 32 + li;
+      if (col >= N) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = m0 + wm * 128 + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+        if (row < M) *C.ptr<SPLIT_OUT>(row, col) = fmaf(-C.lr, acc[a][b][r], w[t & 1][r]);
+      }
+    }
+  } else if (S.split == 1) {
 #pragma unroll
     for (int a = 0; a < 4; ++a)
 #pragma unroll

@@ -38,21 +38,29 @@ struct OpView {
   }
 };
 
-// Device view of a GemmOut: optional ReLU, columns >= c_split go to c1.
+// Device view of a GemmOut: optional ReLU, columns >= c_split go to c1,
+// optional fused SGD step (C <- fmaf(-lr, product, C)).
 struct OutView {
   float* c0;
   float* c1;
   int64_t ldc0, ldc1, c_split;
   int relu;
+  int sgd;
+  float lr;
 
   static OutView from(const GemmOut& c) {
-    return OutView{c.c0, c.c1, c.ldc0, c.ldc1, c.c_split, c.relu ? 1 : 0};
+    return OutView{c.c0, c.c1, c.ldc0, c.ldc1, c.c_split, c.relu ? 1 : 0, c.sgd ? 1 : 0, c.lr};
+  }
+  template <bool SPLIT>
+  __device__ __forceinline__ float* ptr(int64_t row, int64_t col) const {
+    return (SPLIT && col >= c_split) ? c1 + row * ldc1 + (col - c_split) : c0 + row * ldc0 + col;
   }
   template <bool SPLIT>
   __device__ __forceinline__ void store(int64_t row, int64_t col, float v) const {
     if (relu) v = fmaxf(v, 0.f);
-    if (SPLIT && col >= c_split) c1[row * ldc1 + (col - c_split)] = v;
-    else c0[row * ldc0 + col] = v;
+    float* p = ptr<SPLIT>(row, col);
+    if (sgd) v = fmaf(-lr, v, *p);
+    *p = v;
   }
 };
 

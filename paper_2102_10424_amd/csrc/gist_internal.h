@@ -113,6 +113,10 @@ struct Operand {
 
 // C (M x N) = act(A (M x K) * B (K x N)), with B given as an N x K operand.
 // Columns >= c_split go to C1 (column index minus c_split).
+// `sgd`: C holds weights that take one SGD step with the product as their
+// gradient, C <- fmaf(-lr, A B, C) (gist_sgd_update's arithmetic), instead of
+// C <- A B; every element of C is written exactly once, so the step is
+// applied once.
 struct GemmOut {
   float* c0 = nullptr;
   float* c1 = nullptr;
@@ -120,6 +124,8 @@ struct GemmOut {
   int64_t c_split = INT64_MAX;
   bool relu = false;
   int64_t gs0 = 0, gs1 = 0;   // element offsets of c0 / c1 between GEMM groups
+  bool sgd = false;
+  float lr = 0.f;
 };
 
 // `groups` independent products of the same shape: group g reads A and B

@@ -57,6 +57,7 @@ EXPORTED = (
     "gist_last_error", "gist_status_str", "gist_create", "gist_destroy",
     "gist_set_stream", "gist_partition", "gist_build_minibatch_csr", "gist_ladies_sample",
     "gist_layer_workspace_size", "gist_gcn_layer_fwd", "gist_gcn_layer_bwd",
+    "gist_gcn_layer_bwd_sgd",
     "gist_gat_workspace_size", "gist_gat_layer_fwd", "gist_gat_layer_bwd",
     "gist_softmax_xent_workspace", "gist_softmax_xent", "gist_softmax_xent_padded",
     "gist_gather_slice",
@@ -165,6 +166,9 @@ _sigs = {
     "gist_gcn_layer_bwd": (C.c_int, [_P, C.POINTER(gist_layer_desc), C.POINTER(gist_csr_dev),
                                      C.POINTER(gist_csr_dev), _P, _P, _P, _P, _P, _P, _P, _P,
                                      C.c_size_t]),
+    "gist_gcn_layer_bwd_sgd": (C.c_int, [_P, C.POINTER(gist_layer_desc),
+                                         C.POINTER(gist_csr_dev), C.POINTER(gist_csr_dev),
+                                         _P, _P, _P, _P, _P, C.c_float, _P, _P, C.c_size_t]),
     "gist_softmax_xent_workspace": (C.c_size_t, [C.c_int64]),
     "gist_softmax_xent": (C.c_int, [_P, C.c_int64, C.c_int32, _P, _P, _P, _P, _P, C.c_size_t]),
     "gist_softmax_xent_padded": (C.c_int, [_P, C.c_int64, C.c_int32, _P, _P, _P, _P, _P, _P,
@@ -423,6 +427,14 @@ def gist_gcn_layer_bwd(ctx, desc, A, A_T, H, agg_save, H_out, W, dH_out, dW, dH,
                                    C.byref(A_T) if A_T is not None else None, _ptr(H),
                                    _ptr(agg_save), _ptr(H_out), _ptr(W), _ptr(dH_out),
                                    _ptr(dW), _ptr(dH), _ptr(ws), _nbytes(ws)))
+
+
+def gist_gcn_layer_bwd_sgd(ctx, desc, A, A_T, H, agg_save, H_out, W, dH_out, lr, dH, ws):
+    """Backward pass with the SGD step fused: W <- W - lr dW in place, no dW."""
+    _check(_lib.gist_gcn_layer_bwd_sgd(ctx.handle, C.byref(desc), C.byref(A),
+                                       C.byref(A_T) if A_T is not None else None, _ptr(H),
+                                       _ptr(agg_save), _ptr(H_out), _ptr(W), _ptr(dH_out),
+                                       float(lr), _ptr(dH), _ptr(ws), _nbytes(ws)))
 
 
 def gist_softmax_xent_workspace(n):

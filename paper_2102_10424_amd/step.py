@@ -540,10 +540,13 @@ class _Replayer:
         self.cap_ctx = G.Context(ctx.device, stream=self.cap_stream.cuda_stream)
         self.replays = {}
 
-    def _update(self, params, lr, adam):
+    def _backward_update(self, view, params, lr, adam):
+        """The recorded backward pass and update: SGD fused into the backward
+        pass, or Adam with the batch's coefficients."""
         if adam is None:
-            self.run.sgd(params, lr)
+            self.run.backward(view, params, sgd_lr=lr)
         else:
+            self.run.backward(view, params)
             M, V = adam
             self.run.adam_dev(params, M, V, self.coef_dev)
 
@@ -616,8 +619,7 @@ class ClusterGraphRunner(_Replayer):
                             self.d_in, self.X, self.d_in)
         self.run.forward(self.view, params)
         self.run.loss_and_grad(self.view)
-        self.run.backward(self.view, params)
-        self._update(params, lr, adam)
+        self._backward_update(self.view, params, lr, adam)
 
     def step(self, slot, params, lr, adam=None):
         """One sub-GCN step on the batch built in ``slot``; ``adam`` = (M, V)
@@ -670,8 +672,7 @@ class LadiesGraphRunner(_Replayer):
                             self.d_in, self.X, self.d_in)
         self.run.forward(self.view, params)
         self.run.loss_and_grad(self.view)
-        self.run.backward(self.view, params)
-        self._update(params, lr, adam)
+        self._backward_update(self.view, params, lr, adam)
 
     def step(self, slot, params, lr, adam=None):
         """One sub-GCN step on the batch built in ``slot`` (fixed layout): one
@@ -847,7 +848,12 @@ class SubGCN:
             self.alpha = [torch.empty(self.nnz_cap, device=self.device) for _ in range(self.L)]
         self._workspace(batch)
 
-    def backward(self, batch, params):
+    def backward(self, batch, params, sgd_lr=None):
+        """Every layer's backward pass into ``self.dW``; with ``sgd_lr`` also
+        the SGD step: a GCN / SAGE layer then takes it inside its backward
+        pass (``gist_gcn_layer_bwd_sgd``: the weight-gradient GEMM updates
+        the slice in place, after the input gradient has read it; no dW),
+        a GAT layer after the pass (``gist_sgd_update``)."""
         nnz = batch.nnz
         ws = self._workspace(batch)
         dout = self.dlogits[:batch.rows(self.L)]
@@ -862,11 +868,17 @@ class SubGCN:
                 G.gist_gat_layer_bwd(self.ctx, self._ldesc(batch, l), A, Hin,
                                      self.agg[l][:n], self.alpha[l][:nnz], self.H[l + 1][:n],
                                      W, a1, a2, dout, gW, g1, g2, dH, ws)
+            elif sgd_lr is not None:
+                G.gist_gcn_layer_bwd_sgd(self.ctx, self._ldesc(batch, l), A, A_T, Hin,
+                                         self.agg[l][:n], self.H[l + 1][:n], params[l], dout,
+                                         sgd_lr, dH, ws)
             else:
                 G.gist_gcn_layer_bwd(self.ctx, self._ldesc(batch, l), A, A_T, Hin,
                                      self.agg[l][:n], self.H[l + 1][:n], params[l], dout,
                                      self.dW[l], dH, ws)
             dout = dH
+        if sgd_lr is not None and self.gat:
+            self.sgd(params, sgd_lr)
 
     def sgd(self, params, lr):
         for l in range(self.L):
@@ -892,10 +904,10 @@ class SubGCN:
         synced).  ``adam`` = (M, V, step, fresh) selects Adam, else SGD."""
         self.forward(batch, params)
         self.loss_and_grad(batch, loss_out)
-        self.backward(batch, params)
         if adam is None:
-            self.sgd(params, lr)
+            self.backward(batch, params, sgd_lr=lr)
         else:
+            self.backward(batch, params)
             M, V, k, fresh = adam
             self.adam(params, M, V, lr, k, fresh)
 
@@ -991,16 +1003,23 @@ class SubGCNBatch:
             G.gist_softmax_xent(self.ctx, n, C, logits[i], batch.labels, self.loss[i:i + 1],
                                 dlogits[i], self.loss_ws)
 
-    def backward(self, batch, params):
+    def backward(self, batch, params, sgd_lr=None):
+        """Every layer's backward pass into ``self.dW``, or with ``sgd_lr`` the
+        SGD step fused into it (``gist_gcn_layer_bwd_sgd``, all m slices)."""
         n = batch.n
         ws = self._workspace(n)
         dout = self._gm(self._dlogits, n)
         for l in reversed(range(self.L)):
             Hin = batch.X if l == 0 else self.H[l][:n]
             dH = self.dH[l][:n] if l > 0 else None
-            G.gist_gcn_layer_bwd(self.ctx, self.desc(l, n), batch.A, batch.A_T, Hin,
-                                 self.agg[l][:n], self._out(l, n), params[l], dout,
-                                 self.dW[l], dH, ws)
+            if sgd_lr is not None:
+                G.gist_gcn_layer_bwd_sgd(self.ctx, self.desc(l, n), batch.A, batch.A_T, Hin,
+                                         self.agg[l][:n], self._out(l, n), params[l], dout,
+                                         sgd_lr, dH, ws)
+            else:
+                G.gist_gcn_layer_bwd(self.ctx, self.desc(l, n), batch.A, batch.A_T, Hin,
+                                     self.agg[l][:n], self._out(l, n), params[l], dout,
+                                     self.dW[l], dH, ws)
             dout = dH
 
     def step(self, batch, params, lr, adam=None):
@@ -1008,14 +1027,14 @@ class SubGCNBatch:
         Adam with ``adam`` = (M, V, step, fresh) over the stacked moments."""
         self.forward(batch, params)
         self.loss_and_grad(batch)
+        if adam is None:
+            self.backward(batch, params, sgd_lr=lr)
+            return
         self.backward(batch, params)
+        M, V, k, fresh = adam
         for l in range(self.L):
-            if adam is None:
-                G.gist_sgd_update(self.ctx, params[l], self.dW[l], params[l].numel(), lr)
-            else:
-                M, V, k, fresh = adam
-                G.gist_adam_update(self.ctx, params[l], self.dW[l], M[l], V[l], params[l].numel(),
-                                   lr, k, flags=G.GIST_ADAM_FRESH if fresh else 0)
+            G.gist_adam_update(self.ctx, params[l], self.dW[l], M[l], V[l], params[l].numel(),
+                               lr, k, flags=G.GIST_ADAM_FRESH if fresh else 0)
 
 
 class GistModel:

@@ -167,18 +167,29 @@ def test_batched_step_matches_oracle(G, ctx, kind):
     b = slot.load(G.GraphHandle(g), clusters, to_dev(X), y)
     runner = SubGCNBatch(ctx, kind, s, m, b.n)
     params = [to_dev(np.stack([P[i][l] for i in range(m)])) for l in range(L)]   # [m][rows][cols]
-    runner.step(b, params, 0.05)
+    # the gradients (a full SGD step fuses its update into the backward pass
+    # and keeps none), then the full step on a second copy of the weights
+    runner.forward(b, params)
+    runner.loss_and_grad(b)
+    runner.backward(b, params)
+    stepped = [p.clone() for p in params]
+    torch.cuda.synchronize()
+    losses = to_host(runner.loss)
+    logits = [to_host(runner.logits(i)) for i in range(m)]
+    grads = [to_host(runner.dW[L - 1][i]) for i in range(m)]
+    runner.step(b, stepped, 0.05)
     torch.cuda.synchronize()
     csr = MB.build(g, clusters, norm)
     nm = csr["node_map"]
-    losses = to_host(runner.loss)
     for i in range(m):
         pi = [p if kind == "gcn" else (p[:s[l]], p[s[l]:]) for l, p in enumerate(P[i])]
         ref = OG.sub_gcn_step(kind, csr, X[nm], y[nm], pi, 0.05)
         assert abs(losses[i] - ref["loss"]) <= FP32_TOL * abs(ref["loss"])
-        logits = runner.logits(i)
-        assert relerr(to_host(logits), ref["H"][L]) <= FP32_TOL
+        assert relerr(logits[i], ref["H"][L]) <= FP32_TOL
         gl = ref["grads"][L - 1]
         want = gl if kind == "gcn" else np.concatenate(gl)
-        assert relerr(to_host(runner.dW[L - 1][i]), want) <= FP32_TOL
+        assert relerr(grads[i], want) <= FP32_TOL
+        pl = ref["params"][L - 1]
+        assert relerr(to_host(stepped[L - 1][i]), pl if kind == "gcn" else np.concatenate(pl)) \
+            <= FP32_TOL
         log(f"  sub-GCN {i}: loss {losses[i]:.6f} (oracle {ref['loss']:.6f})")
