@@ -850,10 +850,13 @@ class SubGCN:
 
     def backward(self, batch, params, sgd_lr=None):
         """Every layer's backward pass into ``self.dW``; with ``sgd_lr`` also
-        the SGD step: a GCN / SAGE layer then takes it inside its backward
-        pass (``gist_gcn_layer_bwd_sgd``: the weight-gradient GEMM updates
-        the slice in place, after the input gradient has read it; no dW),
-        a GAT layer after the pass (``gist_sgd_update``)."""
+        the SGD step.  With bf16-input GEMMs a GCN / SAGE layer takes it
+        inside its backward pass (``gist_gcn_layer_bwd_sgd``: the
+        weight-gradient GEMM updates the slice in place, after the input
+        gradient has read it; no dW); otherwise after the pass
+        (``gist_sgd_update``): in fp32 the fused epilogue's extra weight
+        reads cost as much as the separate pass."""
+        fused = sgd_lr is not None and not self.gat and self.dtype == G.GIST_DTYPE_BF16_IN
         nnz = batch.nnz
         ws = self._workspace(batch)
         dout = self.dlogits[:batch.rows(self.L)]
@@ -868,7 +871,7 @@ class SubGCN:
                 G.gist_gat_layer_bwd(self.ctx, self._ldesc(batch, l), A, Hin,
                                      self.agg[l][:n], self.alpha[l][:nnz], self.H[l + 1][:n],
                                      W, a1, a2, dout, gW, g1, g2, dH, ws)
-            elif sgd_lr is not None:
+            elif fused:
                 G.gist_gcn_layer_bwd_sgd(self.ctx, self._ldesc(batch, l), A, A_T, Hin,
                                          self.agg[l][:n], self.H[l + 1][:n], params[l], dout,
                                          sgd_lr, dH, ws)
@@ -877,7 +880,7 @@ class SubGCN:
                                      self.agg[l][:n], self.H[l + 1][:n], params[l], dout,
                                      self.dW[l], dH, ws)
             dout = dH
-        if sgd_lr is not None and self.gat:
+        if sgd_lr is not None and not fused:
             self.sgd(params, sgd_lr)
 
     def sgd(self, params, lr):
@@ -1004,15 +1007,17 @@ class SubGCNBatch:
                                 dlogits[i], self.loss_ws)
 
     def backward(self, batch, params, sgd_lr=None):
-        """Every layer's backward pass into ``self.dW``, or with ``sgd_lr`` the
-        SGD step fused into it (``gist_gcn_layer_bwd_sgd``, all m slices)."""
+        """Every layer's backward pass into ``self.dW``, and with ``sgd_lr`` the
+        SGD step: fused into it with bf16-input GEMMs (``gist_gcn_layer_bwd_sgd``,
+        all m slices), after it in fp32 (as ``SubGCN.backward``)."""
+        fused = sgd_lr is not None and self.dtype == G.GIST_DTYPE_BF16_IN
         n = batch.n
         ws = self._workspace(n)
         dout = self._gm(self._dlogits, n)
         for l in reversed(range(self.L)):
             Hin = batch.X if l == 0 else self.H[l][:n]
             dH = self.dH[l][:n] if l > 0 else None
-            if sgd_lr is not None:
+            if fused:
                 G.gist_gcn_layer_bwd_sgd(self.ctx, self.desc(l, n), batch.A, batch.A_T, Hin,
                                          self.agg[l][:n], self._out(l, n), params[l], dout,
                                          sgd_lr, dH, ws)
@@ -1021,6 +1026,9 @@ class SubGCNBatch:
                                      self.agg[l][:n], self._out(l, n), params[l], dout,
                                      self.dW[l], dH, ws)
             dout = dH
+        if sgd_lr is not None and not fused:
+            for l in range(self.L):
+                G.gist_sgd_update(self.ctx, params[l], self.dW[l], params[l].numel(), sgd_lr)
 
     def step(self, batch, params, lr, adam=None):
         """All m sub-GCNs' ``subTrain`` step on the shared batch: SGD, or

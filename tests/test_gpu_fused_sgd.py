@@ -170,3 +170,38 @@ def test_fused_sgd_empty_batch_and_errors(G, ctx):
                                  None, ws)
     with pytest.raises(G.GistError, match="NULL"):
         G.gist_gcn_layer_bwd_sgd(ctx, desc, A, None, None, None, None, None, None, LR, None, ws)
+
+
+@pytest.mark.parametrize("kind", ["sage", "gcn"])
+def test_subgcn_bf16_step_takes_the_fused_path_bitwise(G, ctx, kind):
+    """SubGCN.step with bf16-input GEMMs fuses the SGD step into each layer's
+    backward pass; the weights must equal an explicit backward + SGD."""
+    import torch
+    from paper_2102_10424_amd.step import BatchSlot, SubGCN
+    g = sbm(1500, 10, 30.0, 0.9, seed=7)
+    widths = [40, 512, 512, 7]
+    parts = 2 if kind == "sage" else 1
+    rng = np.random.default_rng(11)
+    X = to_dev(rng.standard_normal((g.n, widths[0])).astype(np.float32))
+    y = rng.integers(0, widths[-1], g.n).astype(np.int32)
+    P = [(rng.standard_normal((parts * widths[l], widths[l + 1])) /
+          np.sqrt(widths[l])).astype(np.float32) for l in range(3)]
+    slot = BatchSlot(ctx, kind, g.n, g.nnz + g.n, widths[0])
+    b = slot.load(G.GraphHandle(g), np.array([0, 3, 5, 8], dtype=np.int32), X, y)
+    out = []
+    for fused in (True, False):
+        run = SubGCN(ctx, kind, widths, b.n, dtype=G.GIST_DTYPE_BF16_IN)
+        params = [to_dev(p) for p in P]
+        if fused:
+            run.step(b, params, LR)
+        else:
+            run.forward(b, params)
+            run.loss_and_grad(b)
+            run.backward(b, params)
+            run.sgd(params, LR)
+        torch.cuda.synchronize()
+        out.append([to_host(p) for p in params])
+    for l, (a, c) in enumerate(zip(*out)):
+        log(f"  {kind} layer {l}: {'bitwise equal' if same(a, c) else 'DIFFERENT'}")
+        assert same(a, c), l
+        assert not np.array_equal(a, P[l])
