@@ -350,8 +350,18 @@ typedef struct gist_gat_desc {
   int32_t act;     /* gist_act                                           */
   int32_t dtype;   /* gist_dtype of the two GEMMs                        */
   float slope;     /* LeakyReLU slope for negative scores (0.2 in the GAT paper) */
-  int32_t reserved;  /* 0 */
+  uint32_t flags;  /* 0 or GIST_GAT_MIRROR_IN_WS                        */
 } gist_gat_desc;
+
+/* GIST_GAT_MIRROR_IN_WS (backward only): the first nnz int32 of the
+ * backward workspace already hold A's mirror map (for each entry (i, j) the
+ * position of (j, i)), as a previous gist_gat_layer_bwd on the same pattern
+ * A left them in the same workspace, and nothing has written that workspace
+ * since.  The map is then not formed again.  The layers of one sub-GCN step
+ * share the mini-batch's pattern: the first backward call forms the map,
+ * the layers below pass the flag.  With a different matrix, or a
+ * workspace written in between (a forward call), results are undefined. */
+enum { GIST_GAT_MIRROR_IN_WS = 1 };
 
 gist_status gist_gat_workspace_size(const gist_gat_desc* D, size_t* fwd_bytes,
                                     size_t* bwd_bytes);

@@ -544,7 +544,8 @@ namespace {
 
 gist_status check_gat(const gist_gat_desc* D, const gist_csr_dev* A, const char* what) {
   if (!D) return set_error(GIST_E_INVAL, std::string(what) + ": NULL descriptor");
-  if (D->n < 0 || D->nnz < 0 || D->s_in < 1 || D->s_out < 1 || D->reserved != 0)
+  if (D->n < 0 || D->nnz < 0 || D->s_in < 1 || D->s_out < 1 ||
+      (D->flags & ~static_cast<uint32_t>(GIST_GAT_MIRROR_IN_WS)))
     return set_error(GIST_E_INVAL, std::string(what) + ": bad sizes");
   if (D->act != GIST_ACT_NONE && D->act != GIST_ACT_RELU)
     return set_error(GIST_E_INVAL, std::string(what) + ": unknown activation");
@@ -559,11 +560,13 @@ gist_status check_gat(const gist_gat_desc* D, const gist_csr_dev* A, const char*
   return GIST_OK;
 }
 
-// backward workspace: [dZ | u | v | dpre | du | dv | tpos | alpha_t | dP | gemv | gemm]
+// backward workspace: [tpos | dZ | u | v | dpre | du | dv | alpha_t | dP | gemv | gemm];
+// the mirror map tpos comes first, so that it stays in place for the next
+// layer's call on the same pattern (GIST_GAT_MIRROR_IN_WS)
 struct GatPlan {
   size_t dz, uv, dpre, dudv, tpos, alpha_t, dp, gemv, gemm;
   size_t total() const {
-    return align256(dz) + align256(uv) + align256(dpre) + align256(dudv) + align256(tpos) +
+    return align256(tpos) + align256(dz) + align256(uv) + align256(dpre) + align256(dudv) +
            align256(alpha_t) + align256(dp) + align256(gemv) + gemm;
   }
 };
@@ -664,13 +667,13 @@ extern "C" gist_status gist_gat_layer_bwd(gist_ctx* ctx, const gist_gat_desc* D,
   }
   char* c = static_cast<char*>(ws);
   auto take = [&](size_t bytes) { char* r = c; c += align256(bytes); return r; };
+  int* tpos = reinterpret_cast<int*>(take(p.tpos));
   float* dZbuf = reinterpret_cast<float*>(take(p.dz));
   float* u = reinterpret_cast<float*>(take(p.uv));
   float* v = u + n;
   float* dpre = reinterpret_cast<float*>(take(p.dpre));
   float* du = reinterpret_cast<float*>(take(p.dudv));
   float* dv = du + n;
-  int* tpos = reinterpret_cast<int*>(take(p.tpos));
   float* alpha_t = reinterpret_cast<float*>(take(p.alpha_t));
   float* dP = reinterpret_cast<float*>(take(p.dp));
   float* part = reinterpret_cast<float*>(take(p.gemv));
@@ -684,7 +687,8 @@ extern "C" gist_status gist_gat_layer_bwd(gist_ctx* ctx, const gist_gat_desc* D,
   GIST_TRY(gist::gat_scores(st, n, s, P_save, so, a_src, a_dst, u, v));
   GIST_TRY(gist::gat_edge_grad(st, n, D->nnz, s, A->rowptr, A->col, alpha_save, dZ, so, P_save, so,
                                u, v, D->slope, dpre, du));
-  GIST_TRY(gist::gat_mirror(st, n, D->nnz, A->rowptr, A->col, tpos));
+  if (!(D->flags & GIST_GAT_MIRROR_IN_WS))
+    GIST_TRY(gist::gat_mirror(st, n, D->nnz, A->rowptr, A->col, tpos));
   GIST_TRY(gist::gat_mirror_sums(st, n, D->nnz, A->rowptr, tpos, dpre, alpha_save, dv, alpha_t));
   // dP = A_alpha^T dZ (the pattern is symmetric: row j lists the i with alpha_ij)
   GIST_TRY(gist::spmm(st, n, D->nnz, A->rowptr, A->col, alpha_t, dZ, so, s, dP, so, nullptr, 0,

@@ -113,7 +113,7 @@ class gist_ladies_layer(C.Structure):
 class gist_gat_desc(C.Structure):
     _fields_ = [("n", C.c_int64), ("nnz", C.c_int64), ("s_in", C.c_int32), ("s_out", C.c_int32),
                 ("act", C.c_int32), ("dtype", C.c_int32), ("slope", C.c_float),
-                ("reserved", C.c_int32)]
+                ("flags", C.c_uint32)]
 
 
 class gist_slice_set(C.Structure):
@@ -483,9 +483,13 @@ def gist_adam_update_dev(ctx, W, dW, m, v, n, coef_dev, beta1=0.9, beta2=0.999, 
                                      float(beta1), float(beta2), float(eps), _ptr(coef_dev)))
 
 
-def gat_desc(n, nnz, s_in, s_out, act, dtype=GIST_DTYPE_F32, slope=0.2):
+GIST_GAT_MIRROR_IN_WS = 1
+
+
+def gat_desc(n, nnz, s_in, s_out, act, dtype=GIST_DTYPE_F32, slope=0.2, flags=0):
+    """``flags``: GIST_GAT_MIRROR_IN_WS (the backward workspace holds A's mirror map)."""
     return gist_gat_desc(int(n), int(nnz), int(s_in), int(s_out), int(act), int(dtype),
-                         float(slope), 0)
+                         float(slope), int(flags))
 
 
 def gist_gat_workspace_size(desc):

@@ -860,6 +860,7 @@ class SubGCN:
         nnz = batch.nnz
         ws = self._workspace(batch)
         dout = self.dlogits[:batch.rows(self.L)]
+        prev_A = None
         for l in reversed(range(self.L)):
             n, n_in = batch.rows(l + 1), batch.rows(l)
             A, A_T = batch.adj(l)
@@ -868,7 +869,11 @@ class SubGCN:
             if self.gat:
                 W, a1, a2 = self._gat_parts(params[l], l)
                 gW, g1, g2 = self._gat_parts(self.dW[l], l)
-                G.gist_gat_layer_bwd(self.ctx, self._ldesc(batch, l), A, Hin,
+                desc = self._ldesc(batch, l)
+                if A is prev_A:   # same pattern: the layer above left its mirror map in ws
+                    desc.flags = G.GIST_GAT_MIRROR_IN_WS
+                prev_A = A
+                G.gist_gat_layer_bwd(self.ctx, desc, A, Hin,
                                      self.agg[l][:n], self.alpha[l][:nnz], self.H[l + 1][:n],
                                      W, a1, a2, dout, gW, g1, g2, dH, ws)
             elif fused:

@@ -117,6 +117,65 @@ def test_gat_bitwise_deterministic(G, ctx):
         assert np.array_equal(a[k].view(np.uint32), b[k].view(np.uint32)), k
 
 
+def test_gat_mirror_map_reused_across_layers(G, ctx):
+    """GIST_GAT_MIRROR_IN_WS: a second backward call on the same pattern,
+    with the workspace a first call on that pattern left (as the layers of
+    one step do), skips forming the mirror map and gives bitwise the
+    gradients of a call that forms it."""
+    import torch
+    g = GRAPHS["sbm1500"]
+    csr = MB.build(g, None, "gcn")
+    n, nnz = csr["n"], csr["nnz"]
+    A, keep = csr_to_dev(csr)
+    rng = np.random.default_rng(9)
+
+    def layer(si, so):
+        d = dict(H=to_dev(rng.standard_normal((n, si)).astype(np.float32)),
+                 W=to_dev((rng.standard_normal((si, so)) / np.sqrt(si)).astype(np.float32)),
+                 a1=to_dev((rng.standard_normal(so) * 0.3).astype(np.float32)),
+                 a2=to_dev((rng.standard_normal(so) * 0.3).astype(np.float32)),
+                 dHo=to_dev(rng.standard_normal((n, so)).astype(np.float32)))
+        d["desc"] = G.gat_desc(n, nnz, si, so, 1)
+        return d
+
+    def fwd_bwd(d, ws):
+        """Forward and backward of layer d in workspace ws (forms the map)."""
+        si, so = d["desc"].s_in, d["desc"].s_out
+        P = torch.empty(n, so, device="cuda")
+        alpha = torch.empty(nnz, device="cuda")
+        Ho = torch.empty(n, so, device="cuda")
+        G.gist_gat_layer_fwd(ctx, d["desc"], A, d["H"], d["W"], d["a1"], d["a2"], P, alpha, Ho,
+                             ws)
+        out = [torch.empty(si, so, device="cuda"), torch.empty(so, device="cuda"),
+               torch.empty(so, device="cuda"), torch.empty(n, si, device="cuda")]
+        G.gist_gat_layer_bwd(ctx, d["desc"], A, d["H"], P, alpha, Ho, d["W"], d["a1"], d["a2"],
+                             d["dHo"], *out, ws)
+        return [to_host(t) for t in out]
+
+    top, below = layer(96, 40), layer(130, 96)
+    sizes = [max(G.gist_gat_workspace_size(d["desc"])) for d in (top, below)]
+    ws = torch.empty(max(sizes), dtype=torch.uint8, device="cuda")
+    ref = fwd_bwd(below, ws)
+    # the step's order: the layer above forms the map, the layer below reuses it
+    fwd_bwd(top, ws)
+    desc = G.gat_desc(n, nnz, 130, 96, 1, flags=G.GIST_GAT_MIRROR_IN_WS)
+    d = below
+    P = torch.empty(n, 96, device="cuda")
+    alpha = torch.empty(nnz, device="cuda")
+    Ho = torch.empty(n, 96, device="cuda")
+    fws = torch.empty(max(sizes), dtype=torch.uint8, device="cuda")   # forward's own workspace
+    G.gist_gat_layer_fwd(ctx, d["desc"], A, d["H"], d["W"], d["a1"], d["a2"], P, alpha, Ho, fws)
+    out = [torch.empty(130, 96, device="cuda"), torch.empty(96, device="cuda"),
+           torch.empty(96, device="cuda"), torch.empty(n, 130, device="cuda")]
+    G.gist_gat_layer_bwd(ctx, desc, A, d["H"], P, alpha, Ho, d["W"], d["a1"], d["a2"], d["dHo"],
+                         *out, ws)
+    got = [to_host(t) for t in out]
+    for name, a, b in zip(("dW", "da_src", "da_dst", "dH"), ref, got):
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32)), name
+    with pytest.raises(G.GistError):
+        G.gist_gat_workspace_size(G.gat_desc(n, nnz, 4, 4, 1, flags=2))
+
+
 def test_gat_errors(G, ctx):
     import torch
     t = torch.zeros(64, device="cuda")
