@@ -312,9 +312,10 @@ gist_status gist_gcn_layer_bwd(gist_ctx* ctx, const gist_layer_desc* L,
 /* The same backward pass with subTrain's SGD step fused in (Algorithm 1; the
  * update of gist_sgd_update): W <- W - lr dW in place, where dW is the
  * weight gradient above, without writing dW anywhere.  The input gradient dH
- * is formed from the weights before the step.  W and dH_out ... ws as in
- * gist_gcn_layer_bwd (W is device memory, updated in place; every group's
- * slice for G > 1).  Bitwise the same W and dH as gist_gcn_layer_bwd
+ * is formed from the weights before the step.  Every other argument has the
+ * meaning, layout and workspace size it has in gist_gcn_layer_bwd; W (device
+ * memory, every group's slice for G > 1) is read and then updated in place,
+ * and there is no dW argument.  Bitwise the same W and dH as gist_gcn_layer_bwd
  * followed by gist_sgd_update(W, dW, lr): the GEMM writing the gradient
  * applies fmaf(-lr, dW_ij, W_ij) to each element once, in its epilogue.
  * Saves the gradient's write and the separate pass that reads it.  With no
