@@ -364,6 +364,17 @@ typedef struct gist_gat_desc {
  * workspace written in between (a forward call), results are undefined. */
 enum { GIST_GAT_MIRROR_IN_WS = 1 };
 
+/* The two per-node halves of the attention scores, u = P a_src and
+ * v = P a_dst (n floats each, device memory), exactly as the layer's forward
+ * and backward passes form them: the score of entry (i, j) is
+ * LeakyReLU(u_i + v_j), its side decided by u_i + v_j > 0 in fp32.  P is
+ * n x s row-major with leading dimension ldp; a_src, a_dst have s entries.
+ * For a caller that needs the attention logits, or the side each score
+ * fell on.  Errors: GIST_E_INVAL (NULL pointers with n > 0, s < 1,
+ * ldp < s, n < 0). */
+gist_status gist_gat_scores(gist_ctx* ctx, int64_t n, int32_t s, const float* P, int64_t ldp,
+                            const float* a_src, const float* a_dst, float* u, float* v);
+
 gist_status gist_gat_workspace_size(const gist_gat_desc* D, size_t* fwd_bytes,
                                     size_t* bwd_bytes);
 gist_status gist_gat_layer_fwd(gist_ctx* ctx, const gist_gat_desc* D, const gist_csr_dev* A,
@@ -524,7 +535,12 @@ typedef struct gist_slice_set {
  * writes instead of 1/m-dense scattered ones.  The partitions of `done`
  * and `next` may differ.  At least one dimension of each set must be
  * partitioned when m > 1, and ranks and offsets come in pairs (GIST_E_INVAL
- * otherwise). */
+ * otherwise).  The slices of `done` and of `next` must not share memory with
+ * each other or with Wg: one grid reads the trained slices and writes the new
+ * ones, so an overlap would let a row's block overwrite entries another block
+ * has not read yet.  The call rejects the one overlap it can see on the host,
+ * both sets naming the same pointer table (GIST_E_INVAL); any other overlap
+ * gives undefined results. */
 gist_status gist_subagg_gather(gist_ctx* ctx, float* Wg, int64_t rows, int64_t cols,
                                int64_t ldg, int32_t m, const gist_slice_set* done,
                                const gist_slice_set* next);

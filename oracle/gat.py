@@ -56,21 +56,39 @@ def gat_forward(csr, H, W, a_src, a_dst, act, slope):
     return dict(P=P, u=u, v=v, pre=pre, alpha=alpha, Z=Z, H_out=relu(Z) if act else Z)
 
 
-def gat_backward(csr, H, fwd, W, a_src, a_dst, dH_out, act, slope, need_dH=True):
-    """Gradients of the GAT layer: dW, da_src, da_dst and (optionally) dH."""
+def gat_backward(csr, H, fwd, W, a_src, a_dst, dH_out, act, slope, need_dH=True, mask=None,
+                 pos=None):
+    """Gradients of the GAT layer: dW, da_src, da_dst and (optionally) dH.
+
+    ``mask`` replaces the ReLU derivative 1[Z > 0] and ``pos`` (one bool per
+    entry, in the pattern's order) the LeakyReLU side 1[u_i + v_j > 0] of
+    each score: the decisions another evaluation of the same forward took
+    where a value lies within rounding distance of zero."""
     n, rp, row, col = _edges(csr)
     P, alpha, pre = fwd["P"], fwd["alpha"], fwd["pre"]
-    dZ = as_f64(dH_out) * (fwd["Z"] > 0) if act else as_f64(dH_out)
+    if not act:
+        dZ = as_f64(dH_out)
+    elif mask is not None:
+        dZ = as_f64(dH_out) * np.asarray(mask, dtype=bool)
+    else:
+        dZ = as_f64(dH_out) * (fwd["Z"] > 0)
+    if pos is None:
+        pos = pre > 0
+    else:
+        pos = np.asarray(pos, dtype=bool)
+        if pos.shape != pre.shape:
+            raise ValueError("pos needs one decision per entry")
     Aa = sp.csr_matrix((alpha, col, rp), shape=(n, n))
     dP = Aa.T @ dZ                                     # through Z = A_alpha P
     dalpha = np.einsum("ek,ek->e", dZ[row], P[col])    # dL/dalpha_ij = dZ_i . P_j
     c = np.bincount(row, weights=alpha * dalpha, minlength=n)
     de = alpha * (dalpha - c[row])                     # softmax backward
-    dpre = de * np.where(pre > 0, 1.0, slope)          # LeakyReLU backward
+    dpre = de * np.where(pos, 1.0, slope)              # LeakyReLU backward
     du = np.bincount(row, weights=dpre, minlength=n)
     dv = np.bincount(col, weights=dpre, minlength=n)
     dP = dP + np.outer(du, as_f64(a_src)) + np.outer(dv, as_f64(a_dst))
-    out = dict(dW=as_f64(H).T @ dP, da_src=P.T @ du, da_dst=P.T @ dv, dP=dP)
+    out = dict(dW=as_f64(H).T @ dP, da_src=P.T @ du, da_dst=P.T @ dv, dP=dP, du=du, dv=dv,
+               dpre=dpre)
     if need_dH:
         out["dH"] = dP @ as_f64(W).T
     return out

@@ -64,46 +64,65 @@ def _layer_csr(kind, csr, l):
     return csr
 
 
-def forward(kind, csr, X, params):
-    """Forward pass; returns the list of layer records (AH, Z, H_out) and inputs."""
+def _opt(seq, l):
+    return None if seq is None else seq[l]
+
+
+def forward(kind, csr, X, params, rnd=None, orders=None):
+    """Forward pass; returns the list of layer records (AH, Z, H_out) and inputs.
+
+    ``rnd`` rounds the operands of every dense product (the bf16-input
+    variant, ``layers.round_bf16``); ``orders[l]`` is GCN layer l's
+    association order ("agg" or "xform"; default "agg").  GAT layers take
+    neither."""
     H = [_l.as_f64(X)]
     recs = []
     L = len(params)
+    if kind == "gat" and rnd is not None:
+        raise ValueError("the GAT layers have no rounded variant here")
     for l in range(L):
         act = l < L - 1
         if kind == "gcn":
-            rec = _l.gcn_forward(_layer_csr(kind, csr, l), H[-1], params[l], act)
+            rec = _l.gcn_forward(_layer_csr(kind, csr, l), H[-1], params[l], act, rnd=rnd,
+                                 order=_opt(orders, l) or "agg")
         elif kind == "gat":
             W, a1, a2 = params[l]
             rec = _g.gat_forward(_layer_csr(kind, csr, l), H[-1], W, a1, a2, act, GAT_SLOPE)
         else:
             rec = _l.sage_forward(_layer_csr(kind, csr, l), H[-1], params[l][0], params[l][1],
-                                  act)
+                                  act, rnd=rnd)
         recs.append(rec)
         H.append(rec["H_out"])
     return H, recs
 
 
-def backward(kind, csr, H, recs, params, dlogits):
-    """Backward pass from dL/dlogits; returns per-layer gradients and dH records."""
+def backward(kind, csr, H, recs, params, dlogits, masks=None, pos=None, rnd=None, orders=None):
+    """Backward pass from dL/dlogits; returns per-layer gradients and dH records.
+
+    ``masks[l]`` (hidden layers) replaces the ReLU derivative 1[Z_l > 0] and,
+    for GAT, ``pos[l]`` the LeakyReLU side of every score of layer l: the
+    decisions another evaluation of the same forward took (``layers``).
+    ``rnd`` and ``orders`` as in :func:`forward`."""
     L = len(params)
     grads = [None] * L
     dHs = [None] * L
     dH = dlogits
     for l in reversed(range(L)):
         act = l < L - 1
+        mask = _opt(masks, l) if act else None
         if kind == "gcn":
             b = _l.gcn_backward(_layer_csr(kind, csr, l), H[l], recs[l], params[l], dH, act,
-                                need_dH=l > 0)
+                                need_dH=l > 0, mask=mask, rnd=rnd,
+                                order=_opt(orders, l) or "agg")
             grads[l] = b["dW"]
         elif kind == "gat":
             W, a1, a2 = params[l]
             b = _g.gat_backward(_layer_csr(kind, csr, l), H[l], recs[l], W, a1, a2, dH, act,
-                                GAT_SLOPE, need_dH=l > 0)
+                                GAT_SLOPE, need_dH=l > 0, mask=mask, pos=_opt(pos, l))
             grads[l] = (b["dW"], b["da_src"], b["da_dst"])
         else:
             b = _l.sage_backward(_layer_csr(kind, csr, l), H[l], recs[l], params[l][0],
-                                 params[l][1], dH, act, need_dH=l > 0)
+                                 params[l][1], dH, act, need_dH=l > 0, mask=mask, rnd=rnd)
             grads[l] = (b["dW_self"], b["dW_neigh"])
         dH = b.get("dH")
         dHs[l] = dH
@@ -115,11 +134,17 @@ def sgd_params(kind, params, grads, lr):
             for p, gr in zip(params, grads)]
 
 
-def sub_gcn_step(kind, csr, X, labels, params, lr):
-    """``subTrain``: one SGD step of a sub-GCN on one mini-batch."""
-    H, recs = forward(kind, csr, X, params)
+def sub_gcn_step(kind, csr, X, labels, params, lr, masks=None, pos=None, rnd=None, orders=None):
+    """``subTrain``: one SGD step of a sub-GCN on one mini-batch.
+
+    The optional arguments are those of :func:`forward` and
+    :func:`backward`: rounded operands and association orders (the
+    bf16-input variant), and the ReLU / LeakyReLU decisions another
+    evaluation of the same forward took."""
+    H, recs = forward(kind, csr, X, params, rnd=rnd, orders=orders)
     loss, dlogits = _l.softmax_xent(H[-1], labels)
-    grads, dHs = backward(kind, csr, H, recs, params, dlogits)
+    grads, dHs = backward(kind, csr, H, recs, params, dlogits, masks=masks, pos=pos, rnd=rnd,
+                          orders=orders)
     return dict(loss=loss, H=H, recs=recs, dlogits=dlogits, grads=grads,
                 dH=dHs, params=sgd_params(kind, params, grads, lr))
 

@@ -30,6 +30,22 @@ def as_f64(x):
     return np.asarray(x, dtype=np.float64)
 
 
+def round_bf16(x):
+    """Operand rounding of the bf16-input variant: each value is taken to
+    fp32 (round to nearest even, as the GPU holds it) and then to the
+    nearest bfloat16 (8 significant bits, ties to even), returned in fp64.
+
+    bfloat16 is the upper half of an IEEE fp32 word, so rounding to nearest
+    even keeps the upper 16 bits after adding 0x7FFF plus the lowest kept bit
+    (a carry into the exponent is the correct rounding up, up to infinity).
+    NaN stays NaN."""
+    f = np.asarray(x, dtype=np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16
+    out = r.astype(np.uint32).view(np.float32).astype(np.float64)
+    return np.where(np.isnan(f), np.nan, out)
+
+
 def adjacency(csr, transpose=False):
     """The stored aggregation matrix (or its explicit transpose) as fp64 CSR.
 
@@ -59,55 +75,105 @@ def relu(z):
     return np.maximum(z, 0.0)
 
 
-def gcn_forward(csr, H, W, act):
+# Options shared by the layers below.
+#
+# ``rnd``: the rounding applied to every operand of a dense product, None for
+# none (plain fp64).  ``round_bf16`` gives the bf16-input variant: the
+# products' inputs are rounded to bfloat16 and the products are then formed
+# exactly (in fp64 here; fp32 accumulation on the GPU).  The aggregation is
+# not a dense product and is never rounded.
+#
+# ``order`` (GCN only): "agg" forms (Abar H) W, "xform" forms Abar (H W).  The
+# two are equal in exact arithmetic (the association order is free, eq. (2)),
+# but not once the operands are rounded, so a rounded oracle follows the
+# order the GPU took.  The backward pass follows the same order: "agg"
+# computes dW = (Abar H)^T dZ and dH = Abar^T (dZ W^T); "xform" computes
+# T = Abar^T dZ, dW = H^T T and dH = T W^T.
+#
+# ``mask`` (backward): the ReLU derivative to use instead of 1[Z > 0] -- the
+# decisions another evaluation of the same forward took.  A pre-activation
+# within rounding distance of zero may fall on either side; with the other
+# side's decisions the backward pass is the chain rule of that other,
+# equally correct, forward.
+
+
+def _rnd(rnd):
+    return as_f64 if rnd is None else rnd
+
+
+def gcn_forward(csr, H, W, act, rnd=None, order="agg"):
     """GCN layer, eq. (2): Z = (Abar H) W, H' = ReLU(Z) if ``act`` else Z."""
+    r = _rnd(rnd)
     AH = aggregate(csr, H)
-    Z = AH @ as_f64(W)
+    if order == "xform":
+        Z = aggregate(csr, r(H) @ r(W))
+    elif order == "agg":
+        Z = r(AH) @ r(W)
+    else:
+        raise ValueError("order is 'agg' or 'xform'")
     return dict(AH=AH, Z=Z, H_out=relu(Z) if act else Z)
 
 
-def sage_forward(csr, H, W_self, W_neigh, act):
+def sage_forward(csr, H, W_self, W_neigh, act, rnd=None):
     """GraphSAGE-mean layer: Z = H W_self + (D^-1 A H) W_neigh."""
+    r = _rnd(rnd)
     H = as_f64(H)
     AH = aggregate(csr, H)
-    Z = H @ as_f64(W_self) + AH @ as_f64(W_neigh)
+    Z = r(H) @ r(W_self) + r(AH) @ r(W_neigh)
     return dict(AH=AH, Z=Z, H_out=relu(Z) if act else Z)
 
 
-def _dz(Z, dH_out, act):
+def _dz(Z, dH_out, act, mask=None):
     dH_out = as_f64(dH_out)
-    return dH_out * (Z > 0.0) if act else dH_out
+    if not act:
+        return dH_out
+    if mask is not None:
+        mask = np.asarray(mask, dtype=bool)
+        if mask.shape != np.shape(Z):
+            raise ValueError("mask shape differs from the pre-activation's")
+        return dH_out * mask
+    return dH_out * (Z > 0.0)
 
 
-def gcn_backward(csr, H, fwd, W, dH_out, act, need_dH=True):
+def gcn_backward(csr, H, fwd, W, dH_out, act, need_dH=True, mask=None, rnd=None, order="agg"):
     """Gradients of the GCN layer: dW = (Abar H)^T dZ, dH = Abar^T (dZ W^T).
 
     Abar^T is the transpose of the stored matrix, formed here.
     """
-    dZ = _dz(fwd["Z"], dH_out, act)
-    out = dict(dZ=dZ, dW=fwd["AH"].T @ dZ)
+    r = _rnd(rnd)
+    dZ = _dz(fwd["Z"], dH_out, act, mask)
+    if order == "xform":
+        T = aggregate_transposed(csr, dZ)
+        out = dict(dZ=dZ, dW=r(H).T @ r(T))
+        if need_dH:
+            out["dH"] = r(T) @ r(W).T
+        return out
+    if order != "agg":
+        raise ValueError("order is 'agg' or 'xform'")
+    out = dict(dZ=dZ, dW=r(fwd["AH"]).T @ r(dZ))
     if need_dH:
-        dP = dZ @ as_f64(W).T
+        dP = r(dZ) @ r(W).T
         out["dH"] = aggregate_transposed(csr, dP)
     return out
 
 
-def sage_backward(csr, H, fwd, W_self, W_neigh, dH_out, act, need_dH=True):
+def sage_backward(csr, H, fwd, W_self, W_neigh, dH_out, act, need_dH=True, mask=None, rnd=None):
     """Gradients of the SAGE-mean layer.
 
     dW_self = H^T dZ, dW_neigh = (Abar H)^T dZ,
     dH = dZ W_self^T + Abar^T (dZ W_neigh^T), with Abar^T the stored transpose.
     """
+    r = _rnd(rnd)
     H = as_f64(H)
-    dZ = _dz(fwd["Z"], dH_out, act)
-    out = dict(dZ=dZ, dW_self=H.T @ dZ, dW_neigh=fwd["AH"].T @ dZ)
+    dZ = _dz(fwd["Z"], dH_out, act, mask)
+    out = dict(dZ=dZ, dW_self=r(H).T @ r(dZ), dW_neigh=r(fwd["AH"]).T @ r(dZ))
     if need_dH:
-        dP = dZ @ as_f64(W_neigh).T
+        dP = r(dZ) @ r(W_neigh).T
         if "t_val" in csr:
             agg_t = adjacency(csr, transpose=True) @ dP
         else:
             agg_t = aggregate_transposed(csr, dP)
-        out["dH"] = dZ @ as_f64(W_self).T + agg_t
+        out["dH"] = r(dZ) @ r(W_self).T + agg_t
     return out
 
 

@@ -602,6 +602,20 @@ extern "C" gist_status gist_gat_workspace_size(const gist_gat_desc* D, size_t* f
   return GIST_OK;
 }
 
+extern "C" gist_status gist_gat_scores(gist_ctx* ctx, int64_t n, int32_t s, const float* P,
+                                       int64_t ldp, const float* a_src, const float* a_dst,
+                                       float* u, float* v) {
+  gist::clear_error();
+  if (!ctx) return set_error(GIST_E_INVAL, "gat_scores: NULL ctx");
+  gist::ProfBind pb(ctx);
+  if (n < 0 || s < 1 || ldp < s) return set_error(GIST_E_INVAL, "gat_scores: bad sizes");
+  if (n > INT32_MAX) return set_error(GIST_E_UNSUPPORTED, "gat_scores: n exceeds int32");
+  if (n == 0) return GIST_OK;
+  if (!P || !a_src || !a_dst || !u || !v) return set_error(GIST_E_INVAL, "gat_scores: NULL pointer");
+  gist::DeviceGuard dg(ctx->device);
+  return gist::gat_scores(ctx->stream, n, s, P, ldp, a_src, a_dst, u, v);
+}
+
 extern "C" gist_status gist_gat_layer_fwd(gist_ctx* ctx, const gist_gat_desc* D,
                                           const gist_csr_dev* A, const float* H, const float* W,
                                           const float* a_src, const float* a_dst, float* P_save,
@@ -908,6 +922,8 @@ extern "C" gist_status gist_subagg_gather(gist_ctx* ctx, float* Wg, int64_t rows
     if (m > 1 && !s->row_rank && !s->col_rank)
       return set_error(GIST_E_INVAL, "subagg_gather: m > 1 needs a partitioned dimension");
   }
+  if (done && next && done->slices == next->slices)
+    return set_error(GIST_E_INVAL, "subagg_gather: done and next share one slice table");
   gist::DeviceGuard dg(ctx->device);
   // algorithmic bytes: the matrix read once (and written once with `done`),
   // plus the slices' elements read (done) and written (next)

@@ -58,7 +58,7 @@ EXPORTED = (
     "gist_set_stream", "gist_partition", "gist_build_minibatch_csr", "gist_ladies_sample",
     "gist_layer_workspace_size", "gist_gcn_layer_fwd", "gist_gcn_layer_bwd",
     "gist_gcn_layer_bwd_sgd",
-    "gist_gat_workspace_size", "gist_gat_layer_fwd", "gist_gat_layer_bwd",
+    "gist_gat_workspace_size", "gist_gat_layer_fwd", "gist_gat_layer_bwd", "gist_gat_scores",
     "gist_softmax_xent_workspace", "gist_softmax_xent", "gist_softmax_xent_padded",
     "gist_gather_slice",
     "gist_sgd_update", "gist_adam_update", "gist_adam_coefficients", "gist_adam_update_dev",
@@ -149,6 +149,7 @@ _sigs = {
                            [_P] * 8 + [C.c_size_t]),
     "gist_gat_layer_bwd": (C.c_int, [_P, C.POINTER(gist_gat_desc), C.POINTER(gist_csr_dev)] +
                            [_P] * 13 + [C.c_size_t]),
+    "gist_gat_scores": (C.c_int, [_P, C.c_int64, C.c_int32, _P, C.c_int64, _P, _P, _P, _P]),
     "gist_last_error": (C.c_char_p, []),
     "gist_status_str": (C.c_char_p, [C.c_int]),
     "gist_create": (C.c_int, [C.c_int, _P, C.POINTER(_P)]),
@@ -511,6 +512,11 @@ def gist_gat_layer_bwd(ctx, desc, A, H, P_save, alpha_save, H_out, W, a_src, a_d
                                    _ptr(a_dst), _ptr(dH_out), _ptr(dW), _ptr(da_src),
                                    _ptr(da_dst), _ptr(dH), _ptr(ws),
                                    0 if ws is None else ws.numel()))
+
+
+def gist_gat_scores(ctx, n, s, P, ldp, a_src, a_dst, u, v):
+    _check(_lib.gist_gat_scores(ctx.handle, int(n), int(s), _ptr(P), int(ldp), _ptr(a_src),
+                                _ptr(a_dst), _ptr(u), _ptr(v)))
 
 
 def slice_set(row_rank, row_offs, col_rank, col_offs, slice_ptrs, ld):

@@ -53,3 +53,13 @@ def csr_to_dev(csr, transpose=False):
                  np.zeros(1, np.float32))
     rows = csr.get("n_in", csr["n"]) if transpose else csr["n"]   # rectangular: n x n_in
     return G.csr_dev(rows, nnz, rp, col, val), (rp, col, val)
+
+
+def gpu_orders(kind, s):
+    """The association order GIST_ORDER_AUTO takes for each GCN layer of
+    slice widths s (include/gist.h: aggregate at min(s_in, s_out),
+    aggregation first on a tie), as oracle order names; None for SAGE and
+    GAT, which always aggregate first."""
+    if kind != "gcn":
+        return None
+    return ["agg" if s[l] <= s[l + 1] else "xform" for l in range(len(s) - 1)]

@@ -26,7 +26,7 @@ from oracle import layers as OL
 from oracle import minibatch as MB
 from oracle import partition as OP
 
-from gpu_util import BF16_TOL, FP32_TOL, csr_to_dev, log, relerr, to_dev, to_host
+from gpu_util import BF16_TOL, FP32_TOL, csr_to_dev, gpu_orders, log, relerr, to_dev, to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -236,17 +236,23 @@ class _Workload:
         return out["layers"], self.X[out["nodes"][0]], self.y[out["nodes"][self.L]]
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("widths,b,s", [((50, 96, 12), 64, 256), ((50, 96, 64, 12), 64, 256),
                                         ((70, 130, 100, 9), 300, 900)])
-def test_ladies_step_matches_oracle(G, ctx, widths, b, s):
-    """fp32 through the whole step (the bf16-input GEMMs are checked layer by
-    layer above, on the oracle's inputs: chained through three layers their
-    rounding moves ReLU decisions, which no per-element bound covers)."""
+def test_ladies_step_matches_oracle(G, ctx, widths, b, s, dtype):
+    """A sub-GCN step on a library-sampled LADIES batch against the oracle's
+    step on the oracle's batch, every tensor: logits, loss, every dW and
+    every updated weight.  The oracle's backward runs through the GPU's own
+    ReLU decisions (H_out > 0), which may differ from its own only where a
+    pre-activation lies within rounding distance of zero; with bf16-input
+    GEMMs the oracle rounds every dense product's operands to bf16, in the
+    association order the GPU takes."""
     import torch
+    from oracle import layers as OLr
     from paper_2102_10424_amd.step import LadiesSlot, SubGCN
-    dtype = 0
+    dt = G.GIST_DTYPE_BF16_IN if dtype == "bf16" else G.GIST_DTYPE_F32
     w = _Workload(4000, 40, widths, b, s)
-    log(f"ladies step widths {widths} b={b} s={s}")
+    log(f"ladies step {dtype} widths {widths} b={b} s={s}")
     key = 31
     slot = LadiesSlot(ctx, w.L, w.b, w.s, w.max_degree, widths[0])
     b = slot.load(G.CsrHandle(w.A), w.batch_nodes(key), key, to_dev(w.X), w.y)
@@ -256,20 +262,36 @@ def test_ladies_step_matches_oracle(G, ctx, widths, b, s):
     assert b.rows(0) > b.rows(w.L)
     lr = 0.05
     params = [to_dev(t.copy()) for t in w.theta]
-    run = SubGCN(ctx, "gcn", widths, 1, dtype=dtype)
+    run = SubGCN(ctx, "gcn", widths, 1, dtype=dt)
     logits = run.forward(b, params)
     run.loss_and_grad(b)
     run.backward(b, params)
     run.sgd(params, lr)
     torch.cuda.synchronize()
-    ref = OG.sub_gcn_step("gcn", layers, Xo, yo, w.theta, lr)
-    tol = FP32_TOL
+    masks = [to_host(run.H[l + 1][:b.rows(l + 1)]) > 0 for l in range(w.L - 1)] + [None]
+    ref = OG.sub_gcn_step("gcn", layers, Xo, yo, w.theta, lr, masks=masks,
+                          rnd=OLr.round_bf16 if dtype == "bf16" else None,
+                          orders=gpu_orders("gcn", widths))
+    tol = BF16_TOL if dtype == "bf16" else FP32_TOL
+    band = 1e-2 if dtype == "bf16" else 1e-5
+    flips = 0
+    for l in range(w.L - 1):
+        Z = ref["recs"][l]["Z"]
+        diff = masks[l] != (Z > 0)
+        assert np.all(np.abs(Z[diff]) <= band * np.max(np.abs(Z)))
+        flips += int(diff.sum())
     e = dict(logits=relerr(to_host(logits), ref["H"][-1]),
-             loss=abs(float(to_host(run.loss)[0]) - ref["loss"]) / abs(ref["loss"]))
+             loss=abs(float(to_host(run.loss)[0]) - ref["loss"]) / abs(ref["loss"]),
+             dlogits=relerr(to_host(run.dlogits[:b.rows(w.L)]), ref["dlogits"]))
     for l in range(w.L):
+        if l < w.L - 1:
+            e[f"H{l + 1}"] = relerr(to_host(run.H[l + 1][:b.rows(l + 1)]), ref["H"][l + 1])
+        if l > 0:
+            e[f"dH{l}"] = relerr(to_host(run.dH[l][:b.rows(l)]), ref["dH"][l])
         e[f"dW{l}"] = relerr(to_host(run.dW[l]), ref["grads"][l])
         e[f"W{l}"] = relerr(to_host(params[l]), ref["params"][l])
-    log("  " + ", ".join(f"{k} {v:.2e}" for k, v in e.items()))
+    log(f"  {flips} decisions differ within the band; " +
+        ", ".join(f"{k} {v:.2e}" for k, v in e.items()))
     assert max(e.values()) <= tol, e
 
 

@@ -9,13 +9,20 @@ Two views of the same step, both through the C ABI:
   outputs.  Because both sides read their ReLU decisions from the same
   numbers, the 1e-4 bar measures the kernels alone.
 * chained: the step exactly as bench.py runs it (host CSR build into pinned
-  memory, upload, feature gather, 4 forward layers, loss, backward, SGD).
-  Forward activations, logits and loss are compared within 1e-4.  The
-  GPU's ReLU decisions must equal the oracle's except where the oracle's
-  pre-activation lies within rounding distance of zero (|Z| <= 1e-5 max|Z|,
-  where either decision is correct); if no decision differs, every
-  gradient and updated weight is compared within 1e-4 too.  For GAT the
-  same holds for the LeakyReLU decisions of the attention scores.
+  memory, upload, feature gather, forward through every layer, loss,
+  backward, SGD), in fp32 (c1-c4, c6) and with bf16-input GEMMs (c1-c4).
+  The GPU's ReLU decisions must equal the oracle's except where the
+  oracle's pre-activation lies within rounding distance of zero (fp32:
+  |Z| <= 1e-5 max|Z|; bf16: 1e-2 max|Z|), where either decision is
+  correct.  The oracle's backward is then evaluated through the GPU's own
+  decisions (its ReLU masks H_out > 0 and, for GAT, the side u_i + v_j > 0
+  of every attention score, from gist_gat_scores), so that both sides
+  differentiate the same function, and every tensor of the step is
+  compared: activations, logits, loss, dlogits, every dW, every dH and
+  every updated weight, within 1e-4 (fp32) or 2e-2 (bf16).  For the bf16
+  variant the oracle rounds every dense product's operands to bf16 as the
+  GPU does (oracle.layers.round_bf16), in the association order the GPU
+  takes.
 """
 
 import numpy as np
@@ -27,7 +34,7 @@ from oracle import layers as OL
 from oracle import minibatch as OM
 from oracle import partition as OP
 
-from gpu_util import BF16_TOL, FP32_TOL, csr_to_dev, log, relerr, to_dev, to_host
+from gpu_util import BF16_TOL, FP32_TOL, csr_to_dev, gpu_orders, log, relerr, to_dev, to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -194,54 +201,91 @@ def test_step_layerwise_gat(G, ctx, dtype):
         assert e_f <= tol and e_b <= tol
 
 
-@pytest.mark.parametrize("name", CONFIGS + ["c6"])
-def test_step_chained(G, ctx, name):
+def chained_gpu_step(G, ctx, w, dtype):
+    """One sub-GCN step through the library exactly as the benchmark runs it
+    (unfused SGD, so that dW is visible), with host copies of every tensor
+    and the decisions the GPU took."""
     import torch
     from paper_2102_10424_amd.step import BatchSlot, SubGCN
-    w = workload(name)
-    cfg, csr, ref = w["cfg"], w["csr"], w["ref"]
+    cfg, csr = w["cfg"], w["csr"]
     kind, L = cfg.kind, cfg.L
     s = cfg.slice_widths()
+    dt = G.GIST_DTYPE_BF16_IN if dtype == "bf16" else G.GIST_DTYPE_F32
     X_all = torch.from_numpy(cfg.features_matrix()).cuda()
     slot = BatchSlot(ctx, w["norm"], csr["n"], csr["nnz"], cfg.widths[0])
     b = slot.load(G.GraphHandle(w["g"]), w["clusters"], X_all, w["labels"])
     assert b.n == csr["n"] and b.nnz == csr["nnz"]
+    n = b.n
     params = [to_dev(stacked(kind, p).astype(np.float32)) for p in w["params"]]
-    run = SubGCN(ctx, kind, s, b.n)
+    run = SubGCN(ctx, kind, s, n, dtype=dt)
     run.forward(b, params)
     run.loss_and_grad(b)
     run.backward(b, params)
+    pos = None
+    if kind == "gat":   # the side of every score, from the GPU's own u and v
+        rows = np.repeat(np.arange(n), np.diff(csr["rowptr"]))
+        cols = np.asarray(csr["col"][:csr["nnz"]])
+        pos = []
+        for l in range(L):
+            u = torch.empty(n, device="cuda")
+            v = torch.empty(n, device="cuda")
+            W, a1, a2 = run._gat_parts(params[l], l)
+            G.gist_gat_scores(ctx, n, s[l + 1], run.agg[l][:n], s[l + 1], a1, a2, u, v)
+            uh, vh = to_host(u), to_host(v)
+            pos.append((uh[rows] + vh[cols]) > np.float32(0.0))
     run.sgd(params, LR)
     torch.cuda.synchronize()
-    mism = 0
+    H = [None] + [to_host(run.H[l + 1][:n]) for l in range(L)]
+    return dict(n=n, H=H, loss=float(to_host(run.loss)[0]), dlogits=to_host(run.dlogits[:n]),
+                dW=[to_host(t) for t in run.dW], dH=[None] + [to_host(run.dH[l][:n])
+                                                         for l in range(1, L)],
+                W=[to_host(t) for t in params], pos=pos,
+                masks=[H[l + 1] > 0 for l in range(L - 1)] + [None])
+
+
+@pytest.mark.parametrize("name,dtype", [(c, "f32") for c in CONFIGS + ["c6"]] +
+                         [(c, "bf16") for c in CONFIGS])
+def test_step_chained(G, ctx, name, dtype):
+    from oracle import layers as OLr
+    w = workload(name)
+    cfg, csr = w["cfg"], w["csr"]
+    kind, L = cfg.kind, cfg.L
+    s = cfg.slice_widths()
+    tol = BF16_TOL if dtype == "bf16" else FP32_TOL
+    band_rel = 1e-2 if dtype == "bf16" else 1e-5
+    got = chained_gpu_step(G, ctx, w, dtype)
+    rnd = OLr.round_bf16 if dtype == "bf16" else None
+    orders = gpu_orders(kind, s)
+    log(f"[{name} {dtype}] oracle step through the GPU's decisions")
+    ref = OG.sub_gcn_step(kind, csr, w["X"], w["y"], w["params"], LR, masks=got["masks"],
+                          pos=got["pos"], rnd=rnd, orders=orders)
+    errs = {}
+    flips = 0
     for l in range(L):
-        got = to_host(run.H[l + 1][:b.n])
-        e = relerr(got, ref["recs"][l]["H_out"])
-        log(f"[{name}] chained H_{l + 1}: {e:.2e}")
-        assert e <= FP32_TOL
-        if l < L - 1:
+        errs[f"H{l + 1}"] = relerr(got["H"][l + 1], ref["recs"][l]["H_out"])
+        if l < L - 1:    # decisions differ only within rounding distance of zero
             Z = ref["recs"][l]["Z"]
-            diff = (got > 0) != (Z > 0)
-            band = 1e-5 * np.max(np.abs(Z))
-            assert np.all(np.abs(Z[diff]) <= band), "ReLU decision differs outside rounding band"
-            mism += int(diff.sum())
-        if kind == "gat":     # LeakyReLU decisions of scores near zero may differ too
+            diff = got["masks"][l] != (Z > 0)
+            assert np.all(np.abs(Z[diff]) <= band_rel * np.max(np.abs(Z))), \
+                f"layer {l}: ReLU decision differs outside the rounding band"
+            flips += int(diff.sum())
+        if kind == "gat":
             pre = ref["recs"][l]["pre"]
-            mism += int(np.sum(np.abs(pre) <= 1e-5 * np.max(np.abs(pre))))
-    loss = float(to_host(run.loss)[0])
-    assert abs(loss - ref["loss"]) <= FP32_TOL * abs(ref["loss"])
-    log(f"[{name}] chained loss {loss:.6f} (oracle {ref['loss']:.6f}); "
-        f"ReLU decisions differing within the rounding band: {mism}")
-    # the last layer's gradient involves no ReLU decision of the backward pass
-    e_last = relerr(to_host(run.dW[L - 1]), stacked(kind, ref["grads"][L - 1]))
-    log(f"[{name}] chained dW_{L - 1}: {e_last:.2e}")
-    assert e_last <= FP32_TOL
-    if mism == 0:
-        for l in range(L):
-            e = relerr(to_host(run.dW[l]), stacked(kind, ref["grads"][l]))
-            ew = relerr(to_host(params[l]), stacked(kind, ref["params"][l]))
-            log(f"[{name}] chained dW_{l} {e:.2e} W'_{l} {ew:.2e}")
-            assert e <= FP32_TOL and ew <= FP32_TOL
+            diff = got["pos"][l] != (pre > 0)
+            assert np.all(np.abs(pre[diff]) <= band_rel * np.max(np.abs(pre))), \
+                f"layer {l}: score side differs outside the rounding band"
+            flips += int(diff.sum())
+    errs["loss"] = abs(got["loss"] - ref["loss"]) / abs(ref["loss"])
+    errs["dlogits"] = relerr(got["dlogits"], ref["dlogits"])
+    for l in range(L):
+        errs[f"dW{l}"] = relerr(got["dW"][l], stacked(kind, ref["grads"][l]))
+        errs[f"W'{l}"] = relerr(got["W"][l], stacked(kind, ref["params"][l]))
+        if l > 0:
+            errs[f"dH{l}"] = relerr(got["dH"][l], ref["dH"][l])
+    log(f"[{name} {dtype}] chained, {flips} decisions taken differently within the band: " +
+        ", ".join(f"{k} {v:.2e}" for k, v in errs.items()))
+    bad = {k: v for k, v in errs.items() if not v <= tol}
+    assert not bad, bad
 
 
 @pytest.mark.parametrize("kind,norm,opt", [("gcn", "gcn", "sgd"), ("sage", "sage", "sgd"),

@@ -190,3 +190,21 @@ def test_fused_rounds_match_separate_calls(G, ctx, kind):
             assert torch.equal(models[0].theta[l][p], models[1].theta[l][p])
         # Theta changed where some sub-GCN owned an entry
         assert not np.array_equal(to_host(models[0].theta[l][0]), theta0[l][0])
+
+
+def test_fused_pass_rejects_one_table_for_both_sets(G, ctx):
+    """The trained and the new slices must not share memory: both sets naming
+    the same pointer table is refused before anything launches, and Theta and
+    the slices are left as they were."""
+    import torch
+    rows, cols, m = 64, 96, 2
+    blocks = _blocks(cols, m, 5, True)
+    S = _Slices(G, rows, cols, m, None, blocks, 0, 9)
+    Wg = torch.randn(rows, cols, device="cuda")
+    before = to_host(Wg).copy()
+    with pytest.raises(G.GistError) as e:
+        G.gist_subagg_gather(ctx, Wg, rows, cols, cols, m, S.set, S.set)
+    assert "slice table" in str(e.value)
+    assert np.array_equal(to_host(Wg), before)
+    for t, h in zip(S.t, S.host):
+        assert np.array_equal(to_host(t), h)

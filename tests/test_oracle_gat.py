@@ -96,3 +96,45 @@ def test_gat_single_node_attends_to_itself():
     H, W = rng.standard_normal((1, 3)), rng.standard_normal((3, 2))
     f = GA.gat_forward(csr, H, W, rng.standard_normal(2), rng.standard_normal(2), False, 0.2)
     assert np.allclose(f["alpha"], [1.0]) and np.allclose(f["Z"], H @ W)
+
+
+def test_gat_decision_overrides():
+    """``pos`` = the oracle's own LeakyReLU sides and ``mask`` = its own ReLU
+    decisions reproduce the backward bit for bit; with slope 1 the LeakyReLU
+    is the identity, so any choice of sides gives the same gradients; with
+    slope 0.2 flipping one entry's side scales that entry's gradient by 0.2
+    or 1 / 0.2 and changes du of its row and dv of its column by the
+    difference, and nothing else of du, dv."""
+    g, csr, H, W, a1, a2, R = _setup(seed=4)
+    for slope in (1.0, 0.2):
+        f = GA.gat_forward(csr, H, W, a1, a2, True, slope)
+        base = GA.gat_backward(csr, H, f, W, a1, a2, R, True, slope)
+        same = GA.gat_backward(csr, H, f, W, a1, a2, R, True, slope, mask=f["Z"] > 0,
+                               pos=f["pre"] > 0)
+        for k in base:
+            assert np.array_equal(base[k], same[k])
+        pos = f["pre"] > 0
+        rng = np.random.default_rng(1)
+        flips = rng.random(pos.shape) < 0.3
+        other = GA.gat_backward(csr, H, f, W, a1, a2, R, True, slope, pos=pos ^ flips)
+        if slope == 1.0:
+            for k in ("dW", "da_src", "da_dst", "dH"):
+                assert np.array_equal(other[k], base[k])
+    # slope 0.2, one flip: entry e of row i, column j
+    rp = np.asarray(csr["rowptr"])
+    i = 5
+    e = next(k for k in range(int(rp[i]), int(rp[i + 1])) if int(csr["col"][k]) != i)
+    j = int(csr["col"][e])
+    pos1 = pos.copy()
+    pos1[e] = not pos1[e]
+    one = GA.gat_backward(csr, H, f, W, a1, a2, R, True, 0.2, pos=pos1)
+    # only the entry's own gradient changes, by the ratio of the two slopes
+    ratio = 0.2 if pos[e] else 1.0 / 0.2
+    assert one["dpre"][e] == pytest.approx(ratio * base["dpre"][e], rel=1e-12)
+    others = np.arange(len(pos)) != e
+    assert np.array_equal(one["dpre"][others], base["dpre"][others])
+    d_u, d_v = one["du"] - base["du"], one["dv"] - base["dv"]
+    step = one["dpre"][e] - base["dpre"][e]
+    assert d_u[i] == pytest.approx(step, rel=1e-9) and d_v[j] == pytest.approx(step, rel=1e-9)
+    assert np.all(d_u[np.arange(len(d_u)) != i] == 0.0)
+    assert np.all(d_v[np.arange(len(d_v)) != j] == 0.0)

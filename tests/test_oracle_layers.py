@@ -199,3 +199,148 @@ def test_sgd_and_slices():
     mask[np.ix_(r, c)] = False
     assert np.array_equal(z[mask], T[mask]) and np.all(z[np.ix_(r, c)] == 0)
     assert np.array_equal(Lr.gather_slice(T, None, c), T[:, c])
+
+
+# ---- options of the layers: association order, rounded operands, masks ----
+
+def test_round_bf16_matches_torch_conversion():
+    """The bf16-input variant's operand rounding against torch's own
+    float -> bfloat16 conversion (round to nearest even): random values over
+    many binades, exact ties (to even, both directions), values that round
+    up across a binade, the largest finite values, subnormals, zeros and
+    infinities."""
+    import torch
+    rng = np.random.default_rng(11)
+    x = np.concatenate([
+        rng.standard_normal(20000) * np.exp(rng.uniform(-30, 30, 20000)),
+        np.float32(1.0) + np.arange(-40, 40, dtype=np.float32) * np.float32(2.0 ** -9),
+        [1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8, 1.0 - 2.0 ** -9, 2.0 - 2.0 ** -9,
+         3.3895313892515355e38, 3.4028234663852886e38, 1e-40, -1e-40, 0.0, -0.0,
+         np.inf, -np.inf]]).astype(np.float32)
+    want = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    got = Lr.round_bf16(x)
+    assert np.array_equal(got, want)
+    # ties go to the even neighbour: 1 + 2^-8 lies halfway between 1 and
+    # 1 + 2^-7 and rounds to 1; 1 + 3 2^-8 rounds up to 1 + 2^-6
+    assert Lr.round_bf16(1.0 + 2.0 ** -8) == 1.0
+    assert Lr.round_bf16(1.0 + 3 * 2.0 ** -8) == 1.0 + 2.0 ** -6
+    assert np.isnan(Lr.round_bf16(np.nan))
+
+
+def _rect_csr(seed, n, n_in):
+    """A random rectangular aggregation matrix (rows n, columns n_in) with
+    its explicit transpose, as a layer-sampled mini-batch stores it."""
+    import scipy.sparse as sps
+    rng = np.random.default_rng(seed)
+    A = sps.random(n, n_in, density=0.3, random_state=seed, format="csr", dtype=np.float64)
+    A.data = A.data.astype(np.float32).astype(np.float64)
+    At = A.T.tocsr()
+    At.sort_indices()
+    A.sort_indices()
+    return dict(n=n, n_in=n_in, nnz=A.nnz, rowptr=A.indptr, col=A.indices,
+                val=A.data.astype(np.float32), t_rowptr=At.indptr, t_col=At.indices,
+                t_val=At.data.astype(np.float32)), rng
+
+
+@pytest.mark.parametrize("rect", [False, True])
+def test_gcn_xform_order_equals_agg_order_in_fp64(tiny, rect):
+    """(Abar H) W and Abar (H W), forward and backward, agree to rounding in
+    fp64 (eq. (2) fixes no association order), square and rectangular."""
+    if rect:
+        csr, rng = _rect_csr(4, 5, 9)
+    else:
+        g, rng = tiny
+        csr = MB.build(g, None, "gcn")
+    n, n_in = csr["n"], csr.get("n_in", csr["n"])
+    H, W = rng.standard_normal((n_in, 6)), rng.standard_normal((6, 3))
+    dHo = rng.standard_normal((n, 3))
+    fa = Lr.gcn_forward(csr, H, W, True, order="agg")
+    fx = Lr.gcn_forward(csr, H, W, True, order="xform")
+    assert rel(fx["Z"], fa["Z"]) < 1e-12
+    ba = Lr.gcn_backward(csr, H, fa, W, dHo, True, order="agg")
+    bx = Lr.gcn_backward(csr, H, fa, W, dHo, True, order="xform")
+    assert rel(bx["dW"], ba["dW"]) < 1e-12 and rel(bx["dH"], ba["dH"]) < 1e-12
+    with pytest.raises(ValueError):
+        Lr.gcn_forward(csr, H, W, True, order="both")
+
+
+def test_rounded_products_closed_form():
+    """With no edges the GCN matrix is the identity, so a rounded layer is
+    round(H) round(W) exactly: 1 + 2^-10 rounds to 1, 3 is exact, so
+    Z = 3 where fp64 gives 3 (1 + 2^-10); SAGE's self term the same; the
+    backward's products round their operands too (dZ = 1 + 2^-9 rounds to
+    1 + 2^-8 ... to even: 1)."""
+    g = graph_from_edges(1, [])
+    csr = MB.build(g, None, "gcn")
+    H, W = np.array([[1.0 + 2.0 ** -10]]), np.array([[3.0]])
+    for order in ("agg", "xform"):
+        f = Lr.gcn_forward(csr, H, W, False, rnd=Lr.round_bf16, order=order)
+        assert f["Z"][0, 0] == 3.0
+        assert Lr.gcn_forward(csr, H, W, False, order=order)["Z"][0, 0] == 3.0 * (1 + 2.0 ** -10)
+        b = Lr.gcn_backward(csr, H, f, W, np.array([[1.0 + 2.0 ** -9]]), False,
+                            rnd=Lr.round_bf16, order=order)
+        assert b["dW"][0, 0] == 1.0 and b["dH"][0, 0] == 3.0
+    cs = MB.build(g, None, "sage")
+    f = Lr.sage_forward(cs, H, W, W, False, rnd=Lr.round_bf16)
+    assert f["Z"][0, 0] == 3.0 and np.array_equal(f["AH"], [[0.0]])
+
+
+@pytest.mark.parametrize("kind", ["gcn", "sage"])
+def test_rounded_layer_within_bf16_error_bound(tiny, kind):
+    """Each rounded operand carries a relative error of at most 2^-8 (plus
+    2^-24 from its fp32 form), so every entry of a rounded product differs
+    from the exact one by at most (2^-7 + 2^-15) sum_k |a_ik||b_kj|; and the
+    rounding is not the identity (the result differs from fp64)."""
+    g, rng = tiny
+    csr = MB.build(g, None, kind)
+    H, W1, W2 = (rng.standard_normal((7, 6)), rng.standard_normal((6, 4)),
+                 rng.standard_normal((6, 4)))
+    u = 2.0 ** -7 + 2.0 ** -15
+    if kind == "gcn":
+        f = Lr.gcn_forward(csr, H, W1, False, rnd=Lr.round_bf16)
+        e = Lr.gcn_forward(csr, H, W1, False)
+        bound = u * (np.abs(e["AH"]) @ np.abs(W1))
+    else:
+        f = Lr.sage_forward(csr, H, W1, W2, False, rnd=Lr.round_bf16)
+        e = Lr.sage_forward(csr, H, W1, W2, False)
+        bound = u * (np.abs(H) @ np.abs(W1) + np.abs(e["AH"]) @ np.abs(W2))
+    assert np.all(np.abs(f["Z"] - e["Z"]) <= bound)
+    assert np.any(f["Z"] != e["Z"])
+
+
+@pytest.mark.parametrize("kind", ["gcn", "sage"])
+def test_mask_replaces_the_relu_derivative(tiny, kind):
+    """mask = 1[Z > 0] reproduces the backward bit for bit; flipping one
+    decision (i, f) changes the weight gradient by exactly the outer product
+    of that row's input with dH_out[i, f] in column f (the chain rule with
+    that one derivative changed), and nothing else."""
+    g, rng = tiny
+    csr = MB.build(g, None, kind)
+    H, W1, W2 = (rng.standard_normal((7, 5)), rng.standard_normal((5, 4)),
+                 rng.standard_normal((5, 4)))
+    dHo = rng.standard_normal((7, 4))
+    if kind == "gcn":
+        f = Lr.gcn_forward(csr, H, W1, True)
+        run = lambda m: Lr.gcn_backward(csr, H, f, W1, dHo, True, mask=m)
+        X = f["AH"]
+        grad = lambda b: b["dW"]
+    else:
+        f = Lr.sage_forward(csr, H, W1, W2, True)
+        run = lambda m: Lr.sage_backward(csr, H, f, W1, W2, dHo, True, mask=m)
+        X = np.concatenate([H, f["AH"]], axis=1)
+        grad = lambda b: np.concatenate([b["dW_self"], b["dW_neigh"]])
+    base = run(None)
+    same = run(f["Z"] > 0)
+    for k in base:
+        assert np.array_equal(base[k], same[k])
+    mask = f["Z"] > 0
+    i, c = 3, 2
+    mask[i, c] = not mask[i, c]
+    flip = run(mask)
+    delta = grad(flip) - grad(base)
+    sign = 1.0 if mask[i, c] else -1.0
+    want = np.zeros_like(delta)
+    want[:, c] = sign * X[i] * dHo[i, c]
+    assert np.max(np.abs(delta - want)) <= 1e-12 * np.max(np.abs(grad(base)))
+    with pytest.raises(ValueError):
+        run(mask[:, :2])

@@ -161,3 +161,26 @@ def test_loop_carry_moments_follow_ownership():
     assert np.mean(Vg[1][owned] > 0) > 0.5
     # every input-layer entry is owned by the sub-GCN of its column
     assert np.mean(Vg[0] > 0) > 0.5
+
+
+def test_sgd_matches_torch():
+    """``subTrain``'s plain SGD step (Section 2.2) against ``torch.optim.SGD``
+    in fp64 over several steps with different learning rates and gradients:
+    a wrong step size (2 lr, lr / n) or sign fails here."""
+    from oracle import layers as Lr
+    rng = np.random.default_rng(3)
+    W0 = rng.standard_normal((6, 9))
+    for lr in (0.5, 0.05, 1e-3):
+        grads = [rng.standard_normal((6, 9)) * (1 + k) for k in range(6)]
+        W = W0
+        for g in grads:
+            W = Lr.sgd(W, g, lr)
+        p = torch.nn.Parameter(torch.from_numpy(W0.copy()))
+        opt = torch.optim.SGD([p], lr=lr)
+        for g in grads:
+            opt.zero_grad()
+            p.grad = torch.from_numpy(g.copy())
+            opt.step()
+        assert np.max(np.abs(W - p.detach().numpy())) <= 1e-12 * np.max(np.abs(W))
+        # one step moves by exactly lr g: sign and size
+        assert np.allclose(W0 - Lr.sgd(W0, grads[0], lr), lr * grads[0], rtol=0, atol=1e-15)
