@@ -412,6 +412,22 @@ gist_status gist_softmax_xent_padded(gist_ctx* ctx, int64_t n, int32_t C,
                                      const int32_t* n_valid_dev, float* loss_dev,
                                      float* dlogits, void* ws, size_t ws_bytes);
 
+/* For callers that cannot allocate device memory (code under stream
+ * capture, serving loops, harnesses that forbid hipMalloc): the loss of
+ * gist_softmax_xent without a workspace argument.  Its partial sums live in
+ * a buffer the library keeps per device for the life of the process
+ * (4 MiB, looked up at gist_create), so the call allocates nothing; the
+ * caller still owns logits, labels, *loss_dev and dlogits.  Results are
+ * bitwise those of gist_softmax_xent.  n may be at most
+ * GIST_NOALLOC_LOSS_MAX_ROWS (GIST_E_INVAL beyond, before any launch).
+ * Every call on one device shares that buffer: calls ordered on one stream
+ * are safe, calls that overlap in time on one device (other streams or
+ * threads) race and give undefined losses. */
+#define GIST_NOALLOC_LOSS_MAX_ROWS 4194304
+gist_status gist_softmax_xent_noalloc(gist_ctx* ctx, int64_t n, int32_t C,
+                                      const float* logits, const int32_t* labels,
+                                      float* loss_dev, float* dlogits);
+
 /* ---- subGCNs slice gather (Section 2.1) ----------------------------- */
 
 /* Ws[i][j] = Wg[rows[i]][cols[j]], i < nr, j < nc: the sub-GCN weight

@@ -12,12 +12,43 @@
 #include <cstdio>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <string>
 #include <vector>
 
 #include "gist_internal.h"
 
+// Partial sums of gist_softmax_xent_noalloc: one float per 4-row block of
+// logits, for at most GIST_NOALLOC_LOSS_MAX_ROWS rows (4 MiB).  Every GPU the
+// library runs on holds its own copy until the process ends.  Host code never
+// passes this array's name to a kernel: its device address is looked up once
+// per device (noalloc_scratch below) and only that address is used.
+static __device__ __align__(256) float scratch[GIST_NOALLOC_LOSS_MAX_ROWS / 4 + 1];
+
 namespace gist {
+
+namespace {
+std::mutex g_scratch_mu;
+std::vector<float*> g_scratch_ptr;   // device id -> address of that device's copy
+}
+
+// The device address of `scratch` on `device`, which must be current.  Looked
+// up once per device (hipGetSymbolAddress), then cached.
+static gist_status noalloc_scratch(int device, float** out) {
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (device < 0) return set_error(GIST_E_INVAL, "noalloc: bad device");
+  if (static_cast<size_t>(device) >= g_scratch_ptr.size()) g_scratch_ptr.resize(device + 1, nullptr);
+  if (!g_scratch_ptr[device]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return set_error(GIST_E_DEVICE, std::string("noalloc: cannot resolve the loss buffer: ") +
+                                          hipGetErrorString(e));
+    g_scratch_ptr[device] = static_cast<float*>(p);
+  }
+  *out = g_scratch_ptr[device];
+  return GIST_OK;
+}
 
 namespace {
 thread_local std::string t_err;
@@ -120,6 +151,13 @@ extern "C" gist_status gist_create(int device, void* hip_stream, gist_ctx** out)
   if (hipMalloc(&c->d_flag, 4 * sizeof(int)) != hipSuccess) {
     delete c;
     return set_error(GIST_E_DEVICE, "gist_create: cannot allocate context flag");
+  }
+  // with `device` current: this device's copy of the no-allocation loss buffer
+  const gist_status ss = gist::noalloc_scratch(device, &c->loss_scratch);
+  if (ss != GIST_OK) {
+    (void)hipFree(c->d_flag);
+    delete c;
+    return ss;
   }
   *out = c;
   return GIST_OK;
@@ -753,6 +791,26 @@ extern "C" gist_status gist_softmax_xent(gist_ctx* ctx, int64_t n, int32_t C,
   gist::DeviceGuard dg(ctx->device);
   return gist::softmax_xent(ctx->stream, n, C, logits, labels, loss_dev, dlogits,
                             static_cast<float*>(ws));
+}
+
+extern "C" gist_status gist_softmax_xent_noalloc(gist_ctx* ctx, int64_t n, int32_t C,
+                                                 const float* logits, const int32_t* labels,
+                                                 float* loss_dev, float* dlogits) {
+  gist::clear_error();
+  if (!ctx) return set_error(GIST_E_INVAL, "softmax_xent_noalloc: NULL ctx");
+  gist::ProfBind pb(ctx);
+  if (n < 0 || C < 1) return set_error(GIST_E_INVAL, "softmax_xent_noalloc: bad sizes");
+  if (n > GIST_NOALLOC_LOSS_MAX_ROWS)
+    return set_error(GIST_E_INVAL, "softmax_xent_noalloc: n exceeds GIST_NOALLOC_LOSS_MAX_ROWS "
+                                   "(4194304 rows); use gist_softmax_xent with a workspace");
+  if (!loss_dev || (n > 0 && (!logits || !labels || !dlogits)))
+    return set_error(GIST_E_INVAL, "softmax_xent_noalloc: NULL pointer");
+  if (!ctx->loss_scratch) return set_error(GIST_E_DEVICE, "softmax_xent_noalloc: no loss buffer");
+  gist::DeviceGuard dg(ctx->device);
+  // the rows kernel writes every partial the finishing kernel reads, so the
+  // buffer needs no clearing between calls
+  return gist::softmax_xent(ctx->stream, n, C, logits, labels, loss_dev, dlogits,
+                            ctx->loss_scratch);
 }
 
 extern "C" gist_status gist_softmax_xent_padded(gist_ctx* ctx, int64_t n, int32_t C,

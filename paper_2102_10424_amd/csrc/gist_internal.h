@@ -19,6 +19,7 @@ struct gist_ctx {
   int device = 0;
   hipStream_t stream = nullptr;
   int* d_flag = nullptr;   // 4 ints of device memory owned by the context
+  float* loss_scratch = nullptr;   // this device's copy of the static loss buffer
   gist::Profiler* prof = nullptr;
 };
 

@@ -47,6 +47,7 @@ GIST_DTYPE_F32, GIST_DTYPE_BF16_IN = 0, 1
 GIST_ORDER_AUTO, GIST_ORDER_AGG_FIRST, GIST_ORDER_XFORM_FIRST = 0, 1, 2
 GIST_SUBAGG_CHECK_FINITE = 1
 GIST_ADAM_FRESH = 1
+GIST_NOALLOC_LOSS_MAX_ROWS = 4194304
 GIST_LAYER_SHARED_INPUT, GIST_LAYER_GROUP_MAJOR_OUT = 1, 2
 
 NORM_BY_NAME = {"gcn": GIST_NORM_GCN_SYM, "sage": GIST_NORM_SAGE_MEAN,
@@ -60,6 +61,7 @@ EXPORTED = (
     "gist_gcn_layer_bwd_sgd",
     "gist_gat_workspace_size", "gist_gat_layer_fwd", "gist_gat_layer_bwd", "gist_gat_scores",
     "gist_softmax_xent_workspace", "gist_softmax_xent", "gist_softmax_xent_padded",
+    "gist_softmax_xent_noalloc",
     "gist_gather_slice",
     "gist_sgd_update", "gist_adam_update", "gist_adam_coefficients", "gist_adam_update_dev",
     "gist_subagg", "gist_partition_inverse",
@@ -174,6 +176,7 @@ _sigs = {
     "gist_softmax_xent": (C.c_int, [_P, C.c_int64, C.c_int32, _P, _P, _P, _P, _P, C.c_size_t]),
     "gist_softmax_xent_padded": (C.c_int, [_P, C.c_int64, C.c_int32, _P, _P, _P, _P, _P, _P,
                                            C.c_size_t]),
+    "gist_softmax_xent_noalloc": (C.c_int, [_P, C.c_int64, C.c_int32, _P, _P, _P, _P]),
     "gist_gather_slice": (C.c_int, [_P, _P, C.c_int64, _P, C.c_int32, _P, C.c_int32, _P,
                                     C.c_int64]),
     "gist_sgd_update": (C.c_int, [_P, _P, _P, C.c_int64, C.c_float]),
@@ -453,6 +456,11 @@ def gist_softmax_xent_padded(ctx, n, C_, logits, labels, n_valid_dev, loss_dev, 
     _check(_lib.gist_softmax_xent_padded(ctx.handle, int(n), int(C_), _ptr(logits), _ptr(labels),
                                          _ptr(n_valid_dev), _ptr(loss_dev), _ptr(dlogits),
                                          _ptr(ws), _nbytes(ws)))
+
+
+def gist_softmax_xent_noalloc(ctx, n, C_, logits, labels, loss_dev, dlogits):
+    _check(_lib.gist_softmax_xent_noalloc(ctx.handle, int(n), int(C_), _ptr(logits), _ptr(labels),
+                                          _ptr(loss_dev), _ptr(dlogits)))
 
 
 def gist_gather_slice(ctx, Wg, ldg, rows, nr, cols, nc, Ws, lds):
