@@ -19,10 +19,16 @@ Inputs are seeded synthetic data resident in HBM before timing starts.
 The reported value is ms per sub-GCN step = round time / (m zeta), with zeta
 local steps per sub-GCN per round (default 1; ``--optimizer adam`` trains
 with Adam as the paper's experiments do, its moments carried with the
-weights through subAgg or reset each round).  Kernel times
-come from HIP events the library records on the launch stream during the
-timed rounds (gist_profile_*).  The CPU baseline is the fp64 oracle timed on
-one sub-GCN step of the same workload.
+weights through subAgg or reset each round).  The timed rounds carry no
+per-kernel instrumentation: a HIP event at every round boundary gives the
+per-round times (p10 / p50 / p90).  Kernel times come from a separate pass
+of the same number of rounds in which the library records HIP event pairs
+on the launch stream around every launch (gist_profile_*).  The default c4
+run then measures, outside the timed region, the two other figures the
+targets name: the full-graph aggregation of c5 (against HBM bandwidth) and
+the bf16-input hidden-layer GEMMs of c4 (against the bf16 MFMA peak).  The
+CPU baseline is the fp64 oracle timed on one sub-GCN step of the same
+workload (and, with the extra figures, on the whole c5 aggregation).
 
 Prints ONE JSON line.  ``--gpus N`` with N > 1 exits: the benchmark runs on
 exactly one GPU.
@@ -111,6 +117,21 @@ def parse():
                     help="skip the library's per-launch event timing")
     ap.add_argument("--copy-calib", action="store_true",
                     help="only run a plain 1 GiB row copy (counter calibration)")
+    ap.add_argument("--loss-curves", action="store_true",
+                    help="only train GIST with Adam for m in {1, 2, 4, 8} and both moment "
+                         "policies on a learnable c3-graph task and print the loss per round")
+    ap.add_argument("--curve-rounds", type=int, default=20)
+    ap.add_argument("--curve-zeta", type=int, default=10)
+    ap.add_argument("--aggregation", default="gather", choices=["tile", "gather"],
+                    help="cluster mini-batches and the c5 matrix: the gather kernel, or the "
+                         "matrix-core tiles of GIST_LAYER_CLUSTERED (slower on these shapes)")
+    ap.add_argument("--curve-hidden", type=int, default=256)
+    ap.add_argument("--curve-lr", type=float, default=0.01)
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the extra figures (c5 aggregation, c4 bf16 GEMMs) measured after "
+                         "the timed region of the default c4 run")
+    ap.add_argument("--profile-steps", type=int, default=0,
+                    help="steps of the separate profiled pass (0: as many as --steps)")
     return ap.parse_args()
 
 
@@ -119,7 +140,7 @@ class RoundWorkload:
     """A GIST round (partition, gather, m sub-GCN steps, subAgg) on one GPU."""
 
     def __init__(self, cfg, ctx, dtype, optimizer="sgd", policy="carry", zeta=1, shared=False,
-                 streams=1, graphs=False, lr=0.01):
+                 streams=1, graphs=False, lr=0.01, clustered=True):
         import torch
         from paper_2102_10424_amd import gist as G
         from paper_2102_10424_amd.step import (BatchPipeline, BatchSlot, ClusterGraphRunner,
@@ -194,7 +215,7 @@ class RoundWorkload:
                                         self._cluster_order(shared, zeta, k, self.nstreams),
                                         depth=8, workers=(12 if graphs else 4) // self.nstreams,
                                         slots=[FixedBatchSlot(c, self.norm, cap_n, cap_nnz,
-                                                              cfg.widths[0])
+                                                              cfg.widths[0], clustered=clustered)
                                                for _ in range(12 if graphs else 8)],
                                         build=self._fixed_build)
                           for k, c in enumerate(self.ctxs)]
@@ -215,7 +236,7 @@ class RoundWorkload:
             elif graphs:
                 self.graph_runners = [
                     ClusterGraphRunner(c, cfg.kind, self.model.slice_widths, cap_n, cap_nnz,
-                                       cfg.widths[0], self.X, dtype=dt)
+                                       cfg.widths[0], self.X, dtype=dt, clustered=clustered)
                     for c in self.ctxs]
         self.t = 0
 
@@ -388,7 +409,7 @@ class LayerWorkload:
     def finish(self):
         pass
 
-    def __init__(self, cfg, ctx, dtype, d_in):
+    def __init__(self, cfg, ctx, dtype, d_in, clustered=True):
         import torch
         from paper_2102_10424_amd import gist as G
         from paper_2102_10424_amd.step import BatchSlot
@@ -400,7 +421,7 @@ class LayerWorkload:
         log(f"[bench] graph n={self.graph.n} nnz={self.graph.nnz} ({time.time() - t0:.1f}s)")
         gh = G.GraphHandle(self.graph)
         n = self.graph.n
-        self.slot = BatchSlot(ctx, "gcn", n, self.graph.nnz + n, d_in)
+        self.slot = BatchSlot(ctx, "gcn", n, self.graph.nnz + n, d_in, clustered=clustered)
         self.X = torch.from_numpy(cfg.features_matrix()).cuda()
         self.b = self.slot.load(gh, None, self.X, cfg.labels())
         torch.cuda.synchronize()
@@ -413,7 +434,8 @@ class LayerWorkload:
                             self.s_out)
         self.dHo = torch.from_numpy(cfg.upstream(n, self.s_out)).cuda()
         self.desc = G.layer_desc(G.GIST_LAYER_GCN, G.GIST_ACT_RELU, n, d_in, self.s_out,
-                                 G.GIST_DTYPE_BF16_IN if dtype == "bf16" else G.GIST_DTYPE_F32)
+                                 G.GIST_DTYPE_BF16_IN if dtype == "bf16" else G.GIST_DTYPE_F32,
+                                 flags=G.GIST_LAYER_CLUSTERED if clustered else 0)
         f, bb = G.gist_layer_workspace_size(self.desc)
         self.ws = torch.empty(max(f, bb), dtype=torch.uint8, device="cuda")
         self.agg = torch.empty(n, d_in, device="cuda")
@@ -477,6 +499,268 @@ def copy_calibration(G, ctx):
                       "gbs": v["bytes"] / (v["ms"] * 1e-3) / 1e9}), flush=True)
 
 
+def cpu_info():
+    """Host facts for the CPU baseline: logical CPUs, the CPU model and the
+    threads the BLAS behind NumPy / SciPy actually uses."""
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    return {"cores": int(threads), "logical_cpus": os.cpu_count(), "cpu_model": model,
+            "blas_threads": int(threads)}
+
+
+def timed_pass(wl, steps):
+    """K steps with no per-kernel instrumentation: a HIP event on the launch
+    stream at every step boundary (per-step times), and the host clock around
+    the whole pass between two device synchronisations (the mean)."""
+    import torch
+    st = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev[0].record(st)
+    for s in range(steps):
+        wl.step()
+        ev[s + 1].record(st)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    return (t1 - t0) * 1e3 / steps, [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+
+
+def merged_profile(G, ctxs):
+    prof, dropped = {}, 0
+    for c in ctxs:   # every stream's launches (their event times may overlap)
+        p, d = G.gist_profile_read(c)
+        G.gist_profile_end(c)
+        dropped += d
+        for k, v in p.items():
+            acc = prof.setdefault(k, dict(launches=0, ms=0.0, flops=0.0, bytes=0.0))
+            for f in acc:
+                acc[f] += v[f]
+    return prof, dropped
+
+
+def is_gemm(name):
+    return name.startswith("gemm_") and "reduce" not in name and "fixup" not in name
+
+
+def hidden_gemms(prof, gflop, peak):
+    """Per variant: rate of the launches that are the hidden layers' products
+    (about `gflop` GFLOP each), as TFLOP/s and fraction of `peak`."""
+    out = {}
+    for k, v in prof.items():
+        if not is_gemm(k) or not v["launches"]:
+            continue
+        per = v["flops"] / v["launches"] / 1e9
+        if abs(per - gflop) > 0.02 * gflop:
+            continue
+        t = v["flops"] / (v["ms"] * 1e-3) / 1e12
+        out[k] = {"tflops": round(t, 2), "frac": round(t / peak, 4), "launches": v["launches"],
+                  "avg_launch_us": round(1e3 * v["ms"] / v["launches"], 2)}
+    return out
+
+
+def north_star_figures(wl, ctx, steps, clustered=True):
+    """The two figures the default line does not time in its own workload,
+    measured after the timed region: the full-graph aggregation of c5 (Abar H
+    over the whole c4 graph, width 256, fp32) against HBM bandwidth, and the
+    bf16-input hidden-layer GEMMs of c4 against the bf16 MFMA peak (sub-GCN
+    steps on the round's own mini-batches and weights, on copies)."""
+    import torch
+    from paper_2102_10424_amd import gist as G
+    from paper_2102_10424_amd.step import BatchSlot, SubGCN
+    out = {}
+    cfg = wl.cfg
+    # --- c4 bf16 hidden GEMMs
+    runner = SubGCN(ctx, cfg.kind, wl.model.slice_widths, wl.runner.n_cap,
+                    dtype=G.GIST_DTYPE_BF16_IN)
+    params = [p.clone() for p in wl.model.params[0]]
+    b = wl.pipes[0].next()
+    runner.step(b, params, wl.lr)       # warm-up: workspace and code objects
+    torch.cuda.synchronize()
+    G.gist_profile_begin(ctx, 1 << 14)
+    for _ in range(steps):
+        runner.step(wl.pipes[0].next(), params, wl.lr)
+    torch.cuda.synchronize()
+    prof, _ = merged_profile(G, [ctx])
+    s = wl.model.slice_widths
+    gf = 2.0 * 2 * s[1] * s[2] * 1633 / 1e9     # [H | Abar H] W at the mean batch size
+    g = hidden_gemms(prof, 109.565, PEAK["bf16"]) or hidden_gemms(prof, gf, PEAK["bf16"])
+    tot_f = sum(prof[k]["flops"] for k in g)
+    tot_ms = sum(prof[k]["ms"] for k in g)
+    out["gemm_c4_bf16"] = {
+        "what": f"c4 hidden-layer products with bf16-input MFMA ({steps} sub-GCN steps on the "
+                "round's mini-batches, copies of sub-GCN 0's slices; library HIP events)",
+        "variants": g, "tflops": round(tot_f / (tot_ms * 1e-3) / 1e12, 2) if tot_ms else None,
+        "peak": PEAK["bf16"], "unit": "TFLOP/s",
+        "frac": round(tot_f / (tot_ms * 1e-3) / 1e12 / PEAK["bf16"], 4) if tot_ms else None,
+        "target_frac": 0.5}
+    del runner, params
+    # --- c5 aggregation over the full graph, width 256
+    n = wl.graph.n
+    w = 256
+    slot = BatchSlot(ctx, "gcn", n, wl.graph.nnz + n, w)
+    gen = torch.Generator(device="cuda").manual_seed(105)
+    X = torch.randn(n, w, device="cuda", generator=gen)
+    bb = slot.load(wl.gh, None, X, wl.labels)
+    desc = G.layer_desc(G.GIST_LAYER_GCN, G.GIST_ACT_RELU, n, w, w, G.GIST_DTYPE_F32,
+                        G.GIST_ORDER_AGG_FIRST, flags=G.GIST_LAYER_CLUSTERED if clustered else 0)
+    fws, bws = G.gist_layer_workspace_size(desc)
+    ws = torch.empty(max(fws, bws, 1), dtype=torch.uint8, device="cuda")
+    W = torch.randn(w, w, device="cuda", generator=gen) / 16.0
+    agg = torch.empty(n, w, device="cuda")
+    Ho = torch.empty(n, w, device="cuda")
+    G.gist_gcn_layer_fwd(ctx, desc, bb.A, bb.X, W, agg, Ho, ws)
+    torch.cuda.synchronize()
+    G.gist_profile_begin(ctx, 1 << 10)
+    for _ in range(steps):
+        G.gist_gcn_layer_fwd(ctx, desc, bb.A, bb.X, W, agg, Ho, ws)
+    torch.cuda.synchronize()
+    prof, _ = merged_profile(G, [ctx])
+    agg_k = {k: v for k, v in prof.items() if k.startswith("spmm")}
+    a_ms = sum(v["ms"] for v in agg_k.values())
+    a_bytes = sum(v["bytes"] for v in agg_k.values())
+    launches = steps
+    gbs = a_bytes / (a_ms * 1e-3) / 1e9 if a_ms else None
+    out["spmm_c5"] = {
+        "what": f"c5: Abar H over the full {n}-node GCN matrix ({bb.nnz} entries), width {w}, "
+                f"fp32, {launches} calls (library HIP events; kernels: {sorted(agg_k)})",
+        "achieved": round(gbs, 1) if gbs else None, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+        "frac": round(gbs / HBM_PEAK_GBS, 4) if gbs else None,
+        "bytes_per_call": round(a_bytes / launches), "ms_per_call": round(a_ms / launches, 4),
+        "target_frac": 0.6,
+        "bytes_def": "4(n+1) + 8 nnz + 4 n w (X read once) + 4 n w (Y written once)"}
+    del slot, X, bb, agg, Ho, ws
+    torch.cuda.synchronize()
+    return out
+
+
+def c5_oracle_spmm_ms(graph, w=256):
+    """The oracle's aggregation over the whole c5 matrix at width 256, timed
+    in full (no extrapolation): fp64 Abar H with Abar from the oracle's own
+    CSR build, as a SciPy CSR product on one thread."""
+    import scipy.sparse as sp
+    from oracle import minibatch as OM
+    csr = OM.build(graph, None, "gcn")
+    n = csr["n"]
+    A = sp.csr_matrix((csr["val"].astype(np.float64), csr["col"], csr["rowptr"]), shape=(n, n))
+    H = np.random.default_rng(105).standard_normal((n, w))
+    t0 = time.perf_counter()
+    A @ H
+    return (time.perf_counter() - t0) * 1e3
+
+
+def loss_curves(G, ctx, rounds, zeta, lr=0.01, hidden=256, eval_clusters=40):
+    """Algorithm 1 trained with Adam (the paper's optimizer, no weight decay)
+    for m = 1 (the full model), 2, 4 and 8, with the moments carried through
+    subAgg or reset each round, on the c3 graph (232,965 nodes, 1,500
+    clusters, 20 per mini-batch) and a 3-layer GraphSAGE-mean 602-h-h-41.
+
+    Uniformly random labels carry no signal, so the labels here are planted
+    by a random one-layer teacher of the same family: y = argmax([X | mean of
+    the neighbours' X] T), T ~ N(0, 1) of shape 1204 x 41 (fp64 on the host).
+    Every run starts from the same Glorot weights and sees the same sequence
+    of mini-batches per (round, sub-GCN, local step).  After each round (its
+    subAgg applied) the global model's loss on a fixed set of 40 clusters is
+    evaluated (loss and accuracy); the mean loss of the round's local steps
+    is reported too."""
+    import torch
+    import scipy.sparse as sp
+    from gist_synth import get_config
+    from paper_2102_10424_amd.step import BatchSlot, GistModel, SubGCN
+    cfg = get_config("c3")
+    g = cfg.make_graph()
+    X = cfg.features_matrix()
+    n = g.n
+    deg = np.diff(g.rowptr).astype(np.float64)
+    A = sp.csr_matrix((np.ones(g.nnz), g.col, g.rowptr), shape=(n, n))
+    mean_nb = (A @ X.astype(np.float64)) / np.maximum(deg, 1.0)[:, None]
+    T = np.random.default_rng(7).standard_normal((2 * X.shape[1], 41))
+    y = np.argmax(np.concatenate([X, mean_nb], axis=1) @ T, axis=1).astype(np.int32)
+    del A, mean_nb
+    widths = [X.shape[1], hidden, hidden, 41]
+    gh = G.GraphHandle(g)
+    Xd = torch.from_numpy(X).cuda()
+    sizes = np.diff(g.cluster_ptr)
+    cap_n = int(np.sort(sizes)[-eval_clusters:].sum())
+    cap_nnz = int(np.sort(np.diff(g.rowptr))[-cap_n:].sum()) + cap_n
+    slot = BatchSlot(ctx, "sage", cap_n, cap_nnz, widths[0])
+    eval_slot = BatchSlot(ctx, "sage", cap_n, cap_nnz, widths[0])
+    eb = eval_slot.load(gh, np.arange(eval_clusters, dtype=np.int32) * 37 % g.n_clusters,
+                        Xd, y)
+    rng = np.random.default_rng(11)
+    theta0 = []
+    for l in range(3):
+        lim = np.sqrt(6.0 / (widths[l] + widths[l + 1]))
+        theta0.append([rng.uniform(-lim, lim, (widths[l], widths[l + 1])).astype(np.float32)
+                       for _ in range(2)])
+    batches = {}
+
+    def batch(t, i, z):
+        key = (t, i, z)
+        if key not in batches:
+            r = np.random.default_rng(1_000_000 + 10_000 * t + 100 * i + z)
+            batches[key] = np.sort(r.choice(g.n_clusters, 20, replace=False)).astype(np.int32)
+        return slot.load(gh, batches[key], Xd, y)
+
+    full = SubGCN(ctx, "sage", widths, cap_n)
+    eval_loss = torch.zeros(1, device="cuda")
+
+    def evaluate(model):
+        model.finalize()
+        params = [torch.cat([model.theta[l][0], model.theta[l][1]], 0) for l in range(3)]
+        logits = full.forward(eb, params)
+        full.loss_and_grad(eb, eval_loss)
+        acc = float((logits.argmax(dim=1).cpu() == eb.labels.cpu().long()).float().mean())
+        return float(eval_loss.cpu()[0]), acc
+
+    curves = {}
+    for m in (1, 2, 4, 8):
+        for policy in ("carry", "reset"):
+            t0 = time.time()
+            th = [[torch.from_numpy(p.copy()).cuda() for p in parts] for parts in theta0]
+            model = GistModel(ctx, "sage", widths, m, th, adam=policy)
+            runner = SubGCN(ctx, "sage", model.slice_widths, cap_n)
+            losses = torch.empty(rounds, m, zeta, device="cuda")
+            ev = [evaluate(model)]
+            train = []
+            for t in range(rounds):
+                model.set_partitions({l: 100 + 10 * t + l for l in (1, 2)})
+                model.begin_round()
+                for i in range(m):
+                    for z in range(zeta):
+                        b = batch(t, i, z)
+                        k, fresh = (t * zeta + z + 1, False) if policy == "carry" else (z + 1, z == 0)
+                        runner.step(b, model.params[i], lr, adam=(model.M[i], model.V[i], k, fresh),
+                                    loss_out=losses[t, i, z:z + 1])
+                model.end_round()
+                ev.append(evaluate(model))
+                train.append(float(losses[t].mean().cpu()))
+            curves[f"m{m}_{policy}"] = {"eval_loss_after_round": [round(v[0], 4) for v in ev],
+                                        "eval_accuracy_after_round": [round(v[1], 4) for v in ev],
+                                        "mean_local_step_loss": [round(v, 4) for v in train]}
+            log(f"[curves] m={m} {policy}: eval loss {ev[0][0]:.3f} -> {ev[-1][0]:.3f}, "
+                f"accuracy {ev[0][1]:.3f} -> {ev[-1][1]:.3f} ({time.time() - t0:.1f}s)")
+    print(json.dumps({"loss_curves": curves, "setup": {
+        "graph": "c3 SBM, 232,965 nodes, 1,500 clusters, mini-batch 20 clusters",
+        "model": "3-layer GraphSAGE-mean " + "-".join(map(str, widths)),
+        "labels": "planted: argmax([X | mean_nbr X] T), T ~ N(0,1) 1204 x 41, seed 7",
+        "optimizer": f"Adam lr {lr}, betas (0.9, 0.999), eps 1e-8, no weight decay",
+        "rounds": rounds, "zeta": zeta,
+        "eval": f"global model after each round's subAgg, {eval_clusters} fixed clusters"}}),
+        flush=True)
+
+
 # ---------------------------------------------------------------------------
 def main():
     args = parse()
@@ -492,59 +776,55 @@ def main():
     if args.copy_calib:
         copy_calibration(G, ctx)
         return
+    if args.loss_curves:
+        loss_curves(G, ctx, args.curve_rounds, args.curve_zeta, lr=args.curve_lr,
+                    hidden=args.curve_hidden)
+        return
     cfg = get_config(args.config)
+    tiles = args.aggregation == "tile"
     if args.config == "c5":
-        wl = LayerWorkload(cfg, ctx, args.dtype, args.d_in)
+        wl = LayerWorkload(cfg, ctx, args.dtype, args.d_in, clustered=tiles)
     else:
+        # the SBM workloads' mini-batches are unions of clusters over block-contiguous ids
         wl = RoundWorkload(cfg, ctx, args.dtype, args.optimizer, args.adam_policy, args.zeta,
-                           args.shared_batch, args.streams, args.graphs, args.lr)
+                           args.shared_batch, args.streams, args.graphs, args.lr,
+                           clustered=tiles and cfg.batch_clusters is not None)
     ctxs = getattr(wl, "ctxs", [ctx])
     for w in range(args.warmup):
         wl.step()
         torch.cuda.synchronize()
         log(f"[bench] warmup {w + 1}/{args.warmup} done")
-    # graph replays carry no per-kernel events: their kernels are profiled in
-    # an eager pass of the same steps after the timed region
-    profile_timed = not args.no_profile and not args.graphs
-    if profile_timed:
-        for c in ctxs:
-            G.gist_profile_begin(c, 1 << 16)
-    torch.cuda.synchronize()
     pipes = getattr(wl, "pipes", [])
     for p in pipes:
         p.wait_s = 0.0
-    t0 = time.perf_counter()
-    for s in range(args.steps):
-        wl.step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
+    # the timed region: no per-kernel instrumentation
+    ms_step, per_step = timed_pass(wl, args.steps)
     host_wait_ms = sum(p.wait_s for p in pipes) * 1e3 / args.steps
     log(f"[bench] timed {args.steps} steps")
-    ms_step = (t1 - t0) * 1e3 / args.steps
+    # per-kernel figures from a separate pass of the same steps (eager when
+    # the timed pass replayed graphs: replays carry no per-kernel events)
     prof, dropped = ({}, 0)
-    if args.graphs and not args.no_profile:
+    psteps = args.profile_steps or args.steps
+    if not args.no_profile:
         wl.use_graphs = False
         for c in ctxs:
             G.gist_profile_begin(c, 1 << 16)
-        for s in range(args.steps):
+        for s in range(psteps):
             wl.step()
         torch.cuda.synchronize()
-        log(f"[bench] profiled {args.steps} eager steps")
-    if not args.no_profile:
-        for c in ctxs:   # every stream's launches (their event times may overlap)
-            p, d = G.gist_profile_read(c)
-            G.gist_profile_end(c)
-            dropped += d
-            for k, v in p.items():
-                acc = prof.setdefault(k, dict(launches=0, ms=0.0, flops=0.0, bytes=0.0))
-                for f in acc:
-                    acc[f] += v[f]
+        prof, dropped = merged_profile(G, ctxs)
+        wl.use_graphs = args.graphs
+        log(f"[bench] profiled {psteps} steps")
+    extras = None
+    if args.config == "c4" and not args.no_extras and not args.shared_batch:
+        extras = north_star_figures(wl, ctx, 8, args.aggregation == "tile")
+        log("[bench] north-star figures measured")
     wl.finish()   # a deferred subAgg (after the timed region and the profile)
     kernels = {}
     for k, v in sorted(prof.items(), key=lambda kv: -kv[1]["ms"]):
-        e = dict(launches=v["launches"], ms_per_step=round(v["ms"] / args.steps, 4),
+        e = dict(launches=v["launches"], ms_per_step=round(v["ms"] / psteps, 4),
                  avg_us=round(1e3 * v["ms"] / v["launches"], 2))
-        if v["flops"] and k.startswith("gemm_") and "reduce" not in k and "fixup" not in k:
+        if v["flops"] and is_gemm(k):
             e["tflops"] = round(v["flops"] / (v["ms"] * 1e-3) / 1e12, 2)
         if v["bytes"]:
             e["gbs"] = round(v["bytes"] / (v["ms"] * 1e-3) / 1e9, 1)
@@ -553,7 +833,7 @@ def main():
     if prof:
         dom, v = max(prof.items(), key=lambda kv: kv[1]["ms"])
         avg_s = v["ms"] * 1e-3 / v["launches"]
-        if dom.startswith("gemm_") and "reduce" not in dom and "fixup" not in dom:
+        if is_gemm(dom):
             peak = PEAK["bf16" if "bf16" in dom else "f32"]
             ach = v["flops"] / v["launches"] / avg_s / 1e12
             roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 2),
@@ -578,18 +858,20 @@ def main():
     value = ms_step / per_unit
     cpu = None
     if not args.no_cpu_baseline:
-        try:
-            from threadpoolctl import threadpool_info
-            threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-        except Exception:
-            threads = os.cpu_count() or 1
         ms, what = wl.cpu_baseline()
-        cpu = {"value": round(ms, 2), "unit": "ms", "cores": int(threads), "kind": "oracle",
-               "sample": what}
+        cpu = dict({"value": round(ms, 2), "unit": "ms", "kind": "oracle", "sample": what},
+                   **cpu_info())
+        if extras is not None:
+            cpu["spmm_c5_ms"] = round(c5_oracle_spmm_ms(wl.graph), 1)
+            cpu["spmm_c5_sample"] = ("fp64 Abar H over all 2,449,029 rows of the c5 matrix at "
+                                     "width 256, SciPy CSR product on one thread, timed in full")
+            log("[bench] oracle c5 aggregation timed")
     out = {
         "metric": METRIC, "value": round(value, 4), "unit": "ms",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 3), "higher_is_better": False, "scaling": "weak",
+        "ms_per_step": round(ms_step, 3),
+        "step_ms_p10_p50_p90": [round(float(x), 3) for x in np.percentile(per_step, [10, 50, 90])],
+        "higher_is_better": False, "scaling": "weak",
         "vs_baseline": None, "dtype": dtype_name,
         "data": "synthetic (seeded SBM / Chung-Lu / ER graphs, N(0,1) features, Glorot weights)",
         "config": dict(wl.describe(), parallelism="single GPU, m sub-GCNs back to back",
@@ -598,8 +880,10 @@ def main():
                        else "ms per layer fwd+bwd"),
         "roofline": roofline, "cpu_baseline": cpu, "kernels": kernels,
         "host_batch_wait_ms_per_step": round(host_wait_ms, 3),
-        "kernels_from": ("an eager pass of the same number of steps after the timed graph "
-                         "replays" if args.graphs else "the timed steps"),
+        "north_star": extras,
+        "kernels_from": (f"a separate profiled pass of {psteps} steps after the timed region "
+                         "(library HIP event pairs around every launch, on its launch stream)" +
+                         (", launched eagerly" if args.graphs else "")),
         "profile_dropped": dropped, "kernel_src_sha256": kernel_source_hash(),
     }
     print(json.dumps(out), flush=True)

@@ -56,6 +56,7 @@ def variant_symbol(variant):
         "gemm_bf16_packed": r"gemm_bf16_kernel<", "gemm_bf16_fixup": r"fixup_bf16_kernel",
         "cvt_bf16_K": r"cvt_bf16_kernel<true,", "cvt_bf16_R": r"cvt_bf16_kernel<false,",
         "gemm_streamk_fixup": r"streamk_fixup", "subagg_gather_rows": r"subagg_gather_rows_kernel<",
+        "spmm_tile": r"spmm_tile_kernel",
         "subagg_gather": r"subagg_gather_kernel<", "gather_slice": r"gather_kernel",
         "subagg_scatter": r"scatter_kernel", "sgd_update": r"sgd_kernel",
         "relu_mask": r"relu_mask_kernel", "subagg_mean": r"subagg_mean_kernel",

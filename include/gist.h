@@ -266,7 +266,24 @@ typedef struct gist_layer_desc {
  *   H_out, dH_out     n x (G s_out), sub-GCN g in columns [g s_out, ...);
  *                     with GIST_LAYER_GROUP_MAJOR_OUT G consecutive
  *                     n x s_out blocks (each sub-GCN's logits contiguous). */
-enum { GIST_LAYER_SHARED_INPUT = 1, GIST_LAYER_GROUP_MAJOR_OUT = 2 };
+enum { GIST_LAYER_SHARED_INPUT = 1, GIST_LAYER_GROUP_MAJOR_OUT = 2, GIST_LAYER_CLUSTERED = 4 };
+
+/* GIST_LAYER_CLUSTERED: a hint that Abar (and A_T) is the matrix of a
+ * cluster mini-batch over block-contiguous node ids (Section 2.2: a union of
+ * clusters), so almost every entry sits within a few hundred columns of its
+ * row's diagonal.  The aggregation then runs on the matrix cores: for every
+ * 32 rows, the entries within 192 of their row's diagonal (a window of at
+ * most 384 columns) form a dense tile whose values and the matching X rows
+ * are each split into two bf16 halves (hi = bf16(v), lo = bf16(v - hi));
+ * the products hi*hi + hi*lo + lo*hi are accumulated in fp32, so every
+ * term carries a relative error below 2^-15; the remaining entries are
+ * gathered and added in storage order.  Results are deterministic and
+ * agree with the plain fp32 aggregation within that bound for any matrix
+ * (only the speed depends on the structure).  The matrix must not repeat
+ * a (row, column) entry (gist_build_minibatch_csr never does).  Off by
+ * default: on batches of 163-node clusters the gather kernel is faster,
+ * because each 32-row tile is a serial chain of memory round trips (entries,
+ * window, X rows) that three resident tiles per CU do not hide. */
 
 /* Workspace (device bytes) that fwd and bwd need for this descriptor. */
 gist_status gist_layer_workspace_size(const gist_layer_desc* L, size_t* fwd_bytes,

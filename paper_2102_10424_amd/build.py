@@ -14,7 +14,8 @@ CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libgist.so")
 BUILD = os.path.join(PKG, "_build")
 
-HIP_SOURCES = ["api.hip", "spmm.hip", "gemm.hip", "gemm_bf16.hip", "elementwise.hip", "gat.hip"]
+HIP_SOURCES = ["api.hip", "spmm.hip", "spmm_tile.hip", "gemm.hip", "gemm_bf16.hip",
+               "elementwise.hip", "gat.hip"]
 HOST_SOURCES = ["host_partition.cpp", "host_minibatch.cpp", "host_ladies.cpp"]
 
 ARCH = "gfx950"

@@ -211,7 +211,8 @@ gist_status check_desc(const gist_layer_desc* L) {
     return set_error(GIST_E_INVAL, "layer: SAGE-mean aggregates first");
   if (L->n < 0 || L->s_in < 1 || L->s_out < 1 || L->groups < 0)
     return set_error(GIST_E_INVAL, "layer: bad sizes");
-  if (L->flags & ~static_cast<uint32_t>(GIST_LAYER_SHARED_INPUT | GIST_LAYER_GROUP_MAJOR_OUT))
+  if (L->flags & ~static_cast<uint32_t>(GIST_LAYER_SHARED_INPUT | GIST_LAYER_GROUP_MAJOR_OUT |
+                                         GIST_LAYER_CLUSTERED))
     return set_error(GIST_E_INVAL, "layer: unknown flags");
   if (L->n > INT32_MAX) return set_error(GIST_E_UNSUPPORTED, "layer: n exceeds int32 rows");
   if (L->n_in < 0) return set_error(GIST_E_INVAL, "layer: bad n_in");
@@ -230,7 +231,7 @@ gist_status check_desc(const gist_layer_desc* L) {
 // dH_out, dZ) tensors and of the weight slices.
 struct Lay {
   int64_t G, n, n_in, si, so, wrows;
-  bool shared, gmajor;
+  bool shared, gmajor, clustered;
   int64_t ld_in, gs_in, ld_out, gs_out, gs_w;
   int64_t gs_out_in;   // group stride of an output-width tensor with n_in rows
   int64_t w_in() const { return shared ? si : G * si; }   // aggregation width on the input side
@@ -243,6 +244,7 @@ Lay layout(const gist_layer_desc* L) {
   y.wrows = (L->kind == GIST_LAYER_SAGE_MEAN ? 2 : 1) * y.si;
   y.shared = (L->flags & GIST_LAYER_SHARED_INPUT) != 0;
   y.gmajor = (L->flags & GIST_LAYER_GROUP_MAJOR_OUT) != 0;
+  y.clustered = (L->flags & GIST_LAYER_CLUSTERED) != 0;
   y.ld_in = y.shared ? y.si : y.G * y.si;
   y.gs_in = y.shared ? 0 : y.si;
   y.ld_out = y.gmajor ? y.so : y.G * y.so;
@@ -252,17 +254,30 @@ Lay layout(const gist_layer_desc* L) {
   return y;
 }
 
+// Abar X (+ Add) (ReLU) for a layer's matrix A (rows x cols): the matrix-core
+// tile kernel for a cluster mini-batch (GIST_LAYER_CLUSTERED), else the
+// gather kernel.
+gist_status aggregate(hipStream_t st, const Lay& y, const gist_csr_dev* A, int64_t rows,
+                      int64_t cols, const float* X, int64_t ldx, int width, float* Y,
+                      int64_t ldy, const float* add, int64_t ld_add, bool relu) {
+  if (y.clustered)
+    return gist::spmm_clustered(st, rows, cols, A->nnz, A->rowptr, A->col, A->val, X, ldx, width,
+                                Y, ldy, add, ld_add, relu);
+  return gist::spmm(st, rows, A->nnz, A->rowptr, A->col, A->val, X, ldx, width, Y, ldy, add,
+                    ld_add, relu);
+}
+
 // A X over output-width tensors (dZ-like layout), A with `rows` rows: one
 // full-width call, or one per group when the groups are stored one after
 // another (group strides gx of X and gy of Y).
 gist_status spmm_out(hipStream_t st, const Lay& y, const gist_csr_dev* A, int64_t rows,
-                     const float* X, int64_t gx, float* Y, int64_t gy, bool relu) {
+                     int64_t cols, const float* X, int64_t gx, float* Y, int64_t gy, bool relu) {
   if (!y.gmajor)
-    return gist::spmm(st, rows, A->nnz, A->rowptr, A->col, A->val, X, y.ld_out, int(y.G * y.so),
-                      Y, y.ld_out, nullptr, 0, relu);
+    return aggregate(st, y, A, rows, cols, X, y.ld_out, int(y.G * y.so), Y, y.ld_out, nullptr, 0,
+                     relu);
   for (int64_t g = 0; g < y.G; ++g)
-    GIST_TRY(gist::spmm(st, rows, A->nnz, A->rowptr, A->col, A->val, X + g * gx, y.so,
-                        int(y.so), Y + g * gy, y.so, nullptr, 0, relu));
+    GIST_TRY(aggregate(st, y, A, rows, cols, X + g * gx, y.so, int(y.so), Y + g * gy, y.so,
+                       nullptr, 0, relu));
   return GIST_OK;
 }
 
@@ -374,8 +389,8 @@ extern "C" gist_status gist_gcn_layer_fwd(gist_ctx* ctx, const gist_layer_desc* 
   b.p0 = W; b.ld0 = so; b.k_major = false; b.gs0 = y.gs_w;
   if (sage || order == GIST_ORDER_AGG_FIRST) {
     // one aggregation over every group's columns (or the shared input once)
-    GIST_TRY(gist::spmm(st, n, A->nnz, A->rowptr, A->col, A->val, H, y.ld_in, int(y.w_in()),
-                        agg_save, y.ld_in, nullptr, 0, false));
+    GIST_TRY(aggregate(st, y, A, n, n_in, H, y.ld_in, int(y.w_in()), agg_save, y.ld_in, nullptr,
+                       0, false));
     gist::Operand a;
     a.k_major = true;
     if (sage) {  // [H_g | Abar H_g], concatenated along K
@@ -398,7 +413,7 @@ extern "C" gist_status gist_gcn_layer_fwd(gist_ctx* ctx, const gist_layer_desc* 
   gist::GemmOut t;
   t.c0 = T; t.ldc0 = y.ld_out; t.gs0 = y.gs_out_in;
   GIST_TRY(gist::gemm(st, n_in, so, si, a, b, t, L->dtype, gws, ws_bytes - tb, G));
-  return spmm_out(st, y, A, n, T, y.gs_out_in, H_out, y.gs_out, relu);
+  return spmm_out(st, y, A, n, n_in, T, y.gs_out_in, H_out, y.gs_out, relu);
 }
 
 namespace {
@@ -508,8 +523,8 @@ gist_status layer_bwd(gist_ctx* ctx, const gist_layer_desc* L, const gist_csr_de
       }
       GIST_TRY(gist::gemm(st, n, y.wrows, so, a2, w_as_b, o2, L->dtype, gws, gbytes, G));
       // dH (+)= Abar^T dP, every group at once
-      return gist::spmm(st, n_in, AT->nnz, AT->rowptr, AT->col, AT->val, tmp, ld_p, int(ld_p),
-                        dH, ld_p, sage ? dH : nullptr, ld_p, false);
+      return aggregate(st, y, AT, n_in, n, tmp, ld_p, int(ld_p), dH, ld_p, sage ? dH : nullptr,
+                       ld_p, false);
     };
     if (fused) {
       GIST_TRY(input_grad());
@@ -520,7 +535,7 @@ gist_status layer_bwd(gist_ctx* ctx, const gist_layer_desc* L, const gist_csr_de
   }
   // GCN transform-first: T = Abar^T dZ (n_in rows, laid out like dZ); dW_g = H_g^T T_g;
   // dH_g = T_g W_g^T
-  GIST_TRY(spmm_out(st, y, AT, n_in, dZ, y.gs_out, tmp, y.gs_out_in, false));
+  GIST_TRY(spmm_out(st, y, AT, n_in, n, dZ, y.gs_out, tmp, y.gs_out_in, false));
   auto weight_grad = [&]() -> gist_status {
     if (p.tdw) {   // node-contiguous copies H^T (si x n_in) and T^T (so x n_in)
       const int64_t n4 = round4(n_in);

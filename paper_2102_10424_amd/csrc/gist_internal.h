@@ -98,6 +98,15 @@ gist_status spmm(hipStream_t st, int64_t n, int64_t nnz, const int32_t* rowptr,
                  int64_t ldx, int width, float* Y, int64_t ldy,
                  const float* add, int64_t ld_add, bool relu);
 
+// The same on the matrix cores for a matrix (n x n_in) whose entries sit
+// mostly near the diagonal (a cluster mini-batch): dense bf16-split tiles
+// for the entries near the diagonal, a gather for the rest (spmm_tile.hip).
+// Requires no repeated (row, column) entry.  `add` may alias Y.
+gist_status spmm_clustered(hipStream_t st, int64_t n, int64_t n_in, int64_t nnz,
+                           const int32_t* rowptr, const int32_t* col, const float* val,
+                           const float* X, int64_t ldx, int width, float* Y, int64_t ldy,
+                           const float* add, int64_t ld_add, bool relu);
+
 // Operand of a GEMM: logical R x K matrix (R = M for A, N for B).
 //   k_major == true : element (r, k) at p[r * ld + k]   (K contiguous)
 //   k_major == false: element (r, k) at p[k * ld + r]   (R contiguous)

@@ -1,0 +1,366 @@
+// Aggregation Y = Abar X (+ Add) (ReLU) for a cluster mini-batch, on the
+// matrix cores -- the sparse half of eq. (2) when Abar is nearly block
+// diagonal.
+//
+// A cluster mini-batch over block-contiguous node ids (Section 2.2: a batch
+// is a union of clusters) has almost every entry of row r inside its own
+// cluster's block around the diagonal.  The gather kernel (spmm.hip) moves
+// one X row from cache to the CUs per entry -- nnz * width * 4 bytes, twenty
+// times the algorithmic bytes at the c5 shape -- so it is bound by cache
+// bandwidth, not HBM.  Here a workgroup takes 32 rows and one 256-column
+// slab of X:
+//
+//   1. window: [clo, clo + K) spans the columns of the tile's entries that
+//      lie within kNear of their row's diagonal, K <= kMaxK, rounded up to
+//      the MFMA depth;
+//   2. the entries inside the window are expanded into a dense 32 x K tile
+//      in LDS, each value split into two bf16 halves, hi = bf16(v) and
+//      lo = bf16(v - hi) (both rounded to nearest even);
+//   3. each wave streams its 64 columns of X rows clo .. clo + K - 1 from
+//      memory straight into MFMA operand registers (a lane holds 8
+//      consecutive rows of one column), three 16-row steps ahead, splits them
+//      the same way and multiplies on v_mfma_f32_32x32x16_bf16 with fp32
+//      accumulation: hi*hi + hi*lo + lo*hi.  The dense tile is the only LDS
+//      operand and read-only here, so the loop has no barrier and the waves
+//      run independently.  Each X row of the window is read once per 32
+//      output rows instead of once per entry;
+//   4. the entries outside the window (edges between clusters) are gathered
+//      one X row each, as the gather kernel does, and added in storage
+//      order; then Add, ReLU and the store.
+//
+// Accuracy: a value's hi + lo carries 16 significant bits, so each split
+// operand is within 2^-17 of its value, and the dropped lo*lo term is below
+// 2^-16 of the product: every product enters the fp32 sum with a relative
+// error below 2^-15 (3.1e-5).  The sum order is fixed (the MFMA k order,
+// then the window's remainder in storage order): results are deterministic.
+// Correct for any matrix; fast when most entries sit near the diagonal.
+
+#include <climits>
+#include <cstdio>
+
+#include "common.cuh"
+#include "gist_internal.h"
+
+namespace gist {
+
+namespace {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float float2v __attribute__((ext_vector_type(2)));
+typedef unsigned uint4v __attribute__((ext_vector_type(4)));
+typedef unsigned short ushort8 __attribute__((ext_vector_type(8)));
+
+constexpr int kRows = 32;          // output rows per workgroup (the MFMA's M)
+constexpr int kCols = 256;         // output columns per workgroup: 4 waves x 64
+constexpr int kMaxK = 320;         // widest dense window (a multiple of kKs)
+constexpr int kNear = 192;         // an entry within this of its row's diagonal sets the window
+constexpr int kKs = 16;            // window rows per step (the MFMA's K)
+constexpr int kDepth = 3;          // X steps in flight ahead of the one multiplied
+// steps are taken kDepth at a time; the tile's zero columns cover the padding
+constexpr int kPadK = (kMaxK / kKs + kDepth - 1) / kDepth * kDepth * kKs;
+constexpr int kALd = kPadK + 8;    // bf16 per row of the dense tile (16 B pad)
+constexpr int kYLd = kCols + 4;    // floats per row of the result tile
+constexpr int kChunk = 8;          // 64-entry chunks a wave loads at once
+constexpr int kBatch = 16;         // outside-window entries gathered at once
+
+// Sixteen zeros in device memory (zero-initialised, never written): a
+// pipelined load that falls outside the window or the matrix reads here, so
+// no load depends on a branch.  Not const, so that the compiler cannot fold
+// such a load away and put the real one behind a branch again.
+__device__ float kZeroRow[16];
+
+typedef __attribute__((address_space(1))) const float gfloat;   // global memory
+
+__device__ __forceinline__ unsigned short bf16_bits(float f) {
+  return __builtin_bit_cast(unsigned short, static_cast<__bf16>(f));
+}
+__device__ __forceinline__ float bf16_value(unsigned short h) {
+  return __uint_as_float(static_cast<unsigned>(h) << 16);
+}
+// Two values to packed bf16 (a in the low half), rounded to nearest even.
+__device__ __forceinline__ unsigned bf16_pair(float a, float b) {
+  return __builtin_bit_cast(unsigned, __builtin_convertvector((float2v){a, b}, bf16x2));
+}
+// Split 8 values into bf16 halves hi = bf16(v), lo = bf16(v - hi), packed as
+// MFMA operands (element i in half i of the fragment).
+__device__ __forceinline__ void split8(const float (&v)[8], bf16x8& hi, bf16x8& lo) {
+  uint4v h, l;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const unsigned hp = bf16_pair(v[2 * i], v[2 * i + 1]);
+    h[i] = hp;
+    l[i] = bf16_pair(v[2 * i] - __uint_as_float(hp << 16),
+                     v[2 * i + 1] - __uint_as_float(hp & 0xffff0000u));
+  }
+  hi = __builtin_bit_cast(bf16x8, h);
+  lo = __builtin_bit_cast(bf16x8, l);
+}
+
+// Wave-uniform row (relative to the wave's first row) of entry e, given the
+// wave's row pointers rp[0..8].
+__device__ __forceinline__ int row_of(int e, const int (&rp)[9]) {
+  int rl = 0;
+#pragma unroll
+  for (int i = 1; i < 8; ++i) rl += e >= rp[i] ? 1 : 0;
+  return rl;
+}
+
+__global__ __launch_bounds__(256) void spmm_tile_kernel(
+    int n, int n_in, const int* __restrict__ rowptr, const int* __restrict__ col,
+    const float* __restrict__ val, const float* __restrict__ X, int64_t ldx, int width,
+    float* Y, int64_t ldy, const float* add, int64_t ld_add, int relu, int tiles,
+    int64_t nblocks) {
+  // dense tile (hi, lo), later the fp32 result tile
+  __shared__ __attribute__((aligned(16))) unsigned short Atile[2 * kRows * kALd];
+  __shared__ int red[8];
+  static_assert(sizeof(float) * kRows * kYLd <= sizeof(unsigned short) * 2 * kRows * kALd,
+                "result tile must fit in the dense tile's space");
+  static_assert(kMaxK % kKs == 0 && kPadK >= kMaxK && kALd % 8 == 0, "tile layout");
+
+  const int t = threadIdx.x;
+  const int lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int li = lane & 31, lh = lane >> 5;
+  const int64_t logical = xcd_remap(blockIdx.x, nblocks);
+  const int slab = static_cast<int>(logical / tiles);
+  const int tile = static_cast<int>(logical - static_cast<int64_t>(slab) * tiles);
+  const int r0 = tile * kRows;
+  const int cs = slab * kCols;
+  const int rw = r0 + 8 * wave;   // this wave's first row
+
+  // this wave's rows rw .. rw + 7 and their entries [rp[0], rp[8])
+  int rp[9];
+#pragma unroll
+  for (int i = 0; i <= 8; ++i) rp[i] = rowptr[min(rw + i, n)];
+  // When the wave's entries fit in kChunk chunks of 64 they stay in
+  // registers for all three passes; longer rows (hubs) are re-read per pass.
+  const bool fit = rp[8] - rp[0] <= 64 * kChunk;
+  int cc[kChunk];
+  float vv[kChunk];
+  auto load_chunks = [&](int base) {
+#pragma unroll
+    for (int u = 0; u < kChunk; ++u) {
+      const int e = base + 64 * u + lane;
+      cc[u] = e < rp[8] ? col[e] : INT_MIN / 2;
+      vv[u] = e < rp[8] ? val[e] : 0.f;
+    }
+  };
+  if (fit) load_chunks(rp[0]);
+
+  // zero the dense tile while the entries arrive
+  {
+    uint4v* z = reinterpret_cast<uint4v*>(Atile);
+    constexpr int units = 2 * kRows * kALd / 8;
+    for (int u = t; u < units; u += 256) z[u] = uint4v{0u, 0u, 0u, 0u};
+  }
+
+  // ---- 1. window: columns of the entries near their row's diagonal
+  int cmin = INT_MAX, cmax = -1;
+  for (int base = rp[0]; base < rp[8]; base += 64 * kChunk) {
+    if (!fit) load_chunks(base);
+#pragma unroll
+    for (int u = 0; u < kChunk; ++u) {
+      const int e = base + 64 * u + lane;
+      if (e < rp[8]) {
+        const int r = rw + row_of(e, rp);
+        if (cc[u] >= r - kNear && cc[u] <= r + kNear) {
+          cmin = min(cmin, cc[u]);
+          cmax = max(cmax, cc[u]);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    cmin = min(cmin, __shfl_xor(cmin, o, 64));
+    cmax = max(cmax, __shfl_xor(cmax, o, 64));
+  }
+  if (lane == 0) {
+    red[wave] = cmin;
+    red[4 + wave] = cmax;
+  }
+  __syncthreads();
+  cmin = min(min(red[0], red[1]), min(red[2], red[3]));
+  cmax = max(max(red[4], red[5]), max(red[6], red[7]));
+  int clo = 0, K = 0;
+  if (cmax >= cmin) {
+    clo = cmin;
+    K = min(kMaxK, (cmax - cmin + kKs) / kKs * kKs);
+  }
+  const int nk = K / kKs;
+
+  // X operand: lane (li, lh) of this wave holds window rows 16 j + 8 lh .. + 7
+  // of columns c0 + li and c0 + 32 + li
+  const int c0 = cs + wave * 64 + li;
+  const bool ok0 = c0 < width, ok1 = c0 + 32 < width;
+  const int rows_left = n_in - clo - 8 * lh;   // window rows this lane may read
+  const float* xp = X + static_cast<int64_t>(clo + 8 * lh) * ldx + c0;
+  float xr[kDepth][2][8];
+  // Every load is issued unconditionally (a row outside the window or the
+  // matrix reads a zero from kZeroRow instead): loads behind branches would
+  // make the compiler drain all of them before each step.
+  auto gload = [&](float (&dst)[2][8], int j) {
+    const float* p = xp + static_cast<int64_t>(j * kKs) * ldx;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const bool in = j < nk && j * kKs + i < rows_left;
+      dst[0][i] = *(gfloat*)((in && ok0) ? p + i * ldx : kZeroRow + i);
+      dst[1][i] = *(gfloat*)((in && ok1) ? p + i * ldx + 32 : kZeroRow + 8 + i);
+    }
+  };
+  // the first steps load while the dense tile is built
+  if (nk > 0) {
+#pragma unroll
+    for (int p = 0; p < kDepth; ++p) gload(xr[p], p);
+  }
+
+  // ---- 2. the window's entries as a dense 32 x K tile (bf16 hi, lo)
+  if (nk > 0) {
+    for (int base = rp[0]; base < rp[8]; base += 64 * kChunk) {
+      if (!fit) load_chunks(base);
+#pragma unroll
+      for (int u = 0; u < kChunk; ++u) {
+        const int e = base + 64 * u + lane;
+        const unsigned k = static_cast<unsigned>(cc[u] - clo);
+        if (e < rp[8] && k < static_cast<unsigned>(K)) {
+          const int rl = 8 * wave + row_of(e, rp);
+          const unsigned short hi = bf16_bits(vv[u]);
+          Atile[rl * kALd + k] = hi;
+          Atile[(kRows + rl) * kALd + k] = bf16_bits(vv[u] - bf16_value(hi));
+        }
+      }
+    }
+  }
+  __syncthreads();
+
+  // ---- 3. Y_tile = A_tile X[clo .. clo + K) on the matrix cores, no barriers
+  floatx16 acc[2];
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[b][r] = 0.f;
+  auto mfma = [&](const float (&src)[2][8], int j) {
+    // A fragment: tile row li, window columns 16 j + 8 lh .. + 7
+    const bf16x8 ah = *reinterpret_cast<const bf16x8*>(Atile + li * kALd + j * kKs + 8 * lh);
+    const bf16x8 al =
+        *reinterpret_cast<const bf16x8*>(Atile + (kRows + li) * kALd + j * kKs + 8 * lh);
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      bf16x8 bh, bl;
+      split8(src[b], bh, bl);
+      acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh, acc[b], 0, 0, 0);
+      acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl, acc[b], 0, 0, 0);
+      acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh, acc[b], 0, 0, 0);
+    }
+  };
+  // steps nk .. (padded to a multiple of kDepth) multiply the tile's zero
+  // columns with zeroed X values
+  for (int j0 = 0; j0 < nk; j0 += kDepth) {
+#pragma unroll
+    for (int p = 0; p < kDepth; ++p) {
+      mfma(xr[p], j0 + p);
+      gload(xr[p], j0 + p + kDepth);
+    }
+  }
+  __syncthreads();   // every wave is past its last read of the dense tile
+
+  // the result tile takes the dense tile's space
+  float* Ys = reinterpret_cast<float*>(Atile);
+  // acc[b] register r of lane l: tile row 8 (r / 4) + 4 (l / 32) + r % 4,
+  // column wave 64 + 32 b + l % 32
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      Ys[(8 * (r / 4) + 4 * lh + (r % 4)) * kYLd + wave * 64 + 32 * b + li] = acc[b][r];
+  __syncthreads();
+
+  // ---- 4. entries outside the window, in storage order, then the store.
+  // This wave owns tile rows 8 wave .. + 7; lane owns columns cs + lane + 64 q.
+  for (int base = rp[0]; base < rp[8]; base += 64 * kChunk) {
+    if (!fit) load_chunks(base);
+#pragma unroll
+    for (int u = 0; u < kChunk; ++u) {
+      const int e = base + 64 * u + lane;
+      const bool out = e < rp[8] && static_cast<unsigned>(cc[u] - clo) >= static_cast<unsigned>(K);
+      uint64_t m = __ballot(out);
+      while (m) {
+        // up to kBatch of this chunk's outside entries at a time, loads first
+        int ec[kBatch], er[kBatch];
+        float ev[kBatch];
+        int cnt = 0;
+#pragma unroll
+        for (int q = 0; q < kBatch; ++q) {
+          if (m) {
+            const int b = __builtin_ctzll(m);
+            m &= m - 1;
+            ec[q] = __builtin_amdgcn_readlane(cc[u], b);
+            ev[q] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(vv[u]), b));
+            er[q] = row_of(base + 64 * u + b, rp);
+            cnt = q + 1;
+          } else {
+            ec[q] = 0;
+            ev[q] = 0.f;
+            er[q] = 0;
+          }
+        }
+        float xv[kBatch][4];
+#pragma unroll
+        for (int q = 0; q < kBatch; ++q)
+#pragma unroll
+          for (int p = 0; p < 4; ++p) {
+            const int c = cs + lane + 64 * p;
+            xv[q][p] = (q < cnt && c < width) ? X[static_cast<int64_t>(ec[q]) * ldx + c] : 0.f;
+          }
+#pragma unroll
+        for (int q = 0; q < kBatch; ++q) {
+          if (q < cnt) {
+            float* yrow = Ys + (8 * wave + er[q]) * kYLd + lane;
+#pragma unroll
+            for (int p = 0; p < 4; ++p) yrow[64 * p] = fmaf(ev[q], xv[q][p], yrow[64 * p]);
+          }
+        }
+      }
+    }
+  }
+  // store this wave's rows (Add, ReLU)
+  for (int i = 0; i < 8; ++i) {
+    const int64_t r = rw + i;
+    if (r >= n) break;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int c = cs + lane + 64 * p;
+      if (c < width) {
+        float y = Ys[(8 * wave + i) * kYLd + lane + 64 * p];
+        if (add) y += add[r * ld_add + c];
+        if (relu) y = fmaxf(y, 0.f);
+        Y[r * ldy + c] = y;
+      }
+    }
+  }
+}
+
+}  // namespace
+
+gist_status spmm_clustered(hipStream_t st, int64_t n, int64_t n_in, int64_t nnz,
+                           const int32_t* rowptr, const int32_t* col, const float* val,
+                           const float* X, int64_t ldx, int width, float* Y, int64_t ldy,
+                           const float* add, int64_t ld_add, bool relu) {
+  if (n <= 0 || width <= 0) return GIST_OK;
+  const int64_t tiles = (n + kRows - 1) / kRows;
+  const int64_t slabs = (width + kCols - 1) / kCols;
+  const int64_t nblocks = tiles * slabs;
+  if (nblocks > INT32_MAX || tiles > INT32_MAX)
+    return set_error(GIST_E_UNSUPPORTED, "spmm_clustered: grid too large");
+  const double bytes = 4.0 * (n + 1) + 8.0 * static_cast<double>(nnz) +
+                       4.0 * static_cast<double>(n) * width * (add ? 3.0 : 2.0);
+  ProfScope ps(st, "spmm_tile", 2.0 * static_cast<double>(nnz) * width, bytes);
+  hipLaunchKernelGGL(spmm_tile_kernel, dim3(static_cast<unsigned>(nblocks)), dim3(256), 0, st,
+                     static_cast<int>(n), static_cast<int>(n_in), rowptr, col, val, X, ldx, width,
+                     Y, ldy, add, ld_add, relu ? 1 : 0, static_cast<int>(tiles), nblocks);
+  return check_launch("spmm_clustered");
+}
+
+}  // namespace gist

@@ -75,10 +75,11 @@ class BatchSlot:
     the device (``gist_gather_slice`` with the local->global node map).
     """
 
-    def __init__(self, ctx, norm, cap_n, cap_nnz, d_in, device="cuda"):
+    def __init__(self, ctx, norm, cap_n, cap_nnz, d_in, device="cuda", clustered=False):
         self.ctx = ctx
         self.norm = norm
         self.sage = norm == "sage"
+        self.clustered = clustered
         self.cap_n, self.cap_nnz = int(cap_n), int(cap_nnz)
         self.device = device
         pin = dict(pin_memory=True)
@@ -139,7 +140,7 @@ class BatchSlot:
         Xb = self.X[:n]
         G.gist_gather_slice(self.ctx, X_dev, self.d_in, self.d["node_map"], n, None,
                             self.d_in, Xb, self.d_in)
-        return _View(n, nnz, self.d, Xb, self.sage)
+        return _View(n, nnz, self.d, Xb, self.sage, self.clustered)
 
     def load(self, graph_struct, clusters, X_dev, labels_host):
         """Build, upload and gather; returns a batch view with n, nnz, A, A_T, X, labels."""
@@ -162,8 +163,9 @@ class FixedBatchSlot:
 
     _ALIGN = 64
 
-    def __init__(self, ctx, norm, cap_n, cap_nnz, d_in, device="cuda"):
+    def __init__(self, ctx, norm, cap_n, cap_nnz, d_in, device="cuda", clustered=False):
         self.ctx, self.d_in, self.device = ctx, d_in, device
+        self.clustered = clustered
         self.norm, self.sage = norm, norm == "sage"
         self.cap_n, self.cap_nnz = int(cap_n), int(cap_nnz)
         self.layout = self.fixed_layout(self.sage, self.cap_n, self.cap_nnz)
@@ -239,7 +241,7 @@ class FixedBatchSlot:
         if n:
             G.gist_gather_slice(c, X_dev, self.d_in, d[o["node_map"]:], n, None, self.d_in, Xb,
                                 self.d_in)
-        return _View(n, self.nnz, v, Xb, self.sage)
+        return _View(n, self.nnz, v, Xb, self.sage, self.clustered)
 
 
 class BatchPipeline:
@@ -323,8 +325,9 @@ class BatchPipeline:
 
 
 class _View:
-    def __init__(self, n, nnz, d, X, sage):
+    def __init__(self, n, nnz, d, X, sage, clustered=False):
         self.n, self.nnz = n, nnz
+        self.clustered = clustered   # a cluster mini-batch: GIST_LAYER_CLUSTERED applies
         self.A = G.csr_dev(n, nnz, d["rowptr"], d["col"], d["val"])
         self.A_T = G.csr_dev(n, nnz, d["t_rowptr"], d["t_col"], d["t_val"]) if sage else None
         self.X = X
@@ -590,7 +593,7 @@ class ClusterGraphRunner(_Replayer):
     """
 
     def __init__(self, ctx, kind, widths, cap_n, cap_nnz, d_in, X_dev, dtype=G.GIST_DTYPE_F32,
-                 device="cuda"):
+                 device="cuda", clustered=False):
         self._init_replay(ctx)
         self.d_in, self.X_dev = d_in, X_dev
         norm = "sage" if kind == "sage" else "gcn"
@@ -607,7 +610,7 @@ class ClusterGraphRunner(_Replayer):
         self.node_map = d[o["node_map"]:o["node_map"] + cap_n]
         self.coef_dev = d[o["coef"]:o["coef"] + 3].view(f32)
         self.X = torch.empty(cap_n, d_in, device=device)
-        self.view = _View(cap_n, cap_nnz, view, self.X, norm == "sage")
+        self.view = _View(cap_n, cap_nnz, view, self.X, norm == "sage", clustered)
         self.view.n_dev = d[o["n_valid"]:o["n_valid"] + 1]
         self.cap_n = cap_n
         self.run = SubGCN(self.cap_ctx, kind, widths, cap_n, dtype=dtype, device=device)
@@ -768,17 +771,20 @@ class SubGCN:
         self.loss_ws = torch.empty(G.gist_softmax_xent_workspace(n_cap), dtype=torch.uint8,
                                    device=d)
 
-    def desc(self, l, n, nnz=0, n_in=0):
-        """Layer l's descriptor for n output rows (n_in input rows, 0: n)."""
+    def desc(self, l, n, nnz=0, n_in=0, clustered=False):
+        """Layer l's descriptor for n output rows (n_in input rows, 0: n);
+        ``clustered``: the batch is a cluster mini-batch (GIST_LAYER_CLUSTERED)."""
         act = G.GIST_ACT_RELU if l < self.L - 1 else G.GIST_ACT_NONE
         if self.gat:
             return G.gat_desc(n, nnz, self.widths[l], self.widths[l + 1], act, self.dtype,
                               GAT_SLOPE)
         return G.layer_desc(self.lkind, act, n, self.widths[l], self.widths[l + 1],
-                            self.dtype, self.order, n_in=n_in)
+                            self.dtype, self.order, n_in=n_in,
+                            flags=G.GIST_LAYER_CLUSTERED if clustered else 0)
 
     def _ldesc(self, batch, l):
-        return self.desc(l, batch.rows(l + 1), batch.nnz, batch.rows(l))
+        return self.desc(l, batch.rows(l + 1), batch.nnz, batch.rows(l),
+                         getattr(batch, "clustered", False))
 
     def _workspace(self, batch):
         need = 0
@@ -945,6 +951,7 @@ class SubGCNBatch:
         self.lkind = G.GIST_LAYER_SAGE_MEAN if kind == "sage" else G.GIST_LAYER_GCN
         self.parts = 2 if kind == "sage" else 1
         self.n_cap = 0
+        self.clustered = False   # the current batch is a cluster mini-batch
         self.ws = torch.empty(0, dtype=torch.uint8, device=device)
         self._alloc(n_cap)
         w = self.widths
@@ -975,7 +982,8 @@ class SubGCNBatch:
     def desc(self, l, n):
         act = G.GIST_ACT_RELU if l < self.L - 1 else G.GIST_ACT_NONE
         flags = (G.GIST_LAYER_SHARED_INPUT if l == 0 else 0) | \
-                (G.GIST_LAYER_GROUP_MAJOR_OUT if l == self.L - 1 else 0)
+                (G.GIST_LAYER_GROUP_MAJOR_OUT if l == self.L - 1 else 0) | \
+                (G.GIST_LAYER_CLUSTERED if self.clustered else 0)
         return G.layer_desc(self.lkind, act, n, self.widths[l], self.widths[l + 1], self.dtype,
                             G.GIST_ORDER_AUTO, groups=self.m, flags=flags)
 
@@ -996,6 +1004,7 @@ class SubGCNBatch:
         if n > self.n_cap:
             raise ValueError("batch larger than the runner's capacity")
         self.n = n
+        self.clustered = getattr(batch, "clustered", False)
         ws = self._workspace(n)
         H = batch.X
         for l in range(self.L):

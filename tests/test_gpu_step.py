@@ -201,10 +201,11 @@ def test_step_layerwise_gat(G, ctx, dtype):
         assert e_f <= tol and e_b <= tol
 
 
-def chained_gpu_step(G, ctx, w, dtype):
+def chained_gpu_step(G, ctx, w, dtype, clustered=False):
     """One sub-GCN step through the library exactly as the benchmark runs it
     (unfused SGD, so that dW is visible), with host copies of every tensor
-    and the decisions the GPU took."""
+    and the decisions the GPU took; ``clustered`` takes the matrix-core
+    aggregation (GIST_LAYER_CLUSTERED) for every layer."""
     import torch
     from paper_2102_10424_amd.step import BatchSlot, SubGCN
     cfg, csr = w["cfg"], w["csr"]
@@ -212,7 +213,7 @@ def chained_gpu_step(G, ctx, w, dtype):
     s = cfg.slice_widths()
     dt = G.GIST_DTYPE_BF16_IN if dtype == "bf16" else G.GIST_DTYPE_F32
     X_all = torch.from_numpy(cfg.features_matrix()).cuda()
-    slot = BatchSlot(ctx, w["norm"], csr["n"], csr["nnz"], cfg.widths[0])
+    slot = BatchSlot(ctx, w["norm"], csr["n"], csr["nnz"], cfg.widths[0], clustered=clustered)
     b = slot.load(G.GraphHandle(w["g"]), w["clusters"], X_all, w["labels"])
     assert b.n == csr["n"] and b.nnz == csr["nnz"]
     n = b.n
@@ -243,9 +244,10 @@ def chained_gpu_step(G, ctx, w, dtype):
                 masks=[H[l + 1] > 0 for l in range(L - 1)] + [None])
 
 
-@pytest.mark.parametrize("name,dtype", [(c, "f32") for c in CONFIGS + ["c6"]] +
-                         [(c, "bf16") for c in CONFIGS])
-def test_step_chained(G, ctx, name, dtype):
+@pytest.mark.parametrize("name,dtype,clustered", [(c, "f32", False) for c in CONFIGS + ["c6"]] +
+                         [(c, "bf16", False) for c in CONFIGS] +
+                         [("c3", "f32", True), ("c4", "f32", True)])
+def test_step_chained(G, ctx, name, dtype, clustered):
     from oracle import layers as OLr
     w = workload(name)
     cfg, csr = w["cfg"], w["csr"]
@@ -253,10 +255,10 @@ def test_step_chained(G, ctx, name, dtype):
     s = cfg.slice_widths()
     tol = BF16_TOL if dtype == "bf16" else FP32_TOL
     band_rel = 1e-2 if dtype == "bf16" else 1e-5
-    got = chained_gpu_step(G, ctx, w, dtype)
+    got = chained_gpu_step(G, ctx, w, dtype, clustered)
     rnd = OLr.round_bf16 if dtype == "bf16" else None
     orders = gpu_orders(kind, s)
-    log(f"[{name} {dtype}] oracle step through the GPU's decisions")
+    log(f"[{name} {dtype}{' tiles' if clustered else ''}] oracle step through the GPU's decisions")
     ref = OG.sub_gcn_step(kind, csr, w["X"], w["y"], w["params"], LR, masks=got["masks"],
                           pos=got["pos"], rnd=rnd, orders=orders)
     errs = {}
