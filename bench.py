@@ -436,6 +436,12 @@ class LayerWorkload:
         self.desc = G.layer_desc(G.GIST_LAYER_GCN, G.GIST_ACT_RELU, n, d_in, self.s_out,
                                  G.GIST_DTYPE_BF16_IN if dtype == "bf16" else G.GIST_DTYPE_F32,
                                  flags=G.GIST_LAYER_CLUSTERED if clustered else 0)
+        # backward as a hidden layer inside a ReLU chain: the upstream gradient
+        # arrives as dZ (the layer above applied this layer's ReLU derivative)
+        # and dH leaves times the layer below's derivative 1[H > 0]
+        self.bdesc = G.layer_desc(G.GIST_LAYER_GCN, G.GIST_ACT_RELU, n, d_in, self.s_out,
+                                  self.desc.dtype, flags=self.desc.flags | G.GIST_LAYER_DZ_IN |
+                                  G.GIST_LAYER_MASK_DH)
         f, bb = G.gist_layer_workspace_size(self.desc)
         self.ws = torch.empty(max(f, bb), dtype=torch.uint8, device="cuda")
         self.agg = torch.empty(n, d_in, device="cuda")
@@ -446,7 +452,7 @@ class LayerWorkload:
     def step(self):
         G, b = self.G, self.b
         G.gist_gcn_layer_fwd(self.ctx, self.desc, b.A, b.X, self.W, self.agg, self.Ho, self.ws)
-        G.gist_gcn_layer_bwd(self.ctx, self.desc, b.A, None, b.X, self.agg, self.Ho, self.W,
+        G.gist_gcn_layer_bwd(self.ctx, self.bdesc, b.A, None, b.X, self.agg, self.Ho, self.W,
                              self.dHo, self.dW, self.dH, self.ws)
 
     def steps_per_unit(self):
@@ -454,7 +460,8 @@ class LayerWorkload:
 
     def describe(self):
         return {"workload": f"c5: one GCN layer fwd+bwd, full graph N={self.graph.n}, "
-                            f"nnz={self.graph.nnz + self.graph.n}, {self.d_in}->{self.s_out}",
+                            f"nnz={self.graph.nnz + self.graph.n}, {self.d_in}->{self.s_out}; "
+                            "backward as a hidden layer of a ReLU chain (dZ in, masked dH out)",
                 "model": "GIST sub-GCN layer", "global_batch": self.graph.n,
                 "d_in": self.d_in, "s_out": self.s_out}
 

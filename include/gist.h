@@ -266,7 +266,30 @@ typedef struct gist_layer_desc {
  *   H_out, dH_out     n x (G s_out), sub-GCN g in columns [g s_out, ...);
  *                     with GIST_LAYER_GROUP_MAJOR_OUT G consecutive
  *                     n x s_out blocks (each sub-GCN's logits contiguous). */
-enum { GIST_LAYER_SHARED_INPUT = 1, GIST_LAYER_GROUP_MAJOR_OUT = 2, GIST_LAYER_CLUSTERED = 4 };
+enum {
+  GIST_LAYER_SHARED_INPUT = 1,
+  GIST_LAYER_GROUP_MAJOR_OUT = 2,
+  GIST_LAYER_CLUSTERED = 4,
+  GIST_LAYER_DZ_IN = 8,
+  GIST_LAYER_MASK_DH = 16
+};
+
+/* The ReLU derivative of a hidden layer, fused into the producer of the
+ * gradient it multiplies (backward pass only; the forward ignores these):
+ *   GIST_LAYER_MASK_DH  the backward pass writes dH * 1[H > 0] instead of dH:
+ *                       the gradient with respect to the pre-activation of
+ *                       the layer below, whose (ReLU) output H is.  The
+ *                       product is applied in the epilogue of the kernel that
+ *                       writes dH (the transposed aggregation, or the dH
+ *                       product of a transform-first GCN layer).
+ *   GIST_LAYER_DZ_IN    dH_out already is dZ = dH_out * 1[H_out > 0] (the
+ *                       layer above was called with GIST_LAYER_MASK_DH), so
+ *                       no ReLU derivative is formed here and H_out may be
+ *                       NULL.
+ * A chain of ReLU layers passes MASK_DH to every layer above the first and
+ * DZ_IN to every hidden layer: no separate ReLU-derivative pass remains, and
+ * the gradients are bitwise those of the unflagged calls (the derivative is
+ * the same select, 1[H > 0], applied to the same values). */
 
 /* GIST_LAYER_CLUSTERED: a hint that Abar (and A_T) is the matrix of a
  * cluster mini-batch over block-contiguous node ids (Section 2.2: a union of
@@ -309,7 +332,7 @@ gist_status gist_gcn_layer_fwd(gist_ctx* ctx, const gist_layer_desc* L,
 
 /* Sub-GCN layer backward (chain rule of the forward).
  *
- *   dZ = dH_out * 1[H_out > 0] (ReLU) or dH_out (identity)
+ *   dZ = dH_out * 1[H_out > 0] (ReLU) or dH_out (identity, or DZ_IN)
  *   GCN:  dW = (Abar H)^T dZ,               dH = Abar^T (dZ W^T)
  *   SAGE: dW = [H | Abar H]^T dZ  ([2 s_in x s_out]),
  *         dH = dZ W_self^T + Abar^T (dZ W_neigh^T)

@@ -212,7 +212,8 @@ gist_status check_desc(const gist_layer_desc* L) {
   if (L->n < 0 || L->s_in < 1 || L->s_out < 1 || L->groups < 0)
     return set_error(GIST_E_INVAL, "layer: bad sizes");
   if (L->flags & ~static_cast<uint32_t>(GIST_LAYER_SHARED_INPUT | GIST_LAYER_GROUP_MAJOR_OUT |
-                                         GIST_LAYER_CLUSTERED))
+                                         GIST_LAYER_CLUSTERED | GIST_LAYER_DZ_IN |
+                                         GIST_LAYER_MASK_DH))
     return set_error(GIST_E_INVAL, "layer: unknown flags");
   if (L->n > INT32_MAX) return set_error(GIST_E_UNSUPPORTED, "layer: n exceeds int32 rows");
   if (L->n_in < 0) return set_error(GIST_E_INVAL, "layer: bad n_in");
@@ -259,12 +260,13 @@ Lay layout(const gist_layer_desc* L) {
 // gather kernel.
 gist_status aggregate(hipStream_t st, const Lay& y, const gist_csr_dev* A, int64_t rows,
                       int64_t cols, const float* X, int64_t ldx, int width, float* Y,
-                      int64_t ldy, const float* add, int64_t ld_add, bool relu) {
+                      int64_t ldy, const float* add, int64_t ld_add, bool relu,
+                      const float* mask = nullptr, int64_t ldm = 0) {
   if (y.clustered)
     return gist::spmm_clustered(st, rows, cols, A->nnz, A->rowptr, A->col, A->val, X, ldx, width,
-                                Y, ldy, add, ld_add, relu);
+                                Y, ldy, add, ld_add, relu, mask, ldm);
   return gist::spmm(st, rows, A->nnz, A->rowptr, A->col, A->val, X, ldx, width, Y, ldy, add,
-                    ld_add, relu);
+                    ld_add, relu, mask, ldm);
 }
 
 // A X over output-width tensors (dZ-like layout), A with `rows` rows: one
@@ -318,7 +320,7 @@ BwdPlan plan_bwd(const gist_layer_desc* L) {
   BwdPlan p;
   const Lay y = layout(L);
   const int64_t n = y.n, n_in = y.n_in, si = y.si, so = y.so, G = y.G;
-  if (L->act == GIST_ACT_RELU) p.dz = fbytes(n, G * so);
+  if (L->act == GIST_ACT_RELU && !(L->flags & GIST_LAYER_DZ_IN)) p.dz = fbytes(n, G * so);
   const int order = resolve_order(L);
   int64_t wm, wk;   // dW = X^T D: M x so, reduced over K nodes
   if (L->kind == GIST_LAYER_SAGE_MEAN || order == GIST_ORDER_AGG_FIRST) {
@@ -439,12 +441,16 @@ gist_status layer_bwd(gist_ctx* ctx, const gist_layer_desc* L, const gist_csr_de
   else if (A_T) GIST_TRY(check_csr(A_T, n_in, wt.c_str()));
   const int order = resolve_order(L);
   const bool relu = L->act == GIST_ACT_RELU;
+  // dH_out already carries this layer's ReLU derivative (the layer above
+  // applied it with GIST_LAYER_MASK_DH); dH takes the layer below's
+  const bool dz_in = (L->flags & GIST_LAYER_DZ_IN) != 0;
+  const float* dh_mask = (L->flags & GIST_LAYER_MASK_DH) ? H : nullptr;
   const bool fused = W_sgd != nullptr;
   if (!W || (!fused && !dW)) return set_error(GIST_E_INVAL, what + ": NULL dW or W");
   if (fused && !std::isfinite(lr)) return set_error(GIST_E_INVAL, what + ": lr not finite");
   if (dH && y.shared)
     return set_error(GIST_E_INVAL, what + ": a shared input has no per-group dH");
-  if (n > 0 && (!H || !dH_out || (relu && !H_out)))
+  if (n > 0 && (!H || !dH_out || (relu && !dz_in && !H_out)))
     return set_error(GIST_E_INVAL, what + ": NULL pointer");
   if (n > 0 && (sage || order == GIST_ORDER_AGG_FIRST) && !agg_save)
     return set_error(GIST_E_INVAL, what + ": agg_save required");
@@ -466,7 +472,7 @@ gist_status layer_bwd(gist_ctx* ctx, const gist_layer_desc* L, const gist_csr_de
                                        align256(p.gemm));
   float* tB = reinterpret_cast<float*>(reinterpret_cast<char*>(tA) + align256(p.ta));
   const float* dZ = dH_out;
-  if (relu) {
+  if (relu && !dz_in) {
     GIST_TRY(gist::relu_mask(st, n * G * so, dH_out, H_out, dZbuf));
     dZ = dZbuf;
   }
@@ -522,9 +528,10 @@ gist_status layer_bwd(gist_ctx* ctx, const gist_layer_desc* L, const gist_csr_de
         o2.c0 = tmp; o2.ldc0 = ld_p; o2.gs0 = si;
       }
       GIST_TRY(gist::gemm(st, n, y.wrows, so, a2, w_as_b, o2, L->dtype, gws, gbytes, G));
-      // dH (+)= Abar^T dP, every group at once
+      // dH (+)= Abar^T dP, every group at once (times the layer below's
+      // ReLU derivative with GIST_LAYER_MASK_DH)
       return aggregate(st, y, AT, n_in, n, tmp, ld_p, int(ld_p), dH, ld_p, sage ? dH : nullptr,
-                       ld_p, false);
+                       ld_p, false, dh_mask, y.ld_in);
     };
     if (fused) {
       GIST_TRY(input_grad());
@@ -558,6 +565,7 @@ gist_status layer_bwd(gist_ctx* ctx, const gist_layer_desc* L, const gist_csr_de
     a2.p0 = tmp; a2.ld0 = y.ld_out; a2.gs0 = y.gs_out_in; a2.k_major = true;
     gist::GemmOut o2;
     o2.c0 = dH; o2.ldc0 = ld_p; o2.gs0 = si;
+    o2.mask = dh_mask; o2.ldm = y.ld_in; o2.gsm = y.gs_in;
     return gist::gemm(st, n_in, si, so, a2, w_as_b, o2, L->dtype, gws, gbytes, G);
   };
   if (fused) {

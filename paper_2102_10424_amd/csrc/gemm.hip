@@ -75,11 +75,14 @@ struct OutDev {
   int64_t gs0, gs1;
   int sgd;     // C <- fmaf(-lr, product, C): a fused SGD step on weights in C
   float lr;
+  const float* mask;   // C <- 0 where mask <= 0 (c0 columns only), or null
+  int64_t ldm, gsm;
 
   __device__ __forceinline__ OutDev group(int64_t g) const {
     OutDev o = *this;
     o.c0 += g * gs0;
     o.c1 += g * gs1;
+    if (mask) o.mask += g * gsm;
     return o;
   }
 };
@@ -272,6 +275,7 @@ __device__ __forceinline__ float* out_ptr(const OutDev& C, int64_t row, int64_t 
 
 __device__ __forceinline__ void store_out(const OutDev& C, int64_t row, int64_t col, float v) {
   if (C.relu) v = fmaxf(v, 0.f);
+  if (C.mask && col < C.c_split && !(C.mask[row * C.ldm + col] > 0.f)) v = 0.f;
   float* p = out_ptr(C, row, col);
   if (C.sgd) v = fmaf(-C.lr, v, *p);
   *p = v;
@@ -555,6 +559,7 @@ __global__ __launch_bounds__(256) void streamk_fixup(int64_t M, int64_t N, Sched
 }
 
 constexpr int64_t kStreamWG = 512;   // two resident 256-thread blocks per CU, 256 CUs
+constexpr int64_t kMinSteps = 8;     // fewest K steps a stream-K workgroup takes
 
 Sched make_sched(int64_t M, int64_t N, int64_t K, int dtype, int64_t groups = 1) {
   const int ks = dtype == GIST_DTYPE_BF16_IN ? KSH : BK;
@@ -568,7 +573,12 @@ Sched make_sched(int64_t M, int64_t N, int64_t K, int dtype, int64_t groups = 1)
   if (tiles >= 4 * kStreamWG) {
     s.ipw = s.nk;   // enough tiles: one whole tile per workgroup
   } else {
-    s.ipw = (s.T + kStreamWG - 1) / kStreamWG;
+    // stream-K over kStreamWG workgroups, but at least kMinSteps K steps
+    // each: a small product (a narrow slice, few tiles) split one step per
+    // workgroup would write a 64 KB partial tile per step for the fix-up to
+    // read back
+    s.ipw = std::max<int64_t>((s.T + kStreamWG - 1) / kStreamWG,
+                              std::min<int64_t>(s.nk, kMinSteps));
   }
   return s;
 }
@@ -632,7 +642,7 @@ gist_status gemm(hipStream_t st, int64_t M, int64_t N, int64_t K, const Operand&
                  int64_t ngroups) {
   if (M <= 0 || N <= 0 || ngroups <= 0) return GIST_OK;
   OutDev c{C.c0, C.c1, C.ldc0, C.ldc1, C.c_split, C.relu ? 1 : 0, C.gs0, C.gs1,
-           C.sgd ? 1 : 0, C.lr};
+           C.sgd ? 1 : 0, C.lr, C.mask, C.ldm, C.gsm};
   if (K <= 0) return set_error(GIST_E_UNSUPPORTED, "gemm: K == 0");
   if (dtype == GIST_DTYPE_BF16_IN && gemm_bf16_packed_eligible(M, N, K)) {
     // the packed path converts each group's operands; groups run in turn
@@ -645,6 +655,7 @@ gist_status gemm(hipStream_t st, int64_t M, int64_t N, int64_t K, const Operand&
       if (B.p1) bg.p1 += g * B.gs1;
       cg.c0 += g * C.gs0;
       if (C.c1) cg.c1 += g * C.gs1;
+      if (C.mask) cg.mask += g * C.gsm;
       gist_status s = gemm_bf16_packed(st, M, N, K, ag, bg, cg, ws, ws_bytes);
       if (s != GIST_OK) return s;
     }

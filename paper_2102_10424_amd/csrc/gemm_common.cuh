@@ -47,9 +47,12 @@ struct OutView {
   int relu;
   int sgd;
   float lr;
+  const float* mask;   // store 0 where mask <= 0 (c0 columns only), or null
+  int64_t ldm;
 
   static OutView from(const GemmOut& c) {
-    return OutView{c.c0, c.c1, c.ldc0, c.ldc1, c.c_split, c.relu ? 1 : 0, c.sgd ? 1 : 0, c.lr};
+    return OutView{c.c0, c.c1, c.ldc0, c.ldc1, c.c_split, c.relu ? 1 : 0, c.sgd ? 1 : 0, c.lr,
+                   c.mask, c.ldm};
   }
   template <bool SPLIT>
   __device__ __forceinline__ float* ptr(int64_t row, int64_t col) const {
@@ -58,6 +61,7 @@ struct OutView {
   template <bool SPLIT>
   __device__ __forceinline__ void store(int64_t row, int64_t col, float v) const {
     if (relu) v = fmaxf(v, 0.f);
+    if (mask && (!SPLIT || col < c_split) && !(mask[row * ldm + col] > 0.f)) v = 0.f;
     float* p = ptr<SPLIT>(row, col);
     if (sgd) v = fmaf(-lr, v, *p);
     *p = v;

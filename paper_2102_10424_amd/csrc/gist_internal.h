@@ -93,10 +93,13 @@ class DeviceGuard {
 
 // Y[r, c] = sum_e val[e] * X[col[e], c]  (+ Add[r, c]) (ReLU optional),
 // r < n, c < width.  Row-major with leading dimensions.  `add` may alias Y.
+// With `mask` (leading dimension ldm), Y[r, c] is stored as 0 where
+// mask[r, c] > 0 fails: the ReLU derivative of the layer whose output mask is.
 gist_status spmm(hipStream_t st, int64_t n, int64_t nnz, const int32_t* rowptr,
                  const int32_t* col, const float* val, const float* X,
                  int64_t ldx, int width, float* Y, int64_t ldy,
-                 const float* add, int64_t ld_add, bool relu);
+                 const float* add, int64_t ld_add, bool relu,
+                 const float* mask = nullptr, int64_t ldm = 0);
 
 // The same on the matrix cores for a matrix (n x n_in) whose entries sit
 // mostly near the diagonal (a cluster mini-batch): dense bf16-split tiles
@@ -105,7 +108,8 @@ gist_status spmm(hipStream_t st, int64_t n, int64_t nnz, const int32_t* rowptr,
 gist_status spmm_clustered(hipStream_t st, int64_t n, int64_t n_in, int64_t nnz,
                            const int32_t* rowptr, const int32_t* col, const float* val,
                            const float* X, int64_t ldx, int width, float* Y, int64_t ldy,
-                           const float* add, int64_t ld_add, bool relu);
+                           const float* add, int64_t ld_add, bool relu,
+                           const float* mask = nullptr, int64_t ldm = 0);
 
 // Operand of a GEMM: logical R x K matrix (R = M for A, N for B).
 //   k_major == true : element (r, k) at p[r * ld + k]   (K contiguous)
@@ -136,6 +140,10 @@ struct GemmOut {
   int64_t gs0 = 0, gs1 = 0;   // element offsets of c0 / c1 between GEMM groups
   bool sgd = false;
   float lr = 0.f;
+  // C[r, c] is stored as 0 where mask[r, c] > 0 fails (the ReLU derivative of
+  // the layer below, applied as its input gradient is written); c0 only
+  const float* mask = nullptr;
+  int64_t ldm = 0, gsm = 0;
 };
 
 // `groups` independent products of the same shape: group g reads A and B

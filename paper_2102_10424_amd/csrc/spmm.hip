@@ -66,7 +66,7 @@ __global__ __launch_bounds__(256) void spmm_kernel(
     int n, const int* __restrict__ rowptr, const int* __restrict__ col,
     const float* __restrict__ val, const float* __restrict__ X, int64_t ldx, int width,
     float* Y, int64_t ldy, const float* add, int64_t ld_add, int relu, int col_tiles,
-    int64_t nblocks) {
+    int64_t nblocks, const float* mask, int64_t ldm) {
   constexpr int RPW = 64 / LPR;  // rows per wave
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -142,6 +142,12 @@ __global__ __launch_bounds__(256) void spmm_kernel(
 #pragma unroll
     for (int v = 0; v < VEC; ++v) acc[v] = fmaxf(acc[v], 0.f);
   }
+  if (mask) {   // the ReLU derivative of the layer whose output is `mask`
+    float mv[VEC];
+    load_vec<VEC>(mask + row * ldm + c0, mv);
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) acc[v] = mv[v] > 0.f ? acc[v] : 0.f;
+  }
   store_vec<VEC>(Y + row * ldy + c0, acc);
 }
 
@@ -154,7 +160,7 @@ __global__ __launch_bounds__(256) void spmm_wide_kernel(
     int n, const int* __restrict__ rowptr, const int* __restrict__ col,
     const float* __restrict__ val, const float* __restrict__ X, int64_t ldx, int width,
     float* Y, int64_t ldy, const float* add, int64_t ld_add, int relu, int col_tiles,
-    int64_t nblocks) {
+    int64_t nblocks, const float* mask, int64_t ldm) {
   constexpr int kUnroll = 8;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -222,13 +228,20 @@ __global__ __launch_bounds__(256) void spmm_wide_kernel(
 #pragma unroll
     for (int v = 0; v < VEC; ++v) acc[v] = fmaxf(acc[v], 0.f);
   }
+  if (mask) {   // the ReLU derivative of the layer whose output is `mask`
+    float mv[VEC];
+    load_vec<VEC>(mask + row * ldm + c0, mv);
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) acc[v] = mv[v] > 0.f ? acc[v] : 0.f;
+  }
   store_vec<VEC>(Y + row * ldy + c0, acc);
 }
 
 template <int VEC, int LPR>
 gist_status launch(hipStream_t st, int64_t n, int64_t nnz, const int32_t* rowptr, const int32_t* col,
                    const float* val, const float* X, int64_t ldx, int width, float* Y,
-                   int64_t ldy, const float* add, int64_t ld_add, bool relu) {
+                   int64_t ldy, const float* add, int64_t ld_add, bool relu, const float* mask,
+                   int64_t ldm) {
   constexpr int RPW = 64 / LPR;
   const int col_tiles = (width + LPR * VEC - 1) / (LPR * VEC);
   const int64_t rblocks = (n + kWaves * RPW - 1) / (kWaves * RPW);
@@ -239,16 +252,17 @@ gist_status launch(hipStream_t st, int64_t n, int64_t nnz, const int32_t* rowptr
   // algorithmic bytes: rowptr, (col, val) per nonzero, X read once, Y written
   // once (and Add read once)
   const double bytes = 4.0 * (n + 1) + 8.0 * static_cast<double>(nnz) +
-                       4.0 * static_cast<double>(n) * width * (add ? 3.0 : 2.0);
+                       4.0 * static_cast<double>(n) * width * (2.0 + (add ? 1.0 : 0.0) +
+                                                                (mask ? 1.0 : 0.0));
   ProfScope ps(st, name, 2.0 * static_cast<double>(nnz) * width, bytes);
   if constexpr (LPR == 64) {
     hipLaunchKernelGGL((spmm_wide_kernel<VEC>), dim3(static_cast<unsigned>(nblocks)), dim3(256),
                        0, st, static_cast<int>(n), rowptr, col, val, X, ldx, width, Y, ldy, add,
-                       ld_add, relu ? 1 : 0, col_tiles, nblocks);
+                       ld_add, relu ? 1 : 0, col_tiles, nblocks, mask, ldm);
   } else {
     hipLaunchKernelGGL((spmm_kernel<VEC, LPR>), dim3(static_cast<unsigned>(nblocks)), dim3(256),
                        0, st, static_cast<int>(n), rowptr, col, val, X, ldx, width, Y, ldy, add,
-                       ld_add, relu ? 1 : 0, col_tiles, nblocks);
+                       ld_add, relu ? 1 : 0, col_tiles, nblocks, mask, ldm);
   }
   return check_launch("spmm");
 }
@@ -256,38 +270,51 @@ gist_status launch(hipStream_t st, int64_t n, int64_t nnz, const int32_t* rowptr
 template <int VEC>
 gist_status launch_vec(hipStream_t st, int64_t n, int64_t nnz, const int32_t* rowptr, const int32_t* col,
                        const float* val, const float* X, int64_t ldx, int width, float* Y,
-                       int64_t ldy, const float* add, int64_t ld_add, bool relu) {
+                       int64_t ldy, const float* add, int64_t ld_add, bool relu,
+                       const float* mask, int64_t ldm) {
   // lanes per row: the smallest power of two covering the row, at most 64
   const int chunks = (width + VEC - 1) / VEC;
   if (chunks > 32)
-    return launch<VEC, 64>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add, relu);
+    return launch<VEC, 64>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add,
+                               relu, mask, ldm);
   if (chunks > 16)
-    return launch<VEC, 32>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add, relu);
+    return launch<VEC, 32>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add,
+                               relu, mask, ldm);
   if (chunks > 8)
-    return launch<VEC, 16>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add, relu);
+    return launch<VEC, 16>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add,
+                               relu, mask, ldm);
   if (chunks > 4)
-    return launch<VEC, 8>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add, relu);
-  return launch<VEC, 4>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add, relu);
+    return launch<VEC, 8>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add,
+                               relu, mask, ldm);
+  return launch<VEC, 4>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add,
+                             relu, mask, ldm);
 }
 
 }  // namespace
 
 gist_status spmm(hipStream_t st, int64_t n, int64_t nnz, const int32_t* rowptr, const int32_t* col,
                  const float* val, const float* X, int64_t ldx, int width, float* Y,
-                 int64_t ldy, const float* add, int64_t ld_add, bool relu) {
+                 int64_t ldy, const float* add, int64_t ld_add, bool relu, const float* mask,
+                 int64_t ldm) {
   if (n <= 0 || width <= 0) return GIST_OK;
   const bool v4 = width % 4 == 0 && ldx % 4 == 0 && ldy % 4 == 0 && aligned16(X) &&
-                  aligned16(Y) && (!add || (ld_add % 4 == 0 && aligned16(add)));
+                  aligned16(Y) && (!add || (ld_add % 4 == 0 && aligned16(add))) &&
+                  (!mask || (ldm % 4 == 0 && aligned16(mask)));
   const bool v2 = width % 2 == 0 && ldx % 2 == 0 && ldy % 2 == 0 && aligned8(X) &&
-                  aligned8(Y) && (!add || (ld_add % 2 == 0 && aligned8(add)));
+                  aligned8(Y) && (!add || (ld_add % 2 == 0 && aligned8(add))) &&
+                  (!mask || (ldm % 2 == 0 && aligned8(mask)));
   // Prefer the widest vector that still fills a 64-lane row; a row that
   // would need fewer than 33 lanes at 16 bytes uses 8-byte vectors instead
   // when that gives a full-wave row (e.g. width 100: 50 lanes x 2 floats).
   if (v4 && (width > 128 || width <= 64))
-    return launch_vec<4>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add, relu);
-  if (v2) return launch_vec<2>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add, relu);
-  if (v4) return launch_vec<4>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add, relu);
-  return launch_vec<1>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add, relu);
+    return launch_vec<4>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add,
+                         ld_add, relu, mask, ldm);
+  if (v2) return launch_vec<2>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add,
+                         ld_add, relu, mask, ldm);
+  if (v4) return launch_vec<4>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add,
+                         ld_add, relu, mask, ldm);
+  return launch_vec<1>(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add,
+                         ld_add, relu, mask, ldm);
 }
 
 }  // namespace gist

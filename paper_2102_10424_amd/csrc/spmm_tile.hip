@@ -111,7 +111,7 @@ __global__ __launch_bounds__(256) void spmm_tile_kernel(
     int n, int n_in, const int* __restrict__ rowptr, const int* __restrict__ col,
     const float* __restrict__ val, const float* __restrict__ X, int64_t ldx, int width,
     float* Y, int64_t ldy, const float* add, int64_t ld_add, int relu, int tiles,
-    int64_t nblocks) {
+    int64_t nblocks, const float* mask, int64_t ldm) {
   // dense tile (hi, lo), later the fp32 result tile
   __shared__ __attribute__((aligned(16))) unsigned short Atile[2 * kRows * kALd];
   __shared__ int red[8];
@@ -336,6 +336,7 @@ __global__ __launch_bounds__(256) void spmm_tile_kernel(
         float y = Ys[(8 * wave + i) * kYLd + lane + 64 * p];
         if (add) y += add[r * ld_add + c];
         if (relu) y = fmaxf(y, 0.f);
+        if (mask && !(mask[r * ldm + c] > 0.f)) y = 0.f;   // ReLU derivative of the layer below
         Y[r * ldy + c] = y;
       }
     }
@@ -347,7 +348,8 @@ __global__ __launch_bounds__(256) void spmm_tile_kernel(
 gist_status spmm_clustered(hipStream_t st, int64_t n, int64_t n_in, int64_t nnz,
                            const int32_t* rowptr, const int32_t* col, const float* val,
                            const float* X, int64_t ldx, int width, float* Y, int64_t ldy,
-                           const float* add, int64_t ld_add, bool relu) {
+                           const float* add, int64_t ld_add, bool relu, const float* mask,
+                           int64_t ldm) {
   if (n <= 0 || width <= 0) return GIST_OK;
   const int64_t tiles = (n + kRows - 1) / kRows;
   const int64_t slabs = (width + kCols - 1) / kCols;
@@ -355,11 +357,13 @@ gist_status spmm_clustered(hipStream_t st, int64_t n, int64_t n_in, int64_t nnz,
   if (nblocks > INT32_MAX || tiles > INT32_MAX)
     return set_error(GIST_E_UNSUPPORTED, "spmm_clustered: grid too large");
   const double bytes = 4.0 * (n + 1) + 8.0 * static_cast<double>(nnz) +
-                       4.0 * static_cast<double>(n) * width * (add ? 3.0 : 2.0);
+                       4.0 * static_cast<double>(n) * width * (2.0 + (add ? 1.0 : 0.0) +
+                                                                (mask ? 1.0 : 0.0));
   ProfScope ps(st, "spmm_tile", 2.0 * static_cast<double>(nnz) * width, bytes);
   hipLaunchKernelGGL(spmm_tile_kernel, dim3(static_cast<unsigned>(nblocks)), dim3(256), 0, st,
                      static_cast<int>(n), static_cast<int>(n_in), rowptr, col, val, X, ldx, width,
-                     Y, ldy, add, ld_add, relu ? 1 : 0, static_cast<int>(tiles), nblocks);
+                     Y, ldy, add, ld_add, relu ? 1 : 0, static_cast<int>(tiles), nblocks, mask,
+                     ldm);
   return check_launch("spmm_clustered");
 }
 

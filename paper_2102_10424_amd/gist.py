@@ -49,6 +49,7 @@ GIST_SUBAGG_CHECK_FINITE = 1
 GIST_ADAM_FRESH = 1
 GIST_NOALLOC_LOSS_MAX_ROWS = 4194304
 GIST_LAYER_SHARED_INPUT, GIST_LAYER_GROUP_MAJOR_OUT, GIST_LAYER_CLUSTERED = 1, 2, 4
+GIST_LAYER_DZ_IN, GIST_LAYER_MASK_DH = 8, 16
 
 NORM_BY_NAME = {"gcn": GIST_NORM_GCN_SYM, "sage": GIST_NORM_SAGE_MEAN,
                 "theory": GIST_NORM_THEORY}

@@ -720,6 +720,15 @@ class LadiesView:
         return self._A[l], self._AT[l]
 
 
+def relu_chain_flags(l, L):
+    """Backward flags of layer l of L that fuse every hidden layer's ReLU
+    derivative into the kernel writing the gradient it multiplies: a hidden
+    layer's dH_out arrives as dZ (GIST_LAYER_DZ_IN), and every layer above the
+    first writes dH times the layer below's derivative (GIST_LAYER_MASK_DH).
+    No separate ReLU-derivative pass runs; the results are bitwise the same."""
+    return (G.GIST_LAYER_DZ_IN if l < L - 1 else 0) | (G.GIST_LAYER_MASK_DH if l > 0 else 0)
+
+
 class SubGCN:
     """Buffers and call sequence of one sub-GCN's training step.
 
@@ -766,7 +775,9 @@ class SubGCN:
         # GCN / SAGE save the aggregation Abar H; GAT saves the transform P = H Theta
         self.agg = [torch.empty(n_cap, w[l + 1] if self.gat else w[l], device=d)
                     for l in range(self.L)]
-        self.dH = [torch.empty(n_cap, w[l], device=d) for l in range(self.L)]  # dH[l] wrt H_l
+        # dH[l]: the gradient reaching H_l; for GCN / SAGE times its ReLU
+        # derivative 1[H_l > 0], which the layer above applies (MASK_DH)
+        self.dH = [torch.empty(n_cap, w[l], device=d) for l in range(self.L)]
         self.dlogits = torch.empty(n_cap, w[self.L], device=d)
         self.loss_ws = torch.empty(G.gist_softmax_xent_workspace(n_cap), dtype=torch.uint8,
                                    device=d)
@@ -883,11 +894,15 @@ class SubGCN:
                                      self.agg[l][:n], self.alpha[l][:nnz], self.H[l + 1][:n],
                                      W, a1, a2, dout, gW, g1, g2, dH, ws)
             elif fused:
-                G.gist_gcn_layer_bwd_sgd(self.ctx, self._ldesc(batch, l), A, A_T, Hin,
+                desc = self._ldesc(batch, l)
+                desc.flags |= relu_chain_flags(l, self.L)
+                G.gist_gcn_layer_bwd_sgd(self.ctx, desc, A, A_T, Hin,
                                          self.agg[l][:n], self.H[l + 1][:n], params[l], dout,
                                          sgd_lr, dH, ws)
             else:
-                G.gist_gcn_layer_bwd(self.ctx, self._ldesc(batch, l), A, A_T, Hin,
+                desc = self._ldesc(batch, l)
+                desc.flags |= relu_chain_flags(l, self.L)
+                G.gist_gcn_layer_bwd(self.ctx, desc, A, A_T, Hin,
                                      self.agg[l][:n], self.H[l + 1][:n], params[l], dout,
                                      self.dW[l], dH, ws)
             dout = dH
@@ -1031,12 +1046,14 @@ class SubGCNBatch:
         for l in reversed(range(self.L)):
             Hin = batch.X if l == 0 else self.H[l][:n]
             dH = self.dH[l][:n] if l > 0 else None
+            desc = self.desc(l, n)
+            desc.flags |= relu_chain_flags(l, self.L)
             if fused:
-                G.gist_gcn_layer_bwd_sgd(self.ctx, self.desc(l, n), batch.A, batch.A_T, Hin,
+                G.gist_gcn_layer_bwd_sgd(self.ctx, desc, batch.A, batch.A_T, Hin,
                                          self.agg[l][:n], self._out(l, n), params[l], dout,
                                          sgd_lr, dH, ws)
             else:
-                G.gist_gcn_layer_bwd(self.ctx, self.desc(l, n), batch.A, batch.A_T, Hin,
+                G.gist_gcn_layer_bwd(self.ctx, desc, batch.A, batch.A_T, Hin,
                                      self.agg[l][:n], self._out(l, n), params[l], dout,
                                      self.dW[l], dH, ws)
             dout = dH

@@ -140,7 +140,7 @@ def test_batched_errors(G, ctx):
     with pytest.raises(G.GistError) as e:   # a shared input has no per-group dH
         G.gist_gcn_layer_bwd(ctx, desc, A, None, t, t, t, t, t, t, t, t)
     assert e.value.status == G.GIST_E_INVAL
-    bad = G.layer_desc(G.GIST_LAYER_GCN, 1, 4, 2, 2, groups=2, flags=8)
+    bad = G.layer_desc(G.GIST_LAYER_GCN, 1, 4, 2, 2, groups=2, flags=64)   # no such flag
     with pytest.raises(G.GistError):
         G.gist_layer_workspace_size(bad)
 

@@ -287,7 +287,8 @@ def test_ladies_step_matches_oracle(G, ctx, widths, b, s, dtype):
         if l < w.L - 1:
             e[f"H{l + 1}"] = relerr(to_host(run.H[l + 1][:b.rows(l + 1)]), ref["H"][l + 1])
         if l > 0:
-            e[f"dH{l}"] = relerr(to_host(run.dH[l][:b.rows(l)]), ref["dH"][l])
+            # the layer above hands this one dH times its ReLU derivative
+            e[f"dH{l}"] = relerr(to_host(run.dH[l][:b.rows(l)]), ref["dH"][l] * masks[l - 1])
         e[f"dW{l}"] = relerr(to_host(run.dW[l]), ref["grads"][l])
         e[f"W{l}"] = relerr(to_host(params[l]), ref["params"][l])
     log(f"  {flips} decisions differ within the band; " +
