@@ -47,6 +47,10 @@ def variant_symbol(variant):
         dt, ak, bk, av, bv = m.groups()
         args = ", ".join([b(ak == "K"), b(bk == "K"), b(av == "v"), b(bv == "v"), b(dt == "bf16")])
         return re.escape(f"gemm_kernel<{args}>") + "$"
+    m = re.fullmatch(r"gemm_bf16_direct_([KR])([KR])", variant)
+    if m:
+        ak, bk = m.groups()
+        return re.escape(f"gemm_bf16_direct_kernel<{b(ak == 'K')}, {b(bk == 'K')},")
     m = re.fullmatch(r"spmm_v(\d+)_l(\d+)", variant)
     if m:
         v, l = m.groups()

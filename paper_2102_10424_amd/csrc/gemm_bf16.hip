@@ -1,28 +1,34 @@
-// bf16-input GEMM for large products: operands are rounded to bf16 once,
-// into padded K-contiguous copies, then multiplied on the bf16 MFMA units
-// with fp32 accumulation.
+// bf16-input GEMM for large products: operands rounded to bf16 (nearest
+// even), multiplied on the bf16 MFMA units with fp32 accumulation, in
+// 256 x 256 tiles.
 //
-// Why a separate path: the bf16 matrix cores run 16x faster than fp32 ones,
-// so a kernel that streams fp32 operands (4 bytes per element) and rounds
-// them while staging cannot feed them.  Here
-//
-//   1. cvt_bf16_kernel rounds an operand (nearest-even, in hardware) into a
-//      bf16 buffer [Rp][Kp], K contiguous, zero-padded to the tile grid
-//      (row-contiguous operands are transposed through LDS on the way);
-//   2. gemm_bf16_kernel multiplies the padded copies in 256 x 256 tiles with
-//      eight waves (two per SIMD, so one wave's MFMAs run while the other
-//      waits on memory), each owning 128 rows x 64 columns (4 x 2 MFMA tiles
-//      of 32 x 32, v_mfma_f32_32x32x16_bf16), K steps of 32, double-buffered
-//      LDS with 80-byte rows (conflict-free 16-byte fragment reads), no
-//      bounds checks in the loads thanks to the padding;
-//   3. work units are (K slice, tile) pairs, K-slice-major, so the units an
+//   1. The product kernel: eight waves (two per SIMD, so one wave's MFMAs
+//      run while the other waits on memory), each owning 128 rows x 64
+//      columns (4 x 2 MFMA tiles of 32 x 32, v_mfma_f32_32x32x16_bf16), K
+//      steps of 32, double-buffered LDS tiles [row][k] with 80-byte rows
+//      (conflict-free 16-byte fragment reads), the next step's operands
+//      loaded into registers while the current one multiplies.
+//   2. Direct staging (the usual path): each step's operand tiles are read
+//      straight from the fp32 operands and rounded in registers on their way
+//      to LDS -- K-contiguous operands with 16-byte loads, row-contiguous
+//      ones with one row per lane (256 contiguous bytes per wave load),
+//      written K-major into the tile either way.  No conversion pass and no
+//      bf16 copies: each operand byte is read once from memory per tile that
+//      uses it, instead of read, written as bf16 and read back.
+//   3. Packed staging (operands the direct loads cannot take: K not a
+//      multiple of 32 for a K-contiguous operand, unaligned bases, a
+//      concatenation split inside a tile): cvt_bf16_kernel first rounds
+//      each operand into a zero-padded K-contiguous bf16 copy [Rp][Kp]
+//      (row-contiguous ones transposed through LDS), which the same product
+//      kernel then reads.
+//   4. Work units are (K slice, tile) pairs, K-slice-major, so the units an
 //      XCD runs together cover neighbouring tiles over the same K range at
 //      the same time and share their operands in L2.  Shapes with too few
 //      tiles to fill the GPU split K into up to kMaxSplit slices whose fp32
 //      partials a fix-up kernel sums in slice order (deterministic).
 //
-// The result equals the in-kernel-rounding path's: both round the same fp32
-// values to bf16 with round-to-nearest-even and accumulate in fp32.
+// Both stagings put the same bf16 values in the same LDS tiles and run the
+// same MFMA sequence, so they give bitwise the same result.
 
 #include <algorithm>
 #include <cstdio>
@@ -132,12 +138,155 @@ struct SchedB {
   int spu;                // K steps per slice
 };
 
-template <bool SPLIT_OUT>
-__global__ __launch_bounds__(kThr) void gemm_bf16_kernel(int64_t M, int64_t N,
-                                                         const unsigned short* __restrict__ A,
-                                                         const unsigned short* __restrict__ B,
-                                                         int64_t Kp, OutView C, SchedB S,
-                                                         float* __restrict__ partials) {
+typedef float float2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef unsigned uint4v __attribute__((ext_vector_type(4)));
+
+// Two values to packed bf16 (a in the low half), rounded to nearest even.
+__device__ __forceinline__ unsigned bf16_pair(float a, float b) {
+  return __builtin_bit_cast(unsigned, __builtin_convertvector((float2v){a, b}, bf16x2));
+}
+__device__ __forceinline__ uint4v pack8(const float* v) {
+  uint4v u;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) u[i] = bf16_pair(v[2 * i], v[2 * i + 1]);
+  return u;
+}
+
+// Staging of one operand's 256 x 32 tile per K step: `load` fetches this
+// thread's share from memory into registers, `store` writes it to the LDS
+// tile [row][k] (row stride LDH halves) as bf16.
+
+// From a padded bf16 copy [Rp][Kp]: rows (t >> 2) + 128 i, K (t & 3) * 8 .. +7.
+struct PackedOp {
+  const unsigned short* p;
+  int64_t Kp;
+};
+struct PackedStage {
+  ushort8 r[2];
+  const unsigned short* row;   // this thread's first row, at its K offset
+  __device__ __forceinline__ void init(const PackedOp& o, int64_t, int64_t, int64_t r0, int t) {
+    row = o.p + (r0 + (t >> 2)) * o.Kp + (t & 3) * 8;
+  }
+  __device__ __forceinline__ void load(const PackedOp& o, int64_t k0) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      r[i] = *reinterpret_cast<const ushort8*>(row + 128 * i * o.Kp + k0);
+  }
+  __device__ __forceinline__ void store(unsigned short* S, int t) const {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      *reinterpret_cast<ushort8*>(S + ((t >> 2) + 128 * i) * LDH + (t & 3) * 8) = r[i];
+  }
+};
+
+// Straight from the fp32 operand, rounded to bf16 (nearest even) on the way
+// to LDS.  Rows past the operand's end read its last rows (they only feed
+// output rows or columns that are never stored).  Each thread's rows are
+// fixed for the whole product, so their offsets are formed once, as 32-bit
+// byte offsets from a per-step base that is the same for the whole wave
+// (scalar address arithmetic, one vector register per load address).
+template <bool KMAJ>
+struct DirectStage;
+
+// K contiguous: rows (t >> 2) + 128 i, K (t & 3) * 8 .. +7 (two 16-byte
+// loads per row).  Needs K and the concatenation split to be multiples of
+// the K step (every step full and on one side of the split), leading
+// dimensions that are multiples of 4 floats and 16-byte bases.
+template <>
+struct DirectStage<true> {
+  float4 x[4];                 // row i: x[2i], x[2i+1] (K kc .. kc+7)
+  unsigned off0[2], off1[2];   // byte offsets of this thread's rows in p0 / p1
+  __device__ __forceinline__ void init(const OpView& o, int64_t R, int64_t, int64_t r0, int t) {
+    const int kc = (t & 3) * 8;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int64_t r = min(r0 + (t >> 2) + 128 * i, R - 1);
+      off0[i] = static_cast<unsigned>((r * o.ld0 + kc) * 4);
+      off1[i] = static_cast<unsigned>((r * o.ld1 + kc) * 4);
+    }
+  }
+  __device__ __forceinline__ void load(const OpView& o, int64_t k0) {
+    const bool first = k0 < o.split;
+    const char* base = reinterpret_cast<const char*>(first ? o.p0 + k0 : o.p1 + (k0 - o.split));
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const char* q = base + (first ? off0[i] : off1[i]);
+      x[2 * i] = *reinterpret_cast<const float4*>(q);
+      x[2 * i + 1] = *reinterpret_cast<const float4*>(q + 16);
+    }
+  }
+  __device__ __forceinline__ void store(unsigned short* S, int t) const {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const float4 a = x[2 * i], b = x[2 * i + 1];
+      const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+      *reinterpret_cast<uint4v*>(S + ((t >> 2) + 128 * i) * LDH + (t & 3) * 8) = pack8(v);
+    }
+  }
+};
+
+// Row-contiguous: row t & 255, K (t >> 8) * 16 .. +15 (the same sixteen K
+// for the whole wave), one 4-byte load per K, so that each wave's load
+// covers 256 contiguous bytes and every loaded value sits in a register of
+// its own (pairs or quads of loaded values that the conversion does not use
+// together would make the compiler move them across the loop, waiting for
+// the loads).  Two 16-byte LDS writes per thread fill the [row][k] tile.
+// K past the end reads zero.  Needs a concatenation split on a tile
+// boundary (a tile on one side of it).
+template <>
+struct DirectStage<false> {
+  float v[16];   // K kc + i of this thread's row
+  const float* p;
+  int64_t ld, kend, kl;
+  unsigned off;   // byte offset of this thread's row
+  int kc;
+  __device__ __forceinline__ void init(const OpView& o, int64_t R, int64_t K, int64_t r0, int t) {
+    const bool first = r0 < o.split;
+    p = first ? o.p0 : o.p1;
+    ld = first ? o.ld0 : o.ld1;
+    const int64_t r = min(r0 + (t & 255), R - 1);
+    off = static_cast<unsigned>((first ? r : r - o.split) * 4);
+    kc = __builtin_amdgcn_readfirstlane((t >> 8) * 16);
+    kend = K;
+  }
+  __device__ __forceinline__ void load(const OpView&, int64_t k0) {
+    kl = k0;
+    // K rows kb .. kb+15, those past the end clamped to the last one: one
+    // 64-bit base per step and a 32-bit step per row, no branch (a branch
+    // here would make the compiler wait for the loads where its paths join)
+    const int64_t kb = k0 + kc;
+    const char* base = reinterpret_cast<const char*>(p + kb * ld);
+    const int last = static_cast<int>(kend - 1 - kb);   // >= -31
+    const int ld4 = static_cast<int>(ld * 4);
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      v[i] = *reinterpret_cast<const float*>(base + min(i, last) * ld4 + off);
+  }
+  // The zeros past K are applied here, where the loaded values are first
+  // used, so that the loads stay in flight until then.
+  __device__ __forceinline__ void store(unsigned short* S, int t) const {
+    unsigned short* d = S + (t & 255) * LDH + (t >> 8) * 16;
+    if (kl + kc + 15 < kend) {
+      *reinterpret_cast<uint4v*>(d) = pack8(&v[0]);
+      *reinterpret_cast<uint4v*>(d + 8) = pack8(&v[8]);
+      return;
+    }
+    float w[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) w[q] = kl + kc + q < kend ? v[q] : 0.f;
+    *reinterpret_cast<uint4v*>(d) = pack8(&w[0]);
+    *reinterpret_cast<uint4v*>(d + 8) = pack8(&w[8]);
+  }
+};
+
+// Padded bf16 copies need no set-up.
+// One work unit (K slice, 256 x 256 tile) of C = A B^T with A staged by SA
+// from OA and B by SB from OB.
+template <class SA, class SB, class OA, class OB, bool SPLIT_OUT>
+__device__ __forceinline__ void gemm_bf16_body(int64_t M, int64_t N, int64_t K, const OA& A,
+                                               const OB& B, const OutView& C, const SchedB& S,
+                                               float* __restrict__ partials) {
   __shared__ __attribute__((aligned(16))) unsigned short lds[2][(TM + TN) * LDH];
   const int t = threadIdx.x;
   const int lane = t & 63, wave = t >> 6;
@@ -161,27 +310,17 @@ __global__ __launch_bounds__(kThr) void gemm_bf16_kernel(int64_t M, int64_t N,
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
-  // loads: 4 threads cover one row's 32 halves (64 B); 128 rows per pass,
-  // two passes for A and two for B
-  ushort8 ra[2], rb[2];
-  const int lrow = t >> 2, lchunk = (t & 3) * 8;
+  SA sa;
+  SB sb;
+  sa.init(A, M, K, m0, t);
+  sb.init(B, N, K, n0, t);
   auto gload = [&](int64_t k) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-      ra[i] = *reinterpret_cast<const ushort8*>(A + (m0 + lrow + 128 * i) * Kp + k + lchunk);
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-      rb[i] = *reinterpret_cast<const ushort8*>(B + (n0 + lrow + 128 * i) * Kp + k + lchunk);
+    sa.load(A, k);
+    sb.load(B, k);
   };
   auto swrite = [&](int buf) {
-    unsigned short* As = lds[buf];
-    unsigned short* Bs = As + TM * LDH;
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-      *reinterpret_cast<ushort8*>(As + (lrow + 128 * i) * LDH + lchunk) = ra[i];
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-      *reinterpret_cast<ushort8*>(Bs + (lrow + 128 * i) * LDH + lchunk) = rb[i];
+    sa.store(lds[buf], t);
+    sb.store(lds[buf] + TM * LDH, t);
   };
   // MFMA fragments of one 16-wide K chunk: A rows wm*128 + a*32 + lane%32,
   // B rows wn*64 + b*32 + lane%32; lane half lh holds K elements 8*lh .. +7.
@@ -209,7 +348,10 @@ __global__ __launch_bounds__(kThr) void gemm_bf16_kernel(int64_t M, int64_t N,
   // Pipeline: step j multiplies LDS buffer (j-kb)&1.  After its first chunk
   // the staging registers (step j+1, loaded during step j-1) go to the other
   // buffer -- last read in step j-1, before the barrier that ended it -- and
-  // after the second chunk the loads of step j+2 are issued.
+  // after the second chunk the loads of step j+2 are issued.  (Reading the
+  // next step's first chunk while the second multiplies needs the barrier
+  // between the two chunks; waves held there leave the matrix cores idle,
+  // and that measured slower.)
   gload(static_cast<int64_t>(kb) * TK);
   swrite(0);
   if (kb + 1 < ke) gload(static_cast<int64_t>(kb + 1) * TK);
@@ -283,6 +425,25 @@ __global__ __launch_bounds__(kThr) void gemm_bf16_kernel(int64_t M, int64_t N,
           part[(wm * 128 + a * 32 + 8 * (r >> 2) + 4 * lh + (r & 3)) * TN + wn * 64 + b * 32 +
                li] = acc[a][b][r];
   }
+}
+
+// Both operands from their padded bf16 copies.
+template <bool SPLIT_OUT>
+__global__ __launch_bounds__(kThr) void gemm_bf16_kernel(int64_t M, int64_t N, int64_t K,
+                                                         PackedOp A, PackedOp B, OutView C,
+                                                         SchedB S, float* __restrict__ partials) {
+  gemm_bf16_body<PackedStage, PackedStage, PackedOp, PackedOp, SPLIT_OUT>(M, N, K, A, B, C, S,
+                                                                          partials);
+}
+
+// Both operands straight from fp32 memory (AK / BK: K contiguous).
+template <bool AK, bool BK, bool SPLIT_OUT>
+__global__ __launch_bounds__(kThr) void gemm_bf16_direct_kernel(int64_t M, int64_t N, int64_t K,
+                                                                OpView A, OpView B, OutView C,
+                                                                SchedB S,
+                                                                float* __restrict__ partials) {
+  gemm_bf16_body<DirectStage<AK>, DirectStage<BK>, OpView, OpView, SPLIT_OUT>(M, N, K, A, B, C,
+                                                                              S, partials);
 }
 
 // Sum the K slices' partials of one tile in slice order.  One block per
@@ -381,10 +542,39 @@ gist_status convert(hipStream_t st, const Operand& o, int64_t R, int64_t K, int6
   return check_launch("bf16 conversion");
 }
 
+// The direct kernel's operand requirements (DirectStage), plus 32-bit byte
+// offsets for every row it reads.
+bool direct_ok(const Operand& o, int64_t R, int64_t K) {
+  auto al = [](const float* p, unsigned a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; };
+  const int64_t lim = int64_t(1) << 30;   // floats addressable by a 32-bit byte offset
+  if (o.k_major) {
+    if (K % TK || o.ld0 % 4 || !al(o.p0, 16) || R * o.ld0 >= lim) return false;
+    return !o.p1 || (o.ld1 % 4 == 0 && al(o.p1, 16) && o.split % TK == 0 && R * o.ld1 < lim);
+  }
+  // (and K-row steps of +-31 leading dimensions within a 32-bit byte offset)
+  const int64_t ldlim = int64_t(1) << 24;
+  if (R >= lim || o.ld0 >= ldlim) return false;
+  return !o.p1 || (o.ld1 < ldlim && o.split % TM == 0);
+}
+
+template <bool SPLIT_OUT>
+void launch_direct(hipStream_t st, dim3 g, int64_t M, int64_t N, int64_t K, const Operand& A,
+                   const Operand& B, const OutView& c, const SchedB& S, float* part) {
+  const OpView a = OpView::from(A), b = OpView::from(B);
+#define GIST_BF16_DIRECT(AK_, BK_)                                                        \
+  hipLaunchKernelGGL((gemm_bf16_direct_kernel<AK_, BK_, SPLIT_OUT>), g, dim3(kThr), 0, st, M, \
+                     N, K, a, b, c, S, part)
+  if (A.k_major && B.k_major) GIST_BF16_DIRECT(true, true);
+  else if (A.k_major) GIST_BF16_DIRECT(true, false);
+  else if (B.k_major) GIST_BF16_DIRECT(false, true);
+  else GIST_BF16_DIRECT(false, false);
+#undef GIST_BF16_DIRECT
+}
+
 }  // namespace
 
 bool gemm_bf16_packed_eligible(int64_t M, int64_t N, int64_t K) {
-  // big enough that the conversion pass pays for itself
+  // big enough for 256 x 256 tiles to pay
   return M >= 512 && N >= 512 && K >= 256;
 }
 
@@ -403,24 +593,38 @@ gist_status gemm_bf16_packed(hipStream_t st, int64_t M, int64_t N, int64_t K, co
   auto* a16 = reinterpret_cast<unsigned short*>(base);
   auto* b16 = reinterpret_cast<unsigned short*>(base + L.a_bytes);
   float* part = reinterpret_cast<float*>(base + L.a_bytes + L.b_bytes);
-  gist_status s = convert(st, A, M, K, L.Mp, L.Kp, a16);
-  if (s != GIST_OK) return s;
-  s = convert(st, B, N, K, L.Np, L.Kp, b16);
-  if (s != GIST_OK) return s;
   OutView c = OutView::from(Cout);
   const bool split_out = Cout.c1 != nullptr;
-  {
-    ProfScope ps(st, "gemm_bf16_packed", 2.0 * static_cast<double>(M) * N * K,
+  const dim3 g(static_cast<unsigned>(units));
+  const double flops = 2.0 * static_cast<double>(M) * N * K;
+  if (direct_ok(A, M, K) && direct_ok(B, N, K)) {
+    // operands rounded while staged: no conversion pass, no bf16 copies
+    // variant name: the K-contiguous (K) / row-contiguous (R) orientation of
+    // A and B as read from memory
+    static const char* const kNames[4] = {"gemm_bf16_direct_RR", "gemm_bf16_direct_RK",
+                                          "gemm_bf16_direct_KR", "gemm_bf16_direct_KK"};
+    ProfScope ps(st, kNames[(A.k_major ? 2 : 0) + (B.k_major ? 1 : 0)], flops,
+                 4.0 * (static_cast<double>(M) * K + static_cast<double>(N) * K) +
+                     4.0 * static_cast<double>(M) * N);
+    if (split_out) launch_direct<true>(st, g, M, N, K, A, B, c, L.S, part);
+    else launch_direct<false>(st, g, M, N, K, A, B, c, L.S, part);
+  } else {
+    gist_status s = convert(st, A, M, K, L.Mp, L.Kp, a16);
+    if (s != GIST_OK) return s;
+    s = convert(st, B, N, K, L.Np, L.Kp, b16);
+    if (s != GIST_OK) return s;
+    const PackedOp pa{a16, L.Kp}, pb{b16, L.Kp};
+    ProfScope ps(st, "gemm_bf16_packed", flops,
                  2.0 * (static_cast<double>(M) * K + static_cast<double>(N) * K) +
                      4.0 * static_cast<double>(M) * N);
     if (split_out)
-      hipLaunchKernelGGL(gemm_bf16_kernel<true>, dim3(static_cast<unsigned>(units)), dim3(kThr), 0,
-                         st, M, N, a16, b16, L.Kp, c, L.S, part);
+      hipLaunchKernelGGL(gemm_bf16_kernel<true>, g, dim3(kThr), 0, st, M, N, K, pa, pb, c, L.S,
+                         part);
     else
-      hipLaunchKernelGGL(gemm_bf16_kernel<false>, dim3(static_cast<unsigned>(units)), dim3(kThr),
-                         0, st, M, N, a16, b16, L.Kp, c, L.S, part);
+      hipLaunchKernelGGL(gemm_bf16_kernel<false>, g, dim3(kThr), 0, st, M, N, K, pa, pb, c, L.S,
+                         part);
   }
-  s = check_launch("gemm bf16");
+  gist_status s = check_launch("gemm bf16");
   if (s != GIST_OK) return s;
   if (L.S.split > 1) {
     ProfScope ps(st, "gemm_bf16_fixup", 0.0,

@@ -36,6 +36,15 @@ struct OpView {
     else p = r < split ? p0 + k * ld0 + r : p1 + k * ld1 + (r - split);
     return *reinterpret_cast<const float4*>(p);
   }
+  // Two consecutive elements along the contiguous dimension (8-byte aligned,
+  // not straddling `split`).
+  template <bool KMAJ>
+  __device__ __forceinline__ float2 at2(int64_t r, int64_t k) const {
+    const float* p;
+    if constexpr (KMAJ) p = k < split ? p0 + r * ld0 + k : p1 + r * ld1 + (k - split);
+    else p = r < split ? p0 + k * ld0 + r : p1 + k * ld1 + (r - split);
+    return *reinterpret_cast<const float2*>(p);
+  }
 };
 
 // Device view of a GemmOut: optional ReLU, columns >= c_split go to c1,

@@ -152,6 +152,51 @@ def test_layer_bf16_inputs(G, ctx, case):
         assert e <= BF16_TOL, (k, e)
 
 
+def test_bf16_direct_and_packed_staging_bitwise(G, ctx):
+    """The bf16 product kernel stages operands straight from fp32 memory when
+    the 16-byte loads allow it, else from a rounded bf16 copy made by a
+    conversion pass; both put the same bf16 values in the same tiles.  A
+    transform-first GCN layer reads H as the forward product's K-contiguous
+    operand: H 16-byte aligned takes the direct staging, the same values at
+    a 4-byte offset take the conversion pass.  Forward and backward outputs
+    agree bit for bit (the backward's K = n products take the direct path in
+    both runs, with a ragged last K step: n = 2000 = 62 * 32 + 16)."""
+    import torch
+    g = GRAPHS["cl2000"]
+    csr = MB.build(g, None, "gcn")
+    n, s_in, s_out = csr["n"], 512, 768
+    rng = np.random.default_rng(11)
+    H = rng.standard_normal((n, s_in)).astype(np.float32)
+    W = (rng.standard_normal((s_in, s_out)) / np.sqrt(s_in)).astype(np.float32)
+    dHo = rng.standard_normal((n, s_out)).astype(np.float32)
+    A, keep = csr_to_dev(csr)
+    desc = G.layer_desc(G.GIST_LAYER_GCN, G.GIST_ACT_RELU, n, s_in, s_out,
+                        G.GIST_DTYPE_BF16_IN, G.GIST_ORDER_XFORM_FIRST)
+    fws, bws = G.gist_layer_workspace_size(desc)
+    ws = torch.empty(max(fws, bws, 1), dtype=torch.uint8, device="cuda")
+    Wd, dHod = to_dev(W), to_dev(dHo)
+    aligned = to_dev(H)
+    buf = torch.empty(n * s_in + 1, device="cuda")
+    shifted = buf[1:].view(n, s_in)
+    shifted.copy_(aligned)
+    assert aligned.data_ptr() % 16 == 0 and shifted.data_ptr() % 16 == 4
+    outs = []
+    for Hd in (aligned, shifted):
+        agg = torch.empty(n, s_in, device="cuda")
+        Ho = torch.empty(n, s_out, device="cuda")
+        G.gist_gcn_layer_fwd(ctx, desc, A, Hd, Wd, agg, Ho, ws)
+        dW = torch.empty(s_in, s_out, device="cuda")
+        dH = torch.empty(n, s_in, device="cuda")
+        G.gist_gcn_layer_bwd(ctx, desc, A, None, Hd, agg, Ho, Wd, dHod, dW, dH, ws)
+        outs.append([to_host(Ho), to_host(dW), to_host(dH)])
+    for a, b in zip(*outs):
+        assert a.tobytes() == b.tobytes()
+    f = OL.gcn_forward(csr, H.astype(np.float64), W.astype(np.float64), True)
+    e = relerr(outs[0][0], f["H_out"])
+    log(f"direct and packed staging bitwise; H_out vs oracle {e:.3e}")
+    assert e <= BF16_TOL
+
+
 def test_layer_zero_batch_no_dH(G, ctx):
     import torch
     desc = G.layer_desc(G.GIST_LAYER_GCN, G.GIST_ACT_RELU, 0, 8, 4)
