@@ -5,9 +5,10 @@
 //   1. The product kernel: eight waves (two per SIMD, so one wave's MFMAs
 //      run while the other waits on memory), each owning 128 rows x 64
 //      columns (4 x 2 MFMA tiles of 32 x 32, v_mfma_f32_32x32x16_bf16), K
-//      steps of 32, double-buffered LDS tiles [row][k] with 80-byte rows
-//      (conflict-free 16-byte fragment reads), the next step's operands
-//      loaded into registers while the current one multiplies.
+//      steps of 32, three LDS tile buffers [row][k] with 64-byte rows
+//      whose 16-byte chunks are XOR-swizzled so that neither the staging
+//      writes nor the fragment reads meet bank conflicts, the next step's
+//      operands loaded into registers while the current one multiplies.
 //   2. Direct staging (the usual path): each step's operand tiles are read
 //      straight from the fp32 operands and rounded in registers on their way
 //      to LDS -- K-contiguous operands with 16-byte loads, row-contiguous
@@ -47,7 +48,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef unsigned short ushort8 __attribute__((ext_vector_type(8)));
 
 constexpr int TM = 256, TN = 256, TK = 32;
-constexpr int LDH = TK + 8;          // LDS row stride in halves (80 B)
+constexpr int LDH = TK;              // LDS row stride in halves (64 B, swizzled)
 constexpr int kThr = 512;            // 8 waves: 2 along M x 4 along N
 constexpr int kCUs = 256;            // MI355X compute units (one workgroup each)
 constexpr int kMaxSplit = 8;
@@ -153,11 +154,29 @@ __device__ __forceinline__ uint4v pack8(const float* v) {
   return u;
 }
 
+// LDS tiles [row][k]: 64-byte rows of four 16-byte chunks (8 K each), chunk
+// q of row r stored at position q ^ ((r ^ (r >> 2)) & 3).  With this
+// swizzle the three access patterns -- staging writes with four lanes per
+// row (chunks 0..3 of 16 rows), staging writes with one row per lane (64
+// rows, one chunk) and MFMA fragment reads (32 rows, one chunk) -- each put
+// every group of lanes the LDS serves together on distinct banks, whether
+// it serves 8 lanes of 16 bytes over 32 banks or 16 lanes over 64.  (Padded
+// 80-byte rows left the four-lanes-per-row writes with bank conflicts.)
+__device__ __forceinline__ int lds_at(int row, int q) {
+  return row * LDH + 8 * (q ^ ((row ^ (row >> 2)) & 3));
+}
+
+// Lane map of K-contiguous staging: rows (t >> 2) + 128 i, chunk t & 3.  Four
+// consecutive lanes read one row's 64 contiguous bytes (bf16) or 128 (fp32),
+// which the load unit merges into whole cache lines.
+__device__ __forceinline__ int kstage_row(int t) { return t >> 2; }
+__device__ __forceinline__ int kstage_q(int t) { return t & 3; }
+
 // Staging of one operand's 256 x 32 tile per K step: `load` fetches this
 // thread's share from memory into registers, `store` writes it to the LDS
-// tile [row][k] (row stride LDH halves) as bf16.
+// tile [row][k] (the lds_at layout) as bf16.
 
-// From a padded bf16 copy [Rp][Kp]: rows (t >> 2) + 128 i, K (t & 3) * 8 .. +7.
+// From a padded bf16 copy [Rp][Kp]: rows kstage_row(t) + 128 i, K chunk kstage_q(t).
 struct PackedOp {
   const unsigned short* p;
   int64_t Kp;
@@ -166,7 +185,7 @@ struct PackedStage {
   ushort8 r[2];
   const unsigned short* row;   // this thread's first row, at its K offset
   __device__ __forceinline__ void init(const PackedOp& o, int64_t, int64_t, int64_t r0, int t) {
-    row = o.p + (r0 + (t >> 2)) * o.Kp + (t & 3) * 8;
+    row = o.p + (r0 + kstage_row(t)) * o.Kp + 8 * kstage_q(t);
   }
   __device__ __forceinline__ void load(const PackedOp& o, int64_t k0) {
 #pragma unroll
@@ -176,7 +195,7 @@ struct PackedStage {
   __device__ __forceinline__ void store(unsigned short* S, int t) const {
 #pragma unroll
     for (int i = 0; i < 2; ++i)
-      *reinterpret_cast<ushort8*>(S + ((t >> 2) + 128 * i) * LDH + (t & 3) * 8) = r[i];
+      *reinterpret_cast<ushort8*>(S + lds_at(kstage_row(t) + 128 * i, kstage_q(t))) = r[i];
   }
 };
 
@@ -189,8 +208,8 @@ struct PackedStage {
 template <bool KMAJ>
 struct DirectStage;
 
-// K contiguous: rows (t >> 2) + 128 i, K (t & 3) * 8 .. +7 (two 16-byte
-// loads per row).  Needs K and the concatenation split to be multiples of
+// K contiguous: rows kstage_row(t) + 128 i, K chunk kstage_q(t) (two
+// 16-byte loads per row).  Needs K and the concatenation split to be multiples of
 // the K step (every step full and on one side of the split), leading
 // dimensions that are multiples of 4 floats and 16-byte bases.
 template <>
@@ -198,10 +217,10 @@ struct DirectStage<true> {
   float4 x[4];                 // row i: x[2i], x[2i+1] (K kc .. kc+7)
   unsigned off0[2], off1[2];   // byte offsets of this thread's rows in p0 / p1
   __device__ __forceinline__ void init(const OpView& o, int64_t R, int64_t, int64_t r0, int t) {
-    const int kc = (t & 3) * 8;
+    const int kc = 8 * kstage_q(t);
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const int64_t r = min(r0 + (t >> 2) + 128 * i, R - 1);
+      const int64_t r = min(r0 + kstage_row(t) + 128 * i, R - 1);
       off0[i] = static_cast<unsigned>((r * o.ld0 + kc) * 4);
       off1[i] = static_cast<unsigned>((r * o.ld1 + kc) * 4);
     }
@@ -221,7 +240,7 @@ struct DirectStage<true> {
     for (int i = 0; i < 2; ++i) {
       const float4 a = x[2 * i], b = x[2 * i + 1];
       const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-      *reinterpret_cast<uint4v*>(S + ((t >> 2) + 128 * i) * LDH + (t & 3) * 8) = pack8(v);
+      *reinterpret_cast<uint4v*>(S + lds_at(kstage_row(t) + 128 * i, kstage_q(t))) = pack8(v);
     }
   }
 };
@@ -266,17 +285,19 @@ struct DirectStage<false> {
   // The zeros past K are applied here, where the loaded values are first
   // used, so that the loads stay in flight until then.
   __device__ __forceinline__ void store(unsigned short* S, int t) const {
-    unsigned short* d = S + (t & 255) * LDH + (t >> 8) * 16;
+    const int r = t & 255, q = (t >> 8) * 2;
+    uint4v* d0 = reinterpret_cast<uint4v*>(S + lds_at(r, q));
+    uint4v* d1 = reinterpret_cast<uint4v*>(S + lds_at(r, q + 1));
     if (kl + kc + 15 < kend) {
-      *reinterpret_cast<uint4v*>(d) = pack8(&v[0]);
-      *reinterpret_cast<uint4v*>(d + 8) = pack8(&v[8]);
+      *d0 = pack8(&v[0]);
+      *d1 = pack8(&v[8]);
       return;
     }
     float w[16];
 #pragma unroll
-    for (int q = 0; q < 16; ++q) w[q] = kl + kc + q < kend ? v[q] : 0.f;
-    *reinterpret_cast<uint4v*>(d) = pack8(&w[0]);
-    *reinterpret_cast<uint4v*>(d + 8) = pack8(&w[8]);
+    for (int i = 0; i < 16; ++i) w[i] = kl + kc + i < kend ? v[i] : 0.f;
+    *d0 = pack8(&w[0]);
+    *d1 = pack8(&w[8]);
   }
 };
 
@@ -287,7 +308,7 @@ template <class SA, class SB, class OA, class OB, bool SPLIT_OUT>
 __device__ __forceinline__ void gemm_bf16_body(int64_t M, int64_t N, int64_t K, const OA& A,
                                                const OB& B, const OutView& C, const SchedB& S,
                                                float* __restrict__ partials) {
-  __shared__ __attribute__((aligned(16))) unsigned short lds[2][(TM + TN) * LDH];
+  __shared__ __attribute__((aligned(16))) unsigned short lds[3][(TM + TN) * LDH];
   const int t = threadIdx.x;
   const int lane = t & 63, wave = t >> 6;
   const int li = lane & 31, lh = lane >> 5;
@@ -330,12 +351,10 @@ __device__ __forceinline__ void gemm_bf16_body(int64_t M, int64_t N, int64_t K, 
     const unsigned short* Bs = As + TM * LDH;
 #pragma unroll
     for (int a = 0; a < 4; ++a)
-      f.a[a] = *reinterpret_cast<const bf16x8*>(As + (wm * 128 + a * 32 + li) * LDH + 16 * c +
-                                                8 * lh);
+      f.a[a] = *reinterpret_cast<const bf16x8*>(As + lds_at(wm * 128 + a * 32 + li, 2 * c + lh));
 #pragma unroll
     for (int b = 0; b < 2; ++b)
-      f.b[b] = *reinterpret_cast<const bf16x8*>(Bs + (wn * 64 + b * 32 + li) * LDH + 16 * c +
-                                                8 * lh);
+      f.b[b] = *reinterpret_cast<const bf16x8*>(Bs + lds_at(wn * 64 + b * 32 + li, 2 * c + lh));
   };
   auto mfma8 = [&](const Frag& f) {
 #pragma unroll
@@ -345,31 +364,59 @@ __device__ __forceinline__ void gemm_bf16_body(int64_t M, int64_t N, int64_t K, 
         acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[a], f.b[b], acc[a][b], 0, 0, 0);
   };
 
-  // Pipeline: step j multiplies LDS buffer (j-kb)&1.  After its first chunk
-  // the staging registers (step j+1, loaded during step j-1) go to the other
-  // buffer -- last read in step j-1, before the barrier that ended it -- and
-  // after the second chunk the loads of step j+2 are issued.  (Reading the
-  // next step's first chunk while the second multiplies needs the barrier
-  // between the two chunks; waves held there leave the matrix cores idle,
-  // and that measured slower.)
+  // Pipeline over three LDS buffers (32 KB each), step j in buffer
+  // (j - kb) % 3, written two steps ahead:
+  //   - chunk 0's fragments of step j were read during step j-1; chunk 1's
+  //     are read while chunk 0 multiplies;
+  //   - then step j+2's staging registers (loaded during step j-1) go to the
+  //     buffer step j-1 used -- whose reads all completed before the barrier
+  //     that ended step j-1 -- and are reloaded at once with step j+3, a
+  //     whole step before they are needed again;
+  //   - chunk 0 of step j+1 is read from its buffer, whole since that same
+  //     barrier, while chunk 1 multiplies; the barrier ends the step.
+  // So no wave waits for fragments after a barrier, and the barrier sits
+  // after both chunks.
   gload(static_cast<int64_t>(kb) * TK);
   swrite(0);
-  if (kb + 1 < ke) gload(static_cast<int64_t>(kb + 1) * TK);
+  if (kb + 1 < ke) {
+    gload(static_cast<int64_t>(kb + 1) * TK);
+    swrite(1);
+  }
+  if (kb + 2 < ke) gload(static_cast<int64_t>(kb + 2) * TK);
   __syncthreads();
+  Frag f0, f1;
+  rfrag(0, 0, f0);
+  int cur = 0;
   for (int j = kb; j < ke; ++j) {
-    const int buf = (j - kb) & 1;
-    Frag f0, f1;
-    rfrag(buf, 0, f0);
-    rfrag(buf, 1, f1);
+    const int nxt = cur == 2 ? 0 : cur + 1;
+    const int prev = nxt == 2 ? 0 : nxt + 1;   // the buffer step j-1 used
+    rfrag(cur, 1, f1);
     __builtin_amdgcn_sched_barrier(0);
+    // chunk 0's MFMAs interleaved with the staging work (conversion, LDS
+    // writes, next loads, next fragment reads): the two waves of a SIMD
+    // reach this phase together, so staging work left between the chunks
+    // would leave the matrix core idle
     mfma8(f0);
-    __builtin_amdgcn_sched_barrier(0);
-    if (j + 1 < ke) swrite(buf ^ 1);
+    // unconditional: on the last two steps these write a buffer no later
+    // step reads and read one whose fragments go unused, and a branch here
+    // would leave the LDS counter unknown where the paths join, so that the
+    // compiler would wait for these reads before chunk 1
+    swrite(prev);
+    if (j + 3 < ke) gload(static_cast<int64_t>(j + 3) * TK);
+    rfrag(nxt, 0, f0);
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);   // up to six VALU
+      __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);   // an LDS write
+      __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);   // up to four loads
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // an LDS read
+    }
     __builtin_amdgcn_sched_barrier(0);
     mfma8(f1);
     __builtin_amdgcn_sched_barrier(0);
-    if (j + 2 < ke) gload(static_cast<int64_t>(j + 2) * TK);
     lds_barrier();
+    cur = nxt;
   }
 
   // acc[a][b] register r of lane l: tile row wm*128 + a*32 + 8(r/4) +
