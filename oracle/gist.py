@@ -263,22 +263,33 @@ def adam_params(kind, params, grads, M, V, step, lr):
     return P, M1, V1
 
 
-def sub_gcn_step_adam(kind, csr, X, labels, params, M, V, step, lr):
-    """``subTrain`` with Adam: forward, loss, backward, one Adam step."""
+def sub_gcn_step_adam(kind, csr, X, labels, params, M, V, step, lr, grad_noise=None):
+    """``subTrain`` with Adam: forward, loss, backward, one Adam step.
+
+    ``grad_noise`` (test use only, default none): a function applied to
+    every gradient array before the Adam step.  A run with a small seeded
+    perturbation beside the plain run shows how strongly each element of
+    the trained weights depends on its gradients' rounding -- Adam divides
+    by the root of the second moment, so elements with small or cancelling
+    gradients move by amounts far more sensitive than the gradients
+    themselves."""
     H, recs = forward(kind, csr, X, params)
     loss, dlogits = _l.softmax_xent(H[-1], labels)
     grads, _ = backward(kind, csr, H, recs, params, dlogits)
+    if grad_noise is not None:
+        grads = [_pack(kind, (grad_noise(x) for x in _parts(kind, g))) for g in grads]
     P, M1, V1 = adam_params(kind, params, grads, M, V, step, lr)
     return dict(loss=loss, grads=grads, params=P, M=M1, V=V1)
 
 
-def gist_train(kind, theta, rounds, zeta, lr, partitions, batches, policy="carry"):
+def gist_train(kind, theta, rounds, zeta, lr, partitions, batches, policy="carry",
+               grad_noise=None):
     """Algorithm 1 with Adam, sub-GCNs back to back on one device.
 
     ``partitions(t)`` -> the round's partitions (as for ``slice_indices``);
     ``batches(t, i, z)`` -> (csr, X, labels) of sub-GCN i's local step z.
     Returns (theta, M, V, losses[t][i][z]); M, V are the global moments
-    ("carry") or None ("reset").
+    ("carry") or None ("reset").  ``grad_noise``: see ``sub_gcn_step_adam``.
     """
     if policy not in ("carry", "reset"):
         raise ValueError("policy is 'carry' or 'reset'")
@@ -302,7 +313,7 @@ def gist_train(kind, theta, rounds, zeta, lr, partitions, batches, policy="carry
             for z in range(zeta):
                 csr, X, y = batches(t, i, z)
                 k = (t * zeta + z + 1) if policy == "carry" else (z + 1)
-                st = sub_gcn_step_adam(kind, csr, X, y, p, mm, vv, k, lr)
+                st = sub_gcn_step_adam(kind, csr, X, y, p, mm, vv, k, lr, grad_noise)
                 p, mm, vv = st["params"], st["M"], st["V"]
                 li.append(st["loss"])
             trained.append((sl, p, mm, vv))

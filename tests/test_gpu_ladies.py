@@ -26,7 +26,8 @@ from oracle import layers as OL
 from oracle import minibatch as MB
 from oracle import partition as OP
 
-from gpu_util import BF16_TOL, FP32_TOL, csr_to_dev, gpu_orders, log, relerr, to_dev, to_host
+from gpu_util import (BF16_TOL, FP32_TOL, adam_noise, check_adam, csr_to_dev, gpu_orders, log,
+                      relerr, to_dev, to_host)
 
 pytestmark = pytest.mark.gpu
 
@@ -299,10 +300,12 @@ def test_ladies_step_matches_oracle(G, ctx, widths, b, s, dtype):
 @pytest.mark.parametrize("policy,size", [("carry", "small"), ("reset", "small"),
                                          ("sgd", "reddit")])
 def test_gist_train_on_ladies_batches(G, ctx, policy, size):
-    """Adam at small sizes; SGD at the full workload's sizes, where Adam's
-    first steps (nearly lr sign(g)) would move any of the 150k weights whose
-    gradient lies within rounding of zero by up to 2 lr on one side only, so
-    an element-wise bound would test the inputs' conditioning, not the path."""
+    """Adam at small sizes, its weight changes held element by element to
+    the oracle's own sensitivity (``check_adam``: 1e-4 where rounding noise
+    in the oracle's gradients does not move them); SGD at the full
+    workload's sizes, where a few ReLU decisions within rounding of zero
+    differ between the two sides (noise on the gradients does not model
+    those, so the weight change is held normwise to 1e-3 there)."""
     import torch
     from paper_2102_10424_amd.step import GistModel, LadiesSlot, SubGCN, gist_train
     if size == "reddit":     # the workload's sizes: 512 outputs, 512 draws, 602-256-41, m = 4
@@ -334,15 +337,25 @@ def test_gist_train_on_ladies_batches(G, ctx, policy, size):
                                         lambda i, z: w.oracle_batch(key(t, i, z)), lr, zeta)
             lo.append(lt)
     else:
-        th_o, _, _, lo = OG.gist_train("gcn", [t for t in w.theta], rounds, zeta, lr, parts,
-                                       lambda t, i, z: w.oracle_batch(key(t, i, z)),
-                                       policy=policy)
+        train = lambda noise: OG.gist_train("gcn", [t for t in w.theta], rounds, zeta, lr,
+                                            parts, lambda t, i, z: w.oracle_batch(key(t, i, z)),
+                                            policy=policy, grad_noise=noise)
+        th_o, _, _, lo = train(None)
+        pert = [train(adam_noise(3e-6, s))[0] for s in (1, 2, 3)]
     for l in range(L):
         got = to_host(model.theta[l][0])
         e = relerr(got, th_o[l])
-        d = relerr(got.astype(np.float64) - w.theta[l], th_o[l] - w.theta[l])
-        log(f"  layer {l}: theta {e:.2e}, change {d:.2e}")
-        assert e <= FP32_TOL and d <= 1e-3
+        if policy == "sgd":
+            # a few ReLU decisions within rounding of zero may differ at this size
+            d = relerr(got.astype(np.float64) - w.theta[l], th_o[l] - w.theta[l])
+            log(f"  layer {l}: theta {e:.2e}, change {d:.2e}")
+            assert e <= FP32_TOL and d <= 1e-3
+        else:
+            d = check_adam(got.astype(np.float64) - w.theta[l], th_o[l] - w.theta[l],
+                           [q[l] - w.theta[l] for q in pert])
+            log(f"  layer {l}: theta {e:.2e}; change: {d[0]:.2e} on the {100 * d[1]:.0f}% "
+                f"well-conditioned entries, worst {d[2]:.2f} of the bound")
+            assert e <= FP32_TOL and d[0] <= FP32_TOL and d[2] <= 1.0
     want_l = np.array([[li for li in lt] for lt in lo])
     assert np.max(np.abs(losses - want_l) / np.abs(want_l)) <= FP32_TOL
 

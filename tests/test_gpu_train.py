@@ -8,7 +8,11 @@ optimizer of the paper's experiments), through the C ABI.
 * gist_train (T rounds x m sub-GCNs x zeta local steps, fused subAgg/gather,
   moments carried with the weights or reset per round) against
   oracle.gist.gist_train on the same seeded inputs: Theta within 1e-4
-  normwise, its change over training within 1e-3, every loss within 1e-4.
+  normwise, every loss within 1e-4; the change of Theta over training and
+  the carried first moments element by element against the oracle's own
+  sensitivity (tests/gpu_util.check_adam: 1e-4 on the entries that rounding
+  noise in the oracle's gradients does not move, a multiple of that
+  movement on the rest).
 * m = 1: the loop equals plain Adam training of the full model on the GPU,
   bit for bit (Section 2.1: one sub-GCN is the whole GCN).
 * GAT models in the same loop (the output layer's attention vectors, which
@@ -25,7 +29,7 @@ from oracle import minibatch as OM
 from oracle import optim as OO
 from oracle import partition as OP
 
-from gpu_util import FP32_TOL, log, relerr, to_dev, to_host
+from gpu_util import FP32_TOL, adam_noise, check_adam, log, relerr, to_dev, to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -181,18 +185,28 @@ def test_gist_train_matches_oracle(G, ctx, kind, policy):
         return csr, X[nm], y[nm]
 
     parts = lambda t: [None] + [OP.partition(widths[l], m, seeds(t)[l]) for l in range(1, L)] + [None]
-    th_o, Mo, Vo, lo = OG.gist_train(kind, _oracle_theta(kind, theta), rounds, zeta, lr, parts,
-                                     batches, policy=policy)
+    train = lambda noise: OG.gist_train(kind, _oracle_theta(kind, theta), rounds, zeta, lr,
+                                        parts, batches, policy=policy, grad_noise=noise)
+    th_o, Mo, Vo, lo = train(None)
+    # the oracle again with rounding-sized noise on its gradients: how far each
+    # trained value moves for reasons the path cannot control
+    pert = [train(adam_noise(3e-6, s)) for s in (1, 2, 3)]
     for l in range(L):
         for p in range(model.parts):
             want = _oracle_part(kind, th_o[l], p)
             got = to_host(model.theta[l][p])
             e = relerr(got, want)
-            d = relerr(got.astype(np.float64) - theta[l][p], want - theta[l][p])
-            log(f"  layer {l} part {p}: theta {e:.2e}, change {d:.2e}")
-            assert e <= FP32_TOL and d <= 1e-3
+            d = check_adam(got.astype(np.float64) - theta[l][p], want - theta[l][p],
+                           [_oracle_part(kind, q[0][l], p) - theta[l][p] for q in pert])
+            msg = f"  layer {l} part {p}: theta {e:.2e}; change: {d[0]:.2e} on the " \
+                  f"{100 * d[1]:.0f}% well-conditioned entries, worst {d[2]:.2f} of the bound"
             if policy == "carry":
-                assert relerr(to_host(model.Mg[l][p]), _oracle_part(kind, Mo[l], p)) <= 1e-3
+                mo = check_adam(to_host(model.Mg[l][p]), _oracle_part(kind, Mo[l], p),
+                                [_oracle_part(kind, q[1][l], p) for q in pert])
+                msg += f"; first moment {mo[0]:.2e} ({100 * mo[1]:.0f}%), {mo[2]:.2f}"
+                assert mo[0] <= FP32_TOL and mo[2] <= 1.0
+            log(msg)
+            assert e <= FP32_TOL and d[0] <= FP32_TOL and d[2] <= 1.0
     want_l = np.array([[li for li in lt] for lt in lo])
     assert np.max(np.abs(losses - want_l) / np.abs(want_l)) <= FP32_TOL
     if kind != "gat":     # four Adam steps on changing batches need not lower a GAT's loss

@@ -184,3 +184,49 @@ def test_sgd_matches_torch():
         assert np.max(np.abs(W - p.detach().numpy())) <= 1e-12 * np.max(np.abs(W))
         # one step moves by exactly lr g: sign and size
         assert np.allclose(W0 - Lr.sgd(W0, grads[0], lr), lr * grads[0], rtol=0, atol=1e-15)
+
+
+def test_grad_noise_hook_and_the_sensitivity_check():
+    """``gist_train(grad_noise=...)`` leaves the run unchanged when absent and
+    perturbs it when present; the element-wise Adam check the GPU training
+    tests use (``tests/gpu_util.check_adam``) passes a run whose gradients
+    carry rounding-sized noise and fails runs with a planted mistake: a step
+    size off by 1%, or one element's update lost."""
+    import sys
+    import os
+    sys.path.insert(0, os.path.dirname(__file__))
+    from gpu_util import adam_noise, check_adam
+    g = erdos_renyi(300, 900, 5)
+    csr = MB.build(g, None, "gcn")
+    rng = np.random.default_rng(11)
+    widths, m = [24, 32, 16, 5], 2
+    X = rng.standard_normal((g.n, widths[0]))
+    y = rng.integers(0, widths[-1], g.n)
+    theta = [rng.standard_normal((widths[l], widths[l + 1])) * 0.3 for l in range(3)]
+    parts = lambda t: [None] + [P.partition(widths[l], m, 77 + 10 * t + l)
+                                for l in (1, 2)] + [None]
+    train = lambda noise, lr=0.01: G.gist_train("gcn", theta, 2, 2, lr, parts,
+                                                lambda t, i, z: (csr, X, y), policy="reset",
+                                                grad_noise=noise)[0]
+    base = train(None)
+    assert all(np.array_equal(a, b) for a, b in zip(base, train(None)))
+    pert = [train(adam_noise(3e-6, s)) for s in (1, 2, 3)]
+    assert any(not np.array_equal(a, b) for a, b in zip(base, pert[0]))
+    change = lambda run: [run[l] - theta[l] for l in range(3)]
+    want, ps = change(base), [change(q) for q in pert]
+    # rounding-sized noise in the gradients: within the bound everywhere
+    for l, got in enumerate(change(train(adam_noise(1e-6, 99)))):
+        e_good, frac, ratio = check_adam(got, want[l], [q[l] for q in ps])
+        assert e_good <= 1e-4 and ratio <= 1.0 and frac > 0.5
+    # a 1% larger step size
+    assert any(check_adam(got, want[l], [q[l] for q in ps])[2] > 1.0
+               for l, got in enumerate(change(train(None, lr=0.0101))))
+    # one well-conditioned element's update lost
+    l = 1
+    e = np.max([np.abs(q[l] - want[l]) for q in ps], axis=0)
+    i = np.unravel_index(np.argmax(np.abs(want[l]) * (e <= 1e-5 * np.abs(want[l]).max())),
+                         want[l].shape)
+    got = want[l].copy()
+    got[i] = 0.0
+    e_good, _, ratio = check_adam(got, want[l], [q[l] for q in ps])
+    assert e_good > 1e-4 and ratio > 1.0
