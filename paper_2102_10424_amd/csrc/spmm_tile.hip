@@ -69,11 +69,9 @@ constexpr int kBatch = 16;         // outside-window entries gathered at once
 // pipelined load that falls outside the window or the matrix reads here, so
 // no load depends on a branch.  Not const, so that the compiler cannot fold
 // such a load away and put the real one behind a branch again.
-__device__ float kZeroRow[64];
-__device__ int kZeroIdx[64];
+__device__ float kZeroRow[16];
 
 typedef __attribute__((address_space(1))) const float gfloat;   // global memory
-typedef __attribute__((address_space(1))) const int gint;
 
 __device__ __forceinline__ unsigned short bf16_bits(float f) {
   return __builtin_bit_cast(unsigned short, static_cast<__bf16>(f));
@@ -141,15 +139,12 @@ __global__ __launch_bounds__(256) void spmm_tile_kernel(
   const bool fit = rp[8] - rp[0] <= 64 * kChunk;
   int cc[kChunk];
   float vv[kChunk];
-  // every load unconditional (lanes past the wave's entries read zeros, and
-  // each use checks e < rp[8]), so that all of them are in flight together
   auto load_chunks = [&](int base) {
 #pragma unroll
     for (int u = 0; u < kChunk; ++u) {
       const int e = base + 64 * u + lane;
-      const bool in = e < rp[8];
-      cc[u] = *(gint*)(in ? col + e : kZeroIdx + lane);
-      vv[u] = *(gfloat*)(in ? val + e : kZeroRow + lane);
+      cc[u] = e < rp[8] ? col[e] : INT_MIN / 2;
+      vv[u] = e < rp[8] ? val[e] : 0.f;
     }
   };
   if (fit) load_chunks(rp[0]);
@@ -211,8 +206,8 @@ __global__ __launch_bounds__(256) void spmm_tile_kernel(
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const bool in = j < nk && j * kKs + i < rows_left;
-      dst[0][i] = *(gfloat*)((in && ok0) ? p + i * ldx : kZeroRow + 2 * i);
-      dst[1][i] = *(gfloat*)((in && ok1) ? p + i * ldx + 32 : kZeroRow + 2 * i + 1);
+      dst[0][i] = *(gfloat*)((in && ok0) ? p + i * ldx : kZeroRow + i);
+      dst[1][i] = *(gfloat*)((in && ok1) ? p + i * ldx + 32 : kZeroRow + 8 + i);
     }
   };
   // the first steps load while the dense tile is built
@@ -315,10 +310,9 @@ __global__ __launch_bounds__(256) void spmm_tile_kernel(
 #pragma unroll
         for (int q = 0; q < kBatch; ++q)
 #pragma unroll
-          for (int p = 0; p < 4; ++p) {   // unconditional loads (zeros past cnt or width)
+          for (int p = 0; p < 4; ++p) {
             const int c = cs + lane + 64 * p;
-            xv[q][p] = *(gfloat*)((q < cnt && c < width) ? X + static_cast<int64_t>(ec[q]) * ldx + c
-                                                          : kZeroRow + lane);
+            xv[q][p] = (q < cnt && c < width) ? X[static_cast<int64_t>(ec[q]) * ldx + c] : 0.f;
           }
 #pragma unroll
         for (int q = 0; q < kBatch; ++q) {
@@ -331,26 +325,20 @@ __global__ __launch_bounds__(256) void spmm_tile_kernel(
       }
     }
   }
-  // store this wave's rows (Add, ReLU, the layer below's ReLU derivative);
-  // the Add and mask loads are unconditional (zeros past the width)
+  // store this wave's rows (Add, ReLU)
   for (int i = 0; i < 8; ++i) {
     const int64_t r = rw + i;
     if (r >= n) break;
-    float a[4], mk[4];
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
       const int c = cs + lane + 64 * p;
-      a[p] = add ? *(gfloat*)(c < width ? add + r * ld_add + c : kZeroRow + lane) : 0.f;
-      mk[p] = mask ? *(gfloat*)(c < width ? mask + r * ldm + c : kZeroRow + lane) : 1.f;
-    }
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const int c = cs + lane + 64 * p;
-      float y = Ys[(8 * wave + i) * kYLd + lane + 64 * p];
-      if (add) y += a[p];
-      if (relu) y = fmaxf(y, 0.f);
-      if (mask && !(mk[p] > 0.f)) y = 0.f;
-      if (c < width) Y[r * ldy + c] = y;
+      if (c < width) {
+        float y = Ys[(8 * wave + i) * kYLd + lane + 64 * p];
+        if (add) y += add[r * ld_add + c];
+        if (relu) y = fmaxf(y, 0.f);
+        if (mask && !(mask[r * ldm + c] > 0.f)) y = 0.f;   // ReLU derivative of the layer below
+        Y[r * ldy + c] = y;
+      }
     }
   }
 }
