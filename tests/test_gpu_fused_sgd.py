@@ -115,6 +115,7 @@ CASES = [
     ("sage", "sbm1100", 1024, 1024, "agg", "f32", 1),  # node-contiguous dW operands
     ("gcn", "sbm1500", 64, 48, "agg", "f32", 3),       # grouped sub-GCNs
     ("sage", "sbm1500", 512, 512, "agg", "bf16", 1),   # packed bf16 kernel
+    ("sage", "sbm1500", 1024, 1024, "agg", "bf16", 1),  # 2048 x 1024 dW, rows of 1500 nodes
     ("gcn", "sbm1500", 100, 64, "agg", "bf16", 1),     # bf16 rounding in the fp32 tiles
 ]
 

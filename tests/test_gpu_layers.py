@@ -132,20 +132,26 @@ def test_layer_fp32(G, ctx, case):
         assert e <= FP32_TOL, (k, e)
 
 
-# bf16 cases include products large enough for the packed-operand MFMA path,
+# bf16 cases include products large enough for the 256 x 256-tile MFMA path,
 # with ragged M / N / K, K split into several slices (one shorter than the
-# others) and the [dH | dP] split output of the SAGE backward.
+# others) and the [dH | dP] split output of the SAGE backward; the last three
+# have weight gradients of at least 1024 x 1024 over ragged node counts (300,
+# 1500, 2000), read row-contiguous (the fp32 path copies such operands
+# node-contiguous first; for bf16 inputs that measured slower).
 @pytest.mark.parametrize("case", [("sage", "sbm1500", 100, 256, 1, 0),
                                   ("gcn", "cl2000", 500, 512, 1, 0),
                                   ("sage", "sbm1500", 602, 520, 1, 0),
-                                  ("gcn", "cl2000", 1433, 600, 1, 0)])
+                                  ("gcn", "cl2000", 1433, 600, 1, 0),
+                                  ("sage", "sbm1500", 1024, 1024, 1, 0),
+                                  ("gcn", "er300", 1030, 1100, 1, 1),
+                                  ("gcn", "cl2000", 1100, 1030, 0, 2)])
 def test_layer_bf16_inputs(G, ctx, case):
     kind, gname, s_in, s_out, act, order = case
     log(f"layer bf16 {case}")
     got, want = run_layer(G, ctx, kind, GRAPHS[gname], s_in, s_out, act, order,
                           G.GIST_DTYPE_BF16_IN)
     for k in want:
-        if k == "agg" and kind == "gcn" and order == 0 and s_in > s_out:
+        if k == "agg" and kind == "gcn" and (order == 2 or (order == 0 and s_in > s_out)):
             continue  # transform-first does not form Abar H
         e = relerr(got[k], want[k])
         log(f"  {k}: {e:.3e}")
