@@ -222,12 +222,17 @@ def sub_agg(kind, theta, sls, trained):
     return theta
 
 
-def gist_round(kind, theta, partitions, batches, lr, zeta=1):
+def gist_round(kind, theta, partitions, batches, lr, zeta=1, masks=None, steps=None):
     """One round of Algorithm 1 on one device, sub-GCNs back to back.
 
     ``theta``: global parameters; ``partitions[l]``: (idx, offs) of hidden
     width l; ``batches(i, z)`` -> (csr, X, labels) of sub-GCN i's local step
     z.  Returns (new theta, per-sub-GCN trained params, per-step losses).
+
+    Test use only: ``masks(i, z)``, if given, returns the ReLU decisions
+    step z of sub-GCN i takes in its backward (as ``sub_gcn_step``'s
+    ``masks``; None keeps its own); ``steps``, if a list, receives every
+    local step's result dict in order.
     """
     L = len(theta)
     m = len(partitions[1][1]) - 1 if L > 1 else 1
@@ -238,7 +243,10 @@ def gist_round(kind, theta, partitions, batches, lr, zeta=1):
         li = []
         for z in range(zeta):
             csr, X, y = batches(i, z)
-            st = sub_gcn_step(kind, csr, X, y, p, lr)
+            st = sub_gcn_step(kind, csr, X, y, p, lr,
+                              masks=None if masks is None else masks(i, z))
+            if steps is not None:
+                steps.append(st)
             p = st["params"]
             li.append(st["loss"])
         trained.append(p)
@@ -263,7 +271,8 @@ def adam_params(kind, params, grads, M, V, step, lr):
     return P, M1, V1
 
 
-def sub_gcn_step_adam(kind, csr, X, labels, params, M, V, step, lr, grad_noise=None):
+def sub_gcn_step_adam(kind, csr, X, labels, params, M, V, step, lr, grad_noise=None,
+                      masks=None):
     """``subTrain`` with Adam: forward, loss, backward, one Adam step.
 
     ``grad_noise`` (test use only, default none): a function applied to
@@ -272,24 +281,28 @@ def sub_gcn_step_adam(kind, csr, X, labels, params, M, V, step, lr, grad_noise=N
     the trained weights depends on its gradients' rounding -- Adam divides
     by the root of the second moment, so elements with small or cancelling
     gradients move by amounts far more sensitive than the gradients
-    themselves."""
+    themselves.  ``masks`` (test use only): the ReLU decisions of the
+    backward, as in ``backward``."""
     H, recs = forward(kind, csr, X, params)
     loss, dlogits = _l.softmax_xent(H[-1], labels)
-    grads, _ = backward(kind, csr, H, recs, params, dlogits)
+    grads, _ = backward(kind, csr, H, recs, params, dlogits, masks=masks)
     if grad_noise is not None:
         grads = [_pack(kind, (grad_noise(x) for x in _parts(kind, g))) for g in grads]
     P, M1, V1 = adam_params(kind, params, grads, M, V, step, lr)
-    return dict(loss=loss, grads=grads, params=P, M=M1, V=V1)
+    return dict(loss=loss, H=H, recs=recs, grads=grads, params=P, M=M1, V=V1)
 
 
 def gist_train(kind, theta, rounds, zeta, lr, partitions, batches, policy="carry",
-               grad_noise=None):
+               grad_noise=None, masks=None, steps=None):
     """Algorithm 1 with Adam, sub-GCNs back to back on one device.
 
     ``partitions(t)`` -> the round's partitions (as for ``slice_indices``);
     ``batches(t, i, z)`` -> (csr, X, labels) of sub-GCN i's local step z.
     Returns (theta, M, V, losses[t][i][z]); M, V are the global moments
     ("carry") or None ("reset").  ``grad_noise``: see ``sub_gcn_step_adam``.
+    Test use only: ``masks(t, i, z)`` -> the ReLU decisions of that step's
+    backward (None keeps its own), ``steps`` (a list) receives every local
+    step's result dict in order.
     """
     if policy not in ("carry", "reset"):
         raise ValueError("policy is 'carry' or 'reset'")
@@ -313,7 +326,10 @@ def gist_train(kind, theta, rounds, zeta, lr, partitions, batches, policy="carry
             for z in range(zeta):
                 csr, X, y = batches(t, i, z)
                 k = (t * zeta + z + 1) if policy == "carry" else (z + 1)
-                st = sub_gcn_step_adam(kind, csr, X, y, p, mm, vv, k, lr, grad_noise)
+                st = sub_gcn_step_adam(kind, csr, X, y, p, mm, vv, k, lr, grad_noise,
+                                       masks=None if masks is None else masks(t, i, z))
+                if steps is not None:
+                    steps.append(st)
                 p, mm, vv = st["params"], st["M"], st["V"]
                 li.append(st["loss"])
             trained.append((sl, p, mm, vv))

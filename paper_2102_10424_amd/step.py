@@ -1377,7 +1377,7 @@ class GistModel:
         self.pending = None
 
 
-def gist_train(model, runner, rounds, zeta, lr, partition_seeds, batch):
+def gist_train(model, runner, rounds, zeta, lr, partition_seeds, batch, after_step=None):
     """Algorithm 1 on one device: ``rounds`` synchronisation rounds, each
     ``subGCNs`` -> ``zeta`` local steps per sub-GCN (``subTrain``, back to
     back) -> ``subAgg``.
@@ -1387,6 +1387,8 @@ def gist_train(model, runner, rounds, zeta, lr, partition_seeds, batch):
     The optimizer is the model's: SGD, or Adam with the bias correction
     counting every local step so far ("carry": k = t zeta + z + 1) or the
     round's steps ("reset": k = z + 1, moments restarted at z = 0).
+    ``after_step(t, i, z, b)``, if given, is called after each local step is
+    launched (for instance to read the runner's activations of batch ``b``).
     Returns the device tensor of losses [rounds, m, zeta]; nothing is synced.
     """
     losses = torch.empty(rounds, model.m, zeta, device=model.device)
@@ -1402,6 +1404,8 @@ def gist_train(model, runner, rounds, zeta, lr, partition_seeds, batch):
                 elif model.adam == "reset":
                     opt = (model.M[i], model.V[i], z + 1, z == 0)
                 runner.step(b, model.params[i], lr, adam=opt, loss_out=losses[t, i, z:z + 1])
+                if after_step is not None:
+                    after_step(t, i, z, b)
         model.end_round()
     model.finalize()
     return losses

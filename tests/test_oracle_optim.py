@@ -230,3 +230,42 @@ def test_grad_noise_hook_and_the_sensitivity_check():
     got[i] = 0.0
     e_good, _, ratio = check_adam(got, want[l], [q[l] for q in ps])
     assert e_good > 1e-4 and ratio > 1.0
+
+
+@pytest.mark.parametrize("loop", ["sgd_round", "adam_train"])
+def test_decision_overrides_in_the_loops(loop):
+    """``masks`` and ``steps`` of ``gist_round`` / ``gist_train`` (test use:
+    the GPU training tests run the oracle's backward through the GPU's own
+    ReLU decisions).  Handing back the decisions the oracle itself took
+    reproduces its run bit for bit; flipping one decision far from zero
+    changes the trained weights; ``steps`` records every local step."""
+    g = erdos_renyi(200, 700, 3)
+    csr = MB.build(g, None, "gcn")
+    rng = np.random.default_rng(5)
+    widths, m, zeta = [10, 24, 12, 4], 2, 2
+    X = rng.standard_normal((g.n, widths[0]))
+    y = rng.integers(0, widths[-1], g.n)
+    theta = [rng.standard_normal((widths[l], widths[l + 1])) * 0.4 for l in range(3)]
+    parts = [None] + [P.partition(widths[l], m, 30 + l) for l in (1, 2)] + [None]
+
+    def run(masks=None, steps=None):
+        if loop == "sgd_round":
+            mk = None if masks is None else (lambda i, z: masks[zeta * i + z])
+            return G.gist_round("gcn", theta, parts, lambda i, z: (csr, X, y), 0.05, zeta,
+                                masks=mk, steps=steps)[0]
+        mk = None if masks is None else (lambda t, i, z: masks[zeta * i + z])
+        return G.gist_train("gcn", theta, 1, zeta, 0.01, lambda t: parts,
+                            lambda t, i, z: (csr, X, y), policy="carry", masks=mk,
+                            steps=steps)[0]
+
+    steps = []
+    base = run(steps=steps)
+    assert len(steps) == m * zeta
+    own = [[st["recs"][l]["Z"] > 0 for l in range(2)] + [None] for st in steps]
+    assert all(np.array_equal(a, b) for a, b in zip(base, run(masks=own)))
+    # flip the decision of the largest pre-activation of sub-GCN 1's last step
+    Z = steps[-1]["recs"][1]["Z"]
+    i = np.unravel_index(np.argmax(np.abs(Z)), Z.shape)
+    flipped = [[mk.copy() if mk is not None else None for mk in s] for s in own]
+    flipped[-1][1][i] = not flipped[-1][1][i]
+    assert any(not np.array_equal(a, b) for a, b in zip(base, run(masks=flipped)))
