@@ -54,24 +54,17 @@ typedef unsigned short ushort8 __attribute__((ext_vector_type(8)));
 
 constexpr int kRows = 32;          // output rows per workgroup (the MFMA's M)
 constexpr int kCols = 256;         // output columns per workgroup: 4 waves x 64
-constexpr int kMaxK = 320;         // widest dense window (a multiple of kKs)
+constexpr int kMaxK = 288;         // widest dense window (a multiple of kKs)
 constexpr int kNear = 192;         // an entry within this of its row's diagonal sets the window
 constexpr int kKs = 16;            // window rows per step (the MFMA's K)
 constexpr int kDepth = 3;          // X steps in flight ahead of the one multiplied
-// steps are taken kDepth at a time; the tile's zero columns cover the padding
-constexpr int kPadK = (kMaxK / kKs + kDepth - 1) / kDepth * kDepth * kKs;
-constexpr int kALd = kPadK + 8;    // bf16 per row of the dense tile (16 B pad)
+constexpr int kALd = kMaxK + 8;    // bf16 per row of the dense tile (16 B pad)
+constexpr int kBlocksPerCU = 4;    // resident workgroups per CU (LDS and registers sized for it)
 constexpr int kYLd = kCols + 4;    // floats per row of the result tile
 constexpr int kChunk = 8;          // 64-entry chunks a wave loads at once
 constexpr int kBatch = 16;         // outside-window entries gathered at once
+constexpr int kList = 64;          // outside-window entries a wave lists before gathering
 
-// Sixteen zeros in device memory (zero-initialised, never written): a
-// pipelined load that falls outside the window or the matrix reads here, so
-// no load depends on a branch.  Not const, so that the compiler cannot fold
-// such a load away and put the real one behind a branch again.
-__device__ float kZeroRow[16];
-
-typedef __attribute__((address_space(1))) const float gfloat;   // global memory
 
 __device__ __forceinline__ unsigned short bf16_bits(float f) {
   return __builtin_bit_cast(unsigned short, static_cast<__bf16>(f));
@@ -107,7 +100,7 @@ __device__ __forceinline__ int row_of(int e, const int (&rp)[9]) {
   return rl;
 }
 
-__global__ __launch_bounds__(256) void spmm_tile_kernel(
+__global__ __launch_bounds__(256, kBlocksPerCU) void spmm_tile_kernel(
     int n, int n_in, const int* __restrict__ rowptr, const int* __restrict__ col,
     const float* __restrict__ val, const float* __restrict__ X, int64_t ldx, int width,
     float* Y, int64_t ldy, const float* add, int64_t ld_add, int relu, int tiles,
@@ -115,9 +108,11 @@ __global__ __launch_bounds__(256) void spmm_tile_kernel(
   // dense tile (hi, lo), later the fp32 result tile
   __shared__ __attribute__((aligned(16))) unsigned short Atile[2 * kRows * kALd];
   __shared__ int red[8];
-  static_assert(sizeof(float) * kRows * kYLd <= sizeof(unsigned short) * 2 * kRows * kALd,
-                "result tile must fit in the dense tile's space");
-  static_assert(kMaxK % kKs == 0 && kPadK >= kMaxK && kALd % 8 == 0, "tile layout");
+  static_assert(sizeof(float) * kRows * kYLd + 4 * sizeof(int) * 3 * kList <=
+                    sizeof(unsigned short) * 2 * kRows * kALd,
+                "result tile and outside-entry lists must fit in the dense tile's space");
+  // steps run kDepth at a time: the padded steps stay inside the zeroed tile
+  static_assert(kMaxK % (kKs * kDepth) == 0 && kALd % 8 == 0, "tile layout");
 
   const int t = threadIdx.x;
   const int lane = t & 63;
@@ -149,82 +144,120 @@ __global__ __launch_bounds__(256) void spmm_tile_kernel(
   };
   if (fit) load_chunks(rp[0]);
 
-  // zero the dense tile while the entries arrive
-  {
+  auto zero_tile = [&]() {
     uint4v* z = reinterpret_cast<uint4v*>(Atile);
     constexpr int units = 2 * kRows * kALd / 8;
     for (int u = t; u < units; u += 256) z[u] = uint4v{0u, 0u, 0u, 0u};
-  }
+  };
+  // pass 0 zeroes the dense tile while the entries arrive
+  zero_tile();
 
-  // ---- 1. window: columns of the entries near their row's diagonal
-  int cmin = INT_MAX, cmax = -1;
-  for (int base = rp[0]; base < rp[8]; base += 64 * kChunk) {
-    if (!fit) load_chunks(base);
+  // X operand: lane (li, lh) of this wave holds window rows 16 j + 8 lh .. + 7
+  // of columns c0 + li and c0 + 32 + li.  Columns past the matrix read its
+  // last column (their results are never stored) and steps past the window
+  // re-read its last step (multiplied by the tile's zero columns), so every
+  // load is unconditional and in bounds: one uniform 64-bit base per step and
+  // 32-bit lane offsets, no address selects (loads behind branches or
+  // selects would make the compiler drain them before each step).
+  const int c0 = cs + wave * 64 + li;
+  const int ld4 = static_cast<int>(ldx * 4);
+  const unsigned off0 = static_cast<unsigned>(8 * lh * ld4 + 4 * min(c0, width - 1));
+  const unsigned off1 = static_cast<unsigned>(8 * lh * ld4 + 4 * min(c0 + 32, width - 1));
+  float xr[kDepth][2][8];
+  floatx16 acc[2];
 #pragma unroll
-    for (int u = 0; u < kChunk; ++u) {
-      const int e = base + 64 * u + lane;
-      if (e < rp[8]) {
-        const int r = rw + row_of(e, rp);
-        if (cc[u] >= r - kNear && cc[u] <= r + kNear) {
-          cmin = min(cmin, cc[u]);
-          cmax = max(cmax, cc[u]);
+  for (int b = 0; b < 2; ++b)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[b][r] = 0.f;
+
+  // Up to two windows, each a pass of steps 1-3: the first spans the
+  // entries near their row's diagonal, the second those of them outside the
+  // first (a tile whose rows straddle two clusters needs about twice kMaxK
+  // columns; two passes keep the tile, and so the workgroups per CU, at one
+  // window's size).  Window p is [lo_p, lo_p + kw_p); an entry belongs to
+  // the first window that holds it, or to step 4.
+  int lo0 = 0, kw0 = 0, lo1 = 0, kw1 = 0;
+  for (int pass = 0; pass < 2; ++pass) {
+    // ---- 1. window: columns of the near entries no earlier window holds
+    int cmin = INT_MAX, cmax = -1;
+    for (int base = rp[0]; base < rp[8]; base += 64 * kChunk) {
+      if (!fit) load_chunks(base);
+#pragma unroll
+      for (int u = 0; u < kChunk; ++u) {
+        const int e = base + 64 * u + lane;
+        if (e < rp[8]) {
+          const int r = rw + row_of(e, rp);
+          const bool fresh =
+              static_cast<unsigned>(cc[u] - lo0) >= static_cast<unsigned>(kw0);
+          if (cc[u] >= r - kNear && cc[u] <= r + kNear && fresh) {
+            cmin = min(cmin, cc[u]);
+            cmax = max(cmax, cc[u]);
+          }
         }
       }
     }
-  }
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    cmin = min(cmin, __shfl_xor(cmin, o, 64));
-    cmax = max(cmax, __shfl_xor(cmax, o, 64));
-  }
-  if (lane == 0) {
-    red[wave] = cmin;
-    red[4 + wave] = cmax;
-  }
-  __syncthreads();
-  cmin = min(min(red[0], red[1]), min(red[2], red[3]));
-  cmax = max(max(red[4], red[5]), max(red[6], red[7]));
-  int clo = 0, K = 0;
-  if (cmax >= cmin) {
-    clo = cmin;
-    K = min(kMaxK, (cmax - cmin + kKs) / kKs * kKs);
-  }
-  const int nk = K / kKs;
-
-  // X operand: lane (li, lh) of this wave holds window rows 16 j + 8 lh .. + 7
-  // of columns c0 + li and c0 + 32 + li
-  const int c0 = cs + wave * 64 + li;
-  const bool ok0 = c0 < width, ok1 = c0 + 32 < width;
-  const int rows_left = n_in - clo - 8 * lh;   // window rows this lane may read
-  const float* xp = X + static_cast<int64_t>(clo + 8 * lh) * ldx + c0;
-  float xr[kDepth][2][8];
-  // Every load is issued unconditionally (a row outside the window or the
-  // matrix reads a zero from kZeroRow instead): loads behind branches would
-  // make the compiler drain all of them before each step.
-  auto gload = [&](float (&dst)[2][8], int j) {
-    const float* p = xp + static_cast<int64_t>(j * kKs) * ldx;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const bool in = j < nk && j * kKs + i < rows_left;
-      dst[0][i] = *(gfloat*)((in && ok0) ? p + i * ldx : kZeroRow + i);
-      dst[1][i] = *(gfloat*)((in && ok1) ? p + i * ldx + 32 : kZeroRow + 8 + i);
+    for (int o = 32; o > 0; o >>= 1) {
+      cmin = min(cmin, __shfl_xor(cmin, o, 64));
+      cmax = max(cmax, __shfl_xor(cmax, o, 64));
     }
-  };
-  // the first steps load while the dense tile is built
-  if (nk > 0) {
+    if (lane == 0) {
+      red[wave] = cmin;
+      red[4 + wave] = cmax;
+    }
+    // (pass 1: also every wave is past pass 0's reads of the dense tile)
+    __syncthreads();
+    cmin = min(min(red[0], red[1]), min(red[2], red[3]));
+    cmax = max(max(red[4], red[5]), max(red[6], red[7]));
+    // The window [clo, clo + K) lies inside the matrix's columns, K a
+    // multiple of kKs (shifted left from cmin where it would pass n_in,
+    // which keeps [cmin, cmax] inside it unless K was capped).  Every
+    // window row is then a real row of X.
+    int clo = 0, K = 0;
+    if (cmax >= cmin) {
+      K = min(min(kMaxK, (cmax - cmin + kKs) / kKs * kKs), n_in / kKs * kKs);
+      clo = min(cmin, n_in - K);
+    }
+    clo = __builtin_amdgcn_readfirstlane(clo);
+    K = __builtin_amdgcn_readfirstlane(K);
+    const int nk = K / kKs;
+    if (nk == 0) break;
+    if (pass == 0) {
+      lo0 = clo;
+      kw0 = K;
+    } else {
+      lo1 = clo;
+      kw1 = K;
+    }
+
+    auto gload = [&](float (&dst)[2][8], int j) {
+      const int jj = min(j, nk - 1);
+      const char* base =
+          reinterpret_cast<const char*>(X + static_cast<int64_t>(clo + jj * kKs) * ldx);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        dst[0][i] = *reinterpret_cast<const float*>(base + i * ld4 + off0);
+        dst[1][i] = *reinterpret_cast<const float*>(base + i * ld4 + off1);
+      }
+    };
+    // the first steps load while the dense tile is built
 #pragma unroll
     for (int p = 0; p < kDepth; ++p) gload(xr[p], p);
-  }
+    if (pass > 0) {
+      zero_tile();
+      __syncthreads();
+    }
 
-  // ---- 2. the window's entries as a dense 32 x K tile (bf16 hi, lo)
-  if (nk > 0) {
+    // ---- 2. this window's entries as a dense 32 x K tile (bf16 hi, lo)
     for (int base = rp[0]; base < rp[8]; base += 64 * kChunk) {
       if (!fit) load_chunks(base);
 #pragma unroll
       for (int u = 0; u < kChunk; ++u) {
         const int e = base + 64 * u + lane;
         const unsigned k = static_cast<unsigned>(cc[u] - clo);
-        if (e < rp[8] && k < static_cast<unsigned>(K)) {
+        const bool fresh =
+            pass == 0 || static_cast<unsigned>(cc[u] - lo0) >= static_cast<unsigned>(kw0);
+        if (e < rp[8] && k < static_cast<unsigned>(K) && fresh) {
           const int rl = 8 * wave + row_of(e, rp);
           const unsigned short hi = bf16_bits(vv[u]);
           Atile[rl * kALd + k] = hi;
@@ -232,36 +265,31 @@ __global__ __launch_bounds__(256) void spmm_tile_kernel(
         }
       }
     }
-  }
-  __syncthreads();
+    __syncthreads();
 
-  // ---- 3. Y_tile = A_tile X[clo .. clo + K) on the matrix cores, no barriers
-  floatx16 acc[2];
+    // ---- 3. Y_tile += A_tile X[clo .. clo + K) on the matrix cores, no barriers
+    auto mfma = [&](const float (&src)[2][8], int j) {
+      // A fragment: tile row li, window columns 16 j + 8 lh .. + 7
+      const bf16x8 ah = *reinterpret_cast<const bf16x8*>(Atile + li * kALd + j * kKs + 8 * lh);
+      const bf16x8 al =
+          *reinterpret_cast<const bf16x8*>(Atile + (kRows + li) * kALd + j * kKs + 8 * lh);
 #pragma unroll
-  for (int b = 0; b < 2; ++b)
+      for (int b = 0; b < 2; ++b) {
+        bf16x8 bh, bl;
+        split8(src[b], bh, bl);
+        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh, acc[b], 0, 0, 0);
+        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl, acc[b], 0, 0, 0);
+        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh, acc[b], 0, 0, 0);
+      }
+    };
+    // steps nk .. (padded to a multiple of kDepth) multiply the tile's zero
+    // columns with the window's last rows
+    for (int j0 = 0; j0 < nk; j0 += kDepth) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[b][r] = 0.f;
-  auto mfma = [&](const float (&src)[2][8], int j) {
-    // A fragment: tile row li, window columns 16 j + 8 lh .. + 7
-    const bf16x8 ah = *reinterpret_cast<const bf16x8*>(Atile + li * kALd + j * kKs + 8 * lh);
-    const bf16x8 al =
-        *reinterpret_cast<const bf16x8*>(Atile + (kRows + li) * kALd + j * kKs + 8 * lh);
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      bf16x8 bh, bl;
-      split8(src[b], bh, bl);
-      acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bh, acc[b], 0, 0, 0);
-      acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah, bl, acc[b], 0, 0, 0);
-      acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al, bh, acc[b], 0, 0, 0);
-    }
-  };
-  // steps nk .. (padded to a multiple of kDepth) multiply the tile's zero
-  // columns with zeroed X values
-  for (int j0 = 0; j0 < nk; j0 += kDepth) {
-#pragma unroll
-    for (int p = 0; p < kDepth; ++p) {
-      mfma(xr[p], j0 + p);
-      gload(xr[p], j0 + p + kDepth);
+      for (int p = 0; p < kDepth; ++p) {
+        mfma(xr[p], j0 + p);
+        gload(xr[p], j0 + p + kDepth);
+      }
     }
   }
   __syncthreads();   // every wave is past its last read of the dense tile
@@ -277,54 +305,75 @@ __global__ __launch_bounds__(256) void spmm_tile_kernel(
       Ys[(8 * (r / 4) + 4 * lh + (r % 4)) * kYLd + wave * 64 + 32 * b + li] = acc[b][r];
   __syncthreads();
 
-  // ---- 4. entries outside the window, in storage order, then the store.
+  // ---- 4. entries outside both windows, in storage order, then the store.
   // This wave owns tile rows 8 wave .. + 7; lane owns columns cs + lane + 64 q.
+  // The wave's outside entries are listed in LDS (behind the result tile)
+  // in storage order, up to kList at a time, and their X rows gathered
+  // kBatch at a time: a wave with a few outside entries in each 64-entry
+  // chunk then waits once per kBatch entries, not once per chunk.
+  int* lst_c = reinterpret_cast<int*>(Atile) + kRows * kYLd + wave * 3 * kList;
+  int* lst_r = lst_c + kList;
+  float* lst_v = reinterpret_cast<float*>(lst_r + kList);
+  const int cl0 = min(cs + lane, width - 1), cl1 = min(cs + lane + 64, width - 1);
+  const int cl2 = min(cs + lane + 128, width - 1), cl3 = min(cs + lane + 192, width - 1);
+  int cnt = 0;
+  auto flush = [&]() {
+    for (int q0 = 0; q0 < cnt; q0 += kBatch) {
+      const int nb = min(kBatch, cnt - q0);
+      int ec[kBatch], er[kBatch];
+      float ev[kBatch];
+#pragma unroll
+      for (int q = 0; q < kBatch; ++q) {
+        const int i = min(q0 + q, cnt - 1);   // past the batch: a listed entry, not added
+        ec[q] = __builtin_amdgcn_readfirstlane(lst_c[i]);
+        er[q] = __builtin_amdgcn_readfirstlane(lst_r[i]);
+        ev[q] = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(lst_v[i])));
+      }
+      // every load in bounds and unconditional (columns past the matrix read
+      // its last column and are never stored)
+      float xv[kBatch][4];
+#pragma unroll
+      for (int q = 0; q < kBatch; ++q) {
+        const float* xrow = X + static_cast<int64_t>(ec[q]) * ldx;
+        xv[q][0] = xrow[cl0];
+        xv[q][1] = xrow[cl1];
+        xv[q][2] = xrow[cl2];
+        xv[q][3] = xrow[cl3];
+      }
+#pragma unroll
+      for (int q = 0; q < kBatch; ++q) {
+        if (q < nb) {
+          float* yrow = Ys + (8 * wave + er[q]) * kYLd + lane;
+#pragma unroll
+          for (int p = 0; p < 4; ++p) yrow[64 * p] = fmaf(ev[q], xv[q][p], yrow[64 * p]);
+        }
+      }
+    }
+    cnt = 0;
+  };
   for (int base = rp[0]; base < rp[8]; base += 64 * kChunk) {
     if (!fit) load_chunks(base);
 #pragma unroll
     for (int u = 0; u < kChunk; ++u) {
       const int e = base + 64 * u + lane;
-      const bool out = e < rp[8] && static_cast<unsigned>(cc[u] - clo) >= static_cast<unsigned>(K);
-      uint64_t m = __ballot(out);
-      while (m) {
-        // up to kBatch of this chunk's outside entries at a time, loads first
-        int ec[kBatch], er[kBatch];
-        float ev[kBatch];
-        int cnt = 0;
-#pragma unroll
-        for (int q = 0; q < kBatch; ++q) {
-          if (m) {
-            const int b = __builtin_ctzll(m);
-            m &= m - 1;
-            ec[q] = __builtin_amdgcn_readlane(cc[u], b);
-            ev[q] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(vv[u]), b));
-            er[q] = row_of(base + 64 * u + b, rp);
-            cnt = q + 1;
-          } else {
-            ec[q] = 0;
-            ev[q] = 0.f;
-            er[q] = 0;
-          }
-        }
-        float xv[kBatch][4];
-#pragma unroll
-        for (int q = 0; q < kBatch; ++q)
-#pragma unroll
-          for (int p = 0; p < 4; ++p) {
-            const int c = cs + lane + 64 * p;
-            xv[q][p] = (q < cnt && c < width) ? X[static_cast<int64_t>(ec[q]) * ldx + c] : 0.f;
-          }
-#pragma unroll
-        for (int q = 0; q < kBatch; ++q) {
-          if (q < cnt) {
-            float* yrow = Ys + (8 * wave + er[q]) * kYLd + lane;
-#pragma unroll
-            for (int p = 0; p < 4; ++p) yrow[64 * p] = fmaf(ev[q], xv[q][p], yrow[64 * p]);
-          }
-        }
+      const bool out = e < rp[8] &&
+                       static_cast<unsigned>(cc[u] - lo0) >= static_cast<unsigned>(kw0) &&
+                       static_cast<unsigned>(cc[u] - lo1) >= static_cast<unsigned>(kw1);
+      const uint64_t m = __ballot(out);
+      const int pc = __builtin_popcountll(m);
+      if (pc == 0) continue;
+      if (cnt + pc > kList) flush();
+      if (out) {
+        const int i = cnt + __builtin_amdgcn_mbcnt_hi(static_cast<unsigned>(m >> 32),
+                                                      __builtin_amdgcn_mbcnt_lo(static_cast<unsigned>(m), 0u));
+        lst_c[i] = cc[u];
+        lst_r[i] = row_of(e, rp);
+        lst_v[i] = vv[u];
       }
+      cnt += pc;
     }
   }
+  flush();
   // store this wave's rows (Add, ReLU)
   for (int i = 0; i < 8; ++i) {
     const int64_t r = rw + i;
@@ -351,6 +400,11 @@ gist_status spmm_clustered(hipStream_t st, int64_t n, int64_t n_in, int64_t nnz,
                            const float* add, int64_t ld_add, bool relu, const float* mask,
                            int64_t ldm) {
   if (n <= 0 || width <= 0) return GIST_OK;
+  // The X loads use 32-bit byte offsets of up to 16 rows: wider rows, or a
+  // matrix with fewer columns than one window step, take the gather kernel.
+  if (ldx > INT32_MAX / 64 || n_in < kKs)
+    return spmm(st, n, nnz, rowptr, col, val, X, ldx, width, Y, ldy, add, ld_add, relu, mask,
+                ldm);
   const int64_t tiles = (n + kRows - 1) / kRows;
   const int64_t slabs = (width + kCols - 1) / kCols;
   const int64_t nblocks = tiles * slabs;
