@@ -49,6 +49,7 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float float2v __attribute__((ext_vector_type(2)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef unsigned uint4v __attribute__((ext_vector_type(4)));
 typedef unsigned short ushort8 __attribute__((ext_vector_type(8)));
 
@@ -104,7 +105,7 @@ __global__ __launch_bounds__(256, kBlocksPerCU) void spmm_tile_kernel(
     int n, int n_in, const int* __restrict__ rowptr, const int* __restrict__ col,
     const float* __restrict__ val, const float* __restrict__ X, int64_t ldx, int width,
     float* Y, int64_t ldy, const float* add, int64_t ld_add, int relu, int tiles,
-    int64_t nblocks, const float* mask, int64_t ldm) {
+    int64_t nblocks, const float* mask, int64_t ldm, int vec) {
   // dense tile (hi, lo), later the fp32 result tile
   __shared__ __attribute__((aligned(16))) unsigned short Atile[2 * kRows * kALd];
   __shared__ int red[8];
@@ -374,7 +375,50 @@ __global__ __launch_bounds__(256, kBlocksPerCU) void spmm_tile_kernel(
     }
   }
   flush();
-  // store this wave's rows (Add, ReLU)
+  // store this wave's rows (Add, ReLU, the layer below's ReLU derivative)
+  if (vec) {
+    // 16-byte accesses, lane owning columns cs + 4 lane .. + 3: all eight
+    // rows' Add and mask values are read before any row is stored (Add may
+    // alias Y element for element), rows and columns past the matrix
+    // clamped so every load is in bounds and unconditional
+    const int c = cs + 4 * lane;
+    const int ccl = min(c, width - 4);
+    floatx4 v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      v[i] = *reinterpret_cast<const floatx4*>(Ys + (8 * wave + i) * kYLd + 4 * lane);
+    if (add) {
+      floatx4 a[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        a[i] = *reinterpret_cast<const floatx4*>(add + static_cast<int64_t>(min(rw + i, n - 1)) * ld_add + ccl);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] += a[i];
+    }
+    if (relu) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[i][q] = fmaxf(v[i][q], 0.f);
+    }
+    if (mask) {
+      floatx4 mk[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        mk[i] = *reinterpret_cast<const floatx4*>(mask + static_cast<int64_t>(min(rw + i, n - 1)) * ldm + ccl);
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (!(mk[i][q] > 0.f)) v[i][q] = 0.f;
+    }
+    if (c < width) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        if (rw + i < n) *reinterpret_cast<floatx4*>(Y + static_cast<int64_t>(rw + i) * ldy + c) = v[i];
+    }
+    return;
+  }
   for (int i = 0; i < 8; ++i) {
     const int64_t r = rw + i;
     if (r >= n) break;
@@ -413,11 +457,16 @@ gist_status spmm_clustered(hipStream_t st, int64_t n, int64_t n_in, int64_t nnz,
   const double bytes = 4.0 * (n + 1) + 8.0 * static_cast<double>(nnz) +
                        4.0 * static_cast<double>(n) * width * (2.0 + (add ? 1.0 : 0.0) +
                                                                 (mask ? 1.0 : 0.0));
+  // 16-byte result stores (and Add / mask reads) where every row allows them
+  auto al16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+  const bool vec = width % 4 == 0 && ldy % 4 == 0 && al16(Y) &&
+                   (!add || (ld_add % 4 == 0 && al16(add))) &&
+                   (!mask || (ldm % 4 == 0 && al16(mask)));
   ProfScope ps(st, "spmm_tile", 2.0 * static_cast<double>(nnz) * width, bytes);
   hipLaunchKernelGGL(spmm_tile_kernel, dim3(static_cast<unsigned>(nblocks)), dim3(256), 0, st,
                      static_cast<int>(n), static_cast<int>(n_in), rowptr, col, val, X, ldx, width,
                      Y, ldy, add, ld_add, relu ? 1 : 0, static_cast<int>(tiles), nblocks, mask,
-                     ldm);
+                     ldm, vec ? 1 : 0);
   return check_launch("spmm_clustered");
 }
 
