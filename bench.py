@@ -122,9 +122,9 @@ def parse():
                          "policies on a learnable c3-graph task and print the loss per round")
     ap.add_argument("--curve-rounds", type=int, default=20)
     ap.add_argument("--curve-zeta", type=int, default=10)
-    ap.add_argument("--aggregation", default="gather", choices=["tile", "gather"],
-                    help="cluster mini-batches and the c5 matrix: the gather kernel, or the "
-                         "matrix-core tiles of GIST_LAYER_CLUSTERED (slower on these shapes)")
+    ap.add_argument("--aggregation", default="tile", choices=["tile", "gather"],
+                    help="cluster mini-batches and the c5 matrix: the matrix-core tiles of "
+                         "GIST_LAYER_CLUSTERED (default), or the gather kernel")
     ap.add_argument("--curve-hidden", type=int, default=256)
     ap.add_argument("--curve-lr", type=float, default=0.01)
     ap.add_argument("--no-extras", action="store_true",

@@ -291,22 +291,24 @@ enum {
  * the gradients are bitwise those of the unflagged calls (the derivative is
  * the same select, 1[H > 0], applied to the same values). */
 
-/* GIST_LAYER_CLUSTERED: a hint that Abar (and A_T) is the matrix of a
+/* GIST_LAYER_CLUSTERED: a hint that almost every entry of Abar (and A_T)
+ * sits within a few hundred columns of its row's diagonal: the matrix of a
  * cluster mini-batch over block-contiguous node ids (Section 2.2: a union of
- * clusters), so almost every entry sits within a few hundred columns of its
- * row's diagonal.  The aggregation then runs on the matrix cores: for every
- * 32 rows, the entries within 192 of their row's diagonal (a window of at
- * most 384 columns) form a dense tile whose values and the matching X rows
- * are each split into two bf16 halves (hi = bf16(v), lo = bf16(v - hi));
- * the products hi*hi + hi*lo + lo*hi are accumulated in fp32, so every
- * term carries a relative error below 2^-15; the remaining entries are
- * gathered and added in storage order.  Results are deterministic and
- * agree with the plain fp32 aggregation within that bound for any matrix
- * (only the speed depends on the structure).  The matrix must not repeat
- * a (row, column) entry (gist_build_minibatch_csr never does).  Off by
- * default: on batches of 163-node clusters the gather kernel is faster,
- * because each 32-row tile is a serial chain of memory round trips (entries,
- * window, X rows) that three resident tiles per CU do not hide. */
+ * clusters), or a whole graph numbered cluster by cluster.  The aggregation
+ * then runs on the matrix cores: for every 32 rows, the entries within 192
+ * of their row's diagonal form up to two dense tiles of at most 288 columns
+ * (the second for rows that straddle two clusters) whose values and the
+ * matching X rows are each split into two bf16 halves (hi = bf16(v),
+ * lo = bf16(v - hi)); the products hi*hi + hi*lo + lo*hi are accumulated in
+ * fp32, so every term carries a relative error below 2^-15; the remaining
+ * entries are gathered and added in storage order.  Results are
+ * deterministic and agree with the plain fp32 aggregation within that bound
+ * for any matrix (only the speed depends on the structure).  The matrix
+ * must not repeat a (row, column) entry (gist_build_minibatch_csr never
+ * does).  On the cluster-structured workloads measured it is faster than the
+ * gather kernel (4.1 against 7.4 ms for the 2.45M-node graph at width 256,
+ * 34 against 55 us for a 10-cluster mini-batch at width 4,096); without the
+ * structure it gathers every entry and is slower. */
 
 /* Workspace (device bytes) that fwd and bwd need for this descriptor. */
 gist_status gist_layer_workspace_size(const gist_layer_desc* L, size_t* fwd_bytes,

@@ -8,7 +8,7 @@ below 2^-15; the checks are therefore elementwise: |got - exact| <=
 aggregation of the backward pass), plus the usual 1e-4 normwise bar on
 every output and gradient.  Matrices cover every branch of the kernel:
 cluster mini-batches (most entries in the dense window), random graphs (all
-entries gathered), bands wider than the window (the 384-column clamp), hub
+entries gathered), bands wider than two windows (the 288-column clamp), hub
 rows longer than the 512 entries a wave loads at once, rectangular LADIES
 layers, ragged row counts and widths (several 256-column slabs), a single
 row, and the SAGE backward whose Add aliases its output.
@@ -57,7 +57,7 @@ def _matrices():
     g2 = sbm(4000, 20, 30.0, 0.9, seed=22)                     # clusters of 200 (> kNear)
     out["sbm_wide_clusters"] = (g2, np.array([0, 3, 7], dtype=np.int32))
     out["er_random"] = (erdos_renyi(700, 2800, seed=5), None)
-    # a band of half-width 260 > 192: windows clamp at 384 columns
+    # a band of half-width 260 > 192: two windows of at most 288 columns, the rest gathered
     n = 900
     out["band_260"] = (_graph_from_edges(n, [(i, j) for i in range(n)
                                              for j in range(i + 1, min(n, i + 261), 7)]), None)
