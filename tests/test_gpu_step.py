@@ -246,7 +246,7 @@ def chained_gpu_step(G, ctx, w, dtype, clustered=False):
 
 @pytest.mark.parametrize("name,dtype,clustered", [(c, "f32", False) for c in CONFIGS + ["c6"]] +
                          [(c, "bf16", False) for c in CONFIGS] +
-                         [("c3", "f32", True), ("c4", "f32", True)])
+                         [(c, d, True) for c in ("c3", "c4") for d in ("f32", "bf16")])
 def test_step_chained(G, ctx, name, dtype, clustered):
     from oracle import layers as OLr
     w = workload(name)
