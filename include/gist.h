@@ -303,7 +303,9 @@ enum {
  * fp32, so every term carries a relative error below 2^-15; the remaining
  * entries are gathered and added in storage order.  Results are
  * deterministic and agree with the plain fp32 aggregation within that bound
- * for any matrix (only the speed depends on the structure).  The matrix
+ * for any matrix and finite X (only the speed depends on the structure; an
+ * Inf or NaN in a window row reaches every output row of that tile, since
+ * the dense tile multiplies it by zero).  The matrix
  * must not repeat a (row, column) entry (gist_build_minibatch_csr never
  * does).  On the cluster-structured workloads measured it is faster than the
  * gather kernel (4.1 against 7.4 ms for the 2.45M-node graph at width 256,
