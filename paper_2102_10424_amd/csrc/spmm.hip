@@ -87,6 +87,16 @@ __global__ __launch_bounds__(256) void spmm_kernel(
     e0 = rowptr[row];
     e1 = rowptr[row + 1];
   }
+  // The epilogue's Add and mask values load before the row's gathers, so
+  // their latency overlaps them (row and column clamped into the matrix:
+  // every load is in bounds; an inactive lane's values are never stored).
+  float a[VEC], mv[VEC];
+  {
+    const int64_t rr = min(row, static_cast<int64_t>(n) - 1);
+    const int cc = min(c0, width - VEC);
+    if (add) load_vec<VEC>(add + rr * ld_add + cc, a);
+    if (mask) load_vec<VEC>(mask + rr * ldm + cc, mv);
+  }
   float acc[VEC];
 #pragma unroll
   for (int v = 0; v < VEC; ++v) acc[v] = 0.f;
@@ -133,8 +143,6 @@ __global__ __launch_bounds__(256) void spmm_kernel(
   }
   if (!active) return;
   if (add) {
-    float a[VEC];
-    load_vec<VEC>(add + row * ld_add + c0, a);
 #pragma unroll
     for (int v = 0; v < VEC; ++v) acc[v] += a[v];
   }
@@ -143,8 +151,6 @@ __global__ __launch_bounds__(256) void spmm_kernel(
     for (int v = 0; v < VEC; ++v) acc[v] = fmaxf(acc[v], 0.f);
   }
   if (mask) {   // the ReLU derivative of the layer whose output is `mask`
-    float mv[VEC];
-    load_vec<VEC>(mask + row * ldm + c0, mv);
 #pragma unroll
     for (int v = 0; v < VEC; ++v) acc[v] = mv[v] > 0.f ? acc[v] : 0.f;
   }
@@ -175,6 +181,14 @@ __global__ __launch_bounds__(256) void spmm_wide_kernel(
   const int c0 = ctile * (64 * VEC) + lane * VEC;
   const bool active = c0 < width;
   const int e0 = rowptr[row], e1 = rowptr[row + 1];
+  // Add and mask values load before the gathers (column clamped into the
+  // row: every load is in bounds; an inactive lane's values are never stored)
+  float a[VEC], mv[VEC];
+  {
+    const int cc = min(c0, width - VEC);
+    if (add) load_vec<VEC>(add + row * ld_add + cc, a);
+    if (mask) load_vec<VEC>(mask + row * ldm + cc, mv);
+  }
   const float* Xc = X + c0;
   float acc[VEC];
 #pragma unroll
@@ -219,8 +233,6 @@ __global__ __launch_bounds__(256) void spmm_wide_kernel(
   }
   if (!active) return;
   if (add) {
-    float a[VEC];
-    load_vec<VEC>(add + row * ld_add + c0, a);
 #pragma unroll
     for (int v = 0; v < VEC; ++v) acc[v] += a[v];
   }
@@ -229,8 +241,6 @@ __global__ __launch_bounds__(256) void spmm_wide_kernel(
     for (int v = 0; v < VEC; ++v) acc[v] = fmaxf(acc[v], 0.f);
   }
   if (mask) {   // the ReLU derivative of the layer whose output is `mask`
-    float mv[VEC];
-    load_vec<VEC>(mask + row * ldm + c0, mv);
 #pragma unroll
     for (int v = 0; v < VEC; ++v) acc[v] = mv[v] > 0.f ? acc[v] : 0.f;
   }

@@ -8,11 +8,11 @@
 // one X row from cache to the CUs per entry -- nnz * width * 4 bytes, twenty
 // times the algorithmic bytes at the c5 shape -- so it is bound by cache
 // bandwidth, not HBM.  Here a workgroup takes 32 rows and one 256-column
-// slab of X:
+// slab of X, four workgroups per CU:
 //
 //   1. window: [clo, clo + K) spans the columns of the tile's entries that
 //      lie within kNear of their row's diagonal, K <= kMaxK, rounded up to
-//      the MFMA depth;
+//      the MFMA depth and kept inside the matrix;
 //   2. the entries inside the window are expanded into a dense 32 x K tile
 //      in LDS, each value split into two bf16 halves, hi = bf16(v) and
 //      lo = bf16(v - hi) (both rounded to nearest even);
@@ -24,16 +24,19 @@
 //      operand and read-only here, so the loop has no barrier and the waves
 //      run independently.  Each X row of the window is read once per 32
 //      output rows instead of once per entry;
-//   4. the entries outside the window (edges between clusters) are gathered
-//      one X row each, as the gather kernel does, and added in storage
-//      order; then Add, ReLU and the store.
+//   steps 1-3 run a second time, over a second window, for the near-diagonal
+//      entries the first could not hold (rows straddling two clusters);
+//   4. the entries outside both windows (edges between clusters) are listed
+//      per wave, gathered one X row each and added in storage order; then
+//      Add, ReLU, the ReLU derivative of the layer below, and the store.
 //
 // Accuracy: a value's hi + lo carries 16 significant bits, so each split
 // operand is within 2^-17 of its value, and the dropped lo*lo term is below
 // 2^-16 of the product: every product enters the fp32 sum with a relative
-// error below 2^-15 (3.1e-5).  The sum order is fixed (the MFMA k order,
-// then the window's remainder in storage order): results are deterministic.
-// Correct for any matrix; fast when most entries sit near the diagonal.
+// error below 2^-15 (3.1e-5).  The sum order is fixed (the MFMA k order of
+// the first window, then of the second, then the remaining entries in
+// storage order): results are deterministic.  Correct for any matrix and
+// finite X; fast when most entries sit near the diagonal.
 
 #include <climits>
 #include <cstdio>
