@@ -410,6 +410,67 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
     }
   };
 
+  // fp32 step j with step j+1's staging (its registers to LDS buffer nbuf,
+  // free since the barrier that ended step j-1) placed among the MFMAs of
+  // chunk 2: the transposes and LDS writes issue while the matrix core runs,
+  // instead of after the last MFMA, when the other wave of the SIMD may be
+  // staging too.  Same arithmetic, same order as compute then stage.
+  auto compute_staged = [&](int buf, int nbuf) {
+    const float* As = lds_f + buf * kStage;
+    const float* Bs = As + kTileF;
+    auto mfma16 = [&](const floatx4 (&av)[2], const floatx4 (&bv)[2]) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+          for (int b = 0; b < 2; ++b)
+            acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[a][q], bv[b][q], acc[a][b], 0, 0, 0);
+    };
+    auto interleave = [&]() {
+#pragma unroll
+      for (int g = 0; g < 8; ++g) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);   // up to four VALU
+        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);   // an LDS write
+      }
+    };
+    if constexpr (kPipeFrag<AK, BK_, AV, BV>()) {
+      floatx4 av[2][2], bv[2][2];
+      auto rd = [&](int c, int p) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          av[p][t] = frag_f32(As, wm * 64 + t * 32 + li, 8 * c + 4 * lh);
+          bv[p][t] = frag_f32(Bs, wn * 64 + t * 32 + li, 8 * c + 4 * lh);
+        }
+      };
+      rd(0, 0);
+#pragma unroll
+      for (int c = 0; c < BK / 8; ++c) {
+        if (c + 1 < BK / 8) rd(c + 1, (c + 1) & 1);
+        __builtin_amdgcn_sched_barrier(0);
+        if (c == 1) stage(nbuf);
+        mfma16(av[c & 1], bv[c & 1]);
+        if (c == 1) interleave();
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < BK / 8; ++c) {
+        floatx4 av[2], bv[2];
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          av[t] = frag_f32(As, wm * 64 + t * 32 + li, 8 * c + 4 * lh);
+          bv[t] = frag_f32(Bs, wn * 64 + t * 32 + li, 8 * c + 4 * lh);
+        }
+        if (c == 1) stage(nbuf);
+        mfma16(av, bv);
+        if (c == 1) interleave();
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  };
+
   const int64_t w = xcd_remap(blockIdx.x, gridDim.x);
   int64_t it = w * S.ipw;
   const int64_t it_end = min(S.T, it + S.ipw);
@@ -450,9 +511,13 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
         // the scheduler sinks the loads next to their LDS stores, and their
         // latency is no longer hidden behind the step's MFMAs
         __builtin_amdgcn_sched_barrier(0);
-        compute((j - kb) & 1);
-        __builtin_amdgcn_sched_barrier(0);
-        stage((j + 1 - kb) & 1);
+        if constexpr (BF16) {
+          compute((j - kb) & 1);
+          __builtin_amdgcn_sched_barrier(0);
+          stage((j + 1 - kb) & 1);
+        } else {
+          compute_staged((j - kb) & 1, (j + 1 - kb) & 1);
+        }
         __syncthreads();
       }
       compute((full_end - 1 - kb) & 1);
