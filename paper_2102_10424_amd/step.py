@@ -867,13 +867,11 @@ class SubGCN:
 
     def backward(self, batch, params, sgd_lr=None):
         """Every layer's backward pass into ``self.dW``; with ``sgd_lr`` also
-        the SGD step.  With bf16-input GEMMs a GCN / SAGE layer takes it
-        inside its backward pass (``gist_gcn_layer_bwd_sgd``: the
-        weight-gradient GEMM updates the slice in place, after the input
-        gradient has read it; no dW); otherwise after the pass
-        (``gist_sgd_update``): in fp32 the fused epilogue's extra weight
-        reads cost as much as the separate pass."""
-        fused = sgd_lr is not None and not self.gat and self.dtype == G.GIST_DTYPE_BF16_IN
+        the SGD step.  A GCN / SAGE layer takes it inside its backward pass
+        (``gist_gcn_layer_bwd_sgd``: the weight-gradient GEMM updates the
+        slice in place, after the input gradient has read it; no dW); GAT
+        layers after the pass (``gist_sgd_update``)."""
+        fused = sgd_lr is not None and not self.gat
         nnz = batch.nnz
         ws = self._workspace(batch)
         dout = self.dlogits[:batch.rows(self.L)]
@@ -1037,9 +1035,8 @@ class SubGCNBatch:
 
     def backward(self, batch, params, sgd_lr=None):
         """Every layer's backward pass into ``self.dW``, and with ``sgd_lr`` the
-        SGD step: fused into it with bf16-input GEMMs (``gist_gcn_layer_bwd_sgd``,
-        all m slices), after it in fp32 (as ``SubGCN.backward``)."""
-        fused = sgd_lr is not None and self.dtype == G.GIST_DTYPE_BF16_IN
+        SGD step fused into it (``gist_gcn_layer_bwd_sgd``, all m slices)."""
+        fused = sgd_lr is not None
         n = batch.n
         ws = self._workspace(n)
         dout = self._gm(self._dlogits, n)

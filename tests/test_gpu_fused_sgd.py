@@ -173,10 +173,12 @@ def test_fused_sgd_empty_batch_and_errors(G, ctx):
         G.gist_gcn_layer_bwd_sgd(ctx, desc, A, None, None, None, None, None, None, LR, None, ws)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("kind", ["sage", "gcn"])
-def test_subgcn_bf16_step_takes_the_fused_path_bitwise(G, ctx, kind):
-    """SubGCN.step with bf16-input GEMMs fuses the SGD step into each layer's
-    backward pass; the weights must equal an explicit backward + SGD."""
+def test_subgcn_step_takes_the_fused_path_bitwise(G, ctx, kind, dtype):
+    """SubGCN.step fuses the SGD step into each GCN / SAGE layer's backward
+    pass, in fp32 and with bf16-input GEMMs; the weights must equal an
+    explicit backward + SGD."""
     import torch
     from paper_2102_10424_amd.step import BatchSlot, SubGCN
     g = sbm(1500, 10, 30.0, 0.9, seed=7)
@@ -191,7 +193,8 @@ def test_subgcn_bf16_step_takes_the_fused_path_bitwise(G, ctx, kind):
     b = slot.load(G.GraphHandle(g), np.array([0, 3, 5, 8], dtype=np.int32), X, y)
     out = []
     for fused in (True, False):
-        run = SubGCN(ctx, kind, widths, b.n, dtype=G.GIST_DTYPE_BF16_IN)
+        run = SubGCN(ctx, kind, widths, b.n,
+                     dtype=G.GIST_DTYPE_BF16_IN if dtype == "bf16" else G.GIST_DTYPE_F32)
         params = [to_dev(p) for p in P]
         if fused:
             run.step(b, params, LR)
