@@ -664,6 +664,43 @@ def c5_oracle_spmm_ms(graph, w=256):
     return (time.perf_counter() - t0) * 1e3
 
 
+def oracle_single_thread_ms(names=("c1", "c2", "c3")):
+    """The oracle's sub-GCN step (fwd + loss + bwd + SGD; round 0, sub-GCN 0,
+    fp64) on the small workloads with the BLAS behind NumPy / SciPy held to
+    one thread (threadpoolctl); graph, batch and parameters are built
+    outside the timed region."""
+    from threadpoolctl import threadpool_limits
+    from gist_synth import get_config
+    from oracle import gist as OG
+    from oracle import minibatch as OM
+    from oracle import partition as OP
+    out = {}
+    for name in names:
+        cfg = get_config(name)
+        graph = cfg.make_graph()
+        parts = [None] * (cfg.L + 1)
+        for l in range(1, cfg.L):
+            parts[l] = OP.partition(cfg.widths[l], cfg.m, cfg.partition_seed(0, l))
+        params = []
+        for l, (r, c) in enumerate(OG.slice_indices(parts, cfg.L, 0)):
+            ps = []
+            for p in range(cfg.n_parts()):
+                th = cfg.theta(l, p, rows=r) if r is not None else cfg.theta(l, p)
+                ps.append(th if c is None else th[:, c])
+            params.append(ps[0] if cfg.kind == "gcn" else (ps[0], ps[1]))
+        mb = cfg.minibatch(0, 0) if cfg.batch_clusters is not None else None
+        csr = OM.build(graph, mb, "sage" if cfg.kind == "sage" else "gcn")
+        nm = csr.get("node_map")
+        X = cfg.features_matrix(rows=nm) if nm is not None else cfg.features_matrix()
+        y = cfg.labels()
+        y = y[nm] if nm is not None else y
+        with threadpool_limits(limits=1):
+            t0 = time.perf_counter()
+            OG.sub_gcn_step(cfg.kind, csr, X, y, params, 0.01)
+            out[name] = round((time.perf_counter() - t0) * 1e3, 1)
+    return out
+
+
 def loss_curves(G, ctx, rounds, zeta, lr=0.01, hidden=256, eval_clusters=40):
     """Algorithm 1 trained with Adam (the paper's optimizer, no weight decay)
     for m = 1 (the full model), 2, 4 and 8, with the moments carried through
@@ -873,6 +910,11 @@ def main():
             cpu["spmm_c5_sample"] = ("fp64 Abar H over all 2,449,029 rows of the c5 matrix at "
                                      "width 256, SciPy CSR product on one thread, timed in full")
             log("[bench] oracle c5 aggregation timed")
+            cpu["single_thread_ms"] = oracle_single_thread_ms()
+            cpu["single_thread_sample"] = ("one sub-GCN step (fwd + loss + bwd + SGD), round 0, "
+                                           "sub-GCN 0, fp64, of the c1 / c2 / c3 workloads, BLAS "
+                                           "held to one thread")
+            log("[bench] oracle single-thread steps timed")
     out = {
         "metric": METRIC, "value": round(value, 4), "unit": "ms",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
