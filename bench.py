@@ -574,7 +574,7 @@ def hidden_gemms(prof, gflop, peak):
     return out
 
 
-def north_star_figures(wl, ctx, steps, clustered=True):
+def target_figures(wl, ctx, steps, clustered=True):
     """The two figures the default line does not time in its own workload,
     measured after the timed region: the full-graph aggregation of c5 (Abar H
     over the whole c4 graph, width 256, fp32) against HBM bandwidth, and the
@@ -858,8 +858,8 @@ def main():
         log(f"[bench] profiled {psteps} steps")
     extras = None
     if args.config == "c4" and not args.no_extras and not args.shared_batch:
-        extras = north_star_figures(wl, ctx, 8, args.aggregation == "tile")
-        log("[bench] north-star figures measured")
+        extras = target_figures(wl, ctx, 8, args.aggregation == "tile")
+        log("[bench] target figures measured")
     wl.finish()   # a deferred subAgg (after the timed region and the profile)
     kernels = {}
     for k, v in sorted(prof.items(), key=lambda kv: -kv[1]["ms"]):
@@ -929,7 +929,7 @@ def main():
                        else "ms per layer fwd+bwd"),
         "roofline": roofline, "cpu_baseline": cpu, "kernels": kernels,
         "host_batch_wait_ms_per_step": round(host_wait_ms, 3),
-        "north_star": extras,
+        "targets": extras,
         "kernels_from": (f"a separate profiled pass of {psteps} steps after the timed region "
                          "(library HIP event pairs around every launch, on its launch stream)" +
                          (", launched eagerly" if args.graphs else "")),
