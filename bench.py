@@ -646,6 +646,46 @@ def target_figures(wl, ctx, steps, clustered=True):
         "bytes_def": "4(n+1) + 8 nnz + 4 n w (X read once) + 4 n w (Y written once)"}
     del slot, X, bb, agg, Ho, ws
     torch.cuda.synchronize()
+    out["library_gemm_c4"] = dict(
+        what="torch.mm (vendor BLAS) on contiguous operands of the c4 hidden-layer shapes at the "
+             "mean batch size, bf16 and fp32; context for gemm_c4_bf16 and the roofline GEMM, "
+             "not part of the product path",
+        **library_gemm_figures(1633, wl.model.slice_widths[1]))
+    return out
+
+
+def library_gemm_figures(m=1633, s=4096, reps=10):
+    """Context for the GEMM figures: torch.mm (the vendor BLAS) on plain
+    contiguous operands of the c4 hidden-layer shapes -- forward (m x 2s) @
+    (2s x s), input gradient (m x s) @ (s x 2s), weight gradient (2s x m) @
+    (m x s) -- in bf16 and in fp32 (TF32 off), timed with events on torch's
+    stream.  No fused epilogue, no concatenated or transposed operands: a
+    library reference point, not part of the product path."""
+    import torch
+    torch.backends.cuda.matmul.allow_tf32 = False
+    shapes = {"forward": (m, s, 2 * s), "input_grad": (m, 2 * s, s), "weight_grad": (2 * s, s, m)}
+    out = {}
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    for dname, dt in (("bf16", torch.bfloat16), ("f32", torch.float32)):
+        row = {}
+        for name, (mm, nn, kk) in shapes.items():
+            a = torch.randn(mm, kk, device="cuda", generator=gen).to(dt).contiguous()
+            b = torch.randn(kk, nn, device="cuda", generator=gen).to(dt).contiguous()
+            for _ in range(2):
+                torch.mm(a, b)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                torch.mm(a, b)
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / reps
+            tf = 2.0 * mm * nn * kk / (us * 1e-6) / 1e12
+            row[name] = {"M": mm, "N": nn, "K": kk, "us": round(us, 1), "tflops": round(tf, 1),
+                         "frac": round(tf / PEAK[dname], 4)}
+            del a, b
+        out[dname] = row
     return out
 
 

@@ -42,10 +42,11 @@ def short(name):
 def variant_symbol(variant):
     """Regex over short kernel names that a library profiler variant launches."""
     b = lambda s: "true" if s else "false"
-    m = re.fullmatch(r"gemm_(f32|bf16)_([KR])([KR])_([vs])([vs])", variant)
+    m = re.fullmatch(r"gemm_(f32|bf16)_([KR])([KR])_([vs])([vs])(_n)?", variant)
     if m:
-        dt, ak, bk, av, bv = m.groups()
-        args = ", ".join([b(ak == "K"), b(bk == "K"), b(av == "v"), b(bv == "v"), b(dt == "bf16")])
+        dt, ak, bk, av, bv, nar = m.groups()
+        args = ", ".join([b(ak == "K"), b(bk == "K"), b(av == "v"), b(bv == "v"), b(dt == "bf16"),
+                          b(nar is not None)])
         return re.escape(f"gemm_kernel<{args}>") + "$"
     m = re.fullmatch(r"gemm_bf16_direct_([KR])([KR])", variant)
     if m:

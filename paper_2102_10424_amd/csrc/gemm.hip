@@ -263,10 +263,12 @@ __device__ __forceinline__ void store_tile_bf16(unsigned short* lds, const float
 
 struct Sched {
   int64_t T;        // total iterations = tiles * nk (tiles of all groups)
-  int64_t ipw;      // iterations per workgroup
+  int64_t ipw;      // iterations per workgroup (stream-K)
   int nk;           // K steps per tile
   int tiles_m, tiles_n;
   int64_t tpg;      // tiles per group (tiles_m * tiles_n)
+  int64_t tiles;    // tiles of all groups
+  int64_t spu;      // > 0: K-slice-major split, K steps per slice; 0: stream-K
 };
 
 __device__ __forceinline__ float* out_ptr(const OutDev& C, int64_t row, int64_t col) {
@@ -291,10 +293,17 @@ constexpr int min_blocks() { return (!BF16 && ((AV && BV) || (AK && BK_))) ? 2 :
 template <bool AK, bool BK_, bool AV, bool BV>
 constexpr bool kPipeFrag() { return AV && BV && AK == BK_; }
 
-template <bool AK, bool BK_, bool AV, bool BV, bool BF16>
+// NARROW (fp32, N <= 64): the tile's columns 64..127 lie past the matrix, so
+// the two waves that would own them take half of every K step instead --
+// waves wn = 0 the step's 8-wide K chunks 0-1, waves wn = 1 chunks 2-3, all
+// on columns 0..63 -- and the two halves are added through LDS before the
+// epilogue (a split of K inside the workgroup, always summed in the same
+// order).  Each step then costs half the MFMA time per wave.
+template <bool AK, bool BK_, bool AV, bool BV, bool BF16, bool NARROW>
 __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) void gemm_kernel(int64_t M, int64_t N, int64_t K,
                                                         OpDev A, OpDev B, OutDev C, Sched S,
                                                         float* partials) {
+  static_assert(!(NARROW && BF16), "the narrow split is an fp32 variant");
   constexpr int kStage = BF16 ? 0 : 2 * kTileF;    // floats per fp32 stage (A + B)
   constexpr int kStageH = BF16 ? 2 * BM * LDKH : 0;
   __shared__ __attribute__((aligned(16))) float lds_f[BF16 ? 1 : 2 * kStage];
@@ -304,6 +313,9 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
   const int wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int li = lane & 31, lh = lane >> 5;
+  constexpr int NC = NARROW ? 2 : BK / 8;   // 8-wide K chunks per wave per fp32 step
+  const int cb = NARROW ? 2 * wn : 0;       // this wave's first chunk
+  const int bw = NARROW ? 0 : wn;           // this wave's 64-column block of the tile
 
   // K per pipeline step: one 32-wide load sub-tile for fp32, two for bf16
   constexpr int KS = BF16 ? KSH : BK;
@@ -369,13 +381,13 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
 #pragma unroll
           for (int t = 0; t < 2; ++t) {
             av[p][t] = frag_f32(As, wm * 64 + t * 32 + li, 8 * c + 4 * lh);
-            bv[p][t] = frag_f32(Bs, wn * 64 + t * 32 + li, 8 * c + 4 * lh);
+            bv[p][t] = frag_f32(Bs, bw * 64 + t * 32 + li, 8 * c + 4 * lh);
           }
         };
-        rd(0, 0);
+        rd(cb, 0);
 #pragma unroll
-        for (int c = 0; c < BK / 8; ++c) {
-          if (c + 1 < BK / 8) rd(c + 1, (c + 1) & 1);
+        for (int c = 0; c < NC; ++c) {
+          if (c + 1 < NC) rd(cb + c + 1, (c + 1) & 1);
           __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
           for (int s = 0; s < 4; ++s)
@@ -389,12 +401,12 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
         }
       } else {
 #pragma unroll
-        for (int c = 0; c < BK / 8; ++c) {
+        for (int c = 0; c < NC; ++c) {
           floatx4 av[2], bv[2];
 #pragma unroll
           for (int t = 0; t < 2; ++t) {
-            av[t] = frag_f32(As, wm * 64 + t * 32 + li, 8 * c + 4 * lh);
-            bv[t] = frag_f32(Bs, wn * 64 + t * 32 + li, 8 * c + 4 * lh);
+            av[t] = frag_f32(As, wm * 64 + t * 32 + li, 8 * (cb + c) + 4 * lh);
+            bv[t] = frag_f32(Bs, bw * 64 + t * 32 + li, 8 * (cb + c) + 4 * lh);
           }
 #pragma unroll
           for (int s = 0; s < 4; ++s)
@@ -441,13 +453,13 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
           av[p][t] = frag_f32(As, wm * 64 + t * 32 + li, 8 * c + 4 * lh);
-          bv[p][t] = frag_f32(Bs, wn * 64 + t * 32 + li, 8 * c + 4 * lh);
+          bv[p][t] = frag_f32(Bs, bw * 64 + t * 32 + li, 8 * c + 4 * lh);
         }
       };
-      rd(0, 0);
+      rd(cb, 0);
 #pragma unroll
-      for (int c = 0; c < BK / 8; ++c) {
-        if (c + 1 < BK / 8) rd(c + 1, (c + 1) & 1);
+      for (int c = 0; c < NC; ++c) {
+        if (c + 1 < NC) rd(cb + c + 1, (c + 1) & 1);
         __builtin_amdgcn_sched_barrier(0);
         if (c == 1) stage(nbuf);
         mfma16(av[c & 1], bv[c & 1]);
@@ -456,12 +468,12 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
       }
     } else {
 #pragma unroll
-      for (int c = 0; c < BK / 8; ++c) {
+      for (int c = 0; c < NC; ++c) {
         floatx4 av[2], bv[2];
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-          av[t] = frag_f32(As, wm * 64 + t * 32 + li, 8 * c + 4 * lh);
-          bv[t] = frag_f32(Bs, wn * 64 + t * 32 + li, 8 * c + 4 * lh);
+          av[t] = frag_f32(As, wm * 64 + t * 32 + li, 8 * (cb + c) + 4 * lh);
+          bv[t] = frag_f32(Bs, bw * 64 + t * 32 + li, 8 * (cb + c) + 4 * lh);
         }
         if (c == 1) stage(nbuf);
         mfma16(av, bv);
@@ -472,8 +484,19 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
   };
 
   const int64_t w = xcd_remap(blockIdx.x, gridDim.x);
-  int64_t it = w * S.ipw;
-  const int64_t it_end = min(S.T, it + S.ipw);
+  int64_t it, it_end;
+  if (S.spu > 0) {
+    // K-slice-major: workgroup w takes K slice w / tiles of tile w % tiles,
+    // so the workgroups an XCD runs together (consecutive w) cover every
+    // tile of the same K range and share its operand rows in L2
+    const int64_t q = w / S.tiles, t = w - q * S.tiles;
+    const int64_t kb = q * S.spu;
+    it = t * S.nk + kb;
+    it_end = t * S.nk + min<int64_t>(S.nk, kb + S.spu);
+  } else {
+    it = w * S.ipw;
+    it_end = min(S.T, it + S.ipw);
+  }
   const int64_t first_tile = it / S.nk;
   const bool k_ragged = K % KS != 0;
 
@@ -531,8 +554,34 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
       compute(buf);
     }
 
+    if constexpr (NARROW) {
+      // each wave adds its partner's K half (waves 2i and 2i+1 hold the two
+      // halves of the same 64 x 64 block; a + b == b + a, so both end with
+      // the same sums), without a branch on the wave
+      __syncthreads();   // every wave is done reading this segment's tiles
+      float* mine = lds_f + wave * 4096;
+      const float* other = lds_f + (wave ^ 1) * 4096;
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) mine[((a * 2 + b) * 16 + r) * 64 + lane] = acc[a][b][r];
+      __syncthreads();
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[a][b][r] += other[((a * 2 + b) * 16 + r) * 64 + lane];
+          __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+
     // Epilogue.  Accumulator register r of lane l holds C row
     // 8 (r / 4) + 4 (l / 32) + (r mod 4), column l mod 32 of its 32 x 32 tile.
+    // (NARROW: the waves of column block 1 hold columns 64.. >= N and store
+    // nothing.)
     if (kb == 0 && ke == S.nk) {
 #pragma unroll
       for (int a = 0; a < 2; ++a)
@@ -563,7 +612,7 @@ __global__ __launch_bounds__(kThreads, (min_blocks<AK, BK_, AV, BV, BF16>())) vo
             if (row < M) store_out(Cg, row, col, acc[a][b][r]);
           }
         }
-    } else {
+    } else if (!NARROW || wn == 0) {
       // partial tile: slot 0 holds this workgroup's first tile, slot 1 its last
       float* part = partials + (w * 2 + (tile == first_tile ? 0 : 1)) * (BM * BN);
 #pragma unroll
@@ -597,8 +646,9 @@ __global__ __launch_bounds__(256) void streamk_fixup(int64_t M, int64_t N, Sched
   __shared__ int64_t slot_off[kMaxFixupParts];
   const int64_t t = blockIdx.x;
   const int chunk = blockIdx.y;
-  const int64_t w_first = (t * S.nk) / S.ipw;
-  const int64_t w_last = ((t + 1) * S.nk - 1) / S.ipw;
+  const bool sliced = S.spu > 0;
+  const int64_t w_first = sliced ? 0 : (t * S.nk) / S.ipw;
+  const int64_t w_last = sliced ? (S.nk + S.spu - 1) / S.spu - 1 : ((t + 1) * S.nk - 1) / S.ipw;
   if (w_first == w_last) return;  // computed whole and stored by one workgroup
   const int64_t grp = t / S.tpg;
   int tm, tn;
@@ -607,8 +657,10 @@ __global__ __launch_bounds__(256) void streamk_fixup(int64_t M, int64_t N, Sched
   if (m0 + chunk * kFixRows >= M) return;   // the chunk lies below the matrix
   const int parts = static_cast<int>(w_last - w_first + 1);
   for (int j = threadIdx.x; j < parts; j += 256) {
+    // sliced: slice j of tile t is workgroup j * tiles + t, its only tile
     const int64_t w = w_first + j;
-    slot_off[j] = (w * 2 + (((w * S.ipw) / S.nk) == t ? 0 : 1)) * (BM * BN);
+    slot_off[j] = sliced ? (j * S.tiles + t) * 2 * (BM * BN)
+                         : (w * 2 + (((w * S.ipw) / S.nk) == t ? 0 : 1)) * (BM * BN);
   }
   __syncthreads();
   const OutDev Cg = C.group(grp);
@@ -634,9 +686,17 @@ Sched make_sched(int64_t M, int64_t N, int64_t K, int dtype, int64_t groups = 1)
   s.nk = static_cast<int>((K + ks - 1) / ks);
   s.tpg = static_cast<int64_t>(s.tiles_m) * s.tiles_n;
   const int64_t tiles = s.tpg * groups;
+  s.tiles = tiles;
   s.T = tiles * s.nk;
+  s.spu = 0;
   if (tiles >= 4 * kStreamWG) {
     s.ipw = s.nk;   // enough tiles: one whole tile per workgroup
+  } else if (tiles * 8 <= kStreamWG && s.nk >= 2 * kMinSteps) {
+    // few tiles, long K (a weight gradient over many nodes): the K range in
+    // slices, K-slice-major over the grid, at least kMinSteps steps each
+    const int64_t slices = std::min<int64_t>(kStreamWG / tiles, s.nk / kMinSteps);
+    s.spu = (s.nk + slices - 1) / slices;
+    s.ipw = s.spu;
   } else {
     // stream-K over kStreamWG workgroups, but at least kMinSteps K steps
     // each: a small product (a narrow slice, few tiles) split one step per
@@ -648,8 +708,11 @@ Sched make_sched(int64_t M, int64_t N, int64_t K, int dtype, int64_t groups = 1)
   return s;
 }
 
-int64_t sched_groups(const Sched& s) { return (s.T + s.ipw - 1) / s.ipw; }
-bool sched_split(const Sched& s) { return s.ipw % s.nk != 0; }
+int64_t sched_slices(const Sched& s) { return (s.nk + s.spu - 1) / s.spu; }
+int64_t sched_groups(const Sched& s) {
+  return s.spu > 0 ? sched_slices(s) * s.tiles : (s.T + s.ipw - 1) / s.ipw;
+}
+bool sched_split(const Sched& s) { return s.spu > 0 ? sched_slices(s) > 1 : s.ipw % s.nk != 0; }
 
 // 16-byte loads along the operand's contiguous dimension are legal when the
 // leading dimensions and base addresses are multiples of 4 floats (and, for
@@ -663,13 +726,13 @@ bool op_vec_ok(const Operand& o, int64_t R) {
   return true;
 }
 
-template <bool AK, bool BK_, bool BF16>
+template <bool AK, bool BK_, bool BF16, bool NARROW>
 void launch_kernel(hipStream_t st, bool av, bool bv, dim3 grid, int64_t M, int64_t N, int64_t K,
                    const OpDev& A, const OpDev& B, const OutDev& C, const Sched& S,
                    float* part) {
 #define GIST_GEMM_LAUNCH(AV_, BV_)                                                         \
-  hipLaunchKernelGGL((gemm_kernel<AK, BK_, AV_, BV_, BF16>), grid, dim3(kThreads), 0, st,    \
-                     M, N, K, A, B, C, S, part)
+  hipLaunchKernelGGL((gemm_kernel<AK, BK_, AV_, BV_, BF16, NARROW>), grid, dim3(kThreads), 0, \
+                     st, M, N, K, A, B, C, S, part)
   if (av && bv) GIST_GEMM_LAUNCH(true, true);
   else if (av) GIST_GEMM_LAUNCH(true, false);
   else if (bv) GIST_GEMM_LAUNCH(false, true);
@@ -677,18 +740,18 @@ void launch_kernel(hipStream_t st, bool av, bool bv, dim3 grid, int64_t M, int64
 #undef GIST_GEMM_LAUNCH
 }
 
-template <bool BF16>
+template <bool BF16, bool NARROW>
 void dispatch(hipStream_t st, const Operand& A, const Operand& B, bool av, bool bv, dim3 grid,
               int64_t M, int64_t N, int64_t K, const OpDev& a, const OpDev& b, const OutDev& c,
               const Sched& S, float* part) {
   if (A.k_major && B.k_major)
-    launch_kernel<true, true, BF16>(st, av, bv, grid, M, N, K, a, b, c, S, part);
+    launch_kernel<true, true, BF16, NARROW>(st, av, bv, grid, M, N, K, a, b, c, S, part);
   else if (A.k_major)
-    launch_kernel<true, false, BF16>(st, av, bv, grid, M, N, K, a, b, c, S, part);
+    launch_kernel<true, false, BF16, NARROW>(st, av, bv, grid, M, N, K, a, b, c, S, part);
   else if (B.k_major)
-    launch_kernel<false, true, BF16>(st, av, bv, grid, M, N, K, a, b, c, S, part);
+    launch_kernel<false, true, BF16, NARROW>(st, av, bv, grid, M, N, K, a, b, c, S, part);
   else
-    launch_kernel<false, false, BF16>(st, av, bv, grid, M, N, K, a, b, c, S, part);
+    launch_kernel<false, false, BF16, NARROW>(st, av, bv, grid, M, N, K, a, b, c, S, part);
 }
 
 }  // namespace
@@ -737,7 +800,7 @@ gist_status gemm(hipStream_t st, int64_t M, int64_t N, int64_t K, const Operand&
   const bool split = sched_split(S);
   if (split) {
     // a tile's iterations span at most ceil(nk / ipw) + 1 workgroups
-    if ((S.nk + S.ipw - 1) / S.ipw + 1 > kMaxFixupParts)
+    if ((S.spu > 0 ? sched_slices(S) : (S.nk + S.ipw - 1) / S.ipw + 1) > kMaxFixupParts)
       return set_error(GIST_E_UNSUPPORTED, "gemm: too many partial tiles per tile");
     const size_t need = gemm_workspace(M, N, K, dtype, ngroups);
     if (!ws || ws_bytes < need) return set_error(GIST_E_NOMEM, "gemm: workspace too small");
@@ -750,21 +813,24 @@ gist_status gemm(hipStream_t st, int64_t M, int64_t N, int64_t K, const Operand&
   const bool bf = dtype == GIST_DTYPE_BF16_IN;
   const bool av = op_vec_ok(A, M);
   const bool bv = op_vec_ok(B, N);
+  const bool narrow = !bf && N <= BN / 2;
   dim3 grid(static_cast<unsigned>(groups));
   {
     // variant name: dtype, the K-contiguous (K) / row-contiguous (R)
-    // orientation of A and B as read from memory, and whether each is read
-    // with 16-byte vector loads (v) or scalar loads (s) -- one name per
-    // kernel instantiation
+    // orientation of A and B as read from memory, whether each is read
+    // with 16-byte vector loads (v) or scalar loads (s), and _n for the
+    // narrow split -- one name per kernel instantiation
     char name[32];
-    snprintf(name, sizeof(name), "gemm_%s_%c%c_%c%c", bf ? "bf16" : "f32",
-             A.k_major ? 'K' : 'R', B.k_major ? 'K' : 'R', av ? 'v' : 's', bv ? 'v' : 's');
+    snprintf(name, sizeof(name), "gemm_%s_%c%c_%c%c%s", bf ? "bf16" : "f32",
+             A.k_major ? 'K' : 'R', B.k_major ? 'K' : 'R', av ? 'v' : 's', bv ? 'v' : 's',
+             narrow ? "_n" : "");
     const double md = static_cast<double>(M), nd = static_cast<double>(N),
                  kd = static_cast<double>(K);
     const double gd = static_cast<double>(ngroups);
     ProfScope ps(st, name, 2.0 * md * nd * kd * gd, 4.0 * (md * kd + kd * nd + md * nd) * gd);
-    if (bf) dispatch<true>(st, A, B, av, bv, grid, M, N, K, a, b, c, S, part);
-    else dispatch<false>(st, A, B, av, bv, grid, M, N, K, a, b, c, S, part);
+    if (bf) dispatch<true, false>(st, A, B, av, bv, grid, M, N, K, a, b, c, S, part);
+    else if (narrow) dispatch<false, true>(st, A, B, av, bv, grid, M, N, K, a, b, c, S, part);
+    else dispatch<false, false>(st, A, B, av, bv, grid, M, N, K, a, b, c, S, part);
   }
   {
     gist_status s = check_launch("gemm");
