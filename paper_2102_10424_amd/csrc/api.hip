@@ -297,17 +297,19 @@ gist_status check_csr(const gist_csr_dev* A, int64_t n, const char* what) {
 // rows (X and D are node-major, the reduction runs over nodes), which the
 // GEMM stages through register transposes at a lower MFMA rate.  For large
 // fp32 products both operands are first transposed into node-contiguous
-// copies (ld rounded up to 4 floats), so the GEMM reads K-contiguous tiles.
+// copies, zero-padded to a multiple of 32 nodes, so the GEMM reads
+// K-contiguous tiles and every K step is whole (a ragged last step would
+// take the per-element edge loads); the zero columns add nothing.
 // The copies cost one read and one write of X and D; at c4 sizes (8192 x
 // 4096 x 1633) the product took 921 instead of 1046 us, for three
 // transposes of 18 us each.
 bool transposed_dw(const gist_layer_desc* L, int64_t M, int64_t N, int64_t K) {
   const int64_t G = L->groups > 1 ? L->groups : 1;
   return L->dtype == GIST_DTYPE_F32 && G == 1 && M >= 1024 && N >= 1024 && K >= 256 &&
-         K <= 65535 * 64;   // the transpose grid covers K rows in 64-row blocks
+         (K + 31) / 32 * 32 <= 65535 * 64;   // the transpose grid: padded K in 64-row blocks
 }
 
-int64_t round4(int64_t x) { return (x + 3) / 4 * 4; }
+int64_t round32(int64_t x) { return (x + 31) / 32 * 32; }
 
 // Workspace layout of the backward pass: [dZ | tmp | gemm scratch | X^T | D^T].
 struct BwdPlan {
@@ -338,8 +340,8 @@ BwdPlan plan_bwd(const gist_layer_desc* L) {
   }
   p.tdw = transposed_dw(L, wm, so, wk);
   if (p.tdw) {
-    p.ta = fbytes(wm, round4(wk));
-    p.tb = fbytes(so, round4(wk));
+    p.ta = fbytes(wm, round32(wk));
+    p.tb = fbytes(so, round32(wk));
   }
   return p;
 }
@@ -492,18 +494,18 @@ gist_status layer_bwd(gist_ctx* ctx, const gist_layer_desc* L, const gist_csr_de
     // transposed activation is act[k * ld + r]
     auto weight_grad = [&]() -> gist_status {
       if (p.tdw) {   // node-contiguous copies: [H | Abar H]^T (wrows x n) and dZ^T (so x n)
-        const int64_t n4 = round4(n);
+        const int64_t n32 = round32(n);
         if (sage) {
-          GIST_TRY(gist::transpose(st, H, n, si, y.ld_in, tA, n4));
-          GIST_TRY(gist::transpose(st, agg_save, n, si, y.ld_in, tA + si * n4, n4));
+          GIST_TRY(gist::transpose(st, H, n, si, y.ld_in, tA, n32));
+          GIST_TRY(gist::transpose(st, agg_save, n, si, y.ld_in, tA + si * n32, n32));
         } else {
-          GIST_TRY(gist::transpose(st, agg_save, n, si, y.ld_in, tA, n4));
+          GIST_TRY(gist::transpose(st, agg_save, n, si, y.ld_in, tA, n32));
         }
-        GIST_TRY(gist::transpose(st, dZ, n, so, y.ld_out, tB, n4));
+        GIST_TRY(gist::transpose(st, dZ, n, so, y.ld_out, tB, n32));
         gist::Operand at, bt;
-        at.p0 = tA; at.ld0 = n4; at.k_major = true;
-        bt.p0 = tB; bt.ld0 = n4; bt.k_major = true;
-        return gist::gemm(st, y.wrows, so, n, at, bt, wout, L->dtype, gws, gbytes, 1);
+        at.p0 = tA; at.ld0 = n32; at.k_major = true;
+        bt.p0 = tB; bt.ld0 = n32; bt.k_major = true;
+        return gist::gemm(st, y.wrows, so, n32, at, bt, wout, L->dtype, gws, gbytes, 1);
       }
       gist::Operand a;
       a.k_major = false;
@@ -545,13 +547,13 @@ gist_status layer_bwd(gist_ctx* ctx, const gist_layer_desc* L, const gist_csr_de
   GIST_TRY(spmm_out(st, y, AT, n_in, n, dZ, y.gs_out, tmp, y.gs_out_in, false));
   auto weight_grad = [&]() -> gist_status {
     if (p.tdw) {   // node-contiguous copies H^T (si x n_in) and T^T (so x n_in)
-      const int64_t n4 = round4(n_in);
-      GIST_TRY(gist::transpose(st, H, n_in, si, y.ld_in, tA, n4));
-      GIST_TRY(gist::transpose(st, tmp, n_in, so, y.ld_out, tB, n4));
+      const int64_t n32 = round32(n_in);
+      GIST_TRY(gist::transpose(st, H, n_in, si, y.ld_in, tA, n32));
+      GIST_TRY(gist::transpose(st, tmp, n_in, so, y.ld_out, tB, n32));
       gist::Operand at, bt;
-      at.p0 = tA; at.ld0 = n4; at.k_major = true;
-      bt.p0 = tB; bt.ld0 = n4; bt.k_major = true;
-      return gist::gemm(st, si, so, n_in, at, bt, wout, L->dtype, gws, gbytes, 1);
+      at.p0 = tA; at.ld0 = n32; at.k_major = true;
+      bt.p0 = tB; bt.ld0 = n32; bt.k_major = true;
+      return gist::gemm(st, si, so, n32, at, bt, wout, L->dtype, gws, gbytes, 1);
     }
     gist::Operand a;
     a.p0 = H; a.ld0 = y.ld_in; a.gs0 = y.gs_in; a.k_major = false;

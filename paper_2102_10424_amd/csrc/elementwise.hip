@@ -169,8 +169,9 @@ __global__ void zero_int_kernel(int* p) {
 
 // dst (cols x rows, leading dimension ldd) = transpose of src (rows x cols,
 // leading dimension lds), through a 64 x 65 LDS tile (the extra column keeps
-// the column reads of the tile free of bank conflicts).  Both the reads and
-// the writes go along the contiguous dimension, 64 floats per wave row.
+// the column reads of the tile free of bank conflicts), and zeros in columns
+// rows .. ldd-1 of every dst row.  Both the reads and the writes go along the
+// contiguous dimension, 64 floats per wave row.
 __global__ __launch_bounds__(kBlock) void transpose_kernel(const float* __restrict__ src,
                                                            int64_t rows, int64_t cols,
                                                            int64_t lds, float* __restrict__ dst,
@@ -186,7 +187,7 @@ __global__ __launch_bounds__(kBlock) void transpose_kernel(const float* __restri
   __syncthreads();
   for (int i = ty; i < 64; i += kBlock / 64) {
     const int64_t c = c0 + i, r = r0 + tx;
-    if (c < cols && r < rows) dst[c * ldd + r] = tile[tx][i];
+    if (c < cols && r < ldd) dst[c * ldd + r] = r < rows ? tile[tx][i] : 0.f;
   }
 }
 
@@ -620,10 +621,11 @@ gist_status fill_zero(hipStream_t st, float* p, int64_t count) {
 gist_status transpose(hipStream_t st, const float* src, int64_t rows, int64_t cols, int64_t lds,
                       float* dst, int64_t ldd) {
   if (rows <= 0 || cols <= 0) return GIST_OK;
-  const int64_t gx = (cols + 63) / 64, gy = (rows + 63) / 64;
+  if (ldd < rows) return set_error(GIST_E_INVAL, "transpose: ldd < rows");
+  const int64_t gx = (cols + 63) / 64, gy = (ldd + 63) / 64;
   if (gx > INT32_MAX || gy > 65535)
     return set_error(GIST_E_UNSUPPORTED, "transpose: matrix too large");
-  ProfScope ps(st, "transpose", 0.0, 8.0 * static_cast<double>(rows) * cols);
+  ProfScope ps(st, "transpose", 0.0, 4.0 * static_cast<double>(rows + ldd) * cols);
   hipLaunchKernelGGL(transpose_kernel, dim3(static_cast<unsigned>(gx), static_cast<unsigned>(gy)),
                      dim3(kBlock), 0, st, src, rows, cols, lds, dst, ldd);
   return check_launch("transpose");

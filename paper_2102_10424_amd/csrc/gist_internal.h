@@ -166,7 +166,8 @@ gist_status scatter(hipStream_t st, float* Wg, int64_t ldg, const int32_t* rows,
 gist_status count_nonfinite(hipStream_t st, const float* Ws, int64_t lds,
                             int32_t nr, int32_t nc, int* d_count);
 gist_status fill_zero(hipStream_t st, float* p, int64_t count);
-// dst (cols x rows, ld ldd) = src^T (src rows x cols, ld lds).
+// dst (cols x rows, ld ldd >= rows) = src^T (src rows x cols, ld lds); columns
+// rows .. ldd-1 of every dst row are set to zero.
 gist_status transpose(hipStream_t st, const float* src, int64_t rows, int64_t cols, int64_t lds,
                       float* dst, int64_t ldd);
 // dst <- src (bytes), by a kernel on the stream; src may be pinned host memory.
