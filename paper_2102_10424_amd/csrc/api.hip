@@ -505,7 +505,7 @@ gist_status layer_bwd(gist_ctx* ctx, const gist_layer_desc* L, const gist_csr_de
         gist::Operand at, bt;
         at.p0 = tA; at.ld0 = n32; at.k_major = true;
         bt.p0 = tB; bt.ld0 = n32; bt.k_major = true;
-        return gist::gemm(st, y.wrows, so, n32, at, bt, wout, L->dtype, gws, gbytes, 1);
+        return gist::gemm(st, y.wrows, so, n32, at, bt, wout, L->dtype, gws, gbytes, 1, n);
       }
       gist::Operand a;
       a.k_major = false;
@@ -553,7 +553,7 @@ gist_status layer_bwd(gist_ctx* ctx, const gist_layer_desc* L, const gist_csr_de
       gist::Operand at, bt;
       at.p0 = tA; at.ld0 = n32; at.k_major = true;
       bt.p0 = tB; bt.ld0 = n32; bt.k_major = true;
-      return gist::gemm(st, si, so, n32, at, bt, wout, L->dtype, gws, gbytes, 1);
+      return gist::gemm(st, si, so, n32, at, bt, wout, L->dtype, gws, gbytes, 1, n_in);
     }
     gist::Operand a;
     a.p0 = H; a.ld0 = y.ld_in; a.gs0 = y.gs_in; a.k_major = false;

@@ -767,7 +767,7 @@ size_t gemm_workspace(int64_t M, int64_t N, int64_t K, int dtype, int64_t groups
 
 gist_status gemm(hipStream_t st, int64_t M, int64_t N, int64_t K, const Operand& A,
                  const Operand& B, const GemmOut& C, int dtype, void* ws, size_t ws_bytes,
-                 int64_t ngroups) {
+                 int64_t ngroups, int64_t k_alg) {
   if (M <= 0 || N <= 0 || ngroups <= 0) return GIST_OK;
   OutDev c{C.c0, C.c1, C.ldc0, C.ldc1, C.c_split, C.relu ? 1 : 0, C.gs0, C.gs1,
            C.sgd ? 1 : 0, C.lr, C.mask, C.ldm, C.gsm};
@@ -825,7 +825,7 @@ gist_status gemm(hipStream_t st, int64_t M, int64_t N, int64_t K, const Operand&
              A.k_major ? 'K' : 'R', B.k_major ? 'K' : 'R', av ? 'v' : 's', bv ? 'v' : 's',
              narrow ? "_n" : "");
     const double md = static_cast<double>(M), nd = static_cast<double>(N),
-                 kd = static_cast<double>(K);
+                 kd = static_cast<double>(k_alg > 0 ? k_alg : K);
     const double gd = static_cast<double>(ngroups);
     ProfScope ps(st, name, 2.0 * md * nd * kd * gd, 4.0 * (md * kd + kd * nd + md * nd) * gd);
     if (bf) dispatch<true, false>(st, A, B, av, bv, grid, M, N, K, a, b, c, S, part);

@@ -149,9 +149,11 @@ struct GemmOut {
 // `groups` independent products of the same shape: group g reads A and B
 // and writes C at the pointers offset by g times their group strides.
 size_t gemm_workspace(int64_t M, int64_t N, int64_t K, int dtype, int64_t groups = 1);
+// k_alg: the reduction length the profiler counts (flops, bytes) when K
+// includes zero padding (0: K itself).
 gist_status gemm(hipStream_t st, int64_t M, int64_t N, int64_t K,
                  const Operand& A, const Operand& B, const GemmOut& C, int dtype,
-                 void* ws, size_t ws_bytes, int64_t groups = 1);
+                 void* ws, size_t ws_bytes, int64_t groups = 1, int64_t k_alg = 0);
 
 // dZ[i] = dH[i] * (Hout[i] > 0) over n x w (ld = w).
 gist_status relu_mask(hipStream_t st, int64_t count, const float* dH,
