@@ -29,7 +29,12 @@
 // is split between workgroups is written as partial tiles to the workspace
 // and summed by a second kernel in workgroup order: deterministic, and no
 // workgroup ever waits on another.  Products with plenty of tiles use one
-// whole tile per workgroup and skip the second kernel.
+// whole tile per workgroup and skip the second kernel.  Products with few
+// tiles and a long K (a weight gradient reduced over many nodes) split K
+// into slices dealt out slice-major, so that the workgroups an XCD runs
+// together share each K range's operand rows in L2.  For N <= 64 the two
+// waves whose columns would lie past the matrix take the second half of
+// every K step instead (see NARROW below).
 
 #include <algorithm>
 #include <cstdio>
