@@ -1225,26 +1225,29 @@ class GistModel:
         if self._events[slot] is not None:
             self._events[slot].synchronize()   # the pinned buffers' last upload is done
         m = self.m
+        if self._gevents[slot] is None:
+            self._gevents[slot] = G.Event()
         for l in range(1, self.L):
             d = self.widths[l]
             if self._pin[slot][l] is None:
-                # int32 [idx; rank] followed by the int64 offsets (as 2(m+1) int32)
-                self._pin[slot][l] = torch.empty(2 * d + 2 * (m + 1), dtype=torch.int32,
-                                                 pin_memory=True)
-                self._dev[slot][l] = torch.empty(2, d, dtype=torch.int32, device=self.device)
-                self._doffs[slot][l] = torch.empty(m + 1, dtype=torch.int64, device=self.device)
+                # int32 [idx; rank] followed by the int64 offsets (as 2(m+1) int32), the
+                # same layout on both sides so that one copy moves all three
+                n32 = 2 * d + 2 * (m + 1)
+                self._pin[slot][l] = torch.empty(n32, dtype=torch.int32, pin_memory=True)
+                buf = torch.empty(n32, dtype=torch.int32, device=self.device)
+                self._dev[slot][l] = buf[:2 * d].view(2, d)
+                self._doffs[slot][l] = buf[2 * d:].view(torch.int64)
             idx, offs = G.gist_partition(d, m, seeds[l])
             rank = G.gist_partition_inverse(idx, offs)
             h = self._pin[slot][l].numpy()
             h[:d], h[d:2 * d] = idx, rank
             h[2 * d:].view(np.int64)[:] = offs
             self._host[slot][l] = (idx, offs)
-            pin = self._pin[slot][l]
-            G.gist_copy(self.ctx, self._dev[slot][l], pin, 8 * d)
-            G.gist_copy(self.ctx, self._doffs[slot][l], pin[2 * d:], 8 * (m + 1))
-        if self._gevents[slot] is None:
-            self._gevents[slot] = G.Event()
-        G.gist_copy(self.ctx, None, None, 0, self._gevents[slot])
+            # the event after the last layer's copy marks the pinned buffers free
+            G.gist_copy(self.ctx, self._dev[slot][l], self._pin[slot][l], 8 * d + 8 * (m + 1),
+                        self._gevents[slot] if l == self.L - 1 else None)
+        if self.L == 1:
+            G.gist_copy(self.ctx, None, None, 0, self._gevents[slot])
         self._events[slot] = self._gevents[slot]
         self._slot = slot
 
