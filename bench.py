@@ -112,6 +112,10 @@ def parse():
     ap.add_argument("--graphs", action="store_true",
                     help="replay every sub-GCN step from a HIP graph (SGD, a mini-batch per "
                          "sub-GCN: cluster or LADIES batches at fixed padded shapes)")
+    ap.add_argument("--round-graphs", action="store_true",
+                    help="with --graphs: replay each whole round (fused subAgg + gather and "
+                         "the m sub-GCN steps) from one HIP graph (SGD, zeta 1, one stream; "
+                         "at least 5 warm-up rounds, which record the graphs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the library's per-launch event timing")
@@ -140,12 +144,12 @@ class RoundWorkload:
     """A GIST round (partition, gather, m sub-GCN steps, subAgg) on one GPU."""
 
     def __init__(self, cfg, ctx, dtype, optimizer="sgd", policy="carry", zeta=1, shared=False,
-                 streams=1, graphs=False, lr=0.01, clustered=True):
+                 streams=1, graphs=False, lr=0.01, clustered=True, round_graphs=False):
         import torch
         from paper_2102_10424_amd import gist as G
         from paper_2102_10424_amd.step import (BatchPipeline, BatchSlot, ClusterGraphRunner,
                                                FixedBatchSlot, GistModel, LadiesGraphRunner,
-                                               SubGCN, SubGCNBatch)
+                                               RoundReplayer, SubGCN, SubGCNBatch)
         self.cfg, self.ctx, self.G = cfg, ctx, G
         self.lr = lr
         self.adam = policy if optimizer == "adam" else None
@@ -172,6 +176,13 @@ class RoundWorkload:
             raise ValueError("LADIES mini-batches are per sub-GCN (no shared batch)")
         if graphs and (shared or not (self.ladies or cfg.batch_clusters)):
             raise ValueError("--graphs replays sub-GCN steps on per-sub-GCN mini-batches")
+        if round_graphs and not (graphs and streams == 1 and zeta == 1 and self.adam is None):
+            raise ValueError("--round-graphs needs --graphs, SGD, zeta 1 and one stream")
+        self.round_graphs = round_graphs
+        # round replays read each round's m mini-batches from the same pipeline
+        # slots every fourth round: a ring of 4m slots (three rounds of builds
+        # ahead; with 2m the builds fell behind)
+        ring = 4 * cfg.m if round_graphs else 12
         # capacities: the largest mini-batch of the clusters, generous nnz bound
         if self.ladies:
             cap_n = self.ladies["batch"] + cfg.L * self.ladies["samples"]
@@ -201,7 +212,7 @@ class RoundWorkload:
                                                self.ladies["samples"], max_deg, cfg.widths[0],
                                                self.A_full, self.X, self.labels,
                                                self._ladies_order(zeta, k, self.nstreams),
-                                               depth=12 if graphs else 8,
+                                               depth=ring if graphs else 8,
                                                workers=(12 if graphs else 8) // self.nstreams,
                                                fixed=graphs)
                           for k, c in enumerate(self.ctxs)]
@@ -216,7 +227,7 @@ class RoundWorkload:
                                         depth=8, workers=(12 if graphs else 4) // self.nstreams,
                                         slots=[FixedBatchSlot(c, self.norm, cap_n, cap_nnz,
                                                               cfg.widths[0], clustered=clustered)
-                                               for _ in range(12 if graphs else 8)],
+                                               for _ in range(ring if graphs else 8)],
                                         build=self._fixed_build)
                           for k, c in enumerate(self.ctxs)]
             self.pipe = self.pipes[0]
@@ -238,6 +249,9 @@ class RoundWorkload:
                     ClusterGraphRunner(c, cfg.kind, self.model.slice_widths, cap_n, cap_nnz,
                                        cfg.widths[0], self.X, dtype=dt, clustered=clustered)
                     for c in self.ctxs]
+            if round_graphs:
+                self.round_replayer = RoundReplayer(self.model, self.graph_runners[0],
+                                                    self.pipes[0], lr)
         self.t = 0
 
     def _coef(self, t, z):
@@ -286,6 +300,10 @@ class RoundWorkload:
     def step(self):
         cfg, m = self.cfg, self.model
         t, zeta = self.t, self.zeta
+        if self.use_graphs and self.round_graphs:
+            self.round_replayer.round({l: cfg.partition_seed(t, l) for l in range(1, cfg.L)})
+            self.t += 1
+            return
         m.set_partitions({l: cfg.partition_seed(t, l) for l in range(1, cfg.L)})
         m.begin_round()   # subAgg of round t-1 fused with the gather of round t
         if self.shared:
@@ -355,7 +373,8 @@ class RoundWorkload:
                 "batching": "m sub-GCNs on one shared mini-batch (batched layers)" if self.shared
                             else "one mini-batch per sub-GCN",
                 "optimizer": f"adam ({self.adam} moments)" if self.adam else "sgd",
-                "launch": "each sub-GCN step replayed from a HIP graph" if self.graphs
+                "launch": ("each round replayed from one HIP graph" if self.round_graphs else
+                           "each sub-GCN step replayed from a HIP graph") if self.graphs
                           else "kernels launched one by one"}
 
     # ---- CPU baseline: the fp64 oracle on one sub-GCN step ---------------------
@@ -869,7 +888,14 @@ def main():
         # the SBM workloads' mini-batches are unions of clusters over block-contiguous ids
         wl = RoundWorkload(cfg, ctx, args.dtype, args.optimizer, args.adam_policy, args.zeta,
                            args.shared_batch, args.streams, args.graphs, args.lr,
-                           clustered=tiles and cfg.batch_clusters is not None)
+                           clustered=tiles and cfg.batch_clusters is not None,
+                           round_graphs=args.round_graphs)
+    if args.round_graphs and args.warmup < 5:
+        # the first five rounds record the round graphs (no subAgg pending,
+        # then the four states of the model's alternating buffers and the
+        # pipeline's four slot sets): none is recorded while timing
+        log("[bench] --round-graphs: 5 warm-up rounds")
+        args.warmup = 5
     ctxs = getattr(wl, "ctxs", [ctx])
     for w in range(args.warmup):
         wl.step()

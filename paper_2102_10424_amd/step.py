@@ -314,6 +314,22 @@ class BatchPipeline:
         self._submit()       # reuses this slot: its build waits for the upload just enqueued
         return out
 
+    def take_many(self, n, use):
+        """Hand the next ``n`` built slots to ``use(slots)`` together, with the
+        contract of :meth:`take` for each of them; then refill them."""
+        import time
+        items = [self.pending.popleft() for _ in range(n)]
+        for slot, fut in items:
+            if not fut.done():
+                t0 = time.perf_counter()
+                fut.result()
+                self.wait_s += max(0.0, time.perf_counter() - t0 - getattr(slot, "sync_s", 0.0))
+            fut.result()
+        out = use([slot for slot, _ in items])
+        for _ in range(n):
+            self._submit()
+        return out
+
     def next(self):
         """The next batch, uploaded on the current stream."""
         return self.take(lambda slot: slot.upload(self.X))
@@ -693,6 +709,73 @@ class LadiesGraphRunner(_Replayer):
                 self.cap_ctx.set_stream(self.cap_stream.cuda_stream)
             return
         self._replay(slot, params, lr, adam)
+
+
+class RoundReplayer:
+    """Whole GIST rounds replayed from HIP graphs: the fused subAgg + gather
+    of :meth:`GistModel.begin_round` and the m sub-GCN steps (each: the copy of
+    its mini-batch from pinned memory, the step recorded by ``runner``, SGD
+    fused into the backward pass) recorded as one graph, so that a round
+    costs the host one partition upload and one launch instead of a few
+    library calls per sub-GCN.
+
+    One recording per state the round starts from: the model's partition
+    slot, slice buffer and pending subAgg, and the pipeline slots that hold
+    the round's m mini-batches (with a ring of 4m slots the state repeats
+    every four rounds, so after the first five rounds every round is a
+    replay).  SGD, one local step per sub-GCN, one stream.  A round with a
+    mini-batch beyond the runner's fixed layout runs step by step instead.
+    """
+
+    def __init__(self, model, runner, pipe, lr):
+        if not model.fused or model.adam is not None:
+            raise ValueError("round replays need the fused subAgg and SGD")
+        self.model, self.runner, self.pipe, self.lr = model, runner, pipe, float(lr)
+        self.replays = {}
+        self.event = G.Event()
+        self.stepwise_rounds = 0
+
+    def _capture(self, slots):
+        m, run = self.model, self.runner
+        torch.cuda.synchronize()    # everything the recording reads exists and is written
+        ctx0 = m.ctx
+        m.ctx = run.cap_ctx
+        G.gist_capture_begin(run.cap_ctx)
+        try:
+            m._begin_state(m._begin_launches())
+            for i, slot in enumerate(slots):
+                G.gist_copy(run.cap_ctx, run.dev, slot.packed_h, run.nbytes)
+                run._body(m.params[i], self.lr, None)
+        finally:
+            replay = G.gist_capture_end(run.cap_ctx)
+            m.ctx = ctx0
+        return replay
+
+    def _round(self, slots):
+        m, run = self.model, self.runner
+        if not all(getattr(s, "fits_fixed", lambda: True)() for s in slots):
+            self.stepwise_rounds += 1
+            m.begin_round()
+            for i, slot in enumerate(slots):
+                run.step(slot, m.params[i], self.lr)
+            return
+        key = (m._slot, m.buf, m.pending, tuple(s.packed_h.data_ptr() for s in slots))
+        r = self.replays.get(key)
+        if r is None:
+            r = self.replays[key] = self._capture(slots)
+        else:
+            m._begin_state(1 - m.buf if m.pending is not None else m.buf)
+        G.gist_replay_launch(run.ctx, r)
+        G.gist_copy(run.ctx, None, None, 0, self.event)   # the slots' batches are read
+        for slot in slots:
+            slot.uploaded = self.event
+
+    def round(self, seeds):
+        """One round: ``subGCNs`` with the partition seeds ``seeds`` ({l: seed}),
+        the replayed round, and the (deferred) subAgg bookkeeping."""
+        self.model.set_partitions(seeds)
+        self.pipe.take_many(self.model.m, self._round)
+        self.model.end_round()
 
 
 class LadiesView:
@@ -1334,6 +1417,11 @@ class GistModel:
             for i in range(self.m):
                 self.gather(i)
             return
+        self._begin_state(self._begin_launches())
+
+    def _begin_launches(self):
+        """The launches of a fused :meth:`begin_round` (pending subAgg with this
+        round's gather), in order; returns the slice buffer they fill."""
         nxt = 1 - self.buf if self.pending is not None else self.buf
         if self.pending is not None:
             self.subagg_shared(self.pending[1])
@@ -1348,6 +1436,11 @@ class GistModel:
                                          self.widths[l + 1], self.widths[l + 1], self.m, done,
                                          self._set(self._slot, tables[nxt], l, p))
         self._gather_shared(nxt)
+        return nxt
+
+    def _begin_state(self, nxt):
+        """The bookkeeping of a fused :meth:`begin_round`: slice buffer ``nxt``
+        becomes the sub-GCNs' parameters, nothing is pending."""
         self._select(nxt)
         self.pending = None
 
