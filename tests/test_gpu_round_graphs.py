@@ -51,3 +51,43 @@ def test_round_replays_match_step_replays(config):
     for l, (a, b) in enumerate(zip(*thetas)):
         for p, (x, y) in enumerate(zip(a, b)):
             assert x.tobytes() == y.tobytes(), (config, l, p)
+
+
+def test_round_with_a_batch_beyond_the_fixed_layout_runs_step_by_step(monkeypatch):
+    """A LADIES batch with more entries than the fixed layout holds is run
+    eagerly at its own shape; a round holding one runs step by step (the
+    fused subAgg + gather eagerly, then each sub-GCN's step replayed or, for
+    that batch, eager).  Such batches are forced here from the host (every
+    batch whose first layer has a multiple of 3 entries reports that it does
+    not fit), identically in both runs, so the rounds with round replays must
+    still match per-step replays bit for bit."""
+    import torch
+    import bench
+    from gist_synth import get_config
+    from paper_2102_10424_amd import gist as G
+    from paper_2102_10424_amd import step as S
+    assert torch.cuda.is_available(), "GPU tests need a visible GPU"
+    real = S.LadiesSlot.fits_fixed
+    monkeypatch.setattr(S.LadiesSlot, "fits_fixed",
+                        lambda self: real(self) and self.built[1][0][2] % 3 != 0)
+    ctx = G.Context(0)
+    cfg = get_config("c7")
+    thetas = []
+    for round_graphs in (False, True):
+        wl = bench.RoundWorkload(cfg, ctx, "f32", graphs=True, lr=0.01,
+                                 round_graphs=round_graphs)
+        for _ in range(ROUNDS):
+            wl.step()
+        wl.finish()
+        torch.cuda.synchronize()
+        if round_graphs:
+            rr = wl.round_replayer
+            log(f"c7 forced: {len(rr.replays)} round graphs, {rr.stepwise_rounds} rounds "
+                "step by step")
+            assert rr.stepwise_rounds >= 1
+        thetas.append([[t.cpu().numpy().copy() for t in parts] for parts in wl.model.theta])
+        del wl
+        torch.cuda.synchronize()
+    for l, (a, b) in enumerate(zip(*thetas)):
+        for p, (x, y) in enumerate(zip(a, b)):
+            assert x.tobytes() == y.tobytes(), (l, p)
