@@ -191,6 +191,46 @@ __global__ __launch_bounds__(kBlock) void transpose_kernel(const float* __restri
   }
 }
 
+// The same with 16-byte accesses on both sides (lds, cols and ldd multiples of
+// 4 floats, 16-byte aligned bases): a thread loads four consecutive columns
+// of a source row and stores four consecutive entries of a destination row
+// (rows past `rows` as zeros), so each wave moves whole 256-byte runs.
+__global__ __launch_bounds__(kBlock) void transpose4_kernel(const float* __restrict__ src,
+                                                            int64_t rows, int64_t cols,
+                                                            int64_t lds, float* __restrict__ dst,
+                                                            int64_t ldd) {
+  __shared__ float tile[64][65];
+  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * 64;
+  const int64_t c0 = static_cast<int64_t>(blockIdx.x) * 64;
+  const int q = threadIdx.x & 15, g = threadIdx.x >> 4;   // 16 float4 per 64-float row
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int lr = g + 16 * i;
+    const int64_t r = r0 + lr, c = c0 + 4 * q;
+    if (r < rows && c < cols) {   // cols % 4 == 0: the four columns are all in
+      const float4 v = *reinterpret_cast<const float4*>(src + r * lds + c);
+      tile[lr][4 * q] = v.x;
+      tile[lr][4 * q + 1] = v.y;
+      tile[lr][4 * q + 2] = v.z;
+      tile[lr][4 * q + 3] = v.w;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int lc = g + 16 * i;
+    const int64_t c = c0 + lc, r = r0 + 4 * q;
+    if (c < cols && r < ldd) {    // ldd % 4 == 0: the four entries are all in
+      float4 o;
+      o.x = r < rows ? tile[4 * q][lc] : 0.f;
+      o.y = r + 1 < rows ? tile[4 * q + 1][lc] : 0.f;
+      o.z = r + 2 < rows ? tile[4 * q + 2][lc] : 0.f;
+      o.w = r + 3 < rows ? tile[4 * q + 3][lc] : 0.f;
+      *reinterpret_cast<float4*>(dst + c * ldd + r) = o;
+    }
+  }
+}
+
 // Copy of `n16` 16-byte words, then `tail` single bytes, from `src` (which
 // may be pinned host memory: the reads then cross the host link) to `dst`.
 __global__ __launch_bounds__(kBlock) void pull_kernel(uint4* __restrict__ dst,
@@ -626,8 +666,14 @@ gist_status transpose(hipStream_t st, const float* src, int64_t rows, int64_t co
   if (gx > INT32_MAX || gy > 65535)
     return set_error(GIST_E_UNSUPPORTED, "transpose: matrix too large");
   ProfScope ps(st, "transpose", 0.0, 4.0 * static_cast<double>(rows + ldd) * cols);
-  hipLaunchKernelGGL(transpose_kernel, dim3(static_cast<unsigned>(gx), static_cast<unsigned>(gy)),
-                     dim3(kBlock), 0, st, src, rows, cols, lds, dst, ldd);
+  const bool vec = lds % 4 == 0 && cols % 4 == 0 && ldd % 4 == 0 && aligned16(src) &&
+                   aligned16(dst);
+  if (vec)
+    hipLaunchKernelGGL(transpose4_kernel, dim3(static_cast<unsigned>(gx), static_cast<unsigned>(gy)),
+                       dim3(kBlock), 0, st, src, rows, cols, lds, dst, ldd);
+  else
+    hipLaunchKernelGGL(transpose_kernel, dim3(static_cast<unsigned>(gx), static_cast<unsigned>(gy)),
+                       dim3(kBlock), 0, st, src, rows, cols, lds, dst, ldd);
   return check_launch("transpose");
 }
 
